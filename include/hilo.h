@@ -1,0 +1,175 @@
+/*
+ * hilo.h -- C ABI of libhilo.so, the MI355X (gfx950) hot path of HiLo-Token: one diffusion-
+ * transformer block run on an input-adaptively compressed token set.
+ *
+ * The six calls follow the method's own order (HiLo-Token, Sec. 2.3 "HiLo-Token Selection"):
+ *   hilo_score      Sobel frequency energy of every latent patch
+ *   hilo_select     2x2 regional pooling of the energy, threshold or top-k, dilated user mask kept
+ *                   fine, and the index map of the compressed grid
+ *   hilo_compress   fine patches copied, every other 2x2 block pooled into one low-frequency token,
+ *                   text tokens appended (concatenation along the token dimension)
+ *   hilo_attention  pre-LN adaLN joint attention over image + text tokens of each sample
+ *   hilo_mlp        pre-LN adaLN GELU MLP
+ *   hilo_decompress scatter fine tokens and broadcast pooled tokens back to the full grid
+ *
+ * Conventions shared by every call
+ *   - Every tensor pointer is a caller-owned DEVICE pointer unless stated otherwise; tensors are
+ *     dense, row-major, with the last index contiguous.  The library never allocates device memory
+ *     and never synchronises; each call validates its arguments on the host, returns an error and
+ *     enqueues nothing when they are wrong, and otherwise enqueues its kernels on `stream` (a
+ *     hipStream_t passed as void*; NULL = the default stream) and returns HILO_OK.
+ *   - A launch failure returns HILO_E_DEVICE.  A fault inside a kernel surfaces at the caller's
+ *     next synchronisation.  No C++ exception crosses this boundary.
+ *   - Token counts never travel back to the host: hilo_select leaves them in device memory and
+ *     the later calls read them there, sizing their grids for the worst case (no compression).
+ *   - Shapes: G = batch * images grids of N = grid_h * grid_w patches (raster order p = i*grid_w+j),
+ *     NB = N / 4 coarse 2x2 blocks (b = (i/2)*(grid_w/2) + j/2), D = dim, L = text_len.
+ *     T_max = batch * (images * N + L) is the longest packed sequence (hilo_max_tokens).
+ *   - The packed sequence of sample s occupies rows [cu_seqlens[s], cu_seqlens[s+1]) of z:
+ *     [grid 0: fine patches in raster order, then pooled blocks in block order ; grid 1 ... ;
+ *      L text tokens].  seg_off[g] is the first row of grid g.
+ *   - The residual stream z is float32 in every dtype; x_img, x_txt, weights and y are `dtype`.
+ *   - Calls that touch disjoint buffers may run concurrently on different streams.
+ */
+#ifndef HILO_H
+#define HILO_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define HILO_ABI_VERSION 1
+
+typedef enum {
+  HILO_OK = 0,
+  HILO_E_NULL = 1,      /* a required pointer is NULL                                        */
+  HILO_E_SHAPE = 2,     /* grid not even/positive, dim != heads*head_dim, size limits (below) */
+  HILO_E_DTYPE = 3,     /* dtype unknown, or head_dim unsupported for the dtype               */
+  HILO_E_PARAM = 4,     /* selection mode unknown, tau not finite, keep out of [0, NB],       */
+                        /* dilate_r negative                                                  */
+  HILO_E_WORKSPACE = 5, /* workspace smaller than hilo_workspace_bytes()                      */
+  HILO_E_DEVICE = 6     /* a HIP launch failed, or no GPU                                     */
+} hilo_status;
+
+typedef enum { HILO_F32 = 0, HILO_BF16 = 1 } hilo_dtype;
+
+typedef enum { HILO_SELECT_THRESHOLD = 0, HILO_SELECT_TOPK = 1 } hilo_select_mode;
+
+/* Problem shape.  Limits (HILO_E_SHAPE otherwise): grid_h, grid_w even and > 0; N/4 <= 16384;
+ * dim == heads * head_dim, dim % 64 == 0, dim <= 8192 (keeps energies exact in int64 and block
+ * sums exact in double); mlp_dim % 64 == 0; text_len >= 0; T_max < 2^31.
+ * head_dim must be 64 or 128 (HILO_E_DTYPE otherwise).                                         */
+typedef struct {
+  int32_t batch, images, grid_h, grid_w, text_len, dim, heads, head_dim, mlp_dim;
+  int32_t dtype; /* hilo_dtype */
+} hilo_shape;
+
+/* Per-stream weights in nn.Linear layout [out][in], element type `dtype`.  Arrays of two:
+ * index 0 = image tokens, index 1 = text tokens (the same pointers may be given for both).      */
+typedef struct {
+  const void *w_qkv; /* [3D][D]  rows 0..D-1 -> q, D..2D-1 -> k, 2D..3D-1 -> v; head h = cols h*hd */
+  const void *b_qkv; /* [3D]                                                                     */
+  const void *w_o;   /* [D][D]                                                                   */
+  const void *b_o;   /* [D]                                                                      */
+} hilo_attn_w;
+
+typedef struct {
+  const void *w1; /* [F][D]  F = mlp_dim */
+  const void *b1; /* [F]                 */
+  const void *w2; /* [D][F]              */
+  const void *b2; /* [D]                 */
+} hilo_mlp_w;
+
+/* S1 -- frequency energy (Sec. 2.3: spatial-frequency map from two Sobel operators).
+ * For every grid g, patch (i,j) and channel c, with x read as float32 and neighbours clamped to
+ * the grid (replicated border):
+ *   gx = ((x[i-1][j+1] + 2x[i][j+1]) + x[i+1][j+1]) - ((x[i-1][j-1] + 2x[i][j-1]) + x[i+1][j-1])
+ *   gy = ((x[i+1][j-1] + 2x[i+1][j]) + x[i+1][j+1]) - ((x[i-1][j-1] + 2x[i-1][j]) + x[i-1][j+1])
+ *   q  = floor(min(gx*gx + gy*gy, 2^22) * 2^16)   (float32, every operation rounded, no fusion;
+ *                                                  a NaN energy counts as 2^22)
+ *   energy[g][p] = sum over c of q, exact in int64.
+ * x_img [G][N][D] dtype  ->  energy [G][N] int64.                                               */
+hilo_status hilo_score(const hilo_shape *shape, const void *x_img, int64_t *energy, void *stream);
+
+/* S2 -- selection (Sec. 2.3: 16x regional pooling of the frequency map onto the token grid,
+ * threshold on the normalised map, dilated user mask combined with the selection).
+ *   B_b  = sum of the 4 energies of block b (exact);  E_max = max_p energy[g][p]
+ *   F    = blocks holding a patch within Chebyshev distance dilate_r of a force pixel
+ *   THRESHOLD: fine_b = (b in F) or (E_max > 0 and (double)B_b > (4.0 * tau[g]) * (double)E_max)
+ *              i.e. the block's mean normalised energy strictly exceeds tau[g]
+ *   TOPK:      F plus the max(0, keep[g] - |F|) other blocks of largest B_b (ties: lower b first)
+ * Outputs (device): idx_map [G][N] int32 (row of patch p within its grid's compressed tokens),
+ * fine_idx [G][N] int32 (patch of fine row k, k < n_fine; rest unspecified), pool_idx [G][NB]
+ * int32 (block of pooled row k, k < n_pool; rest unspecified), counts [G][2] int32
+ * {n_fine = 4 |fine|, n_pool = NB - |fine|}, cu_seqlens [batch+1] int32, seg_off [G] int32.
+ * force: [G][N] uint8 device pointer (nonzero = inside the user mask) or NULL (no mask).
+ * tau, keep: HOST arrays [G]; only the one the mode uses is read (the other may be NULL).      */
+hilo_status hilo_select(const hilo_shape *shape, const int64_t *energy, const uint8_t *force,
+                        int32_t dilate_r, int32_t mode, const double *tau, const int32_t *keep,
+                        int32_t *idx_map, int32_t *fine_idx, int32_t *pool_idx, int32_t *counts,
+                        int32_t *cu_seqlens, int32_t *seg_off, void *stream);
+
+/* S3 -- compress (Sec. 2.3: selected high-frequency tokens concatenated with low-frequency tokens
+ * along the token dimension).  Row seg_off[g] + k of z is x_img[g][fine_idx[g][k]] for k < n_fine
+ * and ((x00 + x01) + (x10 + x11)) * 0.25 over the 4 patches of block pool_idx[g][k - n_fine]
+ * (float32) for n_fine <= k < n_fine + n_pool; the L text rows of sample s (x_txt [B][L][D]
+ * dtype) follow its image rows.  z [T_max][D] float32; rows past cu_seqlens[batch] untouched.  */
+hilo_status hilo_compress(const hilo_shape *shape, const void *x_img, const void *x_txt,
+                          const int32_t *fine_idx, const int32_t *pool_idx, const int32_t *counts,
+                          const int32_t *cu_seqlens, const int32_t *seg_off, float *z, void *stream);
+
+/* S4 -- attention half of the block, in place on z (MMDiT-style joint attention over the image
+ * and text tokens of each sample; image rows use w[0] / mod stream 0, text rows w[1] / stream 1):
+ *   h = LN(z) * (1 + scale1) + shift1;  qkv = h W_qkv^T + b_qkv
+ *   a = softmax(q k^T / sqrt(head_dim)) v per head over all rows of the sample (no mask)
+ *   z = z + gate1 * (a W_o^T + b_o)
+ * LN: biased variance over D, eps 1e-6, no affine.  mod [batch][2][6][D] float32 holds
+ * shift1, scale1, gate1, shift2, scale2, gate2 per sample and stream.  bf16 products accumulate in
+ * float32; h, qkv and a are rounded to `dtype` in the workspace.  workspace: device scratch of
+ * ws_bytes >= hilo_workspace_bytes(shape), owned by the caller, contents undefined after.        */
+hilo_status hilo_attention(const hilo_shape *shape, float *z, const int32_t *cu_seqlens,
+                           const hilo_attn_w w[2], const float *mod, void *workspace,
+                           size_t ws_bytes, void *stream);
+
+/* S5 -- MLP half of the block, in place on z:
+ *   h2 = LN(z) * (1 + scale2) + shift2;  z = z + gate2 * (GELU_tanh(h2 W1^T + b1) W2^T + b2)
+ * GELU_tanh(u) = 0.5 u (1 + tanh(sqrt(2/pi) (u + 0.044715 u^3))).  Arguments as hilo_attention. */
+hilo_status hilo_mlp(const hilo_shape *shape, float *z, const int32_t *cu_seqlens,
+                     const hilo_mlp_w w[2], const float *mod, void *workspace, size_t ws_bytes,
+                     void *stream);
+
+/* S6 -- decompress: y_img[g][p] = z[seg_off[g] + idx_map[g][p]] (fine tokens scatter back to
+ * their patch, pooled tokens broadcast to the 4 patches of their block), y_txt[s][t] = the text
+ * rows of sample s; both rounded to dtype.  y_img [G][N][D], y_txt [B][L][D] or NULL.           */
+hilo_status hilo_decompress(const hilo_shape *shape, const float *z, const int32_t *idx_map,
+                            const int32_t *cu_seqlens, const int32_t *seg_off, void *y_img,
+                            void *y_txt, void *stream);
+
+/* The attention core alone (the softmax(q k^T / sqrt(hd)) v step of hilo_attention), for
+ * localising parity failures and timing: qkv [T_max][3D] dtype -> out [T_max][D] dtype.        */
+hilo_status hilo_attention_core(const hilo_shape *shape, const void *qkv,
+                                const int32_t *cu_seqlens, void *out, void *stream);
+
+size_t hilo_workspace_bytes(const hilo_shape *shape); /* 0 if the shape is invalid */
+int64_t hilo_max_tokens(const hilo_shape *shape);     /* T_max, or -1 if invalid    */
+const char *hilo_status_str(int32_t status);
+int32_t hilo_abi_version(void);
+
+/* Kernel timing.  While enabled, every kernel the library launches is bracketed by a pair of HIP
+ * events recorded on its launch stream; hilo_profile_read returns, after the caller has
+ * synchronised, the summed milliseconds and launch count of one kernel kind since the last
+ * hilo_profile_enable(1).  kind in [0, hilo_profile_kinds()); hilo_profile_name(kind) names it.
+ * Not thread safe; meant for benchmarks.                                                         */
+hilo_status hilo_profile_enable(int32_t on);
+hilo_status hilo_profile_read(int32_t kind, double *total_ms, int64_t *launches);
+int32_t hilo_profile_kinds(void);
+const char *hilo_profile_name(int32_t kind);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HILO_H */

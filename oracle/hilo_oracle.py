@@ -284,6 +284,37 @@ def _w(weights, sigma: int, name: str) -> np.ndarray:
     return np.asarray(weights[sigma][name], dtype=np.float64)
 
 
+def _attend(q: np.ndarray, k: np.ndarray, v: np.ndarray, heads: int) -> np.ndarray:
+    """softmax(q k^T / sqrt(head_dim)) v per head (columns h*hd .. (h+1)*hd), float64."""
+    D = q.shape[1]
+    hd = D // heads
+    out = np.empty((q.shape[0], D), dtype=np.float64)
+    for hh in range(heads):
+        cols = slice(hh * hd, (hh + 1) * hd)
+        sc = (q[:, cols] @ k[:, cols].T) / np.sqrt(hd)
+        sc = sc - sc.max(axis=1, keepdims=True)
+        p = np.exp(sc)
+        p /= p.sum(axis=1, keepdims=True)
+        out[:, cols] = p @ v[:, cols]
+    return out
+
+
+def attention_core(qkv: np.ndarray, cu: np.ndarray, heads: int,
+                   rows: Optional[np.ndarray] = None) -> np.ndarray:
+    """The attention step alone on a packed [T][3D] projection: every row attends to all rows of
+    its own sample.  Returns a for `rows` (all rows when None), float64 [len(rows)][D]."""
+    qkv = np.asarray(qkv, dtype=np.float64)
+    D = qkv.shape[1] // 3
+    rows = np.arange(int(cu[-1])) if rows is None else np.asarray(rows)
+    out = np.empty((rows.size, D), dtype=np.float64)
+    for s in range(len(cu) - 1):
+        lo, hi = int(cu[s]), int(cu[s + 1])
+        sel = np.flatnonzero((rows >= lo) & (rows < hi))
+        if sel.size:
+            out[sel] = _attend(qkv[rows[sel], :D], qkv[lo:hi, D:2 * D], qkv[lo:hi, 2 * D:], heads)
+    return out
+
+
 def attention(Z: np.ndarray, cu: np.ndarray, text_len: int, heads: int, weights, mod: np.ndarray,
               rows: Optional[np.ndarray] = None) -> np.ndarray:
     """Attention half of an MMDiT-style pre-LN adaLN block with per-stream weights:
@@ -297,7 +328,6 @@ def attention(Z: np.ndarray, cu: np.ndarray, text_len: int, heads: int, weights,
     processed by the DiT; Sec. 2.2: memory-efficient attention).  Returns z1 for `rows` (all rows
     when None), float64 [len(rows)][D]."""
     T, D = Z.shape
-    hd = D // heads
     all_rows = np.arange(T) if rows is None else np.asarray(rows)
     out = np.empty((all_rows.size, D), dtype=np.float64)
     for s in range(len(cu) - 1):
@@ -312,17 +342,7 @@ def attention(Z: np.ndarray, cu: np.ndarray, text_len: int, heads: int, weights,
             h = layer_norm(Z[a:b]) * (1.0 + mod[s, sig, 1]) + mod[s, sig, 0]
             qkv[a - lo:b - lo] = h @ _w(weights, sig, "w_qkv").T + _w(weights, sig, "b_qkv")
         r_loc = all_rows[sel] - lo
-        q = qkv[r_loc, :D]
-        k = qkv[:, D:2 * D]
-        v = qkv[:, 2 * D:]
-        a_out = np.empty((r_loc.size, D), dtype=np.float64)
-        for hh in range(heads):
-            cols = slice(hh * hd, (hh + 1) * hd)
-            sc = (q[:, cols] @ k[:, cols].T) / np.sqrt(hd)
-            sc = sc - sc.max(axis=1, keepdims=True)
-            p = np.exp(sc)
-            p /= p.sum(axis=1, keepdims=True)
-            a_out[:, cols] = p @ v[:, cols]
+        a_out = _attend(qkv[r_loc, :D], qkv[:, D:2 * D], qkv[:, 2 * D:], heads)
         text_start = hi - text_len
         for sig in (0, 1):
             m = (all_rows[sel] >= text_start) if sig == 1 else (all_rows[sel] < text_start)

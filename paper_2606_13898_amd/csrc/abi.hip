@@ -1,0 +1,357 @@
+// C ABI of libhilo: argument validation, workspace layout, kernel sequencing and the optional
+// per-kernel event timing.  Nothing here allocates device memory or synchronises.
+#include <cmath>
+#include <vector>
+
+#include "../../include/hilo.h"
+#include "kernels.h"
+
+using namespace hilo;
+
+namespace {
+
+// ----------------------------------------------------------------------------- kernel timing
+
+enum Kind {
+  K_SCORE, K_SELECT, K_LAYOUT, K_COMPRESS, K_NORM_ATTN, K_GEMM_QKV, K_ATTN_CORE, K_GEMM_O,
+  K_NORM_MLP, K_GEMM_FC1, K_GEMM_FC2, K_DECOMPRESS, K_COUNT
+};
+const char *kKindNames[K_COUNT] = {"score", "select", "layout", "compress", "rownorm_attn",
+                                   "gemm_qkv", "attention_core", "gemm_o", "rownorm_mlp",
+                                   "gemm_fc1", "gemm_fc2", "decompress"};
+
+struct ProfRec {
+  int kind;
+  hipEvent_t a, b;
+};
+bool g_prof = false;
+std::vector<ProfRec> g_recs;
+size_t g_used = 0;
+constexpr size_t kMaxRecs = 1 << 16;
+
+// Runs `launch` bracketed by events when timing is on.
+template <typename F>
+hipError_t timed(int kind, hipStream_t st, F &&launch) {
+  if (!g_prof || g_used >= kMaxRecs) return launch();
+  if (g_used == g_recs.size()) {
+    ProfRec r{kind, nullptr, nullptr};
+    if (hipEventCreate(&r.a) != hipSuccess || hipEventCreate(&r.b) != hipSuccess) return launch();
+    g_recs.push_back(r);
+  }
+  ProfRec &r = g_recs[g_used++];
+  r.kind = kind;
+  hipEventRecord(r.a, st);
+  hipError_t e = launch();
+  hipEventRecord(r.b, st);
+  return e;
+}
+
+// ----------------------------------------------------------------------------- validation
+
+int g_ndev = -1;
+bool have_device() {
+  if (g_ndev < 0) {
+    int n = 0;
+    if (hipGetDeviceCount(&n) != hipSuccess) n = 0;
+    g_ndev = n;
+  }
+  return g_ndev > 0;
+}
+
+hilo_status check_grid(const hilo_shape *s) {
+  if (!s) return HILO_E_NULL;
+  if (s->dtype != HILO_F32 && s->dtype != HILO_BF16) return HILO_E_DTYPE;
+  if (s->batch <= 0 || s->images <= 0 || s->grid_h <= 0 || s->grid_w <= 0) return HILO_E_SHAPE;
+  if ((s->grid_h & 1) || (s->grid_w & 1)) return HILO_E_SHAPE;
+  if (s->text_len < 0) return HILO_E_SHAPE;
+  if (s->dim <= 0 || s->dim % 64 != 0 || s->dim > 8192) return HILO_E_SHAPE;
+  const long long N = (long long)s->grid_h * s->grid_w;
+  if (N / 4 > 16384) return HILO_E_SHAPE;
+  const long long tmax = (long long)s->batch * (s->images * N + s->text_len);
+  if (tmax >= (1LL << 31) / 8) return HILO_E_SHAPE;
+  return HILO_OK;
+}
+
+hilo_status check_block(const hilo_shape *s) {
+  hilo_status e = check_grid(s);
+  if (e != HILO_OK) return e;
+  if (s->heads <= 0 || s->head_dim <= 0 || (long long)s->heads * s->head_dim != s->dim)
+    return HILO_E_SHAPE;
+  if (s->mlp_dim <= 0 || s->mlp_dim % 64 != 0 || s->mlp_dim > 65536) return HILO_E_SHAPE;
+  if (s->head_dim != 64 && s->head_dim != 128) return HILO_E_DTYPE;
+  return HILO_OK;
+}
+
+long long tmax_of(const hilo_shape *s) {
+  return (long long)s->batch * ((long long)s->images * s->grid_h * s->grid_w + s->text_len);
+}
+
+size_t esize(const hilo_shape *s) { return s->dtype == HILO_BF16 ? 2 : 4; }
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+size_t ws_attention(const hilo_shape *s) {
+  const size_t T = size_t(tmax_of(s)), D = size_t(s->dim), e = esize(s);
+  return align256(T * D * e) + align256(T * 3 * D * e);  // h (then a) + qkv
+}
+
+size_t ws_mlp(const hilo_shape *s) {
+  const size_t T = size_t(tmax_of(s)), D = size_t(s->dim), F = size_t(s->mlp_dim), e = esize(s);
+  return align256(T * D * e) + align256(T * F * e);  // h2 + hidden
+}
+
+hilo_status dev_status(hipError_t e) { return e == hipSuccess ? HILO_OK : HILO_E_DEVICE; }
+
+GemmProblem base_problem(const hilo_shape *s, const int32_t *cu, const float *mod) {
+  GemmProblem p{};
+  p.mod = mod;
+  p.D = s->dim;
+  p.cu = cu;
+  p.B = s->batch;
+  p.L = s->text_len;
+  p.max_img_rows = s->images * s->grid_h * s->grid_w;
+  return p;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t hilo_abi_version(void) { return HILO_ABI_VERSION; }
+
+const char *hilo_status_str(int32_t st) {
+  switch (st) {
+    case HILO_OK: return "ok";
+    case HILO_E_NULL: return "required pointer is NULL";
+    case HILO_E_SHAPE: return "invalid or unsupported shape";
+    case HILO_E_DTYPE: return "unsupported dtype or head_dim";
+    case HILO_E_PARAM: return "invalid selection parameter";
+    case HILO_E_WORKSPACE: return "workspace too small";
+    case HILO_E_DEVICE: return "HIP launch failed or no GPU";
+    default: return "unknown status";
+  }
+}
+
+int64_t hilo_max_tokens(const hilo_shape *s) {
+  if (check_grid(s) != HILO_OK) return -1;
+  return tmax_of(s);
+}
+
+size_t hilo_workspace_bytes(const hilo_shape *s) {
+  if (check_block(s) != HILO_OK) return 0;
+  const size_t a = ws_attention(s), m = ws_mlp(s);
+  return a > m ? a : m;
+}
+
+hilo_status hilo_score(const hilo_shape *s, const void *x_img, int64_t *energy, void *stream) {
+  hilo_status e = check_grid(s);
+  if (e != HILO_OK) return e;
+  if (!x_img || !energy) return HILO_E_NULL;
+  if (!have_device()) return HILO_E_DEVICE;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  return dev_status(timed(K_SCORE, st, [&] {
+    return launch_score(s->dtype == HILO_BF16, x_img, reinterpret_cast<long long *>(energy),
+                        s->batch * s->images, s->grid_h, s->grid_w, s->dim, st);
+  }));
+}
+
+hilo_status hilo_select(const hilo_shape *s, const int64_t *energy, const uint8_t *force,
+                        int32_t dilate_r, int32_t mode, const double *tau, const int32_t *keep,
+                        int32_t *idx_map, int32_t *fine_idx, int32_t *pool_idx, int32_t *counts,
+                        int32_t *cu_seqlens, int32_t *seg_off, void *stream) {
+  hilo_status e = check_grid(s);
+  if (e != HILO_OK) return e;
+  if (!energy || !idx_map || !fine_idx || !pool_idx || !counts || !cu_seqlens || !seg_off)
+    return HILO_E_NULL;
+  if (mode != HILO_SELECT_THRESHOLD && mode != HILO_SELECT_TOPK) return HILO_E_PARAM;
+  if (dilate_r < 0) return HILO_E_PARAM;
+  const int G = s->batch * s->images;
+  const int NB = s->grid_h * s->grid_w / 4;
+  if (mode == HILO_SELECT_THRESHOLD) {
+    if (!tau) return HILO_E_NULL;
+    for (int g = 0; g < G; ++g)
+      if (!std::isfinite(tau[g])) return HILO_E_PARAM;
+  } else {
+    if (!keep) return HILO_E_NULL;
+    for (int g = 0; g < G; ++g)
+      if (keep[g] < 0 || keep[g] > NB) return HILO_E_PARAM;
+  }
+  if (!have_device()) return HILO_E_DEVICE;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  const int r = dilate_r > s->grid_h + s->grid_w ? s->grid_h + s->grid_w : dilate_r;
+  hipError_t he = timed(K_SELECT, st, [&] {
+    return launch_select(reinterpret_cast<const long long *>(energy), force, G, s->grid_h,
+                         s->grid_w, r, mode, tau, keep, idx_map, fine_idx, pool_idx, counts, st);
+  });
+  if (he != hipSuccess) return HILO_E_DEVICE;
+  return dev_status(timed(K_LAYOUT, st, [&] {
+    return launch_layout(counts, s->batch, s->images, s->text_len, cu_seqlens, seg_off, st);
+  }));
+}
+
+hilo_status hilo_compress(const hilo_shape *s, const void *x_img, const void *x_txt,
+                          const int32_t *fine_idx, const int32_t *pool_idx, const int32_t *counts,
+                          const int32_t *cu_seqlens, const int32_t *seg_off, float *z,
+                          void *stream) {
+  hilo_status e = check_grid(s);
+  if (e != HILO_OK) return e;
+  if (!x_img || !fine_idx || !pool_idx || !counts || !cu_seqlens || !seg_off || !z)
+    return HILO_E_NULL;
+  if (s->text_len > 0 && !x_txt) return HILO_E_NULL;
+  if (!have_device()) return HILO_E_DEVICE;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  return dev_status(timed(K_COMPRESS, st, [&] {
+    return launch_compress(s->dtype == HILO_BF16, x_img, x_txt, fine_idx, pool_idx, counts,
+                           cu_seqlens, seg_off, z, s->batch, s->images, s->grid_h, s->grid_w,
+                           s->dim, s->text_len, st);
+  }));
+}
+
+hilo_status hilo_decompress(const hilo_shape *s, const float *z, const int32_t *idx_map,
+                            const int32_t *cu_seqlens, const int32_t *seg_off, void *y_img,
+                            void *y_txt, void *stream) {
+  hilo_status e = check_grid(s);
+  if (e != HILO_OK) return e;
+  if (!z || !idx_map || !cu_seqlens || !seg_off || !y_img) return HILO_E_NULL;
+  if (!have_device()) return HILO_E_DEVICE;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  return dev_status(timed(K_DECOMPRESS, st, [&] {
+    return launch_decompress(s->dtype == HILO_BF16, z, idx_map, cu_seqlens, seg_off, y_img,
+                             s->text_len > 0 ? y_txt : nullptr, s->batch, s->images,
+                             s->grid_h * s->grid_w, s->dim, s->text_len, st);
+  }));
+}
+
+hilo_status hilo_attention_core(const hilo_shape *s, const void *qkv, const int32_t *cu_seqlens,
+                                void *out, void *stream) {
+  hilo_status e = check_block(s);
+  if (e != HILO_OK) return e;
+  if (!qkv || !cu_seqlens || !out) return HILO_E_NULL;
+  if (!have_device()) return HILO_E_DEVICE;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  const int max_seq = s->images * s->grid_h * s->grid_w + s->text_len;
+  return dev_status(timed(K_ATTN_CORE, st, [&] {
+    return launch_attention(s->dtype == HILO_BF16, qkv, cu_seqlens, out, s->batch, s->heads,
+                            s->head_dim, max_seq, st);
+  }));
+}
+
+hilo_status hilo_attention(const hilo_shape *s, float *z, const int32_t *cu_seqlens,
+                           const hilo_attn_w w[2], const float *mod, void *workspace,
+                           size_t ws_bytes, void *stream) {
+  hilo_status e = check_block(s);
+  if (e != HILO_OK) return e;
+  if (!z || !cu_seqlens || !w || !mod || !workspace) return HILO_E_NULL;
+  for (int k = 0; k < 2; ++k)
+    if (!w[k].w_qkv || !w[k].b_qkv || !w[k].w_o || !w[k].b_o) return HILO_E_NULL;
+  if (ws_bytes < ws_attention(s)) return HILO_E_WORKSPACE;
+  if (!have_device()) return HILO_E_DEVICE;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  const bool bf = s->dtype == HILO_BF16;
+  const int D = s->dim;
+  const int T = int(tmax_of(s));
+  char *ws = reinterpret_cast<char *>(workspace);
+  void *h = ws;  // LN output, later the attention output
+  void *qkv = ws + align256(size_t(T) * D * esize(s));
+
+  hipError_t he = timed(K_NORM_ATTN, st, [&] {
+    return launch_rownorm(bf, z, cu_seqlens, mod, s->batch, s->text_len, D, T, 0, h, st);
+  });
+  if (he != hipSuccess) return HILO_E_DEVICE;
+
+  GemmProblem p = base_problem(s, cu_seqlens, mod);
+  p.A = h; p.lda = D;
+  p.W[0] = w[0].w_qkv; p.W[1] = w[1].w_qkv;
+  p.bias[0] = w[0].b_qkv; p.bias[1] = w[1].b_qkv;
+  p.N = 3 * D; p.K = D;
+  p.out = qkv; p.ldo = 3 * D;
+  he = timed(K_GEMM_QKV, st, [&] { return launch_gemm(bf, EPI_BIAS, p, st); });
+  if (he != hipSuccess) return HILO_E_DEVICE;
+
+  const int max_seq = s->images * s->grid_h * s->grid_w + s->text_len;
+  he = timed(K_ATTN_CORE, st, [&] {
+    return launch_attention(bf, qkv, cu_seqlens, h, s->batch, s->heads, s->head_dim, max_seq, st);
+  });
+  if (he != hipSuccess) return HILO_E_DEVICE;
+
+  GemmProblem q = base_problem(s, cu_seqlens, mod);
+  q.A = h; q.lda = D;
+  q.W[0] = w[0].w_o; q.W[1] = w[1].w_o;
+  q.bias[0] = w[0].b_o; q.bias[1] = w[1].b_o;
+  q.N = D; q.K = D;
+  q.z = z; q.ldz = D; q.gate_idx = 2;
+  return dev_status(timed(K_GEMM_O, st, [&] { return launch_gemm(bf, EPI_RESID, q, st); }));
+}
+
+hilo_status hilo_mlp(const hilo_shape *s, float *z, const int32_t *cu_seqlens,
+                     const hilo_mlp_w w[2], const float *mod, void *workspace, size_t ws_bytes,
+                     void *stream) {
+  hilo_status e = check_block(s);
+  if (e != HILO_OK) return e;
+  if (!z || !cu_seqlens || !w || !mod || !workspace) return HILO_E_NULL;
+  for (int k = 0; k < 2; ++k)
+    if (!w[k].w1 || !w[k].b1 || !w[k].w2 || !w[k].b2) return HILO_E_NULL;
+  if (ws_bytes < ws_mlp(s)) return HILO_E_WORKSPACE;
+  if (!have_device()) return HILO_E_DEVICE;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  const bool bf = s->dtype == HILO_BF16;
+  const int D = s->dim, F = s->mlp_dim;
+  const int T = int(tmax_of(s));
+  char *ws = reinterpret_cast<char *>(workspace);
+  void *h2 = ws;
+  void *hid = ws + align256(size_t(T) * D * esize(s));
+
+  hipError_t he = timed(K_NORM_MLP, st, [&] {
+    return launch_rownorm(bf, z, cu_seqlens, mod, s->batch, s->text_len, D, T, 1, h2, st);
+  });
+  if (he != hipSuccess) return HILO_E_DEVICE;
+
+  GemmProblem p = base_problem(s, cu_seqlens, mod);
+  p.A = h2; p.lda = D;
+  p.W[0] = w[0].w1; p.W[1] = w[1].w1;
+  p.bias[0] = w[0].b1; p.bias[1] = w[1].b1;
+  p.N = F; p.K = D;
+  p.out = hid; p.ldo = F;
+  he = timed(K_GEMM_FC1, st, [&] { return launch_gemm(bf, EPI_GELU, p, st); });
+  if (he != hipSuccess) return HILO_E_DEVICE;
+
+  GemmProblem q = base_problem(s, cu_seqlens, mod);
+  q.A = hid; q.lda = F;
+  q.W[0] = w[0].w2; q.W[1] = w[1].w2;
+  q.bias[0] = w[0].b2; q.bias[1] = w[1].b2;
+  q.N = D; q.K = F;
+  q.z = z; q.ldz = D; q.gate_idx = 5;
+  return dev_status(timed(K_GEMM_FC2, st, [&] { return launch_gemm(bf, EPI_RESID, q, st); }));
+}
+
+hilo_status hilo_profile_enable(int32_t on) {
+  g_prof = on != 0;
+  if (g_prof) g_used = 0;
+  return HILO_OK;
+}
+
+hilo_status hilo_profile_read(int32_t kind, double *total_ms, int64_t *launches) {
+  if (!total_ms || !launches) return HILO_E_NULL;
+  if (kind < 0 || kind >= K_COUNT) return HILO_E_PARAM;
+  double tot = 0.0;
+  int64_t n = 0;
+  for (size_t i = 0; i < g_used; ++i) {
+    if (g_recs[i].kind != kind) continue;
+    float ms = 0.f;
+    if (hipEventSynchronize(g_recs[i].b) != hipSuccess) return HILO_E_DEVICE;
+    if (hipEventElapsedTime(&ms, g_recs[i].a, g_recs[i].b) != hipSuccess) return HILO_E_DEVICE;
+    tot += ms;
+    ++n;
+  }
+  *total_ms = tot;
+  *launches = n;
+  return HILO_OK;
+}
+
+int32_t hilo_profile_kinds(void) { return K_COUNT; }
+
+const char *hilo_profile_name(int32_t kind) {
+  return (kind >= 0 && kind < K_COUNT) ? kKindNames[kind] : "unknown";
+}
+
+}  // extern "C"

@@ -1,0 +1,328 @@
+// Attention core: a = softmax(q k^T / sqrt(hd)) v per sample and head over the packed ragged
+// sequence (joint attention of a sample's image and text tokens, no mask).
+//
+// bf16 path (gfx950 MFMA v_mfma_f32_16x16x32_bf16, fp32 online softmax in base 2):
+//   workgroup = NW waves x QW query rows of one (sample, head); K/V stream through LDS in tiles of
+//   64 keys, double buffered.  Each wave computes S^T = K Q^T so that every lane owns one query
+//   row's scores (4 keys per 16-key subtile): the running max / sum stay lane-local, and the
+//   probabilities are already in the register layout of the second MFMA operand for
+//   O^T = V^T P^T.  The MFMA's k index may be permuted as long as both operands agree: the lane
+//   holding keys {4g..4g+3} and {16+4g..16+4g+3} of a 32-key step feeds exactly those keys of V^T,
+//   which sits transposed in LDS (written once per tile, read as two 8-byte pieces).
+#include "common.h"
+#include "kernels.h"
+
+namespace hilo {
+
+constexpr float kLog2e = 1.4426950408889634f;
+
+template <int HD, int QW, int NW>
+__global__ __launch_bounds__(NW * 64) void k_attn_bf16(const uint16_t *__restrict__ qkv,
+                                                       const int *__restrict__ cu,
+                                                       uint16_t *__restrict__ out, int heads,
+                                                       int qtiles, float scale_log2) {
+  constexpr int BKV = 64;
+  constexpr int QS = QW / 16;       // query subtiles per wave
+  constexpr int KK = HD / 32;       // k-steps of the score MFMA
+  constexpr int DS = HD / 16;       // d subtiles of the output
+  constexpr int KST = HD + 8;       // K tile row stride (elements)
+  constexpr int VST = BKV + 4;      // V^T tile row stride (elements)
+  constexpr int NT = NW * 64;
+  constexpr int KCH = BKV * HD / 8; // 16-byte chunks of a K tile
+  constexpr int KC = (KCH + NT - 1) / NT;
+  constexpr int VGR = (BKV / 4) * (HD / 8);  // 4-key x 8-dim groups of a V tile
+  constexpr int VC = (VGR + NT - 1) / NT;
+  __shared__ __attribute__((aligned(16))) uint16_t sK[2][BKV * KST];
+  __shared__ __attribute__((aligned(16))) uint16_t sV[2][HD * VST];
+
+  const int t = xcd_remap(blockIdx.x, gridDim.x);
+  const int qt = t % qtiles;
+  const int sh = t / qtiles;
+  const int h = sh % heads;
+  const int s = sh / heads;
+  const int lo = cu[s];
+  const int n = cu[s + 1] - lo;
+  const int q0 = qt * (QW * NW);
+  if (q0 >= n) return;
+  const int D = heads * HD;
+  const size_t ld = size_t(3) * D;
+  const uint16_t *Q = qkv + size_t(lo) * ld + size_t(h) * HD;
+  const uint16_t *Kp = Q + D;
+  const uint16_t *Vp = Q + 2 * D;
+
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int lr = lane & 15, lg = lane >> 4;
+
+  // query fragments (second MFMA operand): row q, dims kk*32 + 8*lg .. +7
+  bf16x8 qf[QS][KK];
+#pragma unroll
+  for (int qs = 0; qs < QS; ++qs) {
+    const int q = min(q0 + wid * QW + qs * 16 + lr, n - 1);
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk)
+      qf[qs][kk] = *reinterpret_cast<const bf16x8 *>(Q + size_t(q) * ld + kk * 32 + 8 * lg);
+  }
+
+  uint4 rk[KC];
+  uint4 rv[VC][4];
+  auto gload = [&](int kv0) {
+#pragma unroll
+    for (int c = 0; c < KC; ++c) {
+      const int idx = tid + c * NT;
+      if (idx < KCH) {
+        const int r = idx / (HD / 8), ch = idx % (HD / 8);
+        const int row = min(kv0 + r, n - 1);
+        rk[c] = *reinterpret_cast<const uint4 *>(Kp + size_t(row) * ld + ch * 8);
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < VC; ++c) {
+      const int gidx = tid + c * NT;
+      if (gidx < VGR) {
+        const int b = gidx % (HD / 8), a = gidx / (HD / 8);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int row = min(kv0 + 4 * a + u, n - 1);
+          rv[c][u] = *reinterpret_cast<const uint4 *>(Vp + size_t(row) * ld + b * 8);
+        }
+      }
+    }
+  };
+  auto sstore = [&](int buf) {
+#pragma unroll
+    for (int c = 0; c < KC; ++c) {
+      const int idx = tid + c * NT;
+      if (idx < KCH) {
+        const int r = idx / (HD / 8), ch = idx % (HD / 8);
+        *reinterpret_cast<uint4 *>(&sK[buf][r * KST + ch * 8]) = rk[c];
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < VC; ++c) {
+      const int gidx = tid + c * NT;
+      if (gidx < VGR) {
+        const int b = gidx % (HD / 8), a = gidx / (HD / 8);
+        // transpose 4 keys x 8 dims -> for each dim, 4 consecutive keys (8 bytes)
+        const uint32_t *w0 = reinterpret_cast<const uint32_t *>(&rv[c][0]);
+        const uint32_t *w1 = reinterpret_cast<const uint32_t *>(&rv[c][1]);
+        const uint32_t *w2 = reinterpret_cast<const uint32_t *>(&rv[c][2]);
+        const uint32_t *w3 = reinterpret_cast<const uint32_t *>(&rv[c][3]);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const int sw = j >> 1;
+          const bool hi = j & 1;
+          const uint32_t e0 = hi ? (w0[sw] >> 16) : (w0[sw] & 0xffffu);
+          const uint32_t e1 = hi ? (w1[sw] >> 16) : (w1[sw] & 0xffffu);
+          const uint32_t e2 = hi ? (w2[sw] >> 16) : (w2[sw] & 0xffffu);
+          const uint32_t e3 = hi ? (w3[sw] >> 16) : (w3[sw] & 0xffffu);
+          uint2 v2;
+          v2.x = e0 | (e1 << 16);
+          v2.y = e2 | (e3 << 16);
+          *reinterpret_cast<uint2 *>(&sV[buf][(b * 8 + j) * VST + 4 * a]) = v2;
+        }
+      }
+    }
+  };
+
+  f32x4 o[QS][DS];
+#pragma unroll
+  for (int qs = 0; qs < QS; ++qs)
+#pragma unroll
+    for (int d = 0; d < DS; ++d) o[qs][d] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float mrun[QS], lrun[QS];
+#pragma unroll
+  for (int qs = 0; qs < QS; ++qs) { mrun[qs] = -INFINITY; lrun[qs] = 0.f; }
+
+  const int nkv = (n + BKV - 1) / BKV;
+  gload(0);
+  sstore(0);
+  __syncthreads();
+  for (int it = 0; it < nkv; ++it) {
+    const int buf = it & 1;
+    const int kv0 = it * BKV;
+    if (it + 1 < nkv) gload(kv0 + BKV);
+
+    // S^T for 64 keys x QW queries: sc[ks][qs][e] = score(query qs*16+lr, key ks*16+4*lg+e)
+    f32x4 sc[4][QS];
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+      for (int qs = 0; qs < QS; ++qs) sc[ks][qs] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) {
+        const bf16x8 kf =
+            *reinterpret_cast<const bf16x8 *>(&sK[buf][(ks * 16 + lr) * KST + kk * 32 + 8 * lg]);
+#pragma unroll
+        for (int qs = 0; qs < QS; ++qs)
+          sc[ks][qs] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[qs][kk], sc[ks][qs], 0, 0, 0);
+      }
+    }
+
+    const bool tail = kv0 + BKV > n;
+    bf16x8 pf[QS][2];
+#pragma unroll
+    for (int qs = 0; qs < QS; ++qs) {
+      float mx = -INFINITY;
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          float v = sc[ks][qs][e] * scale_log2;
+          if (tail && kv0 + ks * 16 + 4 * lg + e >= n) v = -INFINITY;
+          sc[ks][qs][e] = v;
+          mx = fmaxf(mx, v);
+        }
+      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      const float mnew = fmaxf(mrun[qs], mx);
+      const float alpha = exp2f(mrun[qs] - mnew);
+      mrun[qs] = mnew;
+      float psum = 0.f;
+      float pv[4][4];
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          pv[ks][e] = exp2f(sc[ks][qs][e] - mnew);
+          psum += pv[ks][e];
+        }
+      lrun[qs] = lrun[qs] * alpha + psum;
+#pragma unroll
+      for (int d = 0; d < DS; ++d) o[qs][d] *= alpha;
+#pragma unroll
+      for (int kk2 = 0; kk2 < 2; ++kk2) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          pf[qs][kk2][e] = static_cast<__bf16>(pv[2 * kk2][e]);
+          pf[qs][kk2][4 + e] = static_cast<__bf16>(pv[2 * kk2 + 1][e]);
+        }
+      }
+    }
+
+    // O^T += V^T P^T
+#pragma unroll
+    for (int d = 0; d < DS; ++d) {
+#pragma unroll
+      for (int kk2 = 0; kk2 < 2; ++kk2) {
+        const uint16_t *vr = &sV[buf][(d * 16 + lr) * VST + 32 * kk2 + 4 * lg];
+        const uint2 v0 = *reinterpret_cast<const uint2 *>(vr);
+        const uint2 v1 = *reinterpret_cast<const uint2 *>(vr + 16);
+        uint4 vv;
+        vv.x = v0.x; vv.y = v0.y; vv.z = v1.x; vv.w = v1.y;
+        const bf16x8 vf = __builtin_bit_cast(bf16x8, vv);
+#pragma unroll
+        for (int qs = 0; qs < QS; ++qs)
+          o[qs][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[qs][kk2], o[qs][d], 0, 0, 0);
+      }
+    }
+
+    if (it + 1 < nkv) sstore(buf ^ 1);
+    __syncthreads();
+  }
+
+#pragma unroll
+  for (int qs = 0; qs < QS; ++qs) {
+    float l = lrun[qs];
+    l += __shfl_xor(l, 16, 64);
+    l += __shfl_xor(l, 32, 64);
+    const float inv = 1.0f / l;
+    const int q = q0 + wid * QW + qs * 16 + lr;
+    if (q >= n) continue;
+    uint16_t *orow = out + size_t(lo + q) * D + size_t(h) * HD;
+#pragma unroll
+    for (int d = 0; d < DS; ++d) {
+      uint2 u;
+      u.x = pack_bf16x2(o[qs][d][0] * inv, o[qs][d][1] * inv);
+      u.y = pack_bf16x2(o[qs][d][2] * inv, o[qs][d][3] * inv);
+      *reinterpret_cast<uint2 *>(orow + d * 16 + 4 * lg) = u;
+    }
+  }
+}
+
+// fp32 path: one thread per query row, keys/values staged through LDS 32 rows at a time.
+template <int HD>
+__global__ __launch_bounds__(64) void k_attn_f32(const float *__restrict__ qkv,
+                                                 const int *__restrict__ cu, float *__restrict__ out,
+                                                 int heads, int qtiles, float scale_log2) {
+  constexpr int BKV = 32;
+  __shared__ float sK[BKV][HD];
+  __shared__ float sV[BKV][HD];
+  const int qt = blockIdx.x % qtiles;
+  const int sh = blockIdx.x / qtiles;
+  const int h = sh % heads, s = sh / heads;
+  const int lo = cu[s], n = cu[s + 1] - lo;
+  const int q0 = qt * 64;
+  if (q0 >= n) return;
+  const int D = heads * HD;
+  const size_t ld = size_t(3) * D;
+  const int q = min(q0 + int(threadIdx.x), n - 1);
+  float qv[HD], o[HD];
+  for (int d = 0; d < HD; ++d) { qv[d] = qkv[size_t(lo + q) * ld + h * HD + d]; o[d] = 0.f; }
+  float m = -INFINITY, l = 0.f;
+  for (int kv0 = 0; kv0 < n; kv0 += BKV) {
+    __syncthreads();
+    for (int e = threadIdx.x; e < BKV * HD; e += 64) {
+      const int r = e / HD, d = e % HD;
+      const int row = min(kv0 + r, n - 1);
+      sK[r][d] = qkv[size_t(lo + row) * ld + D + h * HD + d];
+      sV[r][d] = qkv[size_t(lo + row) * ld + 2 * D + h * HD + d];
+    }
+    __syncthreads();
+    const int nk = min(BKV, n - kv0);
+    for (int r = 0; r < nk; ++r) {
+      float sdot = 0.f;
+      for (int d = 0; d < HD; ++d) sdot += qv[d] * sK[r][d];
+      const float x = sdot * scale_log2;
+      const float mnew = fmaxf(m, x);
+      const float alpha = exp2f(m - mnew);
+      const float p = exp2f(x - mnew);
+      l = l * alpha + p;
+      for (int d = 0; d < HD; ++d) o[d] = o[d] * alpha + p * sV[r][d];
+      m = mnew;
+    }
+  }
+  if (q0 + int(threadIdx.x) < n) {
+    const float inv = 1.0f / l;
+    for (int d = 0; d < HD; ++d) out[size_t(lo + q) * D + h * HD + d] = o[d] * inv;
+  }
+}
+
+template <int HD, int QW, int NW>
+static hipError_t run_attn_bf16(const void *qkv, const int *cu, void *out, int B, int heads,
+                                int max_seq, hipStream_t st) {
+  const int qtiles = (max_seq + QW * NW - 1) / (QW * NW);
+  const long long nblk = (long long)B * heads * qtiles;
+  if (nblk <= 0) return hipSuccess;
+  const float sl2 = kLog2e / sqrtf(float(HD));
+  hipLaunchKernelGGL((k_attn_bf16<HD, QW, NW>), dim3(unsigned(nblk)), dim3(NW * 64), 0, st,
+                     reinterpret_cast<const uint16_t *>(qkv), cu,
+                     reinterpret_cast<uint16_t *>(out), heads, qtiles, sl2);
+  return hipGetLastError();
+}
+
+template <int HD>
+static hipError_t run_attn_f32(const void *qkv, const int *cu, void *out, int B, int heads,
+                               int max_seq, hipStream_t st) {
+  const int qtiles = (max_seq + 63) / 64;
+  const long long nblk = (long long)B * heads * qtiles;
+  if (nblk <= 0) return hipSuccess;
+  const float sl2 = kLog2e / sqrtf(float(HD));
+  hipLaunchKernelGGL((k_attn_f32<HD>), dim3(unsigned(nblk)), dim3(64), 0, st,
+                     reinterpret_cast<const float *>(qkv), cu, reinterpret_cast<float *>(out),
+                     heads, qtiles, sl2);
+  return hipGetLastError();
+}
+
+hipError_t launch_attention(bool bf16, const void *qkv, const int *cu, void *out, int B, int heads,
+                            int hd, int max_seq, hipStream_t st) {
+  if (bf16) {
+    if (hd == 128) return run_attn_bf16<128, 32, 4>(qkv, cu, out, B, heads, max_seq, st);
+    return run_attn_bf16<64, 32, 4>(qkv, cu, out, B, heads, max_seq, st);
+  }
+  if (hd == 128) return run_attn_f32<128>(qkv, cu, out, B, heads, max_seq, st);
+  return run_attn_f32<64>(qkv, cu, out, B, heads, max_seq, st);
+}
+
+}  // namespace hilo

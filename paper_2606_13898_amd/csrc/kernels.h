@@ -1,0 +1,56 @@
+// Internal launchers of libhilo (host side).  Every launcher enqueues on `st` and returns the
+// launch status; argument validation happens in the C ABI layer before any of these is called.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace hilo {
+
+constexpr int kSelMaxGrids = 64;  // grids per select launch (per-grid parameters ride in kernel args)
+
+hipError_t launch_score(bool bf16, const void *x, long long *E, int G, int H, int W, int D,
+                        hipStream_t st);
+size_t select_lds_bytes(int NB);
+hipError_t launch_select(const long long *E, const uint8_t *force, int G, int H, int W, int r,
+                         int mode, const double *tau, const int *keep, int *idx_map, int *fine_idx,
+                         int *pool_idx, int *counts, hipStream_t st);
+hipError_t launch_layout(const int *counts, int B, int I, int L, int *cu, int *seg, hipStream_t st);
+
+hipError_t launch_compress(bool bf16, const void *x_img, const void *x_txt, const int *fine_idx,
+                           const int *pool_idx, const int *counts, const int *cu, const int *seg,
+                           float *z, int B, int I, int H, int W, int D, int L, hipStream_t st);
+hipError_t launch_decompress(bool bf16, const float *z, const int *idx_map, const int *cu,
+                             const int *seg, void *y_img, void *y_txt, int B, int I, int N, int D,
+                             int L, hipStream_t st);
+// h = LN(z) * (1 + mod[s][stream][which*3 + 1]) + mod[s][stream][which*3], rows < cu[B]
+hipError_t launch_rownorm(bool bf16, const float *z, const int *cu, const float *mod, int B, int L,
+                          int D, int Tmax, int which, void *out, hipStream_t st);
+
+enum Epilogue { EPI_BIAS = 0, EPI_GELU = 1, EPI_RESID = 2 };
+
+// Segment-aware C = A W_sigma^T with the epilogue; rows of sample s split into the image segment
+// (stream 0) and the text segment (stream 1), tiles never straddle a segment.
+struct GemmProblem {
+  const void *A;          // [Tmax][K] dtype (row stride lda)
+  int lda;
+  const void *W[2];       // [N][K] dtype per stream
+  const void *bias[2];    // [N] dtype per stream
+  int N, K;
+  void *out;              // EPI_BIAS / EPI_GELU: [Tmax][ldo] dtype
+  int ldo;
+  float *z;               // EPI_RESID: z[m][n] += gate * (acc + bias)
+  int ldz;
+  const float *mod;       // [B][2][6][D]
+  int gate_idx, D;
+  const int *cu;          // [B+1]
+  int B, L, max_img_rows; // max_img_rows = images * N
+};
+hipError_t launch_gemm(bool bf16, int epi, const GemmProblem &p, hipStream_t st);
+
+// qkv [Tmax][3D] -> out [Tmax][D] (ld = D), per sample and head over cu.
+hipError_t launch_attention(bool bf16, const void *qkv, const int *cu, void *out, int B, int heads,
+                            int hd, int max_seq, hipStream_t st);
+
+}  // namespace hilo

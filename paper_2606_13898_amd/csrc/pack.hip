@@ -1,0 +1,246 @@
+// S3 compress, S6 decompress and the row normalisation feeding the block's projections.
+//
+// All three are HBM-bound row gathers/scatters: every thread moves 16-byte vectors along the
+// contiguous channel axis, so each wave touches whole 1 KiB runs of a row.  Grids are sized for
+// the uncompressed worst case (counts live on the device); surplus row slots exit at once.
+#include "common.h"
+#include "kernels.h"
+
+namespace hilo {
+
+constexpr int kPackThreads = 256;
+constexpr int kPackRows = 4;  // row slots per workgroup
+
+template <bool BF16>
+HILO_DEV void load8(const void *base, size_t elem, float *f) {
+  if constexpr (BF16) {
+    uint4 u = *reinterpret_cast<const uint4 *>(reinterpret_cast<const uint16_t *>(base) + elem);
+    unpack8(u, f);
+  } else {
+    const float4 *p = reinterpret_cast<const float4 *>(reinterpret_cast<const float *>(base) + elem);
+    float4 a = p[0], b = p[1];
+    f[0] = a.x; f[1] = a.y; f[2] = a.z; f[3] = a.w; f[4] = b.x; f[5] = b.y; f[6] = b.z; f[7] = b.w;
+  }
+}
+
+template <bool BF16>
+HILO_DEV void store8(void *base, size_t elem, const float *f) {
+  if constexpr (BF16) {
+    uint4 u;
+    u.x = pack_bf16x2(f[0], f[1]);
+    u.y = pack_bf16x2(f[2], f[3]);
+    u.z = pack_bf16x2(f[4], f[5]);
+    u.w = pack_bf16x2(f[6], f[7]);
+    *reinterpret_cast<uint4 *>(reinterpret_cast<uint16_t *>(base) + elem) = u;
+  } else {
+    float4 *p = reinterpret_cast<float4 *>(reinterpret_cast<float *>(base) + elem);
+    p[0] = make_float4(f[0], f[1], f[2], f[3]);
+    p[1] = make_float4(f[4], f[5], f[6], f[7]);
+  }
+}
+
+HILO_DEV void store8_f32(float *z, size_t elem, const float *f) {
+  float4 *p = reinterpret_cast<float4 *>(z + elem);
+  p[0] = make_float4(f[0], f[1], f[2], f[3]);
+  p[1] = make_float4(f[4], f[5], f[6], f[7]);
+}
+
+// Row slots: [0, G*N) are image rows (grid g, compressed row k = slot % N), then B*L text rows.
+template <bool BF16>
+__global__ __launch_bounds__(kPackThreads) void k_compress(
+    const void *__restrict__ x_img, const void *__restrict__ x_txt, const int *__restrict__ fine_idx,
+    const int *__restrict__ pool_idx, const int *__restrict__ counts, const int *__restrict__ cu,
+    const int *__restrict__ seg, float *__restrict__ z, int G, int N, int W, int D, int L,
+    long long nslots) {
+#pragma clang fp contract(off)
+  const int CGn = D / 8;
+  const long long imgSlots = (long long)G * N;
+  for (int rr = 0; rr < kPackRows; ++rr) {
+    const long long slot = (long long)blockIdx.x * kPackRows + rr;
+    if (slot >= nslots) return;
+    size_t dst, s0, s1 = 0, s2 = 0, s3 = 0;
+    bool pooled = false;
+    const void *src = x_img;
+    if (slot < imgSlots) {
+      const int g = int(slot / N), k = int(slot % N);
+      const int nf = counts[2 * g], np = counts[2 * g + 1];
+      if (k >= nf + np) continue;
+      dst = size_t(seg[g] + k);
+      if (k < nf) {
+        s0 = size_t(g) * N + fine_idx[size_t(g) * N + k];
+      } else {
+        const int b = pool_idx[size_t(g) * (N / 4) + (k - nf)];
+        const int W2 = W / 2;
+        const size_t p00 = size_t(g) * N + size_t(b / W2) * 2 * W + size_t(b % W2) * 2;
+        s0 = p00; s1 = p00 + 1; s2 = p00 + W; s3 = p00 + W + 1;
+        pooled = true;
+      }
+    } else {
+      const long long t = slot - imgSlots;
+      const int s = int(t / L), j = int(t % L);
+      dst = size_t(cu[s + 1] - L + j);
+      s0 = size_t(s) * L + j;
+      src = x_txt;
+    }
+    for (int cg = threadIdx.x; cg < CGn; cg += kPackThreads) {
+      const size_t c = size_t(cg) * 8;
+      float a[8];
+      load8<BF16>(src, s0 * D + c, a);
+      if (pooled) {
+        float b[8], e[8], f[8];
+        load8<BF16>(src, s1 * D + c, b);
+        load8<BF16>(src, s2 * D + c, e);
+        load8<BF16>(src, s3 * D + c, f);
+#pragma unroll
+        for (int v = 0; v < 8; ++v) a[v] = ((a[v] + b[v]) + (e[v] + f[v])) * 0.25f;
+      }
+      store8_f32(z, dst * D + c, a);
+    }
+  }
+}
+
+hipError_t launch_compress(bool bf16, const void *x_img, const void *x_txt, const int *fine_idx,
+                           const int *pool_idx, const int *counts, const int *cu, const int *seg,
+                           float *z, int B, int I, int H, int W, int D, int L, hipStream_t st) {
+  const int G = B * I, N = H * W;
+  const long long nslots = (long long)G * N + (long long)B * L;
+  const long long nblk = (nslots + kPackRows - 1) / kPackRows;
+  if (nblk <= 0) return hipSuccess;
+  if (bf16)
+    hipLaunchKernelGGL(k_compress<true>, dim3(unsigned(nblk)), dim3(kPackThreads), 0, st, x_img,
+                       x_txt, fine_idx, pool_idx, counts, cu, seg, z, G, N, W, D, L, nslots);
+  else
+    hipLaunchKernelGGL(k_compress<false>, dim3(unsigned(nblk)), dim3(kPackThreads), 0, st, x_img,
+                       x_txt, fine_idx, pool_idx, counts, cu, seg, z, G, N, W, D, L, nslots);
+  return hipGetLastError();
+}
+
+// Output row slots: [0, G*N) image patches, then B*L text rows.
+template <bool BF16>
+__global__ __launch_bounds__(kPackThreads) void k_decompress(
+    const float *__restrict__ z, const int *__restrict__ idx_map, const int *__restrict__ cu,
+    const int *__restrict__ seg, void *__restrict__ y_img, void *__restrict__ y_txt, int G, int N,
+    int D, int L, long long nslots) {
+  const int CGn = D / 8;
+  const long long imgSlots = (long long)G * N;
+  for (int rr = 0; rr < kPackRows; ++rr) {
+    const long long slot = (long long)blockIdx.x * kPackRows + rr;
+    if (slot >= nslots) return;
+    size_t src, dst;
+    void *out;
+    if (slot < imgSlots) {
+      const int g = int(slot / N);
+      src = size_t(seg[g]) + size_t(idx_map[slot]);
+      dst = size_t(slot);
+      out = y_img;
+    } else {
+      if (!y_txt) return;
+      const long long t = slot - imgSlots;
+      const int s = int(t / L), j = int(t % L);
+      src = size_t(cu[s + 1] - L + j);
+      dst = size_t(t);
+      out = y_txt;
+    }
+    for (int cg = threadIdx.x; cg < CGn; cg += kPackThreads) {
+      const size_t c = size_t(cg) * 8;
+      const float4 *p = reinterpret_cast<const float4 *>(z + src * D + c);
+      float4 a = p[0], b = p[1];
+      float f[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+      store8<BF16>(out, dst * D + c, f);
+    }
+  }
+}
+
+hipError_t launch_decompress(bool bf16, const float *z, const int *idx_map, const int *cu,
+                             const int *seg, void *y_img, void *y_txt, int B, int I, int N, int D,
+                             int L, hipStream_t st) {
+  const int G = B * I;
+  const long long nslots = (long long)G * N + (long long)B * L;
+  const long long nblk = (nslots + kPackRows - 1) / kPackRows;
+  if (nblk <= 0) return hipSuccess;
+  if (bf16)
+    hipLaunchKernelGGL(k_decompress<true>, dim3(unsigned(nblk)), dim3(kPackThreads), 0, st, z,
+                       idx_map, cu, seg, y_img, y_txt, G, N, D, L, nslots);
+  else
+    hipLaunchKernelGGL(k_decompress<false>, dim3(unsigned(nblk)), dim3(kPackThreads), 0, st, z,
+                       idx_map, cu, seg, y_img, y_txt, G, N, D, L, nslots);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------------------- row norm
+
+constexpr int kNormMaxV = 32;  // float4 per lane: D <= 8192
+
+// One wave per row: LN(z) (biased variance, eps 1e-6) * (1 + scale) + shift for the row's sample
+// and stream, written in the projection's input dtype.
+template <bool BF16>
+__global__ __launch_bounds__(256) void k_rownorm(const float *__restrict__ z, const int *__restrict__ cu,
+                                                 const float *__restrict__ mod, int B, int L, int D,
+                                                 int Tmax, int which, void *__restrict__ out) {
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= Tmax || row >= cu[B]) return;
+  const int s = sample_of_row(cu, B, row);
+  const int sigma = row >= cu[s + 1] - L ? 1 : 0;
+  const float *shift = mod + (size_t(s * 2 + sigma) * 6 + which * 3) * D;
+  const float *scale = shift + D;
+  const float *zr = z + size_t(row) * D;
+  float4 v[kNormMaxV];
+  float sum = 0.f;
+#pragma unroll
+  for (int k = 0; k < kNormMaxV; ++k) {
+    const int c = (k * 64 + lane) * 4;
+    if (c < D) {
+      v[k] = *reinterpret_cast<const float4 *>(zr + c);
+      sum += (v[k].x + v[k].y) + (v[k].z + v[k].w);
+    }
+  }
+  const float mean = wave_sum_f32(sum) / float(D);
+  float sq = 0.f;
+#pragma unroll
+  for (int k = 0; k < kNormMaxV; ++k) {
+    const int c = (k * 64 + lane) * 4;
+    if (c < D) {
+      const float a = v[k].x - mean, b = v[k].y - mean, e = v[k].z - mean, f = v[k].w - mean;
+      sq += (a * a + b * b) + (e * e + f * f);
+    }
+  }
+  const float var = wave_sum_f32(sq) / float(D);
+  const float rstd = 1.0f / sqrtf(var + 1e-6f);
+#pragma unroll
+  for (int k = 0; k < kNormMaxV; ++k) {
+    const int c = (k * 64 + lane) * 4;
+    if (c < D) {
+      const float4 sc = *reinterpret_cast<const float4 *>(scale + c);
+      const float4 sh = *reinterpret_cast<const float4 *>(shift + c);
+      const float h0 = (v[k].x - mean) * rstd * (1.f + sc.x) + sh.x;
+      const float h1 = (v[k].y - mean) * rstd * (1.f + sc.y) + sh.y;
+      const float h2 = (v[k].z - mean) * rstd * (1.f + sc.z) + sh.z;
+      const float h3 = (v[k].w - mean) * rstd * (1.f + sc.w) + sh.w;
+      if constexpr (BF16) {
+        uint2 u;
+        u.x = pack_bf16x2(h0, h1);
+        u.y = pack_bf16x2(h2, h3);
+        *reinterpret_cast<uint2 *>(reinterpret_cast<uint16_t *>(out) + size_t(row) * D + c) = u;
+      } else {
+        *reinterpret_cast<float4 *>(reinterpret_cast<float *>(out) + size_t(row) * D + c) =
+            make_float4(h0, h1, h2, h3);
+      }
+    }
+  }
+}
+
+hipError_t launch_rownorm(bool bf16, const float *z, const int *cu, const float *mod, int B, int L,
+                          int D, int Tmax, int which, void *out, hipStream_t st) {
+  const int nblk = (Tmax + 3) / 4;
+  if (nblk <= 0) return hipSuccess;
+  if (bf16)
+    hipLaunchKernelGGL(k_rownorm<true>, dim3(nblk), dim3(256), 0, st, z, cu, mod, B, L, D, Tmax,
+                       which, out);
+  else
+    hipLaunchKernelGGL(k_rownorm<false>, dim3(nblk), dim3(256), 0, st, z, cu, mod, B, L, D, Tmax,
+                       which, out);
+  return hipGetLastError();
+}
+
+}  // namespace hilo

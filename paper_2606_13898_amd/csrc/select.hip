@@ -1,0 +1,393 @@
+// S1 score and S2 select kernels (HiLo-Token, Sec. 2.3 "HiLo-Token Selection").
+//
+// k_score    one read of the latent grid: per patch the Sobel energy of every channel, floored to
+//            2^-16 fixed point and summed exactly over channels (bit-reproducible in any order).
+// k_select   one workgroup per grid: 2x2 block sums, E_max, dilated forced blocks, threshold or
+//            top-k (MSB radix select on the exact 53-bit block sums), then the ordered prefix sums
+//            that produce the compressed grid's index map.
+// k_layout   row offsets of grids and samples in the packed sequence.
+#include "common.h"
+#include "kernels.h"
+
+namespace hilo {
+
+// ------------------------------------------------------------------------------------------ S1
+
+// Channels per 16-byte load.
+template <bool BF16> struct ScoreVec { static constexpr int V = BF16 ? 8 : 4; };
+
+template <bool BF16>
+HILO_DEV void load_vec(const void *base, size_t elem, float *f) {
+  if constexpr (BF16) {
+    uint4 u = *reinterpret_cast<const uint4 *>(reinterpret_cast<const uint16_t *>(base) + elem);
+    unpack8(u, f);
+  } else {
+    float4 u = *reinterpret_cast<const float4 *>(reinterpret_cast<const float *>(base) + elem);
+    f[0] = u.x; f[1] = u.y; f[2] = u.z; f[3] = u.w;
+  }
+}
+
+// Workgroup = one row i of one grid, TJ consecutive patches j0..j0+TJ-1; threads split the
+// channels in 16-byte groups and slide a 3x3 window of columns along j.
+template <bool BF16, int TJ>
+__global__ __launch_bounds__(512) void k_score(const void *__restrict__ x, long long *__restrict__ E,
+                                               int H, int W, int D, int tilesJ) {
+#pragma clang fp contract(off)
+  constexpr int V = ScoreVec<BF16>::V;
+  const int CG = D / V;
+  const int t = xcd_remap(blockIdx.x, gridDim.x);
+  const int jt = t % tilesJ;
+  const int gi = t / tilesJ;  // g * H + i
+  const int i = gi % H;
+  const int g = gi / H;
+  const int j0 = jt * TJ;
+  const int nj = min(TJ, W - j0);
+  const size_t rU = (size_t(g) * H + max(i - 1, 0)) * W;
+  const size_t rM = (size_t(g) * H + i) * W;
+  const size_t rD = (size_t(g) * H + min(i + 1, H - 1)) * W;
+
+  // Each per-channel term is an integer < 2^38 held exactly in a float; partial sums stay below
+  // D * 2^38 <= 2^51, so double accumulation is exact and independent of order.
+  double acc[TJ];
+#pragma unroll
+  for (int k = 0; k < TJ; ++k) acc[k] = 0.0;
+
+  for (int cg = threadIdx.x; cg < CG; cg += blockDim.x) {
+    const size_t c0 = size_t(cg) * V;
+    float Lu[V], Lm[V], Ld[V], Cu[V], Cm[V], Cd[V], Ru[V], Rm[V], Rd[V];
+    const int jl = max(j0 - 1, 0);
+    load_vec<BF16>(x, (rU + jl) * D + c0, Lu);
+    load_vec<BF16>(x, (rM + jl) * D + c0, Lm);
+    load_vec<BF16>(x, (rD + jl) * D + c0, Ld);
+    load_vec<BF16>(x, (rU + j0) * D + c0, Cu);
+    load_vec<BF16>(x, (rM + j0) * D + c0, Cm);
+    load_vec<BF16>(x, (rD + j0) * D + c0, Cd);
+#pragma unroll
+    for (int k = 0; k < TJ; ++k) {
+      if (k < nj) {
+        const int jr = min(j0 + k + 1, W - 1);
+        load_vec<BF16>(x, (rU + jr) * D + c0, Ru);
+        load_vec<BF16>(x, (rM + jr) * D + c0, Rm);
+        load_vec<BF16>(x, (rD + jr) * D + c0, Rd);
+        double dpart = 0.0;
+#pragma unroll
+        for (int v = 0; v < V; ++v) {
+          // horizontal: right column minus left column, rows weighted 1, 2, 1
+          float gx = ((Ru[v] + 2.0f * Rm[v]) + Rd[v]) - ((Lu[v] + 2.0f * Lm[v]) + Ld[v]);
+          // vertical: lower row minus upper row, columns weighted 1, 2, 1
+          float gy = ((Ld[v] + 2.0f * Cd[v]) + Rd[v]) - ((Lu[v] + 2.0f * Cu[v]) + Ru[v]);
+          float t1 = gx * gx;
+          float t2 = gy * gy;
+          float e = t1 + t2;
+          float q = floorf(fminf(e, 4194304.0f) * 65536.0f);  // fminf(NaN, cap) = cap
+          dpart += double(q);
+        }
+        acc[k] += dpart;
+#pragma unroll
+        for (int v = 0; v < V; ++v) {
+          Lu[v] = Cu[v]; Lm[v] = Cm[v]; Ld[v] = Cd[v];
+          Cu[v] = Ru[v]; Cm[v] = Rm[v]; Cd[v] = Rd[v];
+        }
+      }
+    }
+  }
+
+  __shared__ long long red[TJ][8];
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, nw = blockDim.x >> 6;
+#pragma unroll
+  for (int k = 0; k < TJ; ++k) {
+    long long s = wave_sum_i64(static_cast<long long>(acc[k]));
+    if (lane == 0) red[k][wid] = s;
+  }
+  __syncthreads();
+  if (threadIdx.x < nj) {
+    long long s = 0;
+    for (int w = 0; w < nw; ++w) s += red[threadIdx.x][w];
+    E[rM + j0 + threadIdx.x] = s;
+  }
+}
+
+constexpr int kScoreTJ = 8;
+
+hipError_t launch_score(bool bf16, const void *x, long long *E, int G, int H, int W, int D,
+                        hipStream_t st) {
+  const int V = bf16 ? 8 : 4;
+  const int CG = D / V;
+  int threads = ((CG + 63) / 64) * 64;
+  if (threads > 512) threads = 512;
+  const int tilesJ = (W + kScoreTJ - 1) / kScoreTJ;
+  const long long nblk = (long long)G * H * tilesJ;
+  if (nblk <= 0) return hipSuccess;
+  if (bf16)
+    hipLaunchKernelGGL((k_score<true, kScoreTJ>), dim3(unsigned(nblk)), dim3(threads), 0, st, x, E,
+                       H, W, D, tilesJ);
+  else
+    hipLaunchKernelGGL((k_score<false, kScoreTJ>), dim3(unsigned(nblk)), dim3(threads), 0, st, x, E,
+                       H, W, D, tilesJ);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------------------------------ S2
+
+constexpr int kSelThreads = 1024;
+constexpr int kSelWaves = kSelThreads / 64;
+
+// Exclusive prefix sum over the workgroup in thread order; `total` receives the sum.
+HILO_DEV int block_excl_scan(int v, int *tmp, int &total) {
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  int x = v;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    int y = __shfl_up(x, off, 64);
+    if (lane >= off) x += y;
+  }
+  if (lane == 63) tmp[wid] = x;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int run = 0;
+    for (int w = 0; w < kSelWaves; ++w) {
+      int t = tmp[w];
+      tmp[w] = run;
+      run += t;
+    }
+    tmp[kSelWaves] = run;
+  }
+  __syncthreads();
+  const int excl = tmp[wid] + x - v;
+  total = tmp[kSelWaves];
+  __syncthreads();
+  return excl;
+}
+
+HILO_DEV long long block_max_i64(long long v, long long *tmp) {
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  v = wave_max_i64(v);
+  if (lane == 0) tmp[wid] = v;
+  __syncthreads();
+  long long m = tmp[0];
+  for (int w = 1; w < kSelWaves; ++w) m = tmp[w] > m ? tmp[w] : m;
+  __syncthreads();
+  return m;
+}
+
+struct SelChunk {
+  double tau[kSelMaxGrids];
+  int keep[kSelMaxGrids];
+};
+
+// flag bits per block: 1 = fine by score, 2 = forced by the dilated mask
+__global__ __launch_bounds__(kSelThreads) void k_select(
+    const long long *__restrict__ E, const uint8_t *__restrict__ force, int H, int W, int r,
+    int mode, SelChunk prm, int g0, int *__restrict__ idx_map, int *__restrict__ fine_idx,
+    int *__restrict__ pool_idx, int *__restrict__ counts) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  const int gl = blockIdx.x;
+  const int g = g0 + gl;
+  const int N = H * W, NB = N / 4, W2 = W / 2;
+  const int tid = threadIdx.x;
+  long long *Bs = reinterpret_cast<long long *>(smem);                 // [NB] block sums
+  uint8_t *flag = reinterpret_cast<uint8_t *>(Bs + NB);                  // [NB]
+  int *itmp = reinterpret_cast<int *>(flag + ((NB + 15) & ~15));         // [kSelWaves + 1]
+  int *hist = itmp + 32;                                                 // [256]
+  long long *ltmp = reinterpret_cast<long long *>(hist + 256);          // [kSelWaves]
+  int *bcast = reinterpret_cast<int *>(ltmp + kSelWaves);               // [4]
+  const long long *Eg = E + size_t(g) * N;
+
+  // block sums and the grid maximum
+  long long mx = 0;
+  for (int b = tid; b < NB; b += kSelThreads) {
+    const int I = b / W2, J = b % W2;
+    const int p = 2 * I * W + 2 * J;
+    const long long e00 = Eg[p], e01 = Eg[p + 1], e10 = Eg[p + W], e11 = Eg[p + W + 1];
+    Bs[b] = ((e00 + e01) + e10) + e11;
+    long long m = e00 > e01 ? e00 : e01;
+    long long m2 = e10 > e11 ? e10 : e11;
+    m = m > m2 ? m : m2;
+    mx = m > mx ? m : mx;
+    uint8_t f = 0;
+    if (force) {
+      const uint8_t *Fg = force + size_t(g) * N;
+      const int i0 = max(2 * I - r, 0), i1 = min(2 * I + 1 + r, H - 1);
+      const int jj0 = max(2 * J - r, 0), jj1 = min(2 * J + 1 + r, W - 1);
+      for (int ii = i0; ii <= i1 && !f; ++ii)
+        for (int jj = jj0; jj <= jj1; ++jj)
+          if (Fg[ii * W + jj]) { f = 2; break; }
+    }
+    flag[b] = f;
+  }
+  const long long emax = block_max_i64(mx, ltmp);  // includes a barrier: Bs and flag visible
+
+  if (mode == 0) {  // threshold
+    if (emax > 0) {
+      const double rhs = (4.0 * prm.tau[gl]) * double(emax);
+      for (int b = tid; b < NB; b += kSelThreads)
+        if (double(Bs[b]) > rhs) flag[b] |= 1;
+    }
+    __syncthreads();
+  } else {  // top-k
+    int nf_local = 0;
+    for (int b = tid; b < NB; b += kSelThreads) nf_local += (flag[b] & 2) ? 1 : 0;
+    int nF;
+    (void)block_excl_scan(nf_local, itmp, nF);
+    const int kp = max(0, prm.keep[gl] - nF);
+    const int nN = NB - nF;
+    if (kp >= nN) {
+      for (int b = tid; b < NB; b += kSelThreads) flag[b] |= 1;
+      __syncthreads();
+    } else if (kp > 0) {
+      // MSB radix select of the kp-th largest block sum among non-forced blocks (sums < 2^53).
+      long long prefix = 0, mask = 0;
+      int rem = kp;
+      for (int shift = 48; shift >= 0; shift -= 8) {
+        for (int d = tid; d < 256; d += kSelThreads) hist[d] = 0;
+        __syncthreads();
+        for (int b = tid; b < NB; b += kSelThreads) {
+          if (!(flag[b] & 2) && (Bs[b] & mask) == prefix)
+            atomicAdd(&hist[(Bs[b] >> shift) & 255], 1);
+        }
+        __syncthreads();
+        if (tid < 64) {
+          // lane l owns digits 255-4l .. 252-4l (descending); find the digit where the count of
+          // larger-or-equal candidates reaches rem
+          int h[4], s = 0;
+#pragma unroll
+          for (int u = 0; u < 4; ++u) { h[u] = hist[255 - 4 * tid - u]; s += h[u]; }
+          int x = s;
+#pragma unroll
+          for (int off = 1; off < 64; off <<= 1) {
+            int y = __shfl_up(x, off, 64);
+            if (tid >= off) x += y;
+          }
+          const int excl = x - s;
+          if (excl < rem && rem <= x) {
+            int cum = excl, d = 0;
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+              if (cum + h[u] >= rem) { d = 255 - 4 * tid - u; break; }
+              cum += h[u];
+            }
+            bcast[0] = d;
+            bcast[1] = rem - cum;
+          }
+        }
+        __syncthreads();
+        prefix |= (long long)bcast[0] << shift;
+        mask |= 255LL << shift;
+        rem = bcast[1];
+        __syncthreads();
+      }
+      // all candidates above the threshold value, and the first `rem` equal ones in block order
+      const int chunk = (NB + kSelThreads - 1) / kSelThreads;
+      const int b0 = tid * chunk, b1 = min(b0 + chunk, NB);
+      int neq = 0;
+      for (int b = b0; b < b1; ++b)
+        if (!(flag[b] & 2) && Bs[b] == prefix) ++neq;
+      int tot;
+      int before = block_excl_scan(neq, itmp, tot);
+      for (int b = b0; b < b1; ++b) {
+        if (flag[b] & 2) continue;
+        if (Bs[b] > prefix) flag[b] |= 1;
+        else if (Bs[b] == prefix) {
+          if (before < rem) flag[b] |= 1;
+          ++before;
+        }
+      }
+      __syncthreads();
+    }
+  }
+
+  // pooled blocks: ranks in block order (stored over the no longer needed block sums)
+  int *prank = reinterpret_cast<int *>(Bs);
+  {
+    const int chunk = (NB + kSelThreads - 1) / kSelThreads;
+    const int b0 = tid * chunk, b1 = min(b0 + chunk, NB);
+    int np = 0;
+    for (int b = b0; b < b1; ++b) np += flag[b] ? 0 : 1;
+    __syncthreads();  // every thread has read Bs-derived flags before prank overwrites Bs
+    int ntot;
+    int rk = block_excl_scan(np, itmp, ntot);
+    for (int b = b0; b < b1; ++b) {
+      if (!flag[b]) {
+        prank[b] = rk;
+        pool_idx[size_t(g) * NB + rk] = b;
+        ++rk;
+      }
+    }
+    if (tid == 0) counts[2 * g + 1] = ntot;
+  }
+  __syncthreads();
+  // fine patches: ranks in raster order; pooled patches point at their block's row
+  {
+    const int chunk = (N + kSelThreads - 1) / kSelThreads;
+    const int p0 = tid * chunk, p1 = min(p0 + chunk, N);
+    int nfl = 0;
+    for (int p = p0; p < p1; ++p) {
+      const int i = p / W, j = p % W;
+      nfl += flag[(i >> 1) * W2 + (j >> 1)] ? 1 : 0;
+    }
+    int nfine;
+    int rk = block_excl_scan(nfl, itmp, nfine);
+    int *im = idx_map + size_t(g) * N;
+    int *fi = fine_idx + size_t(g) * N;
+    for (int p = p0; p < p1; ++p) {
+      const int i = p / W, j = p % W;
+      const int b = (i >> 1) * W2 + (j >> 1);
+      if (flag[b]) {
+        fi[rk] = p;
+        im[p] = rk;
+        ++rk;
+      } else {
+        im[p] = nfine + prank[b];
+      }
+    }
+    if (tid == 0) counts[2 * g] = nfine;
+  }
+}
+
+size_t select_lds_bytes(int NB) {
+  return size_t(NB) * 8 + ((NB + 15) & ~15) + 32 * 4 + 256 * 4 + kSelWaves * 8 + 16;
+}
+
+hipError_t launch_select(const long long *E, const uint8_t *force, int G, int H, int W, int r,
+                         int mode, const double *tau, const int *keep, int *idx_map, int *fine_idx,
+                         int *pool_idx, int *counts, hipStream_t st) {
+  const int NB = H * W / 4;
+  const size_t lds = select_lds_bytes(NB);
+  for (int g0 = 0; g0 < G; g0 += kSelMaxGrids) {
+    const int n = min(kSelMaxGrids, G - g0);
+    SelChunk c;
+    for (int k = 0; k < kSelMaxGrids; ++k) {
+      c.tau[k] = (mode == 0 && k < n) ? tau[g0 + k] : 0.0;
+      c.keep[k] = (mode == 1 && k < n) ? keep[g0 + k] : 0;
+    }
+    hipLaunchKernelGGL(k_select, dim3(n), dim3(kSelThreads), lds, st, E, force, H, W, r, mode, c,
+                       g0, idx_map, fine_idx, pool_idx, counts);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+__global__ void k_layout(const int *__restrict__ counts, int B, int I, int L, int *__restrict__ cu,
+                         int *__restrict__ seg) {
+  if (threadIdx.x != 0) return;
+  int row = 0;
+  cu[0] = 0;
+  for (int s = 0; s < B; ++s) {
+    for (int i = 0; i < I; ++i) {
+      const int g = s * I + i;
+      seg[g] = row;
+      row += counts[2 * g] + counts[2 * g + 1];
+    }
+    row += L;
+    cu[s + 1] = row;
+  }
+}
+
+hipError_t launch_layout(const int *counts, int B, int I, int L, int *cu, int *seg,
+                         hipStream_t st) {
+  hipLaunchKernelGGL(k_layout, dim3(1), dim3(64), 0, st, counts, B, I, L, cu, seg);
+  return hipGetLastError();
+}
+
+}  // namespace hilo

@@ -263,7 +263,7 @@ def make_workload(name: str, *, with_block: bool = True, keep_frac: Optional[flo
             reg = square_mask(c_reg, h, w, 12)
         elif name == "h2048":
             reg = region_mask(c_reg, h, w, 0.20, 0.03)
-        elif name.startswith("small"):
+        elif name not in SHAPES or name.startswith("small"):
             reg = region_mask(c_reg, h, w, 0.35, 0.10, 1, 3)
         else:
             reg = region_mask(c_reg, h, w, 0.35, 0.03)
@@ -287,7 +287,7 @@ def make_workload(name: str, *, with_block: bool = True, keep_frac: Optional[flo
     elif name == "ragged" or name.startswith("small"):
         keep = np.round(c_frac.uniform(0.05, 0.95, size=G) * NB).astype(np.int32)
     else:
-        keep = np.full(G, int(round(fracs[name] * NB)), dtype=np.int32)
+        keep = np.full(G, int(round(fracs.get(name, 0.4) * NB)), dtype=np.int32)
 
     weights = mod = None
     if with_block:

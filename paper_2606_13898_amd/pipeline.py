@@ -1,0 +1,87 @@
+"""Device buffers for one compressed-block problem and the six library calls in order.
+
+torch is used here for device memory and streams only; every step is a libhilo kernel.
+"""
+from __future__ import annotations
+
+from typing import Optional, Sequence
+
+import numpy as np
+import torch
+
+from . import hilo
+from .inputs import Workload
+
+
+def _dev(a: np.ndarray, dtype: torch.dtype, device) -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(a)).to(dtype).to(device)
+
+
+class DeviceBlock:
+    """All inputs, outputs and scratch of one workload, resident on `device`."""
+
+    def __init__(self, wl: Workload, device: str = "cuda", with_block: bool = True):
+        s = wl.shape
+        self.wl = wl
+        self.shape = hilo.make_shape(s)
+        self.dtype = hilo.TORCH_DTYPES[self.shape.dtype]
+        G, N, NB, B, D, L = s.grids, s.n_patches, s.n_blocks, s.batch, s.dim, s.text_len
+        self.T = hilo.hilo_max_tokens(self.shape)
+        if self.T < 0:
+            raise ValueError(f"invalid shape {s}")
+        self.x_img = _dev(wl.x_img, self.dtype, device)
+        self.x_txt = _dev(wl.x_txt, self.dtype, device)
+        self.force = _dev(wl.force, torch.uint8, device) if wl.force is not None else None
+        i32, i64 = torch.int32, torch.int64
+        self.energy = torch.empty(G, N, dtype=i64, device=device)
+        self.idx_map = torch.empty(G, N, dtype=i32, device=device)
+        self.fine_idx = torch.empty(G, N, dtype=i32, device=device)
+        self.pool_idx = torch.empty(G, NB, dtype=i32, device=device)
+        self.counts = torch.empty(G, 2, dtype=i32, device=device)
+        self.cu = torch.empty(B + 1, dtype=i32, device=device)
+        self.seg = torch.empty(G, dtype=i32, device=device)
+        self.z = torch.empty(self.T, D, dtype=torch.float32, device=device)
+        self.y_img = torch.empty(G, N, D, dtype=self.dtype, device=device)
+        self.y_txt = torch.empty(B, L, D, dtype=self.dtype, device=device) if L > 0 else None
+        self.with_block = with_block
+        if with_block:
+            self.weights = [{k: _dev(v, self.dtype, device) for k, v in w.items()} for w in wl.weights]
+            self.mod = _dev(wl.mod, torch.float32, device)
+            self.ws = torch.empty(hilo.hilo_workspace_bytes(self.shape), dtype=torch.uint8, device=device)
+            self.aw = hilo.attn_weights(self.weights)
+            self.mw = hilo.mlp_weights(self.weights)
+
+    # -- the six steps ---------------------------------------------------------------------
+    def score(self, stream=None):
+        hilo.hilo_score(self.shape, self.x_img, self.energy, stream)
+
+    def select(self, mode: int = hilo.TOPK, keep: Optional[Sequence[int]] = None,
+               tau: Optional[Sequence[float]] = None, dilate_r: Optional[int] = None, stream=None):
+        keep = self.wl.keep if (keep is None and mode == hilo.TOPK) else keep
+        r = self.wl.dilate_r if dilate_r is None else dilate_r
+        hilo.hilo_select(self.shape, self.energy, self.force, r, mode, tau, keep, self.idx_map,
+                         self.fine_idx, self.pool_idx, self.counts, self.cu, self.seg, stream)
+
+    def compress(self, stream=None):
+        hilo.hilo_compress(self.shape, self.x_img, self.x_txt, self.fine_idx, self.pool_idx,
+                           self.counts, self.cu, self.seg, self.z, stream)
+
+    def attention(self, stream=None):
+        hilo.hilo_attention(self.shape, self.z, self.cu, self.aw, self.mod, self.ws, stream)
+
+    def mlp(self, stream=None):
+        hilo.hilo_mlp(self.shape, self.z, self.cu, self.mw, self.mod, self.ws, stream)
+
+    def decompress(self, stream=None):
+        hilo.hilo_decompress(self.shape, self.z, self.idx_map, self.cu, self.seg, self.y_img,
+                             self.y_txt, stream)
+
+    def run(self, mode: int = hilo.TOPK, keep=None, tau=None, dilate_r=None, stream=None):
+        """One pass of the whole hot path: score, select, compress, attention, MLP, decompress."""
+        self.score(stream)
+        self.select(mode, keep, tau, dilate_r, stream)
+        self.compress(stream)
+        if self.with_block:
+            self.attention(stream)
+            self.mlp(stream)
+        self.decompress(stream)

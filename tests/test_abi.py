@@ -1,0 +1,157 @@
+"""The C-ABI library on the host: it loads, exports every declared entry point, and validates its
+arguments before touching a device (CPU only; no kernel is launched here)."""
+import ctypes
+import math
+import os
+import re
+
+import pytest
+import torch
+
+from paper_2606_13898_amd import hilo
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "hilo.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(hilo.LIB_PATH), reason="libhilo.so not built")
+
+
+def declared_symbols():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(hilo_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol():
+    L = hilo.lib()
+    names = declared_symbols()
+    assert len(names) >= 15
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_version_and_status_strings():
+    assert hilo.hilo_abi_version() == 1
+    for st in range(7):
+        assert hilo.status_str(st)
+    assert hilo.status_str(99) == "unknown status"
+
+
+def good_shape(dtype=hilo.BF16):
+    return hilo.hilo_shape(2, 1, 8, 10, 5, 256, 2, 128, 1024, dtype)
+
+
+def test_max_tokens_and_workspace():
+    s = good_shape()
+    assert hilo.hilo_max_tokens(s) == 2 * (80 + 5)
+    T = 170
+    want = max(-(-T * 256 * 2 // 256) * 256 + -(-T * 768 * 2 // 256) * 256,
+               -(-T * 256 * 2 // 256) * 256 + -(-T * 1024 * 2 // 256) * 256)
+    assert hilo.hilo_workspace_bytes(s) == want
+    bad = good_shape()
+    bad.grid_h = 7
+    assert hilo.hilo_max_tokens(bad) == -1
+    assert hilo.hilo_workspace_bytes(bad) == 0
+
+
+FAKE = 0x1000  # never dereferenced: validation rejects or the missing device stops the call
+
+
+def call_score(shape, x=FAKE, e=FAKE):
+    return hilo.lib().hilo_score(ctypes.byref(shape), x, e, None)
+
+
+def call_select(shape, mode=hilo.TOPK, tau=None, keep=None, r=0, ptrs=FAKE):
+    G = shape.batch * shape.images if shape.batch > 0 and shape.images > 0 else 1
+    t = (ctypes.c_double * G)(*(tau or [0.1] * G))
+    k = (ctypes.c_int32 * G)(*(keep or [1] * G))
+    return hilo.lib().hilo_select(ctypes.byref(shape), FAKE, None, r, mode, t, k,
+                                  ptrs, FAKE, FAKE, FAKE, FAKE, FAKE, None)
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("grid_h", 7, 2), ("grid_w", 0, 2), ("batch", 0, 2), ("dim", 100, 2), ("dim", 8256, 2),
+    ("text_len", -1, 2), ("dtype", 5, 3),
+])
+def test_shape_validation(field, value, status):
+    s = good_shape()
+    setattr(s, field, value)
+    assert call_score(s) == status
+
+
+def test_block_shape_validation():
+    L = hilo.lib()
+    s = good_shape()
+    s.heads = 3  # 3 * 128 != 256
+    aw = (hilo.hilo_attn_w * 2)(*[hilo.hilo_attn_w(FAKE, FAKE, FAKE, FAKE)] * 2)
+    assert L.hilo_attention(ctypes.byref(s), FAKE, FAKE, aw, FAKE, FAKE, 1 << 40, None) == 2
+    s = good_shape()
+    s.head_dim, s.heads = 32, 8
+    assert L.hilo_attention(ctypes.byref(s), FAKE, FAKE, aw, FAKE, FAKE, 1 << 40, None) == 3
+    s = good_shape()
+    s.mlp_dim = 1000
+    mw = (hilo.hilo_mlp_w * 2)(*[hilo.hilo_mlp_w(FAKE, FAKE, FAKE, FAKE)] * 2)
+    assert L.hilo_mlp(ctypes.byref(s), FAKE, FAKE, mw, FAKE, FAKE, 1 << 40, None) == 2
+
+
+def test_null_pointers():
+    s = good_shape()
+    assert call_score(s, x=None) == 1
+    assert call_score(s, e=None) == 1
+    assert hilo.lib().hilo_score(None, FAKE, FAKE, None) == 1
+    assert call_select(s, ptrs=None) == 1
+    L = hilo.lib()
+    aw = (hilo.hilo_attn_w * 2)(hilo.hilo_attn_w(FAKE, FAKE, FAKE, FAKE), hilo.hilo_attn_w(FAKE, None, FAKE, FAKE))
+    assert L.hilo_attention(ctypes.byref(s), FAKE, FAKE, aw, FAKE, FAKE, 1 << 40, None) == 1
+    assert L.hilo_decompress(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, None, None, None) == 1
+    assert L.hilo_compress(ctypes.byref(s), FAKE, None, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None) == 1
+
+
+def test_select_parameter_validation():
+    s = good_shape()
+    NB = 8 * 10 // 4
+    assert call_select(s, mode=7) == 4
+    assert call_select(s, r=-1) == 4
+    assert call_select(s, keep=[NB + 1, 0]) == 4
+    assert call_select(s, keep=[-1, 0]) == 4
+    assert call_select(s, mode=hilo.THRESHOLD, tau=[math.nan, 0.1]) == 4
+    assert call_select(s, mode=hilo.THRESHOLD, tau=[math.inf, 0.1]) == 4
+
+
+def test_workspace_too_small():
+    s = good_shape()
+    need = hilo.hilo_workspace_bytes(s)
+    aw = (hilo.hilo_attn_w * 2)(*[hilo.hilo_attn_w(FAKE, FAKE, FAKE, FAKE)] * 2)
+    assert hilo.lib().hilo_attention(ctypes.byref(s), FAKE, FAKE, aw, FAKE, FAKE, 100, None) == 5
+    mw = (hilo.hilo_mlp_w * 2)(*[hilo.hilo_mlp_w(FAKE, FAKE, FAKE, FAKE)] * 2)
+    assert hilo.lib().hilo_mlp(ctypes.byref(s), FAKE, FAKE, mw, FAKE, FAKE, need - 1, None) == 5
+
+
+@pytest.mark.skipif(torch.cuda.is_available(), reason="checks the no-device path")
+def test_valid_calls_without_a_device_report_device_error():
+    s = good_shape()
+    assert call_score(s) == 6
+    assert call_select(s) == 6
+    assert call_select(s, mode=hilo.THRESHOLD, tau=[0.1, 0.2]) == 6
+    aw = (hilo.hilo_attn_w * 2)(*[hilo.hilo_attn_w(FAKE, FAKE, FAKE, FAKE)] * 2)
+    assert hilo.lib().hilo_attention(ctypes.byref(s), FAKE, FAKE, aw, FAKE, FAKE, 1 << 40, None) == 6
+    assert hilo.lib().hilo_attention_core(ctypes.byref(s), FAKE, FAKE, FAKE, None) == 6
+
+
+def test_profile_api():
+    n = hilo.hilo_profile_kinds()
+    assert n >= 10
+    names = [hilo.hilo_profile_name(k) for k in range(n)]
+    assert "attention_core" in names and "score" in names
+    hilo.hilo_profile_enable(True)
+    ms, cnt = hilo.hilo_profile_read(0)
+    assert ms == 0.0 and cnt == 0
+    hilo.hilo_profile_enable(False)
+    with pytest.raises(hilo.HiloError):
+        hilo.hilo_profile_read(n)
+
+
+def test_binding_refuses_host_tensors():
+    s = good_shape()
+    with pytest.raises(ValueError):
+        hilo.hilo_score(s, torch.zeros(4), torch.zeros(4))

@@ -1,0 +1,192 @@
+"""GPU parity of the whole hot path against the CPU oracle on small seeded workloads (every kernel
+is launched through the C ABI).  Sizes span several GEMM / attention tiles and ragged tails while
+the oracle still finishes in seconds."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import hilo_oracle as O
+from paper_2606_13898_amd import hilo, inputs
+from paper_2606_13898_amd.pipeline import DeviceBlock
+
+from parity_util import assert_close, check_selection, midpoint_tau, oracle_for, to_np
+
+pytestmark = pytest.mark.gpu
+
+SMALL = ["tiny", "small128", "small64", "smallf32"]
+
+
+def _stage_compare(db, ref, dtype, tag):
+    T = int(ref["cu"][-1])
+    assert_close(to_np(db.z)[:T], ref["Z"], dtype, f"{tag} Z after compress")
+
+
+@pytest.mark.parametrize("name", SMALL)
+def test_pipeline_parity(name):
+    print(f"[parity] workload={name}", flush=True)
+    wl = inputs.make_workload(name)
+    dt = wl.shape.dtype
+    db = DeviceBlock(wl)
+    ref = oracle_for(wl)
+    db.score()
+    db.select(hilo.TOPK)
+    db.compress()
+    torch.cuda.synchronize()
+    check_selection(db, ref)
+    T = int(ref["cu"][-1])
+    assert_close(to_np(db.z)[:T], ref["Z"], "f32", f"{name} Z after compress")
+    db.attention()
+    torch.cuda.synchronize()
+    assert_close(to_np(db.z)[:T], ref["z1"], dt, f"{name} z after attention")
+    db.mlp()
+    torch.cuda.synchronize()
+    assert_close(to_np(db.z)[:T], ref["z2"], dt, f"{name} z after mlp")
+    db.decompress()
+    torch.cuda.synchronize()
+    assert_close(to_np(db.y_img), ref["y_img"], dt, f"{name} y_img")
+    assert_close(to_np(db.y_txt), ref["y_txt"], dt, f"{name} y_txt")
+    assert np.abs(ref["y_img"]).max() < 8.0
+
+
+@pytest.mark.parametrize("name", ["tiny", "small128", "small64"])
+def test_threshold_selection_matches(name):
+    print(f"[parity] threshold workload={name}", flush=True)
+    wl = inputs.make_workload(name, with_block=False)
+    db = DeviceBlock(wl, with_block=False)
+    E = O.score(wl.x_img, wl.shape.grid_h, wl.shape.grid_w)
+    tau = midpoint_tau(E, wl.force, wl.shape, wl.dilate_r, wl.keep)
+    ref = oracle_for(wl, mode="threshold", tau=tau, with_block=False)
+    db.score()
+    db.select(hilo.THRESHOLD, tau=tau)
+    db.compress()
+    db.decompress()
+    torch.cuda.synchronize()
+    check_selection(db, ref)
+    # the midpoint threshold picks exactly the top-k set
+    ref_k = oracle_for(wl, mode="topk", with_block=False)
+    np.testing.assert_array_equal(ref["idx_map"], ref_k["idx_map"])
+    # without the block, decompress(compress(x)) keeps fine patches bit for bit
+    y = to_np(db.y_img)
+    blk = O.block_of(wl.shape.grid_h, wl.shape.grid_w)
+    for g in range(wl.shape.grids):
+        fp = ref["fine"][g][blk]
+        np.testing.assert_array_equal(y[g][fp], wl.x_img[g][fp])
+
+
+@pytest.mark.parametrize("keep_frac", [0.0, 1.0])
+def test_extreme_keep_fractions(keep_frac):
+    """0% kept (every block pooled) and 100% kept (0% compression: the dense block)."""
+    print(f"[parity] small128 keep_frac={keep_frac}", flush=True)
+    wl = inputs.make_workload("small128", keep_frac=keep_frac)
+    db = DeviceBlock(wl)
+    ref = oracle_for(wl)
+    db.run(hilo.TOPK)
+    torch.cuda.synchronize()
+    check_selection(db, ref)
+    assert_close(to_np(db.y_img), ref["y_img"], "bf16", "y_img")
+    if keep_frac == 1.0:
+        s = wl.shape
+        np.testing.assert_array_equal(to_np(db.idx_map), np.tile(np.arange(s.n_patches), (s.grids, 1)))
+        Zd, cud = O.dense_sequence(wl.x_img, wl.x_txt, s.batch, s.images, s.text_len)
+        _, z2d = O.block(Zd, cud, s.text_len, s.heads, wl.weights, wl.mod)
+        N = s.n_patches
+        dense_y = np.stack([z2d[cud[b] + i * N: cud[b] + (i + 1) * N]
+                            for b in range(s.batch) for i in range(s.images)])
+        assert_close(to_np(db.y_img), dense_y, "bf16", "0% compression vs dense oracle")
+
+
+def test_force_mask_with_dilation():
+    print("[parity] small64 force r=1", flush=True)
+    wl = inputs.make_workload("small64")
+    db = DeviceBlock(wl)
+    ref = oracle_for(wl, r=1)
+    db.run(hilo.TOPK, dilate_r=1)
+    torch.cuda.synchronize()
+    check_selection(db, ref)
+    assert_close(to_np(db.y_img), ref["y_img"], "bf16", "y_img r=1")
+
+
+def test_flat_grid_threshold_keeps_only_forced_blocks():
+    print("[parity] flat grid", flush=True)
+    shp = inputs.BlockShape(1, 2, 8, 12, 0, 64, 1, 64, 256, "bf16")
+    wl = inputs.make_workload("flat", shape=shp, with_block=False, seed=5)
+    wl.x_img[:] = 0.5
+    wl.force = np.zeros((2, 96), np.uint8)
+    wl.force[1, 30] = 1
+    db = DeviceBlock(wl, with_block=False)
+    ref = oracle_for(wl, mode="threshold", tau=[0.1, 0.1], r=0, with_block=False)
+    db.score()
+    db.select(hilo.THRESHOLD, tau=[0.1, 0.1], dilate_r=0)
+    db.compress()
+    db.decompress()
+    torch.cuda.synchronize()
+    check_selection(db, ref)
+    assert to_np(db.counts).tolist() == [[0, 24], [4, 23]]
+    # constant blocks pool and broadcast back losslessly
+    np.testing.assert_array_equal(to_np(db.y_img), wl.x_img)
+
+
+def test_constant_blocks_roundtrip_bitwise():
+    print("[parity] constant blocks", flush=True)
+    shp = inputs.BlockShape(2, 1, 10, 14, 3, 128, 1, 128, 512, "bf16")
+    wl = inputs.make_workload("const", shape=shp, with_block=False, seed=6)
+    coarse = inputs.to_bf16_values(np.random.default_rng(1).standard_normal((2, 5, 7, 128)).astype(np.float32))
+    wl.x_img = np.repeat(np.repeat(coarse, 2, 1), 2, 2).reshape(2, 140, 128).copy()
+    wl.keep = np.array([5, 11], np.int32)
+    db = DeviceBlock(wl, with_block=False)
+    db.score()
+    db.select(hilo.TOPK)
+    db.compress()
+    db.decompress()
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(to_np(db.y_img), wl.x_img)
+    np.testing.assert_array_equal(to_np(db.y_txt), wl.x_txt)
+
+
+def test_no_text_tokens():
+    print("[parity] no text", flush=True)
+    shp = inputs.BlockShape(2, 1, 12, 10, 0, 256, 2, 128, 1024, "bf16")
+    wl = inputs.make_workload("notext", shape=shp, seed=8)
+    wl.keep = np.array([7, 20], np.int32)
+    db = DeviceBlock(wl)
+    ref = oracle_for(wl)
+    db.run(hilo.TOPK)
+    torch.cuda.synchronize()
+    check_selection(db, ref)
+    assert_close(to_np(db.y_img), ref["y_img"], "bf16", "y_img no text")
+
+
+def test_run_to_run_determinism():
+    print("[parity] determinism small128", flush=True)
+    wl = inputs.make_workload("small128")
+    db = DeviceBlock(wl)
+    outs = []
+    for _ in range(2):
+        db.run(hilo.TOPK)
+        torch.cuda.synchronize()
+        outs.append((db.energy.clone(), db.idx_map.clone(), db.z.clone(), db.y_img.clone()))
+    for a, b in zip(*outs):
+        assert torch.equal(a, b)
+
+
+@pytest.mark.parametrize("hd,lens", [(128, [1, 17, 64, 65, 200]), (64, [3, 130, 31])])
+def test_attention_core_ragged(hd, lens):
+    print(f"[parity] attention core hd={hd} lens={lens}", flush=True)
+    heads = 2
+    D = heads * hd
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    T = int(cu[-1])
+    rng = np.random.default_rng(hd + len(lens))
+    qkv = inputs.to_bf16_values(rng.standard_normal((T, 3 * D)).astype(np.float32))
+    want = O.attention_core(qkv, cu, heads)
+    # a shape whose longest possible sample covers the longest length
+    maxlen = max(lens)
+    H = 2
+    W = 2 * ((maxlen + 3) // 4)
+    shp = hilo.hilo_shape(len(lens), 1, H, W, 0, D, heads, hd, 4 * D, hilo.BF16)
+    q = torch.from_numpy(qkv).to(torch.bfloat16).cuda()
+    out = torch.zeros(T, D, dtype=torch.bfloat16, device="cuda")
+    cut = torch.from_numpy(cu).cuda()
+    hilo.hilo_attention_core(shp, q, cut, out)
+    torch.cuda.synchronize()
+    assert_close(to_np(out), want, "bf16", f"attention core hd={hd}")
