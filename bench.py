@@ -1,0 +1,245 @@
+#!/usr/bin/env python3
+"""Benchmark of the HiLo-Token compressed DiT block on one MI355X.
+
+One step = one pass of the whole hot path over one batch: score, select, compress, attention,
+MLP, decompress (six C-ABI calls, all kernels on the GPU), inputs resident in HBM.  Prints ONE JSON
+line with the step latency, throughput, the dense (uncompressed) block for the speedup, per-kernel
+times from HIP events with their roofline fractions, and the CPU oracle timed on a bounded sample.
+
+    python bench.py [--steps K] [--warmup W] [--workload m1024] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "compressed DiT-block latency (ms) + attn TFLOP/s at 64×64 grid; speedup vs dense"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_F32_TFLOPS = 157.3     # MI355X fp32 vector
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+DESCR = {
+    "m1024": "one MMDiT-style DiT block at 1024px: 64x64 latent grid + 512 text tokens, D=3072, "
+             "24 heads x 128, MLP 12288, bf16; 3-5 texture regions (~35% area); top-k keeps 40% of "
+             "2x2 blocks fine",
+    "h2048": "one DiT block at 2048px: 128x128 grid + 512 text tokens, D=3072, 24x128 heads, bf16; "
+             "multi-octave texture on ~20% area; top-k keeps 25% fine",
+    "edit": "edit with reference: two 64x64 grids + 512 text tokens, D=3072, bf16; 15% edit mask "
+            "forced fine; top-k keeps 35% per grid",
+    "ragged": "batch of 8 samples of 64x64 + 512 text tokens, D=3072, bf16; kept fraction per "
+              "sample U[5%,95%]",
+}
+
+
+def kernel_work(shape, counts, cu):
+    """Algorithmic work per launch of every kernel kind: (amount, unit, peak)."""
+    import numpy as np
+
+    s = shape
+    es = 2 if s.dtype == "bf16" else 4
+    G, N, D, F, B, L = s.grids, s.n_patches, s.dim, s.mlp_dim, s.batch, s.text_len
+    nc = int(cu[-1])
+    n_img = int(counts.sum())
+    seqs = np.diff(cu).astype(np.int64)
+    mfma = PEAK_BF16_TFLOPS if s.dtype == "bf16" else PEAK_F32_TFLOPS
+    gemm = lambda n_out, k: (2.0 * nc * n_out * k / 1e12, "TFLOP", mfma)
+    return {
+        "score": ((G * N * D * es + 8 * G * N) / 1e9, "GB", PEAK_HBM_GBS),
+        "compress": ((G * N * D * es + n_img * D * 4 + B * L * D * (es + 4)) / 1e9, "GB", PEAK_HBM_GBS),
+        "rownorm_attn": (nc * D * (4 + es) / 1e9, "GB", PEAK_HBM_GBS),
+        "gemm_qkv": gemm(3 * D, D),
+        "attention_core": (4.0 * float((seqs ** 2).sum()) * D / 1e12, "TFLOP", mfma),
+        "gemm_o": gemm(D, D),
+        "rownorm_mlp": (nc * D * (4 + es) / 1e9, "GB", PEAK_HBM_GBS),
+        "gemm_fc1": gemm(F, D),
+        "gemm_fc2": gemm(D, F),
+        "decompress": ((n_img * D * 4 + G * N * D * es + B * L * D * (4 + es)) / 1e9, "GB", PEAK_HBM_GBS),
+    }
+
+
+def source_digest(paths):
+    h = hashlib.sha256()
+    for p in paths:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_for(kind):
+    """HBM bytes per launch measured with rocprofv3 counters (profiles/traffic.json), or None when
+    the counters are missing or the kernel source changed since they were taken."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        tab = json.load(f)
+    ent = tab.get("kernels", {}).get(kind)
+    if not ent:
+        return None
+    if source_digest(ent["sources"]) != ent["source_digest"]:
+        return None
+    return ent["bytes_per_launch"]
+
+
+def cpu_baseline(wl):
+    """The oracle, untuned, on one full step of the same workload (bounded: ~10-30 s)."""
+    import threadpoolctl
+
+    from oracle import hilo_oracle as O
+
+    info = threadpoolctl.threadpool_info()
+    threads = max([i.get("num_threads", 1) for i in info if i.get("user_api") == "blas"] or [1])
+    t0 = time.perf_counter()
+    O.pipeline(wl.x_img, wl.x_txt, wl.shape, wl.force, wl.dilate_r, "topk", keep=wl.keep,
+               weights=wl.weights, mod=wl.mod)
+    dt = time.perf_counter() - t0
+    return {"value": round(dt * 1e3, 1), "unit": "ms", "cores": int(threads), "kind": "oracle",
+            "sample": f"one full step (score..decompress) of the {wl.name} workload in float64 "
+                      f"numpy, BLAS threads={threads}"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="m1024", choices=sorted(DESCR))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-dense", action="store_true")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: the compressed block runs on a single MI355X; "
+              "multi-GPU runs are not part of this build", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2606_13898_amd import hilo, inputs
+    from paper_2606_13898_amd.pipeline import DeviceBlock
+
+    hilo.lib()  # fail loudly if the library is not built
+    torch.cuda.set_device(0)
+    wl = inputs.make_workload(args.workload)
+    s = wl.shape
+    db = DeviceBlock(wl)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        db.run(hilo.TOPK)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) * 1e3 / args.steps
+    ms = e0.elapsed_time(e1) / args.steps
+    counts = db.counts.cpu().numpy()
+    cu = db.cu.cpu().numpy()
+    nc = int(cu[-1])
+
+    # per-kernel durations: the same steps again with the library's event pairs around each kernel
+    hilo.hilo_profile_enable(True)
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    kinds = {hilo.hilo_profile_name(k): hilo.hilo_profile_read(k) for k in range(hilo.hilo_profile_kinds())}
+    hilo.hilo_profile_enable(False)
+    work = kernel_work(s, counts, cu)
+    kern = {}
+    for name, (tot, n) in kinds.items():
+        if n == 0:
+            continue
+        avg = tot / n
+        ent = {"ms": round(avg, 4), "launches_per_step": n // args.steps}
+        if name in work:
+            amt, unit, peak = work[name]
+            ach = amt / (avg * 1e-3)  # GB/s or TFLOP/s
+            ent.update(achieved=round(ach, 1), unit=unit + "/s", peak=peak,
+                       frac=round(ach / peak, 4), work_per_launch=f"{amt:.4g} {unit}")
+        kern[name] = ent
+    dom = max((k for k in kern if k in work), key=lambda k: kern[k]["ms"])
+    d = kern[dom]
+    roof = {"kernel": dom, "bound": "mfma" if d["unit"] == "TFLOP/s" else "hbm",
+            "achieved": d["achieved"], "peak": d["peak"], "unit": d["unit"], "frac": d["frac"],
+            "traffic": traffic_for(dom)}
+    t_blk = sum(kern[k]["ms"] for k in ("rownorm_attn", "gemm_qkv", "attention_core", "gemm_o",
+                                        "rownorm_mlp", "gemm_fc1", "gemm_fc2") if k in kern)
+
+    # the same block on the uncompressed sequence (every block kept fine)
+    dense = None
+    if not args.no_dense:
+        NB = s.n_blocks
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(args.steps)]
+        db.score()
+        db.select(hilo.TOPK, keep=[NB] * s.grids)
+        for _ in range(args.warmup):
+            db.compress()
+            db.attention()
+            db.mlp()
+        for a, b in ev:
+            db.compress()
+            a.record(stream)
+            db.attention()
+            db.mlp()
+            b.record(stream)
+        torch.cuda.synchronize()
+        dense_ms = sum(a.elapsed_time(b) for a, b in ev) / args.steps
+        n_dense = int(db.cu.cpu().numpy()[-1])
+        dense = {"block_ms": round(dense_ms, 4), "tokens": n_dense}
+
+    attn = kern.get("attention_core", {})
+    out = {
+        "metric": METRIC,
+        "value": round(ms, 4),
+        "unit": "ms",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "wall_ms_per_step": round(wall, 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": s.dtype,
+        "data": "synthetic (seeded latents, random-init weights of the block's shape)",
+        "config": {"workload": f"{args.workload}: {DESCR[args.workload]}",
+                   "batch": s.batch, "images": s.images, "grid": f"{s.grid_h}x{s.grid_w}",
+                   "text_tokens": s.text_len, "dim": s.dim, "heads": s.heads,
+                   "head_dim": s.head_dim, "mlp_dim": s.mlp_dim,
+                   "compressed_tokens": nc, "dense_tokens": s.max_tokens},
+        "block_ms": round(t_blk, 4),
+        "attn_tflops": attn.get("achieved"),
+        "compressed_tokens_per_s": round(nc / (ms * 1e-3), 1),
+        "represented_tokens_per_s": round(s.max_tokens / (ms * 1e-3), 1),
+        "roofline": roof,
+        "kernels": kern,
+    }
+    if dense:
+        out["dense"] = dense
+        out["speedup_vs_dense"] = round(dense["block_ms"] / ms, 3)
+        out["block_speedup_vs_dense"] = round(dense["block_ms"] / t_blk, 3) if t_blk else None
+        out["token_ratio"] = round(dense["tokens"] / nc, 3)
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()
