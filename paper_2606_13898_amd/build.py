@@ -31,6 +31,9 @@ def common_flags():
             "-Wno-unused-function", "-Wno-unused-variable",
             # keep the compiler from forming packed fp32 ops (v_pk_*_f32) on its own
             "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+            # keep MFMA accumulators in VGPRs: with the AGPR form the register allocator copies
+            # every accumulator quad around each MFMA instead of tying it in place
+            "-mllvm", "-amdgpu-mfma-vgpr-form=1",
             "-I", os.path.join(ROOT, "include")]
 
 

@@ -90,20 +90,23 @@ size_t esize(const hilo_shape *s) { return s->dtype == HILO_BF16 ? 2 : 4; }
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
+size_t ws_part(const hilo_shape *s) { return s->dtype == HILO_BF16 ? kSkPartBytes : 0; }
+
 size_t ws_attention(const hilo_shape *s) {
   const size_t T = size_t(tmax_of(s)), D = size_t(s->dim), e = esize(s);
-  return align256(T * D * e) + align256(T * 3 * D * e);  // h (then a) + qkv
+  return align256(T * D * e) + align256(T * 3 * D * e) + ws_part(s);  // h (then a), qkv, partials
 }
 
 size_t ws_mlp(const hilo_shape *s) {
   const size_t T = size_t(tmax_of(s)), D = size_t(s->dim), F = size_t(s->mlp_dim), e = esize(s);
-  return align256(T * D * e) + align256(T * F * e);  // h2 + hidden
+  return align256(T * D * e) + align256(T * F * e) + ws_part(s);  // h2, hidden, partials
 }
 
 hilo_status dev_status(hipError_t e) { return e == hipSuccess ? HILO_OK : HILO_E_DEVICE; }
 
-GemmProblem base_problem(const hilo_shape *s, const int32_t *cu, const float *mod) {
+GemmProblem base_problem(const hilo_shape *s, const int32_t *cu, const float *mod, float *part) {
   GemmProblem p{};
+  p.part = part;
   p.mod = mod;
   p.D = s->dim;
   p.cu = cu;
@@ -253,13 +256,15 @@ hilo_status hilo_attention(const hilo_shape *s, float *z, const int32_t *cu_seql
   char *ws = reinterpret_cast<char *>(workspace);
   void *h = ws;  // LN output, later the attention output
   void *qkv = ws + align256(size_t(T) * D * esize(s));
+  float *part = reinterpret_cast<float *>(ws + align256(size_t(T) * D * esize(s)) +
+                                          align256(size_t(T) * 3 * D * esize(s)));
 
   hipError_t he = timed(K_NORM_ATTN, st, [&] {
     return launch_rownorm(bf, z, cu_seqlens, mod, s->batch, s->text_len, D, T, 0, h, st);
   });
   if (he != hipSuccess) return HILO_E_DEVICE;
 
-  GemmProblem p = base_problem(s, cu_seqlens, mod);
+  GemmProblem p = base_problem(s, cu_seqlens, mod, part);
   p.A = h; p.lda = D;
   p.W[0] = w[0].w_qkv; p.W[1] = w[1].w_qkv;
   p.bias[0] = w[0].b_qkv; p.bias[1] = w[1].b_qkv;
@@ -274,7 +279,7 @@ hilo_status hilo_attention(const hilo_shape *s, float *z, const int32_t *cu_seql
   });
   if (he != hipSuccess) return HILO_E_DEVICE;
 
-  GemmProblem q = base_problem(s, cu_seqlens, mod);
+  GemmProblem q = base_problem(s, cu_seqlens, mod, part);
   q.A = h; q.lda = D;
   q.W[0] = w[0].w_o; q.W[1] = w[1].w_o;
   q.bias[0] = w[0].b_o; q.bias[1] = w[1].b_o;
@@ -300,13 +305,15 @@ hilo_status hilo_mlp(const hilo_shape *s, float *z, const int32_t *cu_seqlens,
   char *ws = reinterpret_cast<char *>(workspace);
   void *h2 = ws;
   void *hid = ws + align256(size_t(T) * D * esize(s));
+  float *part = reinterpret_cast<float *>(ws + align256(size_t(T) * D * esize(s)) +
+                                          align256(size_t(T) * F * esize(s)));
 
   hipError_t he = timed(K_NORM_MLP, st, [&] {
     return launch_rownorm(bf, z, cu_seqlens, mod, s->batch, s->text_len, D, T, 1, h2, st);
   });
   if (he != hipSuccess) return HILO_E_DEVICE;
 
-  GemmProblem p = base_problem(s, cu_seqlens, mod);
+  GemmProblem p = base_problem(s, cu_seqlens, mod, part);
   p.A = h2; p.lda = D;
   p.W[0] = w[0].w1; p.W[1] = w[1].w1;
   p.bias[0] = w[0].b1; p.bias[1] = w[1].b1;
@@ -315,7 +322,7 @@ hilo_status hilo_mlp(const hilo_shape *s, float *z, const int32_t *cu_seqlens,
   he = timed(K_GEMM_FC1, st, [&] { return launch_gemm(bf, EPI_GELU, p, st); });
   if (he != hipSuccess) return HILO_E_DEVICE;
 
-  GemmProblem q = base_problem(s, cu_seqlens, mod);
+  GemmProblem q = base_problem(s, cu_seqlens, mod, part);
   q.A = hid; q.lda = F;
   q.W[0] = w[0].w2; q.W[1] = w[1].w2;
   q.bias[0] = w[0].b2; q.bias[1] = w[1].b2;

@@ -45,9 +45,13 @@ def test_max_tokens_and_workspace():
     s = good_shape()
     assert hilo.hilo_max_tokens(s) == 2 * (80 + 5)
     T = 170
+    part = 256 * 2 * 256 * 256 * 4  # stream-K partial tiles of the bf16 projections
     want = max(-(-T * 256 * 2 // 256) * 256 + -(-T * 768 * 2 // 256) * 256,
-               -(-T * 256 * 2 // 256) * 256 + -(-T * 1024 * 2 // 256) * 256)
+               -(-T * 256 * 2 // 256) * 256 + -(-T * 1024 * 2 // 256) * 256) + part
     assert hilo.hilo_workspace_bytes(s) == want
+    f = good_shape(hilo.F32)
+    assert hilo.hilo_workspace_bytes(f) == max(-(-T * 256 * 4 // 256) * 256 + -(-T * 768 * 4 // 256) * 256,
+                                               -(-T * 256 * 4 // 256) * 256 + -(-T * 1024 * 4 // 256) * 256)
     bad = good_shape()
     bad.grid_h = 7
     assert hilo.hilo_max_tokens(bad) == -1
