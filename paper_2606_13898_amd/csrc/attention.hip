@@ -8,13 +8,42 @@
 //   probabilities are already in the register layout of the second MFMA operand for
 //   O^T = V^T P^T.  The MFMA's k index may be permuted as long as both operands agree: the lane
 //   holding keys {4g..4g+3} and {16+4g..16+4g+3} of a 32-key step feeds exactly those keys of V^T,
-//   which sits transposed in LDS (written once per tile, read as two 8-byte pieces).
+//   which sits transposed in LDS (written once per tile, read as two 8-byte pieces).  K lands in
+//   LDS by direct global->LDS loads; only the last key tile carries the sequence-end mask; the
+//   output is rescaled only in steps where some row's running maximum grew.
 #include "common.h"
 #include "kernels.h"
 
 namespace hilo {
 
 constexpr float kLog2e = 1.4426950408889634f;
+
+// max / sum with the lanes 16 and 32 apart (the 4 lanes holding the same query row)
+HILO_DEV float xmax16_32(float x) {
+  auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+
+HILO_DEV float xsum16_32(float x) {
+  auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
+// K tile rows (head_dim bf16) are stored with 16-byte chunk c of row r at slot c ^ kswz(r), so
+// the 16 lanes reading one chunk of 16 consecutive rows hit 16 distinct bank groups.
+template <int HD>
+HILO_DEV int kswz(int r) {
+  if constexpr (HD == 128) return r & 15;
+  else return (r & 7) ^ ((r >> 3) & 1);
+}
+
+HILO_DEV void g2lds16(const void *g, void *lds_wave_base) {
+  __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void *)lds_wave_base, 16, 0, 0);
+}
 
 template <int HD, int QW, int NW>
 __global__ __launch_bounds__(NW * 64) void k_attn_bf16(const uint16_t *__restrict__ qkv,
@@ -25,14 +54,15 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(const uint16_t *__restric
   constexpr int QS = QW / 16;       // query subtiles per wave
   constexpr int KK = HD / 32;       // k-steps of the score MFMA
   constexpr int DS = HD / 16;       // d subtiles of the output
-  constexpr int KST = HD + 8;       // K tile row stride (elements)
+  constexpr int CPR = HD / 8;       // 16-byte chunks per K row
+  constexpr int RPI = 64 / CPR;     // K rows per wave load instruction (1 KiB)
+  constexpr int KI = BKV / RPI / NW;  // K load instructions per wave per tile
   constexpr int VST = BKV + 4;      // V^T tile row stride (elements)
   constexpr int NT = NW * 64;
-  constexpr int KCH = BKV * HD / 8; // 16-byte chunks of a K tile
-  constexpr int KC = (KCH + NT - 1) / NT;
   constexpr int VGR = (BKV / 4) * (HD / 8);  // 4-key x 8-dim groups of a V tile
   constexpr int VC = (VGR + NT - 1) / NT;
-  __shared__ __attribute__((aligned(16))) uint16_t sK[2][BKV * KST];
+  static_assert(KI * RPI * NW == BKV, "K tile / wave mismatch");
+  __shared__ __attribute__((aligned(1024))) uint16_t sK[2][BKV * HD];
   __shared__ __attribute__((aligned(16))) uint16_t sV[2][HD * VST];
 
   const int t = xcd_remap(blockIdx.x, gridDim.x);
@@ -63,18 +93,19 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(const uint16_t *__restric
       qf[qs][kk] = *reinterpret_cast<const bf16x8 *>(Q + size_t(q) * ld + kk * 32 + 8 * lg);
   }
 
-  uint4 rk[KC];
-  uint4 rv[VC][4];
-  auto gload = [&](int kv0) {
+  // K: direct global->LDS, lane -> (row wid*KI*RPI + RPI*i + lane/CPR, slot lane%CPR)
+  const int krow = lane / CPR, kslot = lane % CPR;
+  auto issue_k = [&](int kv0, int buf) {
 #pragma unroll
-    for (int c = 0; c < KC; ++c) {
-      const int idx = tid + c * NT;
-      if (idx < KCH) {
-        const int r = idx / (HD / 8), ch = idx % (HD / 8);
-        const int row = min(kv0 + r, n - 1);
-        rk[c] = *reinterpret_cast<const uint4 *>(Kp + size_t(row) * ld + ch * 8);
-      }
+    for (int i = 0; i < KI; ++i) {
+      const int r = (wid * KI + i) * RPI + krow;
+      const int row = min(kv0 + r, n - 1);
+      g2lds16(Kp + size_t(row) * ld + ((kslot ^ kswz<HD>(r)) * 8), &sK[buf][(wid * KI + i) * RPI * HD]);
     }
+  };
+  // V: staged through registers and written transposed (4 keys x 8 dims per group)
+  uint4 rv[VC][4];
+  auto load_v = [&](int kv0) {
 #pragma unroll
     for (int c = 0; c < VC; ++c) {
       const int gidx = tid + c * NT;
@@ -88,21 +119,12 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(const uint16_t *__restric
       }
     }
   };
-  auto sstore = [&](int buf) {
-#pragma unroll
-    for (int c = 0; c < KC; ++c) {
-      const int idx = tid + c * NT;
-      if (idx < KCH) {
-        const int r = idx / (HD / 8), ch = idx % (HD / 8);
-        *reinterpret_cast<uint4 *>(&sK[buf][r * KST + ch * 8]) = rk[c];
-      }
-    }
+  auto store_v = [&](int buf) {
 #pragma unroll
     for (int c = 0; c < VC; ++c) {
       const int gidx = tid + c * NT;
       if (gidx < VGR) {
         const int b = gidx % (HD / 8), a = gidx / (HD / 8);
-        // transpose 4 keys x 8 dims -> for each dim, 4 consecutive keys (8 bytes)
         const uint32_t *w0 = reinterpret_cast<const uint32_t *>(&rv[c][0]);
         const uint32_t *w1 = reinterpret_cast<const uint32_t *>(&rv[c][1]);
         const uint32_t *w2 = reinterpret_cast<const uint32_t *>(&rv[c][2]);
@@ -129,19 +151,12 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(const uint16_t *__restric
   for (int qs = 0; qs < QS; ++qs)
 #pragma unroll
     for (int d = 0; d < DS; ++d) o[qs][d] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float mrun[QS], lrun[QS];
+  float mrun[QS], lrun[QS];  // running max (scaled, base 2) and this lane's partial sum
 #pragma unroll
   for (int qs = 0; qs < QS; ++qs) { mrun[qs] = -INFINITY; lrun[qs] = 0.f; }
 
-  const int nkv = (n + BKV - 1) / BKV;
-  gload(0);
-  sstore(0);
-  __syncthreads();
-  for (int it = 0; it < nkv; ++it) {
-    const int buf = it & 1;
-    const int kv0 = it * BKV;
-    if (it + 1 < nkv) gload(kv0 + BKV);
-
+  // one 64-key step; keys >= n (only in the last step) are masked under a uniform branch
+  auto step = [&](int buf, int kv0) {
     // S^T for 64 keys x QW queries: sc[ks][qs][e] = score(query qs*16+lr, key ks*16+4*lg+e)
     f32x4 sc[4][QS];
 #pragma unroll
@@ -150,47 +165,52 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(const uint16_t *__restric
       for (int qs = 0; qs < QS; ++qs) sc[ks][qs] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
+      const int r = ks * 16 + lr;
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk) {
+        const int ch = kk * 4 + lg;
         const bf16x8 kf =
-            *reinterpret_cast<const bf16x8 *>(&sK[buf][(ks * 16 + lr) * KST + kk * 32 + 8 * lg]);
+            *reinterpret_cast<const bf16x8 *>(&sK[buf][r * HD + ((ch ^ kswz<HD>(r)) * 8)]);
 #pragma unroll
         for (int qs = 0; qs < QS; ++qs)
           sc[ks][qs] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[qs][kk], sc[ks][qs], 0, 0, 0);
       }
     }
-
-    const bool tail = kv0 + BKV > n;
-    bf16x8 pf[QS][2];
-#pragma unroll
-    for (int qs = 0; qs < QS; ++qs) {
-      float mx = -INFINITY;
+    if (kv0 + BKV > n) {
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          float v = sc[ks][qs][e] * scale_log2;
-          if (tail && kv0 + ks * 16 + 4 * lg + e >= n) v = -INFINITY;
-          sc[ks][qs][e] = v;
-          mx = fmaxf(mx, v);
-        }
-      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      const float mnew = fmaxf(mrun[qs], mx);
-      const float alpha = exp2f(mrun[qs] - mnew);
-      mrun[qs] = mnew;
+        for (int e = 0; e < 4; ++e)
+          if (kv0 + ks * 16 + 4 * lg + e >= n)
+#pragma unroll
+            for (int qs = 0; qs < QS; ++qs) sc[ks][qs][e] = -INFINITY;
+    }
+    bf16x8 pf[QS][2];
+#pragma unroll
+    for (int qs = 0; qs < QS; ++qs) {
+      float mx = sc[0][qs][0];
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) mx = fmaxf(mx, sc[ks][qs][e]);
+      const float mnew = fmaxf(mrun[qs], xmax16_32(mx) * scale_log2);
+      if (__any(mnew > mrun[qs])) {  // rescale only when some row's maximum grew
+        const float alpha = __builtin_amdgcn_exp2f(mrun[qs] - mnew);
+        lrun[qs] *= alpha;
+#pragma unroll
+        for (int d = 0; d < DS; ++d) o[qs][d] *= alpha;
+        mrun[qs] = mnew;
+      }
       float psum = 0.f;
       float pv[4][4];
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          pv[ks][e] = exp2f(sc[ks][qs][e] - mnew);
+          pv[ks][e] = __builtin_amdgcn_exp2f(fmaf(sc[ks][qs][e], scale_log2, -mnew));
           psum += pv[ks][e];
         }
-      lrun[qs] = lrun[qs] * alpha + psum;
-#pragma unroll
-      for (int d = 0; d < DS; ++d) o[qs][d] *= alpha;
+      lrun[qs] += psum;
 #pragma unroll
       for (int kk2 = 0; kk2 < 2; ++kk2) {
 #pragma unroll
@@ -200,7 +220,6 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(const uint16_t *__restric
         }
       }
     }
-
     // O^T += V^T P^T
 #pragma unroll
     for (int d = 0; d < DS; ++d) {
@@ -217,16 +236,32 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(const uint16_t *__restric
           o[qs][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[qs][kk2], o[qs][d], 0, 0, 0);
       }
     }
+  };
 
-    if (it + 1 < nkv) sstore(buf ^ 1);
+  const int nkv = (n + BKV - 1) / BKV;
+  issue_k(0, 0);
+  load_v(0);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  store_v(0);
+  __syncthreads();
+  for (int it = 0; it < nkv; ++it) {
+    const int buf = it & 1;
+    const int kv0 = it * BKV;
+    if (it + 1 < nkv) {
+      issue_k(kv0 + BKV, buf ^ 1);
+      load_v(kv0 + BKV);
+    }
+    step(buf, kv0);
+    if (it + 1 < nkv) {
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      store_v(buf ^ 1);
+    }
     __syncthreads();
   }
 
 #pragma unroll
   for (int qs = 0; qs < QS; ++qs) {
-    float l = lrun[qs];
-    l += __shfl_xor(l, 16, 64);
-    l += __shfl_xor(l, 32, 64);
+    const float l = xsum16_32(lrun[qs]);
     const float inv = 1.0f / l;
     const int q = q0 + wid * QW + qs * 16 + lr;
     if (q >= n) continue;
