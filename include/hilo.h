@@ -149,9 +149,12 @@ hilo_status hilo_decompress(const hilo_shape *shape, const float *z, const int32
                             void *y_txt, void *stream);
 
 /* The attention core alone (the softmax(q k^T / sqrt(hd)) v step of hilo_attention), for
- * localising parity failures and timing: qkv [T_max][3D] dtype -> out [T_max][D] dtype.        */
+ * localising parity failures and timing: qkv [T_max][3D] dtype -> out [T_max][D] dtype, rows of
+ * sample s attend to the rows of sample s.  workspace: device scratch of ws_bytes >=
+ * hilo_workspace_bytes(shape) for the bf16 path (its partial results); may be NULL for F32.      */
 hilo_status hilo_attention_core(const hilo_shape *shape, const void *qkv,
-                                const int32_t *cu_seqlens, void *out, void *stream);
+                                const int32_t *cu_seqlens, void *out, void *workspace,
+                                size_t ws_bytes, void *stream);
 
 size_t hilo_workspace_bytes(const hilo_shape *shape); /* 0 if the shape is invalid */
 int64_t hilo_max_tokens(const hilo_shape *shape);     /* T_max, or -1 if invalid    */

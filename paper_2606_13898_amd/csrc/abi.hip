@@ -90,7 +90,10 @@ size_t esize(const hilo_shape *s) { return s->dtype == HILO_BF16 ? 2 : 4; }
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
-size_t ws_part(const hilo_shape *s) { return s->dtype == HILO_BF16 ? kSkPartBytes : 0; }
+// Partial-result region shared by the stream-K GEMMs and the stream-K attention core (they never
+// run at the same time on one stream).
+constexpr size_t kPartBytes = kSkPartBytes > kAttnPartBytes ? kSkPartBytes : kAttnPartBytes;
+size_t ws_part(const hilo_shape *s) { return s->dtype == HILO_BF16 ? kPartBytes : 0; }
 
 size_t ws_attention(const hilo_shape *s) {
   const size_t T = size_t(tmax_of(s)), D = size_t(s->dim), e = esize(s);
@@ -226,16 +229,19 @@ hilo_status hilo_decompress(const hilo_shape *s, const float *z, const int32_t *
 }
 
 hilo_status hilo_attention_core(const hilo_shape *s, const void *qkv, const int32_t *cu_seqlens,
-                                void *out, void *stream) {
+                                void *out, void *workspace, size_t ws_bytes, void *stream) {
   hilo_status e = check_block(s);
   if (e != HILO_OK) return e;
   if (!qkv || !cu_seqlens || !out) return HILO_E_NULL;
+  if (ws_part(s) && !workspace) return HILO_E_NULL;
+  if (ws_bytes < ws_part(s)) return HILO_E_WORKSPACE;
   if (!have_device()) return HILO_E_DEVICE;
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   const int max_seq = s->images * s->grid_h * s->grid_w + s->text_len;
   return dev_status(timed(K_ATTN_CORE, st, [&] {
-    return launch_attention(s->dtype == HILO_BF16, qkv, cu_seqlens, out, s->batch, s->heads,
-                            s->head_dim, max_seq, st);
+    return launch_attention(s->dtype == HILO_BF16, qkv, cu_seqlens, out,
+                            reinterpret_cast<float *>(workspace), s->batch, s->heads, s->head_dim,
+                            max_seq, st);
   }));
 }
 
@@ -275,7 +281,8 @@ hilo_status hilo_attention(const hilo_shape *s, float *z, const int32_t *cu_seql
 
   const int max_seq = s->images * s->grid_h * s->grid_w + s->text_len;
   he = timed(K_ATTN_CORE, st, [&] {
-    return launch_attention(bf, qkv, cu_seqlens, h, s->batch, s->heads, s->head_dim, max_seq, st);
+    return launch_attention(bf, qkv, cu_seqlens, h, part, s->batch, s->heads, s->head_dim,
+                            max_seq, st);
   });
   if (he != hipSuccess) return HILO_E_DEVICE;
 

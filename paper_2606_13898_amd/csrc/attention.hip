@@ -45,15 +45,98 @@ HILO_DEV void g2lds16(const void *g, void *lds_wave_base) {
   __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void *)lds_wave_base, 16, 0, 0);
 }
 
+// Stream-K schedule of the attention core.  A unit is (sample, head, query tile of QW*NW rows);
+// it takes nkv(s) = ceil(n_s / 64) key steps.  Units are ordered sample-major, then head, then
+// query tile (the query tiles of one head share its keys in L2), and the P persistent workgroups
+// take equal contiguous ranges of the (unit, key step) space.  A unit fully inside one range is
+// finished there; a cut unit leaves per-range partial results (unnormalised O, running max m and
+// sum l per query row) that k_attn_fix merges in range order: M = max m_i,
+// O = sum exp2(m_i - M) O_i / sum exp2(m_i - M) l_i.
+struct AttnUnit {
+  int s, h, qt, nkv;
+  long long start;  // first iteration of the unit
+};
+
+HILO_DEV long long attn_iterations(const int *cu, int B, int heads, int BQ) {
+  long long I = 0;
+  for (int s = 0; s < B; ++s) {
+    const int n = cu[s + 1] - cu[s];
+    I += (long long)heads * ((n + BQ - 1) / BQ) * ((n + 63) / 64);
+  }
+  return I;
+}
+
+HILO_DEV AttnUnit attn_unit(const int *cu, int B, int heads, int BQ, long long it) {
+  long long base = 0;
+  for (int s = 0; s < B; ++s) {
+    const int n = cu[s + 1] - cu[s];
+    const int qtiles = (n + BQ - 1) / BQ, nkv = (n + 63) / 64;
+    const long long span = (long long)heads * qtiles * nkv;
+    if (it < base + span) {
+      const long long u = (it - base) / nkv;
+      return AttnUnit{s, int(u / qtiles), int(u % qtiles), nkv, base + u * nkv};
+    }
+    base += span;
+  }
+  return AttnUnit{0, 0, 0, 1, 0};
+}
+
+struct AttnArgs {
+  const uint16_t *qkv;
+  const int *cu;
+  uint16_t *out;
+  float *part;  // partial slots: 2 per workgroup
+  int B, heads;
+  float scale_log2;
+};
+
 template <int HD, int QW, int NW>
-__global__ __launch_bounds__(NW * 64) void k_attn_bf16(const uint16_t *__restrict__ qkv,
-                                                       const int *__restrict__ cu,
-                                                       uint16_t *__restrict__ out, int heads,
-                                                       int qtiles, float scale_log2) {
+struct AttnShape {
+  static constexpr int QS = QW / 16;
+  static constexpr int DS = HD / 16;
+  static constexpr int BQ = QW * NW;
+  // partial slot: O (QS*DS float4 per lane) then m and l (QS floats each per lane), per wave
+  static constexpr int kOFloats = NW * QS * DS * 64 * 4;
+  static constexpr int kSlotFloats = kOFloats + NW * QS * 64 * 2;
+  HILO_DEV static size_t o_index(int wid, int qs, int d, int lane) {
+    return ((size_t(wid) * QS + qs) * DS + d) * 256 + lane * 4;
+  }
+  HILO_DEV static size_t ml_index(int wid, int qs, int lane) {
+    return kOFloats + ((size_t(wid) * QS + qs) * 64 + lane) * 2;
+  }
+};
+
+template <int HD, int QW, int NW>
+HILO_DEV void attn_store_out(const AttnArgs &a, const AttnUnit &u, int wid, int lane,
+                             f32x4 (&o)[QW / 16][HD / 16], const float (&l)[QW / 16]) {
+  constexpr int QS = QW / 16, DS = HD / 16;
+  const int lo = a.cu[u.s], n = a.cu[u.s + 1] - lo;
+  const int D = a.heads * HD;
+  const int lr = lane & 15, lg = lane >> 4;
+#pragma unroll
+  for (int qs = 0; qs < QS; ++qs) {
+    const float inv = 1.0f / l[qs];
+    const int q = u.qt * (QW * NW) + wid * QW + qs * 16 + lr;
+    if (q >= n) continue;
+    uint16_t *orow = a.out + size_t(lo + q) * D + size_t(u.h) * HD;
+#pragma unroll
+    for (int d = 0; d < DS; ++d) {
+      uint2 w;
+      w.x = pack_bf16x2(o[qs][d][0] * inv, o[qs][d][1] * inv);
+      w.y = pack_bf16x2(o[qs][d][2] * inv, o[qs][d][3] * inv);
+      *reinterpret_cast<uint2 *>(orow + d * 16 + 4 * lg) = w;
+    }
+  }
+}
+
+template <int HD, int QW, int NW>
+__global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a) {
+  using S = AttnShape<HD, QW, NW>;
   constexpr int BKV = 64;
-  constexpr int QS = QW / 16;       // query subtiles per wave
+  constexpr int QS = S::QS;         // query subtiles per wave
   constexpr int KK = HD / 32;       // k-steps of the score MFMA
-  constexpr int DS = HD / 16;       // d subtiles of the output
+  constexpr int DS = S::DS;         // d subtiles of the output
+  constexpr int BQ = S::BQ;
   constexpr int CPR = HD / 8;       // 16-byte chunks per K row
   constexpr int RPI = 64 / CPR;     // K rows per wave load instruction (1 KiB)
   constexpr int KI = BKV / RPI / NW;  // K load instructions per wave per tile
@@ -65,215 +148,267 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(const uint16_t *__restric
   __shared__ __attribute__((aligned(1024))) uint16_t sK[2][BKV * HD];
   __shared__ __attribute__((aligned(16))) uint16_t sV[2][HD * VST];
 
-  const int t = xcd_remap(blockIdx.x, gridDim.x);
-  const int qt = t % qtiles;
-  const int sh = t / qtiles;
-  const int h = sh % heads;
-  const int s = sh / heads;
-  const int lo = cu[s];
-  const int n = cu[s + 1] - lo;
-  const int q0 = qt * (QW * NW);
-  if (q0 >= n) return;
-  const int D = heads * HD;
+  const int P = gridDim.x;
+  const int pid = xcd_remap(blockIdx.x, P);
+  const long long I = attn_iterations(a.cu, a.B, a.heads, BQ);
+  const long long beg = I * pid / P, end = I * (pid + 1) / P;
+  if (beg >= end) return;
+  const long long head_start = attn_unit(a.cu, a.B, a.heads, BQ, beg).start;
+  const int D = a.heads * HD;
   const size_t ld = size_t(3) * D;
-  const uint16_t *Q = qkv + size_t(lo) * ld + size_t(h) * HD;
-  const uint16_t *Kp = Q + D;
-  const uint16_t *Vp = Q + 2 * D;
-
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int lr = lane & 15, lg = lane >> 4;
-
-  // query fragments (second MFMA operand): row q, dims kk*32 + 8*lg .. +7
-  bf16x8 qf[QS][KK];
-#pragma unroll
-  for (int qs = 0; qs < QS; ++qs) {
-    const int q = min(q0 + wid * QW + qs * 16 + lr, n - 1);
-#pragma unroll
-    for (int kk = 0; kk < KK; ++kk)
-      qf[qs][kk] = *reinterpret_cast<const bf16x8 *>(Q + size_t(q) * ld + kk * 32 + 8 * lg);
-  }
-
-  // K: direct global->LDS, lane -> (row wid*KI*RPI + RPI*i + lane/CPR, slot lane%CPR)
   const int krow = lane / CPR, kslot = lane % CPR;
-  auto issue_k = [&](int kv0, int buf) {
-#pragma unroll
-    for (int i = 0; i < KI; ++i) {
-      const int r = (wid * KI + i) * RPI + krow;
-      const int row = min(kv0 + r, n - 1);
-      g2lds16(Kp + size_t(row) * ld + ((kslot ^ kswz<HD>(r)) * 8), &sK[buf][(wid * KI + i) * RPI * HD]);
-    }
-  };
-  // V: staged through registers and written transposed (4 keys x 8 dims per group)
-  uint4 rv[VC][4];
-  auto load_v = [&](int kv0) {
-#pragma unroll
-    for (int c = 0; c < VC; ++c) {
-      const int gidx = tid + c * NT;
-      if (gidx < VGR) {
-        const int b = gidx % (HD / 8), a = gidx / (HD / 8);
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int row = min(kv0 + 4 * a + u, n - 1);
-          rv[c][u] = *reinterpret_cast<const uint4 *>(Vp + size_t(row) * ld + b * 8);
-        }
-      }
-    }
-  };
-  auto store_v = [&](int buf) {
-#pragma unroll
-    for (int c = 0; c < VC; ++c) {
-      const int gidx = tid + c * NT;
-      if (gidx < VGR) {
-        const int b = gidx % (HD / 8), a = gidx / (HD / 8);
-        const uint32_t *w0 = reinterpret_cast<const uint32_t *>(&rv[c][0]);
-        const uint32_t *w1 = reinterpret_cast<const uint32_t *>(&rv[c][1]);
-        const uint32_t *w2 = reinterpret_cast<const uint32_t *>(&rv[c][2]);
-        const uint32_t *w3 = reinterpret_cast<const uint32_t *>(&rv[c][3]);
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const int sw = j >> 1;
-          const bool hi = j & 1;
-          const uint32_t e0 = hi ? (w0[sw] >> 16) : (w0[sw] & 0xffffu);
-          const uint32_t e1 = hi ? (w1[sw] >> 16) : (w1[sw] & 0xffffu);
-          const uint32_t e2 = hi ? (w2[sw] >> 16) : (w2[sw] & 0xffffu);
-          const uint32_t e3 = hi ? (w3[sw] >> 16) : (w3[sw] & 0xffffu);
-          uint2 v2;
-          v2.x = e0 | (e1 << 16);
-          v2.y = e2 | (e3 << 16);
-          *reinterpret_cast<uint2 *>(&sV[buf][(b * 8 + j) * VST + 4 * a]) = v2;
-        }
-      }
-    }
-  };
 
-  f32x4 o[QS][DS];
-#pragma unroll
-  for (int qs = 0; qs < QS; ++qs)
-#pragma unroll
-    for (int d = 0; d < DS; ++d) o[qs][d] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float mrun[QS], lrun[QS];  // running max (scaled, base 2) and this lane's partial sum
-#pragma unroll
-  for (int qs = 0; qs < QS; ++qs) { mrun[qs] = -INFINITY; lrun[qs] = 0.f; }
+  for (long long it = beg; it < end;) {
+    const AttnUnit u = attn_unit(a.cu, a.B, a.heads, BQ, it);
+    const int kb = int(it - u.start);
+    const int ke = int(min((long long)u.nkv, (long long)kb + (end - it)));
+    const int lo = a.cu[u.s];
+    const int n = a.cu[u.s + 1] - lo;
+    const int q0 = u.qt * BQ;
+    const uint16_t *Q = a.qkv + size_t(lo) * ld + size_t(u.h) * HD;
+    const uint16_t *Kp = Q + D;
+    const uint16_t *Vp = Q + 2 * D;
 
-  // one 64-key step; keys >= n (only in the last step) are masked under a uniform branch
-  auto step = [&](int buf, int kv0) {
-    // S^T for 64 keys x QW queries: sc[ks][qs][e] = score(query qs*16+lr, key ks*16+4*lg+e)
-    f32x4 sc[4][QS];
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks)
-#pragma unroll
-      for (int qs = 0; qs < QS; ++qs) sc[ks][qs] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      const int r = ks * 16 + lr;
-#pragma unroll
-      for (int kk = 0; kk < KK; ++kk) {
-        const int ch = kk * 4 + lg;
-        const bf16x8 kf =
-            *reinterpret_cast<const bf16x8 *>(&sK[buf][r * HD + ((ch ^ kswz<HD>(r)) * 8)]);
-#pragma unroll
-        for (int qs = 0; qs < QS; ++qs)
-          sc[ks][qs] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[qs][kk], sc[ks][qs], 0, 0, 0);
-      }
-    }
-    if (kv0 + BKV > n) {
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks)
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          if (kv0 + ks * 16 + 4 * lg + e >= n)
-#pragma unroll
-            for (int qs = 0; qs < QS; ++qs) sc[ks][qs][e] = -INFINITY;
-    }
-    bf16x8 pf[QS][2];
+    // query fragments (second MFMA operand): row q, dims kk*32 + 8*lg .. +7
+    bf16x8 qf[QS][KK];
 #pragma unroll
     for (int qs = 0; qs < QS; ++qs) {
-      float mx = sc[0][qs][0];
+      const int q = min(q0 + wid * QW + qs * 16 + lr, n - 1);
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) mx = fmaxf(mx, sc[ks][qs][e]);
-      const float mnew = fmaxf(mrun[qs], xmax16_32(mx) * scale_log2);
-      if (__any(mnew > mrun[qs])) {  // rescale only when some row's maximum grew
-        const float alpha = __builtin_amdgcn_exp2f(mrun[qs] - mnew);
-        lrun[qs] *= alpha;
-#pragma unroll
-        for (int d = 0; d < DS; ++d) o[qs][d] *= alpha;
-        mrun[qs] = mnew;
-      }
-      float psum = 0.f;
-      float pv[4][4];
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          pv[ks][e] = __builtin_amdgcn_exp2f(fmaf(sc[ks][qs][e], scale_log2, -mnew));
-          psum += pv[ks][e];
-        }
-      lrun[qs] += psum;
-#pragma unroll
-      for (int kk2 = 0; kk2 < 2; ++kk2) {
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          pf[qs][kk2][e] = static_cast<__bf16>(pv[2 * kk2][e]);
-          pf[qs][kk2][4 + e] = static_cast<__bf16>(pv[2 * kk2 + 1][e]);
-        }
-      }
+      for (int kk = 0; kk < KK; ++kk)
+        qf[qs][kk] = *reinterpret_cast<const bf16x8 *>(Q + size_t(q) * ld + kk * 32 + 8 * lg);
     }
-    // O^T += V^T P^T
-#pragma unroll
-    for (int d = 0; d < DS; ++d) {
-#pragma unroll
-      for (int kk2 = 0; kk2 < 2; ++kk2) {
-        const uint16_t *vr = &sV[buf][(d * 16 + lr) * VST + 32 * kk2 + 4 * lg];
-        const uint2 v0 = *reinterpret_cast<const uint2 *>(vr);
-        const uint2 v1 = *reinterpret_cast<const uint2 *>(vr + 16);
-        uint4 vv;
-        vv.x = v0.x; vv.y = v0.y; vv.z = v1.x; vv.w = v1.y;
-        const bf16x8 vf = __builtin_bit_cast(bf16x8, vv);
-#pragma unroll
-        for (int qs = 0; qs < QS; ++qs)
-          o[qs][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[qs][kk2], o[qs][d], 0, 0, 0);
-      }
-    }
-  };
 
-  const int nkv = (n + BKV - 1) / BKV;
-  issue_k(0, 0);
-  load_v(0);
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  store_v(0);
-  __syncthreads();
-  for (int it = 0; it < nkv; ++it) {
-    const int buf = it & 1;
-    const int kv0 = it * BKV;
-    if (it + 1 < nkv) {
-      issue_k(kv0 + BKV, buf ^ 1);
-      load_v(kv0 + BKV);
-    }
-    step(buf, kv0);
-    if (it + 1 < nkv) {
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-      store_v(buf ^ 1);
-    }
+    // K: direct global->LDS, lane -> (row wid*KI*RPI + RPI*i + lane/CPR, slot lane%CPR)
+    auto issue_k = [&](int kv0, int buf) {
+#pragma unroll
+      for (int i = 0; i < KI; ++i) {
+        const int r = (wid * KI + i) * RPI + krow;
+        const int row = min(kv0 + r, n - 1);
+        g2lds16(Kp + size_t(row) * ld + ((kslot ^ kswz<HD>(r)) * 8),
+                &sK[buf][(wid * KI + i) * RPI * HD]);
+      }
+    };
+    // V: staged through registers and written transposed (4 keys x 8 dims per group)
+    uint4 rv[VC][4];
+    auto load_v = [&](int kv0) {
+#pragma unroll
+      for (int c = 0; c < VC; ++c) {
+        const int gidx = tid + c * NT;
+        if (gidx < VGR) {
+          const int b = gidx % (HD / 8), g4 = gidx / (HD / 8);
+#pragma unroll
+          for (int w = 0; w < 4; ++w) {
+            const int row = min(kv0 + 4 * g4 + w, n - 1);
+            rv[c][w] = *reinterpret_cast<const uint4 *>(Vp + size_t(row) * ld + b * 8);
+          }
+        }
+      }
+    };
+    auto store_v = [&](int buf) {
+#pragma unroll
+      for (int c = 0; c < VC; ++c) {
+        const int gidx = tid + c * NT;
+        if (gidx < VGR) {
+          const int b = gidx % (HD / 8), g4 = gidx / (HD / 8);
+          const uint32_t *w0 = reinterpret_cast<const uint32_t *>(&rv[c][0]);
+          const uint32_t *w1 = reinterpret_cast<const uint32_t *>(&rv[c][1]);
+          const uint32_t *w2 = reinterpret_cast<const uint32_t *>(&rv[c][2]);
+          const uint32_t *w3 = reinterpret_cast<const uint32_t *>(&rv[c][3]);
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            const int sw = j >> 1;
+            const bool hi = j & 1;
+            const uint32_t e0 = hi ? (w0[sw] >> 16) : (w0[sw] & 0xffffu);
+            const uint32_t e1 = hi ? (w1[sw] >> 16) : (w1[sw] & 0xffffu);
+            const uint32_t e2 = hi ? (w2[sw] >> 16) : (w2[sw] & 0xffffu);
+            const uint32_t e3 = hi ? (w3[sw] >> 16) : (w3[sw] & 0xffffu);
+            uint2 v2;
+            v2.x = e0 | (e1 << 16);
+            v2.y = e2 | (e3 << 16);
+            *reinterpret_cast<uint2 *>(&sV[buf][(b * 8 + j) * VST + 4 * g4]) = v2;
+          }
+        }
+      }
+    };
+
+    f32x4 o[QS][DS];
+#pragma unroll
+    for (int qs = 0; qs < QS; ++qs)
+#pragma unroll
+      for (int d = 0; d < DS; ++d) o[qs][d] = f32x4{0.f, 0.f, 0.f, 0.f};
+    float mrun[QS], lrun[QS];  // running max (scaled, base 2) and this lane's partial sum
+#pragma unroll
+    for (int qs = 0; qs < QS; ++qs) { mrun[qs] = -INFINITY; lrun[qs] = 0.f; }
+
+    // one 64-key step; keys >= n (only in the unit's last step) are masked under a uniform branch
+    auto step = [&](int buf, int kv0) {
+      // S^T for 64 keys x QW queries: sc[ks][qs][e] = score(query qs*16+lr, key ks*16+4*lg+e)
+      f32x4 sc[4][QS];
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+        for (int qs = 0; qs < QS; ++qs) sc[ks][qs] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+        const int r = ks * 16 + lr;
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk) {
+          const int ch = kk * 4 + lg;
+          const bf16x8 kf =
+              *reinterpret_cast<const bf16x8 *>(&sK[buf][r * HD + ((ch ^ kswz<HD>(r)) * 8)]);
+#pragma unroll
+          for (int qs = 0; qs < QS; ++qs)
+            sc[ks][qs] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[qs][kk], sc[ks][qs], 0, 0, 0);
+        }
+      }
+      if (kv0 + BKV > n) {
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (kv0 + ks * 16 + 4 * lg + e >= n)
+#pragma unroll
+              for (int qs = 0; qs < QS; ++qs) sc[ks][qs][e] = -INFINITY;
+      }
+      bf16x8 pf[QS][2];
+#pragma unroll
+      for (int qs = 0; qs < QS; ++qs) {
+        float mx = sc[0][qs][0];
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) mx = fmaxf(mx, sc[ks][qs][e]);
+        const float mnew = fmaxf(mrun[qs], xmax16_32(mx) * a.scale_log2);
+        if (__any(mnew > mrun[qs])) {  // rescale only when some row's maximum grew
+          const float alpha = __builtin_amdgcn_exp2f(mrun[qs] - mnew);
+          lrun[qs] *= alpha;
+#pragma unroll
+          for (int d = 0; d < DS; ++d) o[qs][d] *= alpha;
+          mrun[qs] = mnew;
+        }
+        float psum = 0.f;
+        float pv[4][4];
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            pv[ks][e] = __builtin_amdgcn_exp2f(fmaf(sc[ks][qs][e], a.scale_log2, -mnew));
+            psum += pv[ks][e];
+          }
+        lrun[qs] += psum;
+#pragma unroll
+        for (int kk2 = 0; kk2 < 2; ++kk2) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            pf[qs][kk2][e] = static_cast<__bf16>(pv[2 * kk2][e]);
+            pf[qs][kk2][4 + e] = static_cast<__bf16>(pv[2 * kk2 + 1][e]);
+          }
+        }
+      }
+      // O^T += V^T P^T
+#pragma unroll
+      for (int d = 0; d < DS; ++d) {
+#pragma unroll
+        for (int kk2 = 0; kk2 < 2; ++kk2) {
+          const uint16_t *vr = &sV[buf][(d * 16 + lr) * VST + 32 * kk2 + 4 * lg];
+          const uint2 v0 = *reinterpret_cast<const uint2 *>(vr);
+          const uint2 v1 = *reinterpret_cast<const uint2 *>(vr + 16);
+          uint4 vv;
+          vv.x = v0.x; vv.y = v0.y; vv.z = v1.x; vv.w = v1.y;
+          const bf16x8 vf = __builtin_bit_cast(bf16x8, vv);
+#pragma unroll
+          for (int qs = 0; qs < QS; ++qs)
+            o[qs][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[qs][kk2], o[qs][d], 0, 0, 0);
+        }
+      }
+    };
+
+    issue_k(kb * BKV, 0);
+    load_v(kb * BKV);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    store_v(0);
     __syncthreads();
-  }
+    for (int kt = kb; kt < ke; ++kt) {
+      const int buf = (kt - kb) & 1;
+      const int kv0 = kt * BKV;
+      if (kt + 1 < ke) {
+        issue_k(kv0 + BKV, buf ^ 1);
+        load_v(kv0 + BKV);
+      }
+      step(buf, kv0);
+      if (kt + 1 < ke) {
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        store_v(buf ^ 1);
+      }
+      __syncthreads();
+    }
 
+    float lsum[QS];
+#pragma unroll
+    for (int qs = 0; qs < QS; ++qs) lsum[qs] = xsum16_32(lrun[qs]);
+    if (kb == 0 && ke == u.nkv) {
+      attn_store_out<HD, QW, NW>(a, u, wid, lane, o, lsum);
+    } else {
+      float *slot = a.part + (size_t(pid) * 2 + (u.start == head_start ? 0 : 1)) * S::kSlotFloats;
+#pragma unroll
+      for (int qs = 0; qs < QS; ++qs) {
+#pragma unroll
+        for (int d = 0; d < DS; ++d)
+          *reinterpret_cast<f32x4 *>(slot + S::o_index(wid, qs, d, lane)) = o[qs][d];
+        *reinterpret_cast<float2 *>(slot + S::ml_index(wid, qs, lane)) = make_float2(mrun[qs], lsum[qs]);
+      }
+    }
+    it += ke - kb;
+  }
+}
+
+// Merges every unit cut by range boundaries; run by the range holding the unit's first key step.
+template <int HD, int QW, int NW>
+__global__ __launch_bounds__(NW * 64) void k_attn_fix(AttnArgs a) {
+  using S = AttnShape<HD, QW, NW>;
+  constexpr int QS = S::QS, DS = S::DS, BQ = S::BQ;
+  const int P = gridDim.x;
+  const int pid = blockIdx.x;
+  const long long I = attn_iterations(a.cu, a.B, a.heads, BQ);
+  const long long beg = I * pid / P, end = I * (pid + 1) / P;
+  if (beg >= end) return;
+  const AttnUnit u = attn_unit(a.cu, a.B, a.heads, BQ, end - 1);
+  const long long ue = u.start + u.nkv;
+  if (end >= ue) return;      // the unit ends inside this range: not cut here
+  if (beg > u.start) return;  // this range does not hold the unit's first step
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+
+  f32x4 o[QS][DS];
+  float m[QS], l[QS];
 #pragma unroll
   for (int qs = 0; qs < QS; ++qs) {
-    const float l = xsum16_32(lrun[qs]);
-    const float inv = 1.0f / l;
-    const int q = q0 + wid * QW + qs * 16 + lr;
-    if (q >= n) continue;
-    uint16_t *orow = out + size_t(lo + q) * D + size_t(h) * HD;
+    m[qs] = -INFINITY;
+    l[qs] = 0.f;
 #pragma unroll
-    for (int d = 0; d < DS; ++d) {
-      uint2 u;
-      u.x = pack_bf16x2(o[qs][d][0] * inv, o[qs][d][1] * inv);
-      u.y = pack_bf16x2(o[qs][d][2] * inv, o[qs][d][3] * inv);
-      *reinterpret_cast<uint2 *>(orow + d * 16 + 4 * lg) = u;
-    }
+    for (int d = 0; d < DS; ++d) o[qs][d] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
+  for (int q = pid; q < P; ++q) {
+    const long long bq = I * q / P, eq = I * (q + 1) / P;
+    if (bq >= eq) continue;
+    if (bq >= ue) break;
+    const float *slot = a.part + (size_t(q) * 2 + (bq > u.start ? 0 : (bq == u.start ? 0 : 1))) * S::kSlotFloats;
+#pragma unroll
+    for (int qs = 0; qs < QS; ++qs) {
+      const float2 ml = *reinterpret_cast<const float2 *>(slot + S::ml_index(wid, qs, lane));
+      const float mn = fmaxf(m[qs], ml.x);
+      const float ca = __builtin_amdgcn_exp2f(m[qs] - mn), cb = __builtin_amdgcn_exp2f(ml.x - mn);
+      l[qs] = l[qs] * ca + ml.y * cb;
+#pragma unroll
+      for (int d = 0; d < DS; ++d)
+        o[qs][d] = o[qs][d] * ca + *reinterpret_cast<const f32x4 *>(slot + S::o_index(wid, qs, d, lane)) * cb;
+      m[qs] = mn;
+    }
+    if (eq >= ue) break;
+  }
+  attn_store_out<HD, QW, NW>(a, u, wid, lane, o, l);
 }
 
 // fp32 path: one thread per query row, keys/values staged through LDS 32 rows at a time.
@@ -324,16 +459,31 @@ __global__ __launch_bounds__(64) void k_attn_f32(const float *__restrict__ qkv,
   }
 }
 
+int attn_workgroups() {
+  static int ncu[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) dev = 0;
+  if (ncu[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+      n = kAttnMaxWorkgroups / 2;
+    ncu[dev] = n;
+  }
+  const int p = 2 * ncu[dev];  // two workgroups fit on a CU
+  return p < kAttnMaxWorkgroups ? p : kAttnMaxWorkgroups;
+}
+
 template <int HD, int QW, int NW>
-static hipError_t run_attn_bf16(const void *qkv, const int *cu, void *out, int B, int heads,
-                                int max_seq, hipStream_t st) {
-  const int qtiles = (max_seq + QW * NW - 1) / (QW * NW);
-  const long long nblk = (long long)B * heads * qtiles;
-  if (nblk <= 0) return hipSuccess;
-  const float sl2 = kLog2e / sqrtf(float(HD));
-  hipLaunchKernelGGL((k_attn_bf16<HD, QW, NW>), dim3(unsigned(nblk)), dim3(NW * 64), 0, st,
-                     reinterpret_cast<const uint16_t *>(qkv), cu,
-                     reinterpret_cast<uint16_t *>(out), heads, qtiles, sl2);
+static hipError_t run_attn_bf16(const void *qkv, const int *cu, void *out, float *part, int B,
+                                int heads, hipStream_t st) {
+  static_assert(AttnShape<HD, QW, NW>::kSlotFloats <= kAttnSlotFloats, "partial slot too small");
+  AttnArgs a{reinterpret_cast<const uint16_t *>(qkv), cu, reinterpret_cast<uint16_t *>(out), part, B,
+             heads, kLog2e / sqrtf(float(HD))};
+  const int P = attn_workgroups();
+  hipLaunchKernelGGL((k_attn_bf16<HD, QW, NW>), dim3(P), dim3(NW * 64), 0, st, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((k_attn_fix<HD, QW, NW>), dim3(P), dim3(NW * 64), 0, st, a);
   return hipGetLastError();
 }
 
@@ -350,11 +500,11 @@ static hipError_t run_attn_f32(const void *qkv, const int *cu, void *out, int B,
   return hipGetLastError();
 }
 
-hipError_t launch_attention(bool bf16, const void *qkv, const int *cu, void *out, int B, int heads,
-                            int hd, int max_seq, hipStream_t st) {
+hipError_t launch_attention(bool bf16, const void *qkv, const int *cu, void *out, float *part, int B,
+                            int heads, int hd, int max_seq, hipStream_t st) {
   if (bf16) {
-    if (hd == 128) return run_attn_bf16<128, 32, 4>(qkv, cu, out, B, heads, max_seq, st);
-    return run_attn_bf16<64, 32, 4>(qkv, cu, out, B, heads, max_seq, st);
+    if (hd == 128) return run_attn_bf16<128, 32, 4>(qkv, cu, out, part, B, heads, st);
+    return run_attn_bf16<64, 32, 4>(qkv, cu, out, part, B, heads, st);
   }
   if (hd == 128) return run_attn_f32<128>(qkv, cu, out, B, heads, max_seq, st);
   return run_attn_f32<64>(qkv, cu, out, B, heads, max_seq, st);

@@ -55,8 +55,15 @@ constexpr size_t kSkPartFloats = size_t(256) * 256;  // one 256 x 256 fp32 tile 
 constexpr size_t kSkPartBytes = size_t(kSkMaxWorkgroups) * 2 * kSkPartFloats * sizeof(float);
 hipError_t launch_gemm(bool bf16, int epi, const GemmProblem &p, hipStream_t st);
 
-// qkv [Tmax][3D] -> out [Tmax][D] (ld = D), per sample and head over cu.
-hipError_t launch_attention(bool bf16, const void *qkv, const int *cu, void *out, int B, int heads,
-                            int hd, int max_seq, hipStream_t st);
+// Stream-K partial results of the bf16 attention core (part of the caller's workspace): two
+// slots per workgroup, each the unnormalised output and running max / sum of one query tile.
+constexpr int kAttnMaxWorkgroups = 512;
+constexpr size_t kAttnSlotFloats = size_t(4) * 2 * 8 * 64 * 4 + size_t(4) * 2 * 64 * 2;
+constexpr size_t kAttnPartBytes = size_t(kAttnMaxWorkgroups) * 2 * kAttnSlotFloats * sizeof(float);
+
+// qkv [Tmax][3D] -> out [Tmax][D] (ld = D), per sample and head over cu.  part: kAttnPartBytes of
+// device scratch for the bf16 path (unused by the fp32 path).
+hipError_t launch_attention(bool bf16, const void *qkv, const int *cu, void *out, float *part, int B,
+                            int heads, int hd, int max_seq, hipStream_t st);
 
 }  // namespace hilo

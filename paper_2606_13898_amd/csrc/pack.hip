@@ -169,11 +169,10 @@ hipError_t launch_decompress(bool bf16, const float *z, const int *idx_map, cons
 
 // ------------------------------------------------------------------------------- row norm
 
-constexpr int kNormMaxV = 32;  // float4 per lane: D <= 8192
-
 // One wave per row: LN(z) (biased variance, eps 1e-6) * (1 + scale) + shift for the row's sample
-// and stream, written in the projection's input dtype.
-template <bool BF16>
+// and stream, written in the projection's input dtype.  NV = float4s per lane covers D <= 256 NV;
+// the row stays in registers between the mean, variance and output passes.
+template <bool BF16, int NV>
 __global__ __launch_bounds__(256) void k_rownorm(const float *__restrict__ z, const int *__restrict__ cu,
                                                  const float *__restrict__ mod, int B, int L, int D,
                                                  int Tmax, int which, void *__restrict__ out) {
@@ -185,20 +184,18 @@ __global__ __launch_bounds__(256) void k_rownorm(const float *__restrict__ z, co
   const float *shift = mod + (size_t(s * 2 + sigma) * 6 + which * 3) * D;
   const float *scale = shift + D;
   const float *zr = z + size_t(row) * D;
-  float4 v[kNormMaxV];
+  float4 v[NV];
   float sum = 0.f;
 #pragma unroll
-  for (int k = 0; k < kNormMaxV; ++k) {
+  for (int k = 0; k < NV; ++k) {
     const int c = (k * 64 + lane) * 4;
-    if (c < D) {
-      v[k] = *reinterpret_cast<const float4 *>(zr + c);
-      sum += (v[k].x + v[k].y) + (v[k].z + v[k].w);
-    }
+    v[k] = c < D ? *reinterpret_cast<const float4 *>(zr + c) : make_float4(0.f, 0.f, 0.f, 0.f);
+    sum += (v[k].x + v[k].y) + (v[k].z + v[k].w);
   }
   const float mean = wave_sum_f32(sum) / float(D);
   float sq = 0.f;
 #pragma unroll
-  for (int k = 0; k < kNormMaxV; ++k) {
+  for (int k = 0; k < NV; ++k) {
     const int c = (k * 64 + lane) * 4;
     if (c < D) {
       const float a = v[k].x - mean, b = v[k].y - mean, e = v[k].z - mean, f = v[k].w - mean;
@@ -208,7 +205,7 @@ __global__ __launch_bounds__(256) void k_rownorm(const float *__restrict__ z, co
   const float var = wave_sum_f32(sq) / float(D);
   const float rstd = 1.0f / sqrtf(var + 1e-6f);
 #pragma unroll
-  for (int k = 0; k < kNormMaxV; ++k) {
+  for (int k = 0; k < NV; ++k) {
     const int c = (k * 64 + lane) * 4;
     if (c < D) {
       const float4 sc = *reinterpret_cast<const float4 *>(scale + c);
@@ -230,17 +227,28 @@ __global__ __launch_bounds__(256) void k_rownorm(const float *__restrict__ z, co
   }
 }
 
+template <bool BF16>
+static hipError_t run_rownorm(const float *z, const int *cu, const float *mod, int B, int L, int D,
+                              int Tmax, int which, void *out, hipStream_t st) {
+  const int nblk = (Tmax + 3) / 4;
+  const int nv = (D + 255) / 256;
+#define HILO_NORM(NVV)                                                                          \
+  hipLaunchKernelGGL((k_rownorm<BF16, NVV>), dim3(nblk), dim3(256), 0, st, z, cu, mod, B, L, D, \
+                     Tmax, which, out)
+  if (nv <= 4) HILO_NORM(4);
+  else if (nv <= 8) HILO_NORM(8);
+  else if (nv <= 12) HILO_NORM(12);
+  else if (nv <= 16) HILO_NORM(16);
+  else HILO_NORM(32);
+#undef HILO_NORM
+  return hipGetLastError();
+}
+
 hipError_t launch_rownorm(bool bf16, const float *z, const int *cu, const float *mod, int B, int L,
                           int D, int Tmax, int which, void *out, hipStream_t st) {
-  const int nblk = (Tmax + 3) / 4;
-  if (nblk <= 0) return hipSuccess;
-  if (bf16)
-    hipLaunchKernelGGL(k_rownorm<true>, dim3(nblk), dim3(256), 0, st, z, cu, mod, B, L, D, Tmax,
-                       which, out);
-  else
-    hipLaunchKernelGGL(k_rownorm<false>, dim3(nblk), dim3(256), 0, st, z, cu, mod, B, L, D, Tmax,
-                       which, out);
-  return hipGetLastError();
+  if (Tmax <= 0) return hipSuccess;
+  return bf16 ? run_rownorm<true>(z, cu, mod, B, L, D, Tmax, which, out, st)
+              : run_rownorm<false>(z, cu, mod, B, L, D, Tmax, which, out, st);
 }
 
 }  // namespace hilo

@@ -56,7 +56,7 @@ _SIG = {
     "hilo_mlp": [ctypes.POINTER(hilo_shape), _P, _P, ctypes.POINTER(hilo_mlp_w), _P, _P,
                  ctypes.c_size_t, _P],
     "hilo_decompress": [ctypes.POINTER(hilo_shape), _P, _P, _P, _P, _P, _P, _P],
-    "hilo_attention_core": [ctypes.POINTER(hilo_shape), _P, _P, _P, _P],
+    "hilo_attention_core": [ctypes.POINTER(hilo_shape), _P, _P, _P, _P, ctypes.c_size_t, _P],
     "hilo_workspace_bytes": [ctypes.POINTER(hilo_shape)],
     "hilo_max_tokens": [ctypes.POINTER(hilo_shape)],
     "hilo_status_str": [ctypes.c_int32],
@@ -189,9 +189,11 @@ def hilo_decompress(shape, z, idx_map, cu_seqlens, seg_off, y_img, y_txt, stream
         _ptr(y_img), _ptr(y_txt), _stream(stream)))
 
 
-def hilo_attention_core(shape, qkv, cu_seqlens, out, stream=None):
+def hilo_attention_core(shape, qkv, cu_seqlens, out, workspace=None, stream=None):
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
     _check("hilo_attention_core", lib().hilo_attention_core(
-        ctypes.byref(shape), _ptr(qkv), _ptr(cu_seqlens), _ptr(out), _stream(stream)))
+        ctypes.byref(shape), _ptr(qkv), _ptr(cu_seqlens), _ptr(out), _ptr(workspace), ws_bytes,
+        _stream(stream)))
 
 
 def hilo_profile_enable(on: bool):

@@ -45,7 +45,7 @@ def test_max_tokens_and_workspace():
     s = good_shape()
     assert hilo.hilo_max_tokens(s) == 2 * (80 + 5)
     T = 170
-    part = 256 * 2 * 256 * 256 * 4  # stream-K partial tiles of the bf16 projections
+    part = 256 * 2 * 256 * 256 * 4  # stream-K partials (projections; the attention core's fit inside)
     want = max(-(-T * 256 * 2 // 256) * 256 + -(-T * 768 * 2 // 256) * 256,
                -(-T * 256 * 2 // 256) * 256 + -(-T * 1024 * 2 // 256) * 256) + part
     assert hilo.hilo_workspace_bytes(s) == want
@@ -139,7 +139,8 @@ def test_valid_calls_without_a_device_report_device_error():
     assert call_select(s, mode=hilo.THRESHOLD, tau=[0.1, 0.2]) == 6
     aw = (hilo.hilo_attn_w * 2)(*[hilo.hilo_attn_w(FAKE, FAKE, FAKE, FAKE)] * 2)
     assert hilo.lib().hilo_attention(ctypes.byref(s), FAKE, FAKE, aw, FAKE, FAKE, 1 << 40, None) == 6
-    assert hilo.lib().hilo_attention_core(ctypes.byref(s), FAKE, FAKE, FAKE, None) == 6
+    assert hilo.lib().hilo_attention_core(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, 1 << 40, None) == 6
+    assert hilo.lib().hilo_attention_core(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, 10, None) == 5
 
 
 def test_profile_api():

@@ -187,6 +187,7 @@ def test_attention_core_ragged(hd, lens):
     q = torch.from_numpy(qkv).to(torch.bfloat16).cuda()
     out = torch.zeros(T, D, dtype=torch.bfloat16, device="cuda")
     cut = torch.from_numpy(cu).cuda()
-    hilo.hilo_attention_core(shp, q, cut, out)
+    ws = torch.empty(hilo.hilo_workspace_bytes(shp), dtype=torch.uint8, device="cuda")
+    hilo.hilo_attention_core(shp, q, cut, out, ws)
     torch.cuda.synchronize()
     assert_close(to_np(out), want, "bf16", f"attention core hd={hd}")
