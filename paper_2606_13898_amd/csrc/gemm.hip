@@ -279,6 +279,7 @@ __global__ __launch_bounds__(WM *WN * 64) void k_gemm_sk(GemmProblem p) {
 #pragma unroll
           for (int j = 0; j < TN; ++j)
             acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fb[j], fa[i], acc[i][j], 0, 0, 0);
+        __builtin_amdgcn_iglp_opt(1);  // interleave the next step's LDS reads with the MFMAs
       }
     }
 
