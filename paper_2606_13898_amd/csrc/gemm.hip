@@ -5,7 +5,7 @@
 //
 // bf16 path: gfx950 MFMA v_mfma_f32_16x16x32_bf16, fp32 accumulation in VGPRs; 256 x 256 tiles
 // on 8 waves, K steps of 64 through a double-buffered LDS ring filled by direct global->LDS loads,
-// scheduled stream-K over one persistent workgroup per CU.
+// one persistent workgroup per CU running whole data-parallel waves, then a stream-K remainder.
 //
 // The MFMA is issued with the weight fragment as its first operand, so each lane's 4
 // accumulators are 4 consecutive output columns of one row (contiguous epilogue stores).
@@ -14,10 +14,14 @@
 
 namespace hilo {
 
+// tanh-approximated GELU, 0.5 u (1 + tanh(y)) with y = sqrt(2/pi) (u + 0.044715 u^3), evaluated
+// through the identity 0.5 (1 + tanh(y)) = 1 / (1 + exp(-2y)): one hardware exp2 and one
+// reciprocal (about one ulp each) instead of a full tanh.  Very negative u gives exp2 -> inf and
+// the result -0; very positive u gives exp2 -> 0 and the result u.
 HILO_DEV float gelu_tanh(float u) {
-  const float k0 = 0.7978845608028654f;  // sqrt(2 / pi)
-  const float inner = k0 * (u + 0.044715f * u * u * u);
-  return 0.5f * u * (1.0f + tanhf(inner));
+  constexpr float c = -2.0f * 0.7978845608028654f * 1.4426950408889634f;  // -2 sqrt(2/pi) log2(e)
+  const float t = c * u * (1.0f + 0.044715f * u * u);
+  return u * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(t));
 }
 
 // Row range of row-tile t: tiles of sample s are [image tiles][text tiles].
@@ -139,19 +143,52 @@ HILO_DEV TileRows decode_row_tile(const GemmProblem &p, int BM, int r) {
   return tr;
 }
 
-// Stream-K schedule.  The iteration space is (tile, K step) with tiles ordered row-tile fastest
-// (tile t = tn * R + r); the P persistent workgroups take equal contiguous ranges of it, so the
-// load is balanced whatever the ragged tile count.  A tile fully inside one range is finished
-// there; a tile cut by range boundaries leaves fp32 partial sums (at most two per workgroup: the
-// first and the last tile of its range) that k_gemm_fix adds up in workgroup order and finishes
-// with the same epilogue -- deterministic, and no workgroup ever waits for another.
+// Schedule of the bf16 projections over P persistent workgroups (one per CU).  A unit is one
+// K piece of one output tile: tiles are cut into s pieces when there are fewer tiles than
+// workgroups (s = ceil(P / tiles), at most one K step per piece), else s = 1.  Units are ordered
+// piece-major, row tile fastest within a piece.  The first floor(U / P) * P units run
+// data-parallel in whole waves -- the 32 workgroups of an XCD then work on 32 neighbouring tiles
+// at the same K step, so its L2 serves each weight and activation slice to all of them.  The
+// remaining units (all of the same K length) are spread evenly over the P workgroups stream-K,
+// so no CU idles through a partial last wave.  A unit not finished in one place leaves an fp32
+// partial tile (data-parallel unit u: slot u; stream-K range of workgroup w: slots P + 2w for its
+// first unit and P + 2w + 1 for its second); k_gemm_fix adds the partials of each such tile in a
+// fixed order and runs the epilogue -- deterministic, and no workgroup ever waits for another.
+struct SkPlan {
+  int R, T, nk;    // row tiles, tiles, K steps
+  int s, U, dp;    // pieces per tile, units, data-parallel units
+  int len;         // K steps of a stream-K unit
+  long long I;     // stream-K iterations
+};
+
+HILO_DEV SkPlan sk_plan(const GemmProblem &p, int BM, int BN, int P) {
+  SkPlan q;
+  q.R = row_tiles_total(p, BM);
+  q.T = q.R * ((p.N + BN - 1) / BN);
+  q.nk = p.K / 64;
+  q.s = (q.T >= P || q.T == 0) ? 1 : min((P + q.T - 1) / q.T, q.nk);
+  q.U = q.T * q.s;
+  q.dp = q.U / P * P;
+  // the stream-K units all lie in the last piece (or every piece is one K step long)
+  const int tail = q.U - q.dp;
+  const int pc = tail > 0 ? q.dp / q.T : 0;
+  q.len = (pc + 1) * q.nk / q.s - pc * q.nk / q.s;
+  q.I = (long long)tail * q.len;
+  return q;
+}
+
 struct SkRange {
   long long beg, end;
 };
 
-HILO_DEV SkRange sk_range(long long I, int P, int pid) {
-  return SkRange{I * pid / P, I * (pid + 1) / P};
+HILO_DEV SkRange sk_range(long long I, int P, int w) {
+  return SkRange{I * w / P, I * (w + 1) / P};
 }
+
+// The workgroup whose stream-K range holds iteration a.
+HILO_DEV int sk_owner(long long I, int P, long long a) { return int(((a + 1) * P - 1) / I); }
+
+HILO_DEV int piece_k0(const SkPlan &q, int piece) { return piece * q.nk / q.s; }
 
 // WM x WN waves, wave tile (BM/WM) x (BN/WN), K step 64 through a double-buffered LDS ring filled
 // by direct global->LDS loads one step ahead, one barrier per step.
@@ -172,24 +209,15 @@ struct SkTile {
     return ((size_t(wid) * TM * TN + i * TN + j) * 64 + lane) * 4;
   }
 
+  // Epilogue of the accumulator fragment (i, j) of wave wid: 4 consecutive columns of one row.
   template <int EPI>
-  HILO_DEV static void epilogue(const GemmProblem &p, const TileRows &tr, int n0, int wid, int lane,
-                                f32x4 (&acc)[TM][TN]) {
-    const int wrow = (wid / WN) * (BM / WM), wcol = (wid % WN) * (BN / WN);
-    const int lr = lane & 15, lg = lane >> 4;
-#pragma unroll
-    for (int i = 0; i < TM; ++i) {
-      const int rl = wrow + i * 16 + lr;
-      if (rl >= tr.nrows) continue;
-      const int m = tr.row0 + rl;
-#pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        const int n = n0 + wcol + j * 16 + 4 * lg;
-        if (n >= p.N) continue;
-        float a4[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
-        epilogue4<EPI, true>(p, tr, m, n, a4);
-      }
-    }
+  HILO_DEV static void frag(const GemmProblem &p, const TileRows &tr, int n0, int wid, int i, int j,
+                            int lane, const f32x4 &a) {
+    const int rl = (wid / WN) * (BM / WM) + i * 16 + (lane & 15);
+    const int n = n0 + (wid % WN) * (BN / WN) + j * 16 + 4 * (lane >> 4);
+    if (rl >= tr.nrows || n >= p.N) return;
+    float a4[4] = {a[0], a[1], a[2], a[3]};
+    epilogue4<EPI, true>(p, tr, tr.row0 + rl, n, a4);
   }
 };
 
@@ -200,17 +228,12 @@ __global__ __launch_bounds__(WM *WN * 64) void k_gemm_sk(GemmProblem p) {
   __shared__ __attribute__((aligned(1024))) uint16_t sA[2][BM * BK];
   __shared__ __attribute__((aligned(1024))) uint16_t sB[2][BN * BK];
 
-  // logical workgroup index: each XCD gets a contiguous band of the iteration space (a narrow
-  // band of weight columns for all rows), so its L2 serves the weight tiles to all of its CUs
+  // logical workgroup index: each XCD gets a contiguous run of workgroup indices, hence of
+  // neighbouring tiles in every data-parallel wave and of the stream-K iteration space
   const int P = gridDim.x;
   const int pid = xcd_remap(blockIdx.x, P);
-  const int R = row_tiles_total(p, BM);
-  const int tilesN = (p.N + BN - 1) / BN;
-  const int nk = p.K / BK;
-  const long long I = (long long)R * tilesN * nk;
-  const SkRange rg = sk_range(I, P, pid);
-  if (rg.beg >= rg.end) return;
-  const long long head = rg.beg / nk;
+  const SkPlan q = sk_plan(p, BM, BN, P);
+  const SkRange rg = sk_range(q.I, P, pid);
 
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int wrow = (wid / WN) * (BM / WM), wcol = (wid % WN) * (BN / WN);
@@ -218,12 +241,36 @@ __global__ __launch_bounds__(WM *WN * 64) void k_gemm_sk(GemmProblem p) {
   const int lrow = lane >> 3, lslot = lane & 7;
   const uint16_t *A = reinterpret_cast<const uint16_t *>(p.A);
 
-  for (long long it = rg.beg; it < rg.end;) {
-    const long long t = it / nk;
-    const int kb = int(it - t * nk);
-    const int ke = int(min((long long)nk, (long long)kb + (rg.end - it)));
-    const int tn = int(t / R);
-    const TileRows tr = decode_row_tile(p, BM, int(t % R));
+  int u = pid;            // next data-parallel unit of this workgroup
+  long long it = rg.beg;  // next stream-K iteration of this workgroup
+  while (true) {
+    int t, kb, ke;
+    float *slot;          // null: the tile is complete here, run the epilogue
+    if (u < q.dp) {
+      const int pc = u / q.T;
+      t = u - pc * q.T;
+      kb = piece_k0(q, pc);
+      ke = piece_k0(q, pc + 1);
+      slot = q.s == 1 ? nullptr : p.part + size_t(u) * T::kPartFloats;
+      u += P;
+    } else if (it < rg.end) {
+      const long long v = it / q.len;
+      const int k0 = int(it - v * q.len);
+      const int k1 = int(min((long long)q.len, k0 + (rg.end - it)));
+      const int uu = q.dp + int(v);
+      const int pc = uu / q.T;
+      t = uu - pc * q.T;
+      kb = piece_k0(q, pc) + k0;
+      ke = piece_k0(q, pc) + k1;
+      const bool whole = q.s == 1 && k0 == 0 && k1 == q.len;
+      slot = whole ? nullptr
+                   : p.part + (size_t(P) + size_t(pid) * 2 + (it == rg.beg ? 0 : 1)) * T::kPartFloats;
+      it += k1 - k0;
+    } else {
+      break;
+    }
+    const int tn = t / q.R;
+    const TileRows tr = decode_row_tile(p, BM, t - tn * q.R);
     const int n0 = tn * BN;
     const uint16_t *Wt = reinterpret_cast<const uint16_t *>(p.W[tr.sigma]);
 
@@ -283,59 +330,85 @@ __global__ __launch_bounds__(WM *WN * 64) void k_gemm_sk(GemmProblem p) {
       }
     }
 
-    if (kb == 0 && ke == nk) {
-      T::template epilogue<EPI>(p, tr, n0, wid, lane, acc);
+    if (slot == nullptr) {
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) T::template frag<EPI>(p, tr, n0, wid, i, j, lane, acc[i][j]);
     } else {
-      float *slot = p.part + (size_t(pid) * 2 + (t == head ? 0 : 1)) * T::kPartFloats;
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j)
           *reinterpret_cast<f32x4 *>(slot + T::part_index(wid, i, j, lane)) = acc[i][j];
     }
-    it += ke - kb;
-    __syncthreads();  // the next tile's loads reuse the LDS ring
+    __syncthreads();  // the next unit's loads reuse the LDS ring
   }
 }
 
-// Finishes every tile cut by range boundaries: the workgroup whose range holds the tile's first
-// K step sums the partials of all contributors in workgroup order, then runs the epilogue.
-template <int BM, int BN, int WM, int WN, int EPI>
-__global__ __launch_bounds__(WM *WN * 64) void k_gemm_fix(GemmProblem p) {
-  using T = SkTile<BM, BN, WM, WN>;
-  constexpr int BK = T::BK, TM = T::TM, TN = T::TN;
-  const int P = gridDim.x;
-  const int pid = blockIdx.x;
-  const int R = row_tiles_total(p, BM);
-  const int tilesN = (p.N + BN - 1) / BN;
-  const int nk = p.K / BK;
-  const long long I = (long long)R * tilesN * nk;
-  const SkRange rg = sk_range(I, P, pid);
-  if (rg.beg >= rg.end) return;
-  const long long tl = (rg.end - 1) / nk;            // last tile touched by this range
-  if (rg.end >= (tl + 1) * nk) return;                // it ends inside this range: not cut here
-  if (rg.beg > tl * nk) return;                       // this range does not hold its first step
-  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+// Finishes every tile left in partials: (tile, main-kernel wave) work items, 4 waves per
+// workgroup, each wave summing two rows of fragments of that main-kernel wave over the tile's
+// partials (pieces in K order, stream-K contributors in workgroup order), then running the
+// epilogue on them.
+constexpr int kFixThreads = 256;
 
-  f32x4 acc[TM][TN];
+template <int BM, int BN, int WM, int WN, int EPI>
+__global__ __launch_bounds__(kFixThreads) void k_gemm_fix(GemmProblem p, int P) {
+  using T = SkTile<BM, BN, WM, WN>;
+  constexpr int TM = T::TM, TN = T::TN, NW = T::NW, FW = kFixThreads / 64, IPW = TM / FW;
+  static_assert(IPW * FW == TM, "fix waves must split the fragment rows");
+  const SkPlan q = sk_plan(p, BM, BN, P);
+  const int nfix = q.s > 1 ? q.T : q.U - q.dp;
+  const int lane = threadIdx.x & 63, fw = threadIdx.x >> 6;
+  for (int x = blockIdx.x; x < nfix * NW; x += gridDim.x) {
+    const int f = x / NW, wid = x - f * NW;
+    const int t = q.s > 1 ? f : q.dp + f;
+    f32x4 acc[IPW][TN];
 #pragma unroll
-  for (int i = 0; i < TM; ++i)
+    for (int i = 0; i < IPW; ++i)
 #pragma unroll
-    for (int j = 0; j < TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-  for (int q = pid; q < P; ++q) {
-    const SkRange rq = sk_range(I, P, q);
-    if (rq.beg >= rq.end) continue;
-    if (rq.beg >= (tl + 1) * nk) break;
-    const float *slot = p.part + (size_t(q) * 2 + (rq.beg / nk == tl ? 0 : 1)) * T::kPartFloats;
+      for (int j = 0; j < TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    auto add = [&](const float *slot) {
+      f32x4 v[IPW][TN];
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
+      for (int i = 0; i < IPW; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          v[i][j] = *reinterpret_cast<const f32x4 *>(slot + T::part_index(wid, fw * IPW + i, j, lane));
+#pragma unroll
+      for (int i = 0; i < IPW; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] += v[i][j];
+    };
+    bool done_whole = false;
+    for (int pc = 0; pc < q.s; ++pc) {
+      const int u = pc * q.T + t;
+      if (u < q.dp) {
+        add(p.part + size_t(u) * T::kPartFloats);
+        continue;
+      }
+      const int v = u - q.dp;
+      const long long a0 = (long long)v * q.len;
+      const int w0 = sk_owner(q.I, P, a0), w1 = sk_owner(q.I, P, a0 + q.len - 1);
+      if (q.s == 1 && w0 == w1) {  // one workgroup held the whole tile and finished it
+        done_whole = true;
+        break;
+      }
+      for (int w = w0; w <= w1; ++w) {
+        const SkRange rw = sk_range(q.I, P, w);
+        if (rw.beg >= rw.end) continue;
+        add(p.part + (size_t(P) + size_t(w) * 2 + (rw.beg / q.len == v ? 0 : 1)) * T::kPartFloats);
+      }
+    }
+    if (done_whole) continue;
+    const int tn = t / q.R;
+    const TileRows tr = decode_row_tile(p, BM, t - tn * q.R);
+#pragma unroll
+    for (int i = 0; i < IPW; ++i)
 #pragma unroll
       for (int j = 0; j < TN; ++j)
-        acc[i][j] += *reinterpret_cast<const f32x4 *>(slot + T::part_index(wid, i, j, lane));
-    if (rq.end >= (tl + 1) * nk) break;
+        T::template frag<EPI>(p, tr, tn * BN, wid, fw * IPW + i, j, lane, acc[i][j]);
   }
-  const TileRows tr = decode_row_tile(p, BM, int(tl % R));
-  T::template epilogue<EPI>(p, tr, int(tl / R) * BN, wid, lane, acc);
 }
 
 // ------------------------------------------------------------------------------- fp32 path
@@ -409,7 +482,9 @@ static hipError_t run_bf16(const GemmProblem &p, hipStream_t st) {
   hipLaunchKernelGGL((k_gemm_sk<BM, BN, WM, WN, EPI>), dim3(P), dim3(WM * WN * 64), 0, st, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((k_gemm_fix<BM, BN, WM, WN, EPI>), dim3(P), dim3(WM * WN * 64), 0, st, p);
+  // fewer than P tiles are ever left in partials; one work item per (tile, main-kernel wave)
+  hipLaunchKernelGGL((k_gemm_fix<BM, BN, WM, WN, EPI>), dim3(P * WM * WN), dim3(kFixThreads), 0, st,
+                     p, P);
   return hipGetLastError();
 }
 

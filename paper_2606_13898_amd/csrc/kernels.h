@@ -46,13 +46,14 @@ struct GemmProblem {
   int gate_idx, D;
   const int *cu;          // [B+1]
   int B, L, max_img_rows; // max_img_rows = images * N
-  float *part;            // bf16 path: stream-K partial tiles, kSkMaxWorkgroups * 2 slots
+  float *part;            // bf16 path: partial tiles, 3 * kSkMaxWorkgroups slots
 };
 
-// Stream-K partial-sum area of the bf16 GEMMs (part of the caller's workspace).
+// Partial-sum area of the bf16 GEMMs (part of the caller's workspace): one slot per data-parallel
+// unit of a split wave plus two per workgroup for its stream-K range.
 constexpr int kSkMaxWorkgroups = 256;
 constexpr size_t kSkPartFloats = size_t(256) * 256;  // one 256 x 256 fp32 tile per slot
-constexpr size_t kSkPartBytes = size_t(kSkMaxWorkgroups) * 2 * kSkPartFloats * sizeof(float);
+constexpr size_t kSkPartBytes = size_t(kSkMaxWorkgroups) * 3 * kSkPartFloats * sizeof(float);
 hipError_t launch_gemm(bool bf16, int epi, const GemmProblem &p, hipStream_t st);
 
 // Stream-K partial results of the bf16 attention core (part of the caller's workspace): two
