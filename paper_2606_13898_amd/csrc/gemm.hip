@@ -306,7 +306,6 @@ __global__ __launch_bounds__(WM *WN * 64) void k_gemm_sk(GemmProblem p) {
       const int buf = (kt - kb) & 1;
       wait_vmem_le<0>();
       __syncthreads();
-      if (kt + 1 < ke) issue((kt + 1) * BK, buf ^ 1);
 #pragma unroll
       for (int ks = 0; ks < BK / 32; ++ks) {
         const int ch = ks * 4 + lg;
@@ -321,12 +320,20 @@ __global__ __launch_bounds__(WM *WN * 64) void k_gemm_sk(GemmProblem p) {
           const int r = wcol + j * 16 + lr;
           fb[j] = *reinterpret_cast<const bf16x8 *>(&sB[buf][r * BK + ((ch ^ swz<BK>(r)) * 8)]);
         }
+        // the next step's loads go out only after this step's fragment reads are issued: the
+        // LDS then serves the reads first and the MFMAs start sooner after the barrier
+        if (ks == BK / 32 - 1 && kt + 1 < ke) issue((kt + 1) * BK, buf ^ 1);
 #pragma unroll
         for (int i = 0; i < TM; ++i)
 #pragma unroll
           for (int j = 0; j < TN; ++j)
             acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fb[j], fa[i], acc[i][j], 0, 0, 0);
-        __builtin_amdgcn_iglp_opt(1);  // interleave the next step's LDS reads with the MFMAs
+        // alternate single MFMAs and LDS reads while the reads last
+#pragma unroll
+        for (int g = 0; g < TM + TN; ++g) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
+        }
       }
     }
 
