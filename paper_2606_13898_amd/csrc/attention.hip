@@ -244,7 +244,7 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a) {
     for (int qs = 0; qs < QS; ++qs) { mrun[qs] = -INFINITY; lrun[qs] = 0.f; }
 
     // one 64-key step; keys >= n (only in the unit's last step) are masked under a uniform branch
-    auto step = [&](int buf, int kv0) {
+    auto step = [&](int buf, int kv0, auto &&after_scores) {
       // S^T for 64 keys x QW queries: sc[ks][qs][e] = score(query qs*16+lr, key ks*16+4*lg+e)
       f32x4 sc[4][QS];
 #pragma unroll
@@ -264,6 +264,7 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a) {
             sc[ks][qs] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[qs][kk], sc[ks][qs], 0, 0, 0);
         }
       }
+      after_scores();
       if (kv0 + BKV > n) {
 #pragma unroll
         for (int ks = 0; ks < 4; ++ks)
@@ -334,11 +335,13 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a) {
     for (int kt = kb; kt < ke; ++kt) {
       const int buf = (kt - kb) & 1;
       const int kv0 = kt * BKV;
-      if (kt + 1 < ke) {
-        issue_k(kv0 + BKV, buf ^ 1);
-        load_v(kv0 + BKV);
-      }
-      step(buf, kv0);
+      // the next tile's loads go out once this step's K fragments have been read
+      step(buf, kv0, [&]() {
+        if (kt + 1 < ke) {
+          issue_k(kv0 + BKV, buf ^ 1);
+          load_v(kv0 + BKV);
+        }
+      });
       if (kt + 1 < ke) {
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         store_v(buf ^ 1);
