@@ -161,11 +161,23 @@ struct SkPlan {
   long long I;     // stream-K iterations
 };
 
+// A problem with fewer tiles than workgroups and at most this many K steps runs one whole tile per
+// workgroup (some CUs idle) instead of cutting tiles into K pieces: for short K the partial tiles
+// and their fixup cost more than the idle CUs.
+constexpr int kNoSplitSteps = 64;
+
 HILO_DEV SkPlan sk_plan(const GemmProblem &p, int BM, int BN, int P) {
   SkPlan q;
   q.R = row_tiles_total(p, BM);
   q.T = q.R * ((p.N + BN - 1) / BN);
   q.nk = p.K / 64;
+  if (q.T < P && q.nk <= kNoSplitSteps) {
+    q.s = 1;
+    q.U = q.dp = q.T;
+    q.len = q.nk;
+    q.I = 0;
+    return q;
+  }
   q.s = (q.T >= P || q.T == 0) ? 1 : min((P + q.T - 1) / q.T, q.nk);
   q.U = q.T * q.s;
   q.dp = q.U / P * P;

@@ -191,3 +191,24 @@ def test_attention_core_ragged(hd, lens):
     hilo.hilo_attention_core(shp, q, cut, out, ws)
     torch.cuda.synchronize()
     assert_close(to_np(out), want, "bf16", f"attention core hd={hd}")
+
+
+@pytest.mark.parametrize("shp", [
+    # down projection: ~6 tiles, K = 8192 (128 steps) -> tiles cut into K pieces plus a stream-K tail
+    inputs.BlockShape(3, 1, 16, 20, 40, 256, 2, 128, 8192, "bf16"),
+    # a single tile: every K piece is one step, the fixup sums 128 partial tiles
+    inputs.BlockShape(1, 1, 16, 16, 0, 256, 2, 128, 8192, "bf16"),
+], ids=["pieces_and_tail", "one_tile_128_pieces"])
+def test_mlp_split_k(shp):
+    """MLP with a long down-projection K and few output tiles: the projection is split along K
+    and finished by the fixup; every row of z is compared with the oracle."""
+    print(f"[parity] split-K mlp shape={shp}", flush=True)
+    wl = inputs.make_workload("splitk", shape=shp, seed=11)
+    db = DeviceBlock(wl)
+    ref = oracle_for(wl)
+    db.run(hilo.TOPK)
+    torch.cuda.synchronize()
+    check_selection(db, ref)
+    T = int(ref["cu"][-1])
+    assert_close(to_np(db.z)[:T], ref["z2"], "bf16", "z after split-K mlp")
+    assert_close(to_np(db.y_img), ref["y_img"], "bf16", "y_img split-K")
