@@ -114,6 +114,9 @@ def main():
     ap.add_argument("--workload", default="m1024", choices=sorted(DESCR))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
+    ap.add_argument("--copy-mib", type=int, default=0,
+                    help="only run one plain device-to-device copy of this many MiB (the known-size "
+                         "kernel that calibrates the HBM traffic counters) and exit")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -123,6 +126,15 @@ def main():
 
     import numpy as np
     import torch
+
+    if args.copy_mib:
+        a = torch.ones(args.copy_mib << 20, dtype=torch.uint8, device="cuda")
+        b = torch.empty_like(a)
+        torch.cuda.synchronize()
+        b.copy_(a)
+        torch.cuda.synchronize()
+        print(json.dumps({"copied_bytes": a.numel()}))
+        return
 
     from paper_2606_13898_amd import hilo, inputs
     from paper_2606_13898_amd.pipeline import DeviceBlock

@@ -276,7 +276,7 @@ hilo_status hilo_attention(const hilo_shape *s, float *z, const int32_t *cu_seql
   p.bias[0] = w[0].b_qkv; p.bias[1] = w[1].b_qkv;
   p.N = 3 * D; p.K = D;
   p.out = qkv; p.ldo = 3 * D;
-  he = timed(K_GEMM_QKV, st, [&] { return launch_gemm(bf, EPI_BIAS, p, st); });
+  he = timed(K_GEMM_QKV, st, [&] { return launch_gemm(bf, GEMM_QKV, p, st); });
   if (he != hipSuccess) return HILO_E_DEVICE;
 
   const int max_seq = s->images * s->grid_h * s->grid_w + s->text_len;
@@ -292,7 +292,7 @@ hilo_status hilo_attention(const hilo_shape *s, float *z, const int32_t *cu_seql
   q.bias[0] = w[0].b_o; q.bias[1] = w[1].b_o;
   q.N = D; q.K = D;
   q.z = z; q.ldz = D; q.gate_idx = 2;
-  return dev_status(timed(K_GEMM_O, st, [&] { return launch_gemm(bf, EPI_RESID, q, st); }));
+  return dev_status(timed(K_GEMM_O, st, [&] { return launch_gemm(bf, GEMM_O, q, st); }));
 }
 
 hilo_status hilo_mlp(const hilo_shape *s, float *z, const int32_t *cu_seqlens,
@@ -326,7 +326,7 @@ hilo_status hilo_mlp(const hilo_shape *s, float *z, const int32_t *cu_seqlens,
   p.bias[0] = w[0].b1; p.bias[1] = w[1].b1;
   p.N = F; p.K = D;
   p.out = hid; p.ldo = F;
-  he = timed(K_GEMM_FC1, st, [&] { return launch_gemm(bf, EPI_GELU, p, st); });
+  he = timed(K_GEMM_FC1, st, [&] { return launch_gemm(bf, GEMM_FC1, p, st); });
   if (he != hipSuccess) return HILO_E_DEVICE;
 
   GemmProblem q = base_problem(s, cu_seqlens, mod, part);
@@ -335,7 +335,7 @@ hilo_status hilo_mlp(const hilo_shape *s, float *z, const int32_t *cu_seqlens,
   q.bias[0] = w[0].b2; q.bias[1] = w[1].b2;
   q.N = D; q.K = F;
   q.z = z; q.ldz = D; q.gate_idx = 5;
-  return dev_status(timed(K_GEMM_FC2, st, [&] { return launch_gemm(bf, EPI_RESID, q, st); }));
+  return dev_status(timed(K_GEMM_FC2, st, [&] { return launch_gemm(bf, GEMM_FC2, q, st); }));
 }
 
 hilo_status hilo_profile_enable(int32_t on) {

@@ -233,7 +233,7 @@ struct SkTile {
   }
 };
 
-template <int BM, int BN, int WM, int WN, int EPI>
+template <int BM, int BN, int WM, int WN, int EPI, int ROLE>
 __global__ __launch_bounds__(WM *WN * 64) void k_gemm_sk(GemmProblem p) {
   using T = SkTile<BM, BN, WM, WN>;
   constexpr int BK = T::BK, TM = T::TM, TN = T::TN, IA = T::IA, IB = T::IB, NW = T::NW;
@@ -371,7 +371,7 @@ __global__ __launch_bounds__(WM *WN * 64) void k_gemm_sk(GemmProblem p) {
 // epilogue on them.
 constexpr int kFixThreads = 256;
 
-template <int BM, int BN, int WM, int WN, int EPI>
+template <int BM, int BN, int WM, int WN, int EPI, int ROLE>
 __global__ __launch_bounds__(kFixThreads) void k_gemm_fix(GemmProblem p, int P) {
   using T = SkTile<BM, BN, WM, WN>;
   constexpr int TM = T::TM, TN = T::TN, NW = T::NW, FW = kFixThreads / 64, IPW = TM / FW;
@@ -494,15 +494,20 @@ int sk_workgroups() {
   return ncu[dev] < kSkMaxWorkgroups ? ncu[dev] : kSkMaxWorkgroups;
 }
 
-template <int BM, int BN, int WM, int WN, int EPI>
+template <int BM, int BN, int WM, int WN, int ROLE>
 static hipError_t run_bf16(const GemmProblem &p, hipStream_t st) {
   static_assert(size_t(BM) * BN <= kSkPartFloats, "partial slot too small");
   const int P = sk_workgroups();
-  hipLaunchKernelGGL((k_gemm_sk<BM, BN, WM, WN, EPI>), dim3(P), dim3(WM * WN * 64), 0, st, p);
+  hipLaunchKernelGGL((k_gemm_sk<BM, BN, WM, WN, role_epilogue(ROLE), ROLE>), dim3(P), dim3(WM * WN * 64), 0, st, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  // with at most B * (ceil(images * N / BM) + ceil(L / BM)) row tiles, a short-K problem below P
+  // tiles always runs unsplit and leaves no partials: no fixup launch
+  const long long tiles_max = (long long)p.B * ((p.max_img_rows + BM - 1) / BM + (p.L + BM - 1) / BM) *
+                              ((p.N + BN - 1) / BN);
+  if (tiles_max < P && p.K / 64 <= kNoSplitSteps) return hipSuccess;
   // fewer than P tiles are ever left in partials; one work item per (tile, main-kernel wave)
-  hipLaunchKernelGGL((k_gemm_fix<BM, BN, WM, WN, EPI>), dim3(P * WM * WN), dim3(kFixThreads), 0, st,
+  hipLaunchKernelGGL((k_gemm_fix<BM, BN, WM, WN, role_epilogue(ROLE), ROLE>), dim3(P * WM * WN), dim3(kFixThreads), 0, st,
                      p, P);
   return hipGetLastError();
 }
@@ -519,18 +524,19 @@ static hipError_t run_f32(const GemmProblem &p, hipStream_t st) {
   return hipGetLastError();
 }
 
-hipError_t launch_gemm(bool bf16, int epi, const GemmProblem &p, hipStream_t st) {
+hipError_t launch_gemm(bool bf16, int role, const GemmProblem &p, hipStream_t st) {
   if (!bf16) {
-    switch (epi) {
+    switch (role_epilogue(role)) {
       case EPI_BIAS: return run_f32<EPI_BIAS>(p, st);
       case EPI_GELU: return run_f32<EPI_GELU>(p, st);
       default: return run_f32<EPI_RESID>(p, st);
     }
   }
-  switch (epi) {
-    case EPI_BIAS: return run_bf16<256, 256, 2, 4, EPI_BIAS>(p, st);
-    case EPI_GELU: return run_bf16<256, 256, 2, 4, EPI_GELU>(p, st);
-    default: return run_bf16<256, 256, 2, 4, EPI_RESID>(p, st);
+  switch (role) {
+    case GEMM_QKV: return run_bf16<256, 256, 2, 4, GEMM_QKV>(p, st);
+    case GEMM_O: return run_bf16<256, 256, 2, 4, GEMM_O>(p, st);
+    case GEMM_FC1: return run_bf16<256, 256, 2, 4, GEMM_FC1>(p, st);
+    default: return run_bf16<256, 256, 2, 4, GEMM_FC2>(p, st);
   }
 }
 

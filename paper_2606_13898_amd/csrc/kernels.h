@@ -29,6 +29,12 @@ hipError_t launch_rownorm(bool bf16, const float *z, const int *cu, const float 
                           int D, int Tmax, int which, void *out, hipStream_t st);
 
 enum Epilogue { EPI_BIAS = 0, EPI_GELU = 1, EPI_RESID = 2 };
+// The four projections of the block; each gets its own kernel instantiation (so profiles and
+// counters tell them apart) with the epilogue it needs.
+enum GemmRole { GEMM_QKV = 0, GEMM_O = 1, GEMM_FC1 = 2, GEMM_FC2 = 3 };
+constexpr int role_epilogue(int role) {
+  return role == GEMM_QKV ? EPI_BIAS : role == GEMM_FC1 ? EPI_GELU : EPI_RESID;
+}
 
 // Segment-aware C = A W_sigma^T with the epilogue; rows of sample s split into the image segment
 // (stream 0) and the text segment (stream 1), tiles never straddle a segment.
@@ -54,7 +60,7 @@ struct GemmProblem {
 constexpr int kSkMaxWorkgroups = 256;
 constexpr size_t kSkPartFloats = size_t(256) * 256;  // one 256 x 256 fp32 tile per slot
 constexpr size_t kSkPartBytes = size_t(kSkMaxWorkgroups) * 3 * kSkPartFloats * sizeof(float);
-hipError_t launch_gemm(bool bf16, int epi, const GemmProblem &p, hipStream_t st);
+hipError_t launch_gemm(bool bf16, int role, const GemmProblem &p, hipStream_t st);
 
 // Stream-K partial results of the bf16 attention core (part of the caller's workspace): two
 // slots per workgroup, each the unnormalised output and running max / sum of one query tile.

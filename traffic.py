@@ -1,0 +1,142 @@
+#!/usr/bin/env python3
+"""HBM traffic per launch of every kernel kind of the bench, from rocprofv3 counters.
+
+Two counter passes over a short bench run (FETCH_SIZE, then WRITE_SIZE: bytes between the L2 and
+memory, per dispatch) and the same two passes over one plain device copy of known size, which
+calibrates each counter (calibrated bytes = counter / (counter of the copy / bytes the copy moves)).
+The result, profiles/traffic.json, is what bench.py reports as roofline.traffic; each entry carries
+a digest of the kernel sources it was measured on, and bench.py drops it once they change.
+
+    python traffic.py commands OUTDIR        # print the four rocprofv3 commands (run them on the GPU)
+    python traffic.py summarize OUTDIR       # write profiles/traffic.json and profiles/traffic_m1024.md
+"""
+from __future__ import annotations
+
+import collections
+import csv
+import json
+import os
+import sys
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from bench import source_digest  # noqa: E402
+
+COPY_MIB = 256
+BENCH = "python3 {root}/bench.py --steps 2 --warmup 1 --no-dense --no-cpu-baseline"
+COPY = "python3 {root}/bench.py --copy-mib %d" % COPY_MIB
+COUNTERS = ("FETCH_SIZE", "WRITE_SIZE")
+
+CSRC = "paper_2606_13898_amd/csrc/"
+HDRS = [CSRC + "common.h", CSRC + "kernels.h"]
+SOURCES = {
+    "score": [CSRC + "select.hip"], "select": [CSRC + "select.hip"], "layout": [CSRC + "select.hip"],
+    "compress": [CSRC + "pack.hip"], "decompress": [CSRC + "pack.hip"],
+    "rownorm_attn": [CSRC + "pack.hip"], "rownorm_mlp": [CSRC + "pack.hip"],
+    "gemm_qkv": [CSRC + "gemm.hip"], "gemm_o": [CSRC + "gemm.hip"], "gemm_fc1": [CSRC + "gemm.hip"],
+    "gemm_fc2": [CSRC + "gemm.hip"], "attention_core": [CSRC + "attention.hip"],
+}
+ROLES = {"0": "gemm_qkv", "1": "gemm_o", "2": "gemm_fc1", "3": "gemm_fc2"}
+
+
+def commands(out):
+    cmds = []
+    for cnt in COUNTERS:
+        for tag, prog in (("bench", BENCH), ("copy", COPY)):
+            cmds.append(f"timeout -s KILL 120 rocprofv3 --pmc {cnt} --output-format csv "
+                        f"-d {out}/{cnt} -o {tag} -- {prog.format(root=ROOT)}")
+    return cmds
+
+
+def load(out, cnt, tag):
+    """[(dispatch id, kernel name, value)] in dispatch order, values summed per dispatch."""
+    path = os.path.join(out, cnt, f"{tag}_counter_collection.csv")
+    per = collections.OrderedDict()
+    with open(path) as f:
+        for r in csv.DictReader(f):
+            key = int(r["Dispatch_Id"])
+            name = r["Kernel_Name"]
+            per.setdefault(key, [name, 0.0])[1] += float(r["Counter_Value"])
+    return [(d, n, v) for d, (n, v) in sorted(per.items())]
+
+
+def kind_of(name, state):
+    """Bench kernel kind of a dispatch; rownorm launches alternate attention / MLP per step."""
+    base = name.split("(")[0].replace("void ", "").strip()
+    if "k_gemm_sk<" in base or "k_gemm_fix<" in base:
+        role = base.rsplit(",", 1)[1].strip(" >")
+        return ROLES[role]
+    if "k_attn" in base:
+        return "attention_core"
+    if "k_rownorm" in base:
+        state["rownorm"] = state.get("rownorm", 0) + 1
+        return "rownorm_attn" if state["rownorm"] % 2 == 1 else "rownorm_mlp"
+    for k in ("k_score", "k_select", "k_layout", "k_compress", "k_decompress"):
+        if k + "<" in base or base.endswith(k):
+            return k[2:]
+    return None
+
+
+def primary(name):
+    """The first kernel of each kind's call (its dispatch count = the number of calls)."""
+    return "k_gemm_fix" not in name and "k_attn_fix" not in name
+
+
+def summarize(out):
+    factor = {}
+    for cnt in COUNTERS:
+        copy = load(out, cnt, "copy")
+        big = max(copy, key=lambda r: r[2])
+        factor[cnt] = big[2] * 1024.0 / (COPY_MIB << 20)   # counter KiB per byte actually moved
+    tot = collections.defaultdict(lambda: {"FETCH_SIZE": 0.0, "WRITE_SIZE": 0.0})
+    calls = collections.Counter()
+    for cnt in COUNTERS:
+        state = {}
+        for _, name, v in load(out, cnt, "bench"):
+            k = kind_of(name, state)
+            if k is None:
+                continue
+            tot[k][cnt] += v * 1024.0 / factor[cnt]
+            if cnt == "FETCH_SIZE" and primary(name):
+                calls[k] += 1
+    kernels = {}
+    for k, t in tot.items():
+        n = calls[k]
+        if not n or k not in SOURCES:
+            continue
+        srcs = SOURCES[k] + HDRS
+        kernels[k] = {"bytes_per_launch": round((t["FETCH_SIZE"] + t["WRITE_SIZE"]) / n),
+                      "fetch_bytes_per_launch": round(t["FETCH_SIZE"] / n),
+                      "write_bytes_per_launch": round(t["WRITE_SIZE"] / n),
+                      "launches_measured": n, "sources": srcs, "source_digest": source_digest(srcs)}
+    res = {"workload": "m1024", "calibration": {"copy_bytes": COPY_MIB << 20,
+                                                "fetch_counter_per_byte": factor["FETCH_SIZE"],
+                                                "write_counter_per_byte": factor["WRITE_SIZE"]},
+           "commands": commands(out), "kernels": kernels}
+    os.makedirs(os.path.join(ROOT, "profiles"), exist_ok=True)
+    with open(os.path.join(ROOT, "profiles", "traffic.json"), "w") as f:
+        json.dump(res, f, indent=1)
+    lines = ["# HBM traffic per call, m1024 workload (rocprofv3 FETCH_SIZE / WRITE_SIZE)", "",
+             "Counters calibrated on one %d MiB device copy: FETCH_SIZE reads %.3f, WRITE_SIZE %.3f "
+             "of the bytes the copy moves; every figure below is divided by that factor." %
+             (COPY_MIB, factor["FETCH_SIZE"], factor["WRITE_SIZE"]), "",
+             "Commands (then `python traffic.py summarize %s`):" % out, ""]
+    lines += ["    " + c for c in commands(out)]
+    lines += ["", "| kind | read MB | write MB | total MB |", "|---|---:|---:|---:|"]
+    for k, e in sorted(kernels.items(), key=lambda kv: -kv[1]["bytes_per_launch"]):
+        lines.append(f"| {k} | {e['fetch_bytes_per_launch'] / 1e6:.1f} | "
+                     f"{e['write_bytes_per_launch'] / 1e6:.1f} | {e['bytes_per_launch'] / 1e6:.1f} |")
+    with open(os.path.join(ROOT, "profiles", "traffic_m1024.md"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print(json.dumps({k: v["bytes_per_launch"] for k, v in kernels.items()}, indent=1))
+
+
+if __name__ == "__main__":
+    if len(sys.argv) != 3 or sys.argv[1] not in ("commands", "summarize"):
+        print(__doc__)
+        sys.exit(2)
+    if sys.argv[1] == "commands":
+        print("\n".join(commands(sys.argv[2])))
+    else:
+        summarize(sys.argv[2])
