@@ -8,7 +8,8 @@
 //   probabilities are already in the register layout of the second MFMA operand for
 //   O^T = V^T P^T.  The MFMA's k index may be permuted as long as both operands agree: the lane
 //   holding keys {4g..4g+3} and {16+4g..16+4g+3} of a 32-key step feeds exactly those keys of V^T,
-//   which sits transposed in LDS (written once per tile, read as two 8-byte pieces).  K lands in
+//   which sits transposed in LDS with each 32-key half stored in the order 0-3, 16-19, 4-7,
+//   20-23, ... so that those 8 keys are one 16-byte read (16-byte chunks XOR-swizzled per row).  K lands in
 //   LDS by direct global->LDS loads; only the last key tile carries the sequence-end mask; the
 //   output is rescaled only in steps where some row's running maximum grew.
 #include "common.h"
@@ -40,6 +41,16 @@ HILO_DEV int kswz(int r) {
   if constexpr (HD == 128) return r & 15;
   else return (r & 7) ^ ((r >> 3) & 1);
 }
+
+// Position of key k (0..63) in a V^T row: within each 32-key half, keys 4g..4g+3 and
+// 16+4g..16+4g+3 sit next to each other at 8g.
+HILO_DEV int vpos(int k) { return (k & ~31) + (((k & 15) >> 2) << 3) + (((k >> 4) & 1) << 2) + (k & 3); }
+
+// V^T row r (one head dimension, 64 keys = 8 chunks of 16 bytes) keeps logical position p at
+// chunk (p / 8) ^ vswz(r): the 16-byte fragment reads of 8 consecutive rows hit 8 distinct bank
+// groups, and the transposed writes (rows 8 apart) spread over the banks as well.
+HILO_DEV int vswz(int r) { return (r & 7) ^ ((r >> 3) & 7); }
+HILO_DEV int vaddr(int r, int p) { return r * 64 + ((((p >> 3) ^ vswz(r)) << 3) | (p & 7)); }
 
 HILO_DEV void g2lds16(const void *g, void *lds_wave_base) {
   __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void *)lds_wave_base, 16, 0, 0);
@@ -140,13 +151,13 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a) {
   constexpr int CPR = HD / 8;       // 16-byte chunks per K row
   constexpr int RPI = 64 / CPR;     // K rows per wave load instruction (1 KiB)
   constexpr int KI = BKV / RPI / NW;  // K load instructions per wave per tile
-  constexpr int VST = BKV + 4;      // V^T tile row stride (elements)
+  static_assert(BKV == 64, "the V^T swizzle assumes 64-key rows");
   constexpr int NT = NW * 64;
   constexpr int VGR = (BKV / 4) * (HD / 8);  // 4-key x 8-dim groups of a V tile
   constexpr int VC = (VGR + NT - 1) / NT;
   static_assert(KI * RPI * NW == BKV, "K tile / wave mismatch");
   __shared__ __attribute__((aligned(1024))) uint16_t sK[2][BKV * HD];
-  __shared__ __attribute__((aligned(16))) uint16_t sV[2][HD * VST];
+  __shared__ __attribute__((aligned(1024))) uint16_t sV[2][HD * BKV];
 
   const int P = gridDim.x;
   const int pid = xcd_remap(blockIdx.x, P);
@@ -228,7 +239,7 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a) {
             uint2 v2;
             v2.x = e0 | (e1 << 16);
             v2.y = e2 | (e3 << 16);
-            *reinterpret_cast<uint2 *>(&sV[buf][(b * 8 + j) * VST + 4 * g4]) = v2;
+            *reinterpret_cast<uint2 *>(&sV[buf][vaddr(b * 8 + j, vpos(4 * g4))]) = v2;
           }
         }
       }
@@ -314,12 +325,8 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a) {
       for (int d = 0; d < DS; ++d) {
 #pragma unroll
         for (int kk2 = 0; kk2 < 2; ++kk2) {
-          const uint16_t *vr = &sV[buf][(d * 16 + lr) * VST + 32 * kk2 + 4 * lg];
-          const uint2 v0 = *reinterpret_cast<const uint2 *>(vr);
-          const uint2 v1 = *reinterpret_cast<const uint2 *>(vr + 16);
-          uint4 vv;
-          vv.x = v0.x; vv.y = v0.y; vv.z = v1.x; vv.w = v1.y;
-          const bf16x8 vf = __builtin_bit_cast(bf16x8, vv);
+          const bf16x8 vf =
+              *reinterpret_cast<const bf16x8 *>(&sV[buf][vaddr(d * 16 + lr, 32 * kk2 + 8 * lg)]);
 #pragma unroll
           for (int qs = 0; qs < QS; ++qs)
             o[qs][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[qs][kk2], o[qs][d], 0, 0, 0);
