@@ -3,9 +3,11 @@
 // weights, tiles never straddling a segment.  Epilogues fuse the bias, the tanh-GELU, and the
 // gated residual update of the float32 stream z.
 //
-// bf16 path: gfx950 MFMA v_mfma_f32_16x16x32_bf16, fp32 accumulation in VGPRs; 256 x 256 tiles
-// on 8 waves, K steps of 64 through a double-buffered LDS ring filled by direct global->LDS loads,
-// one persistent workgroup per CU running whole data-parallel waves, then a stream-K remainder.
+// bf16 path: gfx950 MFMA v_mfma_f32_16x16x32_bf16, fp32 accumulation in VGPRs; 128 x 128 tiles
+// on 4 waves, K steps of 64 through a double-buffered LDS ring (64 KiB) filled by direct
+// global->LDS loads; two persistent workgroups per CU (their barriers are independent, so one
+// computes while the other waits for its loads) run whole data-parallel waves, then a stream-K
+// remainder.
 //
 // The MFMA is issued with the weight fragment as its first operand, so each lane's 4
 // accumulators are 4 consecutive output columns of one row (contiguous epilogue stores).
@@ -147,8 +149,8 @@ HILO_DEV TileRows decode_row_tile(const GemmProblem &p, int BM, int r) {
 // K piece of one output tile: tiles are cut into s pieces when there are fewer tiles than
 // workgroups (s = ceil(P / tiles), at most one K step per piece), else s = 1.  Units are ordered
 // piece-major, row tile fastest within a piece.  The first floor(U / P) * P units run
-// data-parallel in whole waves -- the 32 workgroups of an XCD then work on 32 neighbouring tiles
-// at the same K step, so its L2 serves each weight and activation slice to all of them.  The
+// data-parallel in whole waves -- the workgroups of an XCD then work on neighbouring tiles at the
+// same K step, so its L2 serves each weight and activation slice to all of them.  The
 // remaining units (all of the same K length) are spread evenly over the P workgroups stream-K,
 // so no CU idles through a partial last wave.  A unit not finished in one place leaves an fp32
 // partial tile (data-parallel unit u: slot u; stream-K range of workgroup w: slots P + 2w for its
@@ -221,15 +223,69 @@ struct SkTile {
     return ((size_t(wid) * TM * TN + i * TN + j) * 64 + lane) * 4;
   }
 
-  // Epilogue of the accumulator fragment (i, j) of wave wid: 4 consecutive columns of one row.
-  template <int EPI>
-  HILO_DEV static void frag(const GemmProblem &p, const TileRows &tr, int n0, int wid, int i, int j,
-                            int lane, const f32x4 &a) {
-    const int rl = (wid / WN) * (BM / WM) + i * 16 + (lane & 15);
-    const int n = n0 + (wid % WN) * (BN / WN) + j * 16 + 4 * (lane >> 4);
-    if (rl >= tr.nrows || n >= p.N) return;
-    float a4[4] = {a[0], a[1], a[2], a[3]};
-    epilogue4<EPI, true>(p, tr, tr.row0 + rl, n, a4);
+  // Epilogue of fragment rows i0 .. i0 + ROWS - 1 of wave wid (each fragment: 4 consecutive
+  // columns of one row).  Every load the epilogue needs (bias, gate, the old z) is issued before
+  // the first store: the compiler cannot prove that the outputs do not alias the inputs, so an
+  // interleaved order would serialise one memory round trip per fragment.  Loads use indices
+  // clamped into the tile; values for rows or columns outside it are never stored.
+  template <int EPI, int ROWS>
+  HILO_DEV static void epilogue_rows(const GemmProblem &p, const TileRows &tr, int n0, int wid, int i0,
+                                     int lane, const f32x4 (&acc)[ROWS][TN]) {
+    const int rbase = (wid / WN) * (BM / WM) + i0 * 16 + (lane & 15);
+    const int cbase = n0 + (wid % WN) * (BN / WN) + 4 * (lane >> 4);
+    const uint16_t *bias = reinterpret_cast<const uint16_t *>(p.bias[tr.sigma]);
+    float bv[TN][4];
+    float4 gt[TN];
+    float4 zv[ROWS][TN];
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const int nc = min(cbase + j * 16, p.N - 4);
+      const uint2 bu = *reinterpret_cast<const uint2 *>(bias + nc);
+      bv[j][0] = __uint_as_float(bu.x << 16); bv[j][1] = __uint_as_float(bu.x & 0xffff0000u);
+      bv[j][2] = __uint_as_float(bu.y << 16); bv[j][3] = __uint_as_float(bu.y & 0xffff0000u);
+      if constexpr (EPI == EPI_RESID)
+        gt[j] = *reinterpret_cast<const float4 *>(p.mod + (size_t(tr.s * 2 + tr.sigma) * 6 + p.gate_idx) * p.D + nc);
+    }
+    if constexpr (EPI == EPI_RESID) {
+#pragma unroll
+      for (int i = 0; i < ROWS; ++i) {
+        const size_t m = size_t(tr.row0 + min(rbase + i * 16, tr.nrows - 1));
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          zv[i][j] = *reinterpret_cast<const float4 *>(p.z + m * p.ldz + min(cbase + j * 16, p.N - 4));
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < ROWS; ++i) {
+      const int rl = rbase + i * 16;
+      if (rl >= tr.nrows) continue;
+      const size_t m = size_t(tr.row0 + rl);
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const int n = cbase + j * 16;
+        if (n >= p.N) continue;
+        float v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = acc[i][j][e] + bv[j][e];
+        if constexpr (EPI == EPI_RESID) {
+          float4 zn = zv[i][j];
+          zn.x += gt[j].x * v[0];
+          zn.y += gt[j].y * v[1];
+          zn.z += gt[j].z * v[2];
+          zn.w += gt[j].w * v[3];
+          *reinterpret_cast<float4 *>(p.z + m * p.ldz + n) = zn;
+        } else {
+          if constexpr (EPI == EPI_GELU) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[e] = gelu_tanh(v[e]);
+          }
+          uint2 u;
+          u.x = pack_bf16x2(v[0], v[1]);
+          u.y = pack_bf16x2(v[2], v[3]);
+          *reinterpret_cast<uint2 *>(reinterpret_cast<uint16_t *>(p.out) + m * p.ldo + n) = u;
+        }
+      }
+    }
   }
 };
 
@@ -255,15 +311,22 @@ __global__ __launch_bounds__(WM *WN * 64) void k_gemm_sk(GemmProblem p) {
 
   int u = pid;            // next data-parallel unit of this workgroup
   long long it = rg.beg;  // next stream-K iteration of this workgroup
-  while (true) {
+
+  // work items: (tile, K steps [kb, ke), partial slot or null for a tile finished here)
+  struct Item {
     int t, kb, ke;
-    float *slot;          // null: the tile is complete here, run the epilogue
+    float *slot;
+    bool valid;
+  };
+  auto next_item = [&]() {
+    Item x{0, 0, 0, nullptr, false};
     if (u < q.dp) {
       const int pc = u / q.T;
-      t = u - pc * q.T;
-      kb = piece_k0(q, pc);
-      ke = piece_k0(q, pc + 1);
-      slot = q.s == 1 ? nullptr : p.part + size_t(u) * T::kPartFloats;
+      x.t = u - pc * q.T;
+      x.kb = piece_k0(q, pc);
+      x.ke = piece_k0(q, pc + 1);
+      x.slot = q.s == 1 ? nullptr : p.part + size_t(u) * T::kPartFloats;
+      x.valid = true;
       u += P;
     } else if (it < rg.end) {
       const long long v = it / q.len;
@@ -271,41 +334,60 @@ __global__ __launch_bounds__(WM *WN * 64) void k_gemm_sk(GemmProblem p) {
       const int k1 = int(min((long long)q.len, k0 + (rg.end - it)));
       const int uu = q.dp + int(v);
       const int pc = uu / q.T;
-      t = uu - pc * q.T;
-      kb = piece_k0(q, pc) + k0;
-      ke = piece_k0(q, pc) + k1;
+      x.t = uu - pc * q.T;
+      x.kb = piece_k0(q, pc) + k0;
+      x.ke = piece_k0(q, pc) + k1;
       const bool whole = q.s == 1 && k0 == 0 && k1 == q.len;
-      slot = whole ? nullptr
-                   : p.part + (size_t(P) + size_t(pid) * 2 + (it == rg.beg ? 0 : 1)) * T::kPartFloats;
+      x.slot = whole ? nullptr
+                     : p.part + (size_t(P) + size_t(pid) * 2 + (it == rg.beg ? 0 : 1)) * T::kPartFloats;
+      x.valid = true;
       it += k1 - k0;
-    } else {
-      break;
     }
+    return x;
+  };
+  // a tile's rows and this lane's load sources: row (wave band + 8 i + lane / 8), chunk
+  // (lane % 8) ^ swz(row); rows past the tile edge re-read the last valid row (never stored)
+  struct Src {
+    TileRows tr;
+    int n0;
+    const uint16_t *a[IA];
+    const uint16_t *b[IB];
+  };
+  auto make_src = [&](int t) {
+    Src x;
     const int tn = t / q.R;
-    const TileRows tr = decode_row_tile(p, BM, t - tn * q.R);
-    const int n0 = tn * BN;
-    const uint16_t *Wt = reinterpret_cast<const uint16_t *>(p.W[tr.sigma]);
-
-    // this lane's load sources: row (wave band + 8 i + lane / 8), chunk (lane % 8) ^ swz(row);
-    // rows past the tile edge re-read the last valid row (their results are never stored)
-    const uint16_t *srcA[IA];
-    const uint16_t *srcB[IB];
+    x.tr = decode_row_tile(p, BM, t - tn * q.R);
+    x.n0 = tn * BN;
+    const uint16_t *Wt = reinterpret_cast<const uint16_t *>(p.W[x.tr.sigma]);
 #pragma unroll
     for (int i = 0; i < IA; ++i) {
       const int r = wid * (BM / NW) + 8 * i + lrow;
-      srcA[i] = A + size_t(tr.row0 + min(r, tr.nrows - 1)) * p.lda + ((lslot ^ swz<BK>(r)) * 8);
+      x.a[i] = A + size_t(x.tr.row0 + min(r, x.tr.nrows - 1)) * p.lda + ((lslot ^ swz<BK>(r)) * 8);
     }
 #pragma unroll
     for (int i = 0; i < IB; ++i) {
       const int r = wid * (BN / NW) + 8 * i + lrow;
-      srcB[i] = Wt + size_t(min(n0 + r, p.N - 1)) * p.K + ((lslot ^ swz<BK>(r)) * 8);
+      x.b[i] = Wt + size_t(min(x.n0 + r, p.N - 1)) * p.K + ((lslot ^ swz<BK>(r)) * 8);
     }
-    auto issue = [&](int k0, int buf) {
+    return x;
+  };
+  auto issue = [&](const Src &x, int k0, int buf) {
 #pragma unroll
-      for (int i = 0; i < IA; ++i) g2lds16(srcA[i] + k0, &sA[buf][(wid * (BM / NW) + 8 * i) * BK]);
+    for (int i = 0; i < IA; ++i) g2lds16(x.a[i] + k0, &sA[buf][(wid * (BM / NW) + 8 * i) * BK]);
 #pragma unroll
-      for (int i = 0; i < IB; ++i) g2lds16(srcB[i] + k0, &sB[buf][(wid * (BN / NW) + 8 * i) * BK]);
-    };
+    for (int i = 0; i < IB; ++i) g2lds16(x.b[i] + k0, &sB[buf][(wid * (BN / NW) + 8 * i) * BK]);
+  };
+
+  Item cur = next_item();
+  if (!cur.valid) return;
+  Src sc = make_src(cur.t);
+  issue(sc, cur.kb * BK, 0);
+  int buf = 0;  // the LDS ring alternates over the steps of all of this workgroup's items
+  while (true) {
+    // the next item is known before this one's last step: its first loads go out then, so they
+    // overlap this item's epilogue instead of starting an empty pipeline after it
+    const Item nxt = next_item();
+    const Src sn = make_src(nxt.valid ? nxt.t : cur.t);
 
     f32x4 acc[TM][TN];
 #pragma unroll
@@ -313,9 +395,10 @@ __global__ __launch_bounds__(WM *WN * 64) void k_gemm_sk(GemmProblem p) {
 #pragma unroll
       for (int j = 0; j < TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    issue(kb * BK, 0);
-    for (int kt = kb; kt < ke; ++kt) {
-      const int buf = (kt - kb) & 1;
+    // one K step: wait for this step's tile, then read fragments and multiply; `next` issues the
+    // following step's loads right after the fragment reads (the LDS then serves the reads first
+    // and the MFMAs start sooner after the barrier)
+    auto step = [&](auto &&next) {
       wait_vmem_le<0>();
       __syncthreads();
 #pragma unroll
@@ -332,41 +415,39 @@ __global__ __launch_bounds__(WM *WN * 64) void k_gemm_sk(GemmProblem p) {
           const int r = wcol + j * 16 + lr;
           fb[j] = *reinterpret_cast<const bf16x8 *>(&sB[buf][r * BK + ((ch ^ swz<BK>(r)) * 8)]);
         }
-        // the next step's loads go out only after this step's fragment reads are issued: the
-        // LDS then serves the reads first and the MFMAs start sooner after the barrier
-        if (ks == BK / 32 - 1 && kt + 1 < ke) issue((kt + 1) * BK, buf ^ 1);
+        if (ks == BK / 32 - 1) next();
 #pragma unroll
         for (int i = 0; i < TM; ++i)
 #pragma unroll
           for (int j = 0; j < TN; ++j)
             acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fb[j], fa[i], acc[i][j], 0, 0, 0);
-        // alternate single MFMAs and LDS reads while the reads last
-#pragma unroll
-        for (int g = 0; g < TM + TN; ++g) {
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
-          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
-        }
       }
-    }
+      buf ^= 1;
+    };
+    // all steps but the last issue their successor unconditionally: no branch inside the loop
+    // body, so the scheduler overlaps each half-step's fragment reads with the previous MFMAs
+    for (int kt = cur.kb; kt < cur.ke - 1; ++kt) step([&] { issue(sc, (kt + 1) * BK, buf ^ 1); });
+    step([&] {
+      if (nxt.valid) issue(sn, nxt.kb * BK, buf ^ 1);
+    });
 
-    if (slot == nullptr) {
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j) T::template frag<EPI>(p, tr, n0, wid, i, j, lane, acc[i][j]);
+    if (cur.slot == nullptr) {
+      T::template epilogue_rows<EPI, TM>(p, sc.tr, sc.n0, wid, 0, lane, acc);
     } else {
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j)
-          *reinterpret_cast<f32x4 *>(slot + T::part_index(wid, i, j, lane)) = acc[i][j];
+          *reinterpret_cast<f32x4 *>(cur.slot + T::part_index(wid, i, j, lane)) = acc[i][j];
     }
-    __syncthreads();  // the next unit's loads reuse the LDS ring
+    if (!nxt.valid) break;
+    cur = nxt;
+    sc = sn;
   }
 }
 
 // Finishes every tile left in partials: (tile, main-kernel wave) work items, 4 waves per
-// workgroup, each wave summing two rows of fragments of that main-kernel wave over the tile's
+// workgroup, each wave summing TM / 4 rows of fragments of that main-kernel wave over the tile's
 // partials (pieces in K order, stream-K contributors in workgroup order), then running the
 // epilogue on them.
 constexpr int kFixThreads = 256;
@@ -422,11 +503,7 @@ __global__ __launch_bounds__(kFixThreads) void k_gemm_fix(GemmProblem p, int P) 
     if (done_whole) continue;
     const int tn = t / q.R;
     const TileRows tr = decode_row_tile(p, BM, t - tn * q.R);
-#pragma unroll
-    for (int i = 0; i < IPW; ++i)
-#pragma unroll
-      for (int j = 0; j < TN; ++j)
-        T::template frag<EPI>(p, tr, tn * BN, wid, fw * IPW + i, j, lane, acc[i][j]);
+    T::template epilogue_rows<EPI, IPW>(p, tr, tn * BN, wid, fw * IPW, lane, acc);
   }
 }
 
@@ -481,6 +558,7 @@ __global__ __launch_bounds__(256) void k_gemm_f32(GemmProblem p, int imgTiles, i
 
 // ------------------------------------------------------------------------------- dispatch
 
+// Persistent workgroups of the bf16 GEMM: two per CU.
 int sk_workgroups() {
   static int ncu[64] = {0};
   int dev = 0;
@@ -488,10 +566,10 @@ int sk_workgroups() {
   if (ncu[dev] == 0) {
     int n = 0;
     if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
-      n = kSkMaxWorkgroups;
+      n = kSkMaxWorkgroups / 2;
     ncu[dev] = n;
   }
-  return ncu[dev] < kSkMaxWorkgroups ? ncu[dev] : kSkMaxWorkgroups;
+  return 2 * ncu[dev] < kSkMaxWorkgroups ? 2 * ncu[dev] : kSkMaxWorkgroups;
 }
 
 template <int BM, int BN, int WM, int WN, int ROLE>
@@ -533,10 +611,10 @@ hipError_t launch_gemm(bool bf16, int role, const GemmProblem &p, hipStream_t st
     }
   }
   switch (role) {
-    case GEMM_QKV: return run_bf16<256, 256, 2, 4, GEMM_QKV>(p, st);
-    case GEMM_O: return run_bf16<256, 256, 2, 4, GEMM_O>(p, st);
-    case GEMM_FC1: return run_bf16<256, 256, 2, 4, GEMM_FC1>(p, st);
-    default: return run_bf16<256, 256, 2, 4, GEMM_FC2>(p, st);
+    case GEMM_QKV: return run_bf16<128, 128, 2, 2, GEMM_QKV>(p, st);
+    case GEMM_O: return run_bf16<128, 128, 2, 2, GEMM_O>(p, st);
+    case GEMM_FC1: return run_bf16<128, 128, 2, 2, GEMM_FC1>(p, st);
+    default: return run_bf16<128, 128, 2, 2, GEMM_FC2>(p, st);
   }
 }
 

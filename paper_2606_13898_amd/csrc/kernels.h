@@ -56,9 +56,9 @@ struct GemmProblem {
 };
 
 // Partial-sum area of the bf16 GEMMs (part of the caller's workspace): one slot per data-parallel
-// unit of a split wave plus two per workgroup for its stream-K range.
-constexpr int kSkMaxWorkgroups = 256;
-constexpr size_t kSkPartFloats = size_t(256) * 256;  // one 256 x 256 fp32 tile per slot
+// unit of a split wave plus two per workgroup for its stream-K range; two workgroups per CU.
+constexpr int kSkMaxWorkgroups = 512;
+constexpr size_t kSkPartFloats = size_t(128) * 128;  // one 128 x 128 fp32 tile per slot
 constexpr size_t kSkPartBytes = size_t(kSkMaxWorkgroups) * 3 * kSkPartFloats * sizeof(float);
 hipError_t launch_gemm(bool bf16, int role, const GemmProblem &p, hipStream_t st);
 
