@@ -400,11 +400,22 @@ __global__ __launch_bounds__(NW * 64) void k_attn_fix(AttnArgs a) {
 #pragma unroll
     for (int d = 0; d < DS; ++d) o[qs][d] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
+  // contributor ranges [b, e) in order; their starts floor(I q / P) advance by additions
+  const long long qI = I / P, rI = I - qI * P;
+  long long b = beg, r = I * pid - beg * P;
   for (int q = pid; q < P; ++q) {
-    const long long bq = I * q / P, eq = I * (q + 1) / P;
+    long long e = b + qI, rn = r + rI;
+    if (rn >= P) {
+      ++e;
+      rn -= P;
+    }
+    const long long bq = b, eq = e;
+    b = e;
+    r = rn;
     if (bq >= eq) continue;
     if (bq >= ue) break;
-    const float *slot = a.part + (size_t(q) * 2 + (bq > u.start ? 0 : (bq == u.start ? 0 : 1))) * S::kSlotFloats;
+    // slot 0 holds the partial of the range's first unit, slot 1 of its last
+    const float *slot = a.part + (size_t(q) * 2 + (bq >= u.start ? 0 : 1)) * S::kSlotFloats;
 #pragma unroll
     for (int qs = 0; qs < QS; ++qs) {
       const float2 ml = *reinterpret_cast<const float2 *>(slot + S::ml_index(wid, qs, lane));

@@ -494,10 +494,20 @@ __global__ __launch_bounds__(kFixThreads) void k_gemm_fix(GemmProblem p, int P) 
         done_whole = true;
         break;
       }
+      // contributors in workgroup order.  Range starts floor(I w / P) advance by additions (no
+      // 64-bit division per contributor); a range's first unit is v exactly when it starts at or
+      // after unit v's first iteration.
+      const long long qI = q.I / P, rI = q.I - qI * P;
+      long long qb = q.I * w0 / P, rb = q.I * w0 - qb * P;
       for (int w = w0; w <= w1; ++w) {
-        const SkRange rw = sk_range(q.I, P, w);
-        if (rw.beg >= rw.end) continue;
-        add(p.part + (size_t(P) + size_t(w) * 2 + (rw.beg / q.len == v ? 0 : 1)) * T::kPartFloats);
+        long long qn = qb + qI, rn = rb + rI;
+        if (rn >= P) {
+          ++qn;
+          rn -= P;
+        }
+        if (qb < qn) add(p.part + (size_t(P) + size_t(w) * 2 + (qb >= a0 ? 0 : 1)) * T::kPartFloats);
+        qb = qn;
+        rb = rn;
       }
     }
     if (done_whole) continue;
