@@ -254,8 +254,8 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a) {
 #pragma unroll
     for (int qs = 0; qs < QS; ++qs) { mrun[qs] = -INFINITY; lrun[qs] = 0.f; }
 
-    // one 64-key step; keys >= n (only in the unit's last step) are masked under a uniform branch
-    auto step = [&](int buf, int kv0, auto &&after_scores) {
+    // one 64-key step; keys >= n exist only in a unit's last step, the only one that masks
+    auto step = [&](int buf, int kv0, bool mask, auto &&after_scores) {
       // S^T for 64 keys x QW queries: sc[ks][qs][e] = score(query qs*16+lr, key ks*16+4*lg+e)
       f32x4 sc[4][QS];
 #pragma unroll
@@ -276,7 +276,7 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a) {
         }
       }
       after_scores();
-      if (kv0 + BKV > n) {
+      if (mask) {
 #pragma unroll
         for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
@@ -339,22 +339,21 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a) {
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     store_v(0);
     __syncthreads();
-    for (int kt = kb; kt < ke; ++kt) {
+    // all steps but the last load the next tile unconditionally (issued once this step's K
+    // fragments are read) and never mask: no branch splits the loop body's schedule
+    for (int kt = kb; kt < ke - 1; ++kt) {
       const int buf = (kt - kb) & 1;
       const int kv0 = kt * BKV;
-      // the next tile's loads go out once this step's K fragments have been read
-      step(buf, kv0, [&]() {
-        if (kt + 1 < ke) {
-          issue_k(kv0 + BKV, buf ^ 1);
-          load_v(kv0 + BKV);
-        }
+      step(buf, kv0, false, [&]() {
+        issue_k(kv0 + BKV, buf ^ 1);
+        load_v(kv0 + BKV);
       });
-      if (kt + 1 < ke) {
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-        store_v(buf ^ 1);
-      }
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      store_v(buf ^ 1);
       __syncthreads();
     }
+    step((ke - 1 - kb) & 1, (ke - 1) * BKV, (ke - 1) * BKV + BKV > n, [] {});
+    __syncthreads();
 
     float lsum[QS];
 #pragma unroll
