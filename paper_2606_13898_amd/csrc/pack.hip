@@ -9,7 +9,8 @@
 namespace hilo {
 
 constexpr int kPackThreads = 256;
-constexpr int kPackRows = 4;  // row slots per workgroup
+constexpr int kPackRows = 4;  // row slots per workgroup, one wave each
+static_assert(kPackThreads == 64 * kPackRows, "one wave per row slot");
 
 template <bool BF16>
 HILO_DEV void load8(const void *base, size_t elem, float *f) {
@@ -46,6 +47,8 @@ HILO_DEV void store8_f32(float *z, size_t elem, const float *f) {
 }
 
 // Row slots: [0, G*N) are image rows (grid g, compressed row k = slot % N), then B*L text rows.
+// One wave per row slot (kPackRows per workgroup): the rows of a workgroup proceed in parallel
+// and each lane issues all of its loads for the row before the stores.
 template <bool BF16>
 __global__ __launch_bounds__(kPackThreads) void k_compress(
     const void *__restrict__ x_img, const void *__restrict__ x_txt, const int *__restrict__ fine_idx,
@@ -54,46 +57,53 @@ __global__ __launch_bounds__(kPackThreads) void k_compress(
     long long nslots) {
 #pragma clang fp contract(off)
   const int CGn = D / 8;
+  const int lane = threadIdx.x & 63;
   const long long imgSlots = (long long)G * N;
-  for (int rr = 0; rr < kPackRows; ++rr) {
-    const long long slot = (long long)blockIdx.x * kPackRows + rr;
-    if (slot >= nslots) return;
-    size_t dst, s0, s1 = 0, s2 = 0, s3 = 0;
-    bool pooled = false;
-    const void *src = x_img;
-    if (slot < imgSlots) {
-      const int g = int(slot / N), k = int(slot % N);
-      const int nf = counts[2 * g], np = counts[2 * g + 1];
-      if (k >= nf + np) continue;
-      dst = size_t(seg[g] + k);
-      if (k < nf) {
-        s0 = size_t(g) * N + fine_idx[size_t(g) * N + k];
-      } else {
-        const int b = pool_idx[size_t(g) * (N / 4) + (k - nf)];
-        const int W2 = W / 2;
-        const size_t p00 = size_t(g) * N + size_t(b / W2) * 2 * W + size_t(b % W2) * 2;
-        s0 = p00; s1 = p00 + 1; s2 = p00 + W; s3 = p00 + W + 1;
-        pooled = true;
-      }
+  const long long slot = (long long)blockIdx.x * kPackRows + (threadIdx.x >> 6);
+  if (slot >= nslots) return;
+  size_t dst, s0, s1 = 0, s2 = 0, s3 = 0;
+  bool pooled = false;
+  const void *src = x_img;
+  if (slot < imgSlots) {
+    const int g = int(slot / N), k = int(slot % N);
+    const int nf = counts[2 * g], np = counts[2 * g + 1];
+    if (k >= nf + np) return;
+    dst = size_t(seg[g] + k);
+    if (k < nf) {
+      s0 = size_t(g) * N + fine_idx[size_t(g) * N + k];
     } else {
-      const long long t = slot - imgSlots;
-      const int s = int(t / L), j = int(t % L);
-      dst = size_t(cu[s + 1] - L + j);
-      s0 = size_t(s) * L + j;
-      src = x_txt;
+      const int b = pool_idx[size_t(g) * (N / 4) + (k - nf)];
+      const int W2 = W / 2;
+      const size_t p00 = size_t(g) * N + size_t(b / W2) * 2 * W + size_t(b % W2) * 2;
+      s0 = p00; s1 = p00 + 1; s2 = p00 + W; s3 = p00 + W + 1;
+      pooled = true;
     }
-    for (int cg = threadIdx.x; cg < CGn; cg += kPackThreads) {
+  } else {
+    const long long t = slot - imgSlots;
+    const int s = int(t / L), j = int(t % L);
+    dst = size_t(cu[s + 1] - L + j);
+    s0 = size_t(s) * L + j;
+    src = x_txt;
+  }
+  if (pooled) {
+#pragma unroll 2
+    for (int cg = lane; cg < CGn; cg += 64) {
+      const size_t c = size_t(cg) * 8;
+      float a[8], b[8], e[8], f[8];
+      load8<BF16>(src, s0 * D + c, a);
+      load8<BF16>(src, s1 * D + c, b);
+      load8<BF16>(src, s2 * D + c, e);
+      load8<BF16>(src, s3 * D + c, f);
+#pragma unroll
+      for (int v = 0; v < 8; ++v) a[v] = ((a[v] + b[v]) + (e[v] + f[v])) * 0.25f;
+      store8_f32(z, dst * D + c, a);
+    }
+  } else {
+#pragma unroll 4
+    for (int cg = lane; cg < CGn; cg += 64) {
       const size_t c = size_t(cg) * 8;
       float a[8];
       load8<BF16>(src, s0 * D + c, a);
-      if (pooled) {
-        float b[8], e[8], f[8];
-        load8<BF16>(src, s1 * D + c, b);
-        load8<BF16>(src, s2 * D + c, e);
-        load8<BF16>(src, s3 * D + c, f);
-#pragma unroll
-        for (int v = 0; v < 8; ++v) a[v] = ((a[v] + b[v]) + (e[v] + f[v])) * 0.25f;
-      }
       store8_f32(z, dst * D + c, a);
     }
   }
@@ -115,39 +125,39 @@ hipError_t launch_compress(bool bf16, const void *x_img, const void *x_txt, cons
   return hipGetLastError();
 }
 
-// Output row slots: [0, G*N) image patches, then B*L text rows.
+// Output row slots: [0, G*N) image patches, then B*L text rows; one wave per row slot.
 template <bool BF16>
 __global__ __launch_bounds__(kPackThreads) void k_decompress(
     const float *__restrict__ z, const int *__restrict__ idx_map, const int *__restrict__ cu,
     const int *__restrict__ seg, void *__restrict__ y_img, void *__restrict__ y_txt, int G, int N,
     int D, int L, long long nslots) {
   const int CGn = D / 8;
+  const int lane = threadIdx.x & 63;
   const long long imgSlots = (long long)G * N;
-  for (int rr = 0; rr < kPackRows; ++rr) {
-    const long long slot = (long long)blockIdx.x * kPackRows + rr;
-    if (slot >= nslots) return;
-    size_t src, dst;
-    void *out;
-    if (slot < imgSlots) {
-      const int g = int(slot / N);
-      src = size_t(seg[g]) + size_t(idx_map[slot]);
-      dst = size_t(slot);
-      out = y_img;
-    } else {
-      if (!y_txt) return;
-      const long long t = slot - imgSlots;
-      const int s = int(t / L), j = int(t % L);
-      src = size_t(cu[s + 1] - L + j);
-      dst = size_t(t);
-      out = y_txt;
-    }
-    for (int cg = threadIdx.x; cg < CGn; cg += kPackThreads) {
-      const size_t c = size_t(cg) * 8;
-      const float4 *p = reinterpret_cast<const float4 *>(z + src * D + c);
-      float4 a = p[0], b = p[1];
-      float f[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
-      store8<BF16>(out, dst * D + c, f);
-    }
+  const long long slot = (long long)blockIdx.x * kPackRows + (threadIdx.x >> 6);
+  if (slot >= nslots) return;
+  size_t src, dst;
+  void *out;
+  if (slot < imgSlots) {
+    const int g = int(slot / N);
+    src = size_t(seg[g]) + size_t(idx_map[slot]);
+    dst = size_t(slot);
+    out = y_img;
+  } else {
+    if (!y_txt) return;
+    const long long t = slot - imgSlots;
+    const int s = int(t / L), j = int(t % L);
+    src = size_t(cu[s + 1] - L + j);
+    dst = size_t(t);
+    out = y_txt;
+  }
+#pragma unroll 4
+  for (int cg = lane; cg < CGn; cg += 64) {
+    const size_t c = size_t(cg) * 8;
+    const float4 *p = reinterpret_cast<const float4 *>(z + src * D + c);
+    const float4 a = p[0], b = p[1];
+    float f[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+    store8<BF16>(out, dst * D + c, f);
   }
 }
 
