@@ -7,11 +7,11 @@
 //   row's scores (4 keys per 16-key subtile): the running max / sum stay lane-local, and the
 //   probabilities are already in the register layout of the second MFMA operand for
 //   O^T = V^T P^T.  The MFMA's k index may be permuted as long as both operands agree: the lane
-//   holding keys {4g..4g+3} and {16+4g..16+4g+3} of a 32-key step feeds exactly those keys of V^T,
-//   which sits transposed in LDS with each 32-key half stored in the order 0-3, 16-19, 4-7,
-//   20-23, ... so that those 8 keys are one 16-byte read (16-byte chunks XOR-swizzled per row).  K lands in
-//   LDS by direct global->LDS loads; only the last key tile carries the sequence-end mask; the
-//   output is rescaled only in steps where some row's running maximum grew.
+//   holding keys {4g..4g+3} and {16+4g..16+4g+3} of a 32-key step feeds exactly those keys of V^T.
+//   K and V both land in LDS in their natural [key][dim] layout by direct global->LDS loads; the
+//   V^T fragments come out of gfx950's transposing LDS read (ds_read_b64_tr_b16), two per
+//   fragment.  Only the last key tile carries the sequence-end mask; the output is rescaled only
+//   in steps where some row's running maximum grew.
 #include "common.h"
 #include "kernels.h"
 
@@ -42,15 +42,24 @@ HILO_DEV int kswz(int r) {
   else return (r & 7) ^ ((r >> 3) & 1);
 }
 
-// Position of key k (0..63) in a V^T row: within each 32-key half, keys 4g..4g+3 and
-// 16+4g..16+4g+3 sit next to each other at 8g.
-HILO_DEV int vpos(int k) { return (k & ~31) + (((k & 15) >> 2) << 3) + (((k >> 4) & 1) << 2) + (k & 3); }
+// V tile rows (head_dim bf16, [key][dim]) keep 16-byte chunk c of row r at slot c ^ vsw(r).  A
+// transposing fragment read has the 16 lanes of a group read 8 bytes each from 4 consecutive rows
+// (a multiple of 4 apart from the group's first) and 2 neighbouring chunks: 2 (r & 3) gives those
+// 8 (row, chunk) pairs distinct slots, and 8 ((r >> 2) & 1) moves the next group (the next 4
+// rows) to the other half of a 256-byte row.
+template <int HD>
+HILO_DEV int vsw(int r) {
+  if constexpr (HD == 128) return (2 * (r & 3)) ^ (8 * ((r >> 2) & 1));
+  else return 2 * (r & 3);
+}
 
-// V^T row r (one head dimension, 64 keys = 8 chunks of 16 bytes) keeps logical position p at
-// chunk (p / 8) ^ vswz(r): the 16-byte fragment reads of 8 consecutive rows hit 8 distinct bank
-// groups, and the transposed writes (rows 8 apart) spread over the banks as well.
-HILO_DEV int vswz(int r) { return (r & 7) ^ ((r >> 3) & 7); }
-HILO_DEV int vaddr(int r, int p) { return r * 64 + ((((p >> 3) ^ vswz(r)) << 3) | (p & 7)); }
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+
+// Transposing LDS read: within each group of 16 lanes, lane i receives element i % 4 of the
+// 8-byte words read by lanes 4m + i / 4 (m = 0..3) of its group.
+HILO_DEV bf16x4 lds_read_tr16(const uint16_t *lds) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4bf16((__attribute__((address_space(3))) bf16x4 *)lds);
+}
 
 HILO_DEV void g2lds16(const void *g, void *lds_wave_base) {
   __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void *)lds_wave_base, 16, 0, 0);
@@ -151,13 +160,9 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a) {
   constexpr int CPR = HD / 8;       // 16-byte chunks per K row
   constexpr int RPI = 64 / CPR;     // K rows per wave load instruction (1 KiB)
   constexpr int KI = BKV / RPI / NW;  // K load instructions per wave per tile
-  static_assert(BKV == 64, "the V^T swizzle assumes 64-key rows");
-  constexpr int NT = NW * 64;
-  constexpr int VGR = (BKV / 4) * (HD / 8);  // 4-key x 8-dim groups of a V tile
-  constexpr int VC = (VGR + NT - 1) / NT;
   static_assert(KI * RPI * NW == BKV, "K tile / wave mismatch");
   __shared__ __attribute__((aligned(1024))) uint16_t sK[2][BKV * HD];
-  __shared__ __attribute__((aligned(1024))) uint16_t sV[2][HD * BKV];
+  __shared__ __attribute__((aligned(1024))) uint16_t sV[2][BKV * HD];
 
   const int P = gridDim.x;
   const int pid = xcd_remap(blockIdx.x, P);
@@ -202,46 +207,14 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a) {
                 &sK[buf][(wid * KI + i) * RPI * HD]);
       }
     };
-    // V: staged through registers and written transposed (4 keys x 8 dims per group)
-    uint4 rv[VC][4];
-    auto load_v = [&](int kv0) {
+    // V: direct global->LDS in the same pattern, chunks placed by vsw
+    auto issue_v = [&](int kv0, int buf) {
 #pragma unroll
-      for (int c = 0; c < VC; ++c) {
-        const int gidx = tid + c * NT;
-        if (gidx < VGR) {
-          const int b = gidx % (HD / 8), g4 = gidx / (HD / 8);
-#pragma unroll
-          for (int w = 0; w < 4; ++w) {
-            const int row = min(kv0 + 4 * g4 + w, n - 1);
-            rv[c][w] = *reinterpret_cast<const uint4 *>(Vp + size_t(row) * ld + b * 8);
-          }
-        }
-      }
-    };
-    auto store_v = [&](int buf) {
-#pragma unroll
-      for (int c = 0; c < VC; ++c) {
-        const int gidx = tid + c * NT;
-        if (gidx < VGR) {
-          const int b = gidx % (HD / 8), g4 = gidx / (HD / 8);
-          const uint32_t *w0 = reinterpret_cast<const uint32_t *>(&rv[c][0]);
-          const uint32_t *w1 = reinterpret_cast<const uint32_t *>(&rv[c][1]);
-          const uint32_t *w2 = reinterpret_cast<const uint32_t *>(&rv[c][2]);
-          const uint32_t *w3 = reinterpret_cast<const uint32_t *>(&rv[c][3]);
-#pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            const int sw = j >> 1;
-            const bool hi = j & 1;
-            const uint32_t e0 = hi ? (w0[sw] >> 16) : (w0[sw] & 0xffffu);
-            const uint32_t e1 = hi ? (w1[sw] >> 16) : (w1[sw] & 0xffffu);
-            const uint32_t e2 = hi ? (w2[sw] >> 16) : (w2[sw] & 0xffffu);
-            const uint32_t e3 = hi ? (w3[sw] >> 16) : (w3[sw] & 0xffffu);
-            uint2 v2;
-            v2.x = e0 | (e1 << 16);
-            v2.y = e2 | (e3 << 16);
-            *reinterpret_cast<uint2 *>(&sV[buf][vaddr(b * 8 + j, vpos(4 * g4))]) = v2;
-          }
-        }
+      for (int i = 0; i < KI; ++i) {
+        const int r = (wid * KI + i) * RPI + krow;
+        const int row = min(kv0 + r, n - 1);
+        g2lds16(Vp + size_t(row) * ld + ((kslot ^ vsw<HD>(r)) * 8),
+                &sV[buf][(wid * KI + i) * RPI * HD]);
       }
     };
 
@@ -325,8 +298,13 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a) {
       for (int d = 0; d < DS; ++d) {
 #pragma unroll
         for (int kk2 = 0; kk2 < 2; ++kk2) {
-          const bf16x8 vf =
-              *reinterpret_cast<const bf16x8 *>(&sV[buf][vaddr(d * 16 + lr, 32 * kk2 + 8 * lg)]);
+          // lane (g = lg, s = lr) reads dims d*16 + 4 (s % 4) .. +3 of key rows 32 kk2 + 4 g + s / 4
+          // and 16 rows further; the transpose gives lane s dim d*16 + s of those 8 keys
+          const int c = 2 * d + ((lr & 3) >> 1), half = (lr & 1) * 4;
+          const int r1 = 32 * kk2 + 4 * lg + (lr >> 2), r2 = r1 + 16;
+          const bf16x4 v1 = lds_read_tr16(&sV[buf][r1 * HD + ((c ^ vsw<HD>(r1)) << 3) + half]);
+          const bf16x4 v2 = lds_read_tr16(&sV[buf][r2 * HD + ((c ^ vsw<HD>(r2)) << 3) + half]);
+          const bf16x8 vf = __builtin_shufflevector(v1, v2, 0, 1, 2, 3, 4, 5, 6, 7);
 #pragma unroll
           for (int qs = 0; qs < QS; ++qs)
             o[qs][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[qs][kk2], o[qs][d], 0, 0, 0);
@@ -335,9 +313,8 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a) {
     };
 
     issue_k(kb * BKV, 0);
-    load_v(kb * BKV);
+    issue_v(kb * BKV, 0);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    store_v(0);
     __syncthreads();
     // all steps but the last load the next tile unconditionally (issued once this step's K
     // fragments are read) and never mask: no branch splits the loop body's schedule
@@ -346,10 +323,9 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a) {
       const int kv0 = kt * BKV;
       step(buf, kv0, false, [&]() {
         issue_k(kv0 + BKV, buf ^ 1);
-        load_v(kv0 + BKV);
+        issue_v(kv0 + BKV, buf ^ 1);
       });
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-      store_v(buf ^ 1);
       __syncthreads();
     }
     step((ke - 1 - kb) & 1, (ke - 1) * BKV, (ke - 1) * BKV + BKV > n, [] {});
