@@ -152,15 +152,19 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    # one event between consecutive steps: the mean over the K steps is the value, the per-step
+    # durations give the median and the 10th / 90th percentiles
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     t0 = time.perf_counter()
-    e0.record(stream)
-    for _ in range(args.steps):
+    evs[0].record(stream)
+    for k in range(args.steps):
         step()
-    e1.record(stream)
+        evs[k + 1].record(stream)
     torch.cuda.synchronize()
     wall = (time.perf_counter() - t0) * 1e3 / args.steps
-    ms = e0.elapsed_time(e1) / args.steps
+    ms = evs[0].elapsed_time(evs[-1]) / args.steps
+    per_step = np.sort([evs[k].elapsed_time(evs[k + 1]) for k in range(args.steps)])
+    pct = lambda q: float(per_step[min(len(per_step) - 1, int(round(q * (len(per_step) - 1))))])
     counts = db.counts.cpu().numpy()
     cu = db.cu.cpu().numpy()
     nc = int(cu[-1])
@@ -226,6 +230,9 @@ def main():
         "warmup": args.warmup,
         "ms_per_step": round(ms, 4),
         "wall_ms_per_step": round(wall, 4),
+        "ms_per_step_median": round(pct(0.5), 4),
+        "ms_per_step_p10": round(pct(0.1), 4),
+        "ms_per_step_p90": round(pct(0.9), 4),
         "higher_is_better": False,
         "scaling": "weak",
         "vs_baseline": None,
