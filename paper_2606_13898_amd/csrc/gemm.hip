@@ -3,14 +3,19 @@
 // weights, tiles never straddling a segment.  Epilogues fuse the bias, the tanh-GELU, and the
 // gated residual update of the float32 stream z.
 //
-// bf16 path: gfx950 MFMA v_mfma_f32_16x16x32_bf16, fp32 accumulation in VGPRs; 128 x 128 tiles
-// on 4 waves, K steps of 64 through a double-buffered LDS ring (64 KiB) filled by direct
-// global->LDS loads; two persistent workgroups per CU (their barriers are independent, so one
-// computes while the other waits for its loads) run whole data-parallel waves, then a stream-K
-// remainder.
+// bf16 path: gfx950 MFMA v_mfma_f32_16x16x32_bf16 with fp32 accumulation, persistent
+// workgroups running whole data-parallel waves of tiles, then a stream-K remainder, in one of two
+// tilings:
+//   * 128 x 128 tiles on 4 waves, accumulators in VGPRs, K steps of 64 through a double-buffered
+//     LDS ring (64 KiB) filled by direct global->LDS loads; two workgroups per CU (their barriers
+//     are independent, so one computes while the other waits for its loads);
+//   * 256 x 256 tiles on 4 waves (k_gemm_big), accumulators in AGPRs, 32-deep stages through a
+//     4-slot ring (128 KiB), one workgroup per CU: half the operand bytes per FLOP.
 //
 // The MFMA is issued with the weight fragment as its first operand, so each lane's 4
 // accumulators are 4 consecutive output columns of one row (contiguous epilogue stores).
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -174,7 +179,10 @@ HILO_DEV SkPlan sk_plan(const GemmProblem &p, int BM, int BN, int P) {
   q.TN = (p.N + BN - 1) / BN;
   q.T = q.R * q.TN;
   q.nk = p.K / 64;
-  if (q.T < P && q.nk <= kNoSplitSteps) {
+  // 256 x 256 tiles: a stream-K tail costs a 256 KiB partial per piece; when the last wave holds
+  // at least half of P tiles, whole tiles in ceil(T / P) waves finish sooner
+  const bool whole_waves = BM * BN >= 256 * 256 && q.T >= P && 2 * (q.T % P) >= P;
+  if ((q.T < P && q.nk <= kNoSplitSteps) || whole_waves) {
     q.s = 1;
     q.U = q.dp = q.T;
     q.len = q.nk;
@@ -215,6 +223,48 @@ HILO_DEV void tile_coords(const SkPlan &q, int t, int &r, int &tn) {
   const int gm = min(kTileGroupRows, q.R - grp * kTileGroupRows);
   r = grp * kTileGroupRows + in % gm;
   tn = in / gm;
+}
+
+// Work items of one workgroup, in order: its data-parallel units (u = pid, pid + P, ...), then the
+// pieces of its stream-K range.  An item is (tile, 64-deep K steps [kb, ke), partial slot or null
+// for a tile finished here).
+struct SkItem {
+  int t, kb, ke;
+  float *slot;
+  bool valid;
+};
+
+struct SkCursor {
+  int u;          // next data-parallel unit
+  long long it;   // next stream-K iteration
+};
+
+HILO_DEV SkItem sk_next_item(SkCursor &c, const SkPlan &q, const SkRange &rg, int P, int pid, float *part,
+                             size_t part_floats) {
+  SkItem x{0, 0, 0, nullptr, false};
+  if (c.u < q.dp) {
+    const int pc = c.u / q.T;
+    x.t = c.u - pc * q.T;
+    x.kb = piece_k0(q, pc);
+    x.ke = piece_k0(q, pc + 1);
+    x.slot = q.s == 1 ? nullptr : part + size_t(c.u) * part_floats;
+    x.valid = true;
+    c.u += P;
+  } else if (c.it < rg.end) {
+    const long long v = c.it / q.len;
+    const int k0 = int(c.it - v * q.len);
+    const int k1 = int(min((long long)q.len, k0 + (rg.end - c.it)));
+    const int uu = q.dp + int(v);
+    const int pc = uu / q.T;
+    x.t = uu - pc * q.T;
+    x.kb = piece_k0(q, pc) + k0;
+    x.ke = piece_k0(q, pc) + k1;
+    const bool whole = q.s == 1 && k0 == 0 && k1 == q.len;
+    x.slot = whole ? nullptr : part + (size_t(P) + size_t(pid) * 2 + (c.it == rg.beg ? 0 : 1)) * part_floats;
+    x.valid = true;
+    c.it += k1 - k0;
+  }
+  return x;
 }
 
 // WM x WN waves, wave tile (BM/WM) x (BN/WN), K step 64 through a double-buffered LDS ring filled
@@ -322,42 +372,8 @@ __global__ __launch_bounds__(WM *WN * 64) void k_gemm_sk(GemmProblem p) {
   const int lrow = lane >> 3, lslot = lane & 7;
   const uint16_t *A = reinterpret_cast<const uint16_t *>(p.A);
 
-  int u = pid;            // next data-parallel unit of this workgroup
-  long long it = rg.beg;  // next stream-K iteration of this workgroup
-
-  // work items: (tile, K steps [kb, ke), partial slot or null for a tile finished here)
-  struct Item {
-    int t, kb, ke;
-    float *slot;
-    bool valid;
-  };
-  auto next_item = [&]() {
-    Item x{0, 0, 0, nullptr, false};
-    if (u < q.dp) {
-      const int pc = u / q.T;
-      x.t = u - pc * q.T;
-      x.kb = piece_k0(q, pc);
-      x.ke = piece_k0(q, pc + 1);
-      x.slot = q.s == 1 ? nullptr : p.part + size_t(u) * T::kPartFloats;
-      x.valid = true;
-      u += P;
-    } else if (it < rg.end) {
-      const long long v = it / q.len;
-      const int k0 = int(it - v * q.len);
-      const int k1 = int(min((long long)q.len, k0 + (rg.end - it)));
-      const int uu = q.dp + int(v);
-      const int pc = uu / q.T;
-      x.t = uu - pc * q.T;
-      x.kb = piece_k0(q, pc) + k0;
-      x.ke = piece_k0(q, pc) + k1;
-      const bool whole = q.s == 1 && k0 == 0 && k1 == q.len;
-      x.slot = whole ? nullptr
-                     : p.part + (size_t(P) + size_t(pid) * 2 + (it == rg.beg ? 0 : 1)) * T::kPartFloats;
-      x.valid = true;
-      it += k1 - k0;
-    }
-    return x;
-  };
+  SkCursor cur_c{pid, rg.beg};
+  auto next_item = [&]() { return sk_next_item(cur_c, q, rg, P, pid, p.part, T::kPartFloats); };
   // a tile's rows and this lane's load sources: row (wave band + 8 i + lane / 8), chunk
   // (lane % 8) ^ swz(row); rows past the tile edge re-read the last valid row (never stored)
   struct Src {
@@ -392,7 +408,7 @@ __global__ __launch_bounds__(WM *WN * 64) void k_gemm_sk(GemmProblem p) {
     for (int i = 0; i < IB; ++i) g2lds16(x.b[i] + k0, &sB[buf][(wid * (BN / NW) + 8 * i) * BK]);
   };
 
-  Item cur = next_item();
+  SkItem cur = next_item();
   if (!cur.valid) return;
   Src sc = make_src(cur.t);
   issue(sc, cur.kb * BK, 0);
@@ -400,7 +416,7 @@ __global__ __launch_bounds__(WM *WN * 64) void k_gemm_sk(GemmProblem p) {
   while (true) {
     // the next item is known before this one's last step: its first loads go out then, so they
     // overlap this item's epilogue instead of starting an empty pipeline after it
-    const Item nxt = next_item();
+    const SkItem nxt = next_item();
     const Src sn = make_src(nxt.valid ? nxt.t : cur.t);
 
     f32x4 acc[TM][TN];
@@ -460,45 +476,355 @@ __global__ __launch_bounds__(WM *WN * 64) void k_gemm_sk(GemmProblem p) {
   }
 }
 
-// Finishes every tile left in partials: (tile, main-kernel wave) work items, 4 waves per
-// workgroup, each wave summing TM / 4 rows of fragments of that main-kernel wave over the tile's
-// partials (pieces in K order, stream-K contributors in workgroup order), then running the
-// epilogue on them.
+// ------------------------------------------------------------------- bf16 MFMA, 256 x 256 tiles
+//
+// One persistent workgroup per CU, 4 waves (2 x 2), wave tile 128 x 128: 256 fp32 accumulators per
+// lane, held in AGPRs.  Per MFMA the wave reads a quarter of the LDS bytes a 64 x 64 wave tile
+// needs, and per K step the CU loads half the operand bytes per FLOP of a 128 x 128 tile.  K runs
+// in 32-deep stages through a 4-slot LDS ring (32 KiB per stage: the stage's 256 A rows, then its
+// 256 W rows, 64 bytes each, 16-byte chunks swizzled), loaded by direct global->LDS loads three
+// stages ahead.  With one wave per SIMD nothing hides a stall of the wave, so the loop is written
+// as a fixed schedule over the 64 MFMAs of a stage (inline asm pins the order):
+//   * each fragment row waits only for its own LDS reads (DS reads complete in order, so an exact
+//     lgkmcnt is known at every point);
+//   * after two of the eight MFMA rows the wave waits for its loads of the *next* stage and meets
+//     the others at the barrier, which also tells it that every wave has finished reading the
+//     slot it is about to refill;
+//   * one of the stage's 8 load instructions (three stages ahead) follows each of the next 8
+//     MFMAs, one of the 16 fragment reads of the next stage each of the following 16.
+// Fragments alternate between two register sets, so a scheduling unit is two stages (one 64-deep
+// K step, the unit of the stream-K plan).  A second cursor over the workgroup's items drives the
+// loads: at the end of an item they already fetch the next item's first stages, so its epilogue
+// overlaps them.  Past the last item the loader repeats the last stage into free slots (valid
+// addresses; keeps the vmcnt arithmetic uniform).
+// Values that are the same on every lane, restated as such (the compiler otherwise keeps some of
+// the stream-K bookkeeping in VGPRs and branches on it with exec masks).
+HILO_DEV int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
+HILO_DEV float *uni(float *ptr) {
+  const uint64_t v = reinterpret_cast<uint64_t>(ptr);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane(uint32_t(v)), hi = __builtin_amdgcn_readfirstlane(uint32_t(v >> 32));
+  return reinterpret_cast<float *>((uint64_t(hi) << 32) | lo);
+}
+HILO_DEV SkItem uni(const SkItem &x) { return SkItem{uni(x.t), uni(x.kb), uni(x.ke), uni(x.slot), uni(int(x.valid)) != 0}; }
+HILO_DEV TileRows uni(const TileRows &x) { return TileRows{uni(x.s), uni(x.sigma), uni(x.row0), uni(x.nrows)}; }
+
+namespace big {
+constexpr int BM = 256, BN = 256, BK = 32, S = 4;
+constexpr int SB = (BM + BN) * BK * 2;  // stage bytes
+constexpr int SPLIT = 2;                // MFMA rows before the barrier
+HILO_DEV int swz(int r) { return ((r >> 1) & 3) ^ ((r >> 3) & 1); }
+}  // namespace big
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+#define HILO_MFMA_AGPR(ACC, FB, FA) \
+  asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(ACC) : "v"(FB), "v"(FA) : "memory")
+// first K stage of a tile: accumulate onto zero (no separate clearing of the AGPRs)
+#define HILO_MFMA_AGPR0(ACC, FB, FA) \
+  asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, 0" : "=a"(ACC) : "v"(FB), "v"(FA) : "memory")
+#define HILO_DS_READ16(DST, ADDR, OFF) \
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(DST) : "v"(ADDR), "i"(OFF) : "memory")
+
+template <int N>
+HILO_DEV void wait_lgkm_le() { asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(N) : "memory"); }
+
+HILO_DEV void wait_lgkm_rt(int n) {  // n is a compile-time constant after unrolling
+  switch (n) {
+    case 0: wait_lgkm_le<0>(); break;   case 1: wait_lgkm_le<1>(); break;
+    case 2: wait_lgkm_le<2>(); break;   case 3: wait_lgkm_le<3>(); break;
+    case 4: wait_lgkm_le<4>(); break;   case 5: wait_lgkm_le<5>(); break;
+    case 6: wait_lgkm_le<6>(); break;   case 7: wait_lgkm_le<7>(); break;
+    case 8: wait_lgkm_le<8>(); break;   case 9: wait_lgkm_le<9>(); break;
+    case 10: wait_lgkm_le<10>(); break; case 11: wait_lgkm_le<11>(); break;
+    case 12: wait_lgkm_le<12>(); break; case 13: wait_lgkm_le<13>(); break;
+    case 14: wait_lgkm_le<14>(); break; default: wait_lgkm_le<15>(); break;
+  }
+}
+
+// Epilogue of a 256 x 256 tile from the AGPR accumulators of wave wid: bias (and gate) depend on
+// the column only and are loaded once, so the bias / GELU epilogues make a single memory round
+// trip; the residual update loads the old z one fragment row at a time (two rows in flight do not
+// fit the register budget next to the next tile's fragments).  Loads use indices clamped into the
+// tile; values outside it are never stored.
+template <int EPI>
+HILO_DEV void big_epilogue(const GemmProblem &p, const TileRows &tr, int n0, int wid, int lane, f32x4 (&acc)[8][8]) {
+  const int rbase = (wid >> 1) * 128 + (lane & 15);
+  const int cbase = n0 + (wid & 1) * 128 + 4 * (lane >> 4);
+  const uint16_t *bias = reinterpret_cast<const uint16_t *>(tr.sigma ? p.bias[1] : p.bias[0]);
+  float bv[8][4];
+  float4 gt[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int nc = min(cbase + j * 16, p.N - 4);
+    const uint2 bu = *reinterpret_cast<const uint2 *>(bias + nc);
+    bv[j][0] = __uint_as_float(bu.x << 16); bv[j][1] = __uint_as_float(bu.x & 0xffff0000u);
+    bv[j][2] = __uint_as_float(bu.y << 16); bv[j][3] = __uint_as_float(bu.y & 0xffff0000u);
+    if constexpr (EPI == EPI_RESID)
+      gt[j] = *reinterpret_cast<const float4 *>(p.mod + (size_t(tr.s * 2 + tr.sigma) * 6 + p.gate_idx) * p.D + nc);
+  }
+  float4 zc[8];  // old z of the current fragment row
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    if constexpr (EPI == EPI_RESID) {
+      const size_t m = size_t(tr.row0 + min(rbase + i * 16, tr.nrows - 1));
+#pragma unroll
+      for (int j = 0; j < 8; ++j) zc[j] = *reinterpret_cast<const float4 *>(p.z + m * p.ldz + min(cbase + j * 16, p.N - 4));
+    }
+    f32x4 row[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {  // copy this row out of the AGPRs here, not all rows up front
+      row[j] = acc[i][j];
+      asm volatile("" : "+v"(row[j]));
+    }
+    const int rl = rbase + i * 16;
+    if (rl < tr.nrows) {
+      const size_t m = size_t(tr.row0 + rl);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int n = cbase + j * 16;
+        if (n >= p.N) continue;
+        float v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = row[j][e] + bv[j][e];
+        if constexpr (EPI == EPI_RESID) {
+          float4 z = zc[j];
+          z.x += gt[j].x * v[0];
+          z.y += gt[j].y * v[1];
+          z.z += gt[j].z * v[2];
+          z.w += gt[j].w * v[3];
+          *reinterpret_cast<float4 *>(p.z + m * p.ldz + n) = z;
+        } else {
+          if constexpr (EPI == EPI_GELU) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[e] = gelu_tanh(v[e]);
+          }
+          uint2 u;
+          u.x = pack_bf16x2(v[0], v[1]);
+          u.y = pack_bf16x2(v[2], v[3]);
+          *reinterpret_cast<uint2 *>(reinterpret_cast<uint16_t *>(p.out) + m * p.ldo + n) = u;
+        }
+      }
+    }
+    asm volatile("" ::: "memory");  // the next row's loads stay below these stores
+  }
+}
+
+template <int EPI, int ROLE>
+__global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
+  using namespace big;
+  using T = SkTile<BM, BN, 2, 2>;
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[S * SB];
+
+  const int P = gridDim.x;
+  const int pid = xcd_remap(blockIdx.x, P);
+  const SkPlan q = sk_plan(p, BM, BN, P);
+  const SkRange rg = sk_range(q.I, P, pid);
+
+  const int lane = threadIdx.x & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lrow = lane >> 2, lslot = lane & 3;
+  const uint16_t *A = reinterpret_cast<const uint16_t *>(p.A);
+
+  // ---- loader: its own cursor over this workgroup's items, three stages ahead of the MFMAs
+  SkCursor lc{pid, rg.beg};
+  const uint16_t *la[4], *lb[4];
+  int lk = 0, lke = 0;  // next stage to load (32-deep, absolute in K) and the end of its item
+  auto ld_src = [&](int t) __attribute__((always_inline)) {
+    int rt, tn;
+    tile_coords(q, t, rt, tn);
+    tn = uni(tn);
+    const TileRows tr = uni(decode_row_tile(p, BM, uni(rt)));
+    const uint16_t *Wt = reinterpret_cast<const uint16_t *>(tr.sigma ? p.W[1] : p.W[0]);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = wid * 64 + 16 * i + lrow, c = (lslot ^ swz(r)) * 8;
+      la[i] = A + size_t(tr.row0 + min(r, tr.nrows - 1)) * p.lda + c;
+      lb[i] = Wt + size_t(min(tn * BN + r, p.N - 1)) * p.K + c;
+    }
+  };
+  auto ld_advance = [&]() __attribute__((always_inline)) {
+    const SkItem x = uni(sk_next_item(lc, q, rg, P, pid, p.part, T::kPartFloats));
+    if (x.valid) {
+      ld_src(x.t);
+      lk = 2 * x.kb;
+      lke = 2 * x.ke;
+    } else {
+      lk = lke - 1;  // no further item: repeat the last stage
+    }
+    lk = uni(lk);
+    lke = uni(lke);
+  };
+  // load instruction j (0..7) of the current loader stage into `slot`: A rows for j < 4
+  auto ld_one = [&](int slot, int j) __attribute__((always_inline)) {
+    uint8_t *base = lds + slot * SB + wid * 64 * 64;
+    const int k0 = lk * BK;
+    if (j < 4) g2lds16(la[j] + k0, base + j * 1024);
+    else g2lds16(lb[j - 4] + k0, base + 16384 + (j - 4) * 1024);
+  };
+
+  // ---- fragment addresses: lane (lr, lg) reads row lr of 16, chunk lg of 4 (swizzle of lr only:
+  // fragment rows start at multiples of 16)
+  const int lr = lane & 15, lg = lane >> 4;
+  const uint32_t lane_off = lr * 64 + ((lg ^ swz(lr)) * 16);
+  const uint32_t lds0 = (uint32_t)(uintptr_t)lds;
+  const uint32_t fa0 = lds0 + (wid >> 1) * 128 * 64 + lane_off;
+  const uint32_t fb0 = lds0 + 16384 + (wid & 1) * 128 * 64 + lane_off;
+  // read t of a stage, in consumption order: W fragments 0..7, then A fragments 0..7
+  auto rd_one = [&](u32x4 (&fa)[8], u32x4 (&fb)[8], uint32_t a, uint32_t b, int t) __attribute__((always_inline)) {
+    switch (t) {
+      case 0: HILO_DS_READ16(fb[0], b, 0); break;     case 1: HILO_DS_READ16(fb[1], b, 1024); break;
+      case 2: HILO_DS_READ16(fb[2], b, 2048); break;  case 3: HILO_DS_READ16(fb[3], b, 3072); break;
+      case 4: HILO_DS_READ16(fb[4], b, 4096); break;  case 5: HILO_DS_READ16(fb[5], b, 5120); break;
+      case 6: HILO_DS_READ16(fb[6], b, 6144); break;  case 7: HILO_DS_READ16(fb[7], b, 7168); break;
+      case 8: HILO_DS_READ16(fa[0], a, 0); break;     case 9: HILO_DS_READ16(fa[1], a, 1024); break;
+      case 10: HILO_DS_READ16(fa[2], a, 2048); break; case 11: HILO_DS_READ16(fa[3], a, 3072); break;
+      case 12: HILO_DS_READ16(fa[4], a, 4096); break; case 13: HILO_DS_READ16(fa[5], a, 5120); break;
+      case 14: HILO_DS_READ16(fa[6], a, 6144); break; default: HILO_DS_READ16(fa[7], a, 7168); break;
+    }
+  };
+
+  f32x4 acc[8][8];
+  u32x4 xa[8], xb[8], ya[8], yb[8];
+
+  // one stage (ring slot gs % S) on fragments (fa, fb); reads stage gs + 1 into (na, nb); the
+  // first stage of a tile (first = true_type) starts the accumulators from zero
+  constexpr int LQ0 = SPLIT * 8, RQ0 = LQ0 + 8;
+  static_assert(RQ0 + 16 <= 64, "stage schedule does not fit");
+  auto stage = [&](auto first, u32x4 (&fa)[8], u32x4 (&fb)[8], u32x4 (&na)[8], u32x4 (&nb)[8], int gs) __attribute__((always_inline)) {
+    const int lslot_w = (gs + S - 1) & (S - 1), nslot = (gs + 1) & (S - 1);
+    const uint32_t a = fa0 + nslot * SB, b = fb0 + nslot * SB;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      // outstanding reads allowed: this stage's A fragments i+1..7 and the next stage's issued so far
+      const int q0 = i * 8;
+      wait_lgkm_rt(7 - i + (q0 <= RQ0 ? 0 : min(q0 - RQ0, 16)));
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int qq = i * 8 + j;
+        if (qq == LQ0) asm volatile("s_waitcnt vmcnt(%0)\n s_barrier" ::"n"((S - 3) * 8) : "memory");
+        if constexpr (decltype(first)::value) HILO_MFMA_AGPR0(acc[i][j], fb[j], fa[i]);
+        else HILO_MFMA_AGPR(acc[i][j], fb[j], fa[i]);
+        if (qq >= LQ0 && qq < LQ0 + 8) ld_one(lslot_w, qq - LQ0);
+        if (qq >= RQ0 && qq < RQ0 + 16) rd_one(na, nb, a, b, qq - RQ0);
+      }
+    }
+    ++lk;
+  };
+
+  SkCursor cc{pid, rg.beg};
+  SkItem cur = uni(sk_next_item(cc, q, rg, P, pid, p.part, T::kPartFloats));
+  if (!cur.valid) return;
+  ld_advance();  // the same first item
+#pragma unroll 1
+  for (int st = 0; st < S - 1; ++st) {
+    if (lk == lke) ld_advance();
+#pragma unroll
+    for (int j = 0; j < 8; ++j) ld_one(st, j);
+    ++lk;
+  }
+  asm volatile("s_waitcnt vmcnt(%0)\n s_barrier" ::"n"((S - 2) * 8) : "memory");
+#pragma unroll
+  for (int t = 0; t < 16; ++t) rd_one(xa, xb, fa0, fb0, t);
+
+  // the loader moves to its next item between stages, outside the MFMA schedule
+  auto ld_check = [&]() __attribute__((always_inline)) {
+    if (lk == lke) ld_advance();
+  };
+  int gs = 0;
+  while (true) {
+    ld_check();
+    stage(std::true_type{}, xa, xb, ya, yb, gs);
+    ld_check();
+    stage(std::false_type{}, ya, yb, xa, xb, gs + 1);
+    gs += 2;
+#pragma unroll 1
+    for (int kt = cur.kb + 1; kt < cur.ke; ++kt) {
+      ld_check();
+      stage(std::false_type{}, xa, xb, ya, yb, gs);
+      ld_check();
+      stage(std::false_type{}, ya, yb, xa, xb, gs + 1);
+      gs += 2;
+    }
+    // The last MFMAs' results must land before the accumulators are read (the empty asm ties each
+    // accumulator to this point, so no read is scheduled above it), and the reads of the next
+    // stage's fragments must be complete before the compiler may move those registers.
+    asm volatile("s_waitcnt lgkmcnt(0)\n s_nop 7\n s_nop 7\n s_nop 7" ::: "memory");
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) asm volatile("" : "+a"(acc[i][j]));
+    if (cur.slot == nullptr) {
+      int rt, tn;
+      tile_coords(q, cur.t, rt, tn);
+      tn = uni(tn);
+      const TileRows tr = uni(decode_row_tile(p, BM, uni(rt)));
+      big_epilogue<EPI>(p, tr, tn * BN, wid, lane, acc);
+    } else {
+      // straight from the AGPRs (no copy of all 256 accumulators through VGPRs)
+      float *base = cur.slot + T::part_index(wid, 0, 0, lane);
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          asm volatile("global_store_dwordx4 %0, %1, off" ::"v"(base + (i * 8 + j) * 256), "a"(acc[i][j]) : "memory");
+    }
+    cur = uni(sk_next_item(cc, q, rg, P, pid, p.part, T::kPartFloats));
+    if (!cur.valid) break;
+  }
+  asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
+}
+
+// Finishes every tile left in partials.  A work item is one fragment row of one main-kernel wave
+// of one tile, taken by one wave of the fixup: it adds the tile's partials (pieces in K order,
+// stream-K contributors in workgroup order) and runs the epilogue on the row.  Contributions are
+// loaded in batches of four (one memory round trip per batch instead of per contributor) and
+// added in the fixed order, so the result does not depend on the batching.
 constexpr int kFixThreads = 256;
+constexpr int kFixBatch = 4;
 
 template <int BM, int BN, int WM, int WN, int EPI, int ROLE>
 __global__ __launch_bounds__(kFixThreads) void k_gemm_fix(GemmProblem p, int P) {
   using T = SkTile<BM, BN, WM, WN>;
-  constexpr int TM = T::TM, TN = T::TN, NW = T::NW, FW = kFixThreads / 64, IPW = TM / FW;
-  static_assert(IPW * FW == TM, "fix waves must split the fragment rows");
+  constexpr int TM = T::TM, TN = T::TN, NW = T::NW, FW = kFixThreads / 64;
   const SkPlan q = sk_plan(p, BM, BN, P);
   const int nfix = q.s > 1 ? q.T : q.U - q.dp;
-  const int lane = threadIdx.x & 63, fw = threadIdx.x >> 6;
-  for (int x = blockIdx.x; x < nfix * NW; x += gridDim.x) {
-    const int f = x / NW, wid = x - f * NW;
+  const int lane = threadIdx.x & 63;
+  const int items = nfix * NW * TM;
+  for (int x = blockIdx.x * FW + (threadIdx.x >> 6); x < items; x += gridDim.x * FW) {
+    const int f = x / (NW * TM), rem = x - f * (NW * TM), wid = rem / TM, i = rem - wid * TM;
     const int t = q.s > 1 ? f : q.dp + f;
-    f32x4 acc[IPW][TN];
+    f32x4 acc[1][TN];
 #pragma unroll
-    for (int i = 0; i < IPW; ++i)
+    for (int j = 0; j < TN; ++j) acc[0][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const float *b[kFixBatch];
+    int nb = 0;
+    auto flush = [&]() {
+      f32x4 v[kFixBatch][TN];
 #pragma unroll
-      for (int j = 0; j < TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-    auto add = [&](const float *slot) {
-      f32x4 v[IPW][TN];
+      for (int c = 0; c < kFixBatch; ++c)
+        if (c < nb) {
 #pragma unroll
-      for (int i = 0; i < IPW; ++i)
+          for (int j = 0; j < TN; ++j) v[c][j] = *reinterpret_cast<const f32x4 *>(b[c] + T::part_index(wid, i, j, lane));
+        }
 #pragma unroll
-        for (int j = 0; j < TN; ++j)
-          v[i][j] = *reinterpret_cast<const f32x4 *>(slot + T::part_index(wid, fw * IPW + i, j, lane));
+      for (int c = 0; c < kFixBatch; ++c)
+        if (c < nb) {
 #pragma unroll
-      for (int i = 0; i < IPW; ++i)
+          for (int j = 0; j < TN; ++j) acc[0][j] += v[c][j];
+        }
+      nb = 0;
+    };
+    auto push = [&](const float *slot) {
 #pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] += v[i][j];
+      for (int c = 0; c < kFixBatch; ++c)
+        if (c == nb) b[c] = slot;
+      if (++nb == kFixBatch) flush();
     };
     bool done_whole = false;
     for (int pc = 0; pc < q.s; ++pc) {
       const int u = pc * q.T + t;
       if (u < q.dp) {
-        add(p.part + size_t(u) * T::kPartFloats);
+        push(p.part + size_t(u) * T::kPartFloats);
         continue;
       }
       const int v = u - q.dp;
@@ -519,16 +845,17 @@ __global__ __launch_bounds__(kFixThreads) void k_gemm_fix(GemmProblem p, int P) 
           ++qn;
           rn -= P;
         }
-        if (qb < qn) add(p.part + (size_t(P) + size_t(w) * 2 + (qb >= a0 ? 0 : 1)) * T::kPartFloats);
+        if (qb < qn) push(p.part + (size_t(P) + size_t(w) * 2 + (qb >= a0 ? 0 : 1)) * T::kPartFloats);
         qb = qn;
         rb = rn;
       }
     }
     if (done_whole) continue;
+    flush();
     int rt, tn;
     tile_coords(q, t, rt, tn);
     const TileRows tr = decode_row_tile(p, BM, rt);
-    T::template epilogue_rows<EPI, IPW>(p, tr, tn * BN, wid, fw * IPW, lane, acc);
+    T::template epilogue_rows<EPI, 1>(p, tr, tn * BN, wid, i, lane, acc);
   }
 }
 
@@ -583,6 +910,20 @@ __global__ __launch_bounds__(256) void k_gemm_f32(GemmProblem p, int imgTiles, i
 
 // ------------------------------------------------------------------------------- dispatch
 
+// CUs of the current device (cached per device).
+int device_cus() {
+  static int ncu[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) dev = 0;
+  if (ncu[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+      n = kBigMaxWorkgroups;
+    ncu[dev] = n;
+  }
+  return ncu[dev];
+}
+
 // Persistent workgroups of the bf16 GEMM: two per CU.
 int sk_workgroups() {
   static int ncu[64] = {0};
@@ -609,9 +950,28 @@ static hipError_t run_bf16(const GemmProblem &p, hipStream_t st) {
   const long long tiles_max = (long long)p.B * ((p.max_img_rows + BM - 1) / BM + (p.L + BM - 1) / BM) *
                               ((p.N + BN - 1) / BN);
   if (tiles_max < P && p.K / 64 <= kNoSplitSteps) return hipSuccess;
-  // fewer than P tiles are ever left in partials; one work item per (tile, main-kernel wave)
-  hipLaunchKernelGGL((k_gemm_fix<BM, BN, WM, WN, role_epilogue(ROLE), ROLE>), dim3(P * WM * WN), dim3(kFixThreads), 0, st,
-                     p, P);
+  // fewer than P tiles are ever left in partials; one fixup wave per (tile, wave, fragment row)
+  constexpr int kFixBlocks = (WM * WN) * (BM / WM / 16) / (kFixThreads / 64);
+  hipLaunchKernelGGL((k_gemm_fix<BM, BN, WM, WN, role_epilogue(ROLE), ROLE>), dim3(P * kFixBlocks), dim3(kFixThreads), 0,
+                     st, p, P);
+  return hipGetLastError();
+}
+
+// 256 x 256 tiles: one persistent workgroup per CU.
+template <int ROLE>
+static hipError_t run_big(const GemmProblem &p, hipStream_t st) {
+  static_assert(size_t(big::BM) * big::BN * 3 * kBigMaxWorkgroups * sizeof(float) <= kSkPartBytes,
+                "partial area too small");
+  const int P = device_cus() < kBigMaxWorkgroups ? device_cus() : kBigMaxWorkgroups;
+  hipLaunchKernelGGL((k_gemm_big<role_epilogue(ROLE), ROLE>), dim3(P), dim3(256), 0, st, p);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const long long tiles_max = (long long)p.B * ((p.max_img_rows + big::BM - 1) / big::BM + (p.L + big::BM - 1) / big::BM) *
+                              ((p.N + big::BN - 1) / big::BN);
+  if (tiles_max < P && p.K / 64 <= kNoSplitSteps) return hipSuccess;
+  constexpr int kFixBlocks = 4 * (big::BM / 2 / 16) / (kFixThreads / 64);
+  hipLaunchKernelGGL((k_gemm_fix<big::BM, big::BN, 2, 2, role_epilogue(ROLE), ROLE>), dim3(P * kFixBlocks), dim3(kFixThreads),
+                     0, st, p, P);
   return hipGetLastError();
 }
 
@@ -635,10 +995,15 @@ hipError_t launch_gemm(bool bf16, int role, const GemmProblem &p, hipStream_t st
       default: return run_f32<EPI_RESID>(p, st);
     }
   }
+  // Tiling per projection, as measured on the 64 x 64 workload (2766 rows): QKV and MLP up run
+  // 256 x 256 tiles (QKV: 396 tiles, two waves of whole tiles; MLP up: 528 tiles, two waves plus a
+  // short stream-K tail); the attention output and MLP down projections have only 132 such tiles
+  // for 256 CUs, so they would need split K with 256 KiB partials, and keep 128 x 128 tiles
+  // (528 of them for 512 workgroups).
   switch (role) {
-    case GEMM_QKV: return run_bf16<128, 128, 2, 2, GEMM_QKV>(p, st);
+    case GEMM_QKV: return run_big<GEMM_QKV>(p, st);
     case GEMM_O: return run_bf16<128, 128, 2, 2, GEMM_O>(p, st);
-    case GEMM_FC1: return run_bf16<128, 128, 2, 2, GEMM_FC1>(p, st);
+    case GEMM_FC1: return run_big<GEMM_FC1>(p, st);
     default: return run_bf16<128, 128, 2, 2, GEMM_FC2>(p, st);
   }
 }

@@ -52,14 +52,18 @@ struct GemmProblem {
   int gate_idx, D;
   const int *cu;          // [B+1]
   int B, L, max_img_rows; // max_img_rows = images * N
-  float *part;            // bf16 path: partial tiles, 3 * kSkMaxWorkgroups slots
+  float *part;            // bf16 path: partial tiles (kSkPartBytes)
 };
 
 // Partial-sum area of the bf16 GEMMs (part of the caller's workspace): one slot per data-parallel
-// unit of a split wave plus two per workgroup for its stream-K range; two workgroups per CU.
+// unit of a split wave plus two per workgroup for its stream-K range.  128 x 128 tiles: two
+// workgroups per CU, at most 512; 256 x 256 tiles: one per CU, at most 256.
 constexpr int kSkMaxWorkgroups = 512;
+constexpr int kBigMaxWorkgroups = 256;
 constexpr size_t kSkPartFloats = size_t(128) * 128;  // one 128 x 128 fp32 tile per slot
-constexpr size_t kSkPartBytes = size_t(kSkMaxWorkgroups) * 3 * kSkPartFloats * sizeof(float);
+constexpr size_t kSkPartBytes = size_t(kBigMaxWorkgroups) * 3 * 256 * 256 * sizeof(float);
+static_assert(size_t(kSkMaxWorkgroups) * 3 * kSkPartFloats * sizeof(float) <= kSkPartBytes,
+              "partial area must hold both tilings");
 hipError_t launch_gemm(bool bf16, int role, const GemmProblem &p, hipStream_t st);
 
 // Stream-K partial results of the bf16 attention core (part of the caller's workspace): two

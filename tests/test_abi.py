@@ -45,7 +45,7 @@ def test_max_tokens_and_workspace():
     s = good_shape()
     assert hilo.hilo_max_tokens(s) == 2 * (80 + 5)
     T = 170
-    part = 512 * 3 * 128 * 128 * 4  # GEMM partial tiles (the attention core's fit inside)
+    part = 256 * 3 * 256 * 256 * 4  # GEMM partial tiles: 3 slots of 256 x 256 fp32 per CU, at most 256 CUs
     want = max(-(-T * 256 * 2 // 256) * 256 + -(-T * 768 * 2 // 256) * 256,
                -(-T * 256 * 2 // 256) * 256 + -(-T * 1024 * 2 // 256) * 256) + part
     assert hilo.hilo_workspace_bytes(s) == want

@@ -212,3 +212,28 @@ def test_mlp_split_k(shp):
     T = int(ref["cu"][-1])
     assert_close(to_np(db.z)[:T], ref["z2"], "bf16", "z after split-K mlp")
     assert_close(to_np(db.y_img), ref["y_img"], "bf16", "y_img split-K")
+
+
+# On a 256-CU device these reach every schedule of the 256 x 256 GEMM tiling (QKV, MLP up); every
+# block is kept fine so the row counts are fixed.
+@pytest.mark.parametrize("shp", [
+    # 17 row tiles x 16 column tiles = 272 MLP-up tiles: one wave of whole tiles plus a 16-tile
+    # stream-K tail finished by the fixup
+    inputs.BlockShape(1, 1, 64, 64, 256, 256, 2, 128, 4096, "bf16"),
+    # 17 x 24 = 408 MLP-up tiles: the last wave holds 152 >= 128 tiles, so two waves of whole tiles
+    inputs.BlockShape(1, 1, 64, 64, 256, 256, 2, 128, 6144, "bf16"),
+    # few tiles and K = 4608 (72 steps): QKV cut into 5 K pieces plus a stream-K tail, MLP up into
+    # 64 pieces of one or two steps
+    inputs.BlockShape(1, 1, 16, 16, 0, 4608, 36, 128, 1024, "bf16"),
+], ids=["sk_tail", "whole_waves", "k_pieces"])
+def test_gemm_256_schedules(shp):
+    print(f"[parity] 256-tile GEMM schedules shape={shp}", flush=True)
+    wl = inputs.make_workload("splitk", shape=shp, seed=5, keep_frac=1.0)
+    db = DeviceBlock(wl)
+    ref = oracle_for(wl)
+    db.run(hilo.TOPK)
+    torch.cuda.synchronize()
+    check_selection(db, ref)
+    T = int(ref["cu"][-1])
+    assert_close(to_np(db.z)[:T], ref["z2"], "bf16", "z after block")
+    assert_close(to_np(db.y_img), ref["y_img"], "bf16", "y_img")

@@ -64,7 +64,7 @@ def load(out, cnt, tag):
 def kind_of(name, state):
     """Bench kernel kind of a dispatch; rownorm launches alternate attention / MLP per step."""
     base = name.split("(")[0].replace("void ", "").strip()
-    if "k_gemm_sk<" in base or "k_gemm_fix<" in base:
+    if "k_gemm_sk<" in base or "k_gemm_fix<" in base or "k_gemm_big<" in base:
         role = base.rsplit(",", 1)[1].strip(" >")
         return ROLES[role]
     if "k_attn" in base:
