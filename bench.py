@@ -106,6 +106,88 @@ def cpu_baseline(wl):
                       f"numpy, BLAS threads={threads}"}
 
 
+def stack_leg(db, wl, n_blocks, steps, stream, reps=3):
+    """The paper's regime (Sec. 2.3, Sec. 3.3): one request = the selection once, then for each
+    sampling step: compress that step's latents, run `n_blocks` blocks on the compressed tokens
+    (hilo_blocks), decompress.  Against it: the same blocks on the uncompressed tokens every step
+    (no selection, compression or decompression).  Every block has its own random-init weights
+    (N(0, 0.02), bf16, generated on the device) and modulation; each step's latents are the
+    previous step's plus N(0, 0.1) changes."""
+    import torch
+
+    from paper_2606_13898_amd import hilo
+
+    s = wl.shape
+    D, F, B, NB = s.dim, s.mlp_dim, s.batch, s.n_blocks
+    dt = db.dtype
+    g = torch.Generator(device="cuda")
+    g.manual_seed(4242)
+
+    def rnd(*shape, std=0.02, dtype=dt):
+        return (torch.randn(*shape, generator=g, device="cuda", dtype=torch.float32) * std).to(dtype)
+
+    weights = [[{"w_qkv": rnd(3 * D, D), "b_qkv": rnd(3 * D), "w_o": rnd(D, D), "b_o": rnd(D),
+                 "w1": rnd(F, D), "b1": rnd(F), "w2": rnd(D, F), "b2": rnd(D)} for _ in range(2)]
+               for _ in range(n_blocks)]
+    aw, mw = hilo.stack_weights(weights)
+    mods = rnd(steps, n_blocks, B, 2, 6, D, std=0.1, dtype=torch.float32)
+    xs = [db.x_img]
+    for _ in range(steps - 1):
+        xs.append((xs[-1].float() + rnd(*xs[-1].shape, std=0.1, dtype=torch.float32)).to(dt))
+    ws = db.ws
+
+    def request(keep):
+        db.x_img = xs[0]
+        db.score()
+        db.select(hilo.TOPK, keep=keep)
+        for t in range(steps):
+            hilo.hilo_compress(db.shape, xs[t], db.x_txt, db.fine_idx, db.pool_idx, db.counts, db.cu,
+                               db.seg, db.z)
+            hilo.hilo_blocks(db.shape, db.z, db.cu, aw, mw, mods[t], n_blocks, ws)
+            hilo.hilo_decompress(db.shape, db.z, db.idx_map, db.cu, db.seg, db.y_img, db.y_txt)
+
+    def dense_blocks():
+        for t in range(steps):
+            hilo.hilo_compress(db.shape, xs[t], db.x_txt, db.fine_idx, db.pool_idx, db.counts, db.cu,
+                               db.seg, db.z)  # every block fine: the dense token order, untimed
+            e0.record(stream)
+            hilo.hilo_blocks(db.shape, db.z, db.cu, aw, mw, mods[t], n_blocks, ws)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            times.append(e0.elapsed_time(e1))
+
+    x0 = db.x_img
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    request(wl.keep)  # warm-up
+    torch.cuda.synchronize()
+    req = []
+    for _ in range(reps):
+        e0.record(stream)
+        request(wl.keep)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        req.append(e0.elapsed_time(e1))
+    nc = int(db.cu.cpu().numpy()[-1])
+    db.score()
+    db.select(hilo.TOPK, keep=[NB] * s.grids)
+    times = []
+    dense_blocks()  # warm-up
+    times = []
+    for _ in range(reps):
+        dense_blocks()
+    db.x_img = x0
+    nd = int(db.cu.cpu().numpy()[-1])
+    req_ms = sorted(req)[len(req) // 2]
+    dense_ms = sorted(times)[len(times) // 2] * steps  # median step, times the steps of a request
+    del weights, aw, mw, mods, xs
+    return {"blocks": n_blocks, "sampling_steps": steps, "requests_timed": reps,
+            "request_ms": round(req_ms, 3), "dense_request_ms": round(dense_ms, 3),
+            "speedup_vs_dense": round(dense_ms / req_ms, 3), "token_ratio": round(nd / nc, 3),
+            "compressed_tokens": nc, "dense_tokens": nd,
+            "ms_per_block": round(req_ms / (steps * n_blocks), 4),
+            "dense_ms_per_block": round(dense_ms / (steps * n_blocks), 4)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -114,6 +196,11 @@ def main():
     ap.add_argument("--workload", default="m1024", choices=sorted(DESCR))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
+    ap.add_argument("--no-stack", action="store_true",
+                    help="skip the request leg (selection once, then per sampling step compress -> "
+                         "a stack of blocks -> decompress, against the same stack on the dense tokens)")
+    ap.add_argument("--stack-blocks", type=int, default=8)
+    ap.add_argument("--stack-steps", type=int, default=8)
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="only run one plain device-to-device copy of this many MiB (the known-size "
                          "kernel that calibrates the HBM traffic counters) and exit")
@@ -220,6 +307,10 @@ def main():
         n_dense = int(db.cu.cpu().numpy()[-1])
         dense = {"block_ms": round(dense_ms, 4), "tokens": n_dense}
 
+    stack = None
+    if not args.no_stack:
+        stack = stack_leg(db, wl, args.stack_blocks, args.stack_steps, stream)
+
     attn = kern.get("attention_core", {})
     out = {
         "metric": METRIC,
@@ -255,6 +346,8 @@ def main():
         out["speedup_vs_dense"] = round(dense["block_ms"] / ms, 3)
         out["block_speedup_vs_dense"] = round(dense["block_ms"] / t_blk, 3) if t_blk else None
         out["token_ratio"] = round(dense["tokens"] / nc, 3)
+    if stack:
+        out["stack"] = stack
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl)
     print(json.dumps(out), flush=True)

@@ -141,6 +141,18 @@ hilo_status hilo_mlp(const hilo_shape *shape, float *z, const int32_t *cu_seqlen
                      const hilo_mlp_w w[2], const float *mod, void *workspace, size_t ws_bytes,
                      void *stream);
 
+/* S4 + S5 for a stack of n_blocks blocks, in order, in place on z: block l runs hilo_attention
+ * then hilo_mlp with attn_w[2l .. 2l+1], mlp_w[2l .. 2l+1] (image / text stream) and its
+ * modulation mod + l * batch * 2 * 6 * dim.  This is the regime of the paper's speedups (Sec. 3.3):
+ * the selection, compression and decompression run once per sampling step, the network's blocks
+ * all run on the compressed sequence in between.  attn_w, mlp_w: HOST arrays [n_blocks][2] of
+ * device weight pointers; mod: DEVICE float32 [n_blocks][batch][2][6][dim].  Every pointer is
+ * checked before anything is enqueued.  n_blocks = 0 enqueues nothing; n_blocks < 0 ->
+ * HILO_E_PARAM.  workspace as hilo_attention (ws_bytes >= hilo_workspace_bytes(shape)).        */
+hilo_status hilo_blocks(const hilo_shape *shape, float *z, const int32_t *cu_seqlens,
+                        const hilo_attn_w *attn_w, const hilo_mlp_w *mlp_w, const float *mod,
+                        int32_t n_blocks, void *workspace, size_t ws_bytes, void *stream);
+
 /* S6 -- decompress: y_img[g][p] = z[seg_off[g] + idx_map[g][p]] (fine tokens scatter back to
  * their patch, pooled tokens broadcast to the 4 patches of their block), y_txt[s][t] = the text
  * rows of sample s; both rounded to dtype.  y_img [G][N][D], y_txt [B][L][D] or NULL.           */

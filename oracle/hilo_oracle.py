@@ -17,6 +17,8 @@ diffusion-transformer block on the shortened sequence and the reassembly of the 
                                                                      carry the blurry global part)
   block      joint attention + MLP over image and text tokens      (Sec. 2.2 / Sec. 4: DiT whose
                                                                      cost is quadratic in tokens)
+  stack      blocks in order; request = one selection, then per   (Sec. 2.3: selection once per
+             step compress -> stack -> decompress                   request; Sec. 3.3: 8 steps)
   decompress scatter fine rows, broadcast pooled rows to 4 patches
 
 Precision.  Floating point that decides an integer (the energy that decides which blocks stay
@@ -29,7 +31,8 @@ Readings of the paper where it is silent or loose are listed in the design notes
 below states the reading it implements.
 
 Parity status per function (what pins it is in tests/test_oracle_*.py):
-  score, dilate, block_sums, select_*, compact, layout, compress, decompress, attention, mlp:
+  score, dilate, block_sums, select_*, compact, layout, compress, decompress, attention, mlp,
+  stack, request:
   pinned by closed forms, library routines (scipy Sobel / binary dilation, torch SDPA / layer_norm
   / gelu), hand-worked fixtures under tests/golden/, and the identities of the method (0% compression
   equals the dense block, pooling a constant block then broadcasting is lossless, kept-token count
@@ -413,6 +416,39 @@ def pipeline(x_img, x_txt, shape, force, r: int, mode: str, tau=None, keep=None,
             y_img, y_txt = decompress(z2, idx_map, cu, seg, shape.text_len, shape.batch)
             res.update(y_img=y_img, y_txt=y_txt)
     return res
+
+
+def stack(Z: np.ndarray, cu: np.ndarray, text_len: int, heads: int, weights_per_block, mods) -> np.ndarray:
+    """Blocks in order on the packed sequence, each one's output the next one's input (the DiT of
+    the paper is a stack of such blocks run on the compressed tokens, Sec. 2.2 / Sec. 3.3)."""
+    z = Z
+    for weights, mod in zip(weights_per_block, mods):
+        _, z = block(z, cu, text_len, heads, weights, mod)
+    return z
+
+
+def request(x_steps, x_txt, shape, force, r: int, mode: str, weights_per_block, mods, tau=None,
+            keep=None) -> Dict[str, object]:
+    """One editing request: the selection runs once, on step 0's latents (Sec. 2.3: it costs a few
+    milliseconds per request), then every sampling step (Sec. 3.3: 8 steps) compresses its own
+    latents with that selection, runs the block stack and decompresses.  mods[t][l] is block l's
+    modulation at step t.  Returns the selection and per step the packed input Z and the outputs."""
+    H, W = shape.grid_h, shape.grid_w
+    E = score(x_steps[0], H, W)
+    fine = select(E, force, H, W, r, mode, tau, keep)
+    idx_map, fine_idx, pool_idx, counts = compact(fine, H, W)
+    cu, seg = layout(counts, shape.batch, shape.images, shape.text_len)
+    out = dict(E=E, fine=fine, idx_map=idx_map, fine_idx=fine_idx, pool_idx=pool_idx, counts=counts, cu=cu,
+               seg=seg, Z=[], z=[], y_img=[], y_txt=[])
+    for t, x in enumerate(x_steps):
+        Z = compress(x, x_txt, H, W, fine_idx, pool_idx, counts, cu, seg, shape.text_len)
+        z = stack(Z, cu, shape.text_len, shape.heads, weights_per_block, mods[t])
+        y_img, y_txt = decompress(z, idx_map, cu, seg, shape.text_len, shape.batch)
+        out["Z"].append(Z)
+        out["z"].append(z)
+        out["y_img"].append(y_img)
+        out["y_txt"].append(y_txt)
+    return out
 
 
 def dense_sequence(x_img, x_txt, batch: int, images: int, text_len: int):

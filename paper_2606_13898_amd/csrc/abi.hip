@@ -245,17 +245,28 @@ hilo_status hilo_attention_core(const hilo_shape *s, const void *qkv, const int3
   }));
 }
 
-hilo_status hilo_attention(const hilo_shape *s, float *z, const int32_t *cu_seqlens,
-                           const hilo_attn_w w[2], const float *mod, void *workspace,
-                           size_t ws_bytes, void *stream) {
-  hilo_status e = check_block(s);
-  if (e != HILO_OK) return e;
-  if (!z || !cu_seqlens || !w || !mod || !workspace) return HILO_E_NULL;
+}  // extern "C"
+
+namespace {
+
+hilo_status check_attn_w(const hilo_attn_w *w) {
+  if (!w) return HILO_E_NULL;
   for (int k = 0; k < 2; ++k)
     if (!w[k].w_qkv || !w[k].b_qkv || !w[k].w_o || !w[k].b_o) return HILO_E_NULL;
-  if (ws_bytes < ws_attention(s)) return HILO_E_WORKSPACE;
-  if (!have_device()) return HILO_E_DEVICE;
-  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  return HILO_OK;
+}
+
+hilo_status check_mlp_w(const hilo_mlp_w *w) {
+  if (!w) return HILO_E_NULL;
+  for (int k = 0; k < 2; ++k)
+    if (!w[k].w1 || !w[k].b1 || !w[k].w2 || !w[k].b2) return HILO_E_NULL;
+  return HILO_OK;
+}
+
+// The attention half, arguments already validated.
+hilo_status enqueue_attention(const hilo_shape *s, float *z, const int32_t *cu_seqlens,
+                              const hilo_attn_w w[2], const float *mod, void *workspace,
+                              hipStream_t st) {
   const bool bf = s->dtype == HILO_BF16;
   const int D = s->dim;
   const int T = int(tmax_of(s));
@@ -295,17 +306,9 @@ hilo_status hilo_attention(const hilo_shape *s, float *z, const int32_t *cu_seql
   return dev_status(timed(K_GEMM_O, st, [&] { return launch_gemm(bf, GEMM_O, q, st); }));
 }
 
-hilo_status hilo_mlp(const hilo_shape *s, float *z, const int32_t *cu_seqlens,
-                     const hilo_mlp_w w[2], const float *mod, void *workspace, size_t ws_bytes,
-                     void *stream) {
-  hilo_status e = check_block(s);
-  if (e != HILO_OK) return e;
-  if (!z || !cu_seqlens || !w || !mod || !workspace) return HILO_E_NULL;
-  for (int k = 0; k < 2; ++k)
-    if (!w[k].w1 || !w[k].b1 || !w[k].w2 || !w[k].b2) return HILO_E_NULL;
-  if (ws_bytes < ws_mlp(s)) return HILO_E_WORKSPACE;
-  if (!have_device()) return HILO_E_DEVICE;
-  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+// The MLP half, arguments already validated.
+hilo_status enqueue_mlp(const hilo_shape *s, float *z, const int32_t *cu_seqlens,
+                        const hilo_mlp_w w[2], const float *mod, void *workspace, hipStream_t st) {
   const bool bf = s->dtype == HILO_BF16;
   const int D = s->dim, F = s->mlp_dim;
   const int T = int(tmax_of(s));
@@ -336,6 +339,57 @@ hilo_status hilo_mlp(const hilo_shape *s, float *z, const int32_t *cu_seqlens,
   q.N = D; q.K = F;
   q.z = z; q.ldz = D; q.gate_idx = 5;
   return dev_status(timed(K_GEMM_FC2, st, [&] { return launch_gemm(bf, GEMM_FC2, q, st); }));
+}
+
+}  // namespace
+
+extern "C" {
+
+hilo_status hilo_attention(const hilo_shape *s, float *z, const int32_t *cu_seqlens,
+                           const hilo_attn_w w[2], const float *mod, void *workspace,
+                           size_t ws_bytes, void *stream) {
+  hilo_status e = check_block(s);
+  if (e != HILO_OK) return e;
+  if (!z || !cu_seqlens || !mod || !workspace) return HILO_E_NULL;
+  if ((e = check_attn_w(w)) != HILO_OK) return e;
+  if (ws_bytes < ws_attention(s)) return HILO_E_WORKSPACE;
+  if (!have_device()) return HILO_E_DEVICE;
+  return enqueue_attention(s, z, cu_seqlens, w, mod, workspace, reinterpret_cast<hipStream_t>(stream));
+}
+
+hilo_status hilo_mlp(const hilo_shape *s, float *z, const int32_t *cu_seqlens,
+                     const hilo_mlp_w w[2], const float *mod, void *workspace, size_t ws_bytes,
+                     void *stream) {
+  hilo_status e = check_block(s);
+  if (e != HILO_OK) return e;
+  if (!z || !cu_seqlens || !mod || !workspace) return HILO_E_NULL;
+  if ((e = check_mlp_w(w)) != HILO_OK) return e;
+  if (ws_bytes < ws_mlp(s)) return HILO_E_WORKSPACE;
+  if (!have_device()) return HILO_E_DEVICE;
+  return enqueue_mlp(s, z, cu_seqlens, w, mod, workspace, reinterpret_cast<hipStream_t>(stream));
+}
+
+hilo_status hilo_blocks(const hilo_shape *s, float *z, const int32_t *cu_seqlens,
+                        const hilo_attn_w *attn_w, const hilo_mlp_w *mlp_w, const float *mod,
+                        int32_t n_blocks, void *workspace, size_t ws_bytes, void *stream) {
+  hilo_status e = check_block(s);
+  if (e != HILO_OK) return e;
+  if (n_blocks < 0) return HILO_E_PARAM;
+  if (!z || !cu_seqlens || !attn_w || !mlp_w || !mod || !workspace) return HILO_E_NULL;
+  for (int l = 0; l < n_blocks; ++l) {
+    if ((e = check_attn_w(attn_w + 2 * l)) != HILO_OK) return e;
+    if ((e = check_mlp_w(mlp_w + 2 * l)) != HILO_OK) return e;
+  }
+  if (ws_bytes < hilo_workspace_bytes(s)) return HILO_E_WORKSPACE;
+  if (!have_device()) return HILO_E_DEVICE;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  const size_t mod_stride = size_t(s->batch) * 2 * 6 * s->dim;
+  for (int l = 0; l < n_blocks; ++l) {
+    const float *ml = mod + l * mod_stride;
+    if ((e = enqueue_attention(s, z, cu_seqlens, attn_w + 2 * l, ml, workspace, st)) != HILO_OK) return e;
+    if ((e = enqueue_mlp(s, z, cu_seqlens, mlp_w + 2 * l, ml, workspace, st)) != HILO_OK) return e;
+  }
+  return HILO_OK;
 }
 
 hilo_status hilo_profile_enable(int32_t on) {

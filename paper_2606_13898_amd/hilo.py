@@ -55,6 +55,8 @@ _SIG = {
                        ctypes.c_size_t, _P],
     "hilo_mlp": [ctypes.POINTER(hilo_shape), _P, _P, ctypes.POINTER(hilo_mlp_w), _P, _P,
                  ctypes.c_size_t, _P],
+    "hilo_blocks": [ctypes.POINTER(hilo_shape), _P, _P, ctypes.POINTER(hilo_attn_w),
+                    ctypes.POINTER(hilo_mlp_w), _P, ctypes.c_int32, _P, ctypes.c_size_t, _P],
     "hilo_decompress": [ctypes.POINTER(hilo_shape), _P, _P, _P, _P, _P, _P, _P],
     "hilo_attention_core": [ctypes.POINTER(hilo_shape), _P, _P, _P, _P, ctypes.c_size_t, _P],
     "hilo_workspace_bytes": [ctypes.POINTER(hilo_shape)],
@@ -181,6 +183,27 @@ def hilo_mlp(shape, z, cu_seqlens, w, mod, workspace, stream=None):
     _check("hilo_mlp", lib().hilo_mlp(
         ctypes.byref(shape), _ptr(z), _ptr(cu_seqlens), w, _ptr(mod), _ptr(workspace),
         workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def stack_weights(blocks: Sequence[Sequence[dict]]):
+    """Host arrays [n_blocks][2] of attention and MLP weight pointers for hilo_blocks."""
+    n = len(blocks)
+    aw = (hilo_attn_w * (2 * n))()
+    mw = (hilo_mlp_w * (2 * n))()
+    for l, ws in enumerate(blocks):
+        for k in range(2):
+            aw[2 * l + k] = hilo_attn_w(_ptr(ws[k]["w_qkv"]), _ptr(ws[k]["b_qkv"]), _ptr(ws[k]["w_o"]),
+                                        _ptr(ws[k]["b_o"]))
+            mw[2 * l + k] = hilo_mlp_w(_ptr(ws[k]["w1"]), _ptr(ws[k]["b1"]), _ptr(ws[k]["w2"]),
+                                       _ptr(ws[k]["b2"]))
+    return aw, mw
+
+
+def hilo_blocks(shape, z, cu_seqlens, aw, mw, mod, n_blocks: int, workspace, stream=None):
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check("hilo_blocks", lib().hilo_blocks(
+        ctypes.byref(shape), _ptr(z), _ptr(cu_seqlens), aw, mw, _ptr(mod), n_blocks, _ptr(workspace),
+        ws_bytes, _stream(stream)))
 
 
 def hilo_decompress(shape, z, idx_map, cu_seqlens, seg_off, y_img, y_txt, stream=None):

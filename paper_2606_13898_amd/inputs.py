@@ -247,6 +247,42 @@ _SEED = {"tiny": 1001, "m1024": 1002, "h2048": 1003, "edit": 1004, "ragged": 100
          "small128": 2001, "small64": 2002, "smallf32": 2003}
 
 
+@dataclasses.dataclass
+class StackWorkload:
+    """One request in the paper's regime: the selection is computed once, from step 0's latents,
+    then each of `steps` sampling steps compresses that step's latents with it, runs `n_blocks`
+    blocks on the compressed sequence and decompresses.
+
+    base     Workload of step 0 (shape, x_txt, force, keep, dilate_r; its weights are block 0's)
+    x_steps  list of `steps` arrays [G][N][D] (x_steps[0] is base.x_img): each step's latents are
+             the previous step's plus N(0, 0.1) changes, stored in the shape's dtype
+    weights  list of `n_blocks` weight sets (block_weights)
+    mods     [steps][n_blocks][B][2][6][D] float32: the modulation of block l at step t
+    """
+
+    base: Workload
+    x_steps: List[np.ndarray]
+    weights: List[List[Dict[str, np.ndarray]]]
+    mods: np.ndarray
+
+
+def make_stack(name: str, n_blocks: int, steps: int, *, seed: Optional[int] = None,
+               shape: Optional[BlockShape] = None, keep_frac: Optional[float] = None) -> StackWorkload:
+    base = make_workload(name, seed=seed, shape=shape, keep_frac=keep_frac)
+    shp = base.shape
+    ss = np.random.SeedSequence((seed if seed is not None else _SEED.get(name, 3000)) + 7919)
+    c_w, c_mod, c_x = [np.random.default_rng(s) for s in ss.spawn(3)]
+    weights = [base.weights] + [block_weights(c_w, shp.dim, shp.mlp_dim, shp.dtype)
+                                for _ in range(n_blocks - 1)]
+    mods = np.stack([np.stack([modulation(c_mod, shp.batch, shp.dim) for _ in range(n_blocks)])
+                     for _ in range(steps)])
+    x_steps = [base.x_img]
+    for _ in range(steps - 1):
+        x_steps.append(_store(x_steps[-1] + c_x.normal(0.0, 0.1, size=x_steps[-1].shape).astype(np.float32),
+                              shp.dtype))
+    return StackWorkload(base, x_steps, weights, mods)
+
+
 def make_workload(name: str, *, with_block: bool = True, keep_frac: Optional[float] = None,
                   seed: Optional[int] = None, shape: Optional[BlockShape] = None) -> Workload:
     """Build the named workload.  `keep_frac` overrides the kept-fine block fraction of every grid

@@ -10,7 +10,7 @@ import numpy as np
 import torch
 
 from . import hilo
-from .inputs import Workload
+from .inputs import StackWorkload, Workload
 
 
 def _dev(a: np.ndarray, dtype: torch.dtype, device) -> torch.Tensor:
@@ -85,3 +85,41 @@ class DeviceBlock:
             self.attention(stream)
             self.mlp(stream)
         self.decompress(stream)
+
+
+class DeviceStack:
+    """One request of the paper's regime on the device: the selection once (from step 0's
+    latents), then per sampling step compress -> n_blocks blocks (hilo_blocks) -> decompress."""
+
+    def __init__(self, st: StackWorkload, device: str = "cuda"):
+        self.st = st
+        self.db = DeviceBlock(st.base, device, with_block=False)
+        db = self.db
+        self.x_steps = [_dev(x, db.dtype, device) for x in st.x_steps]
+        self.weights = [[{k: _dev(v, db.dtype, device) for k, v in w.items()} for w in ws] for ws in st.weights]
+        self.aw, self.mw = hilo.stack_weights(self.weights)
+        self.mods = _dev(st.mods, torch.float32, device)  # [steps][n_blocks][B][2][6][D]
+        self.n_blocks = len(st.weights)
+        self.ws = torch.empty(hilo.hilo_workspace_bytes(db.shape), dtype=torch.uint8, device=device)
+        self.y_img = [torch.empty_like(db.y_img) for _ in st.x_steps]
+        self.y_txt = [torch.empty_like(db.y_txt) if db.y_txt is not None else None for _ in st.x_steps]
+
+    def select(self, mode: int = hilo.TOPK, stream=None):
+        db = self.db
+        db.x_img = self.x_steps[0]
+        db.score(stream)
+        db.select(mode, stream=stream)
+
+    def step(self, t: int, stream=None):
+        db = self.db
+        hilo.hilo_compress(db.shape, self.x_steps[t], db.x_txt, db.fine_idx, db.pool_idx, db.counts,
+                           db.cu, db.seg, db.z, stream)
+        hilo.hilo_blocks(db.shape, db.z, db.cu, self.aw, self.mw, self.mods[t], self.n_blocks, self.ws,
+                         stream)
+        hilo.hilo_decompress(db.shape, db.z, db.idx_map, db.cu, db.seg, self.y_img[t], self.y_txt[t],
+                             stream)
+
+    def run(self, mode: int = hilo.TOPK, stream=None):
+        self.select(mode, stream)
+        for t in range(len(self.x_steps)):
+            self.step(t, stream)

@@ -23,9 +23,12 @@ def float_report(got, want):
     return max_abs, rel
 
 
-def assert_close(got, want, dtype, what=""):
+def assert_close(got, want, dtype, what="", blocks=1):
+    """`blocks` consecutive blocks: each adds at most one block's rounding error to a residual
+    stream it passes on with unit gain, so the bound is `blocks` times the one-block bound."""
     max_abs, rel = float_report(got, want)
     a, r = TOL[dtype]
+    a, r = a * blocks, r * blocks
     assert np.isfinite(np.asarray(got, dtype=np.float64)).all(), f"{what}: non-finite values"
     assert max_abs <= a and rel <= r, f"{what}: max_abs {max_abs:.3g} (<= {a}), rel_l2 {rel:.3g} (<= {r})"
     return max_abs, rel

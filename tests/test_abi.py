@@ -160,3 +160,26 @@ def test_binding_refuses_host_tensors():
     s = good_shape()
     with pytest.raises(ValueError):
         hilo.hilo_score(s, torch.zeros(4), torch.zeros(4))
+
+
+def test_blocks_validation():
+    """hilo_blocks checks every block's pointers and the count before enqueuing anything."""
+    s = good_shape()
+    L = hilo.lib()
+    need = hilo.hilo_workspace_bytes(s)
+    n = 3
+    aw = (hilo.hilo_attn_w * (2 * n))(*[hilo.hilo_attn_w(FAKE, FAKE, FAKE, FAKE)] * (2 * n))
+    mw = (hilo.hilo_mlp_w * (2 * n))(*[hilo.hilo_mlp_w(FAKE, FAKE, FAKE, FAKE)] * (2 * n))
+    assert L.hilo_blocks(ctypes.byref(s), FAKE, FAKE, aw, mw, FAKE, -1, FAKE, need, None) == 4
+    assert L.hilo_blocks(ctypes.byref(s), None, FAKE, aw, mw, FAKE, n, FAKE, need, None) == 1
+    assert L.hilo_blocks(ctypes.byref(s), FAKE, FAKE, None, mw, FAKE, n, FAKE, need, None) == 1
+    assert L.hilo_blocks(ctypes.byref(s), FAKE, FAKE, aw, mw, None, n, FAKE, need, None) == 1
+    assert L.hilo_blocks(ctypes.byref(s), FAKE, FAKE, aw, mw, FAKE, n, FAKE, need - 1, None) == 5
+    bad_aw = (hilo.hilo_attn_w * (2 * n))(*[hilo.hilo_attn_w(FAKE, FAKE, FAKE, FAKE)] * (2 * n))
+    bad_aw[5] = hilo.hilo_attn_w(FAKE, FAKE, None, FAKE)  # last block's text stream
+    assert L.hilo_blocks(ctypes.byref(s), FAKE, FAKE, bad_aw, mw, FAKE, n, FAKE, need, None) == 1
+    bad_mw = (hilo.hilo_mlp_w * (2 * n))(*[hilo.hilo_mlp_w(FAKE, FAKE, FAKE, FAKE)] * (2 * n))
+    bad_mw[2] = hilo.hilo_mlp_w(FAKE, FAKE, FAKE, None)
+    assert L.hilo_blocks(ctypes.byref(s), FAKE, FAKE, aw, bad_mw, FAKE, n, FAKE, need, None) == 1
+    s.heads, s.head_dim = 8, 32  # a head size the attention kernels do not take
+    assert L.hilo_blocks(ctypes.byref(s), FAKE, FAKE, aw, mw, FAKE, n, FAKE, need, None) == 3

@@ -7,7 +7,7 @@ import torch
 
 from oracle import hilo_oracle as O
 from paper_2606_13898_amd import hilo, inputs
-from paper_2606_13898_amd.pipeline import DeviceBlock
+from paper_2606_13898_amd.pipeline import DeviceBlock, DeviceStack
 
 from parity_util import assert_close, check_selection, midpoint_tau, oracle_for, to_np
 
@@ -237,3 +237,22 @@ def test_gemm_256_schedules(shp):
     T = int(ref["cu"][-1])
     assert_close(to_np(db.z)[:T], ref["z2"], "bf16", "z after block")
     assert_close(to_np(db.y_img), ref["y_img"], "bf16", "y_img")
+
+
+@pytest.mark.parametrize("name,n_blocks,steps", [("small128", 2, 2), ("small64", 3, 2)])
+def test_request_block_stack(name, n_blocks, steps):
+    """One request: selection once from step 0, then per step compress -> hilo_blocks (n_blocks
+    blocks) -> decompress; every step's outputs against the oracle's request loop."""
+    print(f"[parity] request {name} blocks={n_blocks} steps={steps}", flush=True)
+    st = inputs.make_stack(name, n_blocks, steps, seed=21)
+    ds = DeviceStack(st)
+    ds.run(hilo.TOPK)
+    torch.cuda.synchronize()
+    wl = st.base
+    ref = O.request(st.x_steps, wl.x_txt, wl.shape, wl.force, wl.dilate_r, "topk", st.weights, st.mods,
+                    keep=wl.keep)
+    check_selection(ds.db, ref)
+    dt = wl.shape.dtype
+    for t in range(steps):
+        assert_close(to_np(ds.y_img[t]), ref["y_img"][t], dt, f"{name} step {t} y_img", blocks=n_blocks)
+        assert_close(to_np(ds.y_txt[t]), ref["y_txt"][t], dt, f"{name} step {t} y_txt", blocks=n_blocks)
