@@ -106,6 +106,37 @@ def cpu_baseline(wl):
                       f"numpy, BLAS threads={threads}"}
 
 
+def token_set_leg(db, steps, warmup, stream, dense_ms):
+    """The whole step with the other token sets (same selection rule): overlap -- every block's
+    pooled token kept next to the fine patches, the paper's own token set (Sec. 2.3) -- and drop --
+    the fine patches alone (Sec. 3.2) -- both reassembled in the delta form; partition with the
+    delta form for comparison."""
+    import torch
+
+    from paper_2606_13898_amd import hilo
+
+    res = {}
+    for name, tokens in (("overlap", hilo.OVERLAP), ("drop", hilo.DROP), ("partition", hilo.PARTITION)):
+        for _ in range(warmup):
+            db.run(hilo.TOPK, tokens=tokens, delta=True)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(steps):
+            db.run(hilo.TOPK, tokens=tokens, delta=True)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / steps
+        nc = int(db.cu.cpu().numpy()[-1])
+        ent = {"ms_per_step": round(ms, 4), "compressed_tokens": nc, "decompress": "delta"}
+        if dense_ms:
+            ent["speedup_vs_dense"] = round(dense_ms / ms, 3)
+        res[name] = ent
+    db.run(hilo.TOPK)  # leave the buffers as the default step left them
+    torch.cuda.synchronize()
+    return res
+
+
 def stack_leg(db, wl, n_blocks, steps, stream, reps=3):
     """The paper's regime (Sec. 2.3, Sec. 3.3): one request = the selection once, then for each
     sampling step: compress that step's latents, run `n_blocks` blocks on the compressed tokens
@@ -199,6 +230,9 @@ def main():
     ap.add_argument("--no-stack", action="store_true",
                     help="skip the request leg (selection once, then per sampling step compress -> "
                          "a stack of blocks -> decompress, against the same stack on the dense tokens)")
+    ap.add_argument("--no-token-sets", action="store_true",
+                    help="skip the token-set leg (the step with every block's pooled token kept next "
+                         "to the fine patches, and with the fine patches alone)")
     ap.add_argument("--stack-blocks", type=int, default=8)
     ap.add_argument("--stack-steps", type=int, default=8)
     ap.add_argument("--copy-mib", type=int, default=0,
@@ -307,6 +341,11 @@ def main():
         n_dense = int(db.cu.cpu().numpy()[-1])
         dense = {"block_ms": round(dense_ms, 4), "tokens": n_dense}
 
+    token_sets = None
+    if not args.no_token_sets:
+        token_sets = token_set_leg(db, args.steps, args.warmup, stream,
+                                   dense["block_ms"] if dense else None)
+
     stack = None
     if not args.no_stack:
         stack = stack_leg(db, wl, args.stack_blocks, args.stack_steps, stream)
@@ -346,6 +385,8 @@ def main():
         out["speedup_vs_dense"] = round(dense["block_ms"] / ms, 3)
         out["block_speedup_vs_dense"] = round(dense["block_ms"] / t_blk, 3) if t_blk else None
         out["token_ratio"] = round(dense["tokens"] / nc, 3)
+    if token_sets:
+        out["token_sets"] = token_sets
     if stack:
         out["stack"] = stack
     if not args.no_cpu_baseline:

@@ -41,15 +41,15 @@
 extern "C" {
 #endif
 
-#define HILO_ABI_VERSION 1
+#define HILO_ABI_VERSION 2
 
 typedef enum {
   HILO_OK = 0,
   HILO_E_NULL = 1,      /* a required pointer is NULL                                        */
   HILO_E_SHAPE = 2,     /* grid not even/positive, dim != heads*head_dim, size limits (below) */
   HILO_E_DTYPE = 3,     /* dtype unknown, or head_dim unsupported for the dtype               */
-  HILO_E_PARAM = 4,     /* selection mode unknown, tau not finite, keep out of [0, NB],       */
-                        /* dilate_r negative                                                  */
+  HILO_E_PARAM = 4,     /* selection mode or token set unknown, tau not finite, keep out of   */
+                        /* [0, NB], dilate_r negative, n_blocks negative                      */
   HILO_E_WORKSPACE = 5, /* workspace smaller than hilo_workspace_bytes()                      */
   HILO_E_DEVICE = 6     /* a HIP launch failed, or no GPU                                     */
 } hilo_status;
@@ -57,6 +57,17 @@ typedef enum {
 typedef enum { HILO_F32 = 0, HILO_BF16 = 1 } hilo_dtype;
 
 typedef enum { HILO_SELECT_THRESHOLD = 0, HILO_SELECT_TOPK = 1 } hilo_select_mode;
+
+/* What a grid's compressed tokens are, besides the 4 fine patches of every kept block:
+ *   PARTITION  one pooled (low-frequency) token per block that is not kept: every patch is
+ *              represented exactly once (n_img = NB + 3 K)
+ *   OVERLAP    one pooled token per block, kept blocks included (Sec. 2.3: all low-frequency
+ *              tokens are retained and concatenated with the selected high-frequency tokens;
+ *              n_img = NB + 4 K)
+ *   DROP       nothing else (Sec. 3.2: for text-prompted generative fill the tokens outside the
+ *              dilated mask can be pruned entirely; n_img = 4 K) -- patches of other blocks have
+ *              no token (idx_map -1)                                                            */
+typedef enum { HILO_TOKENS_PARTITION = 0, HILO_TOKENS_OVERLAP = 1, HILO_TOKENS_DROP = 2 } hilo_token_set;
 
 /* Problem shape.  Limits (HILO_E_SHAPE otherwise): grid_h, grid_w even and > 0; N/4 <= 16384;
  * dim == heads * head_dim, dim % 64 == 0, dim <= 8192 (keeps energies exact in int64 and block
@@ -112,6 +123,16 @@ hilo_status hilo_select(const hilo_shape *shape, const int64_t *energy, const ui
                         int32_t *idx_map, int32_t *fine_idx, int32_t *pool_idx, int32_t *counts,
                         int32_t *cu_seqlens, int32_t *seg_off, void *stream);
 
+/* S2 with a token set (hilo_token_set; hilo_select is PARTITION).  The kept blocks are chosen as
+ * above.  OVERLAP: pool_idx[g][k] = k for all NB blocks, counts {4 |fine|, NB}, and idx_map of a
+ * patch in a kept block is its fine row, otherwise n_fine + its block.  DROP: counts
+ * {4 |fine|, 0}, idx_map -1 for patches outside kept blocks.  token_set unknown -> HILO_E_PARAM. */
+hilo_status hilo_select_tokens(const hilo_shape *shape, const int64_t *energy, const uint8_t *force,
+                               int32_t dilate_r, int32_t mode, const double *tau,
+                               const int32_t *keep, int32_t token_set, int32_t *idx_map,
+                               int32_t *fine_idx, int32_t *pool_idx, int32_t *counts,
+                               int32_t *cu_seqlens, int32_t *seg_off, void *stream);
+
 /* S3 -- compress (Sec. 2.3: selected high-frequency tokens concatenated with low-frequency tokens
  * along the token dimension).  Row seg_off[g] + k of z is x_img[g][fine_idx[g][k]] for k < n_fine
  * and ((x00 + x01) + (x10 + x11)) * 0.25 over the 4 patches of block pool_idx[g][k - n_fine]
@@ -155,10 +176,24 @@ hilo_status hilo_blocks(const hilo_shape *shape, float *z, const int32_t *cu_seq
 
 /* S6 -- decompress: y_img[g][p] = z[seg_off[g] + idx_map[g][p]] (fine tokens scatter back to
  * their patch, pooled tokens broadcast to the 4 patches of their block), y_txt[s][t] = the text
- * rows of sample s; both rounded to dtype.  y_img [G][N][D], y_txt [B][L][D] or NULL.           */
+ * rows of sample s; both rounded to dtype.  y_img [G][N][D], y_txt [B][L][D] or NULL.  A patch
+ * without a token (idx_map -1, token set DROP) gets zeros: use hilo_decompress_delta there.     */
 hilo_status hilo_decompress(const hilo_shape *shape, const float *z, const int32_t *idx_map,
                             const int32_t *cu_seqlens, const int32_t *seg_off, void *y_img,
                             void *y_txt, void *stream);
+
+/* S6, delta form (for the OVERLAP and DROP token sets): the block's change of a token is added to
+ * the patches it stands for, y_img[g][p] = x_img[g][p] + (z[row] - z0[row]) with row =
+ * seg_off[g] + idx_map[g][p] and z0[row] the value hilo_compress wrote there, recomputed from
+ * x_img with the same float32 operations (the patch itself for a fine row, the block mean
+ * ((x00 + x01) + (x10 + x11)) * 0.25 for a pooled row; a row is fine when idx_map < counts[g][0]).
+ * Patches without a token keep x_img.  A pooled token's update thus reaches its 4 patches on top
+ * of their own high-frequency detail instead of replacing them by the block mean.  Text rows as
+ * in hilo_decompress.  Float32 arithmetic, rounded to dtype once.                                */
+hilo_status hilo_decompress_delta(const hilo_shape *shape, const float *z, const void *x_img,
+                                  const int32_t *idx_map, const int32_t *counts,
+                                  const int32_t *cu_seqlens, const int32_t *seg_off, void *y_img,
+                                  void *y_txt, void *stream);
 
 /* The attention core alone (the softmax(q k^T / sqrt(hd)) v step of hilo_attention), for
  * localising parity failures and timing: qkv [T_max][3D] dtype -> out [T_max][D] dtype, rows of
@@ -169,7 +204,9 @@ hilo_status hilo_attention_core(const hilo_shape *shape, const void *qkv,
                                 size_t ws_bytes, void *stream);
 
 size_t hilo_workspace_bytes(const hilo_shape *shape); /* 0 if the shape is invalid */
-int64_t hilo_max_tokens(const hilo_shape *shape);     /* T_max, or -1 if invalid    */
+/* T_max = batch * (images * (N + N/4) + text_len): the most rows any token set can produce
+ * (OVERLAP with every block kept); z and the workspace are sized for it, -1 if invalid.         */
+int64_t hilo_max_tokens(const hilo_shape *shape);
 const char *hilo_status_str(int32_t status);
 int32_t hilo_abi_version(void);
 

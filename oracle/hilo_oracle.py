@@ -174,13 +174,22 @@ def select_topk(E: np.ndarray, force: Optional[np.ndarray], grid_h: int, grid_w:
     return fine
 
 
-def compact(fine: np.ndarray, grid_h: int, grid_w: int) -> Tuple[np.ndarray, ...]:
+TOKEN_SETS = ("partition", "overlap", "drop")
+
+
+def compact(fine: np.ndarray, grid_h: int, grid_w: int, tokens: str = "partition") -> Tuple[np.ndarray, ...]:
     """Index map of the compressed grid (Sec. 2.3: selected HF tokens are concatenated with the LF
     tokens along the token dimension).
 
     Per grid the compressed image tokens are [fine patches in raster order ; pooled blocks in block
-    raster order].  Returns
-      idx_map  [G][N]    compressed row of every patch (a fine patch's own row, else its block's row)
+    raster order].  Which blocks get a pooled (LF) token depends on the token set:
+      partition  the blocks that are not fine (every patch represented once)
+      overlap    every block (Sec. 2.3: all LF tokens are kept, next to the selected HF tokens)
+      drop       none (Sec. 3.2: for text-prompted fill the tokens outside the dilated mask can be
+                 pruned entirely); patches of other blocks then have no row (idx_map -1)
+    Returns
+      idx_map  [G][N]    compressed row of every patch (a fine patch's own row, else its block's row,
+                         or -1 without one)
       fine_idx [G][N]    patch index of compressed row k < n_fine (entries >= n_fine are -1)
       pool_idx [G][N/4]  block index of pooled row k < n_pool (rest -1)
       counts   [G][2]    (n_fine, n_pool)
@@ -192,16 +201,20 @@ def compact(fine: np.ndarray, grid_h: int, grid_w: int) -> Tuple[np.ndarray, ...
     fine_idx = np.full((G, N), -1, dtype=np.int32)
     pool_idx = np.full((G, NB), -1, dtype=np.int32)
     counts = np.empty((G, 2), dtype=np.int32)
+    if tokens not in TOKEN_SETS:
+        raise ValueError(tokens)
     for g in range(G):
         fine_patch = fine[g][blk]
         fp = np.flatnonzero(fine_patch)
-        pb = np.flatnonzero(~fine[g])
+        pooled = {"partition": ~fine[g], "overlap": np.ones(NB, dtype=bool), "drop": np.zeros(NB, dtype=bool)}[tokens]
+        pb = np.flatnonzero(pooled)
         n_fine, n_pool = fp.size, pb.size
         fine_idx[g, :n_fine] = fp
         pool_idx[g, :n_pool] = pb
         rank_fine = np.cumsum(fine_patch) - 1
-        rank_pool = np.cumsum(~fine[g]) - 1
-        idx_map[g] = np.where(fine_patch, rank_fine, n_fine + rank_pool[blk])
+        rank_pool = np.cumsum(pooled) - 1
+        other = np.where(pooled[blk], n_fine + rank_pool[blk], -1)
+        idx_map[g] = np.where(fine_patch, rank_fine, other)
         counts[g] = (n_fine, n_pool)
     return idx_map, fine_idx, pool_idx, counts
 
@@ -251,11 +264,26 @@ def compress(x_img: np.ndarray, x_txt: np.ndarray, grid_h: int, grid_w: int, fin
 
 
 def decompress(Z: np.ndarray, idx_map: np.ndarray, cu: np.ndarray, seg: np.ndarray,
-               text_len: int, batch: int) -> Tuple[np.ndarray, np.ndarray]:
-    """Reassemble the full grid: Y_img[g][p] = Z[seg[g] + idx_map[g][p]] (fine rows scatter back to
-    their patch, pooled rows broadcast to the 4 patches of their block); Y_txt = text rows."""
+               text_len: int, batch: int, x_img: Optional[np.ndarray] = None,
+               Z_in: Optional[np.ndarray] = None) -> Tuple[np.ndarray, np.ndarray]:
+    """Reassemble the full grid (the paper is silent on this step).
+
+    Broadcast form (Z_in None): Y_img[g][p] = Z[seg[g] + idx_map[g][p]] -- fine rows scatter back
+    to their patch, pooled rows broadcast to the 4 patches of their block; a patch without a row
+    gets zeros.  Delta form (x_img and Z_in, the sequence as compressed): Y_img[g][p] = x[g][p] +
+    (Z[row] - Z_in[row]) -- the block's change of the token is added to every patch it stands for;
+    a patch without a row keeps x.  Y_txt = the text rows of Z in both forms."""
     G, N = idx_map.shape
-    y_img = np.stack([Z[int(seg[g]) + idx_map[g].astype(np.int64)] for g in range(G)])
+    y_img = np.zeros((G, N, Z.shape[1]), dtype=np.float64)
+    for g in range(G):
+        has = idx_map[g] >= 0
+        rows = int(seg[g]) + idx_map[g][has].astype(np.int64)
+        if Z_in is None:
+            y_img[g][has] = Z[rows]
+        else:
+            x = x_img[g].astype(np.float64)
+            y_img[g] = x
+            y_img[g][has] = x[has] + (Z[rows] - Z_in[rows])
     y_txt = np.stack([Z[int(cu[s + 1]) - text_len:int(cu[s + 1])] for s in range(batch)])
     return y_img, y_txt
 
@@ -397,14 +425,16 @@ def select(E, force, grid_h, grid_w, r, mode: str, tau=None, keep=None) -> np.nd
 
 
 def pipeline(x_img, x_txt, shape, force, r: int, mode: str, tau=None, keep=None, weights=None,
-             mod=None, rows: Optional[np.ndarray] = None, with_block: bool = True) -> Dict[str, np.ndarray]:
+             mod=None, rows: Optional[np.ndarray] = None, with_block: bool = True,
+             tokens: str = "partition", delta: bool = False) -> Dict[str, np.ndarray]:
     """All six steps on one batch.  `shape` needs grid_h, grid_w, batch, images, text_len, heads.
     With `rows` the block is evaluated only for those packed rows (z1, z2 and y are then partial:
-    y_img / y_txt are not formed)."""
+    y_img / y_txt are not formed).  `tokens` picks the token set (compact), `delta` the delta form
+    of the reassembly (decompress)."""
     H, W = shape.grid_h, shape.grid_w
     E = score(x_img, H, W)
     fine = select(E, force, H, W, r, mode, tau, keep)
-    idx_map, fine_idx, pool_idx, counts = compact(fine, H, W)
+    idx_map, fine_idx, pool_idx, counts = compact(fine, H, W, tokens)
     cu, seg = layout(counts, shape.batch, shape.images, shape.text_len)
     Z = compress(x_img, x_txt, H, W, fine_idx, pool_idx, counts, cu, seg, shape.text_len)
     res = dict(E=E, fine=fine, idx_map=idx_map, fine_idx=fine_idx, pool_idx=pool_idx, counts=counts,
@@ -413,7 +443,8 @@ def pipeline(x_img, x_txt, shape, force, r: int, mode: str, tau=None, keep=None,
         z1, z2 = block(Z, cu, shape.text_len, shape.heads, weights, mod, rows)
         res.update(z1=z1, z2=z2)
         if rows is None:
-            y_img, y_txt = decompress(z2, idx_map, cu, seg, shape.text_len, shape.batch)
+            y_img, y_txt = decompress(z2, idx_map, cu, seg, shape.text_len, shape.batch,
+                                      x_img if delta else None, Z if delta else None)
             res.update(y_img=y_img, y_txt=y_txt)
     return res
 

@@ -67,7 +67,7 @@ hilo_status check_grid(const hilo_shape *s) {
   if (s->dim <= 0 || s->dim % 64 != 0 || s->dim > 8192) return HILO_E_SHAPE;
   const long long N = (long long)s->grid_h * s->grid_w;
   if (N / 4 > 16384) return HILO_E_SHAPE;
-  const long long tmax = (long long)s->batch * (s->images * N + s->text_len);
+  const long long tmax = (long long)s->batch * (s->images * (N + N / 4) + s->text_len);
   if (tmax >= (1LL << 31) / 8) return HILO_E_SHAPE;
   return HILO_OK;
 }
@@ -82,8 +82,15 @@ hilo_status check_block(const hilo_shape *s) {
   return HILO_OK;
 }
 
+// image rows per grid: at most every patch fine plus one pooled token per block (token set
+// "overlap"); partition and drop sets stay within N
+long long grid_rows_max(const hilo_shape *s) {
+  const long long N = (long long)s->grid_h * s->grid_w;
+  return N + N / 4;
+}
+
 long long tmax_of(const hilo_shape *s) {
-  return (long long)s->batch * ((long long)s->images * s->grid_h * s->grid_w + s->text_len);
+  return (long long)s->batch * ((long long)s->images * grid_rows_max(s) + s->text_len);
 }
 
 size_t esize(const hilo_shape *s) { return s->dtype == HILO_BF16 ? 2 : 4; }
@@ -115,7 +122,7 @@ GemmProblem base_problem(const hilo_shape *s, const int32_t *cu, const float *mo
   p.cu = cu;
   p.B = s->batch;
   p.L = s->text_len;
-  p.max_img_rows = s->images * s->grid_h * s->grid_w;
+  p.max_img_rows = int(s->images * grid_rows_max(s));
   return p;
 }
 
@@ -165,11 +172,23 @@ hilo_status hilo_select(const hilo_shape *s, const int64_t *energy, const uint8_
                         int32_t dilate_r, int32_t mode, const double *tau, const int32_t *keep,
                         int32_t *idx_map, int32_t *fine_idx, int32_t *pool_idx, int32_t *counts,
                         int32_t *cu_seqlens, int32_t *seg_off, void *stream) {
+  return hilo_select_tokens(s, energy, force, dilate_r, mode, tau, keep, HILO_TOKENS_PARTITION,
+                            idx_map, fine_idx, pool_idx, counts, cu_seqlens, seg_off, stream);
+}
+
+hilo_status hilo_select_tokens(const hilo_shape *s, const int64_t *energy, const uint8_t *force,
+                               int32_t dilate_r, int32_t mode, const double *tau,
+                               const int32_t *keep, int32_t token_set, int32_t *idx_map,
+                               int32_t *fine_idx, int32_t *pool_idx, int32_t *counts,
+                               int32_t *cu_seqlens, int32_t *seg_off, void *stream) {
   hilo_status e = check_grid(s);
   if (e != HILO_OK) return e;
   if (!energy || !idx_map || !fine_idx || !pool_idx || !counts || !cu_seqlens || !seg_off)
     return HILO_E_NULL;
   if (mode != HILO_SELECT_THRESHOLD && mode != HILO_SELECT_TOPK) return HILO_E_PARAM;
+  if (token_set != HILO_TOKENS_PARTITION && token_set != HILO_TOKENS_OVERLAP &&
+      token_set != HILO_TOKENS_DROP)
+    return HILO_E_PARAM;
   if (dilate_r < 0) return HILO_E_PARAM;
   const int G = s->batch * s->images;
   const int NB = s->grid_h * s->grid_w / 4;
@@ -187,7 +206,8 @@ hilo_status hilo_select(const hilo_shape *s, const int64_t *energy, const uint8_
   const int r = dilate_r > s->grid_h + s->grid_w ? s->grid_h + s->grid_w : dilate_r;
   hipError_t he = timed(K_SELECT, st, [&] {
     return launch_select(reinterpret_cast<const long long *>(energy), force, G, s->grid_h,
-                         s->grid_w, r, mode, tau, keep, idx_map, fine_idx, pool_idx, counts, st);
+                         s->grid_w, r, mode, token_set, tau, keep, idx_map, fine_idx, pool_idx,
+                         counts, st);
   });
   if (he != hipSuccess) return HILO_E_DEVICE;
   return dev_status(timed(K_LAYOUT, st, [&] {
@@ -228,6 +248,22 @@ hilo_status hilo_decompress(const hilo_shape *s, const float *z, const int32_t *
   }));
 }
 
+hilo_status hilo_decompress_delta(const hilo_shape *s, const float *z, const void *x_img,
+                                  const int32_t *idx_map, const int32_t *counts,
+                                  const int32_t *cu_seqlens, const int32_t *seg_off, void *y_img,
+                                  void *y_txt, void *stream) {
+  hilo_status e = check_grid(s);
+  if (e != HILO_OK) return e;
+  if (!z || !x_img || !idx_map || !counts || !cu_seqlens || !seg_off || !y_img) return HILO_E_NULL;
+  if (!have_device()) return HILO_E_DEVICE;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  return dev_status(timed(K_DECOMPRESS, st, [&] {
+    return launch_decompress_delta(s->dtype == HILO_BF16, z, x_img, idx_map, counts, cu_seqlens,
+                                   seg_off, y_img, s->text_len > 0 ? y_txt : nullptr, s->batch,
+                                   s->images, s->grid_h, s->grid_w, s->dim, s->text_len, st);
+  }));
+}
+
 hilo_status hilo_attention_core(const hilo_shape *s, const void *qkv, const int32_t *cu_seqlens,
                                 void *out, void *workspace, size_t ws_bytes, void *stream) {
   hilo_status e = check_block(s);
@@ -237,7 +273,7 @@ hilo_status hilo_attention_core(const hilo_shape *s, const void *qkv, const int3
   if (ws_bytes < ws_part(s)) return HILO_E_WORKSPACE;
   if (!have_device()) return HILO_E_DEVICE;
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  const int max_seq = s->images * s->grid_h * s->grid_w + s->text_len;
+  const int max_seq = int(s->images * grid_rows_max(s) + s->text_len);
   return dev_status(timed(K_ATTN_CORE, st, [&] {
     return launch_attention(s->dtype == HILO_BF16, qkv, cu_seqlens, out,
                             reinterpret_cast<float *>(workspace), s->batch, s->heads, s->head_dim,
@@ -290,7 +326,7 @@ hilo_status enqueue_attention(const hilo_shape *s, float *z, const int32_t *cu_s
   he = timed(K_GEMM_QKV, st, [&] { return launch_gemm(bf, GEMM_QKV, p, st); });
   if (he != hipSuccess) return HILO_E_DEVICE;
 
-  const int max_seq = s->images * s->grid_h * s->grid_w + s->text_len;
+  const int max_seq = int(s->images * grid_rows_max(s) + s->text_len);
   he = timed(K_ATTN_CORE, st, [&] {
     return launch_attention(bf, qkv, cu_seqlens, h, part, s->batch, s->heads, s->head_dim,
                             max_seq, st);

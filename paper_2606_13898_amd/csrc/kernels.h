@@ -13,9 +13,10 @@ constexpr int kSelMaxGrids = 64;  // grids per select launch (per-grid parameter
 hipError_t launch_score(bool bf16, const void *x, long long *E, int G, int H, int W, int D,
                         hipStream_t st);
 size_t select_lds_bytes(int NB);
+// tokens: 0 partition, 1 overlap, 2 drop (see k_select)
 hipError_t launch_select(const long long *E, const uint8_t *force, int G, int H, int W, int r,
-                         int mode, const double *tau, const int *keep, int *idx_map, int *fine_idx,
-                         int *pool_idx, int *counts, hipStream_t st);
+                         int mode, int tokens, const double *tau, const int *keep, int *idx_map,
+                         int *fine_idx, int *pool_idx, int *counts, hipStream_t st);
 hipError_t launch_layout(const int *counts, int B, int I, int L, int *cu, int *seg, hipStream_t st);
 
 hipError_t launch_compress(bool bf16, const void *x_img, const void *x_txt, const int *fine_idx,
@@ -24,6 +25,9 @@ hipError_t launch_compress(bool bf16, const void *x_img, const void *x_txt, cons
 hipError_t launch_decompress(bool bf16, const float *z, const int *idx_map, const int *cu,
                              const int *seg, void *y_img, void *y_txt, int B, int I, int N, int D,
                              int L, hipStream_t st);
+hipError_t launch_decompress_delta(bool bf16, const float *z, const void *x_img, const int *idx_map,
+                                   const int *counts, const int *cu, const int *seg, void *y_img,
+                                   void *y_txt, int B, int I, int H, int W, int D, int L, hipStream_t st);
 // h = LN(z) * (1 + mod[s][stream][which*3 + 1]) + mod[s][stream][which*3], rows < cu[B]
 hipError_t launch_rownorm(bool bf16, const float *z, const int *cu, const float *mod, int B, int L,
                           int D, int Tmax, int which, void *out, hipStream_t st);

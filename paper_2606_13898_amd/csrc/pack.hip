@@ -58,14 +58,15 @@ __global__ __launch_bounds__(kPackThreads) void k_compress(
 #pragma clang fp contract(off)
   const int CGn = D / 8;
   const int lane = threadIdx.x & 63;
-  const long long imgSlots = (long long)G * N;
+  const int R = N + N / 4;  // row slots per grid: at most N fine rows and N / 4 pooled ones
+  const long long imgSlots = (long long)G * R;
   const long long slot = (long long)blockIdx.x * kPackRows + (threadIdx.x >> 6);
   if (slot >= nslots) return;
   size_t dst, s0, s1 = 0, s2 = 0, s3 = 0;
   bool pooled = false;
   const void *src = x_img;
   if (slot < imgSlots) {
-    const int g = int(slot / N), k = int(slot % N);
+    const int g = int(slot / R), k = int(slot % R);
     const int nf = counts[2 * g], np = counts[2 * g + 1];
     if (k >= nf + np) return;
     dst = size_t(seg[g] + k);
@@ -113,7 +114,7 @@ hipError_t launch_compress(bool bf16, const void *x_img, const void *x_txt, cons
                            const int *pool_idx, const int *counts, const int *cu, const int *seg,
                            float *z, int B, int I, int H, int W, int D, int L, hipStream_t st) {
   const int G = B * I, N = H * W;
-  const long long nslots = (long long)G * N + (long long)B * L;
+  const long long nslots = (long long)G * (N + N / 4) + (long long)B * L;
   const long long nblk = (nslots + kPackRows - 1) / kPackRows;
   if (nblk <= 0) return hipSuccess;
   if (bf16)
@@ -140,9 +141,15 @@ __global__ __launch_bounds__(kPackThreads) void k_decompress(
   void *out;
   if (slot < imgSlots) {
     const int g = int(slot / N);
-    src = size_t(seg[g]) + size_t(idx_map[slot]);
+    const int idx = idx_map[slot];
     dst = size_t(slot);
     out = y_img;
+    if (idx < 0) {  // a dropped patch (token set "drop"): no token, zeros
+      const float f[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+      for (int cg = lane; cg < CGn; cg += 64) store8<BF16>(out, dst * D + size_t(cg) * 8, f);
+      return;
+    }
+    src = size_t(seg[g]) + size_t(idx);
   } else {
     if (!y_txt) return;
     const long long t = slot - imgSlots;
@@ -159,6 +166,87 @@ __global__ __launch_bounds__(kPackThreads) void k_decompress(
     float f[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
     store8<BF16>(out, dst * D + c, f);
   }
+}
+
+// Delta form: y[p] = x[p] + (z[row] - z0[row]) where z0 is what compress wrote to the row, rebuilt
+// here from x with the same float32 operations (the patch itself for a fine row; for a pooled row
+// ((x00 + x01) + (x10 + x11)) * 0.25 over its block); a patch without a token keeps x[p].  Text
+// rows are copied as in k_decompress.
+template <bool BF16>
+__global__ __launch_bounds__(kPackThreads) void k_decompress_delta(
+    const float *__restrict__ z, const void *__restrict__ x_img, const int *__restrict__ idx_map,
+    const int *__restrict__ counts, const int *__restrict__ cu, const int *__restrict__ seg,
+    void *__restrict__ y_img, void *__restrict__ y_txt, int G, int N, int W, int D, int L,
+    long long nslots) {
+#pragma clang fp contract(off)
+  const int CGn = D / 8;
+  const int lane = threadIdx.x & 63;
+  const long long imgSlots = (long long)G * N;
+  const long long slot = (long long)blockIdx.x * kPackRows + (threadIdx.x >> 6);
+  if (slot >= nslots) return;
+  if (slot >= imgSlots) {
+    if (!y_txt) return;
+    const long long t = slot - imgSlots;
+    const int s = int(t / L), j = int(t % L);
+    const size_t src = size_t(cu[s + 1] - L + j);
+    for (int cg = lane; cg < CGn; cg += 64) {
+      const size_t c = size_t(cg) * 8;
+      const float4 *q = reinterpret_cast<const float4 *>(z + src * D + c);
+      const float4 a = q[0], b = q[1];
+      float f[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+      store8<BF16>(y_txt, size_t(t) * D + c, f);
+    }
+    return;
+  }
+  const int g = int(slot / N), p = int(slot % N);
+  const int idx = idx_map[slot];
+  const int nf = counts[2 * g];
+  const size_t row = size_t(seg[g]) + size_t(idx < 0 ? 0 : idx);
+  const int i = p / W, j = p % W;
+  const size_t p00 = size_t(g) * N + size_t(i & ~1) * W + size_t(j & ~1);
+#pragma unroll 2
+  for (int cg = lane; cg < CGn; cg += 64) {
+    const size_t c = size_t(cg) * 8;
+    float x[8];
+    load8<BF16>(x_img, slot * size_t(D) + c, x);
+    if (idx >= 0) {
+      float z0[8];
+      if (idx < nf) {
+#pragma unroll
+        for (int v = 0; v < 8; ++v) z0[v] = x[v];
+      } else {
+        float a[8], b[8], e[8], f[8];
+        load8<BF16>(x_img, p00 * D + c, a);
+        load8<BF16>(x_img, (p00 + 1) * D + c, b);
+        load8<BF16>(x_img, (p00 + W) * D + c, e);
+        load8<BF16>(x_img, (p00 + W + 1) * D + c, f);
+#pragma unroll
+        for (int v = 0; v < 8; ++v) z0[v] = ((a[v] + b[v]) + (e[v] + f[v])) * 0.25f;
+      }
+      const float4 *q = reinterpret_cast<const float4 *>(z + row * D + c);
+      const float4 za = q[0], zb = q[1];
+      const float zz[8] = {za.x, za.y, za.z, za.w, zb.x, zb.y, zb.z, zb.w};
+#pragma unroll
+      for (int v = 0; v < 8; ++v) x[v] = x[v] + (zz[v] - z0[v]);
+    }
+    store8<BF16>(y_img, slot * size_t(D) + c, x);
+  }
+}
+
+hipError_t launch_decompress_delta(bool bf16, const float *z, const void *x_img, const int *idx_map,
+                                   const int *counts, const int *cu, const int *seg, void *y_img,
+                                   void *y_txt, int B, int I, int H, int W, int D, int L, hipStream_t st) {
+  const int G = B * I, N = H * W;
+  const long long nslots = (long long)G * N + (long long)B * L;
+  const long long nblk = (nslots + kPackRows - 1) / kPackRows;
+  if (nblk <= 0) return hipSuccess;
+  if (bf16)
+    hipLaunchKernelGGL(k_decompress_delta<true>, dim3(unsigned(nblk)), dim3(kPackThreads), 0, st, z,
+                       x_img, idx_map, counts, cu, seg, y_img, y_txt, G, N, W, D, L, nslots);
+  else
+    hipLaunchKernelGGL(k_decompress_delta<false>, dim3(unsigned(nblk)), dim3(kPackThreads), 0, st, z,
+                       x_img, idx_map, counts, cu, seg, y_img, y_txt, G, N, W, D, L, nslots);
+  return hipGetLastError();
 }
 
 hipError_t launch_decompress(bool bf16, const float *z, const int *idx_map, const int *cu,

@@ -176,9 +176,12 @@ struct SelChunk {
 };
 
 // flag bits per block: 1 = fine by score, 2 = forced by the dilated mask
+// token set (what the compressed grid holds besides the fine patches of the kept blocks):
+// 0 partition -- one pooled token per other block; 1 overlap -- one pooled token per block, kept
+// blocks included; 2 drop -- nothing else (patches of other blocks get idx_map -1)
 __global__ __launch_bounds__(kSelThreads) void k_select(
     const long long *__restrict__ E, const uint8_t *__restrict__ force, int H, int W, int r,
-    int mode, SelChunk prm, int g0, int *__restrict__ idx_map, int *__restrict__ fine_idx,
+    int mode, int tokens, SelChunk prm, int g0, int *__restrict__ idx_map, int *__restrict__ fine_idx,
     int *__restrict__ pool_idx, int *__restrict__ counts) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   const int gl = blockIdx.x;
@@ -301,13 +304,14 @@ __global__ __launch_bounds__(kSelThreads) void k_select(
   {
     const int chunk = (NB + kSelThreads - 1) / kSelThreads;
     const int b0 = tid * chunk, b1 = min(b0 + chunk, NB);
+    auto pooled = [&](int b) { return tokens == 1 || (tokens == 0 && !flag[b]); };
     int np = 0;
-    for (int b = b0; b < b1; ++b) np += flag[b] ? 0 : 1;
+    for (int b = b0; b < b1; ++b) np += pooled(b) ? 1 : 0;
     __syncthreads();  // every thread has read Bs-derived flags before prank overwrites Bs
     int ntot;
     int rk = block_excl_scan(np, itmp, ntot);
     for (int b = b0; b < b1; ++b) {
-      if (!flag[b]) {
+      if (pooled(b)) {
         prank[b] = rk;
         pool_idx[size_t(g) * NB + rk] = b;
         ++rk;
@@ -337,7 +341,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(
         im[p] = rk;
         ++rk;
       } else {
-        im[p] = nfine + prank[b];
+        im[p] = tokens == 2 ? -1 : nfine + prank[b];
       }
     }
     if (tid == 0) counts[2 * g] = nfine;
@@ -349,8 +353,8 @@ size_t select_lds_bytes(int NB) {
 }
 
 hipError_t launch_select(const long long *E, const uint8_t *force, int G, int H, int W, int r,
-                         int mode, const double *tau, const int *keep, int *idx_map, int *fine_idx,
-                         int *pool_idx, int *counts, hipStream_t st) {
+                         int mode, int tokens, const double *tau, const int *keep, int *idx_map,
+                         int *fine_idx, int *pool_idx, int *counts, hipStream_t st) {
   const int NB = H * W / 4;
   const size_t lds = select_lds_bytes(NB);
   for (int g0 = 0; g0 < G; g0 += kSelMaxGrids) {
@@ -360,8 +364,8 @@ hipError_t launch_select(const long long *E, const uint8_t *force, int G, int H,
       c.tau[k] = (mode == 0 && k < n) ? tau[g0 + k] : 0.0;
       c.keep[k] = (mode == 1 && k < n) ? keep[g0 + k] : 0;
     }
-    hipLaunchKernelGGL(k_select, dim3(n), dim3(kSelThreads), lds, st, E, force, H, W, r, mode, c,
-                       g0, idx_map, fine_idx, pool_idx, counts);
+    hipLaunchKernelGGL(k_select, dim3(n), dim3(kSelThreads), lds, st, E, force, H, W, r, mode, tokens,
+                       c, g0, idx_map, fine_idx, pool_idx, counts);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }

@@ -18,6 +18,7 @@ LIB_PATH = os.path.join(_PKG, "libhilo.so")
 
 F32, BF16 = 0, 1
 THRESHOLD, TOPK = 0, 1
+PARTITION, OVERLAP, DROP = 0, 1, 2  # hilo_token_set
 DTYPES = {"f32": F32, "bf16": BF16}
 TORCH_DTYPES = {F32: torch.float32, BF16: torch.bfloat16}
 
@@ -50,7 +51,11 @@ _SIG = {
     "hilo_select": [ctypes.POINTER(hilo_shape), _P, _P, ctypes.c_int32, ctypes.c_int32,
                     ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int32),
                     _P, _P, _P, _P, _P, _P, _P],
+    "hilo_select_tokens": [ctypes.POINTER(hilo_shape), _P, _P, ctypes.c_int32, ctypes.c_int32,
+                           ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int32),
+                           ctypes.c_int32, _P, _P, _P, _P, _P, _P, _P],
     "hilo_compress": [ctypes.POINTER(hilo_shape), _P, _P, _P, _P, _P, _P, _P, _P, _P],
+    "hilo_decompress_delta": [ctypes.POINTER(hilo_shape), _P, _P, _P, _P, _P, _P, _P, _P, _P],
     "hilo_attention": [ctypes.POINTER(hilo_shape), _P, _P, ctypes.POINTER(hilo_attn_w), _P, _P,
                        ctypes.c_size_t, _P],
     "hilo_mlp": [ctypes.POINTER(hilo_shape), _P, _P, ctypes.POINTER(hilo_mlp_w), _P, _P,
@@ -148,6 +153,24 @@ def hilo_select(shape, energy, force, dilate_r: int, mode: int, tau: Optional[Se
         ctypes.byref(shape), _ptr(energy), _ptr(force), int(dilate_r), int(mode), tau_arr, keep_arr,
         _ptr(idx_map), _ptr(fine_idx), _ptr(pool_idx), _ptr(counts), _ptr(cu_seqlens),
         _ptr(seg_off), _stream(stream)))
+
+
+def hilo_select_tokens(shape, energy, force, dilate_r: int, mode: int, tau: Optional[Sequence[float]],
+                       keep: Optional[Sequence[int]], token_set: int, idx_map, fine_idx, pool_idx, counts,
+                       cu_seqlens, seg_off, stream=None):
+    G = shape.batch * shape.images
+    tau_arr = (ctypes.c_double * G)(*[float(t) for t in tau]) if tau is not None else None
+    keep_arr = (ctypes.c_int32 * G)(*[int(k) for k in keep]) if keep is not None else None
+    _check("hilo_select_tokens", lib().hilo_select_tokens(
+        ctypes.byref(shape), _ptr(energy), _ptr(force), int(dilate_r), int(mode), tau_arr, keep_arr,
+        int(token_set), _ptr(idx_map), _ptr(fine_idx), _ptr(pool_idx), _ptr(counts), _ptr(cu_seqlens),
+        _ptr(seg_off), _stream(stream)))
+
+
+def hilo_decompress_delta(shape, z, x_img, idx_map, counts, cu_seqlens, seg_off, y_img, y_txt, stream=None):
+    _check("hilo_decompress_delta", lib().hilo_decompress_delta(
+        ctypes.byref(shape), _ptr(z), _ptr(x_img), _ptr(idx_map), _ptr(counts), _ptr(cu_seqlens),
+        _ptr(seg_off), _ptr(y_img), _ptr(y_txt), _stream(stream)))
 
 
 def hilo_compress(shape, x_img, x_txt, fine_idx, pool_idx, counts, cu_seqlens, seg_off, z,

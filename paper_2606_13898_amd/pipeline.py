@@ -56,11 +56,17 @@ class DeviceBlock:
         hilo.hilo_score(self.shape, self.x_img, self.energy, stream)
 
     def select(self, mode: int = hilo.TOPK, keep: Optional[Sequence[int]] = None,
-               tau: Optional[Sequence[float]] = None, dilate_r: Optional[int] = None, stream=None):
+               tau: Optional[Sequence[float]] = None, dilate_r: Optional[int] = None, stream=None,
+               tokens: int = hilo.PARTITION):
         keep = self.wl.keep if (keep is None and mode == hilo.TOPK) else keep
         r = self.wl.dilate_r if dilate_r is None else dilate_r
-        hilo.hilo_select(self.shape, self.energy, self.force, r, mode, tau, keep, self.idx_map,
-                         self.fine_idx, self.pool_idx, self.counts, self.cu, self.seg, stream)
+        if tokens == hilo.PARTITION:
+            hilo.hilo_select(self.shape, self.energy, self.force, r, mode, tau, keep, self.idx_map,
+                             self.fine_idx, self.pool_idx, self.counts, self.cu, self.seg, stream)
+        else:
+            hilo.hilo_select_tokens(self.shape, self.energy, self.force, r, mode, tau, keep, tokens,
+                                    self.idx_map, self.fine_idx, self.pool_idx, self.counts, self.cu,
+                                    self.seg, stream)
 
     def compress(self, stream=None):
         hilo.hilo_compress(self.shape, self.x_img, self.x_txt, self.fine_idx, self.pool_idx,
@@ -72,19 +78,24 @@ class DeviceBlock:
     def mlp(self, stream=None):
         hilo.hilo_mlp(self.shape, self.z, self.cu, self.mw, self.mod, self.ws, stream)
 
-    def decompress(self, stream=None):
-        hilo.hilo_decompress(self.shape, self.z, self.idx_map, self.cu, self.seg, self.y_img,
-                             self.y_txt, stream)
+    def decompress(self, stream=None, delta: bool = False):
+        if delta:
+            hilo.hilo_decompress_delta(self.shape, self.z, self.x_img, self.idx_map, self.counts, self.cu,
+                                       self.seg, self.y_img, self.y_txt, stream)
+        else:
+            hilo.hilo_decompress(self.shape, self.z, self.idx_map, self.cu, self.seg, self.y_img,
+                                 self.y_txt, stream)
 
-    def run(self, mode: int = hilo.TOPK, keep=None, tau=None, dilate_r=None, stream=None):
+    def run(self, mode: int = hilo.TOPK, keep=None, tau=None, dilate_r=None, stream=None,
+            tokens: int = hilo.PARTITION, delta: bool = False):
         """One pass of the whole hot path: score, select, compress, attention, MLP, decompress."""
         self.score(stream)
-        self.select(mode, keep, tau, dilate_r, stream)
+        self.select(mode, keep, tau, dilate_r, stream, tokens)
         self.compress(stream)
         if self.with_block:
             self.attention(stream)
             self.mlp(stream)
-        self.decompress(stream)
+        self.decompress(stream, delta)
 
 
 class DeviceStack:

@@ -31,7 +31,7 @@ def test_exports_every_declared_symbol():
 
 
 def test_version_and_status_strings():
-    assert hilo.hilo_abi_version() == 1
+    assert hilo.hilo_abi_version() == 2
     for st in range(7):
         assert hilo.status_str(st)
     assert hilo.status_str(99) == "unknown status"
@@ -43,8 +43,8 @@ def good_shape(dtype=hilo.BF16):
 
 def test_max_tokens_and_workspace():
     s = good_shape()
-    assert hilo.hilo_max_tokens(s) == 2 * (80 + 5)
-    T = 170
+    assert hilo.hilo_max_tokens(s) == 2 * (80 + 20 + 5)  # every patch fine plus a pooled token per block
+    T = 210
     part = 256 * 3 * 256 * 256 * 4  # GEMM partial tiles: 3 slots of 256 x 256 fp32 per CU, at most 256 CUs
     want = max(-(-T * 256 * 2 // 256) * 256 + -(-T * 768 * 2 // 256) * 256,
                -(-T * 256 * 2 // 256) * 256 + -(-T * 1024 * 2 // 256) * 256) + part
@@ -183,3 +183,16 @@ def test_blocks_validation():
     assert L.hilo_blocks(ctypes.byref(s), FAKE, FAKE, aw, bad_mw, FAKE, n, FAKE, need, None) == 1
     s.heads, s.head_dim = 8, 32  # a head size the attention kernels do not take
     assert L.hilo_blocks(ctypes.byref(s), FAKE, FAKE, aw, mw, FAKE, n, FAKE, need, None) == 3
+
+
+def test_select_tokens_validation():
+    s = good_shape()
+    L = hilo.lib()
+    G = 2
+    keep = (ctypes.c_int32 * G)(1, 2)
+    args = lambda tset: (ctypes.byref(s), FAKE, None, 0, hilo.TOPK, None, keep, tset, FAKE, FAKE, FAKE, FAKE,
+                         FAKE, FAKE, None)
+    assert L.hilo_select_tokens(*args(3)) == 4
+    assert L.hilo_select_tokens(*args(-1)) == 4
+    assert L.hilo_decompress_delta(ctypes.byref(s), FAKE, None, FAKE, FAKE, FAKE, FAKE, FAKE, None, None) == 1
+    assert L.hilo_decompress_delta(ctypes.byref(s), FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE, None, None) == 1

@@ -256,3 +256,27 @@ def test_request_block_stack(name, n_blocks, steps):
     for t in range(steps):
         assert_close(to_np(ds.y_img[t]), ref["y_img"][t], dt, f"{name} step {t} y_img", blocks=n_blocks)
         assert_close(to_np(ds.y_txt[t]), ref["y_txt"][t], dt, f"{name} step {t} y_txt", blocks=n_blocks)
+
+
+TOKEN_SET = {"overlap": hilo.OVERLAP, "drop": hilo.DROP}
+
+
+@pytest.mark.parametrize("name,tokens,delta", [
+    ("small128", "overlap", False), ("small128", "overlap", True), ("small64", "overlap", True),
+    ("small64", "drop", True), ("small64", "drop", False), ("smallf32", "overlap", True),
+])
+def test_token_sets(name, tokens, delta):
+    """Every block's low-frequency token next to the kept fine patches (overlap), or the kept fine
+    patches alone (drop), reassembled by broadcast or by the delta form."""
+    print(f"[parity] token set {tokens} delta={delta} workload={name}", flush=True)
+    wl = inputs.make_workload(name)
+    db = DeviceBlock(wl)
+    ref = oracle_for(wl, tokens=tokens, delta=delta)
+    db.run(hilo.TOPK, tokens=TOKEN_SET[tokens], delta=delta)
+    torch.cuda.synchronize()
+    check_selection(db, ref)
+    dt = wl.shape.dtype
+    T = int(ref["cu"][-1])
+    assert_close(to_np(db.z)[:T], ref["z2"], dt, f"{name} {tokens} z2")
+    assert_close(to_np(db.y_img), ref["y_img"], dt, f"{name} {tokens} y_img")
+    assert_close(to_np(db.y_txt), ref["y_txt"], dt, f"{name} {tokens} y_txt")
