@@ -106,6 +106,44 @@ def cpu_baseline(wl):
                       f"numpy, BLAS threads={threads}"}
 
 
+def pixel_leg(db, steps, warmup, stream):
+    """The paper's own selector input: Sobel on the RGB image at 16x the token grid (1024 x 1024
+    pixels for the 64 x 64 grid), summed per token (hilo_score_pixels), then its threshold 0.1 on
+    the normalised map.  The image is synthetic (inputs.pixel_image).  HBM-bound: one read of the
+    image plus the 8-byte energies."""
+    import numpy as np
+    import torch
+
+    from paper_2606_13898_amd import hilo, inputs
+
+    s = db.wl.shape
+    G, N = s.grids, s.n_patches
+    rgb = torch.from_numpy(inputs.pixel_image(s, 5)).cuda()
+    E = torch.empty(G, N, dtype=torch.int64, device="cuda")
+    for _ in range(warmup):
+        hilo.hilo_score_pixels(db.shape, rgb, E)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(steps):
+        hilo.hilo_score_pixels(db.shape, rgb, E)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    nbytes = rgb.numel() * 4 + E.numel() * 8
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    db.energy.copy_(E)
+    db.select(hilo.THRESHOLD, tau=[0.1] * G)
+    counts = db.counts.cpu().numpy()
+    res = {"ms": round(ms, 4), "image": f"{G}x3x{16 * s.grid_h}x{16 * s.grid_w} float32",
+           "achieved": round(gbs, 1), "unit": "GB/s", "peak": 8000.0, "frac": round(gbs / 8000.0, 4),
+           "work_per_launch": f"{nbytes / 1e9:.4g} GB",
+           "kept_fine_fraction_tau_0.1": round(float(counts[:, 0].sum()) / (G * N), 4)}
+    db.run(hilo.TOPK)  # leave the buffers as the default step left them
+    torch.cuda.synchronize()
+    return res
+
+
 def token_set_leg(db, steps, warmup, stream, dense_ms):
     """The whole step with the other token sets (same selection rule): overlap -- every block's
     pooled token kept next to the fine patches, the paper's own token set (Sec. 2.3) -- and drop --
@@ -233,6 +271,8 @@ def main():
     ap.add_argument("--no-token-sets", action="store_true",
                     help="skip the token-set leg (the step with every block's pooled token kept next "
                          "to the fine patches, and with the fine patches alone)")
+    ap.add_argument("--no-pixel-score", action="store_true",
+                    help="skip the pixel-space scorer leg (Sobel on the 16x-resolution RGB image)")
     ap.add_argument("--stack-blocks", type=int, default=8)
     ap.add_argument("--stack-steps", type=int, default=8)
     ap.add_argument("--copy-mib", type=int, default=0,
@@ -346,6 +386,10 @@ def main():
         token_sets = token_set_leg(db, args.steps, args.warmup, stream,
                                    dense["block_ms"] if dense else None)
 
+    pixel = None
+    if not args.no_pixel_score:
+        pixel = pixel_leg(db, args.steps, args.warmup, stream)
+
     stack = None
     if not args.no_stack:
         stack = stack_leg(db, wl, args.stack_blocks, args.stack_steps, stream)
@@ -387,6 +431,8 @@ def main():
         out["token_ratio"] = round(dense["tokens"] / nc, 3)
     if token_sets:
         out["token_sets"] = token_sets
+    if pixel:
+        out["pixel_score"] = pixel
     if stack:
         out["stack"] = stack
     if not args.no_cpu_baseline:

@@ -105,6 +105,14 @@ typedef struct {
  * x_img [G][N][D] dtype  ->  energy [G][N] int64.                                               */
 hilo_status hilo_score(const hilo_shape *shape, const void *x_img, int64_t *energy, void *stream);
 
+/* S1 in pixel space (the paper's own selector input, Sec. 2.3: Sobel on the image, 16x pooling
+ * onto the token grid).  rgb: DEVICE float32 [G][3][16 grid_h][16 grid_w] (planar channels, any
+ * value range).  For every pixel and channel the energy and fixed point of hilo_score (same
+ * formulas, neighbours clamped to the image), summed exactly over the token's 16 x 16 pixels and 3
+ * channels: energy [G][N] int64, ready for hilo_select (e.g. THRESHOLD with tau = 0.1, the
+ * paper's value).  HILO_E_SHAPE if the image has 2^31 or more values.                           */
+hilo_status hilo_score_pixels(const hilo_shape *shape, const float *rgb, int64_t *energy, void *stream);
+
 /* S2 -- selection (Sec. 2.3: 16x regional pooling of the frequency map onto the token grid,
  * threshold on the normalised map, dilated user mask combined with the selection).
  *   B_b  = sum of the 4 energies of block b (exact);  E_max = max_p energy[g][p]

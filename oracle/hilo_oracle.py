@@ -10,6 +10,8 @@ paper's description of HiLo-Token selection (Sec. 2.3, "HiLo-Token Selection"), 
 diffusion-transformer block on the shortened sequence and the reassembly of the full grid:
 
   score      Sobel frequency energy per latent patch              (Sec. 2.3, Sobel operators)
+  score_pixels  the same energy on the RGB image, summed over each  (Sec. 2.3, Sobel on the image,
+             token's 16 x 16 pixels                                 16x pooling to the token grid)
   select     2x2 regional pooling, threshold or top-k, dilated    (Sec. 2.3, regionalisation +
              user mask forced fine                                  dilated mask; Sec. 1)
   compact    index map: fine patches, pooled blocks, their ranks   (Sec. 2.3, token-dim concat)
@@ -31,8 +33,8 @@ Readings of the paper where it is silent or loose are listed in the design notes
 below states the reading it implements.
 
 Parity status per function (what pins it is in tests/test_oracle_*.py):
-  score, dilate, block_sums, select_*, compact, layout, compress, decompress, attention, mlp,
-  stack, request:
+  score, score_pixels, dilate, block_sums, select_*, compact, layout, compress, decompress,
+  attention, mlp, stack, request:
   pinned by closed forms, library routines (scipy Sobel / binary dilation, torch SDPA / layer_norm
   / gelu), hand-worked fixtures under tests/golden/, and the identities of the method (0% compression
   equals the dense block, pooling a constant block then broadcasting is lossless, kept-token count
@@ -88,6 +90,25 @@ def score(x_img: np.ndarray, grid_h: int, grid_w: int) -> np.ndarray:
         q = np.floor(np.fmin(v, CAP) * SCALE).astype(np.int64)  # fmin: a NaN energy takes the cap
         E[g] = q.sum(axis=-1, dtype=np.int64).reshape(N)
     return E
+
+
+PIX_PER_TOKEN = 16  # image pixels per token side: 8x VAE x 2x patch embedding (Sec. 2.3)
+
+
+def score_pixels(rgb: np.ndarray, grid_h: int, grid_w: int) -> np.ndarray:
+    """Per-token frequency energy from the image itself, the paper's selector (Sec. 2.3: Sobel
+    operators on the image, then 16x spatial pooling onto the token grid).  The per-pixel energy is
+    `score`'s (float32 per operation, capped, 2^-16 fixed point, replicated border) on the pixel
+    grid with the 3 colour channels as channels; a token's energy is the exact sum over its 16 x 16
+    pixels (a sum rather than a mean: the normalisation by the maximum cancels the factor).
+
+    rgb [G][3][16 grid_h][16 grid_w] float32  ->  E [G][grid_h * grid_w] int64"""
+    rgb = np.asarray(rgb, dtype=np.float32)
+    G, C, Hp, Wp = rgb.shape
+    T = PIX_PER_TOKEN
+    assert Hp == T * grid_h and Wp == T * grid_w
+    per_pixel = score(rgb.transpose(0, 2, 3, 1).reshape(G, Hp * Wp, C), Hp, Wp)
+    return per_pixel.reshape(G, grid_h, T, grid_w, T).sum(axis=(2, 4), dtype=np.int64).reshape(G, grid_h * grid_w)
 
 
 # ------------------------------------------------------------------------------------------------

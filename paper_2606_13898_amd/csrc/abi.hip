@@ -168,6 +168,19 @@ hilo_status hilo_score(const hilo_shape *s, const void *x_img, int64_t *energy, 
   }));
 }
 
+hilo_status hilo_score_pixels(const hilo_shape *s, const float *rgb, int64_t *energy, void *stream) {
+  hilo_status e = check_grid(s);
+  if (e != HILO_OK) return e;
+  if (!rgb || !energy) return HILO_E_NULL;
+  if ((long long)s->grid_h * 16 * s->grid_w * 16 * 3 * s->batch * s->images >= (1LL << 31)) return HILO_E_SHAPE;
+  if (!have_device()) return HILO_E_DEVICE;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  return dev_status(timed(K_SCORE, st, [&] {
+    return launch_score_pixels(rgb, reinterpret_cast<long long *>(energy), s->batch * s->images,
+                               s->grid_h, s->grid_w, st);
+  }));
+}
+
 hilo_status hilo_select(const hilo_shape *s, const int64_t *energy, const uint8_t *force,
                         int32_t dilate_r, int32_t mode, const double *tau, const int32_t *keep,
                         int32_t *idx_map, int32_t *fine_idx, int32_t *pool_idx, int32_t *counts,

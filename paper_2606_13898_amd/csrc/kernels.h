@@ -12,6 +12,8 @@ constexpr int kSelMaxGrids = 64;  // grids per select launch (per-grid parameter
 
 hipError_t launch_score(bool bf16, const void *x, long long *E, int G, int H, int W, int D,
                         hipStream_t st);
+// rgb [G][3][16 H][16 W] float32 -> E [G][H * W]: per-token pixel-space Sobel energy
+hipError_t launch_score_pixels(const float *rgb, long long *E, int G, int H, int W, hipStream_t st);
 size_t select_lds_bytes(int NB);
 // tokens: 0 partition, 1 overlap, 2 drop (see k_select)
 hipError_t launch_select(const long long *E, const uint8_t *force, int G, int H, int W, int r,

@@ -127,6 +127,57 @@ hipError_t launch_score(bool bf16, const void *x, long long *E, int G, int H, in
   return hipGetLastError();
 }
 
+// Pixel-space score (the paper's own selector input, Sec. 2.3): Sobel on each channel of the RGB
+// image, with the per-pixel float32 energy, cap and 2^-16 fixed point of k_score, summed exactly
+// over the 16 x 16 pixels and 3 channels of a token (the 16x pooling onto the token grid; the
+// normalisation by the maximum cancels the 1/256 of a mean).  One workgroup per token: each
+// channel's 18 x 18 pixel tile (token plus a one-pixel ring, replicated at the image edge) goes
+// through LDS, one thread per pixel.
+constexpr int kPixPerTok = 16;
+
+__global__ __launch_bounds__(256) void k_score_pixels(const float *__restrict__ rgb,
+                                                      long long *__restrict__ E, int H, int W) {
+#pragma clang fp contract(off)
+  constexpr int T = kPixPerTok, TT = T + 2;
+  __shared__ float tile[TT][TT + 1];
+  __shared__ long long red[4];
+  const int Hp = H * T, Wp = W * T;
+  const int tok = xcd_remap(blockIdx.x, gridDim.x);
+  const int g = tok / (H * W), rem = tok - g * (H * W), ti = rem / W, tj = rem - ti * W;
+  const int ty = threadIdx.x / T, tx = threadIdx.x % T;
+  const int y = ty + 1, x = tx + 1;
+  double acc = 0.0;  // integers < 2^38 each, three of them: exact
+  for (int c = 0; c < 3; ++c) {
+    const float *plane = rgb + (size_t(g) * 3 + c) * size_t(Hp) * Wp;
+    for (int e = threadIdx.x; e < TT * TT; e += 256) {
+      const int ly = e / TT, lx = e - ly * TT;
+      const int py = min(max(ti * T + ly - 1, 0), Hp - 1), px = min(max(tj * T + lx - 1, 0), Wp - 1);
+      tile[ly][lx] = plane[size_t(py) * Wp + px];
+    }
+    __syncthreads();
+    const float gx = ((tile[y - 1][x + 1] + 2.0f * tile[y][x + 1]) + tile[y + 1][x + 1]) -
+                     ((tile[y - 1][x - 1] + 2.0f * tile[y][x - 1]) + tile[y + 1][x - 1]);
+    const float gy = ((tile[y + 1][x - 1] + 2.0f * tile[y + 1][x]) + tile[y + 1][x + 1]) -
+                     ((tile[y - 1][x - 1] + 2.0f * tile[y - 1][x]) + tile[y - 1][x + 1]);
+    const float t1 = gx * gx;
+    const float t2 = gy * gy;
+    const float e = t1 + t2;
+    acc += double(floorf(fminf(e, 4194304.0f) * 65536.0f));  // fminf(NaN, cap) = cap
+    __syncthreads();  // the tile is refilled for the next channel
+  }
+  const long long s = wave_sum_i64(static_cast<long long>(acc));
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s;
+  __syncthreads();
+  if (threadIdx.x == 0) E[tok] = (red[0] + red[1]) + (red[2] + red[3]);
+}
+
+hipError_t launch_score_pixels(const float *rgb, long long *E, int G, int H, int W, hipStream_t st) {
+  const long long nblk = (long long)G * H * W;
+  if (nblk <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_score_pixels, dim3(unsigned(nblk)), dim3(256), 0, st, rgb, E, H, W);
+  return hipGetLastError();
+}
+
 // ------------------------------------------------------------------------------------------ S2
 
 constexpr int kSelThreads = 1024;

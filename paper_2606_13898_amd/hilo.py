@@ -48,6 +48,7 @@ _lib = None
 _P = ctypes.c_void_p
 _SIG = {
     "hilo_score": [ctypes.POINTER(hilo_shape), _P, _P, _P],
+    "hilo_score_pixels": [ctypes.POINTER(hilo_shape), _P, _P, _P],
     "hilo_select": [ctypes.POINTER(hilo_shape), _P, _P, ctypes.c_int32, ctypes.c_int32,
                     ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int32),
                     _P, _P, _P, _P, _P, _P, _P],
@@ -141,6 +142,11 @@ def hilo_workspace_bytes(shape: hilo_shape) -> int:
 def hilo_score(shape, x_img, energy, stream=None):
     _check("hilo_score", lib().hilo_score(ctypes.byref(shape), _ptr(x_img), _ptr(energy),
                                           _stream(stream)))
+
+
+def hilo_score_pixels(shape, rgb, energy, stream=None):
+    _check("hilo_score_pixels", lib().hilo_score_pixels(ctypes.byref(shape), _ptr(rgb), _ptr(energy),
+                                                        _stream(stream)))
 
 
 def hilo_select(shape, energy, force, dilate_r: int, mode: int, tau: Optional[Sequence[float]],

@@ -247,6 +247,29 @@ _SEED = {"tiny": 1001, "m1024": 1002, "h2048": 1003, "edit": 1004, "ragged": 100
          "small128": 2001, "small64": 2002, "smallf32": 2003}
 
 
+def pixel_image(shape: BlockShape, seed: int) -> np.ndarray:
+    """A synthetic RGB image of the token grid's size, planar float32 [G][3][16 H][16 W]: per
+    channel a smooth degree-3 polynomial background (values around 0.5) plus N(0, 0.15) pixel
+    noise inside 1-3 seeded regions covering ~35% of the image (the textured, high-frequency
+    areas), the stand-in for the paper's input images."""
+    rng = np.random.default_rng(seed)
+    T = 16
+    G, h, w = shape.grids, shape.grid_h, shape.grid_w
+    Hp, Wp = h * T, w * T
+    img = np.empty((G, 3, Hp, Wp), dtype=np.float32)
+    u, v = _coords(Hp, Wp)
+    basis = np.stack([u ** a * v ** b for a in range(4) for b in range(4 - a)], axis=0).astype(np.float32)
+    for g in range(G):
+        reg = region_mask(rng, h, w, 0.35, 0.10, 1, 3)
+        reg_px = np.repeat(np.repeat(reg, T, axis=0), T, axis=1)
+        for c in range(3):
+            alpha = rng.normal(0.0, 0.1, size=basis.shape[0]).astype(np.float32)
+            field = 0.5 + np.tensordot(alpha, basis, axes=1)
+            field += np.where(reg_px, rng.normal(0.0, 0.15, size=(Hp, Wp)), 0.0).astype(np.float32)
+            img[g, c] = field
+    return img
+
+
 @dataclasses.dataclass
 class StackWorkload:
     """One request in the paper's regime: the selection is computed once, from step 0's latents,

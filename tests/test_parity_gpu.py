@@ -280,3 +280,35 @@ def test_token_sets(name, tokens, delta):
     assert_close(to_np(db.z)[:T], ref["z2"], dt, f"{name} {tokens} z2")
     assert_close(to_np(db.y_img), ref["y_img"], dt, f"{name} {tokens} y_img")
     assert_close(to_np(db.y_txt), ref["y_txt"], dt, f"{name} {tokens} y_txt")
+
+
+@pytest.mark.parametrize("shp", [
+    inputs.BlockShape(1, 1, 8, 10, 0, 64, 1, 64, 256, "f32"),
+    inputs.BlockShape(2, 2, 16, 20, 8, 64, 1, 64, 256, "bf16"),
+    inputs.BlockShape(1, 1, 64, 64, 512, 3072, 24, 128, 12288, "bf16"),  # the 1024 px image
+], ids=["8x10", "batch2x2_16x20", "1024px"])
+def test_pixel_score_and_paper_threshold(shp):
+    """Sobel on the RGB image summed per token (bit for bit), then the paper's threshold 0.1 on the
+    normalised map selects the same blocks as the oracle."""
+    print(f"[parity] pixel score {shp.grid_h}x{shp.grid_w} grids={shp.grids}", flush=True)
+    rgb = inputs.pixel_image(shp, 41)
+    H, W, G, N = shp.grid_h, shp.grid_w, shp.grids, shp.n_patches
+    want = O.score_pixels(rgb, H, W)
+    shape = hilo.make_shape(shp)
+    rgb_d = torch.from_numpy(rgb).cuda()
+    E = torch.empty(G, N, dtype=torch.int64, device="cuda")
+    hilo.hilo_score_pixels(shape, rgb_d, E)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(to_np(E), want)
+    tau = [0.1] * G
+    fine = O.select(want, None, H, W, 0, "threshold", tau=tau)
+    idx_map, _, _, counts = O.compact(fine, H, W)
+    i32 = dict(dtype=torch.int32, device="cuda")
+    im, fi = torch.empty(G, N, **i32), torch.empty(G, N, **i32)
+    pi, cnt = torch.empty(G, N // 4, **i32), torch.empty(G, 2, **i32)
+    cu, seg = torch.empty(shp.batch + 1, **i32), torch.empty(G, **i32)
+    hilo.hilo_select(shape, E, None, 0, hilo.THRESHOLD, tau, None, im, fi, pi, cnt, cu, seg)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(to_np(cnt), counts)
+    np.testing.assert_array_equal(to_np(im), idx_map)
+    assert 0 < counts[:, 0].sum() < G * N
