@@ -509,8 +509,7 @@ HILO_DEV SkItem uni(const SkItem &x) { return SkItem{uni(x.t), uni(x.kb), uni(x.
 HILO_DEV TileRows uni(const TileRows &x) { return TileRows{uni(x.s), uni(x.sigma), uni(x.row0), uni(x.nrows)}; }
 
 namespace big {
-constexpr int BM = 256, BN = 256, BK = 32, S = 4;
-constexpr int SB = (BM + BN) * BK * 2;  // stage bytes
+constexpr int BM = 256, BK = 32, S = 4;
 constexpr int SPLIT = 2;                // MFMA rows before the barrier
 HILO_DEV int swz(int r) { return ((r >> 1) & 3) ^ ((r >> 3) & 1); }
 }  // namespace big
@@ -541,20 +540,20 @@ HILO_DEV void wait_lgkm_rt(int n) {  // n is a compile-time constant after unrol
   }
 }
 
-// Epilogue of a 256 x 256 tile from the AGPR accumulators of wave wid: bias (and gate) depend on
+// Epilogue of a 256 x (32 TNW) tile from the AGPR accumulators of wave wid (wave tile 128 x 16 TNW): bias (and gate) depend on
 // the column only and are loaded once, so the bias / GELU epilogues make a single memory round
 // trip; the residual update loads the old z one fragment row at a time (two rows in flight do not
 // fit the register budget next to the next tile's fragments).  Loads use indices clamped into the
 // tile; values outside it are never stored.
-template <int EPI>
-HILO_DEV void big_epilogue(const GemmProblem &p, const TileRows &tr, int n0, int wid, int lane, f32x4 (&acc)[8][8]) {
+template <int EPI, int TNW>
+HILO_DEV void big_epilogue(const GemmProblem &p, const TileRows &tr, int n0, int wid, int lane, f32x4 (&acc)[8][TNW]) {
   const int rbase = (wid >> 1) * 128 + (lane & 15);
-  const int cbase = n0 + (wid & 1) * 128 + 4 * (lane >> 4);
+  const int cbase = n0 + (wid & 1) * (16 * TNW) + 4 * (lane >> 4);
   const uint16_t *bias = reinterpret_cast<const uint16_t *>(tr.sigma ? p.bias[1] : p.bias[0]);
-  float bv[8][4];
-  float4 gt[8];
+  float bv[TNW][4];
+  float4 gt[TNW];
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
+  for (int j = 0; j < TNW; ++j) {
     const int nc = min(cbase + j * 16, p.N - 4);
     const uint2 bu = *reinterpret_cast<const uint2 *>(bias + nc);
     bv[j][0] = __uint_as_float(bu.x << 16); bv[j][1] = __uint_as_float(bu.x & 0xffff0000u);
@@ -562,17 +561,17 @@ HILO_DEV void big_epilogue(const GemmProblem &p, const TileRows &tr, int n0, int
     if constexpr (EPI == EPI_RESID)
       gt[j] = *reinterpret_cast<const float4 *>(p.mod + (size_t(tr.s * 2 + tr.sigma) * 6 + p.gate_idx) * p.D + nc);
   }
-  float4 zc[8];  // old z of the current fragment row
+  float4 zc[TNW];  // old z of the current fragment row
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
     if constexpr (EPI == EPI_RESID) {
       const size_t m = size_t(tr.row0 + min(rbase + i * 16, tr.nrows - 1));
 #pragma unroll
-      for (int j = 0; j < 8; ++j) zc[j] = *reinterpret_cast<const float4 *>(p.z + m * p.ldz + min(cbase + j * 16, p.N - 4));
+      for (int j = 0; j < TNW; ++j) zc[j] = *reinterpret_cast<const float4 *>(p.z + m * p.ldz + min(cbase + j * 16, p.N - 4));
     }
-    f32x4 row[8];
+    f32x4 row[TNW];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {  // copy this row out of the AGPRs here, not all rows up front
+    for (int j = 0; j < TNW; ++j) {  // copy this row out of the AGPRs here, not all rows up front
       row[j] = acc[i][j];
       asm volatile("" : "+v"(row[j]));
     }
@@ -580,7 +579,7 @@ HILO_DEV void big_epilogue(const GemmProblem &p, const TileRows &tr, int n0, int
     if (rl < tr.nrows) {
       const size_t m = size_t(tr.row0 + rl);
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
+      for (int j = 0; j < TNW; ++j) {
         const int n = cbase + j * 16;
         if (n >= p.N) continue;
         float v[4];
@@ -609,10 +608,21 @@ HILO_DEV void big_epilogue(const GemmProblem &p, const TileRows &tr, int n0, int
   }
 }
 
-template <int EPI, int ROLE>
+// BN = 256 or 128: wave tile 128 x BN/2, TNW = BN/32 weight fragments per wave.
+template <int EPI, int ROLE, int BN>
 __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
-  using namespace big;
+  using big::BM;
+  using big::BK;
+  using big::S;
+  using big::SPLIT;
+  using big::swz;
   using T = SkTile<BM, BN, 2, 2>;
+  constexpr int TNW = BN / 32;          // weight fragments per wave
+  constexpr int LB = BN / 64;           // weight load instructions per wave per stage (A: 4)
+  constexpr int LQ = 4 + LB;            // load instructions per wave per stage
+  constexpr int NR = 8 + TNW;           // fragment reads per wave per stage
+  constexpr int AB = BM * BK * 2;       // bytes of a stage's A rows
+  constexpr int SB = (BM + BN) * BK * 2;
   __shared__ __attribute__((aligned(1024))) uint8_t lds[S * SB];
 
   const int P = gridDim.x;
@@ -627,7 +637,7 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
 
   // ---- loader: its own cursor over this workgroup's items, three stages ahead of the MFMAs
   SkCursor lc{pid, rg.beg};
-  const uint16_t *la[4], *lb[4];
+  const uint16_t *la[4], *lb[LB];
   int lk = 0, lke = 0;  // next stage to load (32-deep, absolute in K) and the end of its item
   auto ld_src = [&](int t) __attribute__((always_inline)) {
     int rt, tn;
@@ -637,9 +647,13 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
     const uint16_t *Wt = reinterpret_cast<const uint16_t *>(tr.sigma ? p.W[1] : p.W[0]);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int r = wid * 64 + 16 * i + lrow, c = (lslot ^ swz(r)) * 8;
-      la[i] = A + size_t(tr.row0 + min(r, tr.nrows - 1)) * p.lda + c;
-      lb[i] = Wt + size_t(min(tn * BN + r, p.N - 1)) * p.K + c;
+      const int r = wid * 64 + 16 * i + lrow;
+      la[i] = A + size_t(tr.row0 + min(r, tr.nrows - 1)) * p.lda + (lslot ^ swz(r)) * 8;
+    }
+#pragma unroll
+    for (int i = 0; i < LB; ++i) {
+      const int r = wid * (BN / 4) + 16 * i + lrow;
+      lb[i] = Wt + size_t(min(tn * BN + r, p.N - 1)) * p.K + (lslot ^ swz(r)) * 8;
     }
   };
   auto ld_advance = [&]() __attribute__((always_inline)) {
@@ -654,12 +668,12 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
     lk = uni(lk);
     lke = uni(lke);
   };
-  // load instruction j (0..7) of the current loader stage into `slot`: A rows for j < 4
+  // load instruction j (0..LQ-1) of the current loader stage into `slot`: A rows for j < 4
   auto ld_one = [&](int slot, int j) __attribute__((always_inline)) {
-    uint8_t *base = lds + slot * SB + wid * 64 * 64;
+    uint8_t *base = lds + slot * SB;
     const int k0 = lk * BK;
-    if (j < 4) g2lds16(la[j] + k0, base + j * 1024);
-    else g2lds16(lb[j - 4] + k0, base + 16384 + (j - 4) * 1024);
+    if (j < 4) g2lds16(la[j] + k0, base + wid * 64 * 64 + j * 1024);
+    else g2lds16(lb[j - 4] + k0, base + AB + wid * (BN / 4) * 64 + (j - 4) * 1024);
   };
 
   // ---- fragment addresses: lane (lr, lg) reads row lr of 16, chunk lg of 4 (swizzle of lr only:
@@ -668,44 +682,46 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
   const uint32_t lane_off = lr * 64 + ((lg ^ swz(lr)) * 16);
   const uint32_t lds0 = (uint32_t)(uintptr_t)lds;
   const uint32_t fa0 = lds0 + (wid >> 1) * 128 * 64 + lane_off;
-  const uint32_t fb0 = lds0 + 16384 + (wid & 1) * 128 * 64 + lane_off;
-  // read t of a stage, in consumption order: W fragments 0..7, then A fragments 0..7
-  auto rd_one = [&](u32x4 (&fa)[8], u32x4 (&fb)[8], uint32_t a, uint32_t b, int t) __attribute__((always_inline)) {
+  const uint32_t fb0 = lds0 + AB + (wid & 1) * (BN / 2) * 64 + lane_off;
+  // read t of a stage, in consumption order: W fragments 0..TNW-1, then A fragments 0..7
+  auto rd_one = [&](u32x4 (&fa)[8], u32x4 (&fb)[TNW], uint32_t a, uint32_t b, int t) __attribute__((always_inline)) {
+#define HILO_RD_CASE(C)                                                        \
+  case C:                                                                      \
+    if constexpr (C < TNW) HILO_DS_READ16(fb[C < TNW ? C : 0], b, (C < TNW ? C : 0) * 1024); \
+    else if constexpr (C - TNW < 8) HILO_DS_READ16(fa[(C - TNW) & 7], a, ((C - TNW) & 7) * 1024); \
+    break;
     switch (t) {
-      case 0: HILO_DS_READ16(fb[0], b, 0); break;     case 1: HILO_DS_READ16(fb[1], b, 1024); break;
-      case 2: HILO_DS_READ16(fb[2], b, 2048); break;  case 3: HILO_DS_READ16(fb[3], b, 3072); break;
-      case 4: HILO_DS_READ16(fb[4], b, 4096); break;  case 5: HILO_DS_READ16(fb[5], b, 5120); break;
-      case 6: HILO_DS_READ16(fb[6], b, 6144); break;  case 7: HILO_DS_READ16(fb[7], b, 7168); break;
-      case 8: HILO_DS_READ16(fa[0], a, 0); break;     case 9: HILO_DS_READ16(fa[1], a, 1024); break;
-      case 10: HILO_DS_READ16(fa[2], a, 2048); break; case 11: HILO_DS_READ16(fa[3], a, 3072); break;
-      case 12: HILO_DS_READ16(fa[4], a, 4096); break; case 13: HILO_DS_READ16(fa[5], a, 5120); break;
-      case 14: HILO_DS_READ16(fa[6], a, 6144); break; default: HILO_DS_READ16(fa[7], a, 7168); break;
+      HILO_RD_CASE(0) HILO_RD_CASE(1) HILO_RD_CASE(2) HILO_RD_CASE(3) HILO_RD_CASE(4) HILO_RD_CASE(5)
+      HILO_RD_CASE(6) HILO_RD_CASE(7) HILO_RD_CASE(8) HILO_RD_CASE(9) HILO_RD_CASE(10) HILO_RD_CASE(11)
+      HILO_RD_CASE(12) HILO_RD_CASE(13) HILO_RD_CASE(14) HILO_RD_CASE(15)
+      default: break;
     }
+#undef HILO_RD_CASE
   };
 
-  f32x4 acc[8][8];
-  u32x4 xa[8], xb[8], ya[8], yb[8];
+  f32x4 acc[8][TNW];
+  u32x4 xa[8], xb[TNW], ya[8], yb[TNW];
 
   // one stage (ring slot gs % S) on fragments (fa, fb); reads stage gs + 1 into (na, nb); the
   // first stage of a tile (first = true_type) starts the accumulators from zero
-  constexpr int LQ0 = SPLIT * 8, RQ0 = LQ0 + 8;
-  static_assert(RQ0 + 16 <= 64, "stage schedule does not fit");
-  auto stage = [&](auto first, u32x4 (&fa)[8], u32x4 (&fb)[8], u32x4 (&na)[8], u32x4 (&nb)[8], int gs) __attribute__((always_inline)) {
+  constexpr int LQ0 = SPLIT * TNW, RQ0 = LQ0 + LQ;
+  static_assert(RQ0 + NR <= 8 * TNW, "stage schedule does not fit");
+  auto stage = [&](auto first, u32x4 (&fa)[8], u32x4 (&fb)[TNW], u32x4 (&na)[8], u32x4 (&nb)[TNW], int gs) __attribute__((always_inline)) {
     const int lslot_w = (gs + S - 1) & (S - 1), nslot = (gs + 1) & (S - 1);
     const uint32_t a = fa0 + nslot * SB, b = fb0 + nslot * SB;
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       // outstanding reads allowed: this stage's A fragments i+1..7 and the next stage's issued so far
-      const int q0 = i * 8;
-      wait_lgkm_rt(7 - i + (q0 <= RQ0 ? 0 : min(q0 - RQ0, 16)));
+      const int q0 = i * TNW;
+      wait_lgkm_rt(7 - i + (q0 <= RQ0 ? 0 : min(q0 - RQ0, NR)));
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int qq = i * 8 + j;
-        if (qq == LQ0) asm volatile("s_waitcnt vmcnt(%0)\n s_barrier" ::"n"((S - 3) * 8) : "memory");
+      for (int j = 0; j < TNW; ++j) {
+        const int qq = i * TNW + j;
+        if (qq == LQ0) asm volatile("s_waitcnt vmcnt(%0)\n s_barrier" ::"n"((S - 3) * LQ) : "memory");
         if constexpr (decltype(first)::value) HILO_MFMA_AGPR0(acc[i][j], fb[j], fa[i]);
         else HILO_MFMA_AGPR(acc[i][j], fb[j], fa[i]);
-        if (qq >= LQ0 && qq < LQ0 + 8) ld_one(lslot_w, qq - LQ0);
-        if (qq >= RQ0 && qq < RQ0 + 16) rd_one(na, nb, a, b, qq - RQ0);
+        if (qq >= LQ0 && qq < LQ0 + LQ) ld_one(lslot_w, qq - LQ0);
+        if (qq >= RQ0 && qq < RQ0 + NR) rd_one(na, nb, a, b, qq - RQ0);
       }
     }
     ++lk;
@@ -719,12 +735,12 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
   for (int st = 0; st < S - 1; ++st) {
     if (lk == lke) ld_advance();
 #pragma unroll
-    for (int j = 0; j < 8; ++j) ld_one(st, j);
+    for (int j = 0; j < LQ; ++j) ld_one(st, j);
     ++lk;
   }
-  asm volatile("s_waitcnt vmcnt(%0)\n s_barrier" ::"n"((S - 2) * 8) : "memory");
+  asm volatile("s_waitcnt vmcnt(%0)\n s_barrier" ::"n"((S - 2) * LQ) : "memory");
 #pragma unroll
-  for (int t = 0; t < 16; ++t) rd_one(xa, xb, fa0, fb0, t);
+  for (int t = 0; t < NR; ++t) rd_one(xa, xb, fa0, fb0, t);
 
   // the loader moves to its next item between stages, outside the MFMA schedule
   auto ld_check = [&]() __attribute__((always_inline)) {
@@ -752,21 +768,21 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
 #pragma unroll
     for (int i = 0; i < 8; ++i)
 #pragma unroll
-      for (int j = 0; j < 8; ++j) asm volatile("" : "+a"(acc[i][j]));
+      for (int j = 0; j < TNW; ++j) asm volatile("" : "+a"(acc[i][j]));
     if (cur.slot == nullptr) {
       int rt, tn;
       tile_coords(q, cur.t, rt, tn);
       tn = uni(tn);
       const TileRows tr = uni(decode_row_tile(p, BM, uni(rt)));
-      big_epilogue<EPI>(p, tr, tn * BN, wid, lane, acc);
+      big_epilogue<EPI, TNW>(p, tr, tn * BN, wid, lane, acc);
     } else {
       // straight from the AGPRs (no copy of all 256 accumulators through VGPRs)
       float *base = cur.slot + T::part_index(wid, 0, 0, lane);
 #pragma unroll
       for (int i = 0; i < 8; ++i)
 #pragma unroll
-        for (int j = 0; j < 8; ++j)
-          asm volatile("global_store_dwordx4 %0, %1, off" ::"v"(base + (i * 8 + j) * 256), "a"(acc[i][j]) : "memory");
+        for (int j = 0; j < TNW; ++j)
+          asm volatile("global_store_dwordx4 %0, %1, off" ::"v"(base + (i * TNW + j) * 256), "a"(acc[i][j]) : "memory");
     }
     cur = uni(sk_next_item(cc, q, rg, P, pid, p.part, T::kPartFloats));
     if (!cur.valid) break;
@@ -957,21 +973,21 @@ static hipError_t run_bf16(const GemmProblem &p, hipStream_t st) {
   return hipGetLastError();
 }
 
-// 256 x 256 tiles: one persistent workgroup per CU.
-template <int ROLE>
+// 256 x BN tiles: one persistent workgroup per CU.
+template <int ROLE, int BN>
 static hipError_t run_big(const GemmProblem &p, hipStream_t st) {
-  static_assert(size_t(big::BM) * big::BN * 3 * kBigMaxWorkgroups * sizeof(float) <= kSkPartBytes,
-                "partial area too small");
+  constexpr int BM = big::BM;
+  static_assert(size_t(BM) * BN * 3 * kBigMaxWorkgroups * sizeof(float) <= kSkPartBytes, "partial area too small");
   const int P = device_cus() < kBigMaxWorkgroups ? device_cus() : kBigMaxWorkgroups;
-  hipLaunchKernelGGL((k_gemm_big<role_epilogue(ROLE), ROLE>), dim3(P), dim3(256), 0, st, p);
+  hipLaunchKernelGGL((k_gemm_big<role_epilogue(ROLE), ROLE, BN>), dim3(P), dim3(256), 0, st, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const long long tiles_max = (long long)p.B * ((p.max_img_rows + big::BM - 1) / big::BM + (p.L + big::BM - 1) / big::BM) *
-                              ((p.N + big::BN - 1) / big::BN);
+  const long long tiles_max = (long long)p.B * ((p.max_img_rows + BM - 1) / BM + (p.L + BM - 1) / BM) *
+                              ((p.N + BN - 1) / BN);
   if (tiles_max < P && p.K / 64 <= kNoSplitSteps) return hipSuccess;
-  constexpr int kFixBlocks = 4 * (big::BM / 2 / 16) / (kFixThreads / 64);
-  hipLaunchKernelGGL((k_gemm_fix<big::BM, big::BN, 2, 2, role_epilogue(ROLE), ROLE>), dim3(P * kFixBlocks), dim3(kFixThreads),
-                     0, st, p, P);
+  constexpr int kFixBlocks = 4 * (BM / 2 / 16) / (kFixThreads / 64);
+  hipLaunchKernelGGL((k_gemm_fix<BM, BN, 2, 2, role_epilogue(ROLE), ROLE>), dim3(P * kFixBlocks), dim3(kFixThreads), 0,
+                     st, p, P);
   return hipGetLastError();
 }
 
@@ -999,11 +1015,13 @@ hipError_t launch_gemm(bool bf16, int role, const GemmProblem &p, hipStream_t st
   // 256 x 256 tiles (QKV: 396 tiles, two waves of whole tiles; MLP up: 528 tiles, two waves plus a
   // short stream-K tail); the attention output and MLP down projections have only 132 such tiles
   // for 256 CUs, so they would need split K with 256 KiB partials, and keep 128 x 128 tiles
-  // (528 of them for 512 workgroups).
+  // (528 of them for 512 workgroups).  256 x 128 tiles for these two (264 tiles: one wave and an
+  // 8-tile stream-K tail) measured slower than 128 x 128 (attention output 81 -> 88 us, MLP down
+  // 226 -> 234 us in isolation): with a 128 x 64 wave tile the stage reads more LDS per MFMA.
   switch (role) {
-    case GEMM_QKV: return run_big<GEMM_QKV>(p, st);
+    case GEMM_QKV: return run_big<GEMM_QKV, 256>(p, st);
     case GEMM_O: return run_bf16<128, 128, 2, 2, GEMM_O>(p, st);
-    case GEMM_FC1: return run_big<GEMM_FC1>(p, st);
+    case GEMM_FC1: return run_big<GEMM_FC1, 256>(p, st);
     default: return run_bf16<128, 128, 2, 2, GEMM_FC2>(p, st);
   }
 }
