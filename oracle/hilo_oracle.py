@@ -21,6 +21,8 @@ diffusion-transformer block on the shortened sequence and the reassembly of the 
                                                                      cost is quadratic in tokens)
   stack      blocks in order; request = one selection, then per   (Sec. 2.3: selection once per
              step compress -> stack -> decompress                   request; Sec. 3.3: 8 steps)
+  fp8        per-row E4M3 quantisation of the QKV / MLP-up        (Sec. 3.3: FP8 quantisation
+             operands                                               on top of the compression)
   decompress scatter fine rows, broadcast pooled rows to 4 patches
 
 Precision.  Floating point that decides an integer (the energy that decides which blocks stay
@@ -34,7 +36,7 @@ below states the reading it implements.
 
 Parity status per function (what pins it is in tests/test_oracle_*.py):
   score, score_pixels, dilate, block_sums, select_*, compact, layout, compress, decompress,
-  attention, mlp, stack, request:
+  attention, mlp, stack, request, e4m3_value, quantize_rows:
   pinned by closed forms, library routines (scipy Sobel / binary dilation, torch SDPA / layer_norm
   / gelu), hand-worked fixtures under tests/golden/, and the identities of the method (0% compression
   equals the dense block, pooling a constant block then broadcasting is lossless, kept-token count
@@ -332,6 +334,54 @@ def _segments(cu: np.ndarray, text_len: int):
         yield s, 1, int(cu[s + 1]) - text_len, int(cu[s + 1])
 
 
+# ------------------------------------------------------------------------------------------------
+# FP8 (Sec. 3.3: the compressed DiT combines with FP8 quantisation)
+# ------------------------------------------------------------------------------------------------
+
+E4M3_MAX = np.float32(448.0)
+
+
+def e4m3_value(codes: np.ndarray) -> np.ndarray:
+    """Value of OCP FP8 E4M3 codes (1 sign, 4 exponent bits with bias 7, 3 mantissa bits; exponent
+    0 is subnormal; 0x7f / 0xff are NaN, there is no infinity), float64."""
+    c = np.asarray(codes, dtype=np.uint8).astype(np.int64)
+    sign = np.where(c & 0x80, -1.0, 1.0)
+    e = (c >> 3) & 0xF
+    m = (c & 0x7).astype(np.float64)
+    v = np.where(e == 0, m / 8.0 * 2.0 ** -6, (1.0 + m / 8.0) * np.exp2(e.astype(np.float64) - 7.0))
+    v = np.where((e == 15) & (m == 7), np.nan, v)
+    return sign * v
+
+
+def quantize_rows(x: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
+    """Per-row FP8 E4M3 quantisation, every step one float32 operation:
+      amax = max |x| over the row;  inv = 448 / amax (correctly rounded; 0 for an all-zero row)
+      code = round-to-nearest-even E4M3 of clamp(x * inv, -448, 448);  scale = amax / 448
+    so code value * scale approximates x.  x [R][C] float32 -> codes uint8 [R][C], scale float32 [R].
+    (The rounding to E4M3 uses torch's float8_e4m3fn cast as a library primitive.)"""
+    import torch
+
+    x = np.asarray(x, dtype=np.float32)
+    amax = np.abs(x).max(axis=1)
+    with np.errstate(divide="ignore"):
+        inv = np.where(amax > 0, E4M3_MAX / amax, np.float32(0)).astype(np.float32)
+    y = np.clip(x * inv[:, None], -E4M3_MAX, E4M3_MAX).astype(np.float32)
+    codes = torch.from_numpy(y).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+    scale = (amax / E4M3_MAX).astype(np.float32)
+    return codes, scale
+
+
+def dequant_rows(codes: np.ndarray, scale: np.ndarray) -> np.ndarray:
+    return e4m3_value(codes) * np.asarray(scale, dtype=np.float64)[:, None]
+
+
+def _fp8_matmul(h: np.ndarray, q) -> np.ndarray:
+    """h @ W^T with both operands FP8 per row (h rounded to float32 first, as the device holds it)."""
+    hc, hs = quantize_rows(h.astype(np.float32))
+    wc, ws = q
+    return dequant_rows(hc, hs) @ dequant_rows(wc, ws).T
+
+
 def _w(weights, sigma: int, name: str) -> np.ndarray:
     return np.asarray(weights[sigma][name], dtype=np.float64)
 
@@ -368,7 +418,7 @@ def attention_core(qkv: np.ndarray, cu: np.ndarray, heads: int,
 
 
 def attention(Z: np.ndarray, cu: np.ndarray, text_len: int, heads: int, weights, mod: np.ndarray,
-              rows: Optional[np.ndarray] = None) -> np.ndarray:
+              rows: Optional[np.ndarray] = None, fp8=None) -> np.ndarray:
     """Attention half of an MMDiT-style pre-LN adaLN block with per-stream weights:
 
       h   = LN(z) * (1 + scale1) + shift1
@@ -378,7 +428,8 @@ def attention(Z: np.ndarray, cu: np.ndarray, text_len: int, heads: int, weights,
 
     Joint attention over image + text tokens of one sample, no mask (Sec. 2.3: the HiLo tokens are
     processed by the DiT; Sec. 2.2: memory-efficient attention).  Returns z1 for `rows` (all rows
-    when None), float64 [len(rows)][D]."""
+    when None), float64 [len(rows)][D].  With `fp8` (per stream {"w_qkv": (codes, scale)}) the QKV
+    projection multiplies FP8 rows of h by FP8 rows of W_qkv (quantize_rows)."""
     T, D = Z.shape
     all_rows = np.arange(T) if rows is None else np.asarray(rows)
     out = np.empty((all_rows.size, D), dtype=np.float64)
@@ -392,7 +443,8 @@ def attention(Z: np.ndarray, cu: np.ndarray, text_len: int, heads: int, weights,
             if ss != s or b <= a:
                 continue
             h = layer_norm(Z[a:b]) * (1.0 + mod[s, sig, 1]) + mod[s, sig, 0]
-            qkv[a - lo:b - lo] = h @ _w(weights, sig, "w_qkv").T + _w(weights, sig, "b_qkv")
+            prod = _fp8_matmul(h, fp8[sig]["w_qkv"]) if fp8 is not None else h @ _w(weights, sig, "w_qkv").T
+            qkv[a - lo:b - lo] = prod + _w(weights, sig, "b_qkv")
         r_loc = all_rows[sel] - lo
         a_out = _attend(qkv[r_loc, :D], qkv[:, D:2 * D], qkv[:, 2 * D:], heads)
         text_start = hi - text_len
@@ -406,10 +458,12 @@ def attention(Z: np.ndarray, cu: np.ndarray, text_len: int, heads: int, weights,
 
 
 def mlp(Z1: np.ndarray, row_ids: np.ndarray, cu: np.ndarray, text_len: int, weights,
-        mod: np.ndarray) -> np.ndarray:
+        mod: np.ndarray, fp8=None) -> np.ndarray:
     """MLP half of the block: z2 = z1 + gate2 * (GELU_tanh(h2 W1^T + b1) W2^T + b2) with
     h2 = LN(z1) * (1 + scale2) + shift2.  Z1 holds the rows `row_ids` of the packed sequence (their
-    sample and stream follow from cu_seqlens).  Returns float64 [len(row_ids)][D]."""
+    sample and stream follow from cu_seqlens).  Returns float64 [len(row_ids)][D].  With `fp8`
+    (per stream {"w1": (codes, scale)}) the up projection multiplies FP8 rows of h2 by FP8 rows of
+    W1."""
     out = np.empty_like(Z1, dtype=np.float64)
     row_ids = np.asarray(row_ids)
     for (s, sig, a, b) in _segments(cu, text_len):
@@ -418,19 +472,28 @@ def mlp(Z1: np.ndarray, row_ids: np.ndarray, cu: np.ndarray, text_len: int, weig
             continue
         z = Z1[m]
         h2 = layer_norm(z) * (1.0 + mod[s, sig, 4]) + mod[s, sig, 3]
-        u = h2 @ _w(weights, sig, "w1").T + _w(weights, sig, "b1")
+        prod = _fp8_matmul(h2, fp8[sig]["w1"]) if fp8 is not None else h2 @ _w(weights, sig, "w1").T
+        u = prod + _w(weights, sig, "b1")
         o = gelu_tanh(u) @ _w(weights, sig, "w2").T + _w(weights, sig, "b2")
         out[m] = z + mod[s, sig, 5] * o
     return out
 
 
 def block(Z: np.ndarray, cu: np.ndarray, text_len: int, heads: int, weights, mod: np.ndarray,
-          rows: Optional[np.ndarray] = None) -> Tuple[np.ndarray, np.ndarray]:
-    """Whole block on the packed sequence: returns (z1, z2) for `rows` (all rows when None)."""
+          rows: Optional[np.ndarray] = None, fp8=None) -> Tuple[np.ndarray, np.ndarray]:
+    """Whole block on the packed sequence: returns (z1, z2) for `rows` (all rows when None).
+    `fp8`: per stream {"w_qkv": (codes, scale), "w1": (codes, scale)} for FP8 QKV and MLP-up
+    projections (quantize_fp8_weights)."""
     rows = np.arange(Z.shape[0]) if rows is None else np.asarray(rows)
-    z1 = attention(Z, cu, text_len, heads, weights, mod, rows)
-    z2 = mlp(z1, rows, cu, text_len, weights, mod)
+    z1 = attention(Z, cu, text_len, heads, weights, mod, rows, fp8)
+    z2 = mlp(z1, rows, cu, text_len, weights, mod, fp8)
     return z1, z2
+
+
+def quantize_fp8_weights(weights) -> List[Dict[str, Tuple[np.ndarray, np.ndarray]]]:
+    """Per stream, the FP8 rows (per output channel) of W_qkv and W1."""
+    return [{name: quantize_rows(np.asarray(w[name], dtype=np.float32)) for name in ("w_qkv", "w1")}
+            for w in weights]
 
 
 # ------------------------------------------------------------------------------------------------
@@ -447,7 +510,7 @@ def select(E, force, grid_h, grid_w, r, mode: str, tau=None, keep=None) -> np.nd
 
 def pipeline(x_img, x_txt, shape, force, r: int, mode: str, tau=None, keep=None, weights=None,
              mod=None, rows: Optional[np.ndarray] = None, with_block: bool = True,
-             tokens: str = "partition", delta: bool = False) -> Dict[str, np.ndarray]:
+             tokens: str = "partition", delta: bool = False, fp8: bool = False) -> Dict[str, np.ndarray]:
     """All six steps on one batch.  `shape` needs grid_h, grid_w, batch, images, text_len, heads.
     With `rows` the block is evaluated only for those packed rows (z1, z2 and y are then partial:
     y_img / y_txt are not formed).  `tokens` picks the token set (compact), `delta` the delta form
@@ -461,7 +524,8 @@ def pipeline(x_img, x_txt, shape, force, r: int, mode: str, tau=None, keep=None,
     res = dict(E=E, fine=fine, idx_map=idx_map, fine_idx=fine_idx, pool_idx=pool_idx, counts=counts,
                cu=cu, seg=seg, Z=Z)
     if with_block:
-        z1, z2 = block(Z, cu, shape.text_len, shape.heads, weights, mod, rows)
+        z1, z2 = block(Z, cu, shape.text_len, shape.heads, weights, mod, rows,
+                       quantize_fp8_weights(weights) if fp8 else None)
         res.update(z1=z1, z2=z2)
         if rows is None:
             y_img, y_txt = decompress(z2, idx_map, cu, seg, shape.text_len, shape.batch,

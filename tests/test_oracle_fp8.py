@@ -1,0 +1,50 @@
+"""FP8 E4M3 codes and per-row quantisation of the oracle, pinned by hand-worked bit patterns."""
+import numpy as np
+import pytest
+
+from oracle import hilo_oracle as O
+from paper_2606_13898_amd import inputs
+
+
+def test_e4m3_decoding_of_hand_worked_codes():
+    # 0x38 = 0 0111 000 = 1.0; 0x30 = 0.5; 0x7e = 0 1111 110 = 1.75 * 2^8 = 448; 0x77 = 1.875 * 2^7
+    # = 240; 0x01 = 2^-9 (smallest subnormal); 0x08 = 2^-6 (smallest normal); 0xb8 = -1.0
+    codes = np.array([0x38, 0x30, 0x7e, 0x77, 0x01, 0x08, 0xb8, 0x00, 0x3a], dtype=np.uint8)
+    np.testing.assert_array_equal(O.e4m3_value(codes), [1.0, 0.5, 448.0, 240.0, 2.0 ** -9, 2.0 ** -6, -1.0, 0.0, 1.25])
+    assert np.isnan(O.e4m3_value(np.array([0x7f], dtype=np.uint8)))[0]
+
+
+def test_quantize_row_with_max_448_keeps_exact_values_and_rounds_ties_to_even():
+    # amax = 448 -> inv = 1: values encode directly.  1.0625 lies halfway between 1.0 (mantissa 000)
+    # and 1.125 (001): even -> 1.0; 1.1875 halfway between 1.125 (001) and 1.25 (010): even -> 1.25
+    x = np.array([[448.0, -448.0, 1.0, 0.5, 240.0, 1.0625, 1.1875, 0.0]], dtype=np.float32)
+    codes, scale = O.quantize_rows(x)
+    np.testing.assert_array_equal(codes[0], [0x7e, 0xfe, 0x38, 0x30, 0x77, 0x38, 0x3a, 0x00])
+    assert scale[0] == np.float32(1.0)
+
+
+def test_quantize_zero_row_and_scaled_row():
+    codes, scale = O.quantize_rows(np.zeros((1, 8), dtype=np.float32))
+    assert (codes == 0).all() and scale[0] == 0
+    # row [2, 1, 0.5]: amax 2 -> inv 224, values 448, 224, 112 -> codes 0x7e, 0x76 (1.75 * 2^7), 0x6e
+    codes, scale = O.quantize_rows(np.array([[2.0, 1.0, 0.5]], dtype=np.float32))
+    np.testing.assert_array_equal(codes[0], [0x7e, 0x76, 0x6e])
+    assert scale[0] == np.float32(2.0 / 448.0)
+    np.testing.assert_allclose(O.dequant_rows(codes, scale)[0], [2.0, 1.0, 0.5], rtol=1e-6)
+
+
+def test_quantisation_error_is_within_half_an_e4m3_step():
+    rng = np.random.default_rng(0)
+    x = rng.standard_normal((16, 256)).astype(np.float32)
+    codes, scale = O.quantize_rows(x)
+    err = np.abs(O.dequant_rows(codes, scale) - x) / np.abs(x).max(axis=1, keepdims=True)
+    assert err.max() <= 2.0 ** -4 / 2 * 448 / 256 + 1e-6  # half a step at the top binade, relative to amax
+
+
+def test_fp8_block_stays_close_to_the_bf16_block():
+    shp = inputs.BlockShape(1, 1, 8, 10, 4, 256, 2, 128, 1024, "bf16")
+    wl = inputs.make_workload("smallx", shape=shp, seed=51)
+    a = O.pipeline(wl.x_img, wl.x_txt, shp, None, 0, "topk", keep=wl.keep, weights=wl.weights, mod=wl.mod)
+    b = O.pipeline(wl.x_img, wl.x_txt, shp, None, 0, "topk", keep=wl.keep, weights=wl.weights, mod=wl.mod, fp8=True)
+    d = np.abs(b["y_img"] - a["y_img"]).max()
+    assert 0 < d < 0.1
