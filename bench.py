@@ -23,6 +23,7 @@ if ROOT not in sys.path:
 
 METRIC = "compressed DiT-block latency (ms) + attn TFLOP/s at 64×64 grid; speedup vs dense"
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_FP8_TFLOPS = 5000.0    # MI355X dense fp8 MFMA
 PEAK_F32_TFLOPS = 157.3     # MI355X fp32 vector
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 
@@ -175,6 +176,73 @@ def token_set_leg(db, steps, warmup, stream, dense_ms):
     return res
 
 
+def fp8_leg(db, steps, warmup, stream, work, bf16_ms):
+    """The step with the QKV and MLP-up projections in FP8 (per-row E4M3 operands: one scale per
+    token for the normalised activations, one per output channel for the weights; Sec. 3.3 combines
+    the compression with FP8 quantisation): step latency, the two projections' rates against the
+    fp8 MFMA peak, and how far the block's update of the compressed tokens moves from the bf16
+    step's (relative L2 over all rows)."""
+    import numpy as np
+    import torch
+
+    from paper_2606_13898_amd import hilo
+
+    db.prepare_fp8()
+    db.score()
+    db.select(hilo.TOPK)
+    db.compress()
+    z0 = db.z.clone()
+    db.attention()
+    db.mlp()
+    z16 = db.z.clone()
+    db.compress()
+    db.attention(fp8=True)
+    db.mlp(fp8=True)
+    torch.cuda.synchronize()
+    nc = int(db.cu.cpu().numpy()[-1])
+    upd16 = (z16 - z0)[:nc].double()
+    upd8 = (db.z - z0)[:nc].double()
+    rel = float(torch.linalg.norm(upd8 - upd16) / torch.linalg.norm(upd16))
+
+    for _ in range(warmup):
+        db.run(hilo.TOPK, fp8=True)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    torch.cuda.synchronize()
+    evs[0].record(stream)
+    for k in range(steps):
+        db.run(hilo.TOPK, fp8=True)
+        evs[k + 1].record(stream)
+    torch.cuda.synchronize()
+    ms = evs[0].elapsed_time(evs[-1]) / steps
+    per_step = np.sort([evs[k].elapsed_time(evs[k + 1]) for k in range(steps)])
+
+    hilo.hilo_profile_enable(True)
+    for _ in range(steps):
+        db.run(hilo.TOPK, fp8=True)
+    torch.cuda.synchronize()
+    kern = {}
+    for k in range(hilo.hilo_profile_kinds()):
+        name = hilo.hilo_profile_name(k)
+        tot, n = hilo.hilo_profile_read(k)
+        if n and name in ("rownorm_attn", "gemm_qkv", "rownorm_mlp", "gemm_fc1"):
+            avg = tot / n
+            ent = {"ms": round(avg, 4)}
+            if name.startswith("gemm"):
+                ach = work[name][0] / (avg * 1e-3)
+                ent.update(achieved=round(ach, 1), unit="TFLOP/s", peak=PEAK_FP8_TFLOPS,
+                           frac=round(ach / PEAK_FP8_TFLOPS, 4))
+            kern[name] = ent
+    hilo.hilo_profile_enable(False)
+    db.run(hilo.TOPK)  # leave the buffers as the default step left them
+    torch.cuda.synchronize()
+    res = {"ms_per_step": round(ms, 4), "ms_per_step_median": round(float(per_step[len(per_step) // 2]), 4),
+           "projections_in_fp8": ["qkv", "mlp_up"], "kernels": kern,
+           "block_update_rel_l2_vs_bf16": round(rel, 5)}
+    if bf16_ms:
+        res["speedup_vs_bf16_step"] = round(bf16_ms / ms, 3)
+    return res
+
+
 def stack_leg(db, wl, n_blocks, steps, stream, reps=3):
     """The paper's regime (Sec. 2.3, Sec. 3.3): one request = the selection once, then for each
     sampling step: compress that step's latents, run `n_blocks` blocks on the compressed tokens
@@ -273,6 +341,8 @@ def main():
                          "to the fine patches, and with the fine patches alone)")
     ap.add_argument("--no-pixel-score", action="store_true",
                     help="skip the pixel-space scorer leg (Sobel on the 16x-resolution RGB image)")
+    ap.add_argument("--no-fp8", action="store_true",
+                    help="skip the step with FP8 QKV / MLP-up projections")
     ap.add_argument("--stack-blocks", type=int, default=8)
     ap.add_argument("--stack-steps", type=int, default=8)
     ap.add_argument("--copy-mib", type=int, default=0,
@@ -390,6 +460,10 @@ def main():
     if not args.no_pixel_score:
         pixel = pixel_leg(db, args.steps, args.warmup, stream)
 
+    fp8 = None
+    if not args.no_fp8 and s.dtype == "bf16" and s.dim % 128 == 0:
+        fp8 = fp8_leg(db, args.steps, args.warmup, stream, work, ms)
+
     stack = None
     if not args.no_stack:
         stack = stack_leg(db, wl, args.stack_blocks, args.stack_steps, stream)
@@ -433,6 +507,8 @@ def main():
         out["token_sets"] = token_sets
     if pixel:
         out["pixel_score"] = pixel
+    if fp8:
+        out["fp8"] = fp8
     if stack:
         out["stack"] = stack
     if not args.no_cpu_baseline:

@@ -41,7 +41,7 @@
 extern "C" {
 #endif
 
-#define HILO_ABI_VERSION 2
+#define HILO_ABI_VERSION 3
 
 typedef enum {
   HILO_OK = 0,
@@ -181,6 +181,59 @@ hilo_status hilo_mlp(const hilo_shape *shape, float *z, const int32_t *cu_seqlen
 hilo_status hilo_blocks(const hilo_shape *shape, float *z, const int32_t *cu_seqlens,
                         const hilo_attn_w *attn_w, const hilo_mlp_w *mlp_w, const float *mod,
                         int32_t n_blocks, void *workspace, size_t ws_bytes, void *stream);
+
+/* FP8 projections (Sec. 3.3: the token compression composes with FP8 quantisation of the network).
+ * Format: OCP FP8 E4M3 (sign, 4 exponent bits with bias 7, 3 mantissa bits, subnormals, largest
+ * finite 448, codes 0x7f / 0xff NaN, no infinity), one float32 scale per row.  A row x of C values
+ * is quantised as (every step one float32 operation)
+ *   amax = max |x|;  inv = 448 / amax (correctly rounded; 0 when amax == 0)
+ *   code = round-to-nearest-even E4M3 of clamp(x * inv, -448, 448);  scale = amax / 448
+ * so that value(code) * scale approximates x.  The FP8 block runs the QKV and MLP-up projections
+ * on such rows -- activations per token, weights per output channel -- with exact products and
+ * float32 accumulation: acc = sum_k value(hcode[m][k]) value(wcode[n][k]), then
+ * out = acc * (hscale[m] * wscale[n]) + bias.  Everything else is as in the bf16 block.         */
+
+/* Weights of the FP8 block: W_qkv and W1 as E4M3 codes with one float32 scale per output channel
+ * (per row of the [out][in] matrix, hilo_quantize_rows), the other tensors bf16 as in
+ * hilo_attn_w / hilo_mlp_w.  Arrays of two per block: image stream, text stream.                */
+typedef struct {
+  const uint8_t *w_qkv; /* [3D][D] E4M3 codes */
+  const float *s_qkv;   /* [3D] row scales    */
+  const void *b_qkv;    /* [3D] bf16          */
+  const void *w_o;      /* [D][D] bf16        */
+  const void *b_o;      /* [D] bf16           */
+} hilo_attn_w_fp8;
+
+typedef struct {
+  const uint8_t *w1; /* [F][D] E4M3 codes */
+  const float *s1;   /* [F] row scales    */
+  const void *b1;    /* [F] bf16          */
+  const void *w2;    /* [D][F] bf16       */
+  const void *b2;    /* [D] bf16          */
+} hilo_mlp_w_fp8;
+
+/* Per-row E4M3 quantisation (as above) of x [rows][cols], dtype HILO_F32 or HILO_BF16 (read
+ * exactly as float32): codes [rows][cols] uint8, scale [rows] float32, all device memory.  For
+ * preparing FP8 weights once per model.  cols > 0 and cols % 4 == 0, 0 <= rows < 2^31 - 4
+ * (HILO_E_SHAPE otherwise); rows == 0 enqueues nothing.                                          */
+hilo_status hilo_quantize_rows(int32_t dtype, const void *x, int64_t rows, int64_t cols,
+                               uint8_t *codes, float *scale, void *stream);
+
+/* hilo_attention with the QKV projection in FP8: h = LN(z) * (1 + scale1) + shift1 is formed in
+ * float32 and quantised per row straight from registers (no bf16 rounding first), then multiplied
+ * by the FP8 W_qkv as described above; qkv is rounded to bf16.  The attention core and the output
+ * projection are those of hilo_attention.  shape->dtype must be HILO_BF16 (HILO_E_DTYPE) and dim a
+ * multiple of 128 (HILO_E_SHAPE).  workspace as hilo_attention.                                  */
+hilo_status hilo_attention_fp8(const hilo_shape *shape, float *z, const int32_t *cu_seqlens,
+                               const hilo_attn_w_fp8 w[2], const float *mod, void *workspace,
+                               size_t ws_bytes, void *stream);
+
+/* hilo_mlp with the up projection in FP8 (h2 quantised per row, W1 as codes and scales); GELU,
+ * the down projection and the gated residual as in hilo_mlp.  Requirements as
+ * hilo_attention_fp8.                                                                            */
+hilo_status hilo_mlp_fp8(const hilo_shape *shape, float *z, const int32_t *cu_seqlens,
+                         const hilo_mlp_w_fp8 w[2], const float *mod, void *workspace,
+                         size_t ws_bytes, void *stream);
 
 /* S6 -- decompress: y_img[g][p] = z[seg_off[g] + idx_map[g][p]] (fine tokens scatter back to
  * their patch, pooled tokens broadcast to the 4 patches of their block), y_txt[s][t] = the text

@@ -102,14 +102,22 @@ size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 constexpr size_t kPartBytes = kSkPartBytes > kAttnPartBytes ? kSkPartBytes : kAttnPartBytes;
 size_t ws_part(const hilo_shape *s) { return s->dtype == HILO_BF16 ? kPartBytes : 0; }
 
+// The normalised rows: T x D of dtype, or for the FP8 projections T x D codes followed (at
+// align256(T D)) by T float32 row scales.  The attention output reuses the region.
+size_t ws_h(const hilo_shape *s) {
+  const size_t T = size_t(tmax_of(s)), D = size_t(s->dim);
+  const size_t a = align256(T * D * esize(s)), f8 = align256(T * D) + align256(T * sizeof(float));
+  return a > f8 ? a : f8;
+}
+
 size_t ws_attention(const hilo_shape *s) {
   const size_t T = size_t(tmax_of(s)), D = size_t(s->dim), e = esize(s);
-  return align256(T * D * e) + align256(T * 3 * D * e) + ws_part(s);  // h (then a), qkv, partials
+  return ws_h(s) + align256(T * 3 * D * e) + ws_part(s);  // h (then a), qkv, partials
 }
 
 size_t ws_mlp(const hilo_shape *s) {
-  const size_t T = size_t(tmax_of(s)), D = size_t(s->dim), F = size_t(s->mlp_dim), e = esize(s);
-  return align256(T * D * e) + align256(T * F * e) + ws_part(s);  // h2, hidden, partials
+  const size_t T = size_t(tmax_of(s)), F = size_t(s->mlp_dim), e = esize(s);
+  return ws_h(s) + align256(T * F * e) + ws_part(s);  // h2, hidden, partials
 }
 
 hilo_status dev_status(hipError_t e) { return e == hipSuccess ? HILO_OK : HILO_E_DEVICE; }
@@ -312,31 +320,70 @@ hilo_status check_mlp_w(const hilo_mlp_w *w) {
   return HILO_OK;
 }
 
-// The attention half, arguments already validated.
+hilo_status check_attn_w8(const hilo_attn_w_fp8 *w) {
+  if (!w) return HILO_E_NULL;
+  for (int k = 0; k < 2; ++k)
+    if (!w[k].w_qkv || !w[k].s_qkv || !w[k].b_qkv || !w[k].w_o || !w[k].b_o) return HILO_E_NULL;
+  return HILO_OK;
+}
+
+hilo_status check_mlp_w8(const hilo_mlp_w_fp8 *w) {
+  if (!w) return HILO_E_NULL;
+  for (int k = 0; k < 2; ++k)
+    if (!w[k].w1 || !w[k].s1 || !w[k].b1 || !w[k].w2 || !w[k].b2) return HILO_E_NULL;
+  return HILO_OK;
+}
+
+// The FP8 block: bf16 activations and weights elsewhere, K = dim in whole 128-deep steps.
+hilo_status check_fp8_block(const hilo_shape *s) {
+  hilo_status e = check_block(s);
+  if (e != HILO_OK) return e;
+  if (s->dtype != HILO_BF16) return HILO_E_DTYPE;
+  if (s->dim % 128 != 0) return HILO_E_SHAPE;
+  return HILO_OK;
+}
+
+// Row scales of the FP8 normalised rows, behind their codes.
+float *fp8_row_scales(const hilo_shape *s, void *h) {
+  return reinterpret_cast<float *>(reinterpret_cast<char *>(h) + align256(size_t(tmax_of(s)) * s->dim));
+}
+
+// The attention half, arguments already validated: bf16 / float32 weights w, or (w8 non-null) the
+// FP8 QKV projection.
 hilo_status enqueue_attention(const hilo_shape *s, float *z, const int32_t *cu_seqlens,
-                              const hilo_attn_w w[2], const float *mod, void *workspace,
-                              hipStream_t st) {
+                              const hilo_attn_w *w, const hilo_attn_w_fp8 *w8, const float *mod,
+                              void *workspace, hipStream_t st) {
   const bool bf = s->dtype == HILO_BF16;
   const int D = s->dim;
   const int T = int(tmax_of(s));
   char *ws = reinterpret_cast<char *>(workspace);
   void *h = ws;  // LN output, later the attention output
-  void *qkv = ws + align256(size_t(T) * D * esize(s));
-  float *part = reinterpret_cast<float *>(ws + align256(size_t(T) * D * esize(s)) +
-                                          align256(size_t(T) * 3 * D * esize(s)));
+  void *qkv = ws + ws_h(s);
+  float *part = reinterpret_cast<float *>(ws + ws_h(s) + align256(size_t(T) * 3 * D * esize(s)));
+  float *hs = fp8_row_scales(s, h);
 
   hipError_t he = timed(K_NORM_ATTN, st, [&] {
-    return launch_rownorm(bf, z, cu_seqlens, mod, s->batch, s->text_len, D, T, 0, h, st);
+    return w8 ? launch_rownorm_fp8(z, cu_seqlens, mod, s->batch, s->text_len, D, T, 0,
+                                   reinterpret_cast<uint8_t *>(h), hs, st)
+              : launch_rownorm(bf, z, cu_seqlens, mod, s->batch, s->text_len, D, T, 0, h, st);
   });
   if (he != hipSuccess) return HILO_E_DEVICE;
 
   GemmProblem p = base_problem(s, cu_seqlens, mod, part);
   p.A = h; p.lda = D;
-  p.W[0] = w[0].w_qkv; p.W[1] = w[1].w_qkv;
-  p.bias[0] = w[0].b_qkv; p.bias[1] = w[1].b_qkv;
   p.N = 3 * D; p.K = D;
   p.out = qkv; p.ldo = 3 * D;
-  he = timed(K_GEMM_QKV, st, [&] { return launch_gemm(bf, GEMM_QKV, p, st); });
+  if (w8) {
+    p.W[0] = w8[0].w_qkv; p.W[1] = w8[1].w_qkv;
+    p.bias[0] = w8[0].b_qkv; p.bias[1] = w8[1].b_qkv;
+    p.a_scale = hs;
+    p.w_scale[0] = w8[0].s_qkv; p.w_scale[1] = w8[1].s_qkv;
+    he = timed(K_GEMM_QKV, st, [&] { return launch_gemm_fp8(GEMM_QKV, p, st); });
+  } else {
+    p.W[0] = w[0].w_qkv; p.W[1] = w[1].w_qkv;
+    p.bias[0] = w[0].b_qkv; p.bias[1] = w[1].b_qkv;
+    he = timed(K_GEMM_QKV, st, [&] { return launch_gemm(bf, GEMM_QKV, p, st); });
+  }
   if (he != hipSuccess) return HILO_E_DEVICE;
 
   const int max_seq = int(s->images * grid_rows_max(s) + s->text_len);
@@ -348,43 +395,55 @@ hilo_status enqueue_attention(const hilo_shape *s, float *z, const int32_t *cu_s
 
   GemmProblem q = base_problem(s, cu_seqlens, mod, part);
   q.A = h; q.lda = D;
-  q.W[0] = w[0].w_o; q.W[1] = w[1].w_o;
-  q.bias[0] = w[0].b_o; q.bias[1] = w[1].b_o;
+  q.W[0] = w8 ? w8[0].w_o : w[0].w_o; q.W[1] = w8 ? w8[1].w_o : w[1].w_o;
+  q.bias[0] = w8 ? w8[0].b_o : w[0].b_o; q.bias[1] = w8 ? w8[1].b_o : w[1].b_o;
   q.N = D; q.K = D;
   q.z = z; q.ldz = D; q.gate_idx = 2;
   return dev_status(timed(K_GEMM_O, st, [&] { return launch_gemm(bf, GEMM_O, q, st); }));
 }
 
-// The MLP half, arguments already validated.
+// The MLP half, arguments already validated: bf16 / float32 weights w, or (w8 non-null) the FP8
+// up projection.
 hilo_status enqueue_mlp(const hilo_shape *s, float *z, const int32_t *cu_seqlens,
-                        const hilo_mlp_w w[2], const float *mod, void *workspace, hipStream_t st) {
+                        const hilo_mlp_w *w, const hilo_mlp_w_fp8 *w8, const float *mod,
+                        void *workspace, hipStream_t st) {
   const bool bf = s->dtype == HILO_BF16;
   const int D = s->dim, F = s->mlp_dim;
   const int T = int(tmax_of(s));
   char *ws = reinterpret_cast<char *>(workspace);
   void *h2 = ws;
-  void *hid = ws + align256(size_t(T) * D * esize(s));
-  float *part = reinterpret_cast<float *>(ws + align256(size_t(T) * D * esize(s)) +
-                                          align256(size_t(T) * F * esize(s)));
+  void *hid = ws + ws_h(s);
+  float *part = reinterpret_cast<float *>(ws + ws_h(s) + align256(size_t(T) * F * esize(s)));
+  float *hs = fp8_row_scales(s, h2);
 
   hipError_t he = timed(K_NORM_MLP, st, [&] {
-    return launch_rownorm(bf, z, cu_seqlens, mod, s->batch, s->text_len, D, T, 1, h2, st);
+    return w8 ? launch_rownorm_fp8(z, cu_seqlens, mod, s->batch, s->text_len, D, T, 1,
+                                   reinterpret_cast<uint8_t *>(h2), hs, st)
+              : launch_rownorm(bf, z, cu_seqlens, mod, s->batch, s->text_len, D, T, 1, h2, st);
   });
   if (he != hipSuccess) return HILO_E_DEVICE;
 
   GemmProblem p = base_problem(s, cu_seqlens, mod, part);
   p.A = h2; p.lda = D;
-  p.W[0] = w[0].w1; p.W[1] = w[1].w1;
-  p.bias[0] = w[0].b1; p.bias[1] = w[1].b1;
   p.N = F; p.K = D;
   p.out = hid; p.ldo = F;
-  he = timed(K_GEMM_FC1, st, [&] { return launch_gemm(bf, GEMM_FC1, p, st); });
+  if (w8) {
+    p.W[0] = w8[0].w1; p.W[1] = w8[1].w1;
+    p.bias[0] = w8[0].b1; p.bias[1] = w8[1].b1;
+    p.a_scale = hs;
+    p.w_scale[0] = w8[0].s1; p.w_scale[1] = w8[1].s1;
+    he = timed(K_GEMM_FC1, st, [&] { return launch_gemm_fp8(GEMM_FC1, p, st); });
+  } else {
+    p.W[0] = w[0].w1; p.W[1] = w[1].w1;
+    p.bias[0] = w[0].b1; p.bias[1] = w[1].b1;
+    he = timed(K_GEMM_FC1, st, [&] { return launch_gemm(bf, GEMM_FC1, p, st); });
+  }
   if (he != hipSuccess) return HILO_E_DEVICE;
 
   GemmProblem q = base_problem(s, cu_seqlens, mod, part);
   q.A = hid; q.lda = F;
-  q.W[0] = w[0].w2; q.W[1] = w[1].w2;
-  q.bias[0] = w[0].b2; q.bias[1] = w[1].b2;
+  q.W[0] = w8 ? w8[0].w2 : w[0].w2; q.W[1] = w8 ? w8[1].w2 : w[1].w2;
+  q.bias[0] = w8 ? w8[0].b2 : w[0].b2; q.bias[1] = w8 ? w8[1].b2 : w[1].b2;
   q.N = D; q.K = F;
   q.z = z; q.ldz = D; q.gate_idx = 5;
   return dev_status(timed(K_GEMM_FC2, st, [&] { return launch_gemm(bf, GEMM_FC2, q, st); }));
@@ -403,7 +462,7 @@ hilo_status hilo_attention(const hilo_shape *s, float *z, const int32_t *cu_seql
   if ((e = check_attn_w(w)) != HILO_OK) return e;
   if (ws_bytes < ws_attention(s)) return HILO_E_WORKSPACE;
   if (!have_device()) return HILO_E_DEVICE;
-  return enqueue_attention(s, z, cu_seqlens, w, mod, workspace, reinterpret_cast<hipStream_t>(stream));
+  return enqueue_attention(s, z, cu_seqlens, w, nullptr, mod, workspace, reinterpret_cast<hipStream_t>(stream));
 }
 
 hilo_status hilo_mlp(const hilo_shape *s, float *z, const int32_t *cu_seqlens,
@@ -415,7 +474,43 @@ hilo_status hilo_mlp(const hilo_shape *s, float *z, const int32_t *cu_seqlens,
   if ((e = check_mlp_w(w)) != HILO_OK) return e;
   if (ws_bytes < ws_mlp(s)) return HILO_E_WORKSPACE;
   if (!have_device()) return HILO_E_DEVICE;
-  return enqueue_mlp(s, z, cu_seqlens, w, mod, workspace, reinterpret_cast<hipStream_t>(stream));
+  return enqueue_mlp(s, z, cu_seqlens, w, nullptr, mod, workspace, reinterpret_cast<hipStream_t>(stream));
+}
+
+hilo_status hilo_attention_fp8(const hilo_shape *s, float *z, const int32_t *cu_seqlens,
+                               const hilo_attn_w_fp8 w[2], const float *mod, void *workspace,
+                               size_t ws_bytes, void *stream) {
+  hilo_status e = check_fp8_block(s);
+  if (e != HILO_OK) return e;
+  if (!z || !cu_seqlens || !mod || !workspace) return HILO_E_NULL;
+  if ((e = check_attn_w8(w)) != HILO_OK) return e;
+  if (ws_bytes < ws_attention(s)) return HILO_E_WORKSPACE;
+  if (!have_device()) return HILO_E_DEVICE;
+  return enqueue_attention(s, z, cu_seqlens, nullptr, w, mod, workspace, reinterpret_cast<hipStream_t>(stream));
+}
+
+hilo_status hilo_mlp_fp8(const hilo_shape *s, float *z, const int32_t *cu_seqlens,
+                         const hilo_mlp_w_fp8 w[2], const float *mod, void *workspace, size_t ws_bytes,
+                         void *stream) {
+  hilo_status e = check_fp8_block(s);
+  if (e != HILO_OK) return e;
+  if (!z || !cu_seqlens || !mod || !workspace) return HILO_E_NULL;
+  if ((e = check_mlp_w8(w)) != HILO_OK) return e;
+  if (ws_bytes < ws_mlp(s)) return HILO_E_WORKSPACE;
+  if (!have_device()) return HILO_E_DEVICE;
+  return enqueue_mlp(s, z, cu_seqlens, nullptr, w, mod, workspace, reinterpret_cast<hipStream_t>(stream));
+}
+
+hilo_status hilo_quantize_rows(int32_t dtype, const void *x, int64_t rows, int64_t cols, uint8_t *codes,
+                               float *scale, void *stream) {
+  if (dtype != HILO_F32 && dtype != HILO_BF16) return HILO_E_DTYPE;
+  if (rows < 0 || rows >= (1LL << 31) - 4 || cols <= 0 || cols % 4 != 0 || cols > (1LL << 31) - 1)
+    return HILO_E_SHAPE;
+  if (!x || !codes || !scale) return HILO_E_NULL;
+  if (rows == 0) return HILO_OK;
+  if (!have_device()) return HILO_E_DEVICE;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  return dev_status(launch_quantize_rows(dtype == HILO_BF16, x, int(rows), int(cols), codes, scale, st));
 }
 
 hilo_status hilo_blocks(const hilo_shape *s, float *z, const int32_t *cu_seqlens,
@@ -435,8 +530,8 @@ hilo_status hilo_blocks(const hilo_shape *s, float *z, const int32_t *cu_seqlens
   const size_t mod_stride = size_t(s->batch) * 2 * 6 * s->dim;
   for (int l = 0; l < n_blocks; ++l) {
     const float *ml = mod + l * mod_stride;
-    if ((e = enqueue_attention(s, z, cu_seqlens, attn_w + 2 * l, ml, workspace, st)) != HILO_OK) return e;
-    if ((e = enqueue_mlp(s, z, cu_seqlens, mlp_w + 2 * l, ml, workspace, st)) != HILO_OK) return e;
+    if ((e = enqueue_attention(s, z, cu_seqlens, attn_w + 2 * l, nullptr, ml, workspace, st)) != HILO_OK) return e;
+    if ((e = enqueue_mlp(s, z, cu_seqlens, mlp_w + 2 * l, nullptr, ml, workspace, st)) != HILO_OK) return e;
   }
   return HILO_OK;
 }

@@ -173,12 +173,12 @@ struct SkPlan {
 // and their fixup cost more than the idle CUs.
 constexpr int kNoSplitSteps = 64;
 
-HILO_DEV SkPlan sk_plan(const GemmProblem &p, int BM, int BN, int P) {
+HILO_DEV SkPlan sk_plan(const GemmProblem &p, int BM, int BN, int P, int kstep = 64) {
   SkPlan q;
   q.R = row_tiles_total(p, BM);
   q.TN = (p.N + BN - 1) / BN;
   q.T = q.R * q.TN;
-  q.nk = p.K / 64;
+  q.nk = p.K / kstep;
   // 256 x 256 tiles: a stream-K tail costs a 256 KiB partial per piece; when the last wave holds
   // at least half of P tiles, whole tiles in ceil(T / P) waves finish sooner
   const bool whole_waves = BM * BN >= 256 * 256 && q.T >= P && 2 * (q.T % P) >= P;
@@ -291,7 +291,7 @@ struct SkTile {
   // the first store: the compiler cannot prove that the outputs do not alias the inputs, so an
   // interleaved order would serialise one memory round trip per fragment.  Loads use indices
   // clamped into the tile; values for rows or columns outside it are never stored.
-  template <int EPI, int ROWS>
+  template <int EPI, int ROWS, bool F8 = false>
   HILO_DEV static void epilogue_rows(const GemmProblem &p, const TileRows &tr, int n0, int wid, int i0,
                                      int lane, const f32x4 (&acc)[ROWS][TN]) {
     const int rbase = (wid / WN) * (BM / WM) + i0 * 16 + (lane & 15);
@@ -308,6 +308,15 @@ struct SkTile {
       bv[j][2] = __uint_as_float(bu.y << 16); bv[j][3] = __uint_as_float(bu.y & 0xffff0000u);
       if constexpr (EPI == EPI_RESID)
         gt[j] = *reinterpret_cast<const float4 *>(p.mod + (size_t(tr.s * 2 + tr.sigma) * 6 + p.gate_idx) * p.D + nc);
+    }
+    float4 wsc[TN];
+    float asc[ROWS];
+    if constexpr (F8) {
+      const float *ws = tr.sigma ? p.w_scale[1] : p.w_scale[0];
+#pragma unroll
+      for (int j = 0; j < TN; ++j) wsc[j] = *reinterpret_cast<const float4 *>(ws + min(cbase + j * 16, p.N - 4));
+#pragma unroll
+      for (int i = 0; i < ROWS; ++i) asc[i] = p.a_scale[tr.row0 + min(rbase + i * 16, tr.nrows - 1)];
     }
     if constexpr (EPI == EPI_RESID) {
 #pragma unroll
@@ -328,8 +337,15 @@ struct SkTile {
         const int n = cbase + j * 16;
         if (n >= p.N) continue;
         float v[4];
+        if constexpr (F8) {
+          v[0] = acc[i][j][0] * (asc[i] * wsc[j].x) + bv[j][0];
+          v[1] = acc[i][j][1] * (asc[i] * wsc[j].y) + bv[j][1];
+          v[2] = acc[i][j][2] * (asc[i] * wsc[j].z) + bv[j][2];
+          v[3] = acc[i][j][3] * (asc[i] * wsc[j].w) + bv[j][3];
+        } else {
 #pragma unroll
-        for (int e = 0; e < 4; ++e) v[e] = acc[i][j][e] + bv[j][e];
+          for (int e = 0; e < 4; ++e) v[e] = acc[i][j][e] + bv[j][e];
+        }
         if constexpr (EPI == EPI_RESID) {
           float4 zn = zv[i][j];
           zn.x += gt[j].x * v[0];
@@ -521,6 +537,14 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 // first K stage of a tile: accumulate onto zero (no separate clearing of the AGPRs)
 #define HILO_MFMA_AGPR0(ACC, FB, FA) \
   asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, 0" : "=a"(ACC) : "v"(FB), "v"(FA) : "memory")
+// FP8: 32 x 32 output block, 64-deep K, E4M3 codes in both operands (8 registers per operand)
+typedef uint32_t u32x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+#define HILO_MFMA8_AGPR(ACC, FB, FA) \
+  asm volatile("v_mfma_f32_32x32x64_f8f6f4 %0, %1, %2, %0" : "+a"(ACC) : "v"(FB), "v"(FA) : "memory")
+#define HILO_MFMA8_AGPR0(ACC, FB, FA) \
+  asm volatile("v_mfma_f32_32x32x64_f8f6f4 %0, %1, %2, 0" : "=a"(ACC) : "v"(FB), "v"(FA) : "memory")
+HILO_DEV u32x8 cat8(u32x4 lo, u32x4 hi) { return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7); }
 #define HILO_DS_READ16(DST, ADDR, OFF) \
   asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(DST) : "v"(ADDR), "i"(OFF) : "memory")
 
@@ -608,8 +632,68 @@ HILO_DEV void big_epilogue(const GemmProblem &p, const TileRows &tr, int n0, int
   }
 }
 
+// Epilogue of a 256 x 256 FP8 tile (wave tile 128 x 128 in 4 x 4 blocks of 32 x 32).  Lane l of
+// block (bi, bj) holds row 32 bi + l % 32 of the wave tile and, in register 4 b + e, column
+// 32 bj + 8 b + 4 (l / 32) + e.  acc * (row scale * column scale) + bias, then GELU for MLP up;
+// the column-only operands (bias, weight scales) and the four row scales are loaded once.
+template <int EPI>
+HILO_DEV void big_epilogue8(const GemmProblem &p, const TileRows &tr, int n0, int wid, int lane, f32x16 (&acc)[4][4]) {
+  static_assert(EPI != EPI_RESID, "FP8 projections end in a bias or GELU epilogue");
+  const int rbase = (wid >> 1) * 128 + (lane & 31);
+  const int cbase = n0 + (wid & 1) * 128 + 4 * (lane >> 5);
+  const uint16_t *bias = reinterpret_cast<const uint16_t *>(tr.sigma ? p.bias[1] : p.bias[0]);
+  const float *wsp = tr.sigma ? p.w_scale[1] : p.w_scale[0];
+  uint2 bu[4][4];
+  float4 ws[4][4];
+  float as[4];
+#pragma unroll
+  for (int bj = 0; bj < 4; ++bj)
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      const int nc = min(cbase + 32 * bj + 8 * b, p.N - 4);
+      bu[bj][b] = *reinterpret_cast<const uint2 *>(bias + nc);
+      ws[bj][b] = *reinterpret_cast<const float4 *>(wsp + nc);
+    }
+#pragma unroll
+  for (int bi = 0; bi < 4; ++bi) as[bi] = p.a_scale[tr.row0 + min(rbase + 32 * bi, tr.nrows - 1)];
+#pragma unroll
+  for (int bi = 0; bi < 4; ++bi) {
+    const int rl = rbase + 32 * bi;
+#pragma unroll
+    for (int bj = 0; bj < 4; ++bj) {
+      f32x16 blk = acc[bi][bj];  // one block out of the AGPRs at a time
+      asm volatile("" : "+v"(blk));
+      if (rl < tr.nrows) {
+        const size_t m = size_t(tr.row0 + rl);
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+          const int n = cbase + 32 * bj + 8 * b;
+          if (n >= p.N) continue;
+          const float sa = as[bi];
+          float v[4];
+          v[0] = blk[4 * b + 0] * (sa * ws[bj][b].x) + __uint_as_float(bu[bj][b].x << 16);
+          v[1] = blk[4 * b + 1] * (sa * ws[bj][b].y) + __uint_as_float(bu[bj][b].x & 0xffff0000u);
+          v[2] = blk[4 * b + 2] * (sa * ws[bj][b].z) + __uint_as_float(bu[bj][b].y << 16);
+          v[3] = blk[4 * b + 3] * (sa * ws[bj][b].w) + __uint_as_float(bu[bj][b].y & 0xffff0000u);
+          if constexpr (EPI == EPI_GELU) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[e] = gelu_tanh(v[e]);
+          }
+          uint2 u;
+          u.x = pack_bf16x2(v[0], v[1]);
+          u.y = pack_bf16x2(v[2], v[3]);
+          *reinterpret_cast<uint2 *>(reinterpret_cast<uint16_t *>(p.out) + m * p.ldo + n) = u;
+        }
+      }
+      asm volatile("" ::: "memory");
+    }
+  }
+}
+
 // BN = 256 or 128: wave tile 128 x BN/2, TNW = BN/32 weight fragments per wave.
-template <int EPI, int ROLE, int BN>
+// F8 (BN = 256 only): E4M3 operands, a stage holds 64 K values per row (the same 64 bytes), and the
+// wave tile is 4 x 4 MFMAs of 32 x 32 x 64; each fragment is two 16-byte LDS reads per lane.
+template <int EPI, int ROLE, int BN, bool F8>
 __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
   using big::BM;
   using big::BK;
@@ -623,37 +707,39 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
   constexpr int NR = 8 + TNW;           // fragment reads per wave per stage
   constexpr int AB = BM * BK * 2;       // bytes of a stage's A rows
   constexpr int SB = (BM + BN) * BK * 2;
+  constexpr int ESZ = F8 ? 1 : 2;       // operand bytes per element
+  static_assert(!F8 || BN == 256, "FP8 runs 256 x 256 tiles");
   __shared__ __attribute__((aligned(1024))) uint8_t lds[S * SB];
 
   const int P = gridDim.x;
   const int pid = xcd_remap(blockIdx.x, P);
-  const SkPlan q = sk_plan(p, BM, BN, P);
+  const SkPlan q = sk_plan(p, BM, BN, P, F8 ? 128 : 64);
   const SkRange rg = sk_range(q.I, P, pid);
 
   const int lane = threadIdx.x & 63;
   const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lrow = lane >> 2, lslot = lane & 3;
-  const uint16_t *A = reinterpret_cast<const uint16_t *>(p.A);
+  const uint8_t *A = reinterpret_cast<const uint8_t *>(p.A);
 
   // ---- loader: its own cursor over this workgroup's items, three stages ahead of the MFMAs
   SkCursor lc{pid, rg.beg};
-  const uint16_t *la[4], *lb[LB];
-  int lk = 0, lke = 0;  // next stage to load (32-deep, absolute in K) and the end of its item
+  const uint8_t *la[4], *lb[LB];
+  int lk = 0, lke = 0;  // next stage to load (64 bytes of each row, absolute in K) and the end of its item
   auto ld_src = [&](int t) __attribute__((always_inline)) {
     int rt, tn;
     tile_coords(q, t, rt, tn);
     tn = uni(tn);
     const TileRows tr = uni(decode_row_tile(p, BM, uni(rt)));
-    const uint16_t *Wt = reinterpret_cast<const uint16_t *>(tr.sigma ? p.W[1] : p.W[0]);
+    const uint8_t *Wt = reinterpret_cast<const uint8_t *>(tr.sigma ? p.W[1] : p.W[0]);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int r = wid * 64 + 16 * i + lrow;
-      la[i] = A + size_t(tr.row0 + min(r, tr.nrows - 1)) * p.lda + (lslot ^ swz(r)) * 8;
+      la[i] = A + size_t(tr.row0 + min(r, tr.nrows - 1)) * p.lda * ESZ + (lslot ^ swz(r)) * 16;
     }
 #pragma unroll
     for (int i = 0; i < LB; ++i) {
       const int r = wid * (BN / 4) + 16 * i + lrow;
-      lb[i] = Wt + size_t(min(tn * BN + r, p.N - 1)) * p.K + (lslot ^ swz(r)) * 8;
+      lb[i] = Wt + size_t(min(tn * BN + r, p.N - 1)) * p.K * ESZ + (lslot ^ swz(r)) * 16;
     }
   };
   auto ld_advance = [&]() __attribute__((always_inline)) {
@@ -671,7 +757,7 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
   // load instruction j (0..LQ-1) of the current loader stage into `slot`: A rows for j < 4
   auto ld_one = [&](int slot, int j) __attribute__((always_inline)) {
     uint8_t *base = lds + slot * SB;
-    const int k0 = lk * BK;
+    const int k0 = lk * 64;  // bytes
     if (j < 4) g2lds16(la[j] + k0, base + wid * 64 * 64 + j * 1024);
     else g2lds16(lb[j - 4] + k0, base + AB + wid * (BN / 4) * 64 + (j - 4) * 1024);
   };
@@ -699,7 +785,30 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
 #undef HILO_RD_CASE
   };
 
+  // FP8 fragments: lane (r, g) = (lane % 32, lane / 32) reads bytes 32 g .. 32 g + 31 of row r of
+  // a 32-row fragment, as chunk 2 g (low half) and chunk 2 g + 1 (high half)
+  const int r8 = lane & 31, g8 = lane >> 5;
+  const uint32_t lo8 = r8 * 64 + (((2 * g8) ^ swz(r8)) * 16), hi8 = r8 * 64 + (((2 * g8 + 1) ^ swz(r8)) * 16);
+  const uint32_t fa8 = lds0 + (wid >> 1) * 128 * 64, fb8 = lds0 + AB + (wid & 1) * 128 * 64;
+  const uint32_t fa8l = fa8 + lo8, fa8h = fa8 + hi8, fb8l = fb8 + lo8, fb8h = fb8 + hi8;
+  // read t of a stage (slot byte offset so): W fragment t / 2 (halves t % 2) for t < 8, then A
+  auto rd_one8 = [&](u32x4 (&fa)[8], u32x4 (&fb)[8], uint32_t so, int t) __attribute__((always_inline)) {
+#define HILO_RD8_CASE(C)                                                                                      \
+  case C:                                                                                                     \
+    if constexpr (C < 8) HILO_DS_READ16(fb[C & 7], ((C & 1) ? fb8h : fb8l) + so, ((C & 7) >> 1) * 2048);      \
+    else HILO_DS_READ16(fa[C & 7], ((C & 1) ? fa8h : fa8l) + so, ((C & 7) >> 1) * 2048);                      \
+    break;
+    switch (t) {
+      HILO_RD8_CASE(0) HILO_RD8_CASE(1) HILO_RD8_CASE(2) HILO_RD8_CASE(3) HILO_RD8_CASE(4) HILO_RD8_CASE(5)
+      HILO_RD8_CASE(6) HILO_RD8_CASE(7) HILO_RD8_CASE(8) HILO_RD8_CASE(9) HILO_RD8_CASE(10) HILO_RD8_CASE(11)
+      HILO_RD8_CASE(12) HILO_RD8_CASE(13) HILO_RD8_CASE(14) HILO_RD8_CASE(15)
+      default: break;
+    }
+#undef HILO_RD8_CASE
+  };
+
   f32x4 acc[8][TNW];
+  f32x16 acc8[4][4];
   u32x4 xa[8], xb[TNW], ya[8], yb[TNW];
 
   // one stage (ring slot gs % S) on fragments (fa, fb); reads stage gs + 1 into (na, nb); the
@@ -726,6 +835,35 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
     }
     ++lk;
   };
+  // FP8 stage: 16 MFMAs (block row bi, block column bj); the barrier before MFMA 4, then after each
+  // of MFMAs 4..11 one load of the stage three ahead and two fragment reads of the next stage
+  auto stage8 = [&](auto first, u32x4 (&fa)[8], u32x4 (&fb)[8], u32x4 (&na)[8], u32x4 (&nb)[8], int gs) __attribute__((always_inline)) {
+    const int lslot_w = (gs + S - 1) & (S - 1);
+    const uint32_t so = uint32_t(((gs + 1) & (S - 1)) * SB);
+#pragma unroll
+    for (int bi = 0; bi < 4; ++bi) {
+      // outstanding reads allowed: this stage's A halves of blocks bi+1..3, the next stage's so far
+      wait_lgkm_rt(2 * (3 - bi) + 2 * min(max(4 * bi - 4, 0), 8));
+      const u32x8 a8 = cat8(fa[2 * bi], fa[2 * bi + 1]);
+#pragma unroll
+      for (int bj = 0; bj < 4; ++bj) {
+        const int qq = 4 * bi + bj;
+        if (qq == 4) asm volatile("s_waitcnt vmcnt(%0)\n s_barrier" ::"n"((S - 3) * LQ) : "memory");
+        if constexpr (decltype(first)::value) HILO_MFMA8_AGPR0(acc8[bi][bj], cat8(fb[2 * bj], fb[2 * bj + 1]), a8);
+        else HILO_MFMA8_AGPR(acc8[bi][bj], cat8(fb[2 * bj], fb[2 * bj + 1]), a8);
+        if (qq >= 4 && qq < 12) {
+          ld_one(lslot_w, qq - 4);
+          rd_one8(na, nb, so, 2 * (qq - 4));
+          rd_one8(na, nb, so, 2 * (qq - 4) + 1);
+        }
+      }
+    }
+    ++lk;
+  };
+  auto run_stage = [&](auto first, u32x4 (&fa)[8], u32x4 (&fb)[TNW], u32x4 (&na)[8], u32x4 (&nb)[TNW], int gs) __attribute__((always_inline)) {
+    if constexpr (F8) stage8(first, fa, fb, na, nb, gs);
+    else stage(first, fa, fb, na, nb, gs);
+  };
 
   SkCursor cc{pid, rg.beg};
   SkItem cur = uni(sk_next_item(cc, q, rg, P, pid, p.part, T::kPartFloats));
@@ -740,7 +878,10 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
   }
   asm volatile("s_waitcnt vmcnt(%0)\n s_barrier" ::"n"((S - 2) * LQ) : "memory");
 #pragma unroll
-  for (int t = 0; t < NR; ++t) rd_one(xa, xb, fa0, fb0, t);
+  for (int t = 0; t < NR; ++t) {
+    if constexpr (F8) rd_one8(xa, xb, 0, t);
+    else rd_one(xa, xb, fa0, fb0, t);
+  }
 
   // the loader moves to its next item between stages, outside the MFMA schedule
   auto ld_check = [&]() __attribute__((always_inline)) {
@@ -749,32 +890,57 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
   int gs = 0;
   while (true) {
     ld_check();
-    stage(std::true_type{}, xa, xb, ya, yb, gs);
+    run_stage(std::true_type{}, xa, xb, ya, yb, gs);
     ld_check();
-    stage(std::false_type{}, ya, yb, xa, xb, gs + 1);
+    run_stage(std::false_type{}, ya, yb, xa, xb, gs + 1);
     gs += 2;
 #pragma unroll 1
     for (int kt = cur.kb + 1; kt < cur.ke; ++kt) {
       ld_check();
-      stage(std::false_type{}, xa, xb, ya, yb, gs);
+      run_stage(std::false_type{}, xa, xb, ya, yb, gs);
       ld_check();
-      stage(std::false_type{}, ya, yb, xa, xb, gs + 1);
+      run_stage(std::false_type{}, ya, yb, xa, xb, gs + 1);
       gs += 2;
     }
     // The last MFMAs' results must land before the accumulators are read (the empty asm ties each
     // accumulator to this point, so no read is scheduled above it), and the reads of the next
     // stage's fragments must be complete before the compiler may move those registers.
-    asm volatile("s_waitcnt lgkmcnt(0)\n s_nop 7\n s_nop 7\n s_nop 7" ::: "memory");
+    asm volatile("s_waitcnt lgkmcnt(0)\n s_nop 7\n s_nop 7\n s_nop 7\n s_nop 7" ::: "memory");
+    if constexpr (F8) {
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
+      for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int j = 0; j < TNW; ++j) asm volatile("" : "+a"(acc[i][j]));
+        for (int j = 0; j < 4; ++j) asm volatile("" : "+a"(acc8[i][j]));
+    } else {
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int j = 0; j < TNW; ++j) asm volatile("" : "+a"(acc[i][j]));
+    }
     if (cur.slot == nullptr) {
       int rt, tn;
       tile_coords(q, cur.t, rt, tn);
       tn = uni(tn);
       const TileRows tr = uni(decode_row_tile(p, BM, uni(rt)));
-      big_epilogue<EPI, TNW>(p, tr, tn * BN, wid, lane, acc);
+      if constexpr (F8) big_epilogue8<EPI>(p, tr, tn * BN, wid, lane, acc8);
+      else big_epilogue<EPI, TNW>(p, tr, tn * BN, wid, lane, acc);
+    } else if constexpr (F8) {
+      // the partial tile in the layout of the 16 x 16 fragments (k_gemm_fix reads that layout):
+      // row 32 bi + l % 32 = fragment row 2 bi + (l % 32) / 16, lane l % 16 + 16 (l / 32) + 32 (b % 2)
+      // of fragment column 2 bj + b / 2
+      float *base = cur.slot + (size_t(wid) * 64 * 64 + ((lane & 31) >> 4) * 8 * 64 + (lane & 15) + 16 * (lane >> 5)) * 4;
+#pragma unroll
+      for (int bi = 0; bi < 4; ++bi)
+#pragma unroll
+        for (int bj = 0; bj < 4; ++bj) {
+          f32x16 blk = acc8[bi][bj];
+          asm volatile("" : "+v"(blk));
+#pragma unroll
+          for (int b = 0; b < 4; ++b)
+            *reinterpret_cast<f32x4 *>(base + ((2 * bi * 8 + 2 * bj + b / 2) * 64 + 32 * (b % 2)) * 4) =
+                f32x4{blk[4 * b], blk[4 * b + 1], blk[4 * b + 2], blk[4 * b + 3]};
+          asm volatile("" ::: "memory");
+        }
     } else {
       // straight from the AGPRs (no copy of all 256 accumulators through VGPRs)
       float *base = cur.slot + T::part_index(wid, 0, 0, lane);
@@ -798,11 +964,11 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
 constexpr int kFixThreads = 256;
 constexpr int kFixBatch = 4;
 
-template <int BM, int BN, int WM, int WN, int EPI, int ROLE>
+template <int BM, int BN, int WM, int WN, int EPI, int ROLE, bool F8 = false>
 __global__ __launch_bounds__(kFixThreads) void k_gemm_fix(GemmProblem p, int P) {
   using T = SkTile<BM, BN, WM, WN>;
   constexpr int TM = T::TM, TN = T::TN, NW = T::NW, FW = kFixThreads / 64;
-  const SkPlan q = sk_plan(p, BM, BN, P);
+  const SkPlan q = sk_plan(p, BM, BN, P, F8 ? 128 : 64);
   const int nfix = q.s > 1 ? q.T : q.U - q.dp;
   const int lane = threadIdx.x & 63;
   const int items = nfix * NW * TM;
@@ -871,7 +1037,7 @@ __global__ __launch_bounds__(kFixThreads) void k_gemm_fix(GemmProblem p, int P) 
     int rt, tn;
     tile_coords(q, t, rt, tn);
     const TileRows tr = decode_row_tile(p, BM, rt);
-    T::template epilogue_rows<EPI, 1>(p, tr, tn * BN, wid, i, lane, acc);
+    T::template epilogue_rows<EPI, 1, F8>(p, tr, tn * BN, wid, i, lane, acc);
   }
 }
 
@@ -974,20 +1140,20 @@ static hipError_t run_bf16(const GemmProblem &p, hipStream_t st) {
 }
 
 // 256 x BN tiles: one persistent workgroup per CU.
-template <int ROLE, int BN>
+template <int ROLE, int BN, bool F8 = false>
 static hipError_t run_big(const GemmProblem &p, hipStream_t st) {
   constexpr int BM = big::BM;
   static_assert(size_t(BM) * BN * 3 * kBigMaxWorkgroups * sizeof(float) <= kSkPartBytes, "partial area too small");
   const int P = device_cus() < kBigMaxWorkgroups ? device_cus() : kBigMaxWorkgroups;
-  hipLaunchKernelGGL((k_gemm_big<role_epilogue(ROLE), ROLE, BN>), dim3(P), dim3(256), 0, st, p);
+  hipLaunchKernelGGL((k_gemm_big<role_epilogue(ROLE), ROLE, BN, F8>), dim3(P), dim3(256), 0, st, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const long long tiles_max = (long long)p.B * ((p.max_img_rows + BM - 1) / BM + (p.L + BM - 1) / BM) *
                               ((p.N + BN - 1) / BN);
-  if (tiles_max < P && p.K / 64 <= kNoSplitSteps) return hipSuccess;
+  if (tiles_max < P && p.K / (F8 ? 128 : 64) <= kNoSplitSteps) return hipSuccess;
   constexpr int kFixBlocks = 4 * (BM / 2 / 16) / (kFixThreads / 64);
-  hipLaunchKernelGGL((k_gemm_fix<BM, BN, 2, 2, role_epilogue(ROLE), ROLE>), dim3(P * kFixBlocks), dim3(kFixThreads), 0,
-                     st, p, P);
+  hipLaunchKernelGGL((k_gemm_fix<BM, BN, 2, 2, role_epilogue(ROLE), ROLE, F8>), dim3(P * kFixBlocks), dim3(kFixThreads),
+                     0, st, p, P);
   return hipGetLastError();
 }
 
@@ -1023,6 +1189,14 @@ hipError_t launch_gemm(bool bf16, int role, const GemmProblem &p, hipStream_t st
     case GEMM_O: return run_bf16<128, 128, 2, 2, GEMM_O>(p, st);
     case GEMM_FC1: return run_big<GEMM_FC1, 256>(p, st);
     default: return run_bf16<128, 128, 2, 2, GEMM_FC2>(p, st);
+  }
+}
+
+hipError_t launch_gemm_fp8(int role, const GemmProblem &p, hipStream_t st) {
+  switch (role) {
+    case GEMM_QKV: return run_big<GEMM_QKV, 256, true>(p, st);
+    case GEMM_FC1: return run_big<GEMM_FC1, 256, true>(p, st);
+    default: return hipErrorInvalidValue;
   }
 }
 

@@ -33,6 +33,12 @@ hipError_t launch_decompress_delta(bool bf16, const float *z, const void *x_img,
 // h = LN(z) * (1 + mod[s][stream][which*3 + 1]) + mod[s][stream][which*3], rows < cu[B]
 hipError_t launch_rownorm(bool bf16, const float *z, const int *cu, const float *mod, int B, int L,
                           int D, int Tmax, int which, void *out, hipStream_t st);
+// the same rows as FP8 E4M3 codes [Tmax][D] plus a float32 scale per row (D % 4 == 0)
+hipError_t launch_rownorm_fp8(const float *z, const int *cu, const float *mod, int B, int L, int D,
+                              int Tmax, int which, uint8_t *codes, float *row_scale, hipStream_t st);
+// per-row FP8 E4M3 codes and scales of x [rows][cols] (cols % 4 == 0)
+hipError_t launch_quantize_rows(bool bf16, const void *x, int rows, int cols, uint8_t *codes, float *scale,
+                                hipStream_t st);
 
 enum Epilogue { EPI_BIAS = 0, EPI_GELU = 1, EPI_RESID = 2 };
 // The four projections of the block; each gets its own kernel instantiation (so profiles and
@@ -59,6 +65,8 @@ struct GemmProblem {
   const int *cu;          // [B+1]
   int B, L, max_img_rows; // max_img_rows = images * N
   float *part;            // bf16 path: partial tiles (kSkPartBytes)
+  const float *a_scale;   // FP8 operands: A row m is codes * a_scale[m] ...
+  const float *w_scale[2];  // ... and W row n of stream s is codes * w_scale[s][n]
 };
 
 // Partial-sum area of the bf16 GEMMs (part of the caller's workspace): one slot per data-parallel
@@ -71,6 +79,9 @@ constexpr size_t kSkPartBytes = size_t(kBigMaxWorkgroups) * 3 * 256 * 256 * size
 static_assert(size_t(kSkMaxWorkgroups) * 3 * kSkPartFloats * sizeof(float) <= kSkPartBytes,
               "partial area must hold both tilings");
 hipError_t launch_gemm(bool bf16, int role, const GemmProblem &p, hipStream_t st);
+// FP8 E4M3 operands (A [Tmax][K] codes, W[s] [N][K] codes, per-row scales), bf16 bias and output;
+// the QKV and MLP-up roles only, K % 128 == 0, N % 4 == 0.
+hipError_t launch_gemm_fp8(int role, const GemmProblem &p, hipStream_t st);
 
 // Stream-K partial results of the bf16 attention core (part of the caller's workspace): two
 // slots per workgroup, each the unnormalised output and running max / sum of one query tile.

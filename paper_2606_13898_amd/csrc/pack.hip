@@ -267,13 +267,26 @@ hipError_t launch_decompress(bool bf16, const float *z, const int *idx_map, cons
 
 // ------------------------------------------------------------------------------- row norm
 
+// FP8 E4M3 quantisation of one value after scaling: clamp to the format's range (the conversion
+// itself would turn an overflow into NaN), then round to nearest even.
+HILO_DEV uint32_t fp8x4(float a, float b, float c, float d) {
+  const float m = 448.0f;
+  a = fminf(fmaxf(a, -m), m); b = fminf(fmaxf(b, -m), m);
+  c = fminf(fmaxf(c, -m), m); d = fminf(fmaxf(d, -m), m);
+  int w = __builtin_amdgcn_cvt_pk_fp8_f32(a, b, 0, false);
+  w = __builtin_amdgcn_cvt_pk_fp8_f32(c, d, w, true);
+  return uint32_t(w);
+}
+
 // One wave per row: LN(z) (biased variance, eps 1e-6) * (1 + scale) + shift for the row's sample
-// and stream, written in the projection's input dtype.  NV = float4s per lane covers D <= 256 NV;
-// the row stays in registers between the mean, variance and output passes.
-template <bool BF16, int NV>
+// and stream, written in the projection's input form: OUT 0 float32, 1 bf16, 2 FP8 E4M3 codes plus
+// the row's scale (amax / 448; codes of h * (448 / amax), both divisions correctly rounded).
+// NV = float4s per lane covers D <= 256 NV; the row stays in registers between the passes.
+template <int OUT, int NV>
 __global__ __launch_bounds__(256) void k_rownorm(const float *__restrict__ z, const int *__restrict__ cu,
                                                  const float *__restrict__ mod, int B, int L, int D,
-                                                 int Tmax, int which, void *__restrict__ out) {
+                                                 int Tmax, int which, void *__restrict__ out,
+                                                 float *__restrict__ row_scale) {
   const int lane = threadIdx.x & 63;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= Tmax || row >= cu[B]) return;
@@ -302,6 +315,34 @@ __global__ __launch_bounds__(256) void k_rownorm(const float *__restrict__ z, co
   }
   const float var = wave_sum_f32(sq) / float(D);
   const float rstd = 1.0f / sqrtf(var + 1e-6f);
+  if constexpr (OUT == 2) {
+    float amax = 0.f;
+#pragma unroll
+    for (int k = 0; k < NV; ++k) {
+      const int c = (k * 64 + lane) * 4;
+      if (c < D) {
+        const float4 sc = *reinterpret_cast<const float4 *>(scale + c);
+        const float4 sh = *reinterpret_cast<const float4 *>(shift + c);
+        v[k].x = (v[k].x - mean) * rstd * (1.f + sc.x) + sh.x;
+        v[k].y = (v[k].y - mean) * rstd * (1.f + sc.y) + sh.y;
+        v[k].z = (v[k].z - mean) * rstd * (1.f + sc.z) + sh.z;
+        v[k].w = (v[k].w - mean) * rstd * (1.f + sc.w) + sh.w;
+        amax = fmaxf(amax, fmaxf(fmaxf(fabsf(v[k].x), fabsf(v[k].y)), fmaxf(fabsf(v[k].z), fabsf(v[k].w))));
+      }
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) amax = fmaxf(amax, __shfl_xor(amax, off, 64));
+    const float inv = amax > 0.f ? __fdiv_rn(448.0f, amax) : 0.f;
+    if (lane == 0) row_scale[row] = __fdiv_rn(amax, 448.0f);
+    uint8_t *o = reinterpret_cast<uint8_t *>(out) + size_t(row) * D;
+#pragma unroll
+    for (int k = 0; k < NV; ++k) {
+      const int c = (k * 64 + lane) * 4;
+      if (c < D)
+        *reinterpret_cast<uint32_t *>(o + c) = fp8x4(v[k].x * inv, v[k].y * inv, v[k].z * inv, v[k].w * inv);
+    }
+    return;
+  }
 #pragma unroll
   for (int k = 0; k < NV; ++k) {
     const int c = (k * 64 + lane) * 4;
@@ -312,7 +353,7 @@ __global__ __launch_bounds__(256) void k_rownorm(const float *__restrict__ z, co
       const float h1 = (v[k].y - mean) * rstd * (1.f + sc.y) + sh.y;
       const float h2 = (v[k].z - mean) * rstd * (1.f + sc.z) + sh.z;
       const float h3 = (v[k].w - mean) * rstd * (1.f + sc.w) + sh.w;
-      if constexpr (BF16) {
+      if constexpr (OUT == 1) {
         uint2 u;
         u.x = pack_bf16x2(h0, h1);
         u.y = pack_bf16x2(h2, h3);
@@ -325,14 +366,14 @@ __global__ __launch_bounds__(256) void k_rownorm(const float *__restrict__ z, co
   }
 }
 
-template <bool BF16>
+template <int OUT>
 static hipError_t run_rownorm(const float *z, const int *cu, const float *mod, int B, int L, int D,
-                              int Tmax, int which, void *out, hipStream_t st) {
+                              int Tmax, int which, void *out, float *row_scale, hipStream_t st) {
   const int nblk = (Tmax + 3) / 4;
   const int nv = (D + 255) / 256;
-#define HILO_NORM(NVV)                                                                          \
-  hipLaunchKernelGGL((k_rownorm<BF16, NVV>), dim3(nblk), dim3(256), 0, st, z, cu, mod, B, L, D, \
-                     Tmax, which, out)
+#define HILO_NORM(NVV)                                                                         \
+  hipLaunchKernelGGL((k_rownorm<OUT, NVV>), dim3(nblk), dim3(256), 0, st, z, cu, mod, B, L, D, \
+                     Tmax, which, out, row_scale)
   if (nv <= 4) HILO_NORM(4);
   else if (nv <= 8) HILO_NORM(8);
   else if (nv <= 12) HILO_NORM(12);
@@ -345,8 +386,60 @@ static hipError_t run_rownorm(const float *z, const int *cu, const float *mod, i
 hipError_t launch_rownorm(bool bf16, const float *z, const int *cu, const float *mod, int B, int L,
                           int D, int Tmax, int which, void *out, hipStream_t st) {
   if (Tmax <= 0) return hipSuccess;
-  return bf16 ? run_rownorm<true>(z, cu, mod, B, L, D, Tmax, which, out, st)
-              : run_rownorm<false>(z, cu, mod, B, L, D, Tmax, which, out, st);
+  return bf16 ? run_rownorm<1>(z, cu, mod, B, L, D, Tmax, which, out, nullptr, st)
+              : run_rownorm<0>(z, cu, mod, B, L, D, Tmax, which, out, nullptr, st);
+}
+
+hipError_t launch_rownorm_fp8(const float *z, const int *cu, const float *mod, int B, int L, int D,
+                              int Tmax, int which, uint8_t *codes, float *row_scale, hipStream_t st) {
+  if (Tmax <= 0) return hipSuccess;
+  return run_rownorm<2>(z, cu, mod, B, L, D, Tmax, which, codes, row_scale, st);
+}
+
+// Per-row FP8 quantisation of a [rows][cols] matrix (bf16 or float32), one wave per row: the row's
+// amax, then the codes of x * (448 / amax) and the scale amax / 448 (as k_rownorm's FP8 output).
+template <bool BF16>
+__global__ __launch_bounds__(256) void k_quantize_rows(const void *__restrict__ x, int rows, int cols,
+                                                       uint8_t *__restrict__ codes, float *__restrict__ scale) {
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  auto ld4 = [&](int c, float *f) {
+    if constexpr (BF16) {
+      const uint2 u = *reinterpret_cast<const uint2 *>(reinterpret_cast<const uint16_t *>(x) + size_t(row) * cols + c);
+      f[0] = __uint_as_float(u.x << 16); f[1] = __uint_as_float(u.x & 0xffff0000u);
+      f[2] = __uint_as_float(u.y << 16); f[3] = __uint_as_float(u.y & 0xffff0000u);
+    } else {
+      const float4 u = *reinterpret_cast<const float4 *>(reinterpret_cast<const float *>(x) + size_t(row) * cols + c);
+      f[0] = u.x; f[1] = u.y; f[2] = u.z; f[3] = u.w;
+    }
+  };
+  float amax = 0.f;
+  for (int c = lane * 4; c < cols; c += 256) {
+    float f[4];
+    ld4(c, f);
+    amax = fmaxf(amax, fmaxf(fmaxf(fabsf(f[0]), fabsf(f[1])), fmaxf(fabsf(f[2]), fabsf(f[3]))));
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) amax = fmaxf(amax, __shfl_xor(amax, off, 64));
+  const float inv = amax > 0.f ? __fdiv_rn(448.0f, amax) : 0.f;
+  if (lane == 0) scale[row] = __fdiv_rn(amax, 448.0f);
+  for (int c = lane * 4; c < cols; c += 256) {
+    float f[4];
+    ld4(c, f);
+    *reinterpret_cast<uint32_t *>(codes + size_t(row) * cols + c) = fp8x4(f[0] * inv, f[1] * inv, f[2] * inv, f[3] * inv);
+  }
+}
+
+hipError_t launch_quantize_rows(bool bf16, const void *x, int rows, int cols, uint8_t *codes, float *scale,
+                                hipStream_t st) {
+  if (rows <= 0) return hipSuccess;
+  const int nblk = (rows + 3) / 4;
+  if (bf16)
+    hipLaunchKernelGGL(k_quantize_rows<true>, dim3(nblk), dim3(256), 0, st, x, rows, cols, codes, scale);
+  else
+    hipLaunchKernelGGL(k_quantize_rows<false>, dim3(nblk), dim3(256), 0, st, x, rows, cols, codes, scale);
+  return hipGetLastError();
 }
 
 }  // namespace hilo

@@ -43,6 +43,14 @@ class hilo_mlp_w(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in ("w1", "b1", "w2", "b2")]
 
 
+class hilo_attn_w_fp8(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in ("w_qkv", "s_qkv", "b_qkv", "w_o", "b_o")]
+
+
+class hilo_mlp_w_fp8(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in ("w1", "s1", "b1", "w2", "b2")]
+
+
 _lib = None
 
 _P = ctypes.c_void_p
@@ -61,6 +69,11 @@ _SIG = {
                        ctypes.c_size_t, _P],
     "hilo_mlp": [ctypes.POINTER(hilo_shape), _P, _P, ctypes.POINTER(hilo_mlp_w), _P, _P,
                  ctypes.c_size_t, _P],
+    "hilo_attention_fp8": [ctypes.POINTER(hilo_shape), _P, _P, ctypes.POINTER(hilo_attn_w_fp8), _P, _P,
+                           ctypes.c_size_t, _P],
+    "hilo_mlp_fp8": [ctypes.POINTER(hilo_shape), _P, _P, ctypes.POINTER(hilo_mlp_w_fp8), _P, _P,
+                     ctypes.c_size_t, _P],
+    "hilo_quantize_rows": [ctypes.c_int32, _P, ctypes.c_int64, ctypes.c_int64, _P, _P, _P],
     "hilo_blocks": [ctypes.POINTER(hilo_shape), _P, _P, ctypes.POINTER(hilo_attn_w),
                     ctypes.POINTER(hilo_mlp_w), _P, ctypes.c_int32, _P, ctypes.c_size_t, _P],
     "hilo_decompress": [ctypes.POINTER(hilo_shape), _P, _P, _P, _P, _P, _P, _P],
@@ -210,6 +223,59 @@ def hilo_attention(shape, z, cu_seqlens, w, mod, workspace, stream=None):
 
 def hilo_mlp(shape, z, cu_seqlens, w, mod, workspace, stream=None):
     _check("hilo_mlp", lib().hilo_mlp(
+        ctypes.byref(shape), _ptr(z), _ptr(cu_seqlens), w, _ptr(mod), _ptr(workspace),
+        workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def hilo_quantize_rows(x, codes, scale, stream=None):
+    """Per-row E4M3 codes (uint8 [rows][cols]) and float32 scales [rows] of x (float32 or bf16)."""
+    dt = {torch.float32: F32, torch.bfloat16: BF16}.get(x.dtype, -1)
+    rows, cols = (x.shape[0], x.shape[1]) if x.dim() == 2 else (-1, -1)
+    _check("hilo_quantize_rows", lib().hilo_quantize_rows(
+        dt, _ptr(x), rows, cols, _ptr(codes), _ptr(scale), _stream(stream)))
+
+
+def quantize_fp8_weights(ws: Sequence[dict], stream=None):
+    """Per stream, the FP8 codes and scales of w_qkv and w1 (hilo_quantize_rows) next to the other
+    bf16 tensors: the weight dicts hilo_attention_fp8 / hilo_mlp_fp8 take (keys w_qkv, s_qkv, b_qkv,
+    w_o, b_o, w1, s1, b1, w2, b2)."""
+    out = []
+    for w in ws:
+        d = dict(w)
+        for name, sname in (("w_qkv", "s_qkv"), ("w1", "s1")):
+            src = w[name]
+            codes = torch.empty(src.shape, dtype=torch.uint8, device=src.device)
+            scale = torch.empty(src.shape[0], dtype=torch.float32, device=src.device)
+            hilo_quantize_rows(src, codes, scale, stream)
+            d[name], d[sname] = codes, scale
+        out.append(d)
+    return out
+
+
+def attn_weights_fp8(ws: Sequence[dict]):
+    arr = (hilo_attn_w_fp8 * 2)()
+    for k in range(2):
+        arr[k] = hilo_attn_w_fp8(_ptr(ws[k]["w_qkv"]), _ptr(ws[k]["s_qkv"]), _ptr(ws[k]["b_qkv"]),
+                                 _ptr(ws[k]["w_o"]), _ptr(ws[k]["b_o"]))
+    return arr
+
+
+def mlp_weights_fp8(ws: Sequence[dict]):
+    arr = (hilo_mlp_w_fp8 * 2)()
+    for k in range(2):
+        arr[k] = hilo_mlp_w_fp8(_ptr(ws[k]["w1"]), _ptr(ws[k]["s1"]), _ptr(ws[k]["b1"]),
+                                _ptr(ws[k]["w2"]), _ptr(ws[k]["b2"]))
+    return arr
+
+
+def hilo_attention_fp8(shape, z, cu_seqlens, w, mod, workspace, stream=None):
+    _check("hilo_attention_fp8", lib().hilo_attention_fp8(
+        ctypes.byref(shape), _ptr(z), _ptr(cu_seqlens), w, _ptr(mod), _ptr(workspace),
+        workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def hilo_mlp_fp8(shape, z, cu_seqlens, w, mod, workspace, stream=None):
+    _check("hilo_mlp_fp8", lib().hilo_mlp_fp8(
         ctypes.byref(shape), _ptr(z), _ptr(cu_seqlens), w, _ptr(mod), _ptr(workspace),
         workspace.numel() * workspace.element_size(), _stream(stream)))
 

@@ -72,11 +72,26 @@ class DeviceBlock:
         hilo.hilo_compress(self.shape, self.x_img, self.x_txt, self.fine_idx, self.pool_idx,
                            self.counts, self.cu, self.seg, self.z, stream)
 
-    def attention(self, stream=None):
-        hilo.hilo_attention(self.shape, self.z, self.cu, self.aw, self.mod, self.ws, stream)
+    def prepare_fp8(self, stream=None):
+        """FP8 codes and per-output-channel scales of W_qkv and W1 (once; weights are static)."""
+        if getattr(self, "weights8", None) is None:
+            self.weights8 = hilo.quantize_fp8_weights(self.weights, stream)
+            self.aw8 = hilo.attn_weights_fp8(self.weights8)
+            self.mw8 = hilo.mlp_weights_fp8(self.weights8)
 
-    def mlp(self, stream=None):
-        hilo.hilo_mlp(self.shape, self.z, self.cu, self.mw, self.mod, self.ws, stream)
+    def attention(self, stream=None, fp8: bool = False):
+        if fp8:
+            self.prepare_fp8(stream)
+            hilo.hilo_attention_fp8(self.shape, self.z, self.cu, self.aw8, self.mod, self.ws, stream)
+        else:
+            hilo.hilo_attention(self.shape, self.z, self.cu, self.aw, self.mod, self.ws, stream)
+
+    def mlp(self, stream=None, fp8: bool = False):
+        if fp8:
+            self.prepare_fp8(stream)
+            hilo.hilo_mlp_fp8(self.shape, self.z, self.cu, self.mw8, self.mod, self.ws, stream)
+        else:
+            hilo.hilo_mlp(self.shape, self.z, self.cu, self.mw, self.mod, self.ws, stream)
 
     def decompress(self, stream=None, delta: bool = False):
         if delta:
@@ -87,14 +102,15 @@ class DeviceBlock:
                                  self.y_txt, stream)
 
     def run(self, mode: int = hilo.TOPK, keep=None, tau=None, dilate_r=None, stream=None,
-            tokens: int = hilo.PARTITION, delta: bool = False):
-        """One pass of the whole hot path: score, select, compress, attention, MLP, decompress."""
+            tokens: int = hilo.PARTITION, delta: bool = False, fp8: bool = False):
+        """One pass of the whole hot path: score, select, compress, attention, MLP, decompress
+        (fp8: the QKV and MLP-up projections in FP8)."""
         self.score(stream)
         self.select(mode, keep, tau, dilate_r, stream, tokens)
         self.compress(stream)
         if self.with_block:
-            self.attention(stream)
-            self.mlp(stream)
+            self.attention(stream, fp8)
+            self.mlp(stream, fp8)
         self.decompress(stream, delta)
 
 

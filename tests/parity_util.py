@@ -57,10 +57,10 @@ def check_selection(db: DeviceBlock, ref: dict):
 
 
 def oracle_for(wl: inputs.Workload, mode="topk", keep=None, tau=None, r=None, rows=None,
-               with_block=True, tokens="partition", delta=False):
+               with_block=True, tokens="partition", delta=False, fp8=False):
     return O.pipeline(wl.x_img, wl.x_txt, wl.shape, wl.force, wl.dilate_r if r is None else r,
                       mode, tau=tau, keep=wl.keep if keep is None else keep, weights=wl.weights,
-                      mod=wl.mod, rows=rows, with_block=with_block, tokens=tokens, delta=delta)
+                      mod=wl.mod, rows=rows, with_block=with_block, tokens=tokens, delta=delta, fp8=fp8)
 
 
 def midpoint_tau(E, force, shape, r, keep):

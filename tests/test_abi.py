@@ -31,7 +31,7 @@ def test_exports_every_declared_symbol():
 
 
 def test_version_and_status_strings():
-    assert hilo.hilo_abi_version() == 2
+    assert hilo.hilo_abi_version() == 3
     for st in range(7):
         assert hilo.status_str(st)
     assert hilo.status_str(99) == "unknown status"
@@ -196,3 +196,40 @@ def test_select_tokens_validation():
     assert L.hilo_select_tokens(*args(-1)) == 4
     assert L.hilo_decompress_delta(ctypes.byref(s), FAKE, None, FAKE, FAKE, FAKE, FAKE, FAKE, None, None) == 1
     assert L.hilo_decompress_delta(ctypes.byref(s), FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE, None, None) == 1
+
+
+def test_fp8_validation():
+    """The FP8 block takes bf16 shapes with dim % 128 == 0 and every weight pointer, scales included;
+    the row quantiser takes float32 / bf16 rows of a multiple of 4 columns."""
+    L = hilo.lib()
+    s = good_shape()
+    need = hilo.hilo_workspace_bytes(s)
+    aw = (hilo.hilo_attn_w_fp8 * 2)(*[hilo.hilo_attn_w_fp8(FAKE, FAKE, FAKE, FAKE, FAKE)] * 2)
+    mw = (hilo.hilo_mlp_w_fp8 * 2)(*[hilo.hilo_mlp_w_fp8(FAKE, FAKE, FAKE, FAKE, FAKE)] * 2)
+    f = good_shape(hilo.F32)
+    assert L.hilo_attention_fp8(ctypes.byref(f), FAKE, FAKE, aw, FAKE, FAKE, 1 << 40, None) == 3
+    assert L.hilo_mlp_fp8(ctypes.byref(f), FAKE, FAKE, mw, FAKE, FAKE, 1 << 40, None) == 3
+    odd = hilo.hilo_shape(2, 1, 8, 10, 5, 192, 3, 64, 1024, hilo.BF16)  # 192 is not a multiple of 128
+    assert L.hilo_attention_fp8(ctypes.byref(odd), FAKE, FAKE, aw, FAKE, FAKE, 1 << 40, None) == 2
+    assert L.hilo_mlp_fp8(ctypes.byref(odd), FAKE, FAKE, mw, FAKE, FAKE, 1 << 40, None) == 2
+    bad_aw = (hilo.hilo_attn_w_fp8 * 2)(*[hilo.hilo_attn_w_fp8(FAKE, FAKE, FAKE, FAKE, FAKE)] * 2)
+    bad_aw[1] = hilo.hilo_attn_w_fp8(FAKE, None, FAKE, FAKE, FAKE)  # text stream without scales
+    assert L.hilo_attention_fp8(ctypes.byref(s), FAKE, FAKE, bad_aw, FAKE, FAKE, need, None) == 1
+    bad_mw = (hilo.hilo_mlp_w_fp8 * 2)(*[hilo.hilo_mlp_w_fp8(FAKE, FAKE, FAKE, FAKE, FAKE)] * 2)
+    bad_mw[0] = hilo.hilo_mlp_w_fp8(FAKE, None, FAKE, FAKE, FAKE)
+    assert L.hilo_mlp_fp8(ctypes.byref(s), FAKE, FAKE, bad_mw, FAKE, FAKE, need, None) == 1
+    assert L.hilo_attention_fp8(ctypes.byref(s), FAKE, FAKE, aw, FAKE, FAKE, 100, None) == 5
+    assert L.hilo_mlp_fp8(ctypes.byref(s), FAKE, FAKE, mw, FAKE, FAKE, need - 1, None) == 5
+    assert L.hilo_attention_fp8(ctypes.byref(s), None, FAKE, aw, FAKE, FAKE, need, None) == 1
+    q = L.hilo_quantize_rows
+    assert q(2, FAKE, 4, 8, FAKE, FAKE, None) == 3      # dtype
+    assert q(hilo.BF16, FAKE, 4, 6, FAKE, FAKE, None) == 2   # cols % 4
+    assert q(hilo.BF16, FAKE, -1, 8, FAKE, FAKE, None) == 2
+    assert q(hilo.BF16, FAKE, 4, 0, FAKE, FAKE, None) == 2
+    assert q(hilo.BF16, FAKE, 1 << 31, 8, FAKE, FAKE, None) == 2
+    assert q(hilo.BF16, FAKE, 4, 8, None, FAKE, None) == 1
+    assert q(hilo.F32, FAKE, 0, 8, FAKE, FAKE, None) == 0    # nothing to do
+    if not torch.cuda.is_available():
+        assert q(hilo.F32, FAKE, 4, 8, FAKE, FAKE, None) == 6
+        assert L.hilo_attention_fp8(ctypes.byref(s), FAKE, FAKE, aw, FAKE, FAKE, need, None) == 6
+        assert L.hilo_mlp_fp8(ctypes.byref(s), FAKE, FAKE, mw, FAKE, FAKE, need, None) == 6
