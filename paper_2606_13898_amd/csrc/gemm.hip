@@ -368,6 +368,76 @@ struct SkTile {
   }
 };
 
+// Epilogue of a WR x WC wave tile held as 32 x 32 blocks: lane (r, g) of block (i, j) holds row
+// 32 i + r and, in register 4 b + e, column 32 j + 8 b + 4 g + e (four runs of 4 columns).  For the
+// residual form the gate and bias of the lane's columns and the old z of one block row are loaded
+// before anything is stored (the compiler cannot prove that outputs do not alias inputs, so an
+// interleaved order would serialise one memory round trip per fragment).  Loads use indices
+// clamped into the tile; values outside it are never stored.
+template <int EPI, int WR, int WC>
+HILO_DEV void epilogue32(const GemmProblem &p, const TileRows &tr, int c0, int r0, int lane,
+                         const f32x16 (&acc)[WR / 32][WC / 32]) {
+  constexpr int TM2 = WR / 32, TN2 = WC / 32;
+  const int r32 = lane & 31, cg = c0 + 4 * (lane >> 5);
+  const uint16_t *bias = reinterpret_cast<const uint16_t *>(p.bias[tr.sigma]);
+  float bv[TN2][4][4];
+  float4 gt[TN2][4];
+#pragma unroll
+  for (int j = 0; j < TN2; ++j)
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      const int nc = min(cg + 32 * j + 8 * b, p.N - 4);
+      const uint2 bu = *reinterpret_cast<const uint2 *>(bias + nc);
+      bv[j][b][0] = __uint_as_float(bu.x << 16); bv[j][b][1] = __uint_as_float(bu.x & 0xffff0000u);
+      bv[j][b][2] = __uint_as_float(bu.y << 16); bv[j][b][3] = __uint_as_float(bu.y & 0xffff0000u);
+      if constexpr (EPI == EPI_RESID)
+        gt[j][b] = *reinterpret_cast<const float4 *>(p.mod + (size_t(tr.s * 2 + tr.sigma) * 6 + p.gate_idx) * p.D + nc);
+    }
+#pragma unroll
+  for (int i = 0; i < TM2; ++i) {
+    const int rl = r0 + 32 * i + r32;
+    float4 zv[TN2][4];
+    if constexpr (EPI == EPI_RESID) {
+      const size_t mz = size_t(tr.row0 + min(rl, tr.nrows - 1));
+#pragma unroll
+      for (int j = 0; j < TN2; ++j)
+#pragma unroll
+        for (int b = 0; b < 4; ++b)
+          zv[j][b] = *reinterpret_cast<const float4 *>(p.z + mz * p.ldz + min(cg + 32 * j + 8 * b, p.N - 4));
+    }
+    if (rl < tr.nrows) {
+      const size_t m = size_t(tr.row0 + rl);
+#pragma unroll
+      for (int j = 0; j < TN2; ++j)
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+          const int n = cg + 32 * j + 8 * b;
+          if (n >= p.N) continue;
+          float v[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = acc[i][j][4 * b + e] + bv[j][b][e];
+          if constexpr (EPI == EPI_RESID) {
+            float4 z = zv[j][b];
+            z.x += gt[j][b].x * v[0];
+            z.y += gt[j][b].y * v[1];
+            z.z += gt[j][b].z * v[2];
+            z.w += gt[j][b].w * v[3];
+            *reinterpret_cast<float4 *>(p.z + m * p.ldz + n) = z;
+          } else {
+            if constexpr (EPI == EPI_GELU) {
+#pragma unroll
+              for (int e = 0; e < 4; ++e) v[e] = gelu_tanh(v[e]);
+            }
+            uint2 u;
+            u.x = pack_bf16x2(v[0], v[1]);
+            u.y = pack_bf16x2(v[2], v[3]);
+            *reinterpret_cast<uint2 *>(reinterpret_cast<uint16_t *>(p.out) + m * p.ldo + n) = u;
+          }
+        }
+    }
+  }
+}
+
 template <int BM, int BN, int WM, int WN, int EPI, int ROLE>
 __global__ __launch_bounds__(WM *WN * 64) void k_gemm_sk(GemmProblem p) {
   using T = SkTile<BM, BN, WM, WN>;
@@ -384,7 +454,8 @@ __global__ __launch_bounds__(WM *WN * 64) void k_gemm_sk(GemmProblem p) {
 
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int wrow = (wid / WN) * (BM / WM), wcol = (wid % WN) * (BN / WN);
-  const int lr = lane & 15, lg = lane >> 4;
+  constexpr int TM2 = BM / WM / 32, TN2 = BN / WN / 32;
+  const int r32 = lane & 31, g32 = lane >> 5;
   const int lrow = lane >> 3, lslot = lane & 7;
   const uint16_t *A = reinterpret_cast<const uint16_t *>(p.A);
 
@@ -435,56 +506,68 @@ __global__ __launch_bounds__(WM *WN * 64) void k_gemm_sk(GemmProblem p) {
     const SkItem nxt = next_item();
     const Src sn = make_src(nxt.valid ? nxt.t : cur.t);
 
-    f32x4 acc[TM][TN];
+    // wave tile (BM / WM) x (BN / WN) as TM2 x TN2 blocks of 32 x 32 (v_mfma_f32_32x32x16_bf16);
+    // lane (r, g) = (lane % 32, lane / 32) of a fragment reads row r, chunk h + (BK / 16) g for the
+    // K slice h of 16 values (chunks {h, h + BK / 16}): each half-wave reads one chunk of 32
+    // consecutive rows, which the swizzle spreads over all banks (the 16 x 16 fragment order, 16
+    // rows of several chunks per half-wave, measured 2-way bank conflicts)
+    f32x16 acc[TM2][TN2];
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
+    for (int i = 0; i < TM2; ++i)
 #pragma unroll
-      for (int j = 0; j < TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int j = 0; j < TN2; ++j) acc[i][j] = f32x16{};
 
     // one K step: wait for this step's tile, then read fragments and multiply; `next` issues the
-    // following step's loads right after the fragment reads (the LDS then serves the reads first
-    // and the MFMAs start sooner after the barrier)
+    // following step's loads right after the last fragment reads (the LDS then serves the reads
+    // first and the MFMAs start sooner after the barrier)
     auto step = [&](auto &&next) {
       wait_vmem_le<0>();
       __syncthreads();
 #pragma unroll
-      for (int ks = 0; ks < BK / 32; ++ks) {
-        const int ch = ks * 4 + lg;
-        bf16x8 fa[TM], fb[TN];
+      for (int h = 0; h < BK / 16; ++h) {
+        const int ch = h + (BK / 16) * g32;
+        bf16x8 fa[TM2], fb[TN2];
 #pragma unroll
-        for (int i = 0; i < TM; ++i) {
-          const int r = wrow + i * 16 + lr;
+        for (int i = 0; i < TM2; ++i) {
+          const int r = wrow + i * 32 + r32;
           fa[i] = *reinterpret_cast<const bf16x8 *>(&sA[buf][r * BK + ((ch ^ swz<BK>(r)) * 8)]);
         }
 #pragma unroll
-        for (int j = 0; j < TN; ++j) {
-          const int r = wcol + j * 16 + lr;
+        for (int j = 0; j < TN2; ++j) {
+          const int r = wcol + j * 32 + r32;
           fb[j] = *reinterpret_cast<const bf16x8 *>(&sB[buf][r * BK + ((ch ^ swz<BK>(r)) * 8)]);
         }
-        if (ks == BK / 32 - 1) next();
+        if (h == BK / 16 - 1) next();
 #pragma unroll
-        for (int i = 0; i < TM; ++i)
+        for (int i = 0; i < TM2; ++i)
 #pragma unroll
-          for (int j = 0; j < TN; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fb[j], fa[i], acc[i][j], 0, 0, 0);
+          for (int j = 0; j < TN2; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[j], fa[i], acc[i][j], 0, 0, 0);
       }
       buf ^= 1;
     };
     // all steps but the last issue their successor unconditionally: no branch inside the loop
-    // body, so the scheduler overlaps each half-step's fragment reads with the previous MFMAs
+    // body, so the scheduler overlaps each slice's fragment reads with the previous MFMAs
     for (int kt = cur.kb; kt < cur.ke - 1; ++kt) step([&] { issue(sc, (kt + 1) * BK, buf ^ 1); });
     step([&] {
       if (nxt.valid) issue(sn, nxt.kb * BK, buf ^ 1);
     });
 
     if (cur.slot == nullptr) {
-      T::template epilogue_rows<EPI, TM>(p, sc.tr, sc.n0, wid, 0, lane, acc);
+      epilogue32<EPI, BM / WM, BN / WN>(p, sc.tr, sc.n0 + wcol, wrow, lane, acc);
     } else {
+      // the partial tile in the 16 x 16 fragment layout k_gemm_fix reads: row 32 i + r is fragment
+      // row 2 i + r / 16; columns 32 j + 8 b + 4 g .. + 3 are lane r % 16 + 16 (2 (b % 2) + g) of
+      // fragment column 2 j + b / 2
+      float *base = cur.slot + (size_t(wid) * TM * TN * 64 + (r32 >> 4) * TN * 64 + (r32 & 15) + 16 * g32) * 4;
 #pragma unroll
-      for (int i = 0; i < TM; ++i)
+      for (int i = 0; i < TM2; ++i)
 #pragma unroll
-        for (int j = 0; j < TN; ++j)
-          *reinterpret_cast<f32x4 *>(cur.slot + T::part_index(wid, i, j, lane)) = acc[i][j];
+        for (int j = 0; j < TN2; ++j)
+#pragma unroll
+          for (int b = 0; b < 4; ++b)
+            *reinterpret_cast<f32x4 *>(base + ((2 * i * TN + 2 * j + b / 2) * 64 + 32 * (b % 2)) * 4) =
+                f32x4{acc[i][j][4 * b], acc[i][j][4 * b + 1], acc[i][j][4 * b + 2], acc[i][j][4 * b + 3]};
     }
     if (!nxt.valid) break;
     cur = nxt;
@@ -492,27 +575,34 @@ __global__ __launch_bounds__(WM *WN * 64) void k_gemm_sk(GemmProblem p) {
   }
 }
 
-// ------------------------------------------------------------------- bf16 MFMA, 256 x 256 tiles
+// ------------------------------------------------------------------- MFMA, 256 x 256 tiles
 //
-// One persistent workgroup per CU, 4 waves (2 x 2), wave tile 128 x 128: 256 fp32 accumulators per
-// lane, held in AGPRs.  Per MFMA the wave reads a quarter of the LDS bytes a 64 x 64 wave tile
-// needs, and per K step the CU loads half the operand bytes per FLOP of a 128 x 128 tile.  K runs
-// in 32-deep stages through a 4-slot LDS ring (32 KiB per stage: the stage's 256 A rows, then its
-// 256 W rows, 64 bytes each, 16-byte chunks swizzled), loaded by direct global->LDS loads three
-// stages ahead.  With one wave per SIMD nothing hides a stall of the wave, so the loop is written
-// as a fixed schedule over the 64 MFMAs of a stage (inline asm pins the order):
-//   * each fragment row waits only for its own LDS reads (DS reads complete in order, so an exact
+// One persistent workgroup per CU, 4 waves (2 x 2), wave tile 128 x 128 as 4 x 4 blocks of 32 x 32:
+// 256 fp32 accumulators per lane, held in AGPRs.  Per K step the CU loads half the operand bytes
+// per FLOP of a 128 x 128 tile.  K runs in stages of 64 bytes per row (32 bf16 or 64 FP8 values)
+// through a 4-slot LDS ring (32 KiB per stage: the stage's 256 A rows, then its 256 W rows, 16-byte
+// chunks swizzled), loaded by direct global->LDS loads three stages ahead.  A stage is 16 blocks:
+//   * bf16: two v_mfma_f32_32x32x16_bf16 per block, one per K half (chunks {h, h + 2});
+//   * FP8:  one v_mfma_f32_32x32x64_f8f6f4 per block (all four chunks, 8 registers per operand).
+// Either way lane (r, g) = (l % 32, l / 32) of a fragment reads chunks 2 g and 2 g + 1 of row r of a
+// 32-row fragment: each half-wave reads one chunk of 32 consecutive rows, which the swizzle spreads
+// over all banks (the 16 x 16 fragment order, 16 rows of two chunks per half-wave, measured 2-way
+// bank conflicts on every read).  With one wave per SIMD nothing hides a stall of the wave, so the
+// loop is a fixed schedule (inline asm pins the order):
+//   * each block row waits only for its own fragment reads (DS reads complete in order, so an exact
 //     lgkmcnt is known at every point);
-//   * after two of the eight MFMA rows the wave waits for its loads of the *next* stage and meets
-//     the others at the barrier, which also tells it that every wave has finished reading the
-//     slot it is about to refill;
-//   * one of the stage's 8 load instructions (three stages ahead) follows each of the next 8
-//     MFMAs, one of the 16 fragment reads of the next stage each of the following 16.
-// Fragments alternate between two register sets, so a scheduling unit is two stages (one 64-deep
-// K step, the unit of the stream-K plan).  A second cursor over the workgroup's items drives the
-// loads: at the end of an item they already fetch the next item's first stages, so its epilogue
-// overlaps them.  Past the last item the loader repeats the last stage into free slots (valid
-// addresses; keeps the vmcnt arithmetic uniform).
+//   * before block 4 the wave waits for its loads of the *next* stage and meets the others at the
+//     barrier, which also tells it that every wave has finished reading the slot it is about to
+//     refill;
+//   * after each of blocks 4..11: one of the stage's 8 loads (three stages ahead) and two of the 16
+//     fragment reads of the next stage.
+// Fragments alternate between two register sets, so a scheduling unit is two stages (the K step of
+// the stream-K plan: 64 bf16 or 128 FP8 values).  A second cursor over the workgroup's items drives
+// the loads: at the end of an item they already fetch the next item's first stages, so its
+// epilogue overlaps them.  Past the last item the loader repeats the last stage into free slots
+// (valid addresses; keeps the vmcnt arithmetic uniform).  The epilogue's per-column and per-row
+// operands (bias, FP8 scales, gate) reach LDS by a DMA issued in the item's first stage, so the
+// epilogue never waits on the prefetch loads in flight behind them.
 // Values that are the same on every lane, restated as such (the compiler otherwise keeps some of
 // the stream-K bookkeeping in VGPRs and branches on it with exec masks).
 HILO_DEV int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
@@ -525,21 +615,31 @@ HILO_DEV SkItem uni(const SkItem &x) { return SkItem{uni(x.t), uni(x.kb), uni(x.
 HILO_DEV TileRows uni(const TileRows &x) { return TileRows{uni(x.s), uni(x.sigma), uni(x.row0), uni(x.nrows)}; }
 
 namespace big {
-constexpr int BM = 256, BK = 32, S = 4;
-constexpr int SPLIT = 2;                // MFMA rows before the barrier
+constexpr int BM = 256, BN = 256, S = 4;
+constexpr int LQ = 8;                  // load instructions per wave per stage
+constexpr int NR = 16;                 // fragment reads per wave per stage
+constexpr int AB = BM * 64;            // bytes of a stage's A rows
+constexpr int SB = (BM + BN) * 64;     // bytes of a stage
+// per wave, behind the ring: the wave's 128 columns of bias (bf16, 256 B), of the FP8 weight scales
+// or the residual gate (float32, 512 B), and its 128 rows of FP8 activation scales (512 B)
+constexpr int kEpiWave = 1280, kEpiBias = 0, kEpiCol = 256, kEpiRow = 768;
 HILO_DEV int swz(int r) { return ((r >> 1) & 3) ^ ((r >> 3) & 1); }
+// W row read by fragment lane r.  The 32 x 32 MFMA's output row i (the W side) lands in
+// accumulator register 4 (i / 8) + i % 4 of the lanes of half (i / 4) % 2; reading W row perm_w(i)
+// there gives lane half g the columns 16 g .. 16 g + 15 in register order.  These LDS reads are
+// conflict-free like the natural order (measured; shifting the second half by 8 rows is not).
+HILO_DEV int perm_w(int r) { return ((r & 4) ? 16 : 0) + 4 * (r >> 3) + (r & 3); }
 }  // namespace big
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-
-#define HILO_MFMA_AGPR(ACC, FB, FA) \
-  asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(ACC) : "v"(FB), "v"(FA) : "memory")
-// first K stage of a tile: accumulate onto zero (no separate clearing of the AGPRs)
-#define HILO_MFMA_AGPR0(ACC, FB, FA) \
-  asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, 0" : "=a"(ACC) : "v"(FB), "v"(FA) : "memory")
-// FP8: 32 x 32 output block, 64-deep K, E4M3 codes in both operands (8 registers per operand)
 typedef uint32_t u32x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+#define HILO_MFMA16_AGPR(ACC, FB, FA) \
+  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(ACC) : "v"(FB), "v"(FA) : "memory")
+// first MFMA of a tile: accumulate onto zero (no separate clearing of the AGPRs)
+#define HILO_MFMA16_AGPR0(ACC, FB, FA) \
+  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=a"(ACC) : "v"(FB), "v"(FA) : "memory")
 #define HILO_MFMA8_AGPR(ACC, FB, FA) \
   asm volatile("v_mfma_f32_32x32x64_f8f6f4 %0, %1, %2, %0" : "+a"(ACC) : "v"(FB), "v"(FA) : "memory")
 #define HILO_MFMA8_AGPR0(ACC, FB, FA) \
@@ -547,6 +647,11 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 HILO_DEV u32x8 cat8(u32x4 lo, u32x4 hi) { return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7); }
 #define HILO_DS_READ16(DST, ADDR, OFF) \
   asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(DST) : "v"(ADDR), "i"(OFF) : "memory")
+
+// One 4-byte global load per lane straight into LDS: lane l lands at byte 4 l of the destination.
+HILO_DEV void g2lds4(const void *g, void *lds_wave_base) {
+  __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void *)lds_wave_base, 4, 0, 0);
+}
 
 template <int N>
 HILO_DEV void wait_lgkm_le() { asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(N) : "memory"); }
@@ -564,152 +669,87 @@ HILO_DEV void wait_lgkm_rt(int n) {  // n is a compile-time constant after unrol
   }
 }
 
-// Epilogue of a 256 x (32 TNW) tile from the AGPR accumulators of wave wid (wave tile 128 x 16 TNW): bias (and gate) depend on
-// the column only and are loaded once, so the bias / GELU epilogues make a single memory round
-// trip; the residual update loads the old z one fragment row at a time (two rows in flight do not
-// fit the register budget next to the next tile's fragments).  Loads use indices clamped into the
-// tile; values outside it are never stored.
-template <int EPI, int TNW>
-HILO_DEV void big_epilogue(const GemmProblem &p, const TileRows &tr, int n0, int wid, int lane, f32x4 (&acc)[8][TNW]) {
-  const int rbase = (wid >> 1) * 128 + (lane & 15);
-  const int cbase = n0 + (wid & 1) * (16 * TNW) + 4 * (lane >> 4);
-  const uint16_t *bias = reinterpret_cast<const uint16_t *>(tr.sigma ? p.bias[1] : p.bias[0]);
-  float bv[TNW][4];
-  float4 gt[TNW];
+// Epilogue of a 256 x 256 tile from the AGPR accumulators of wave wid.  The W fragments are read
+// in the row order perm_w, so lane l of block (bi, bj) holds row 32 bi + l % 32 of the wave tile and,
+// in register v, column 32 bj + 16 (l / 32) + v: 16 consecutive columns, stored as two 16-byte
+// pieces (bf16) or four (float32 z).  Column operands (bias; FP8 weight scales or the gate) come from
+// the wave's LDS area `epi`, once per block column; FP8 row scales once per tile.  Bias / GELU
+// outputs are rounded to bf16, the residual update adds gate * (acc + bias) to the float32 z.
+// Blocks leave the AGPRs one at a time.
+template <int EPI, bool F8>
+HILO_DEV void big_epilogue(const GemmProblem &p, const TileRows &tr, int n0, int wid, int lane,
+                           const uint8_t *epi, f32x16 (&acc)[4][4]) {
+  static_assert(!(F8 && EPI == EPI_RESID), "FP8 projections end in a bias or GELU epilogue");
+  using namespace big;
+  const int rbase = (wid >> 1) * 128 + (lane & 31);
+  const int cl0 = 16 * (lane >> 5);              // this lane's first column within a 32-column block
+  const int cbase = n0 + (wid & 1) * 128 + cl0;
+  float sa[4];
 #pragma unroll
-  for (int j = 0; j < TNW; ++j) {
-    const int nc = min(cbase + j * 16, p.N - 4);
-    const uint2 bu = *reinterpret_cast<const uint2 *>(bias + nc);
-    bv[j][0] = __uint_as_float(bu.x << 16); bv[j][1] = __uint_as_float(bu.x & 0xffff0000u);
-    bv[j][2] = __uint_as_float(bu.y << 16); bv[j][3] = __uint_as_float(bu.y & 0xffff0000u);
-    if constexpr (EPI == EPI_RESID)
-      gt[j] = *reinterpret_cast<const float4 *>(p.mod + (size_t(tr.s * 2 + tr.sigma) * 6 + p.gate_idx) * p.D + nc);
-  }
-  float4 zc[TNW];  // old z of the current fragment row
+  for (int bi = 0; bi < 4; ++bi)
+    sa[bi] = F8 ? *reinterpret_cast<const float *>(epi + kEpiRow + 4 * (32 * bi + (lane & 31))) : 1.f;
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    if constexpr (EPI == EPI_RESID) {
-      const size_t m = size_t(tr.row0 + min(rbase + i * 16, tr.nrows - 1));
+  for (int bj = 0; bj < 4; ++bj) {
+    const int cl = cl0 + 32 * bj, n = cbase + 32 * bj;
+    u32x4 bu[2];
+    f32x4 cv[4];  // FP8 weight scales or the residual gate of the lane's 16 columns
 #pragma unroll
-      for (int j = 0; j < TNW; ++j) zc[j] = *reinterpret_cast<const float4 *>(p.z + m * p.ldz + min(cbase + j * 16, p.N - 4));
+    for (int h = 0; h < 2; ++h) bu[h] = *reinterpret_cast<const u32x4 *>(epi + kEpiBias + 2 * cl + 16 * h);
+    if constexpr (F8 || EPI == EPI_RESID) {
+#pragma unroll
+      for (int h = 0; h < 4; ++h) cv[h] = *reinterpret_cast<const f32x4 *>(epi + kEpiCol + 4 * cl + 16 * h);
     }
-    f32x4 row[TNW];
 #pragma unroll
-    for (int j = 0; j < TNW; ++j) {  // copy this row out of the AGPRs here, not all rows up front
-      row[j] = acc[i][j];
-      asm volatile("" : "+v"(row[j]));
-    }
-    const int rl = rbase + i * 16;
-    if (rl < tr.nrows) {
-      const size_t m = size_t(tr.row0 + rl);
+    for (int bi = 0; bi < 4; ++bi) {
+      f32x16 blk = acc[bi][bj];  // one block out of the AGPRs at a time
+      asm volatile("" : "+v"(blk));
+      const int rl = rbase + 32 * bi;
+      if (rl < tr.nrows && n < p.N) {  // N % 16 == 0: a lane's 16 columns are all inside or all out
+        const size_t m = size_t(tr.row0 + rl);
+        float v[16];
 #pragma unroll
-      for (int j = 0; j < TNW; ++j) {
-        const int n = cbase + j * 16;
-        if (n >= p.N) continue;
-        float v[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) v[e] = row[j][e] + bv[j][e];
+        for (int e = 0; e < 16; ++e) {
+          const uint32_t w = bu[e >> 3][(e >> 1) & 3];
+          const float bias = __uint_as_float((e & 1) ? (w & 0xffff0000u) : (w << 16));
+          if constexpr (F8) v[e] = blk[e] * (sa[bi] * cv[e >> 2][e & 3]) + bias;
+          else v[e] = blk[e] + bias;
+        }
         if constexpr (EPI == EPI_RESID) {
-          float4 z = zc[j];
-          z.x += gt[j].x * v[0];
-          z.y += gt[j].y * v[1];
-          z.z += gt[j].z * v[2];
-          z.w += gt[j].w * v[3];
-          *reinterpret_cast<float4 *>(p.z + m * p.ldz + n) = z;
+          float4 *zp = reinterpret_cast<float4 *>(p.z + m * p.ldz + n);
+          float4 z[4];
+#pragma unroll
+          for (int h = 0; h < 4; ++h) z[h] = zp[h];
+#pragma unroll
+          for (int h = 0; h < 4; ++h) {
+            z[h].x += cv[h][0] * v[4 * h + 0];
+            z[h].y += cv[h][1] * v[4 * h + 1];
+            z[h].z += cv[h][2] * v[4 * h + 2];
+            z[h].w += cv[h][3] * v[4 * h + 3];
+            zp[h] = z[h];
+          }
         } else {
           if constexpr (EPI == EPI_GELU) {
 #pragma unroll
-            for (int e = 0; e < 4; ++e) v[e] = gelu_tanh(v[e]);
+            for (int e = 0; e < 16; ++e) v[e] = gelu_tanh(v[e]);
           }
-          uint2 u;
-          u.x = pack_bf16x2(v[0], v[1]);
-          u.y = pack_bf16x2(v[2], v[3]);
-          *reinterpret_cast<uint2 *>(reinterpret_cast<uint16_t *>(p.out) + m * p.ldo + n) = u;
+          uint4 *op = reinterpret_cast<uint4 *>(reinterpret_cast<uint16_t *>(p.out) + m * p.ldo + n);
+#pragma unroll
+          for (int h = 0; h < 2; ++h)
+            op[h] = make_uint4(pack_bf16x2(v[8 * h + 0], v[8 * h + 1]), pack_bf16x2(v[8 * h + 2], v[8 * h + 3]),
+                               pack_bf16x2(v[8 * h + 4], v[8 * h + 5]), pack_bf16x2(v[8 * h + 6], v[8 * h + 7]));
         }
       }
-    }
-    asm volatile("" ::: "memory");  // the next row's loads stay below these stores
-  }
-}
-
-// Epilogue of a 256 x 256 FP8 tile (wave tile 128 x 128 in 4 x 4 blocks of 32 x 32).  Lane l of
-// block (bi, bj) holds row 32 bi + l % 32 of the wave tile and, in register 4 b + e, column
-// 32 bj + 8 b + 4 (l / 32) + e.  acc * (row scale * column scale) + bias, then GELU for MLP up;
-// the column-only operands (bias, weight scales) and the four row scales are loaded once.
-template <int EPI>
-HILO_DEV void big_epilogue8(const GemmProblem &p, const TileRows &tr, int n0, int wid, int lane, f32x16 (&acc)[4][4]) {
-  static_assert(EPI != EPI_RESID, "FP8 projections end in a bias or GELU epilogue");
-  const int rbase = (wid >> 1) * 128 + (lane & 31);
-  const int cbase = n0 + (wid & 1) * 128 + 4 * (lane >> 5);
-  const uint16_t *bias = reinterpret_cast<const uint16_t *>(tr.sigma ? p.bias[1] : p.bias[0]);
-  const float *wsp = tr.sigma ? p.w_scale[1] : p.w_scale[0];
-  uint2 bu[4][4];
-  float4 ws[4][4];
-  float as[4];
-#pragma unroll
-  for (int bj = 0; bj < 4; ++bj)
-#pragma unroll
-    for (int b = 0; b < 4; ++b) {
-      const int nc = min(cbase + 32 * bj + 8 * b, p.N - 4);
-      bu[bj][b] = *reinterpret_cast<const uint2 *>(bias + nc);
-      ws[bj][b] = *reinterpret_cast<const float4 *>(wsp + nc);
-    }
-#pragma unroll
-  for (int bi = 0; bi < 4; ++bi) as[bi] = p.a_scale[tr.row0 + min(rbase + 32 * bi, tr.nrows - 1)];
-#pragma unroll
-  for (int bi = 0; bi < 4; ++bi) {
-    const int rl = rbase + 32 * bi;
-#pragma unroll
-    for (int bj = 0; bj < 4; ++bj) {
-      f32x16 blk = acc[bi][bj];  // one block out of the AGPRs at a time
-      asm volatile("" : "+v"(blk));
-      if (rl < tr.nrows) {
-        const size_t m = size_t(tr.row0 + rl);
-#pragma unroll
-        for (int b = 0; b < 4; ++b) {
-          const int n = cbase + 32 * bj + 8 * b;
-          if (n >= p.N) continue;
-          const float sa = as[bi];
-          float v[4];
-          v[0] = blk[4 * b + 0] * (sa * ws[bj][b].x) + __uint_as_float(bu[bj][b].x << 16);
-          v[1] = blk[4 * b + 1] * (sa * ws[bj][b].y) + __uint_as_float(bu[bj][b].x & 0xffff0000u);
-          v[2] = blk[4 * b + 2] * (sa * ws[bj][b].z) + __uint_as_float(bu[bj][b].y << 16);
-          v[3] = blk[4 * b + 3] * (sa * ws[bj][b].w) + __uint_as_float(bu[bj][b].y & 0xffff0000u);
-          if constexpr (EPI == EPI_GELU) {
-#pragma unroll
-            for (int e = 0; e < 4; ++e) v[e] = gelu_tanh(v[e]);
-          }
-          uint2 u;
-          u.x = pack_bf16x2(v[0], v[1]);
-          u.y = pack_bf16x2(v[2], v[3]);
-          *reinterpret_cast<uint2 *>(reinterpret_cast<uint16_t *>(p.out) + m * p.ldo + n) = u;
-        }
-      }
-      asm volatile("" ::: "memory");
+      asm volatile("" ::: "memory");  // the next block's loads stay below these stores
     }
   }
 }
 
-// BN = 256 or 128: wave tile 128 x BN/2, TNW = BN/32 weight fragments per wave.
-// F8 (BN = 256 only): E4M3 operands, a stage holds 64 K values per row (the same 64 bytes), and the
-// wave tile is 4 x 4 MFMAs of 32 x 32 x 64; each fragment is two 16-byte LDS reads per lane.
-template <int EPI, int ROLE, int BN, bool F8>
+template <int EPI, int ROLE, bool F8>
 __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
-  using big::BM;
-  using big::BK;
-  using big::S;
-  using big::SPLIT;
-  using big::swz;
-  using T = SkTile<BM, BN, 2, 2>;
-  constexpr int TNW = BN / 32;          // weight fragments per wave
-  constexpr int LB = BN / 64;           // weight load instructions per wave per stage (A: 4)
-  constexpr int LQ = 4 + LB;            // load instructions per wave per stage
-  constexpr int NR = 8 + TNW;           // fragment reads per wave per stage
-  constexpr int AB = BM * BK * 2;       // bytes of a stage's A rows
-  constexpr int SB = (BM + BN) * BK * 2;
+  using namespace big;
+  using T = SkTile<BM, BN, 2, 2>;       // partial slot size and layout (16 x 16 fragment order)
   constexpr int ESZ = F8 ? 1 : 2;       // operand bytes per element
-  static_assert(!F8 || BN == 256, "FP8 runs 256 x 256 tiles");
-  __shared__ __attribute__((aligned(1024))) uint8_t lds[S * SB];
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[S * SB + 4 * kEpiWave];
 
   const int P = gridDim.x;
   const int pid = xcd_remap(blockIdx.x, P);
@@ -723,8 +763,8 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
 
   // ---- loader: its own cursor over this workgroup's items, three stages ahead of the MFMAs
   SkCursor lc{pid, rg.beg};
-  const uint8_t *la[4], *lb[LB];
-  int lk = 0, lke = 0;  // next stage to load (64 bytes of each row, absolute in K) and the end of its item
+  const uint8_t *la[4], *lb[4];
+  int lk = 0, lke = 0;  // next stage to load (absolute in K) and the end of its item
   auto ld_src = [&](int t) __attribute__((always_inline)) {
     int rt, tn;
     tile_coords(q, t, rt, tn);
@@ -735,10 +775,6 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
     for (int i = 0; i < 4; ++i) {
       const int r = wid * 64 + 16 * i + lrow;
       la[i] = A + size_t(tr.row0 + min(r, tr.nrows - 1)) * p.lda * ESZ + (lslot ^ swz(r)) * 16;
-    }
-#pragma unroll
-    for (int i = 0; i < LB; ++i) {
-      const int r = wid * (BN / 4) + 16 * i + lrow;
       lb[i] = Wt + size_t(min(tn * BN + r, p.N - 1)) * p.K * ESZ + (lslot ^ swz(r)) * 16;
     }
   };
@@ -754,27 +790,27 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
     lk = uni(lk);
     lke = uni(lke);
   };
-  // load instruction j (0..LQ-1) of the current loader stage into `slot`: A rows for j < 4
+  // load instruction j (0..7) of the current loader stage into `slot`: A rows for j < 4
   auto ld_one = [&](int slot, int j) __attribute__((always_inline)) {
     uint8_t *base = lds + slot * SB;
     const int k0 = lk * 64;  // bytes
     if (j < 4) g2lds16(la[j] + k0, base + wid * 64 * 64 + j * 1024);
-    else g2lds16(lb[j - 4] + k0, base + AB + wid * (BN / 4) * 64 + (j - 4) * 1024);
+    else g2lds16(lb[j - 4] + k0, base + AB + wid * 64 * 64 + (j - 4) * 1024);
   };
 
-  // ---- fragment addresses: lane (lr, lg) reads row lr of 16, chunk lg of 4 (swizzle of lr only:
-  // fragment rows start at multiples of 16)
-  const int lr = lane & 15, lg = lane >> 4;
-  const uint32_t lane_off = lr * 64 + ((lg ^ swz(lr)) * 16);
+  // ---- fragment reads: lane (r, g) = (lane % 32, lane / 32) reads chunk 2 g (low half) and 2 g + 1
+  // (high half) of row r (A) or perm_w(r) (W) of a 32-row fragment; read t of a stage (slot byte
+  // offset so) is half t % 2 of W fragment t / 2 for t < 8, then of A fragment (t - 8) / 2
+  const int r8 = lane & 31, g8 = lane >> 5, w8 = perm_w(r8);
   const uint32_t lds0 = (uint32_t)(uintptr_t)lds;
-  const uint32_t fa0 = lds0 + (wid >> 1) * 128 * 64 + lane_off;
-  const uint32_t fb0 = lds0 + AB + (wid & 1) * (BN / 2) * 64 + lane_off;
-  // read t of a stage, in consumption order: W fragments 0..TNW-1, then A fragments 0..7
-  auto rd_one = [&](u32x4 (&fa)[8], u32x4 (&fb)[TNW], uint32_t a, uint32_t b, int t) __attribute__((always_inline)) {
-#define HILO_RD_CASE(C)                                                        \
-  case C:                                                                      \
-    if constexpr (C < TNW) HILO_DS_READ16(fb[C < TNW ? C : 0], b, (C < TNW ? C : 0) * 1024); \
-    else if constexpr (C - TNW < 8) HILO_DS_READ16(fa[(C - TNW) & 7], a, ((C - TNW) & 7) * 1024); \
+  const uint32_t fa8 = lds0 + (wid >> 1) * 128 * 64, fb8 = lds0 + AB + (wid & 1) * 128 * 64;
+  const uint32_t fa8l = fa8 + r8 * 64 + (((2 * g8) ^ swz(r8)) * 16), fa8h = fa8 + r8 * 64 + (((2 * g8 + 1) ^ swz(r8)) * 16);
+  const uint32_t fb8l = fb8 + w8 * 64 + (((2 * g8) ^ swz(w8)) * 16), fb8h = fb8 + w8 * 64 + (((2 * g8 + 1) ^ swz(w8)) * 16);
+  auto rd_one = [&](u32x4 (&fa)[8], u32x4 (&fb)[8], uint32_t so, int t) __attribute__((always_inline)) {
+#define HILO_RD_CASE(C)                                                                                  \
+  case C:                                                                                                \
+    if constexpr (C < 8) HILO_DS_READ16(fb[C & 7], ((C & 1) ? fb8h : fb8l) + so, ((C & 7) >> 1) * 2048); \
+    else HILO_DS_READ16(fa[C & 7], ((C & 1) ? fa8h : fa8l) + so, ((C & 7) >> 1) * 2048);                 \
     break;
     switch (t) {
       HILO_RD_CASE(0) HILO_RD_CASE(1) HILO_RD_CASE(2) HILO_RD_CASE(3) HILO_RD_CASE(4) HILO_RD_CASE(5)
@@ -785,84 +821,67 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
 #undef HILO_RD_CASE
   };
 
-  // FP8 fragments: lane (r, g) = (lane % 32, lane / 32) reads bytes 32 g .. 32 g + 31 of row r of
-  // a 32-row fragment, as chunk 2 g (low half) and chunk 2 g + 1 (high half)
-  const int r8 = lane & 31, g8 = lane >> 5;
-  const uint32_t lo8 = r8 * 64 + (((2 * g8) ^ swz(r8)) * 16), hi8 = r8 * 64 + (((2 * g8 + 1) ^ swz(r8)) * 16);
-  const uint32_t fa8 = lds0 + (wid >> 1) * 128 * 64, fb8 = lds0 + AB + (wid & 1) * 128 * 64;
-  const uint32_t fa8l = fa8 + lo8, fa8h = fa8 + hi8, fb8l = fb8 + lo8, fb8h = fb8 + hi8;
-  // read t of a stage (slot byte offset so): W fragment t / 2 (halves t % 2) for t < 8, then A
-  auto rd_one8 = [&](u32x4 (&fa)[8], u32x4 (&fb)[8], uint32_t so, int t) __attribute__((always_inline)) {
-#define HILO_RD8_CASE(C)                                                                                      \
-  case C:                                                                                                     \
-    if constexpr (C < 8) HILO_DS_READ16(fb[C & 7], ((C & 1) ? fb8h : fb8l) + so, ((C & 7) >> 1) * 2048);      \
-    else HILO_DS_READ16(fa[C & 7], ((C & 1) ? fa8h : fa8l) + so, ((C & 7) >> 1) * 2048);                      \
-    break;
-    switch (t) {
-      HILO_RD8_CASE(0) HILO_RD8_CASE(1) HILO_RD8_CASE(2) HILO_RD8_CASE(3) HILO_RD8_CASE(4) HILO_RD8_CASE(5)
-      HILO_RD8_CASE(6) HILO_RD8_CASE(7) HILO_RD8_CASE(8) HILO_RD8_CASE(9) HILO_RD8_CASE(10) HILO_RD8_CASE(11)
-      HILO_RD8_CASE(12) HILO_RD8_CASE(13) HILO_RD8_CASE(14) HILO_RD8_CASE(15)
-      default: break;
+  // ---- epilogue operands of the current item: this wave's 128 columns (and FP8 rows) into its
+  // LDS area, by DMA (4 bytes per lane), indices clamped into the tile
+  uint8_t *epi = lds + S * SB + wid * kEpiWave;
+  TileRows etr{0, 0, 0, 1};
+  int en0 = 0;
+  auto epi_load = [&]() __attribute__((always_inline)) {
+    const int c0 = en0 + (wid & 1) * 128;
+    const uint16_t *bias = reinterpret_cast<const uint16_t *>(etr.sigma ? p.bias[1] : p.bias[0]);
+    g2lds4(bias + min(c0 + 2 * lane, p.N - 2), epi + kEpiBias);
+    if constexpr (F8 || EPI == EPI_RESID) {
+      const float *col = F8 ? (etr.sigma ? p.w_scale[1] : p.w_scale[0])
+                            : p.mod + (size_t(etr.s * 2 + etr.sigma) * 6 + p.gate_idx) * p.D;
+      g2lds4(col + min(c0 + lane, p.N - 1), epi + kEpiCol);
+      g2lds4(col + min(c0 + 64 + lane, p.N - 1), epi + kEpiCol + 256);
     }
-#undef HILO_RD8_CASE
+    if constexpr (F8) {
+      const int r0 = (wid >> 1) * 128;
+      g2lds4(p.a_scale + etr.row0 + min(r0 + lane, etr.nrows - 1), epi + kEpiRow);
+      g2lds4(p.a_scale + etr.row0 + min(r0 + 64 + lane, etr.nrows - 1), epi + kEpiRow + 256);
+    }
   };
 
-  f32x4 acc[8][TNW];
-  f32x16 acc8[4][4];
-  u32x4 xa[8], xb[TNW], ya[8], yb[TNW];
+  f32x16 acc[4][4];
+  u32x4 xa[8], xb[8], ya[8], yb[8];
 
-  // one stage (ring slot gs % S) on fragments (fa, fb); reads stage gs + 1 into (na, nb); the
-  // first stage of a tile (first = true_type) starts the accumulators from zero
-  constexpr int LQ0 = SPLIT * TNW, RQ0 = LQ0 + LQ;
-  static_assert(RQ0 + NR <= 8 * TNW, "stage schedule does not fit");
-  auto stage = [&](auto first, u32x4 (&fa)[8], u32x4 (&fb)[TNW], u32x4 (&na)[8], u32x4 (&nb)[TNW], int gs) __attribute__((always_inline)) {
-    const int lslot_w = (gs + S - 1) & (S - 1), nslot = (gs + 1) & (S - 1);
-    const uint32_t a = fa0 + nslot * SB, b = fb0 + nslot * SB;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      // outstanding reads allowed: this stage's A fragments i+1..7 and the next stage's issued so far
-      const int q0 = i * TNW;
-      wait_lgkm_rt(7 - i + (q0 <= RQ0 ? 0 : min(q0 - RQ0, NR)));
-#pragma unroll
-      for (int j = 0; j < TNW; ++j) {
-        const int qq = i * TNW + j;
-        if (qq == LQ0) asm volatile("s_waitcnt vmcnt(%0)\n s_barrier" ::"n"((S - 3) * LQ) : "memory");
-        if constexpr (decltype(first)::value) HILO_MFMA_AGPR0(acc[i][j], fb[j], fa[i]);
-        else HILO_MFMA_AGPR(acc[i][j], fb[j], fa[i]);
-        if (qq >= LQ0 && qq < LQ0 + LQ) ld_one(lslot_w, qq - LQ0);
-        if (qq >= RQ0 && qq < RQ0 + NR) rd_one(na, nb, a, b, qq - RQ0);
-      }
-    }
-    ++lk;
-  };
-  // FP8 stage: 16 MFMAs (block row bi, block column bj); the barrier before MFMA 4, then after each
-  // of MFMAs 4..11 one load of the stage three ahead and two fragment reads of the next stage
-  auto stage8 = [&](auto first, u32x4 (&fa)[8], u32x4 (&fb)[8], u32x4 (&na)[8], u32x4 (&nb)[8], int gs) __attribute__((always_inline)) {
+  // one stage (ring slot gs % S) on fragments (fa, fb); reads stage gs + 1 into (na, nb); the first
+  // stage of a tile (first = true_type) starts the accumulators from zero and, for a tile finished
+  // here, fetches the epilogue operands after its loads
+  auto stage = [&](auto first, u32x4 (&fa)[8], u32x4 (&fb)[8], u32x4 (&na)[8], u32x4 (&nb)[8], int gs,
+                   bool with_epi) __attribute__((always_inline)) {
     const int lslot_w = (gs + S - 1) & (S - 1);
     const uint32_t so = uint32_t(((gs + 1) & (S - 1)) * SB);
 #pragma unroll
     for (int bi = 0; bi < 4; ++bi) {
       // outstanding reads allowed: this stage's A halves of blocks bi+1..3, the next stage's so far
       wait_lgkm_rt(2 * (3 - bi) + 2 * min(max(4 * bi - 4, 0), 8));
-      const u32x8 a8 = cat8(fa[2 * bi], fa[2 * bi + 1]);
 #pragma unroll
       for (int bj = 0; bj < 4; ++bj) {
         const int qq = 4 * bi + bj;
         if (qq == 4) asm volatile("s_waitcnt vmcnt(%0)\n s_barrier" ::"n"((S - 3) * LQ) : "memory");
-        if constexpr (decltype(first)::value) HILO_MFMA8_AGPR0(acc8[bi][bj], cat8(fb[2 * bj], fb[2 * bj + 1]), a8);
-        else HILO_MFMA8_AGPR(acc8[bi][bj], cat8(fb[2 * bj], fb[2 * bj + 1]), a8);
+        if constexpr (F8) {
+          if constexpr (decltype(first)::value)
+            HILO_MFMA8_AGPR0(acc[bi][bj], cat8(fb[2 * bj], fb[2 * bj + 1]), cat8(fa[2 * bi], fa[2 * bi + 1]));
+          else
+            HILO_MFMA8_AGPR(acc[bi][bj], cat8(fb[2 * bj], fb[2 * bj + 1]), cat8(fa[2 * bi], fa[2 * bi + 1]));
+        } else {
+          if constexpr (decltype(first)::value) HILO_MFMA16_AGPR0(acc[bi][bj], fb[2 * bj], fa[2 * bi]);
+          else HILO_MFMA16_AGPR(acc[bi][bj], fb[2 * bj], fa[2 * bi]);
+          HILO_MFMA16_AGPR(acc[bi][bj], fb[2 * bj + 1], fa[2 * bi + 1]);
+        }
         if (qq >= 4 && qq < 12) {
           ld_one(lslot_w, qq - 4);
-          rd_one8(na, nb, so, 2 * (qq - 4));
-          rd_one8(na, nb, so, 2 * (qq - 4) + 1);
+          rd_one(na, nb, so, 2 * (qq - 4));
+          rd_one(na, nb, so, 2 * (qq - 4) + 1);
+        }
+        if constexpr (decltype(first)::value) {
+          if (qq == 11 && with_epi) epi_load();
         }
       }
     }
     ++lk;
-  };
-  auto run_stage = [&](auto first, u32x4 (&fa)[8], u32x4 (&fb)[TNW], u32x4 (&na)[8], u32x4 (&nb)[TNW], int gs) __attribute__((always_inline)) {
-    if constexpr (F8) stage8(first, fa, fb, na, nb, gs);
-    else stage(first, fa, fb, na, nb, gs);
   };
 
   SkCursor cc{pid, rg.beg};
@@ -878,10 +897,7 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
   }
   asm volatile("s_waitcnt vmcnt(%0)\n s_barrier" ::"n"((S - 2) * LQ) : "memory");
 #pragma unroll
-  for (int t = 0; t < NR; ++t) {
-    if constexpr (F8) rd_one8(xa, xb, 0, t);
-    else rd_one(xa, xb, fa0, fb0, t);
-  }
+  for (int t = 0; t < NR; ++t) rd_one(xa, xb, 0, t);
 
   // the loader moves to its next item between stages, outside the MFMA schedule
   auto ld_check = [&]() __attribute__((always_inline)) {
@@ -889,66 +905,56 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
   };
   int gs = 0;
   while (true) {
+    const bool whole = cur.slot == nullptr;
+    if (whole) {
+      int rt, tn;
+      tile_coords(q, cur.t, rt, tn);
+      en0 = uni(tn) * BN;
+      etr = uni(decode_row_tile(p, BM, uni(rt)));
+    }
     ld_check();
-    run_stage(std::true_type{}, xa, xb, ya, yb, gs);
+    stage(std::true_type{}, xa, xb, ya, yb, gs, whole);
     ld_check();
-    run_stage(std::false_type{}, ya, yb, xa, xb, gs + 1);
+    stage(std::false_type{}, ya, yb, xa, xb, gs + 1, false);
     gs += 2;
 #pragma unroll 1
     for (int kt = cur.kb + 1; kt < cur.ke; ++kt) {
       ld_check();
-      run_stage(std::false_type{}, xa, xb, ya, yb, gs);
+      stage(std::false_type{}, xa, xb, ya, yb, gs, false);
       ld_check();
-      run_stage(std::false_type{}, ya, yb, xa, xb, gs + 1);
+      stage(std::false_type{}, ya, yb, xa, xb, gs + 1, false);
       gs += 2;
     }
     // The last MFMAs' results must land before the accumulators are read (the empty asm ties each
     // accumulator to this point, so no read is scheduled above it), and the reads of the next
     // stage's fragments must be complete before the compiler may move those registers.
     asm volatile("s_waitcnt lgkmcnt(0)\n s_nop 7\n s_nop 7\n s_nop 7\n s_nop 7" ::: "memory");
-    if constexpr (F8) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) asm volatile("" : "+a"(acc8[i][j]));
+      for (int j = 0; j < 4; ++j) asm volatile("" : "+a"(acc[i][j]));
+    if (whole) {
+      // the epilogue-operand DMA of the first stage is complete once two later stages have passed
+      // their barriers (each waits for all but the last stage's loads); a one-step item waits here
+      if (cur.ke - cur.kb < 2) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      big_epilogue<EPI, F8>(p, etr, en0, wid, lane, epi, acc);
     } else {
-#pragma unroll
-      for (int i = 0; i < 8; ++i)
-#pragma unroll
-        for (int j = 0; j < TNW; ++j) asm volatile("" : "+a"(acc[i][j]));
-    }
-    if (cur.slot == nullptr) {
-      int rt, tn;
-      tile_coords(q, cur.t, rt, tn);
-      tn = uni(tn);
-      const TileRows tr = uni(decode_row_tile(p, BM, uni(rt)));
-      if constexpr (F8) big_epilogue8<EPI>(p, tr, tn * BN, wid, lane, acc8);
-      else big_epilogue<EPI, TNW>(p, tr, tn * BN, wid, lane, acc);
-    } else if constexpr (F8) {
-      // the partial tile in the layout of the 16 x 16 fragments (k_gemm_fix reads that layout):
-      // row 32 bi + l % 32 = fragment row 2 bi + (l % 32) / 16, lane l % 16 + 16 (l / 32) + 32 (b % 2)
-      // of fragment column 2 bj + b / 2
-      float *base = cur.slot + (size_t(wid) * 64 * 64 + ((lane & 31) >> 4) * 8 * 64 + (lane & 15) + 16 * (lane >> 5)) * 4;
+      // the partial tile in the 16 x 16 fragment layout k_gemm_fix reads: row 32 bi + l % 32 is
+      // fragment row 2 bi + (l % 32) / 16; columns 32 bj + 16 (l / 32) + 4 b .. + 3 are lane
+      // l % 16 + 16 b of fragment column 2 bj + l / 32
+      float *base = cur.slot + (size_t(wid) * 64 * 64 + ((lane & 31) >> 4) * 8 * 64 + (lane >> 5) * 64 + (lane & 15)) * 4;
 #pragma unroll
       for (int bi = 0; bi < 4; ++bi)
 #pragma unroll
         for (int bj = 0; bj < 4; ++bj) {
-          f32x16 blk = acc8[bi][bj];
+          f32x16 blk = acc[bi][bj];
           asm volatile("" : "+v"(blk));
 #pragma unroll
           for (int b = 0; b < 4; ++b)
-            *reinterpret_cast<f32x4 *>(base + ((2 * bi * 8 + 2 * bj + b / 2) * 64 + 32 * (b % 2)) * 4) =
+            *reinterpret_cast<f32x4 *>(base + ((2 * bi * 8 + 2 * bj) * 64 + 16 * b) * 4) =
                 f32x4{blk[4 * b], blk[4 * b + 1], blk[4 * b + 2], blk[4 * b + 3]};
           asm volatile("" ::: "memory");
         }
-    } else {
-      // straight from the AGPRs (no copy of all 256 accumulators through VGPRs)
-      float *base = cur.slot + T::part_index(wid, 0, 0, lane);
-#pragma unroll
-      for (int i = 0; i < 8; ++i)
-#pragma unroll
-        for (int j = 0; j < TNW; ++j)
-          asm volatile("global_store_dwordx4 %0, %1, off" ::"v"(base + (i * TNW + j) * 256), "a"(acc[i][j]) : "memory");
     }
     cur = uni(sk_next_item(cc, q, rg, P, pid, p.part, T::kPartFloats));
     if (!cur.valid) break;
@@ -1140,12 +1146,12 @@ static hipError_t run_bf16(const GemmProblem &p, hipStream_t st) {
 }
 
 // 256 x BN tiles: one persistent workgroup per CU.
-template <int ROLE, int BN, bool F8 = false>
+template <int ROLE, bool F8 = false>
 static hipError_t run_big(const GemmProblem &p, hipStream_t st) {
-  constexpr int BM = big::BM;
+  constexpr int BM = big::BM, BN = big::BN;
   static_assert(size_t(BM) * BN * 3 * kBigMaxWorkgroups * sizeof(float) <= kSkPartBytes, "partial area too small");
   const int P = device_cus() < kBigMaxWorkgroups ? device_cus() : kBigMaxWorkgroups;
-  hipLaunchKernelGGL((k_gemm_big<role_epilogue(ROLE), ROLE, BN, F8>), dim3(P), dim3(256), 0, st, p);
+  hipLaunchKernelGGL((k_gemm_big<role_epilogue(ROLE), ROLE, F8>), dim3(P), dim3(256), 0, st, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const long long tiles_max = (long long)p.B * ((p.max_img_rows + BM - 1) / BM + (p.L + BM - 1) / BM) *
@@ -1185,17 +1191,17 @@ hipError_t launch_gemm(bool bf16, int role, const GemmProblem &p, hipStream_t st
   // 8-tile stream-K tail) measured slower than 128 x 128 (attention output 81 -> 88 us, MLP down
   // 226 -> 234 us in isolation): with a 128 x 64 wave tile the stage reads more LDS per MFMA.
   switch (role) {
-    case GEMM_QKV: return run_big<GEMM_QKV, 256>(p, st);
+    case GEMM_QKV: return run_big<GEMM_QKV>(p, st);
     case GEMM_O: return run_bf16<128, 128, 2, 2, GEMM_O>(p, st);
-    case GEMM_FC1: return run_big<GEMM_FC1, 256>(p, st);
+    case GEMM_FC1: return run_big<GEMM_FC1>(p, st);
     default: return run_bf16<128, 128, 2, 2, GEMM_FC2>(p, st);
   }
 }
 
 hipError_t launch_gemm_fp8(int role, const GemmProblem &p, hipStream_t st) {
   switch (role) {
-    case GEMM_QKV: return run_big<GEMM_QKV, 256, true>(p, st);
-    case GEMM_FC1: return run_big<GEMM_FC1, 256, true>(p, st);
+    case GEMM_QKV: return run_big<GEMM_QKV, true>(p, st);
+    case GEMM_FC1: return run_big<GEMM_FC1, true>(p, st);
     default: return hipErrorInvalidValue;
   }
 }
