@@ -182,7 +182,10 @@ HILO_DEV SkPlan sk_plan(const GemmProblem &p, int BM, int BN, int P, int kstep =
   // 256 x 256 tiles: a stream-K tail costs a 256 KiB partial per piece; when the last wave holds
   // at least half of P tiles, whole tiles in ceil(T / P) waves finish sooner
   const bool whole_waves = BM * BN >= 256 * 256 && q.T >= P && 2 * (q.T % P) >= P;
-  if ((q.T < P && q.nk <= kNoSplitSteps) || whole_waves) {
+  // a single wave that fills at least 7/8 of the workgroups also runs whole tiles (cutting K would
+  // add a partial per tile to save at most an eighth)
+  const bool full_wave = q.T < P && 8 * q.T >= 7 * P;
+  if ((q.T < P && q.nk <= kNoSplitSteps) || whole_waves || full_wave) {
     q.s = 1;
     q.U = q.dp = q.T;
     q.len = q.nk;
@@ -615,13 +618,9 @@ HILO_DEV SkItem uni(const SkItem &x) { return SkItem{uni(x.t), uni(x.kb), uni(x.
 HILO_DEV TileRows uni(const TileRows &x) { return TileRows{uni(x.s), uni(x.sigma), uni(x.row0), uni(x.nrows)}; }
 
 namespace big {
-constexpr int BM = 256, BN = 256, S = 4;
-constexpr int LQ = 8;                  // load instructions per wave per stage
-constexpr int NR = 16;                 // fragment reads per wave per stage
-constexpr int AB = BM * 64;            // bytes of a stage's A rows
-constexpr int SB = (BM + BN) * 64;     // bytes of a stage
-// per wave, behind the ring: the wave's 128 columns of bias (bf16, 256 B), of the FP8 weight scales
-// or the residual gate (float32, 512 B), and its 128 rows of FP8 activation scales (512 B)
+constexpr int S = 4;                   // LDS ring slots
+// per wave, behind the ring: the wave's columns of bias (bf16, <= 256 B), of the FP8 weight scales
+// or the residual gate (float32, <= 512 B), and its rows of FP8 activation scales (<= 512 B)
 constexpr int kEpiWave = 1280, kEpiBias = 0, kEpiCol = 256, kEpiRow = 768;
 HILO_DEV int swz(int r) { return ((r >> 1) & 3) ^ ((r >> 3) & 1); }
 // W row read by fragment lane r.  The 32 x 32 MFMA's output row i (the W side) lands in
@@ -629,6 +628,17 @@ HILO_DEV int swz(int r) { return ((r >> 1) & 3) ^ ((r >> 3) & 1); }
 // there gives lane half g the columns 16 g .. 16 g + 15 in register order.  These LDS reads are
 // conflict-free like the natural order (measured; shifting the second half by 8 rows is not).
 HILO_DEV int perm_w(int r) { return ((r & 4) ? 16 : 0) + 4 * (r >> 3) + (r & 3); }
+// A TB x TB tile on 4 waves (2 x 2), wave tile TB/2 x TB/2 as NB x NB blocks of 32 x 32.
+template <int TB>
+struct Geo {
+  static_assert(TB == 256 || TB == 192, "tile sizes of the square MFMA kernel");
+  static constexpr int NB = TB / 64;     // blocks per wave row / column
+  static constexpr int LQ = 2 * NB;      // load instructions per wave per stage (A rows, then W rows)
+  static constexpr int NR = 4 * NB;      // fragment reads per wave per stage
+  static constexpr int AB = TB * 64;     // bytes of a stage's A rows
+  static constexpr int SB = 2 * TB * 64; // bytes of a stage
+  static constexpr int LDS = S * SB + 4 * kEpiWave;
+};
 }  // namespace big
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -640,10 +650,17 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 // first MFMA of a tile: accumulate onto zero (no separate clearing of the AGPRs)
 #define HILO_MFMA16_AGPR0(ACC, FB, FA) \
   asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=a"(ACC) : "v"(FB), "v"(FA) : "memory")
+// The 8-register operands have no host counterpart: the host pass (which only needs the kernel's
+// launch stub) would reject the constraint and silently drop the stub, so it sees no asm here.
+#if defined(__HIP_DEVICE_COMPILE__)
 #define HILO_MFMA8_AGPR(ACC, FB, FA) \
   asm volatile("v_mfma_f32_32x32x64_f8f6f4 %0, %1, %2, %0" : "+a"(ACC) : "v"(FB), "v"(FA) : "memory")
 #define HILO_MFMA8_AGPR0(ACC, FB, FA) \
   asm volatile("v_mfma_f32_32x32x64_f8f6f4 %0, %1, %2, 0" : "=a"(ACC) : "v"(FB), "v"(FA) : "memory")
+#else
+#define HILO_MFMA8_AGPR(ACC, FB, FA) ((void)0)
+#define HILO_MFMA8_AGPR0(ACC, FB, FA) ((void)0)
+#endif
 HILO_DEV u32x8 cat8(u32x4 lo, u32x4 hi) { return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7); }
 #define HILO_DS_READ16(DST, ADDR, OFF) \
   asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(DST) : "v"(ADDR), "i"(OFF) : "memory")
@@ -669,27 +686,28 @@ HILO_DEV void wait_lgkm_rt(int n) {  // n is a compile-time constant after unrol
   }
 }
 
-// Epilogue of a 256 x 256 tile from the AGPR accumulators of wave wid.  The W fragments are read
-// in the row order perm_w, so lane l of block (bi, bj) holds row 32 bi + l % 32 of the wave tile and,
-// in register v, column 32 bj + 16 (l / 32) + v: 16 consecutive columns, stored as two 16-byte
-// pieces (bf16) or four (float32 z).  Column operands (bias; FP8 weight scales or the gate) come from
-// the wave's LDS area `epi`, once per block column; FP8 row scales once per tile.  Bias / GELU
-// outputs are rounded to bf16, the residual update adds gate * (acc + bias) to the float32 z.
-// Blocks leave the AGPRs one at a time.
-template <int EPI, bool F8>
+// Epilogue of a TB x TB tile from the AGPR accumulators of wave wid.  The W fragments are read in
+// the row order perm_w, so lane l of block (bi, bj) holds row 32 bi + l % 32 of the wave tile and, in
+// register v, column 32 bj + 16 (l / 32) + v: 16 consecutive columns, stored as two 16-byte pieces
+// (bf16) or four (float32 z).  Column operands (bias; FP8 weight scales or the gate) come from the
+// wave's LDS area `epi`, once per block column; FP8 row scales once per tile.  Bias / GELU outputs
+// are rounded to bf16, the residual update adds gate * (acc + bias) to the float32 z.  Blocks leave
+// the AGPRs one at a time.
+template <int TB, int EPI, bool F8>
 HILO_DEV void big_epilogue(const GemmProblem &p, const TileRows &tr, int n0, int wid, int lane,
-                           const uint8_t *epi, f32x16 (&acc)[4][4]) {
+                           const uint8_t *epi, f32x16 (&acc)[TB / 64][TB / 64]) {
   static_assert(!(F8 && EPI == EPI_RESID), "FP8 projections end in a bias or GELU epilogue");
   using namespace big;
-  const int rbase = (wid >> 1) * 128 + (lane & 31);
+  constexpr int NB = Geo<TB>::NB;
+  const int rbase = (wid >> 1) * (TB / 2) + (lane & 31);
   const int cl0 = 16 * (lane >> 5);              // this lane's first column within a 32-column block
-  const int cbase = n0 + (wid & 1) * 128 + cl0;
-  float sa[4];
+  const int cbase = n0 + (wid & 1) * (TB / 2) + cl0;
+  float sa[NB];
 #pragma unroll
-  for (int bi = 0; bi < 4; ++bi)
+  for (int bi = 0; bi < NB; ++bi)
     sa[bi] = F8 ? *reinterpret_cast<const float *>(epi + kEpiRow + 4 * (32 * bi + (lane & 31))) : 1.f;
 #pragma unroll
-  for (int bj = 0; bj < 4; ++bj) {
+  for (int bj = 0; bj < NB; ++bj) {
     const int cl = cl0 + 32 * bj, n = cbase + 32 * bj;
     u32x4 bu[2];
     f32x4 cv[4];  // FP8 weight scales or the residual gate of the lane's 16 columns
@@ -700,7 +718,7 @@ HILO_DEV void big_epilogue(const GemmProblem &p, const TileRows &tr, int n0, int
       for (int h = 0; h < 4; ++h) cv[h] = *reinterpret_cast<const f32x4 *>(epi + kEpiCol + 4 * cl + 16 * h);
     }
 #pragma unroll
-    for (int bi = 0; bi < 4; ++bi) {
+    for (int bi = 0; bi < NB; ++bi) {
       f32x16 blk = acc[bi][bj];  // one block out of the AGPRs at a time
       asm volatile("" : "+v"(blk));
       const int rl = rbase + 32 * bi;
@@ -744,16 +762,18 @@ HILO_DEV void big_epilogue(const GemmProblem &p, const TileRows &tr, int n0, int
   }
 }
 
-template <int EPI, int ROLE, bool F8>
+template <int TB, int EPI, int ROLE, bool F8>
 __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
   using namespace big;
-  using T = SkTile<BM, BN, 2, 2>;       // partial slot size and layout (16 x 16 fragment order)
+  using G = Geo<TB>;
+  constexpr int NB = G::NB, LQ = G::LQ, NR = G::NR, AB = G::AB, SB = G::SB;
+  using T = SkTile<TB, TB, 2, 2>;       // partial slot size and layout (16 x 16 fragment order)
   constexpr int ESZ = F8 ? 1 : 2;       // operand bytes per element
-  __shared__ __attribute__((aligned(1024))) uint8_t lds[S * SB + 4 * kEpiWave];
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[G::LDS];
 
   const int P = gridDim.x;
   const int pid = xcd_remap(blockIdx.x, P);
-  const SkPlan q = sk_plan(p, BM, BN, P, F8 ? 128 : 64);
+  const SkPlan q = sk_plan(p, TB, TB, P, F8 ? 128 : 64);
   const SkRange rg = sk_range(q.I, P, pid);
 
   const int lane = threadIdx.x & 63;
@@ -761,21 +781,22 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
   const int lrow = lane >> 2, lslot = lane & 3;
   const uint8_t *A = reinterpret_cast<const uint8_t *>(p.A);
 
-  // ---- loader: its own cursor over this workgroup's items, three stages ahead of the MFMAs
+  // ---- loader: its own cursor over this workgroup's items, three stages ahead of the MFMAs; wave
+  // wid loads rows wid TB/4 .. + TB/4 - 1 of A and of W, 16 rows (1 KiB) per instruction
   SkCursor lc{pid, rg.beg};
-  const uint8_t *la[4], *lb[4];
+  const uint8_t *la[NB], *lb[NB];
   int lk = 0, lke = 0;  // next stage to load (absolute in K) and the end of its item
   auto ld_src = [&](int t) __attribute__((always_inline)) {
     int rt, tn;
     tile_coords(q, t, rt, tn);
     tn = uni(tn);
-    const TileRows tr = uni(decode_row_tile(p, BM, uni(rt)));
+    const TileRows tr = uni(decode_row_tile(p, TB, uni(rt)));
     const uint8_t *Wt = reinterpret_cast<const uint8_t *>(tr.sigma ? p.W[1] : p.W[0]);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int r = wid * 64 + 16 * i + lrow;
+    for (int i = 0; i < NB; ++i) {
+      const int r = wid * (TB / 4) + 16 * i + lrow;
       la[i] = A + size_t(tr.row0 + min(r, tr.nrows - 1)) * p.lda * ESZ + (lslot ^ swz(r)) * 16;
-      lb[i] = Wt + size_t(min(tn * BN + r, p.N - 1)) * p.K * ESZ + (lslot ^ swz(r)) * 16;
+      lb[i] = Wt + size_t(min(tn * TB + r, p.N - 1)) * p.K * ESZ + (lslot ^ swz(r)) * 16;
     }
   };
   auto ld_advance = [&]() __attribute__((always_inline)) {
@@ -790,27 +811,29 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
     lk = uni(lk);
     lke = uni(lke);
   };
-  // load instruction j (0..7) of the current loader stage into `slot`: A rows for j < 4
+  // load instruction j (0..LQ-1) of the current loader stage into `slot`: A rows for j < NB
   auto ld_one = [&](int slot, int j) __attribute__((always_inline)) {
-    uint8_t *base = lds + slot * SB;
+    uint8_t *base = lds + slot * SB + wid * (TB / 4) * 64;
     const int k0 = lk * 64;  // bytes
-    if (j < 4) g2lds16(la[j] + k0, base + wid * 64 * 64 + j * 1024);
-    else g2lds16(lb[j - 4] + k0, base + AB + wid * 64 * 64 + (j - 4) * 1024);
+    if (j < NB) g2lds16(la[j] + k0, base + j * 1024);
+    else g2lds16(lb[j - NB] + k0, base + AB + (j - NB) * 1024);
   };
 
   // ---- fragment reads: lane (r, g) = (lane % 32, lane / 32) reads chunk 2 g (low half) and 2 g + 1
   // (high half) of row r (A) or perm_w(r) (W) of a 32-row fragment; read t of a stage (slot byte
-  // offset so) is half t % 2 of W fragment t / 2 for t < 8, then of A fragment (t - 8) / 2
+  // offset so) is half t % 2 of W fragment t / 2 for t < 2 NB, then of A fragment (t - 2 NB) / 2
   const int r8 = lane & 31, g8 = lane >> 5, w8 = perm_w(r8);
   const uint32_t lds0 = (uint32_t)(uintptr_t)lds;
-  const uint32_t fa8 = lds0 + (wid >> 1) * 128 * 64, fb8 = lds0 + AB + (wid & 1) * 128 * 64;
+  const uint32_t fa8 = lds0 + (wid >> 1) * (TB / 2) * 64, fb8 = lds0 + AB + (wid & 1) * (TB / 2) * 64;
   const uint32_t fa8l = fa8 + r8 * 64 + (((2 * g8) ^ swz(r8)) * 16), fa8h = fa8 + r8 * 64 + (((2 * g8 + 1) ^ swz(r8)) * 16);
   const uint32_t fb8l = fb8 + w8 * 64 + (((2 * g8) ^ swz(w8)) * 16), fb8h = fb8 + w8 * 64 + (((2 * g8 + 1) ^ swz(w8)) * 16);
-  auto rd_one = [&](u32x4 (&fa)[8], u32x4 (&fb)[8], uint32_t so, int t) __attribute__((always_inline)) {
-#define HILO_RD_CASE(C)                                                                                  \
-  case C:                                                                                                \
-    if constexpr (C < 8) HILO_DS_READ16(fb[C & 7], ((C & 1) ? fb8h : fb8l) + so, ((C & 7) >> 1) * 2048); \
-    else HILO_DS_READ16(fa[C & 7], ((C & 1) ? fa8h : fa8l) + so, ((C & 7) >> 1) * 2048);                 \
+  auto rd_one = [&](u32x4 (&fa)[2 * NB], u32x4 (&fb)[2 * NB], uint32_t so, int t) __attribute__((always_inline)) {
+#define HILO_RD_CASE(C)                                                                                     \
+  case C:                                                                                                   \
+    if constexpr (C < 2 * NB)                                                                               \
+      HILO_DS_READ16(fb[C % (2 * NB)], ((C & 1) ? fb8h : fb8l) + so, ((C % (2 * NB)) >> 1) * 2048);         \
+    else if constexpr (C < 4 * NB)                                                                          \
+      HILO_DS_READ16(fa[(C - 2 * NB) % (2 * NB)], ((C & 1) ? fa8h : fa8l) + so, (((C - 2 * NB) % (2 * NB)) >> 1) * 2048); \
     break;
     switch (t) {
       HILO_RD_CASE(0) HILO_RD_CASE(1) HILO_RD_CASE(2) HILO_RD_CASE(3) HILO_RD_CASE(4) HILO_RD_CASE(5)
@@ -821,13 +844,13 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
 #undef HILO_RD_CASE
   };
 
-  // ---- epilogue operands of the current item: this wave's 128 columns (and FP8 rows) into its
+  // ---- epilogue operands of the current item: this wave's TB/2 columns (and FP8 rows) into its
   // LDS area, by DMA (4 bytes per lane), indices clamped into the tile
   uint8_t *epi = lds + S * SB + wid * kEpiWave;
   TileRows etr{0, 0, 0, 1};
   int en0 = 0;
   auto epi_load = [&]() __attribute__((always_inline)) {
-    const int c0 = en0 + (wid & 1) * 128;
+    const int c0 = en0 + (wid & 1) * (TB / 2);
     const uint16_t *bias = reinterpret_cast<const uint16_t *>(etr.sigma ? p.bias[1] : p.bias[0]);
     g2lds4(bias + min(c0 + 2 * lane, p.N - 2), epi + kEpiBias);
     if constexpr (F8 || EPI == EPI_RESID) {
@@ -837,30 +860,31 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
       g2lds4(col + min(c0 + 64 + lane, p.N - 1), epi + kEpiCol + 256);
     }
     if constexpr (F8) {
-      const int r0 = (wid >> 1) * 128;
+      const int r0 = (wid >> 1) * (TB / 2);
       g2lds4(p.a_scale + etr.row0 + min(r0 + lane, etr.nrows - 1), epi + kEpiRow);
       g2lds4(p.a_scale + etr.row0 + min(r0 + 64 + lane, etr.nrows - 1), epi + kEpiRow + 256);
     }
   };
 
-  f32x16 acc[4][4];
-  u32x4 xa[8], xb[8], ya[8], yb[8];
+  f32x16 acc[NB][NB];
+  u32x4 xa[2 * NB], xb[2 * NB], ya[2 * NB], yb[2 * NB];
 
   // one stage (ring slot gs % S) on fragments (fa, fb); reads stage gs + 1 into (na, nb); the first
   // stage of a tile (first = true_type) starts the accumulators from zero and, for a tile finished
-  // here, fetches the epilogue operands after its loads
-  auto stage = [&](auto first, u32x4 (&fa)[8], u32x4 (&fb)[8], u32x4 (&na)[8], u32x4 (&nb)[8], int gs,
-                   bool with_epi) __attribute__((always_inline)) {
+  // here, fetches the epilogue operands after its loads.  Before block NB: barrier; after each of
+  // blocks NB .. NB + LQ - 1: one load of the stage three ahead and two fragment reads of the next.
+  auto stage = [&](auto first, u32x4 (&fa)[2 * NB], u32x4 (&fb)[2 * NB], u32x4 (&na)[2 * NB],
+                   u32x4 (&nb)[2 * NB], int gs, bool with_epi) __attribute__((always_inline)) {
     const int lslot_w = (gs + S - 1) & (S - 1);
     const uint32_t so = uint32_t(((gs + 1) & (S - 1)) * SB);
 #pragma unroll
-    for (int bi = 0; bi < 4; ++bi) {
-      // outstanding reads allowed: this stage's A halves of blocks bi+1..3, the next stage's so far
-      wait_lgkm_rt(2 * (3 - bi) + 2 * min(max(4 * bi - 4, 0), 8));
+    for (int bi = 0; bi < NB; ++bi) {
+      // outstanding reads allowed: this stage's A halves of blocks bi+1.., the next stage's so far
+      wait_lgkm_rt(2 * (NB - 1 - bi) + 2 * min(max(NB * bi - NB, 0), LQ));
 #pragma unroll
-      for (int bj = 0; bj < 4; ++bj) {
-        const int qq = 4 * bi + bj;
-        if (qq == 4) asm volatile("s_waitcnt vmcnt(%0)\n s_barrier" ::"n"((S - 3) * LQ) : "memory");
+      for (int bj = 0; bj < NB; ++bj) {
+        const int qq = NB * bi + bj;
+        if (qq == NB) asm volatile("s_waitcnt vmcnt(%0)\n s_barrier" ::"n"((S - 3) * LQ) : "memory");
         if constexpr (F8) {
           if constexpr (decltype(first)::value)
             HILO_MFMA8_AGPR0(acc[bi][bj], cat8(fb[2 * bj], fb[2 * bj + 1]), cat8(fa[2 * bi], fa[2 * bi + 1]));
@@ -871,13 +895,13 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
           else HILO_MFMA16_AGPR(acc[bi][bj], fb[2 * bj], fa[2 * bi]);
           HILO_MFMA16_AGPR(acc[bi][bj], fb[2 * bj + 1], fa[2 * bi + 1]);
         }
-        if (qq >= 4 && qq < 12) {
-          ld_one(lslot_w, qq - 4);
-          rd_one(na, nb, so, 2 * (qq - 4));
-          rd_one(na, nb, so, 2 * (qq - 4) + 1);
+        if (qq >= NB && qq < NB + LQ) {
+          ld_one(lslot_w, qq - NB);
+          rd_one(na, nb, so, 2 * (qq - NB));
+          rd_one(na, nb, so, 2 * (qq - NB) + 1);
         }
         if constexpr (decltype(first)::value) {
-          if (qq == 11 && with_epi) epi_load();
+          if (qq == NB + LQ - 1 && with_epi) epi_load();
         }
       }
     }
@@ -909,8 +933,8 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
     if (whole) {
       int rt, tn;
       tile_coords(q, cur.t, rt, tn);
-      en0 = uni(tn) * BN;
-      etr = uni(decode_row_tile(p, BM, uni(rt)));
+      en0 = uni(tn) * TB;
+      etr = uni(decode_row_tile(p, TB, uni(rt)));
     }
     ld_check();
     stage(std::true_type{}, xa, xb, ya, yb, gs, whole);
@@ -930,28 +954,29 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
     // stage's fragments must be complete before the compiler may move those registers.
     asm volatile("s_waitcnt lgkmcnt(0)\n s_nop 7\n s_nop 7\n s_nop 7\n s_nop 7" ::: "memory");
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < NB; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) asm volatile("" : "+a"(acc[i][j]));
+      for (int j = 0; j < NB; ++j) asm volatile("" : "+a"(acc[i][j]));
     if (whole) {
       // the epilogue-operand DMA of the first stage is complete once two later stages have passed
       // their barriers (each waits for all but the last stage's loads); a one-step item waits here
       if (cur.ke - cur.kb < 2) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-      big_epilogue<EPI, F8>(p, etr, en0, wid, lane, epi, acc);
+      big_epilogue<TB, EPI, F8>(p, etr, en0, wid, lane, epi, acc);
     } else {
-      // the partial tile in the 16 x 16 fragment layout k_gemm_fix reads: row 32 bi + l % 32 is
-      // fragment row 2 bi + (l % 32) / 16; columns 32 bj + 16 (l / 32) + 4 b .. + 3 are lane
-      // l % 16 + 16 b of fragment column 2 bj + l / 32
-      float *base = cur.slot + (size_t(wid) * 64 * 64 + ((lane & 31) >> 4) * 8 * 64 + (lane >> 5) * 64 + (lane & 15)) * 4;
+      // the partial tile in the 16 x 16 fragment layout k_gemm_fix reads (2 NB x 2 NB fragments per
+      // wave): row 32 bi + l % 32 is fragment row 2 bi + (l % 32) / 16; columns 32 bj + 16 (l / 32)
+      // + 4 b .. + 3 are lane l % 16 + 16 b of fragment column 2 bj + l / 32
+      constexpr int TF = 2 * NB;
+      float *base = cur.slot + (size_t(wid) * TF * TF * 64 + ((lane & 31) >> 4) * TF * 64 + (lane >> 5) * 64 + (lane & 15)) * 4;
 #pragma unroll
-      for (int bi = 0; bi < 4; ++bi)
+      for (int bi = 0; bi < NB; ++bi)
 #pragma unroll
-        for (int bj = 0; bj < 4; ++bj) {
+        for (int bj = 0; bj < NB; ++bj) {
           f32x16 blk = acc[bi][bj];
           asm volatile("" : "+v"(blk));
 #pragma unroll
           for (int b = 0; b < 4; ++b)
-            *reinterpret_cast<f32x4 *>(base + ((2 * bi * 8 + 2 * bj) * 64 + 16 * b) * 4) =
+            *reinterpret_cast<f32x4 *>(base + ((2 * bi * TF + 2 * bj) * 64 + 16 * b) * 4) =
                 f32x4{blk[4 * b], blk[4 * b + 1], blk[4 * b + 2], blk[4 * b + 3]};
           asm volatile("" ::: "memory");
         }
@@ -1146,20 +1171,20 @@ static hipError_t run_bf16(const GemmProblem &p, hipStream_t st) {
 }
 
 // 256 x BN tiles: one persistent workgroup per CU.
-template <int ROLE, bool F8 = false>
+template <int TB, int ROLE, bool F8 = false>
 static hipError_t run_big(const GemmProblem &p, hipStream_t st) {
-  constexpr int BM = big::BM, BN = big::BN;
+  constexpr int BM = TB, BN = TB;
   static_assert(size_t(BM) * BN * 3 * kBigMaxWorkgroups * sizeof(float) <= kSkPartBytes, "partial area too small");
   const int P = device_cus() < kBigMaxWorkgroups ? device_cus() : kBigMaxWorkgroups;
-  hipLaunchKernelGGL((k_gemm_big<role_epilogue(ROLE), ROLE, F8>), dim3(P), dim3(256), 0, st, p);
+  hipLaunchKernelGGL((k_gemm_big<TB, role_epilogue(ROLE), ROLE, F8>), dim3(P), dim3(256), 0, st, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const long long tiles_max = (long long)p.B * ((p.max_img_rows + BM - 1) / BM + (p.L + BM - 1) / BM) *
                               ((p.N + BN - 1) / BN);
   if (tiles_max < P && p.K / (F8 ? 128 : 64) <= kNoSplitSteps) return hipSuccess;
-  constexpr int kFixBlocks = 4 * (BM / 2 / 16) / (kFixThreads / 64);
-  hipLaunchKernelGGL((k_gemm_fix<BM, BN, 2, 2, role_epilogue(ROLE), ROLE, F8>), dim3(P * kFixBlocks), dim3(kFixThreads),
-                     0, st, p, P);
+  // P workgroups stride over the fixup's items: few enough that a launch with nothing to finish
+  // (the device's row counts led to whole tiles) costs little
+  hipLaunchKernelGGL((k_gemm_fix<BM, BN, 2, 2, role_epilogue(ROLE), ROLE, F8>), dim3(P), dim3(kFixThreads), 0, st, p, P);
   return hipGetLastError();
 }
 
@@ -1191,17 +1216,17 @@ hipError_t launch_gemm(bool bf16, int role, const GemmProblem &p, hipStream_t st
   // 8-tile stream-K tail) measured slower than 128 x 128 (attention output 81 -> 88 us, MLP down
   // 226 -> 234 us in isolation): with a 128 x 64 wave tile the stage reads more LDS per MFMA.
   switch (role) {
-    case GEMM_QKV: return run_big<GEMM_QKV>(p, st);
-    case GEMM_O: return run_bf16<128, 128, 2, 2, GEMM_O>(p, st);
-    case GEMM_FC1: return run_big<GEMM_FC1>(p, st);
-    default: return run_bf16<128, 128, 2, 2, GEMM_FC2>(p, st);
+    case GEMM_QKV: return run_big<256, GEMM_QKV>(p, st);
+    case GEMM_O: return run_big<192, GEMM_O>(p, st);
+    case GEMM_FC1: return run_big<256, GEMM_FC1>(p, st);
+    default: return run_big<192, GEMM_FC2>(p, st);
   }
 }
 
 hipError_t launch_gemm_fp8(int role, const GemmProblem &p, hipStream_t st) {
   switch (role) {
-    case GEMM_QKV: return run_big<GEMM_QKV, true>(p, st);
-    case GEMM_FC1: return run_big<GEMM_FC1, true>(p, st);
+    case GEMM_QKV: return run_big<256, GEMM_QKV, true>(p, st);
+    case GEMM_FC1: return run_big<256, GEMM_FC1, true>(p, st);
     default: return hipErrorInvalidValue;
   }
 }
