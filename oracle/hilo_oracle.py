@@ -21,8 +21,8 @@ diffusion-transformer block on the shortened sequence and the reassembly of the 
                                                                      cost is quadratic in tokens)
   stack      blocks in order; request = one selection, then per   (Sec. 2.3: selection once per
              step compress -> stack -> decompress                   request; Sec. 3.3: 8 steps)
-  fp8        per-row E4M3 quantisation of the QKV / MLP-up        (Sec. 3.3: FP8 quantisation
-             operands                                               on top of the compression)
+  fp8        per-row E4M3 quantisation of the operands of the     (Sec. 3.3: FP8 quantisation
+             four projections                                       on top of the compression)
   decompress scatter fine rows, broadcast pooled rows to 4 patches
 
 Precision.  Floating point that decides an integer (the energy that decides which blocks stay
@@ -376,7 +376,8 @@ def dequant_rows(codes: np.ndarray, scale: np.ndarray) -> np.ndarray:
 
 
 def _fp8_matmul(h: np.ndarray, q) -> np.ndarray:
-    """h @ W^T with both operands FP8 per row (h rounded to float32 first, as the device holds it)."""
+    """h @ W^T with both operands FP8 per row: h quantised per row (rounded to float32 first), W given
+    as its per-output-channel codes and scales q = quantize_rows(W)."""
     hc, hs = quantize_rows(h.astype(np.float32))
     wc, ws = q
     return dequant_rows(hc, hs) @ dequant_rows(wc, ws).T
@@ -428,8 +429,9 @@ def attention(Z: np.ndarray, cu: np.ndarray, text_len: int, heads: int, weights,
 
     Joint attention over image + text tokens of one sample, no mask (Sec. 2.3: the HiLo tokens are
     processed by the DiT; Sec. 2.2: memory-efficient attention).  Returns z1 for `rows` (all rows
-    when None), float64 [len(rows)][D].  With `fp8` (per stream {"w_qkv": (codes, scale)}) the QKV
-    projection multiplies FP8 rows of h by FP8 rows of W_qkv (quantize_rows)."""
+    when None), float64 [len(rows)][D].  With `fp8` (per stream {"w_qkv": (codes, scale), "w_o": ...})
+    both projections multiply FP8 rows of their input (h, then a) by FP8 rows of the weight
+    (quantize_rows)."""
     T, D = Z.shape
     all_rows = np.arange(T) if rows is None else np.asarray(rows)
     out = np.empty((all_rows.size, D), dtype=np.float64)
@@ -452,7 +454,8 @@ def attention(Z: np.ndarray, cu: np.ndarray, text_len: int, heads: int, weights,
             m = (all_rows[sel] >= text_start) if sig == 1 else (all_rows[sel] < text_start)
             if not m.any():
                 continue
-            o = a_out[m] @ _w(weights, sig, "w_o").T + _w(weights, sig, "b_o")
+            prod = _fp8_matmul(a_out[m], fp8[sig]["w_o"]) if fp8 is not None else a_out[m] @ _w(weights, sig, "w_o").T
+            o = prod + _w(weights, sig, "b_o")
             out[sel[m]] = Z[all_rows[sel][m]] + mod[s, sig, 2] * o
     return out
 
@@ -462,8 +465,8 @@ def mlp(Z1: np.ndarray, row_ids: np.ndarray, cu: np.ndarray, text_len: int, weig
     """MLP half of the block: z2 = z1 + gate2 * (GELU_tanh(h2 W1^T + b1) W2^T + b2) with
     h2 = LN(z1) * (1 + scale2) + shift2.  Z1 holds the rows `row_ids` of the packed sequence (their
     sample and stream follow from cu_seqlens).  Returns float64 [len(row_ids)][D].  With `fp8`
-    (per stream {"w1": (codes, scale)}) the up projection multiplies FP8 rows of h2 by FP8 rows of
-    W1."""
+    (per stream {"w1": (codes, scale), "w2": ...}) both projections multiply FP8 rows of their input
+    (h2, then the GELU output) by FP8 rows of the weight."""
     out = np.empty_like(Z1, dtype=np.float64)
     row_ids = np.asarray(row_ids)
     for (s, sig, a, b) in _segments(cu, text_len):
@@ -474,7 +477,9 @@ def mlp(Z1: np.ndarray, row_ids: np.ndarray, cu: np.ndarray, text_len: int, weig
         h2 = layer_norm(z) * (1.0 + mod[s, sig, 4]) + mod[s, sig, 3]
         prod = _fp8_matmul(h2, fp8[sig]["w1"]) if fp8 is not None else h2 @ _w(weights, sig, "w1").T
         u = prod + _w(weights, sig, "b1")
-        o = gelu_tanh(u) @ _w(weights, sig, "w2").T + _w(weights, sig, "b2")
+        g = gelu_tanh(u)
+        prod = _fp8_matmul(g, fp8[sig]["w2"]) if fp8 is not None else g @ _w(weights, sig, "w2").T
+        o = prod + _w(weights, sig, "b2")
         out[m] = z + mod[s, sig, 5] * o
     return out
 
@@ -482,17 +487,20 @@ def mlp(Z1: np.ndarray, row_ids: np.ndarray, cu: np.ndarray, text_len: int, weig
 def block(Z: np.ndarray, cu: np.ndarray, text_len: int, heads: int, weights, mod: np.ndarray,
           rows: Optional[np.ndarray] = None, fp8=None) -> Tuple[np.ndarray, np.ndarray]:
     """Whole block on the packed sequence: returns (z1, z2) for `rows` (all rows when None).
-    `fp8`: per stream {"w_qkv": (codes, scale), "w1": (codes, scale)} for FP8 QKV and MLP-up
-    projections (quantize_fp8_weights)."""
+    `fp8`: per stream {name: (codes, scale)} for name in w_qkv, w_o, w1, w2: all four projections on
+    FP8 operands (quantize_fp8_weights)."""
     rows = np.arange(Z.shape[0]) if rows is None else np.asarray(rows)
     z1 = attention(Z, cu, text_len, heads, weights, mod, rows, fp8)
     z2 = mlp(z1, rows, cu, text_len, weights, mod, fp8)
     return z1, z2
 
 
+FP8_WEIGHTS = ("w_qkv", "w_o", "w1", "w2")
+
+
 def quantize_fp8_weights(weights) -> List[Dict[str, Tuple[np.ndarray, np.ndarray]]]:
-    """Per stream, the FP8 rows (per output channel) of W_qkv and W1."""
-    return [{name: quantize_rows(np.asarray(w[name], dtype=np.float32)) for name in ("w_qkv", "w1")}
+    """Per stream, the FP8 rows (per output channel) of the four projection weights."""
+    return [{name: quantize_rows(np.asarray(w[name], dtype=np.float32)) for name in FP8_WEIGHTS}
             for w in weights]
 
 

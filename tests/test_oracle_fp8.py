@@ -48,3 +48,38 @@ def test_fp8_block_stays_close_to_the_bf16_block():
     b = O.pipeline(wl.x_img, wl.x_txt, shp, None, 0, "topk", keep=wl.keep, weights=wl.weights, mod=wl.mod, fp8=True)
     d = np.abs(b["y_img"] - a["y_img"]).max()
     assert 0 < d < 0.1
+
+
+def test_fp8_product_of_exactly_representable_rows_is_the_plain_product():
+    # rows whose amax is 448 and whose entries are E4M3 values quantise to themselves (scale 1), so
+    # the FP8 product is the exact product; a row scaled by 2^-3 keeps exact codes with scale 2^-3
+    rng = np.random.default_rng(5)
+    vals = O.e4m3_value(np.arange(0x00, 0x7f, dtype=np.uint8))
+    h = rng.choice(vals, size=(3, 16)) * rng.choice([-1.0, 1.0], size=(3, 16))
+    w = rng.choice(vals, size=(5, 16)) * rng.choice([-1.0, 1.0], size=(5, 16))
+    h[:, 0], w[:, 0] = 448.0, 448.0
+    h[2] *= 0.125
+    got = O._fp8_matmul(h.astype(np.float32), O.quantize_rows(w.astype(np.float32)))
+    np.testing.assert_array_equal(got, h @ w.T)
+
+
+def test_fp8_block_quantises_all_four_projections():
+    # zero the output and down projection weights of one stream's FP8 codes only: the FP8 block's
+    # update then differs from the one with full codes, so those projections do read FP8 weights
+    shp = inputs.BlockShape(1, 1, 8, 10, 4, 256, 2, 128, 1024, "bf16")
+    wl = inputs.make_workload("smallx", shape=shp, seed=52)
+    res = O.pipeline(wl.x_img, wl.x_txt, shp, None, 0, "topk", keep=wl.keep, with_block=False)
+    q = O.quantize_fp8_weights(wl.weights)
+    assert set(q[0]) == {"w_qkv", "w_o", "w1", "w2"}
+    z1, z2 = O.block(res["Z"], res["cu"], shp.text_len, shp.heads, wl.weights, wl.mod, fp8=q)
+    for name in ("w_o", "w2"):
+        q0 = [dict(d) for d in q]
+        for d in q0:
+            d[name] = (np.zeros_like(d[name][0]), d[name][1])
+        y1, y2 = O.block(res["Z"], res["cu"], shp.text_len, shp.heads, wl.weights, wl.mod, fp8=q0)
+        assert np.abs(y2 - z2).max() > 1e-4, name
+        if name == "w_o":
+            # with the output projection zeroed the attention half adds the gated bias only
+            Z = res["Z"]
+            for (s_, sig, a, b) in O._segments(res["cu"], shp.text_len):
+                np.testing.assert_allclose(y1[a:b], Z[a:b] + wl.mod[s_, sig, 2] * np.asarray(wl.weights[sig]["b_o"], np.float64), atol=1e-12)
