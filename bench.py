@@ -177,11 +177,11 @@ def token_set_leg(db, steps, warmup, stream, dense_ms):
 
 
 def fp8_leg(db, steps, warmup, stream, work, bf16_ms):
-    """The step with the QKV and MLP-up projections in FP8 (per-row E4M3 operands: one scale per
-    token for the normalised activations, one per output channel for the weights; Sec. 3.3 combines
-    the compression with FP8 quantisation): step latency, the two projections' rates against the
-    fp8 MFMA peak, and how far the block's update of the compressed tokens moves from the bf16
-    step's (relative L2 over all rows)."""
+    """The step with all four projections in FP8 (per-row E4M3 operands: one scale per token for the
+    activations, one per output channel for the weights; Sec. 3.3 combines the compression with FP8
+    quantisation): step latency, the projections' rates against the fp8 MFMA peak, the two passes
+    that quantise the attention and GELU outputs, and how far the block's update of the compressed
+    tokens moves from the bf16 step's (relative L2 over all rows)."""
     import numpy as np
     import torch
 
@@ -224,7 +224,8 @@ def fp8_leg(db, steps, warmup, stream, work, bf16_ms):
     for k in range(hilo.hilo_profile_kinds()):
         name = hilo.hilo_profile_name(k)
         tot, n = hilo.hilo_profile_read(k)
-        if n and name in ("rownorm_attn", "gemm_qkv", "rownorm_mlp", "gemm_fc1"):
+        if n and name in ("rownorm_attn", "gemm_qkv", "quantize_attn", "gemm_o", "rownorm_mlp", "gemm_fc1",
+                          "quantize_mlp", "gemm_fc2"):
             avg = tot / n
             ent = {"ms": round(avg, 4)}
             if name.startswith("gemm"):
@@ -236,7 +237,7 @@ def fp8_leg(db, steps, warmup, stream, work, bf16_ms):
     db.run(hilo.TOPK)  # leave the buffers as the default step left them
     torch.cuda.synchronize()
     res = {"ms_per_step": round(ms, 4), "ms_per_step_median": round(float(per_step[len(per_step) // 2]), 4),
-           "projections_in_fp8": ["qkv", "mlp_up"], "kernels": kern,
+           "projections_in_fp8": ["qkv", "attention_output", "mlp_up", "mlp_down"], "kernels": kern,
            "block_update_rel_l2_vs_bf16": round(rel, 5)}
     if bf16_ms:
         res["speedup_vs_bf16_step"] = round(bf16_ms / ms, 3)
@@ -342,7 +343,7 @@ def main():
     ap.add_argument("--no-pixel-score", action="store_true",
                     help="skip the pixel-space scorer leg (Sobel on the 16x-resolution RGB image)")
     ap.add_argument("--no-fp8", action="store_true",
-                    help="skip the step with FP8 QKV / MLP-up projections")
+                    help="skip the step with FP8 projections")
     ap.add_argument("--stack-blocks", type=int, default=8)
     ap.add_argument("--stack-steps", type=int, default=8)
     ap.add_argument("--copy-mib", type=int, default=0,
@@ -461,7 +462,7 @@ def main():
         pixel = pixel_leg(db, args.steps, args.warmup, stream)
 
     fp8 = None
-    if not args.no_fp8 and s.dtype == "bf16" and s.dim % 128 == 0:
+    if not args.no_fp8 and s.dtype == "bf16" and s.dim % 128 == 0 and s.mlp_dim % 128 == 0:
         fp8 = fp8_leg(db, args.steps, args.warmup, stream, work, ms)
 
     stack = None

@@ -41,7 +41,7 @@
 extern "C" {
 #endif
 
-#define HILO_ABI_VERSION 3
+#define HILO_ABI_VERSION 4
 
 typedef enum {
   HILO_OK = 0,
@@ -188,19 +188,23 @@ hilo_status hilo_blocks(const hilo_shape *shape, float *z, const int32_t *cu_seq
  * is quantised as (every step one float32 operation)
  *   amax = max |x|;  inv = 448 / amax (correctly rounded; 0 when amax == 0)
  *   code = round-to-nearest-even E4M3 of clamp(x * inv, -448, 448);  scale = amax / 448
- * so that value(code) * scale approximates x.  The FP8 block runs the QKV and MLP-up projections
- * on such rows -- activations per token, weights per output channel -- with exact products and
- * float32 accumulation: acc = sum_k value(hcode[m][k]) value(wcode[n][k]), then
- * out = acc * (hscale[m] * wscale[n]) + bias.  Everything else is as in the bf16 block.         */
+ * so that value(code) * scale approximates x.  The FP8 block runs all four projections (QKV,
+ * attention output, MLP up, MLP down) on such rows -- activations per token, weights per output
+ * channel -- with exact products and float32 accumulation: acc = sum_k value(xcode[m][k])
+ * value(wcode[n][k]), then out = acc * (xscale[m] * wscale[n]) + bias.  The normalised rows h and
+ * h2 are quantised where they are formed (float32, no bf16 rounding first); the attention output
+ * and the GELU output, which other kernels produce in bf16, by a pass over their rows.  Everything
+ * else is as in the bf16 block.                                                                  */
 
-/* Weights of the FP8 block: W_qkv and W1 as E4M3 codes with one float32 scale per output channel
- * (per row of the [out][in] matrix, hilo_quantize_rows), the other tensors bf16 as in
- * hilo_attn_w / hilo_mlp_w.  Arrays of two per block: image stream, text stream.                */
+/* Weights of the FP8 block: the four projection weights as E4M3 codes with one float32 scale per
+ * output channel (per row of the [out][in] matrix, hilo_quantize_rows), biases bf16.  Arrays of
+ * two per block: image stream, text stream.                                                      */
 typedef struct {
   const uint8_t *w_qkv; /* [3D][D] E4M3 codes */
   const float *s_qkv;   /* [3D] row scales    */
   const void *b_qkv;    /* [3D] bf16          */
-  const void *w_o;      /* [D][D] bf16        */
+  const uint8_t *w_o;   /* [D][D] E4M3 codes  */
+  const float *s_o;     /* [D] row scales     */
   const void *b_o;      /* [D] bf16           */
 } hilo_attn_w_fp8;
 
@@ -208,7 +212,8 @@ typedef struct {
   const uint8_t *w1; /* [F][D] E4M3 codes */
   const float *s1;   /* [F] row scales    */
   const void *b1;    /* [F] bf16          */
-  const void *w2;    /* [D][F] bf16       */
+  const uint8_t *w2; /* [D][F] E4M3 codes */
+  const float *s2;   /* [D] row scales    */
   const void *b2;    /* [D] bf16          */
 } hilo_mlp_w_fp8;
 
@@ -219,18 +224,22 @@ typedef struct {
 hilo_status hilo_quantize_rows(int32_t dtype, const void *x, int64_t rows, int64_t cols,
                                uint8_t *codes, float *scale, void *stream);
 
-/* hilo_attention with the QKV projection in FP8: h = LN(z) * (1 + scale1) + shift1 is formed in
- * float32 and quantised per row straight from registers (no bf16 rounding first), then multiplied
- * by the FP8 W_qkv as described above; qkv is rounded to bf16.  The attention core and the output
- * projection are those of hilo_attention.  shape->dtype must be HILO_BF16 (HILO_E_DTYPE) and dim a
- * multiple of 128 (HILO_E_SHAPE).  workspace as hilo_attention.                                  */
+/* Workspace of the FP8 block (hilo_attention_fp8, hilo_mlp_fp8): hilo_workspace_bytes plus the
+ * hidden rows' codes and scales; 0 if the shape is invalid for the FP8 block.                    */
+size_t hilo_workspace_bytes_fp8(const hilo_shape *shape);
+
+/* hilo_attention with both projections in FP8: h = LN(z) * (1 + scale1) + shift1 is formed in
+ * float32 and quantised per row straight from registers, then multiplied by the FP8 W_qkv; the
+ * attention core is that of hilo_attention (bf16 q, k, v, output); its output rows are quantised and
+ * multiplied by the FP8 W_o.  shape->dtype must be HILO_BF16 (HILO_E_DTYPE), dim and mlp_dim
+ * multiples of 128 (HILO_E_SHAPE).  workspace: ws_bytes >= hilo_workspace_bytes(shape).           */
 hilo_status hilo_attention_fp8(const hilo_shape *shape, float *z, const int32_t *cu_seqlens,
                                const hilo_attn_w_fp8 w[2], const float *mod, void *workspace,
                                size_t ws_bytes, void *stream);
 
-/* hilo_mlp with the up projection in FP8 (h2 quantised per row, W1 as codes and scales); GELU,
- * the down projection and the gated residual as in hilo_mlp.  Requirements as
- * hilo_attention_fp8.                                                                            */
+/* hilo_mlp with both projections in FP8 (h2 quantised where it is formed, the GELU output by a pass
+ * over its bf16 rows); the gated residual as in hilo_mlp.  Requirements as hilo_attention_fp8;
+ * workspace: ws_bytes >= hilo_workspace_bytes_fp8(shape).                                        */
 hilo_status hilo_mlp_fp8(const hilo_shape *shape, float *z, const int32_t *cu_seqlens,
                          const hilo_mlp_w_fp8 w[2], const float *mod, void *workspace,
                          size_t ws_bytes, void *stream);

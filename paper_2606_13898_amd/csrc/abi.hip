@@ -14,11 +14,12 @@ namespace {
 
 enum Kind {
   K_SCORE, K_SELECT, K_LAYOUT, K_COMPRESS, K_NORM_ATTN, K_GEMM_QKV, K_ATTN_CORE, K_GEMM_O,
-  K_NORM_MLP, K_GEMM_FC1, K_GEMM_FC2, K_DECOMPRESS, K_COUNT
+  K_NORM_MLP, K_GEMM_FC1, K_GEMM_FC2, K_DECOMPRESS, K_QUANT_ATTN, K_QUANT_MLP, K_COUNT
 };
 const char *kKindNames[K_COUNT] = {"score", "select", "layout", "compress", "rownorm_attn",
                                    "gemm_qkv", "attention_core", "gemm_o", "rownorm_mlp",
-                                   "gemm_fc1", "gemm_fc2", "decompress"};
+                                   "gemm_fc1", "gemm_fc2", "decompress", "quantize_attn",
+                                   "quantize_mlp"};
 
 struct ProfRec {
   int kind;
@@ -118,6 +119,12 @@ size_t ws_attention(const hilo_shape *s) {
 size_t ws_mlp(const hilo_shape *s) {
   const size_t T = size_t(tmax_of(s)), F = size_t(s->mlp_dim), e = esize(s);
   return ws_h(s) + align256(T * F * e) + ws_part(s);  // h2, hidden, partials
+}
+
+// The FP8 MLP also holds the hidden rows as codes [T][F] and T row scales, behind the rest.
+size_t ws_mlp_fp8(const hilo_shape *s) {
+  const size_t T = size_t(tmax_of(s)), F = size_t(s->mlp_dim);
+  return ws_mlp(s) + align256(T * F) + align256(T * sizeof(float));
 }
 
 hilo_status dev_status(hipError_t e) { return e == hipSuccess ? HILO_OK : HILO_E_DEVICE; }
@@ -323,23 +330,23 @@ hilo_status check_mlp_w(const hilo_mlp_w *w) {
 hilo_status check_attn_w8(const hilo_attn_w_fp8 *w) {
   if (!w) return HILO_E_NULL;
   for (int k = 0; k < 2; ++k)
-    if (!w[k].w_qkv || !w[k].s_qkv || !w[k].b_qkv || !w[k].w_o || !w[k].b_o) return HILO_E_NULL;
+    if (!w[k].w_qkv || !w[k].s_qkv || !w[k].b_qkv || !w[k].w_o || !w[k].s_o || !w[k].b_o) return HILO_E_NULL;
   return HILO_OK;
 }
 
 hilo_status check_mlp_w8(const hilo_mlp_w_fp8 *w) {
   if (!w) return HILO_E_NULL;
   for (int k = 0; k < 2; ++k)
-    if (!w[k].w1 || !w[k].s1 || !w[k].b1 || !w[k].w2 || !w[k].b2) return HILO_E_NULL;
+    if (!w[k].w1 || !w[k].s1 || !w[k].b1 || !w[k].w2 || !w[k].s2 || !w[k].b2) return HILO_E_NULL;
   return HILO_OK;
 }
 
-// The FP8 block: bf16 activations and weights elsewhere, K = dim in whole 128-deep steps.
+// The FP8 block: bf16 shape; every projection's K (dim, mlp_dim) in whole 128-deep steps.
 hilo_status check_fp8_block(const hilo_shape *s) {
   hilo_status e = check_block(s);
   if (e != HILO_OK) return e;
   if (s->dtype != HILO_BF16) return HILO_E_DTYPE;
-  if (s->dim % 128 != 0) return HILO_E_SHAPE;
+  if (s->dim % 128 != 0 || s->mlp_dim % 128 != 0) return HILO_E_SHAPE;
   return HILO_OK;
 }
 
@@ -395,10 +402,23 @@ hilo_status enqueue_attention(const hilo_shape *s, float *z, const int32_t *cu_s
 
   GemmProblem q = base_problem(s, cu_seqlens, mod, part);
   q.A = h; q.lda = D;
-  q.W[0] = w8 ? w8[0].w_o : w[0].w_o; q.W[1] = w8 ? w8[1].w_o : w[1].w_o;
-  q.bias[0] = w8 ? w8[0].b_o : w[0].b_o; q.bias[1] = w8 ? w8[1].b_o : w[1].b_o;
   q.N = D; q.K = D;
   q.z = z; q.ldz = D; q.gate_idx = 2;
+  if (w8) {
+    // the attention output's rows as FP8 codes and scales, in the QKV region (free again)
+    uint8_t *ac = reinterpret_cast<uint8_t *>(qkv);
+    float *as = reinterpret_cast<float *>(ac + align256(size_t(T) * D));
+    he = timed(K_QUANT_ATTN, st, [&] { return launch_quantize_rows(true, h, T, D, ac, as, st, cu_seqlens + s->batch); });
+    if (he != hipSuccess) return HILO_E_DEVICE;
+    q.A = ac;
+    q.W[0] = w8[0].w_o; q.W[1] = w8[1].w_o;
+    q.bias[0] = w8[0].b_o; q.bias[1] = w8[1].b_o;
+    q.a_scale = as;
+    q.w_scale[0] = w8[0].s_o; q.w_scale[1] = w8[1].s_o;
+    return dev_status(timed(K_GEMM_O, st, [&] { return launch_gemm_fp8(GEMM_O, q, st); }));
+  }
+  q.W[0] = w[0].w_o; q.W[1] = w[1].w_o;
+  q.bias[0] = w[0].b_o; q.bias[1] = w[1].b_o;
   return dev_status(timed(K_GEMM_O, st, [&] { return launch_gemm(bf, GEMM_O, q, st); }));
 }
 
@@ -442,10 +462,23 @@ hilo_status enqueue_mlp(const hilo_shape *s, float *z, const int32_t *cu_seqlens
 
   GemmProblem q = base_problem(s, cu_seqlens, mod, part);
   q.A = hid; q.lda = F;
-  q.W[0] = w8 ? w8[0].w2 : w[0].w2; q.W[1] = w8 ? w8[1].w2 : w[1].w2;
-  q.bias[0] = w8 ? w8[0].b2 : w[0].b2; q.bias[1] = w8 ? w8[1].b2 : w[1].b2;
   q.N = D; q.K = F;
   q.z = z; q.ldz = D; q.gate_idx = 5;
+  if (w8) {
+    // the hidden rows as FP8 codes and scales, behind everything the bf16 MLP uses
+    uint8_t *hc = reinterpret_cast<uint8_t *>(ws + ws_mlp(s));
+    float *hs8 = reinterpret_cast<float *>(hc + align256(size_t(T) * F));
+    he = timed(K_QUANT_MLP, st, [&] { return launch_quantize_rows(true, hid, T, F, hc, hs8, st, cu_seqlens + s->batch); });
+    if (he != hipSuccess) return HILO_E_DEVICE;
+    q.A = hc;
+    q.W[0] = w8[0].w2; q.W[1] = w8[1].w2;
+    q.bias[0] = w8[0].b2; q.bias[1] = w8[1].b2;
+    q.a_scale = hs8;
+    q.w_scale[0] = w8[0].s2; q.w_scale[1] = w8[1].s2;
+    return dev_status(timed(K_GEMM_FC2, st, [&] { return launch_gemm_fp8(GEMM_FC2, q, st); }));
+  }
+  q.W[0] = w[0].w2; q.W[1] = w[1].w2;
+  q.bias[0] = w[0].b2; q.bias[1] = w[1].b2;
   return dev_status(timed(K_GEMM_FC2, st, [&] { return launch_gemm(bf, GEMM_FC2, q, st); }));
 }
 
@@ -477,6 +510,12 @@ hilo_status hilo_mlp(const hilo_shape *s, float *z, const int32_t *cu_seqlens,
   return enqueue_mlp(s, z, cu_seqlens, w, nullptr, mod, workspace, reinterpret_cast<hipStream_t>(stream));
 }
 
+size_t hilo_workspace_bytes_fp8(const hilo_shape *s) {
+  if (check_fp8_block(s) != HILO_OK) return 0;
+  const size_t a = ws_attention(s), m = ws_mlp_fp8(s);
+  return a > m ? a : m;
+}
+
 hilo_status hilo_attention_fp8(const hilo_shape *s, float *z, const int32_t *cu_seqlens,
                                const hilo_attn_w_fp8 w[2], const float *mod, void *workspace,
                                size_t ws_bytes, void *stream) {
@@ -496,7 +535,7 @@ hilo_status hilo_mlp_fp8(const hilo_shape *s, float *z, const int32_t *cu_seqlen
   if (e != HILO_OK) return e;
   if (!z || !cu_seqlens || !mod || !workspace) return HILO_E_NULL;
   if ((e = check_mlp_w8(w)) != HILO_OK) return e;
-  if (ws_bytes < ws_mlp(s)) return HILO_E_WORKSPACE;
+  if (ws_bytes < ws_mlp_fp8(s)) return HILO_E_WORKSPACE;
   if (!have_device()) return HILO_E_DEVICE;
   return enqueue_mlp(s, z, cu_seqlens, nullptr, w, mod, workspace, reinterpret_cast<hipStream_t>(stream));
 }

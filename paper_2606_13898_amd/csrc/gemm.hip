@@ -620,8 +620,9 @@ HILO_DEV TileRows uni(const TileRows &x) { return TileRows{uni(x.s), uni(x.sigma
 namespace big {
 constexpr int S = 4;                   // LDS ring slots
 // per wave, behind the ring: the wave's columns of bias (bf16, <= 256 B), of the FP8 weight scales
-// or the residual gate (float32, <= 512 B), and its rows of FP8 activation scales (<= 512 B)
-constexpr int kEpiWave = 1280, kEpiBias = 0, kEpiCol = 256, kEpiRow = 768;
+// (float32, <= 512 B), its rows of FP8 activation scales (<= 512 B) and its columns of the residual
+// gate (float32, <= 512 B)
+constexpr int kEpiWave = 1792, kEpiBias = 0, kEpiCol = 256, kEpiRow = 768, kEpiGate = 1280;
 HILO_DEV int swz(int r) { return ((r >> 1) & 3) ^ ((r >> 3) & 1); }
 // W row read by fragment lane r.  The 32 x 32 MFMA's output row i (the W side) lands in
 // accumulator register 4 (i / 8) + i % 4 of the lanes of half (i / 4) % 2; reading W row perm_w(i)
@@ -689,14 +690,13 @@ HILO_DEV void wait_lgkm_rt(int n) {  // n is a compile-time constant after unrol
 // Epilogue of a TB x TB tile from the AGPR accumulators of wave wid.  The W fragments are read in
 // the row order perm_w, so lane l of block (bi, bj) holds row 32 bi + l % 32 of the wave tile and, in
 // register v, column 32 bj + 16 (l / 32) + v: 16 consecutive columns, stored as two 16-byte pieces
-// (bf16) or four (float32 z).  Column operands (bias; FP8 weight scales or the gate) come from the
+// (bf16) or four (float32 z).  Column operands (bias, FP8 weight scales, the gate) come from the
 // wave's LDS area `epi`, once per block column; FP8 row scales once per tile.  Bias / GELU outputs
 // are rounded to bf16, the residual update adds gate * (acc + bias) to the float32 z.  Blocks leave
 // the AGPRs one at a time.
 template <int TB, int EPI, bool F8>
 HILO_DEV void big_epilogue(const GemmProblem &p, const TileRows &tr, int n0, int wid, int lane,
                            const uint8_t *epi, f32x16 (&acc)[TB / 64][TB / 64]) {
-  static_assert(!(F8 && EPI == EPI_RESID), "FP8 projections end in a bias or GELU epilogue");
   using namespace big;
   constexpr int NB = Geo<TB>::NB;
   const int rbase = (wid >> 1) * (TB / 2) + (lane & 31);
@@ -710,12 +710,16 @@ HILO_DEV void big_epilogue(const GemmProblem &p, const TileRows &tr, int n0, int
   for (int bj = 0; bj < NB; ++bj) {
     const int cl = cl0 + 32 * bj, n = cbase + 32 * bj;
     u32x4 bu[2];
-    f32x4 cv[4];  // FP8 weight scales or the residual gate of the lane's 16 columns
+    f32x4 cv[4], gv[4];  // FP8 weight scales and the residual gate of the lane's 16 columns
 #pragma unroll
     for (int h = 0; h < 2; ++h) bu[h] = *reinterpret_cast<const u32x4 *>(epi + kEpiBias + 2 * cl + 16 * h);
-    if constexpr (F8 || EPI == EPI_RESID) {
+    if constexpr (F8) {
 #pragma unroll
       for (int h = 0; h < 4; ++h) cv[h] = *reinterpret_cast<const f32x4 *>(epi + kEpiCol + 4 * cl + 16 * h);
+    }
+    if constexpr (EPI == EPI_RESID) {
+#pragma unroll
+      for (int h = 0; h < 4; ++h) gv[h] = *reinterpret_cast<const f32x4 *>(epi + kEpiGate + 4 * cl + 16 * h);
     }
 #pragma unroll
     for (int bi = 0; bi < NB; ++bi) {
@@ -739,10 +743,10 @@ HILO_DEV void big_epilogue(const GemmProblem &p, const TileRows &tr, int n0, int
           for (int h = 0; h < 4; ++h) z[h] = zp[h];
 #pragma unroll
           for (int h = 0; h < 4; ++h) {
-            z[h].x += cv[h][0] * v[4 * h + 0];
-            z[h].y += cv[h][1] * v[4 * h + 1];
-            z[h].z += cv[h][2] * v[4 * h + 2];
-            z[h].w += cv[h][3] * v[4 * h + 3];
+            z[h].x += gv[h][0] * v[4 * h + 0];
+            z[h].y += gv[h][1] * v[4 * h + 1];
+            z[h].z += gv[h][2] * v[4 * h + 2];
+            z[h].w += gv[h][3] * v[4 * h + 3];
             zp[h] = z[h];
           }
         } else {
@@ -853,11 +857,15 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
     const int c0 = en0 + (wid & 1) * (TB / 2);
     const uint16_t *bias = reinterpret_cast<const uint16_t *>(etr.sigma ? p.bias[1] : p.bias[0]);
     g2lds4(bias + min(c0 + 2 * lane, p.N - 2), epi + kEpiBias);
-    if constexpr (F8 || EPI == EPI_RESID) {
-      const float *col = F8 ? (etr.sigma ? p.w_scale[1] : p.w_scale[0])
-                            : p.mod + (size_t(etr.s * 2 + etr.sigma) * 6 + p.gate_idx) * p.D;
-      g2lds4(col + min(c0 + lane, p.N - 1), epi + kEpiCol);
-      g2lds4(col + min(c0 + 64 + lane, p.N - 1), epi + kEpiCol + 256);
+    if constexpr (F8) {
+      const float *ws = etr.sigma ? p.w_scale[1] : p.w_scale[0];
+      g2lds4(ws + min(c0 + lane, p.N - 1), epi + kEpiCol);
+      g2lds4(ws + min(c0 + 64 + lane, p.N - 1), epi + kEpiCol + 256);
+    }
+    if constexpr (EPI == EPI_RESID) {
+      const float *gate = p.mod + (size_t(etr.s * 2 + etr.sigma) * 6 + p.gate_idx) * p.D;
+      g2lds4(gate + min(c0 + lane, p.N - 1), epi + kEpiGate);
+      g2lds4(gate + min(c0 + 64 + lane, p.N - 1), epi + kEpiGate + 256);
     }
     if constexpr (F8) {
       const int r0 = (wid >> 1) * (TB / 2);
@@ -1226,8 +1234,9 @@ hipError_t launch_gemm(bool bf16, int role, const GemmProblem &p, hipStream_t st
 hipError_t launch_gemm_fp8(int role, const GemmProblem &p, hipStream_t st) {
   switch (role) {
     case GEMM_QKV: return run_big<256, GEMM_QKV, true>(p, st);
+    case GEMM_O: return run_big<192, GEMM_O, true>(p, st);
     case GEMM_FC1: return run_big<256, GEMM_FC1, true>(p, st);
-    default: return hipErrorInvalidValue;
+    default: return run_big<192, GEMM_FC2, true>(p, st);
   }
 }
 

@@ -36,9 +36,10 @@ hipError_t launch_rownorm(bool bf16, const float *z, const int *cu, const float 
 // the same rows as FP8 E4M3 codes [Tmax][D] plus a float32 scale per row (D % 4 == 0)
 hipError_t launch_rownorm_fp8(const float *z, const int *cu, const float *mod, int B, int L, int D,
                               int Tmax, int which, uint8_t *codes, float *row_scale, hipStream_t st);
-// per-row FP8 E4M3 codes and scales of x [rows][cols] (cols % 4 == 0)
+// per-row FP8 E4M3 codes and scales of x [rows][cols] (cols % 4 == 0); with row_limit (device
+// pointer), only rows below *row_limit
 hipError_t launch_quantize_rows(bool bf16, const void *x, int rows, int cols, uint8_t *codes, float *scale,
-                                hipStream_t st);
+                                hipStream_t st, const int *row_limit = nullptr);
 
 enum Epilogue { EPI_BIAS = 0, EPI_GELU = 1, EPI_RESID = 2 };
 // The four projections of the block; each gets its own kernel instantiation (so profiles and
@@ -79,8 +80,8 @@ constexpr size_t kSkPartBytes = size_t(kBigMaxWorkgroups) * 3 * 256 * 256 * size
 static_assert(size_t(kSkMaxWorkgroups) * 3 * kSkPartFloats * sizeof(float) <= kSkPartBytes,
               "partial area must hold both tilings");
 hipError_t launch_gemm(bool bf16, int role, const GemmProblem &p, hipStream_t st);
-// FP8 E4M3 operands (A [Tmax][K] codes, W[s] [N][K] codes, per-row scales), bf16 bias and output;
-// the QKV and MLP-up roles only, K % 128 == 0, N % 4 == 0.
+// FP8 E4M3 operands (A [Tmax][K] codes, W[s] [N][K] codes, per-row scales), bf16 bias; the
+// epilogue of the role (bf16 output or the float32 residual update); K % 128 == 0, N % 16 == 0.
 hipError_t launch_gemm_fp8(int role, const GemmProblem &p, hipStream_t st);
 
 // Stream-K partial results of the bf16 attention core (part of the caller's workspace): two

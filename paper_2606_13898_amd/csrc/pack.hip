@@ -400,10 +400,11 @@ hipError_t launch_rownorm_fp8(const float *z, const int *cu, const float *mod, i
 // amax, then the codes of x * (448 / amax) and the scale amax / 448 (as k_rownorm's FP8 output).
 template <bool BF16>
 __global__ __launch_bounds__(256) void k_quantize_rows(const void *__restrict__ x, int rows, int cols,
-                                                       uint8_t *__restrict__ codes, float *__restrict__ scale) {
+                                                       uint8_t *__restrict__ codes, float *__restrict__ scale,
+                                                       const int *__restrict__ row_limit) {
   const int lane = threadIdx.x & 63;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (row >= rows) return;
+  if (row >= rows || (row_limit && row >= *row_limit)) return;
   auto ld4 = [&](int c, float *f) {
     if constexpr (BF16) {
       const uint2 u = *reinterpret_cast<const uint2 *>(reinterpret_cast<const uint16_t *>(x) + size_t(row) * cols + c);
@@ -432,13 +433,13 @@ __global__ __launch_bounds__(256) void k_quantize_rows(const void *__restrict__ 
 }
 
 hipError_t launch_quantize_rows(bool bf16, const void *x, int rows, int cols, uint8_t *codes, float *scale,
-                                hipStream_t st) {
+                                hipStream_t st, const int *row_limit) {
   if (rows <= 0) return hipSuccess;
   const int nblk = (rows + 3) / 4;
   if (bf16)
-    hipLaunchKernelGGL(k_quantize_rows<true>, dim3(nblk), dim3(256), 0, st, x, rows, cols, codes, scale);
+    hipLaunchKernelGGL(k_quantize_rows<true>, dim3(nblk), dim3(256), 0, st, x, rows, cols, codes, scale, row_limit);
   else
-    hipLaunchKernelGGL(k_quantize_rows<false>, dim3(nblk), dim3(256), 0, st, x, rows, cols, codes, scale);
+    hipLaunchKernelGGL(k_quantize_rows<false>, dim3(nblk), dim3(256), 0, st, x, rows, cols, codes, scale, row_limit);
   return hipGetLastError();
 }
 

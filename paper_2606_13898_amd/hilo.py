@@ -44,11 +44,11 @@ class hilo_mlp_w(ctypes.Structure):
 
 
 class hilo_attn_w_fp8(ctypes.Structure):
-    _fields_ = [(n, ctypes.c_void_p) for n in ("w_qkv", "s_qkv", "b_qkv", "w_o", "b_o")]
+    _fields_ = [(n, ctypes.c_void_p) for n in ("w_qkv", "s_qkv", "b_qkv", "w_o", "s_o", "b_o")]
 
 
 class hilo_mlp_w_fp8(ctypes.Structure):
-    _fields_ = [(n, ctypes.c_void_p) for n in ("w1", "s1", "b1", "w2", "b2")]
+    _fields_ = [(n, ctypes.c_void_p) for n in ("w1", "s1", "b1", "w2", "s2", "b2")]
 
 
 _lib = None
@@ -79,6 +79,7 @@ _SIG = {
     "hilo_decompress": [ctypes.POINTER(hilo_shape), _P, _P, _P, _P, _P, _P, _P],
     "hilo_attention_core": [ctypes.POINTER(hilo_shape), _P, _P, _P, _P, ctypes.c_size_t, _P],
     "hilo_workspace_bytes": [ctypes.POINTER(hilo_shape)],
+    "hilo_workspace_bytes_fp8": [ctypes.POINTER(hilo_shape)],
     "hilo_max_tokens": [ctypes.POINTER(hilo_shape)],
     "hilo_status_str": [ctypes.c_int32],
     "hilo_abi_version": [],
@@ -88,7 +89,7 @@ _SIG = {
     "hilo_profile_kinds": [],
     "hilo_profile_name": [ctypes.c_int32],
 }
-_RES = {"hilo_workspace_bytes": ctypes.c_size_t, "hilo_max_tokens": ctypes.c_int64,
+_RES = {"hilo_workspace_bytes": ctypes.c_size_t, "hilo_workspace_bytes_fp8": ctypes.c_size_t, "hilo_max_tokens": ctypes.c_int64,
         "hilo_status_str": ctypes.c_char_p, "hilo_profile_name": ctypes.c_char_p}
 
 
@@ -146,6 +147,10 @@ def hilo_abi_version() -> int:
 
 def hilo_max_tokens(shape: hilo_shape) -> int:
     return lib().hilo_max_tokens(ctypes.byref(shape))
+
+
+def hilo_workspace_bytes_fp8(shape: hilo_shape) -> int:
+    return int(lib().hilo_workspace_bytes_fp8(ctypes.byref(shape)))
 
 
 def hilo_workspace_bytes(shape: hilo_shape) -> int:
@@ -236,13 +241,13 @@ def hilo_quantize_rows(x, codes, scale, stream=None):
 
 
 def quantize_fp8_weights(ws: Sequence[dict], stream=None):
-    """Per stream, the FP8 codes and scales of w_qkv and w1 (hilo_quantize_rows) next to the other
-    bf16 tensors: the weight dicts hilo_attention_fp8 / hilo_mlp_fp8 take (keys w_qkv, s_qkv, b_qkv,
-    w_o, b_o, w1, s1, b1, w2, b2)."""
+    """Per stream, the FP8 codes and scales of the four projection weights (hilo_quantize_rows) next
+    to the bf16 biases: the weight dicts hilo_attention_fp8 / hilo_mlp_fp8 take (keys w_qkv, s_qkv,
+    b_qkv, w_o, s_o, b_o, w1, s1, b1, w2, s2, b2)."""
     out = []
     for w in ws:
         d = dict(w)
-        for name, sname in (("w_qkv", "s_qkv"), ("w1", "s1")):
+        for name, sname in (("w_qkv", "s_qkv"), ("w_o", "s_o"), ("w1", "s1"), ("w2", "s2")):
             src = w[name]
             codes = torch.empty(src.shape, dtype=torch.uint8, device=src.device)
             scale = torch.empty(src.shape[0], dtype=torch.float32, device=src.device)
@@ -256,7 +261,7 @@ def attn_weights_fp8(ws: Sequence[dict]):
     arr = (hilo_attn_w_fp8 * 2)()
     for k in range(2):
         arr[k] = hilo_attn_w_fp8(_ptr(ws[k]["w_qkv"]), _ptr(ws[k]["s_qkv"]), _ptr(ws[k]["b_qkv"]),
-                                 _ptr(ws[k]["w_o"]), _ptr(ws[k]["b_o"]))
+                                 _ptr(ws[k]["w_o"]), _ptr(ws[k]["s_o"]), _ptr(ws[k]["b_o"]))
     return arr
 
 
@@ -264,7 +269,7 @@ def mlp_weights_fp8(ws: Sequence[dict]):
     arr = (hilo_mlp_w_fp8 * 2)()
     for k in range(2):
         arr[k] = hilo_mlp_w_fp8(_ptr(ws[k]["w1"]), _ptr(ws[k]["s1"]), _ptr(ws[k]["b1"]),
-                                _ptr(ws[k]["w2"]), _ptr(ws[k]["b2"]))
+                                _ptr(ws[k]["w2"]), _ptr(ws[k]["s2"]), _ptr(ws[k]["b2"]))
     return arr
 
 

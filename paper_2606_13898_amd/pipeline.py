@@ -47,7 +47,9 @@ class DeviceBlock:
         if with_block:
             self.weights = [{k: _dev(v, self.dtype, device) for k, v in w.items()} for w in wl.weights]
             self.mod = _dev(wl.mod, torch.float32, device)
-            self.ws = torch.empty(hilo.hilo_workspace_bytes(self.shape), dtype=torch.uint8, device=device)
+            # sized for the FP8 block too when the shape allows it (it needs the hidden rows' codes)
+            nbytes = max(hilo.hilo_workspace_bytes(self.shape), hilo.hilo_workspace_bytes_fp8(self.shape))
+            self.ws = torch.empty(nbytes, dtype=torch.uint8, device=device)
             self.aw = hilo.attn_weights(self.weights)
             self.mw = hilo.mlp_weights(self.weights)
 

@@ -11,7 +11,14 @@ from paper_2606_13898_amd.pipeline import DeviceBlock
 #  bf16 storage: max-abs 2e-2 and relative L2 5e-3 (the target stated for this block).
 #  f32 storage: max-abs 1e-4 and relative L2 1e-5 -- fp32 products over K <= 4096 terms of O(1)
 #  values carry a rounding error of order sqrt(K) * 2^-24 * |terms| ~ 1e-6 relative.
-TOL = {"bf16": (2e-2, 5e-3), "f32": (1e-4, 1e-5)}
+#  fp8 (the FP8 block against the FP8 oracle): max-abs 6e-2 and relative L2 1e-2.  The block takes
+#  its E4M3 decisions on operands that carry the device's bf16 rounding (q, k, v and the stored
+#  activations); an operand one bf16 ulp (2^-8) away from the oracle's crosses an E4M3 rounding
+#  midpoint with probability ~2^-4 and then moves by one E4M3 step (2^-3 relative), so a few percent
+#  of the codes move and a projection's output deviates by ~sqrt(p) 2^-3 ~ 1-3% of its RMS (measured:
+#  0.5% on hidden size 256, 1-3% on 4608) -- about three times the bf16 path's deviation in z.  The
+#  FP8 kernels themselves are checked exactly on the device's own operands (codes bit for bit).
+TOL = {"bf16": (2e-2, 5e-3), "f32": (1e-4, 1e-5), "fp8": (6e-2, 1e-2)}
 
 
 def float_report(got, want):

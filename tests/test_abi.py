@@ -31,7 +31,7 @@ def test_exports_every_declared_symbol():
 
 
 def test_version_and_status_strings():
-    assert hilo.hilo_abi_version() == 3
+    assert hilo.hilo_abi_version() == 4
     for st in range(7):
         assert hilo.status_str(st)
     assert hilo.status_str(99) == "unknown status"
@@ -204,22 +204,29 @@ def test_fp8_validation():
     L = hilo.lib()
     s = good_shape()
     need = hilo.hilo_workspace_bytes(s)
-    aw = (hilo.hilo_attn_w_fp8 * 2)(*[hilo.hilo_attn_w_fp8(FAKE, FAKE, FAKE, FAKE, FAKE)] * 2)
-    mw = (hilo.hilo_mlp_w_fp8 * 2)(*[hilo.hilo_mlp_w_fp8(FAKE, FAKE, FAKE, FAKE, FAKE)] * 2)
+    aw = (hilo.hilo_attn_w_fp8 * 2)(*[hilo.hilo_attn_w_fp8(*[FAKE] * 6)] * 2)
+    mw = (hilo.hilo_mlp_w_fp8 * 2)(*[hilo.hilo_mlp_w_fp8(*[FAKE] * 6)] * 2)
+    need8 = hilo.hilo_workspace_bytes_fp8(s)
+    assert need8 > need  # the hidden rows' codes and scales come on top
+    T, F = hilo.hilo_max_tokens(s), s.mlp_dim
+    assert need8 == need + -(-T * F // 256) * 256 + -(-T * 4 // 256) * 256
     f = good_shape(hilo.F32)
     assert L.hilo_attention_fp8(ctypes.byref(f), FAKE, FAKE, aw, FAKE, FAKE, 1 << 40, None) == 3
     assert L.hilo_mlp_fp8(ctypes.byref(f), FAKE, FAKE, mw, FAKE, FAKE, 1 << 40, None) == 3
     odd = hilo.hilo_shape(2, 1, 8, 10, 5, 192, 3, 64, 1024, hilo.BF16)  # 192 is not a multiple of 128
     assert L.hilo_attention_fp8(ctypes.byref(odd), FAKE, FAKE, aw, FAKE, FAKE, 1 << 40, None) == 2
     assert L.hilo_mlp_fp8(ctypes.byref(odd), FAKE, FAKE, mw, FAKE, FAKE, 1 << 40, None) == 2
-    bad_aw = (hilo.hilo_attn_w_fp8 * 2)(*[hilo.hilo_attn_w_fp8(FAKE, FAKE, FAKE, FAKE, FAKE)] * 2)
-    bad_aw[1] = hilo.hilo_attn_w_fp8(FAKE, None, FAKE, FAKE, FAKE)  # text stream without scales
-    assert L.hilo_attention_fp8(ctypes.byref(s), FAKE, FAKE, bad_aw, FAKE, FAKE, need, None) == 1
-    bad_mw = (hilo.hilo_mlp_w_fp8 * 2)(*[hilo.hilo_mlp_w_fp8(FAKE, FAKE, FAKE, FAKE, FAKE)] * 2)
-    bad_mw[0] = hilo.hilo_mlp_w_fp8(FAKE, None, FAKE, FAKE, FAKE)
-    assert L.hilo_mlp_fp8(ctypes.byref(s), FAKE, FAKE, bad_mw, FAKE, FAKE, need, None) == 1
+    odd_f = hilo.hilo_shape(2, 1, 8, 10, 5, 256, 2, 128, 1088, hilo.BF16)  # mlp_dim 1088: K of MLP down
+    assert L.hilo_mlp_fp8(ctypes.byref(odd_f), FAKE, FAKE, mw, FAKE, FAKE, 1 << 40, None) == 2
+    assert hilo.hilo_workspace_bytes_fp8(odd_f) == 0
+    bad_aw = (hilo.hilo_attn_w_fp8 * 2)(*[hilo.hilo_attn_w_fp8(*[FAKE] * 6)] * 2)
+    bad_aw[1] = hilo.hilo_attn_w_fp8(FAKE, FAKE, FAKE, FAKE, None, FAKE)  # text stream without W_o scales
+    assert L.hilo_attention_fp8(ctypes.byref(s), FAKE, FAKE, bad_aw, FAKE, FAKE, need8, None) == 1
+    bad_mw = (hilo.hilo_mlp_w_fp8 * 2)(*[hilo.hilo_mlp_w_fp8(*[FAKE] * 6)] * 2)
+    bad_mw[0] = hilo.hilo_mlp_w_fp8(FAKE, None, FAKE, FAKE, FAKE, FAKE)
+    assert L.hilo_mlp_fp8(ctypes.byref(s), FAKE, FAKE, bad_mw, FAKE, FAKE, need8, None) == 1
     assert L.hilo_attention_fp8(ctypes.byref(s), FAKE, FAKE, aw, FAKE, FAKE, 100, None) == 5
-    assert L.hilo_mlp_fp8(ctypes.byref(s), FAKE, FAKE, mw, FAKE, FAKE, need - 1, None) == 5
+    assert L.hilo_mlp_fp8(ctypes.byref(s), FAKE, FAKE, mw, FAKE, FAKE, need8 - 1, None) == 5
     assert L.hilo_attention_fp8(ctypes.byref(s), None, FAKE, aw, FAKE, FAKE, need, None) == 1
     q = L.hilo_quantize_rows
     assert q(2, FAKE, 4, 8, FAKE, FAKE, None) == 3      # dtype
@@ -232,4 +239,4 @@ def test_fp8_validation():
     if not torch.cuda.is_available():
         assert q(hilo.F32, FAKE, 4, 8, FAKE, FAKE, None) == 6
         assert L.hilo_attention_fp8(ctypes.byref(s), FAKE, FAKE, aw, FAKE, FAKE, need, None) == 6
-        assert L.hilo_mlp_fp8(ctypes.byref(s), FAKE, FAKE, mw, FAKE, FAKE, need, None) == 6
+        assert L.hilo_mlp_fp8(ctypes.byref(s), FAKE, FAKE, mw, FAKE, FAKE, need8, None) == 6

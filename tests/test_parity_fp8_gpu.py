@@ -1,4 +1,4 @@
-"""GPU parity of the FP8 projections (QKV and MLP up on per-row E4M3 operands) against the oracle's
+"""GPU parity of the FP8 block (all four projections on per-row E4M3 operands) against the oracle's
 FP8 block, through the C ABI: the row quantiser bit for bit, the normalised rows' codes up to
 float32-versus-float64 rounding of the layer norm, and the block outputs to the bf16 tolerances."""
 import numpy as np
@@ -56,6 +56,50 @@ def _code_order(c):
     return np.where(c & 0x80, -(c & 0x7F), c & 0x7F)
 
 
+def _align(x):
+    return -(-x // 256) * 256
+
+
+def _ws_h(Tmax, D):
+    """Bytes of the workspace's first region: bf16 rows, or FP8 codes plus row scales."""
+    return max(_align(Tmax * D * 2), _align(Tmax * D) + _align(Tmax * 4))
+
+
+def _bf16_rows(ws, off, T, C):
+    return torch.from_numpy(ws[off:off + T * C * 2].copy()).view(torch.bfloat16).float().numpy().reshape(T, C)
+
+
+def _codes_and_scales(ws, off, Tmax, T, C):
+    codes = ws[off:off + T * C].reshape(T, C)
+    soff = off + _align(Tmax * C)
+    return codes, ws[soff:soff + 4 * T].view(np.float32)
+
+
+def _check_projection_exact(db, wl, T, z_in, z_out, x_bf16, codes, scales, wname, bname, gate_idx):
+    """One FP8 projection on the device's own operands: the codes of its bf16 input rows bit for
+    bit, then z_out = z_in + gate (dequant(x) dequant(W)^T + b) to float32-accumulation accuracy."""
+    want_c, want_s = O.quantize_rows(x_bf16.astype(np.float32))
+    np.testing.assert_array_equal(codes, want_c)
+    np.testing.assert_array_equal(scales, want_s)
+    s = wl.shape
+    cu = to_np(db.cu)
+    x = O.dequant_rows(codes, scales)
+    want = np.empty_like(z_in, dtype=np.float64)
+    sname = {"w_o": "s_o", "w2": "s2"}[wname]
+    for (smp, sig, a, b) in O._segments(cu, s.text_len):
+        wc = db.weights8[sig][wname].cpu().numpy()
+        ws = db.weights8[sig][sname].cpu().numpy()
+        bias = db.weights[sig][bname].float().cpu().numpy().astype(np.float64)
+        o = x[a:b] @ O.dequant_rows(wc, ws).T + bias
+        want[a:b] = z_in[a:b] + wl.mod[smp, sig, gate_idx] * o
+    # float32 accumulation (the MFMA's own rounding stays below ~1.3e-4 of each 64-term chunk's sum
+    # of |terms|) against float64: far inside any FP8 effect, and an O(1) error for a wrong code,
+    # scale or column
+    ma, rel = float_report(z_out, want)
+    assert ma <= 5e-3 and rel <= 1e-3, f"{wname} on the device's codes: max_abs {ma:.3g}, rel {rel:.3g}"
+    return ma, rel
+
+
 def _check_h2_codes(db, z1_dev, wl, T):
     """The MLP's FP8 operand rows as the device left them in the workspace (codes [T][D], then the
     row scales at the next 256-byte boundary) against the oracle's quantisation of
@@ -90,7 +134,7 @@ def test_fp8_block_parity(name):
     ref16 = oracle_for(wl)
     db.prepare_fp8()
     for k in range(2):  # weight codes and scales bit for bit
-        for name_w, name_s in (("w_qkv", "s_qkv"), ("w1", "s1")):
+        for name_w, name_s in (("w_qkv", "s_qkv"), ("w_o", "s_o"), ("w1", "s1"), ("w2", "s2")):
             want_c, want_s = O.quantize_rows(np.asarray(wl.weights[k][name_w], dtype=np.float32))
             np.testing.assert_array_equal(db.weights8[k][name_w].cpu().numpy(), want_c)
             np.testing.assert_array_equal(db.weights8[k][name_s].cpu().numpy(), want_s)
@@ -101,14 +145,26 @@ def test_fp8_block_parity(name):
     check_selection(db, ref)
     T = int(ref["cu"][-1])
     Z = ref["Z"][:T]
+    z0 = to_np(db.z)[:T].copy()
     db.attention(fp8=True)
     torch.cuda.synchronize()
     z1 = to_np(db.z)[:T].copy()
-    assert_close(z1, ref["z1"], "bf16", f"{name} z after FP8 attention")
+    assert_close(z1, ref["z1"], "fp8", f"{name} z after FP8 attention")
+    s_ = wl.shape
+    Tmax, D, F = db.T, s_.dim, s_.mlp_dim
+    ws = db.ws.cpu().numpy()
+    hsz = _ws_h(Tmax, D)
+    a_codes, a_scales = _codes_and_scales(ws, hsz, Tmax, T, D)  # in the QKV region, free after attention
+    _check_projection_exact(db, wl, T, z0, z1, _bf16_rows(ws, 0, T, D), a_codes, a_scales, "w_o", "b_o", 2)
     db.mlp(fp8=True)
     torch.cuda.synchronize()
     z2 = to_np(db.z)[:T]
-    assert_close(z2, ref["z2"], "bf16", f"{name} z after FP8 mlp")
+    assert_close(z2, ref["z2"], "fp8", f"{name} z after FP8 mlp")
+    ws = db.ws.cpu().numpy()
+    # the hidden rows' codes and scales are the last two regions of the FP8 workspace
+    hid_off = hilo.hilo_workspace_bytes_fp8(db.shape) - _align(Tmax * F) - _align(Tmax * 4)
+    h_codes, h_scales = _codes_and_scales(ws, hid_off, Tmax, T, F)
+    _check_projection_exact(db, wl, T, z1, z2, _bf16_rows(ws, hsz, T, F), h_codes, h_scales, "w2", "b2", 5)
     frac = _check_h2_codes(db, z1, wl, T)
     # the device follows the FP8 block, not the bf16 one: on each half's update of z the FP8 and
     # bf16 oracles differ by ~3% (relative L2); the device is well inside that
@@ -121,8 +177,8 @@ def test_fp8_block_parity(name):
         assert e8 < 0.4 * gap, f"{tag}: device update is not closer to the FP8 oracle ({e8:.3g} vs {gap:.3g})"
     db.decompress()
     torch.cuda.synchronize()
-    assert_close(to_np(db.y_img), ref["y_img"], "bf16", f"{name} y_img")
-    assert_close(to_np(db.y_txt), ref["y_txt"], "bf16", f"{name} y_txt")
+    assert_close(to_np(db.y_img), ref["y_img"], "fp8", f"{name} y_img")
+    assert_close(to_np(db.y_txt), ref["y_txt"], "fp8", f"{name} y_txt")
     print(f"[parity-fp8] {name}: h2 codes equal {frac:.5f}", flush=True)
 
 
@@ -136,8 +192,9 @@ def test_fp8_block_parity(name):
     inputs.BlockShape(1, 1, 64, 64, 256, 256, 2, 128, 4096, "bf16"),
     # 17 x 24 = 408 MLP-up tiles: two waves of whole tiles
     inputs.BlockShape(1, 1, 64, 64, 256, 256, 2, 128, 6144, "bf16"),
-    # K = 4608 in 36 steps of 128, few tiles: whole tiles; MLP up N = 1088 ends in a 64-column tile
-    inputs.BlockShape(1, 1, 16, 16, 0, 4608, 36, 128, 1088, "bf16"),
+    # K = 4608 in 36 steps of 128, few tiles: whole tiles; MLP up N = 1152 ends in a 128-column tile;
+    # MLP down has K = 1152, 9 steps of 128
+    inputs.BlockShape(1, 1, 16, 16, 0, 4608, 36, 128, 1152, "bf16"),
 ], ids=["sk_tail", "whole_waves", "long_k"])
 def test_fp8_gemm_schedules(shp):
     print(f"[parity-fp8] 256-tile FP8 schedules shape={shp}", flush=True)
@@ -148,8 +205,8 @@ def test_fp8_gemm_schedules(shp):
     torch.cuda.synchronize()
     check_selection(db, ref)
     T = int(ref["cu"][-1])
-    assert_close(to_np(db.z)[:T], ref["z2"], "bf16", "z after FP8 block")
-    assert_close(to_np(db.y_img), ref["y_img"], "bf16", "y_img")
+    assert_close(to_np(db.z)[:T], ref["z2"], "fp8", "z after FP8 block")
+    assert_close(to_np(db.y_img), ref["y_img"], "fp8", "y_img")
 
 
 def test_fp8_full_size_sampled():
@@ -169,5 +226,5 @@ def test_fp8_full_size_sampled():
     q8 = O.quantize_fp8_weights(wl.weights)
     _, z2 = O.block(front["Z"], front["cu"], s.text_len, s.heads, wl.weights, wl.mod, rows, q8)
     got = to_np(db.z)[rows]
-    ma, rel = assert_close(got, z2, "bf16", "m1024 FP8 z at sampled rows")
+    ma, rel = assert_close(got, z2, "fp8", "m1024 FP8 z at sampled rows")
     print(f"[parity-fp8] m1024: {rows.size} rows, max_abs {ma:.3g}, rel_l2 {rel:.3g}", flush=True)
