@@ -432,9 +432,63 @@ __global__ __launch_bounds__(256) void k_quantize_rows(const void *__restrict__ 
   }
 }
 
+// The same quantisation for bf16 rows of up to 16384 columns in one pass over HBM: one workgroup
+// per row, the row held in registers (NC chunks of 4 columns per thread, packed bf16), the amax
+// reduced over the workgroup.
+template <int NC>
+__global__ __launch_bounds__(256) void k_quantize_rows_wg(const uint16_t *__restrict__ x, int cols,
+                                                          uint8_t *__restrict__ codes, float *__restrict__ scale,
+                                                          const int *__restrict__ row_limit) {
+  __shared__ float red[4];
+  const int row = blockIdx.x, tid = threadIdx.x;
+  if (row_limit && row >= *row_limit) return;
+  const uint16_t *xr = x + size_t(row) * cols;
+  uint2 v[NC];
+  float amax = 0.f;
+#pragma unroll
+  for (int k = 0; k < NC; ++k) {
+    const int c = (k * 256 + tid) * 4;
+    v[k] = c < cols ? *reinterpret_cast<const uint2 *>(xr + c) : make_uint2(0u, 0u);
+    amax = fmaxf(amax, fmaxf(fmaxf(fabsf(__uint_as_float(v[k].x << 16)), fabsf(__uint_as_float(v[k].x & 0xffff0000u))),
+                             fmaxf(fabsf(__uint_as_float(v[k].y << 16)), fabsf(__uint_as_float(v[k].y & 0xffff0000u)))));
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) amax = fmaxf(amax, __shfl_xor(amax, off, 64));
+  if ((tid & 63) == 0) red[tid >> 6] = amax;
+  __syncthreads();
+  amax = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  const float inv = amax > 0.f ? __fdiv_rn(448.0f, amax) : 0.f;
+  if (tid == 0) scale[row] = __fdiv_rn(amax, 448.0f);
+  uint8_t *o = codes + size_t(row) * cols;
+#pragma unroll
+  for (int k = 0; k < NC; ++k) {
+    const int c = (k * 256 + tid) * 4;
+    if (c < cols)
+      *reinterpret_cast<uint32_t *>(o + c) =
+          fp8x4(__uint_as_float(v[k].x << 16) * inv, __uint_as_float(v[k].x & 0xffff0000u) * inv,
+                __uint_as_float(v[k].y << 16) * inv, __uint_as_float(v[k].y & 0xffff0000u) * inv);
+  }
+}
+
 hipError_t launch_quantize_rows(bool bf16, const void *x, int rows, int cols, uint8_t *codes, float *scale,
                                 hipStream_t st, const int *row_limit) {
   if (rows <= 0) return hipSuccess;
+  if (bf16 && cols <= 16384) {
+    const uint16_t *xb = reinterpret_cast<const uint16_t *>(x);
+    const int nc = (cols + 1023) / 1024;
+#define HILO_QWG(NCV) \
+  hipLaunchKernelGGL(k_quantize_rows_wg<NCV>, dim3(rows), dim3(256), 0, st, xb, cols, codes, scale, row_limit)
+    if (nc <= 1) HILO_QWG(1);
+    else if (nc <= 2) HILO_QWG(2);
+    else if (nc <= 3) HILO_QWG(3);
+    else if (nc <= 4) HILO_QWG(4);
+    else if (nc <= 6) HILO_QWG(6);
+    else if (nc <= 8) HILO_QWG(8);
+    else if (nc <= 12) HILO_QWG(12);
+    else HILO_QWG(16);
+#undef HILO_QWG
+    return hipGetLastError();
+  }
   const int nblk = (rows + 3) / 4;
   if (bf16)
     hipLaunchKernelGGL(k_quantize_rows<true>, dim3(nblk), dim3(256), 0, st, x, rows, cols, codes, scale, row_limit);
