@@ -24,7 +24,8 @@ sys.path.insert(0, ROOT)
 from bench import source_digest  # noqa: E402
 
 COPY_MIB = 256
-BENCH = "python3 {root}/bench.py --steps 2 --warmup 1 --no-dense --no-cpu-baseline"
+BENCH = ("python3 {root}/bench.py --steps 2 --warmup 1 --no-dense --no-cpu-baseline --no-fp8 --no-stack "
+         "--no-token-sets --no-pixel-score")
 COPY = "python3 {root}/bench.py --copy-mib %d" % COPY_MIB
 COUNTERS = ("FETCH_SIZE", "WRITE_SIZE")
 
@@ -61,12 +62,18 @@ def load(out, cnt, tag):
     return [(d, n, v) for d, (n, v) in sorted(per.items())]
 
 
+def gemm_role(base):
+    """Projection of a GEMM kernel from its template arguments: k_gemm_sk<BM, BN, WM, WN, EPI, ROLE>,
+    k_gemm_fix<BM, BN, WM, WN, EPI, ROLE, F8>, k_gemm_big<TB, EPI, ROLE, F8>."""
+    args = [a.strip() for a in base[base.index("<") + 1:base.rindex(">")].split(",")]
+    return ROLES[args[2] if base.startswith("hilo::k_gemm_big") else args[5]]
+
+
 def kind_of(name, state):
     """Bench kernel kind of a dispatch; rownorm launches alternate attention / MLP per step."""
     base = name.split("(")[0].replace("void ", "").strip()
     if "k_gemm_sk<" in base or "k_gemm_fix<" in base or "k_gemm_big<" in base:
-        role = base.rsplit(",", 1)[1].strip(" >")
-        return ROLES[role]
+        return gemm_role(base)
     if "k_attn" in base:
         return "attention_core"
     if "k_rownorm" in base:
