@@ -17,6 +17,9 @@ BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libhilo.so")
 SOURCES = ["select.hip", "pack.hip", "gemm.hip", "attention.hip", "abi.hip"]
 ARCH = "gfx950"
+# Per-source flags.  attention.hip: its maxima see only finite scores and -inf masks, and without
+# NaN semantics fmaxf needs no quieting of each MFMA result before the comparison
+FILE_FLAGS = {"attention.hip": ["-fno-honor-nans"]}
 
 
 def hipcc() -> str:
@@ -39,7 +42,7 @@ def common_flags():
 
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-    cmd = [hipcc(), *common_flags(), "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [hipcc(), *common_flags(), *FILE_FLAGS.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError(f"compiling {src} failed:\n{' '.join(cmd)}\n{res.stdout}\n{res.stderr}")

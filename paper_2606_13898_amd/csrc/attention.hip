@@ -4,34 +4,32 @@
 // bf16 path (gfx950 MFMA v_mfma_f32_16x16x32_bf16, fp32 online softmax in base 2):
 //   workgroup = NW waves x QW query rows of one (sample, head); K/V stream through LDS in tiles of
 //   64 keys, double buffered.  Each wave computes S^T = K Q^T so that every lane owns one query
-//   row's scores (4 keys per 16-key subtile): the running max / sum stay lane-local, and the
+//   row's scores (4 keys per 16-key subtile): the running max stays lane-local, and the
 //   probabilities are already in the register layout of the second MFMA operand for
 //   O^T = V^T P^T.  The MFMA's k index may be permuted as long as both operands agree: the lane
 //   holding keys {4g..4g+3} and {16+4g..16+4g+3} of a 32-key step feeds exactly those keys of V^T.
 //   K and V both land in LDS in their natural [key][dim] layout by direct global->LDS loads; the
 //   V^T fragments come out of gfx950's transposing LDS read (ds_read_b64_tr_b16), two per
-//   fragment.  Only the last key tile carries the sequence-end mask; the output is rescaled only
-//   in steps where some row's running maximum grew.
+//   fragment.  Fragments are read ahead of their MFMAs (K one key subtile, V two output subtiles)
+//   through inline asm with explicit waits, and the next tile's transfer starts at the top of a
+//   step.  Only the last key tile carries the sequence-end mask.  The row sums of P come from one
+//   more MFMA against a fragment of ones, and the reference maximum of the online softmax moves
+//   (rescaling O and l) only when a row maximum exceeds it by more than 2^8.
 #include "common.h"
 #include "kernels.h"
 
 namespace hilo {
 
 constexpr float kLog2e = 1.4426950408889634f;
+// online softmax: the reference maximum lags the true one by at most this much (base 2)
+constexpr float kLazyRescale = 8.0f;
 
-// max / sum with the lanes 16 and 32 apart (the 4 lanes holding the same query row)
+// max with the lanes 16 and 32 apart (the 4 lanes holding the same query row)
 HILO_DEV float xmax16_32(float x) {
   auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
   x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
   auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
   return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
-}
-
-HILO_DEV float xsum16_32(float x) {
-  auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  x = __uint_as_float(a[0]) + __uint_as_float(a[1]);
-  auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 
 // K tile rows (head_dim bf16) are stored with 16-byte chunk c of row r at slot c ^ kswz(r), so
@@ -55,10 +53,42 @@ HILO_DEV int vsw(int r) {
 
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 
+// MFMA fragments leave LDS through inline asm with explicit waits.  The compiler then sees no LDS
+// load that might alias the global->LDS transfer in flight into the other buffer; for one it can
+// see, it waits for that whole transfer before the first fragment read of the step.
+HILO_DEV void lds_read_b128(bf16x8 &dst, uint32_t addr) {
+  asm volatile("ds_read_b128 %0, %1" : "=v"(dst) : "v"(addr) : "memory");
+}
 // Transposing LDS read: within each group of 16 lanes, lane i receives element i % 4 of the
 // 8-byte words read by lanes 4m + i / 4 (m = 0..3) of its group.
-HILO_DEV bf16x4 lds_read_tr16(const uint16_t *lds) {
-  return __builtin_amdgcn_ds_read_tr16_b64_v4bf16((__attribute__((address_space(3))) bf16x4 *)lds);
+template <int OFF>
+HILO_DEV void lds_read_tr16(bf16x4 &dst, uint32_t addr) {
+  asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(dst) : "v"(addr), "n"(OFF) : "memory");
+}
+// Waits until at most N LDS reads of this wave are outstanding (they complete in order) and makes
+// x depend on the wait, so that no use of x is scheduled above it; lds_tie orders further values.
+template <int N, typename T>
+HILO_DEV void lds_wait(T &x) {
+  asm volatile("s_waitcnt lgkmcnt(%1)" : "+v"(x) : "n"(N) : "memory");
+}
+// the same with n a constant once the caller's loops are unrolled (larger n wait for all reads)
+template <typename T>
+HILO_DEV void lds_wait_n(int n, T &x) {
+  switch (n) {
+    case 8: lds_wait<8>(x); break;
+    case 7: lds_wait<7>(x); break;
+    case 6: lds_wait<6>(x); break;
+    case 5: lds_wait<5>(x); break;
+    case 4: lds_wait<4>(x); break;
+    case 3: lds_wait<3>(x); break;
+    case 2: lds_wait<2>(x); break;
+    case 1: lds_wait<1>(x); break;
+    default: lds_wait<0>(x); break;
+  }
+}
+template <typename T>
+HILO_DEV void lds_tie(T &x) {
+  asm volatile("" : "+v"(x));
 }
 
 HILO_DEV void g2lds16(const void *g, void *lds_wave_base) {
@@ -197,25 +227,49 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a) {
         qf[qs][kk] = *reinterpret_cast<const bf16x8 *>(Q + size_t(q) * ld + kk * 32 + 8 * lg);
     }
 
-    // K: direct global->LDS, lane -> (row wid*KI*RPI + RPI*i + lane/CPR, slot lane%CPR)
-    auto issue_k = [&](int kv0, int buf) {
+    // K and V: direct global->LDS, lane -> (row wid*KI*RPI + RPI*i + lane/CPR, slot lane%CPR),
+    // V's chunks placed by vsw; rows past the sequence end re-read its last row
+    auto issue_kv = [&](int kv0, int buf) {
 #pragma unroll
       for (int i = 0; i < KI; ++i) {
         const int r = (wid * KI + i) * RPI + krow;
-        const int row = min(kv0 + r, n - 1);
-        g2lds16(Kp + size_t(row) * ld + ((kslot ^ kswz<HD>(r)) * 8),
-                &sK[buf][(wid * KI + i) * RPI * HD]);
+        const size_t row = size_t(min(kv0 + r, n - 1)) * ld;
+        g2lds16(Kp + row + ((kslot ^ kswz<HD>(r)) * 8), &sK[buf][(wid * KI + i) * RPI * HD]);
+        g2lds16(Vp + row + ((kslot ^ vsw<HD>(r)) * 8), &sV[buf][(wid * KI + i) * RPI * HD]);
       }
     };
-    // V: direct global->LDS in the same pattern, chunks placed by vsw
-    auto issue_v = [&](int kv0, int buf) {
+    // LDS byte addresses of this lane's fragments in buffer 0 (buffer 1 is kTileBytes further).
+    // K (first MFMA operand) of key subtile ks, k-step kk: row ks*16 + lr, chunk kk*4 + lg; the
+    // swizzle depends on lr only, so ks is an immediate offset
+    constexpr uint32_t kTileBytes = BKV * HD * 2;
+    const uint32_t sK0 = (uint32_t)(uintptr_t)&sK[0][0], sV0 = (uint32_t)(uintptr_t)&sV[0][0];
+    uint32_t kaddr[KK];
 #pragma unroll
-      for (int i = 0; i < KI; ++i) {
-        const int r = (wid * KI + i) * RPI + krow;
-        const int row = min(kv0 + r, n - 1);
-        g2lds16(Vp + size_t(row) * ld + ((kslot ^ vsw<HD>(r)) * 8),
-                &sV[buf][(wid * KI + i) * RPI * HD]);
+    for (int kk = 0; kk < KK; ++kk) kaddr[kk] = sK0 + (lr * HD + (((kk * 4 + lg) ^ kswz<HD>(lr)) * 8)) * 2;
+    // V^T of output subtile d: lane (g = lg, s = lr) reads dims d*16 + 4 (s % 4) .. +3 of key rows
+    // 32 kk2 + 4 g + s / 4 and 16 rows further (the transpose gives lane s dim d*16 + s of those 8
+    // keys); the swizzle of those rows depends on lane bits only, so kk2 and the +16 rows are
+    // immediate offsets
+    uint32_t vaddr[DS];
+    {
+      const int r1 = 4 * lg + (lr >> 2);
+#pragma unroll
+      for (int d = 0; d < DS; ++d) {
+        const int c = 2 * d + ((lr & 3) >> 1);
+        vaddr[d] = sV0 + (r1 * HD + ((c ^ vsw<HD>(r1)) << 3) + (lr & 1) * 4) * 2;
       }
+    }
+    auto read_k = [&](uint32_t boff, int ks, bf16x8 (&kf)[KK]) {
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) lds_read_b128(kf[kk], kaddr[kk] + boff + uint32_t(ks * 16 * HD * 2));
+    };
+    // two 8-byte halves per k-step: [kk2][0] rows r1, [kk2][1] rows r1 + 16
+    auto read_v = [&](uint32_t boff, int d, bf16x4 (&vh)[2][2]) {
+      const uint32_t ad = vaddr[d] + boff;
+      lds_read_tr16<0>(vh[0][0], ad);
+      lds_read_tr16<16 * HD * 2>(vh[0][1], ad);
+      lds_read_tr16<32 * HD * 2>(vh[1][0], ad);
+      lds_read_tr16<48 * HD * 2>(vh[1][1], ad);
     };
 
     f32x4 o[QS][DS];
@@ -223,32 +277,46 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a) {
     for (int qs = 0; qs < QS; ++qs)
 #pragma unroll
       for (int d = 0; d < DS; ++d) o[qs][d] = f32x4{0.f, 0.f, 0.f, 0.f};
-    float mrun[QS], lrun[QS];  // running max (scaled, base 2) and this lane's partial sum
+    // running reference maximum (scaled, base 2) and the row sums of P, accumulated by the MFMA
+    // against a fragment of ones (every lane gets its query's full sum over the 32 keys of a
+    // k-step, of the same bf16-rounded probabilities that weight V)
+    float mrun[QS];
+    f32x4 lacc[QS];
 #pragma unroll
-    for (int qs = 0; qs < QS; ++qs) { mrun[qs] = -INFINITY; lrun[qs] = 0.f; }
+    for (int qs = 0; qs < QS; ++qs) { mrun[qs] = -INFINITY; lacc[qs] = f32x4{0.f, 0.f, 0.f, 0.f}; }
+    bf16x8 ones;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) ones[e] = static_cast<__bf16>(1.0f);
 
-    // one 64-key step; keys >= n exist only in a unit's last step, the only one that masks
-    auto step = [&](int buf, int kv0, bool mask, auto &&after_scores) {
-      // S^T for 64 keys x QW queries: sc[ks][qs][e] = score(query qs*16+lr, key ks*16+4*lg+e)
+    // one 64-key step; keys >= n exist only in a unit's last step, the only one that masks.  The
+    // next tile's transfer (into the buffer every wave left at the last barrier) starts first.
+    auto step = [&](int buf, int kv0, bool mask, auto &&prefetch) {
+      prefetch();
+      const uint32_t boff = buf ? kTileBytes : 0u;
+      // S^T for 64 keys x QW queries: sc[ks][qs][e] = score(query qs*16+lr, key ks*16+4*lg+e);
+      // K fragments are read one key subtile ahead of the MFMAs that use them
       f32x4 sc[4][QS];
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
         for (int qs = 0; qs < QS; ++qs) sc[ks][qs] = f32x4{0.f, 0.f, 0.f, 0.f};
+      bf16x8 kf[2][KK];
+      read_k(boff, 0, kf[0]);
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) {
-        const int r = ks * 16 + lr;
+        if (ks + 1 < 4) read_k(boff, ks + 1, kf[(ks + 1) & 1]);
 #pragma unroll
         for (int kk = 0; kk < KK; ++kk) {
-          const int ch = kk * 4 + lg;
-          const bf16x8 kf =
-              *reinterpret_cast<const bf16x8 *>(&sK[buf][r * HD + ((ch ^ kswz<HD>(r)) * 8)]);
+          lds_wait_n((KK - 1 - kk) + (ks + 1 < 4 ? KK : 0), kf[ks & 1][kk]);
 #pragma unroll
           for (int qs = 0; qs < QS; ++qs)
-            sc[ks][qs] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[qs][kk], sc[ks][qs], 0, 0, 0);
+            sc[ks][qs] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[ks & 1][kk], qf[qs][kk], sc[ks][qs], 0, 0, 0);
         }
       }
-      after_scores();
+      // the first two V^T subtiles load while the softmax runs, later ones two subtiles ahead
+      bf16x4 vh[3][2][2];
+      read_v(boff, 0, vh[0]);
+      read_v(boff, 1, vh[1]);
       if (mask) {
 #pragma unroll
         for (int ks = 0; ks < 4; ++ks)
@@ -261,50 +329,46 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a) {
       bf16x8 pf[QS][2];
 #pragma unroll
       for (int qs = 0; qs < QS; ++qs) {
-        float mx = sc[0][qs][0];
+        float m4[4];
 #pragma unroll
         for (int ks = 0; ks < 4; ++ks)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) mx = fmaxf(mx, sc[ks][qs][e]);
-        const float mnew = fmaxf(mrun[qs], xmax16_32(mx) * a.scale_log2);
-        if (__any(mnew > mrun[qs])) {  // rescale only when some row's maximum grew
+          m4[ks] = fmaxf(fmaxf(sc[ks][qs][0], sc[ks][qs][1]), fmaxf(sc[ks][qs][2], sc[ks][qs][3]));
+        const float mt = xmax16_32(fmaxf(fmaxf(m4[0], m4[1]), fmaxf(m4[2], m4[3]))) * a.scale_log2;
+        // The reference maximum moves only when some row's tile maximum exceeds it by more than
+        // kLazyRescale: O and l share it, so the result does not depend on it, and the
+        // probabilities stay below 2^kLazyRescale
+        if (__any(mt > mrun[qs] + kLazyRescale)) {
+          const float mnew = fmaxf(mrun[qs], mt);
           const float alpha = __builtin_amdgcn_exp2f(mrun[qs] - mnew);
-          lrun[qs] *= alpha;
+          lacc[qs] *= alpha;
 #pragma unroll
           for (int d = 0; d < DS; ++d) o[qs][d] *= alpha;
           mrun[qs] = mnew;
         }
-        float psum = 0.f;
-        float pv[4][4];
-#pragma unroll
-        for (int ks = 0; ks < 4; ++ks)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            pv[ks][e] = __builtin_amdgcn_exp2f(fmaf(sc[ks][qs][e], a.scale_log2, -mnew));
-            psum += pv[ks][e];
-          }
-        lrun[qs] += psum;
 #pragma unroll
         for (int kk2 = 0; kk2 < 2; ++kk2) {
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            pf[qs][kk2][e] = static_cast<__bf16>(pv[2 * kk2][e]);
-            pf[qs][kk2][4 + e] = static_cast<__bf16>(pv[2 * kk2 + 1][e]);
+            pf[qs][kk2][e] =
+                static_cast<__bf16>(__builtin_amdgcn_exp2f(fmaf(sc[2 * kk2][qs][e], a.scale_log2, -mrun[qs])));
+            pf[qs][kk2][4 + e] =
+                static_cast<__bf16>(__builtin_amdgcn_exp2f(fmaf(sc[2 * kk2 + 1][qs][e], a.scale_log2, -mrun[qs])));
           }
+          lacc[qs] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf[qs][kk2], lacc[qs], 0, 0, 0);
         }
       }
       // O^T += V^T P^T
 #pragma unroll
       for (int d = 0; d < DS; ++d) {
+        if (d + 2 < DS) read_v(boff, d + 2, vh[(d + 2) % 3]);
+        bf16x4 (&h)[2][2] = vh[d % 3];
+        lds_wait_n(4 * (d + 2 < DS ? 2 : DS - 1 - d), h[1][1]);
+        lds_tie(h[0][0]);
+        lds_tie(h[0][1]);
+        lds_tie(h[1][0]);
 #pragma unroll
         for (int kk2 = 0; kk2 < 2; ++kk2) {
-          // lane (g = lg, s = lr) reads dims d*16 + 4 (s % 4) .. +3 of key rows 32 kk2 + 4 g + s / 4
-          // and 16 rows further; the transpose gives lane s dim d*16 + s of those 8 keys
-          const int c = 2 * d + ((lr & 3) >> 1), half = (lr & 1) * 4;
-          const int r1 = 32 * kk2 + 4 * lg + (lr >> 2), r2 = r1 + 16;
-          const bf16x4 v1 = lds_read_tr16(&sV[buf][r1 * HD + ((c ^ vsw<HD>(r1)) << 3) + half]);
-          const bf16x4 v2 = lds_read_tr16(&sV[buf][r2 * HD + ((c ^ vsw<HD>(r2)) << 3) + half]);
-          const bf16x8 vf = __builtin_shufflevector(v1, v2, 0, 1, 2, 3, 4, 5, 6, 7);
+          const bf16x8 vf = __builtin_shufflevector(h[kk2][0], h[kk2][1], 0, 1, 2, 3, 4, 5, 6, 7);
 #pragma unroll
           for (int qs = 0; qs < QS; ++qs)
             o[qs][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[qs][kk2], o[qs][d], 0, 0, 0);
@@ -312,19 +376,15 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a) {
       }
     };
 
-    issue_k(kb * BKV, 0);
-    issue_v(kb * BKV, 0);
+    issue_kv(kb * BKV, 0);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
-    // all steps but the last load the next tile unconditionally (issued once this step's K
-    // fragments are read) and never mask: no branch splits the loop body's schedule
+    // all steps but the last load the next tile unconditionally and never mask: no branch splits
+    // the loop body's schedule
     for (int kt = kb; kt < ke - 1; ++kt) {
       const int buf = (kt - kb) & 1;
       const int kv0 = kt * BKV;
-      step(buf, kv0, false, [&]() {
-        issue_k(kv0 + BKV, buf ^ 1);
-        issue_v(kv0 + BKV, buf ^ 1);
-      });
+      step(buf, kv0, false, [&]() { issue_kv(kv0 + BKV, buf ^ 1); });
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
       __syncthreads();
     }
@@ -333,7 +393,7 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a) {
 
     float lsum[QS];
 #pragma unroll
-    for (int qs = 0; qs < QS; ++qs) lsum[qs] = xsum16_32(lrun[qs]);
+    for (int qs = 0; qs < QS; ++qs) lsum[qs] = lacc[qs][0];
     if (kb == 0 && ke == u.nkv) {
       attn_store_out<HD, QW, NW>(a, u, wid, lane, o, lsum);
     } else {
