@@ -56,8 +56,9 @@ typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 // MFMA fragments leave LDS through inline asm with explicit waits.  The compiler then sees no LDS
 // load that might alias the global->LDS transfer in flight into the other buffer; for one it can
 // see, it waits for that whole transfer before the first fragment read of the step.
+template <int OFF>
 HILO_DEV void lds_read_b128(bf16x8 &dst, uint32_t addr) {
-  asm volatile("ds_read_b128 %0, %1" : "=v"(dst) : "v"(addr) : "memory");
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(dst) : "v"(addr), "n"(OFF) : "memory");
 }
 // Transposing LDS read: within each group of 16 lanes, lane i receives element i % 4 of the
 // 8-byte words read by lanes 4m + i / 4 (m = 0..3) of its group.
@@ -202,7 +203,7 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a) {
   const long long head_start = attn_unit(a.cu, a.B, a.heads, BQ, beg).start;
   const int D = a.heads * HD;
   const size_t ld = size_t(3) * D;
-  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wid = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lr = lane & 15, lg = lane >> 4;
   const int krow = lane / CPR, kslot = lane % CPR;
 
@@ -228,14 +229,35 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a) {
     }
 
     // K and V: direct global->LDS, lane -> (row wid*KI*RPI + RPI*i + lane/CPR, slot lane%CPR),
-    // V's chunks placed by vsw; rows past the sequence end re-read its last row
-    auto issue_kv = [&](int kv0, int buf) {
+    // V's chunks placed by vsw.  A tile's address is a uniform base (key row kv0, in scalar
+    // registers) plus this lane's fixed 32-bit byte offset, so the loads of a step need no vector
+    // address arithmetic; only a tile reaching past the sequence end (a unit's last, at most once)
+    // re-forms the offsets with the rows clamped to the last one.
+    const uint32_t ldb = uint32_t(ld) * 2;  // bytes per token row
+    uint32_t koff[KI], voff[KI];
 #pragma unroll
-      for (int i = 0; i < KI; ++i) {
-        const int r = (wid * KI + i) * RPI + krow;
-        const size_t row = size_t(min(kv0 + r, n - 1)) * ld;
-        g2lds16(Kp + row + ((kslot ^ kswz<HD>(r)) * 8), &sK[buf][(wid * KI + i) * RPI * HD]);
-        g2lds16(Vp + row + ((kslot ^ vsw<HD>(r)) * 8), &sV[buf][(wid * KI + i) * RPI * HD]);
+    for (int i = 0; i < KI; ++i) {
+      const int r = (wid * KI + i) * RPI + krow;
+      koff[i] = uint32_t(r) * ldb + uint32_t((kslot ^ kswz<HD>(r)) * 16);
+      voff[i] = uint32_t(r) * ldb + uint32_t((kslot ^ vsw<HD>(r)) * 16);
+    }
+    auto issue_kv = [&](int kv0, int buf) {
+      const char *kb = reinterpret_cast<const char *>(Kp) + size_t(kv0) * ldb;
+      const char *vb = reinterpret_cast<const char *>(Vp) + size_t(kv0) * ldb;
+      if (kv0 + BKV <= n) {
+#pragma unroll
+        for (int i = 0; i < KI; ++i) {
+          g2lds16(kb + koff[i], &sK[buf][(wid * KI + i) * RPI * HD]);
+          g2lds16(vb + voff[i], &sV[buf][(wid * KI + i) * RPI * HD]);
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < KI; ++i) {
+          const int r = (wid * KI + i) * RPI + krow;
+          const uint32_t back = uint32_t(r - (min(kv0 + r, n - 1) - kv0)) * ldb;  // rows re-read
+          g2lds16(kb + (koff[i] - back), &sK[buf][(wid * KI + i) * RPI * HD]);
+          g2lds16(vb + (voff[i] - back), &sV[buf][(wid * KI + i) * RPI * HD]);
+        }
       }
     };
     // LDS byte addresses of this lane's fragments in buffer 0 (buffer 1 is kTileBytes further).
@@ -259,9 +281,17 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a) {
         vaddr[d] = sV0 + (r1 * HD + ((c ^ vsw<HD>(r1)) << 3) + (lr & 1) * 4) * 2;
       }
     }
-    auto read_k = [&](uint32_t boff, int ks, bf16x8 (&kf)[KK]) {
+    // (the key subtile is the instruction's immediate offset)
+    auto read_k = [&](const uint32_t (&kb)[KK], int ks, bf16x8 (&kf)[KK]) {
 #pragma unroll
-      for (int kk = 0; kk < KK; ++kk) lds_read_b128(kf[kk], kaddr[kk] + boff + uint32_t(ks * 16 * HD * 2));
+      for (int kk = 0; kk < KK; ++kk) {
+        switch (ks) {
+          case 0: lds_read_b128<0>(kf[kk], kb[kk]); break;
+          case 1: lds_read_b128<16 * HD * 2>(kf[kk], kb[kk]); break;
+          case 2: lds_read_b128<32 * HD * 2>(kf[kk], kb[kk]); break;
+          default: lds_read_b128<48 * HD * 2>(kf[kk], kb[kk]); break;
+        }
+      }
     };
     // two 8-byte halves per k-step: [kk2][0] rows r1, [kk2][1] rows r1 + 16
     auto read_v = [&](uint32_t boff, int d, bf16x4 (&vh)[2][2]) {
@@ -293,6 +323,9 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a) {
     auto step = [&](int buf, int kv0, bool mask, auto &&prefetch) {
       prefetch();
       const uint32_t boff = buf ? kTileBytes : 0u;
+      uint32_t kb[KK];
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) kb[kk] = kaddr[kk] + boff;
       // S^T for 64 keys x QW queries: sc[ks][qs][e] = score(query qs*16+lr, key ks*16+4*lg+e);
       // K fragments are read one key subtile ahead of the MFMAs that use them
       f32x4 sc[4][QS];
@@ -301,10 +334,10 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a) {
 #pragma unroll
         for (int qs = 0; qs < QS; ++qs) sc[ks][qs] = f32x4{0.f, 0.f, 0.f, 0.f};
       bf16x8 kf[2][KK];
-      read_k(boff, 0, kf[0]);
+      read_k(kb, 0, kf[0]);
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) {
-        if (ks + 1 < 4) read_k(boff, ks + 1, kf[(ks + 1) & 1]);
+        if (ks + 1 < 4) read_k(kb, ks + 1, kf[(ks + 1) & 1]);
 #pragma unroll
         for (int kk = 0; kk < KK; ++kk) {
           lds_wait_n((KK - 1 - kk) + (ks + 1 < 4 ? KK : 0), kf[ks & 1][kk]);
@@ -383,8 +416,7 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a) {
     // the loop body's schedule
     for (int kt = kb; kt < ke - 1; ++kt) {
       const int buf = (kt - kb) & 1;
-      const int kv0 = kt * BKV;
-      step(buf, kv0, false, [&]() { issue_kv(kv0 + BKV, buf ^ 1); });
+      step(buf, kt * BKV, false, [&]() { issue_kv((kt + 1) * BKV, buf ^ 1); });
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
       __syncthreads();
     }
