@@ -444,7 +444,7 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a) {
 
 // Merges every unit cut by range boundaries; run by the range holding the unit's first key step.
 template <int HD, int QW, int NW>
-__global__ __launch_bounds__(NW * 64) void k_attn_fix(AttnArgs a) {
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2))) void k_attn_fix(AttnArgs a) {
   using S = AttnShape<HD, QW, NW>;
   constexpr int QS = S::QS, DS = S::DS, BQ = S::BQ;
   const int P = gridDim.x;
@@ -467,7 +467,33 @@ __global__ __launch_bounds__(NW * 64) void k_attn_fix(AttnArgs a) {
 #pragma unroll
     for (int d = 0; d < DS; ++d) o[qs][d] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
-  // contributor ranges [b, e) in order; their starts floor(I q / P) advance by additions
+  // one contributor's partial: (m, l) per query subtile and the unnormalised O
+  struct Part {
+    float2 ml[QS];
+    f32x4 o[QS][DS];
+  };
+  auto load = [&](const float *slot, Part &c) __attribute__((always_inline)) {
+#pragma unroll
+    for (int qs = 0; qs < QS; ++qs) {
+      c.ml[qs] = *reinterpret_cast<const float2 *>(slot + S::ml_index(wid, qs, lane));
+#pragma unroll
+      for (int d = 0; d < DS; ++d) c.o[qs][d] = *reinterpret_cast<const f32x4 *>(slot + S::o_index(wid, qs, d, lane));
+    }
+  };
+  auto merge = [&](const Part &c) __attribute__((always_inline)) {
+#pragma unroll
+    for (int qs = 0; qs < QS; ++qs) {
+      const float mn = fmaxf(m[qs], c.ml[qs].x);
+      const float ca = __builtin_amdgcn_exp2f(m[qs] - mn), cb = __builtin_amdgcn_exp2f(c.ml[qs].x - mn);
+      l[qs] = l[qs] * ca + c.ml[qs].y * cb;
+#pragma unroll
+      for (int d = 0; d < DS; ++d) o[qs][d] = o[qs][d] * ca + c.o[qs][d] * cb;
+      m[qs] = mn;
+    }
+  };
+  // contributor ranges [b, e) in order; their starts floor(I q / P) advance by additions.  They are
+  // merged in that order, two at a time: both partials' loads are in flight together
+  const float *pend = nullptr;
   const long long qI = I / P, rI = I - qI * P;
   long long b = beg, r = I * pid - beg * P;
   for (int q = pid; q < P; ++q) {
@@ -483,18 +509,22 @@ __global__ __launch_bounds__(NW * 64) void k_attn_fix(AttnArgs a) {
     if (bq >= ue) break;
     // slot 0 holds the partial of the range's first unit, slot 1 of its last
     const float *slot = a.part + (size_t(q) * 2 + (bq >= u.start ? 0 : 1)) * S::kSlotFloats;
-#pragma unroll
-    for (int qs = 0; qs < QS; ++qs) {
-      const float2 ml = *reinterpret_cast<const float2 *>(slot + S::ml_index(wid, qs, lane));
-      const float mn = fmaxf(m[qs], ml.x);
-      const float ca = __builtin_amdgcn_exp2f(m[qs] - mn), cb = __builtin_amdgcn_exp2f(ml.x - mn);
-      l[qs] = l[qs] * ca + ml.y * cb;
-#pragma unroll
-      for (int d = 0; d < DS; ++d)
-        o[qs][d] = o[qs][d] * ca + *reinterpret_cast<const f32x4 *>(slot + S::o_index(wid, qs, d, lane)) * cb;
-      m[qs] = mn;
+    if (pend == nullptr) {
+      pend = slot;
+    } else {
+      Part c0, c1;
+      load(pend, c0);
+      load(slot, c1);
+      merge(c0);
+      merge(c1);
+      pend = nullptr;
     }
     if (eq >= ue) break;
+  }
+  if (pend != nullptr) {
+    Part c0;
+    load(pend, c0);
+    merge(c0);
   }
   attn_store_out<HD, QW, NW>(a, u, wid, lane, o, l);
 }
