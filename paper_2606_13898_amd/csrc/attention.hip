@@ -2,8 +2,9 @@
 // sequence (joint attention of a sample's image and text tokens, no mask).
 //
 // bf16 path (gfx950 MFMA v_mfma_f32_16x16x32_bf16, fp32 online softmax in base 2):
-//   workgroup = NW waves x QW query rows of one (sample, head); K/V stream through LDS in tiles of
-//   64 keys, double buffered.  Each wave computes S^T = K Q^T so that every lane owns one query
+//   workgroup = NW waves x QW query rows of one (sample, head) (head dim 128: 8 x 32, one
+//   workgroup per CU; 64: 4 x 32, two per CU); K/V stream through LDS in tiles of 64 keys, double
+//   buffered.  Each wave computes S^T = K Q^T so that every lane owns one query
 //   row's scores (4 keys per 16-key subtile): the running max stays lane-local, and the
 //   probabilities are already in the register layout of the second MFMA operand for
 //   O^T = V^T P^T.  The MFMA's k index may be permuted as long as both operands agree: the lane
@@ -181,7 +182,7 @@ HILO_DEV void attn_store_out(const AttnArgs &a, const AttnUnit &u, int wid, int 
 }
 
 template <int HD, int QW, int NW>
-__global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a) {
+__global__ __launch_bounds__(NW * 64, 8 / NW) void k_attn_bf16(AttnArgs a) {
   using S = AttnShape<HD, QW, NW>;
   constexpr int BKV = 64;
   constexpr int QS = S::QS;         // query subtiles per wave
@@ -444,7 +445,7 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a) {
 
 // Merges every unit cut by range boundaries; run by the range holding the unit's first key step.
 template <int HD, int QW, int NW>
-__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 2))) void k_attn_fix(AttnArgs a) {
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_attn_fix(AttnArgs a) {
   using S = AttnShape<HD, QW, NW>;
   constexpr int QS = S::QS, DS = S::DS, BQ = S::BQ;
   const int P = gridDim.x;
@@ -577,7 +578,9 @@ __global__ __launch_bounds__(64) void k_attn_f32(const float *__restrict__ qkv,
   }
 }
 
-int attn_workgroups() {
+// Persistent workgroups of the bf16 core: per_cu on every CU, capped so that their two partial
+// slots each (slot_floats) fit the partial area of the workspace.
+int attn_workgroups(int per_cu, size_t slot_floats) {
   static int ncu[64] = {0};
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) dev = 0;
@@ -587,17 +590,20 @@ int attn_workgroups() {
       n = kAttnMaxWorkgroups / 2;
     ncu[dev] = n;
   }
-  const int p = 2 * ncu[dev];  // two workgroups fit on a CU
-  return p < kAttnMaxWorkgroups ? p : kAttnMaxWorkgroups;
+  const int cap = int(kAttnPartBytes / (2 * slot_floats * sizeof(float)));
+  const int p = per_cu * ncu[dev];
+  return p < cap ? p : cap;
 }
 
 template <int HD, int QW, int NW>
 static hipError_t run_attn_bf16(const void *qkv, const int *cu, void *out, float *part, int B,
                                 int heads, hipStream_t st) {
-  static_assert(AttnShape<HD, QW, NW>::kSlotFloats <= kAttnSlotFloats, "partial slot too small");
+  using S = AttnShape<HD, QW, NW>;
+  static_assert(S::kSlotFloats <= 2 * kAttnSlotFloats, "partial slot too large for the workspace");
   AttnArgs a{reinterpret_cast<const uint16_t *>(qkv), cu, reinterpret_cast<uint16_t *>(out), part, B,
              heads, kLog2e / sqrtf(float(HD))};
-  const int P = attn_workgroups();
+  // 4 waves: two workgroups per CU; 8 waves: one (two waves per SIMD either way)
+  const int P = attn_workgroups(NW == 8 ? 1 : 2, S::kSlotFloats);
   hipLaunchKernelGGL((k_attn_bf16<HD, QW, NW>), dim3(P), dim3(NW * 64), 0, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -621,7 +627,7 @@ static hipError_t run_attn_f32(const void *qkv, const int *cu, void *out, int B,
 hipError_t launch_attention(bool bf16, const void *qkv, const int *cu, void *out, float *part, int B,
                             int heads, int hd, int max_seq, hipStream_t st) {
   if (bf16) {
-    if (hd == 128) return run_attn_bf16<128, 32, 4>(qkv, cu, out, part, B, heads, st);
+    if (hd == 128) return run_attn_bf16<128, 32, 8>(qkv, cu, out, part, B, heads, st);
     return run_attn_bf16<64, 32, 4>(qkv, cu, out, part, B, heads, st);
   }
   if (hd == 128) return run_attn_f32<128>(qkv, cu, out, B, heads, max_seq, st);
