@@ -233,11 +233,14 @@ hilo_status hilo_select_tokens(const hilo_shape *s, const int64_t *energy, const
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   const int r = dilate_r > s->grid_h + s->grid_w ? s->grid_h + s->grid_w : dilate_r;
   hipError_t he = timed(K_SELECT, st, [&] {
+    // one grid: the selection writes the layout itself (one launch less)
+    const bool one = G == 1;
     return launch_select(reinterpret_cast<const long long *>(energy), force, G, s->grid_h,
                          s->grid_w, r, mode, token_set, tau, keep, idx_map, fine_idx, pool_idx,
-                         counts, st);
+                         counts, one ? cu_seqlens : nullptr, one ? seg_off : nullptr, s->text_len, st);
   });
   if (he != hipSuccess) return HILO_E_DEVICE;
+  if (G == 1) return HILO_OK;
   return dev_status(timed(K_LAYOUT, st, [&] {
     return launch_layout(counts, s->batch, s->images, s->text_len, cu_seqlens, seg_off, st);
   }));

@@ -15,10 +15,12 @@ hipError_t launch_score(bool bf16, const void *x, long long *E, int G, int H, in
 // rgb [G][3][16 H][16 W] float32 -> E [G][H * W]: per-token pixel-space Sobel energy
 hipError_t launch_score_pixels(const float *rgb, long long *E, int G, int H, int W, hipStream_t st);
 size_t select_lds_bytes(int NB);
-// tokens: 0 partition, 1 overlap, 2 drop (see k_select)
+// tokens: 0 partition, 1 overlap, 2 drop (see k_select).  With G == 1, cu and seg (both or
+// neither) receive the sequence layout as well (L text rows), so launch_layout is not needed.
 hipError_t launch_select(const long long *E, const uint8_t *force, int G, int H, int W, int r,
                          int mode, int tokens, const double *tau, const int *keep, int *idx_map,
-                         int *fine_idx, int *pool_idx, int *counts, hipStream_t st);
+                         int *fine_idx, int *pool_idx, int *counts, int *cu, int *seg, int L,
+                         hipStream_t st);
 hipError_t launch_layout(const int *counts, int B, int I, int L, int *cu, int *seg, hipStream_t st);
 
 hipError_t launch_compress(bool bf16, const void *x_img, const void *x_txt, const int *fine_idx,

@@ -233,7 +233,8 @@ struct SelChunk {
 __global__ __launch_bounds__(kSelThreads) void k_select(
     const long long *__restrict__ E, const uint8_t *__restrict__ force, int H, int W, int r,
     int mode, int tokens, SelChunk prm, int g0, int *__restrict__ idx_map, int *__restrict__ fine_idx,
-    int *__restrict__ pool_idx, int *__restrict__ counts) {
+    int *__restrict__ pool_idx, int *__restrict__ counts, int *__restrict__ cu_out,
+    int *__restrict__ seg_out, int L) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   const int gl = blockIdx.x;
   const int g = g0 + gl;
@@ -395,7 +396,16 @@ __global__ __launch_bounds__(kSelThreads) void k_select(
         im[p] = tokens == 2 ? -1 : nfine + prank[b];
       }
     }
-    if (tid == 0) counts[2 * g] = nfine;
+    if (tid == 0) {
+      counts[2 * g] = nfine;
+      // a selection of a single grid (one sample, one image) also writes the sequence layout: the
+      // grid's rows start at 0 and the text rows follow them (the counts are this thread's own)
+      if (cu_out != nullptr) {
+        seg_out[0] = 0;
+        cu_out[0] = 0;
+        cu_out[1] = counts[2 * g + 1] + nfine + L;
+      }
+    }
   }
 }
 
@@ -405,7 +415,9 @@ size_t select_lds_bytes(int NB) {
 
 hipError_t launch_select(const long long *E, const uint8_t *force, int G, int H, int W, int r,
                          int mode, int tokens, const double *tau, const int *keep, int *idx_map,
-                         int *fine_idx, int *pool_idx, int *counts, hipStream_t st) {
+                         int *fine_idx, int *pool_idx, int *counts, int *cu, int *seg, int L,
+                         hipStream_t st) {
+  if ((cu != nullptr) != (seg != nullptr) || (cu != nullptr && G != 1)) return hipErrorInvalidValue;
   const int NB = H * W / 4;
   const size_t lds = select_lds_bytes(NB);
   for (int g0 = 0; g0 < G; g0 += kSelMaxGrids) {
@@ -416,7 +428,7 @@ hipError_t launch_select(const long long *E, const uint8_t *force, int G, int H,
       c.keep[k] = (mode == 1 && k < n) ? keep[g0 + k] : 0;
     }
     hipLaunchKernelGGL(k_select, dim3(n), dim3(kSelThreads), lds, st, E, force, H, W, r, mode, tokens,
-                       c, g0, idx_map, fine_idx, pool_idx, counts);
+                       c, g0, idx_map, fine_idx, pool_idx, counts, cu, seg, L);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
