@@ -166,12 +166,17 @@ struct SkPlan {
   int s, U, dp;    // pieces per tile, units, data-parallel units
   int len;         // K steps of a stream-K unit
   long long I;     // stream-K iterations
+  int Pk;          // workgroups sharing them (0 .. Pk-1; the others get empty ranges)
 };
 
 // A problem with fewer tiles than workgroups and at most this many K steps runs one whole tile per
 // workgroup (some CUs idle) instead of cutting tiles into K pieces: for short K the partial tiles
 // and their fixup cost more than the idle CUs.
 constexpr int kNoSplitSteps = 64;
+
+// Stream-K ranges hold at least this many K steps: every range cut leaves a partial tile (256 KiB
+// at 256 x 256) that the fixup reads back, so a short tail goes to fewer workgroups.
+constexpr int kSkMinSteps = 6;
 
 HILO_DEV SkPlan sk_plan(const GemmProblem &p, int BM, int BN, int P, int kstep = 64) {
   SkPlan q;
@@ -190,6 +195,7 @@ HILO_DEV SkPlan sk_plan(const GemmProblem &p, int BM, int BN, int P, int kstep =
     q.U = q.dp = q.T;
     q.len = q.nk;
     q.I = 0;
+    q.Pk = P;
     return q;
   }
   q.s = (q.T >= P || q.T == 0) ? 1 : min((P + q.T - 1) / q.T, q.nk);
@@ -200,6 +206,9 @@ HILO_DEV SkPlan sk_plan(const GemmProblem &p, int BM, int BN, int P, int kstep =
   const int pc = tail > 0 ? q.dp / q.T : 0;
   q.len = (pc + 1) * q.nk / q.s - pc * q.nk / q.s;
   q.I = (long long)tail * q.len;
+  // at least one workgroup per tail unit, so no range is longer than a unit and a range touches at
+  // most two units (the two partial slots of its workgroup)
+  q.Pk = int(min((long long)P, max((long long)tail, (q.I + kSkMinSteps - 1) / kSkMinSteps)));
   return q;
 }
 
@@ -209,6 +218,11 @@ struct SkRange {
 
 HILO_DEV SkRange sk_range(long long I, int P, int w) {
   return SkRange{I * w / P, I * (w + 1) / P};
+}
+
+// Workgroup w's stream-K range under plan q (empty past the plan's Pk workgroups).
+HILO_DEV SkRange sk_range(const SkPlan &q, int w) {
+  return w < q.Pk ? sk_range(q.I, q.Pk, w) : SkRange{q.I, q.I};
 }
 
 // The workgroup whose stream-K range holds iteration a.
@@ -453,7 +467,7 @@ __global__ __launch_bounds__(WM *WN * 64) void k_gemm_sk(GemmProblem p) {
   const int P = gridDim.x;
   const int pid = xcd_remap(blockIdx.x, P);
   const SkPlan q = sk_plan(p, BM, BN, P);
-  const SkRange rg = sk_range(q.I, P, pid);
+  const SkRange rg = sk_range(q, pid);
 
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int wrow = (wid / WN) * (BM / WM), wcol = (wid % WN) * (BN / WN);
@@ -778,7 +792,7 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
   const int P = gridDim.x;
   const int pid = xcd_remap(blockIdx.x, P);
   const SkPlan q = sk_plan(p, TB, TB, P, F8 ? 128 : 64);
-  const SkRange rg = sk_range(q.I, P, pid);
+  const SkRange rg = sk_range(q, pid);
 
   const int lane = threadIdx.x & 63;
   const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -1050,21 +1064,22 @@ __global__ __launch_bounds__(kFixThreads) void k_gemm_fix(GemmProblem p, int P) 
       }
       const int v = u - q.dp;
       const long long a0 = (long long)v * q.len;
-      const int w0 = sk_owner(q.I, P, a0), w1 = sk_owner(q.I, P, a0 + q.len - 1);
+      const int w0 = sk_owner(q.I, q.Pk, a0), w1 = sk_owner(q.I, q.Pk, a0 + q.len - 1);
       if (q.s == 1 && w0 == w1) {  // one workgroup held the whole tile and finished it
         done_whole = true;
         break;
       }
-      // contributors in workgroup order.  Range starts floor(I w / P) advance by additions (no
+      // contributors in workgroup order.  Range starts floor(I w / Pk) advance by additions (no
       // 64-bit division per contributor); a range's first unit is v exactly when it starts at or
       // after unit v's first iteration.
-      const long long qI = q.I / P, rI = q.I - qI * P;
-      long long qb = q.I * w0 / P, rb = q.I * w0 - qb * P;
+      const int Pk = q.Pk;
+      const long long qI = q.I / Pk, rI = q.I - qI * Pk;
+      long long qb = q.I * w0 / Pk, rb = q.I * w0 - qb * Pk;
       for (int w = w0; w <= w1; ++w) {
         long long qn = qb + qI, rn = rb + rI;
-        if (rn >= P) {
+        if (rn >= Pk) {
           ++qn;
-          rn -= P;
+          rn -= Pk;
         }
         if (qb < qn) push(p.part + (size_t(P) + size_t(w) * 2 + (qb >= a0 ? 0 : 1)) * T::kPartFloats);
         qb = qn;
