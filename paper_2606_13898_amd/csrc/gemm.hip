@@ -176,7 +176,7 @@ constexpr int kNoSplitSteps = 64;
 
 // Stream-K ranges hold at least this many K steps: every range cut leaves a partial tile (256 KiB
 // at 256 x 256) that the fixup reads back, so a short tail goes to fewer workgroups.
-constexpr int kSkMinSteps = 6;
+constexpr int kSkMinSteps = 12;
 
 HILO_DEV SkPlan sk_plan(const GemmProblem &p, int BM, int BN, int P, int kstep = 64) {
   SkPlan q;

@@ -13,7 +13,7 @@ import random
 import pytest
 
 NO_SPLIT_STEPS = 64   # kNoSplitSteps
-MIN_STEPS = 6         # kSkMinSteps
+MIN_STEPS = 12        # kSkMinSteps
 
 
 def plan(T, P, nk):
@@ -116,9 +116,9 @@ def test_schedule_fixed_cases(T, P, nk):
 
 
 def test_mlp_up_tail_goes_to_fewer_workgroups():
-    # 528 tiles on 256 workgroups: two whole waves, then 16 tiles x 48 steps over 128 workgroups
+    # 528 tiles on 256 workgroups: two whole waves, then 16 tiles x 48 steps over 64 workgroups
     s, U, dp, ln, I, Pk = plan(528, 256, 48)
-    assert (s, dp, ln, I, Pk) == (1, 512, 48, 768, 128)
+    assert (s, dp, ln, I, Pk) == (1, 512, 48, 768, 64)
 
 
 def test_schedule_random_cases():
