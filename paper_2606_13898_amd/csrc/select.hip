@@ -54,14 +54,20 @@ __global__ __launch_bounds__(512) void k_score(const void *__restrict__ x, long 
 
   for (int cg = threadIdx.x; cg < CG; cg += blockDim.x) {
     const size_t c0 = size_t(cg) * V;
-    float Lu[V], Lm[V], Ld[V], Cu[V], Cm[V], Cd[V], Ru[V], Rm[V], Rd[V];
+    // per column: the upper and lower rows (for gy) and the column sum (u + 2 m) + d (for gx),
+    // formed once per column and slid along j; gx = sum(right) - sum(left) in the same order
+    float Lu[V], Ld[V], Ls[V], Cu[V], Cd[V], Cs[V], Ru[V], Rm[V], Rd[V], Rs[V];
     const int jl = max(j0 - 1, 0);
     load_vec<BF16>(x, (rU + jl) * D + c0, Lu);
-    load_vec<BF16>(x, (rM + jl) * D + c0, Lm);
+    load_vec<BF16>(x, (rM + jl) * D + c0, Rm);
     load_vec<BF16>(x, (rD + jl) * D + c0, Ld);
+#pragma unroll
+    for (int v = 0; v < V; ++v) Ls[v] = (Lu[v] + 2.0f * Rm[v]) + Ld[v];
     load_vec<BF16>(x, (rU + j0) * D + c0, Cu);
-    load_vec<BF16>(x, (rM + j0) * D + c0, Cm);
+    load_vec<BF16>(x, (rM + j0) * D + c0, Rm);
     load_vec<BF16>(x, (rD + j0) * D + c0, Cd);
+#pragma unroll
+    for (int v = 0; v < V; ++v) Cs[v] = (Cu[v] + 2.0f * Rm[v]) + Cd[v];
 #pragma unroll
     for (int k = 0; k < TJ; ++k) {
       if (k < nj) {
@@ -73,7 +79,8 @@ __global__ __launch_bounds__(512) void k_score(const void *__restrict__ x, long 
 #pragma unroll
         for (int v = 0; v < V; ++v) {
           // horizontal: right column minus left column, rows weighted 1, 2, 1
-          float gx = ((Ru[v] + 2.0f * Rm[v]) + Rd[v]) - ((Lu[v] + 2.0f * Lm[v]) + Ld[v]);
+          Rs[v] = (Ru[v] + 2.0f * Rm[v]) + Rd[v];
+          float gx = Rs[v] - Ls[v];
           // vertical: lower row minus upper row, columns weighted 1, 2, 1
           float gy = ((Ld[v] + 2.0f * Cd[v]) + Rd[v]) - ((Lu[v] + 2.0f * Cu[v]) + Ru[v]);
           float t1 = gx * gx;
@@ -85,8 +92,8 @@ __global__ __launch_bounds__(512) void k_score(const void *__restrict__ x, long 
         acc[k] += dpart;
 #pragma unroll
         for (int v = 0; v < V; ++v) {
-          Lu[v] = Cu[v]; Lm[v] = Cm[v]; Ld[v] = Cd[v];
-          Cu[v] = Ru[v]; Cm[v] = Rm[v]; Cd[v] = Rd[v];
+          Lu[v] = Cu[v]; Ld[v] = Cd[v]; Ls[v] = Cs[v];
+          Cu[v] = Ru[v]; Cd[v] = Rd[v]; Cs[v] = Rs[v];
         }
       }
     }
