@@ -304,8 +304,21 @@ __global__ __launch_bounds__(kSelThreads) void k_select(
         for (int d = tid; d < 256; d += kSelThreads) hist[d] = 0;
         __syncthreads();
         for (int b = tid; b < NB; b += kSelThreads) {
-          if (!(flag[b] & 2) && (Bs[b] & mask) == prefix)
-            atomicAdd(&hist[(Bs[b] >> shift) & 255], 1);
+          const long long v = Bs[b];
+          const bool cand = !(flag[b] & 2) && (v & mask) == prefix;
+          const int dg = int((v >> shift) & 255);
+          // a wave whose candidates share one digit (the leading digits of the sums mostly do)
+          // adds their count with one atomic instead of 64 serialised on one address
+          const unsigned long long cm = __ballot(cand);
+          if (cm != 0) {
+            const int first = __ffsll(cm) - 1;
+            const int d0 = __shfl(dg, first, 64);
+            if (__ballot(cand && dg != d0) == 0) {
+              if ((tid & 63) == first) atomicAdd(&hist[d0], __popcll(cm));
+            } else if (cand) {
+              atomicAdd(&hist[dg], 1);
+            }
+          }
         }
         __syncthreads();
         if (tid < 64) {
