@@ -277,7 +277,10 @@ __global__ __launch_bounds__(kSelThreads) void k_select(
     }
     flag[b] = f;
   }
-  const long long emax = block_max_i64(mx, ltmp);  // includes a barrier: Bs and flag visible
+  // the grid maximum only enters the threshold rule; either way a barrier makes Bs and flag visible
+  long long emax = 0;
+  if (mode == 0) emax = block_max_i64(mx, ltmp);
+  else __syncthreads();
 
   if (mode == 0) {  // threshold
     if (emax > 0) {
