@@ -371,14 +371,6 @@ def quantize_rows(x: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
     return codes, scale
 
 
-def round_bf16(x: np.ndarray) -> np.ndarray:
-    """x rounded to bfloat16 (via float32, round to nearest even; torch's cast as the library
-    primitive), returned as float64."""
-    import torch
-
-    return torch.from_numpy(np.asarray(x, dtype=np.float32)).to(torch.bfloat16).to(torch.float64).numpy()
-
-
 def dequant_rows(codes: np.ndarray, scale: np.ndarray) -> np.ndarray:
     return e4m3_value(codes) * np.asarray(scale, dtype=np.float64)[:, None]
 
@@ -438,8 +430,10 @@ def attention(Z: np.ndarray, cu: np.ndarray, text_len: int, heads: int, weights,
     Joint attention over image + text tokens of one sample, no mask (Sec. 2.3: the HiLo tokens are
     processed by the DiT; Sec. 2.2: memory-efficient attention).  Returns z1 for `rows` (all rows
     when None), float64 [len(rows)][D].  With `fp8` (per stream {"w_qkv": (codes, scale), "w_o": ...})
-    both projections multiply FP8 rows of their input by FP8 rows of the weight (quantize_rows): h as
-    formed, a as the bf16 rows the block stores between its kernels."""
+    both projections multiply FP8 rows of their input by FP8 rows of the weight (quantize_rows): each
+    input row is quantised from the value the block computes (h, then the attention output a), in
+    float64 rounded once to float32 (Sec. 3.3 names FP8 quantisation of the network and nothing about
+    an intermediate storage precision, so none is assumed)."""
     T, D = Z.shape
     all_rows = np.arange(T) if rows is None else np.asarray(rows)
     out = np.empty((all_rows.size, D), dtype=np.float64)
@@ -462,8 +456,7 @@ def attention(Z: np.ndarray, cu: np.ndarray, text_len: int, heads: int, weights,
             m = (all_rows[sel] >= text_start) if sig == 1 else (all_rows[sel] < text_start)
             if not m.any():
                 continue
-            # FP8: the attention output is quantised from the bf16 rows the block stores (R21)
-            prod = (_fp8_matmul(round_bf16(a_out[m]), fp8[sig]["w_o"]) if fp8 is not None
+            prod = (_fp8_matmul(a_out[m], fp8[sig]["w_o"]) if fp8 is not None
                     else a_out[m] @ _w(weights, sig, "w_o").T)
             o = prod + _w(weights, sig, "b_o")
             out[sel[m]] = Z[all_rows[sel][m]] + mod[s, sig, 2] * o
@@ -476,7 +469,7 @@ def mlp(Z1: np.ndarray, row_ids: np.ndarray, cu: np.ndarray, text_len: int, weig
     h2 = LN(z1) * (1 + scale2) + shift2.  Z1 holds the rows `row_ids` of the packed sequence (their
     sample and stream follow from cu_seqlens).  Returns float64 [len(row_ids)][D].  With `fp8`
     (per stream {"w1": (codes, scale), "w2": ...}) both projections multiply FP8 rows of their input
-    by FP8 rows of the weight: h2 as formed, the GELU output as the bf16 rows the block stores."""
+    by FP8 rows of the weight: h2 and the GELU output are quantised from their computed values."""
     out = np.empty_like(Z1, dtype=np.float64)
     row_ids = np.asarray(row_ids)
     for (s, sig, a, b) in _segments(cu, text_len):
@@ -488,8 +481,7 @@ def mlp(Z1: np.ndarray, row_ids: np.ndarray, cu: np.ndarray, text_len: int, weig
         prod = _fp8_matmul(h2, fp8[sig]["w1"]) if fp8 is not None else h2 @ _w(weights, sig, "w1").T
         u = prod + _w(weights, sig, "b1")
         g = gelu_tanh(u)
-        # FP8: the GELU output is quantised from the bf16 rows the block stores (R21)
-        prod = _fp8_matmul(round_bf16(g), fp8[sig]["w2"]) if fp8 is not None else g @ _w(weights, sig, "w2").T
+        prod = _fp8_matmul(g, fp8[sig]["w2"]) if fp8 is not None else g @ _w(weights, sig, "w2").T
         o = prod + _w(weights, sig, "b2")
         out[m] = z + mod[s, sig, 5] * o
     return out

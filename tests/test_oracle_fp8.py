@@ -83,11 +83,3 @@ def test_fp8_block_quantises_all_four_projections():
             Z = res["Z"]
             for (s_, sig, a, b) in O._segments(res["cu"], shp.text_len):
                 np.testing.assert_allclose(y1[a:b], Z[a:b] + wl.mod[s_, sig, 2] * np.asarray(wl.weights[sig]["b_o"], np.float64), atol=1e-12)
-
-
-def test_round_bf16_hand_worked_ties():
-    # bf16 keeps 7 mantissa bits: 1 + 2^-8 is halfway between 1 and 1 + 2^-7 -> even 1.0;
-    # 1 + 3 * 2^-8 is halfway between 1 + 2^-7 (odd) and 1 + 2^-6 (even) -> 1 + 2^-6; 448 and 2^-9
-    # are exact
-    x = np.array([1 + 2.0 ** -8, 1 + 3 * 2.0 ** -8, -(1 + 2.0 ** -8), 448.0, 2.0 ** -9])
-    np.testing.assert_array_equal(O.round_bf16(x), [1.0, 1 + 2.0 ** -6, -1.0, 448.0, 2.0 ** -9])
