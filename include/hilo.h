@@ -24,7 +24,8 @@
  *     the later calls read them there, sizing their grids for the worst case (no compression).
  *   - Shapes: G = batch * images grids of N = grid_h * grid_w patches (raster order p = i*grid_w+j),
  *     NB = N / 4 coarse 2x2 blocks (b = (i/2)*(grid_w/2) + j/2), D = dim, L = text_len.
- *     T_max = batch * (images * N + L) is the longest packed sequence (hilo_max_tokens).
+ *     T_max = batch * (images * (N + NB) + L) bounds the packed sequence of every token set
+ *     (hilo_max_tokens; the PARTITION set of hilo_select never exceeds batch * (images * N + L)).
  *   - The packed sequence of sample s occupies rows [cu_seqlens[s], cu_seqlens[s+1]) of z:
  *     [grid 0: fine patches in raster order, then pooled blocks in block order ; grid 1 ... ;
  *      L text tokens].  seg_off[g] is the first row of grid g.
@@ -41,7 +42,7 @@
 extern "C" {
 #endif
 
-#define HILO_ABI_VERSION 4
+#define HILO_ABI_VERSION 5
 
 typedef enum {
   HILO_OK = 0,
@@ -109,8 +110,9 @@ hilo_status hilo_score(const hilo_shape *shape, const void *x_img, int64_t *ener
  * onto the token grid).  rgb: DEVICE float32 [G][3][16 grid_h][16 grid_w] (planar channels, any
  * value range).  For every pixel and channel the energy and fixed point of hilo_score (same
  * formulas, neighbours clamped to the image), summed exactly over the token's 16 x 16 pixels and 3
- * channels: energy [G][N] int64, ready for hilo_select (e.g. THRESHOLD with tau = 0.1, the
- * paper's value).  HILO_E_SHAPE if the image has 2^31 or more values.                           */
+ * channels: energy [G][N] int64, ready for hilo_select.  The paper cuts its normalised Sobel
+ * magnitude at 0.1; the energy is the magnitude squared, so its counterpart here is THRESHOLD
+ * with tau = 0.01.  HILO_E_SHAPE if the image has 2^31 or more values.                          */
 hilo_status hilo_score_pixels(const hilo_shape *shape, const float *rgb, int64_t *energy, void *stream);
 
 /* S2 -- selection (Sec. 2.3: 16x regional pooling of the frequency map onto the token grid,
@@ -150,20 +152,27 @@ hilo_status hilo_compress(const hilo_shape *shape, const void *x_img, const void
                           const int32_t *fine_idx, const int32_t *pool_idx, const int32_t *counts,
                           const int32_t *cu_seqlens, const int32_t *seg_off, float *z, void *stream);
 
-/* S4 -- attention half of the block, in place on z (MMDiT-style joint attention over the image
- * and text tokens of each sample; image rows use w[0] / mod stream 0, text rows w[1] / stream 1):
+/* S4 -- attention half of the block, in place on z (Sec. 2.3: the concatenated HiLo tokens are
+ * what the DiT processes; Sec. 2.2 and Sec. 4: attention over all tokens is the quadratic cost the
+ * compression removes).  MMDiT-style joint attention over the image and text tokens of each
+ * sample; image rows use w[0] / mod stream 0, text rows w[1] / stream 1:
  *   h = LN(z) * (1 + scale1) + shift1;  qkv = h W_qkv^T + b_qkv
  *   a = softmax(q k^T / sqrt(head_dim)) v per head over all rows of the sample (no mask)
  *   z = z + gate1 * (a W_o^T + b_o)
  * LN: biased variance over D, eps 1e-6, no affine.  mod [batch][2][6][D] float32 holds
  * shift1, scale1, gate1, shift2, scale2, gate2 per sample and stream.  bf16 products accumulate in
  * float32; h, qkv and a are rounded to `dtype` in the workspace.  workspace: device scratch of
- * ws_bytes >= hilo_workspace_bytes(shape), owned by the caller, contents undefined after.        */
+ * ws_bytes >= hilo_workspace_bytes(shape), owned by the caller, contents undefined after.
+ * The block needs only the sample boundaries (cu_seqlens) and the image/text split (the last
+ * text_len rows of each sample): the per-grid counts and offsets of hilo_select do not change it,
+ * since attention is equivariant to the order of a sample's rows and the weights depend only on
+ * the stream.                                                                                   */
 hilo_status hilo_attention(const hilo_shape *shape, float *z, const int32_t *cu_seqlens,
                            const hilo_attn_w w[2], const float *mod, void *workspace,
                            size_t ws_bytes, void *stream);
 
-/* S5 -- MLP half of the block, in place on z:
+/* S5 -- MLP half of the block, in place on z (Sec. 2.3: the DiT runs on the HiLo tokens; Sec. 2.2:
+ * the DiT is most of the model's latency):
  *   h2 = LN(z) * (1 + scale2) + shift2;  z = z + gate2 * (GELU_tanh(h2 W1^T + b1) W2^T + b2)
  * GELU_tanh(u) = 0.5 u (1 + tanh(sqrt(2/pi) (u + 0.044715 u^3))).  Arguments as hilo_attention. */
 hilo_status hilo_mlp(const hilo_shape *shape, float *z, const int32_t *cu_seqlens,
@@ -224,15 +233,16 @@ typedef struct {
 hilo_status hilo_quantize_rows(int32_t dtype, const void *x, int64_t rows, int64_t cols,
                                uint8_t *codes, float *scale, void *stream);
 
-/* Workspace of the FP8 block (hilo_attention_fp8, hilo_mlp_fp8): hilo_workspace_bytes plus the
- * hidden rows' codes and scales; 0 if the shape is invalid for the FP8 block.                    */
+/* Workspace of the FP8 block (hilo_attention_fp8, hilo_mlp_fp8): hilo_workspace_bytes plus one
+ * region that holds the attention output's bf16 rows in the attention half and the hidden rows'
+ * codes and scales in the MLP half; 0 if the shape is invalid for the FP8 block.                 */
 size_t hilo_workspace_bytes_fp8(const hilo_shape *shape);
 
 /* hilo_attention with both projections in FP8: h = LN(z) * (1 + scale1) + shift1 is formed in
  * float32 and quantised per row straight from registers, then multiplied by the FP8 W_qkv; the
  * attention core is that of hilo_attention (bf16 q, k, v, output); its output rows are quantised and
  * multiplied by the FP8 W_o.  shape->dtype must be HILO_BF16 (HILO_E_DTYPE), dim and mlp_dim
- * multiples of 128 (HILO_E_SHAPE).  workspace: ws_bytes >= hilo_workspace_bytes(shape).           */
+ * multiples of 128 (HILO_E_SHAPE).  workspace: ws_bytes >= hilo_workspace_bytes_fp8(shape).       */
 hilo_status hilo_attention_fp8(const hilo_shape *shape, float *z, const int32_t *cu_seqlens,
                                const hilo_attn_w_fp8 w[2], const float *mod, void *workspace,
                                size_t ws_bytes, void *stream);
@@ -244,7 +254,9 @@ hilo_status hilo_mlp_fp8(const hilo_shape *shape, float *z, const int32_t *cu_se
                          const hilo_mlp_w_fp8 w[2], const float *mod, void *workspace,
                          size_t ws_bytes, void *stream);
 
-/* S6 -- decompress: y_img[g][p] = z[seg_off[g] + idx_map[g][p]] (fine tokens scatter back to
+/* S6 -- decompress.  The paper does not say how the DiT's output on the HiLo tokens returns to the
+ * full grid; this is the plain reading (each patch takes its token's output):
+ * y_img[g][p] = z[seg_off[g] + idx_map[g][p]] (fine tokens scatter back to
  * their patch, pooled tokens broadcast to the 4 patches of their block), y_txt[s][t] = the text
  * rows of sample s; both rounded to dtype.  y_img [G][N][D], y_txt [B][L][D] or NULL.  A patch
  * without a token (idx_map -1, token set DROP) gets zeros: use hilo_decompress_delta there.     */

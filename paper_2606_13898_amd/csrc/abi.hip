@@ -121,11 +121,22 @@ size_t ws_mlp(const hilo_shape *s) {
   return ws_h(s) + align256(T * F * e) + ws_part(s);  // h2, hidden, partials
 }
 
-// The FP8 MLP also holds the hidden rows as codes [T][F] and T row scales, behind the rest.
-size_t ws_mlp_fp8(const hilo_shape *s) {
-  const size_t T = size_t(tmax_of(s)), F = size_t(s->mlp_dim);
-  return ws_mlp(s) + align256(T * F) + align256(T * sizeof(float));
+// The FP8 block keeps one more region behind everything the bf16 block uses (at
+// hilo_workspace_bytes): the attention output's bf16 rows in the attention half (the normalised
+// rows' codes in the first region stay intact), the hidden rows' codes [T][F] and T row scales in
+// the MLP half.
+size_t ws_fp8_base(const hilo_shape *s) {
+  const size_t a = ws_attention(s), m = ws_mlp(s);
+  return a > m ? a : m;
 }
+
+size_t ws_fp8_extra(const hilo_shape *s) {
+  const size_t T = size_t(tmax_of(s)), D = size_t(s->dim), F = size_t(s->mlp_dim);
+  const size_t codes = align256(T * F) + align256(T * sizeof(float)), aout = align256(T * D * 2);
+  return codes > aout ? codes : aout;
+}
+
+size_t ws_fp8(const hilo_shape *s) { return ws_fp8_base(s) + ws_fp8_extra(s); }
 
 hilo_status dev_status(hipError_t e) { return e == hipSuccess ? HILO_OK : HILO_E_DEVICE; }
 
@@ -397,8 +408,11 @@ hilo_status enqueue_attention(const hilo_shape *s, float *z, const int32_t *cu_s
   if (he != hipSuccess) return HILO_E_DEVICE;
 
   const int max_seq = int(s->images * grid_rows_max(s) + s->text_len);
+  // the attention output: over the normalised rows (bf16 block), or behind the bf16 block's
+  // regions (FP8 block, whose normalised-row codes stay in place)
+  void *aout = w8 ? static_cast<void *>(ws + ws_fp8_base(s)) : h;
   he = timed(K_ATTN_CORE, st, [&] {
-    return launch_attention(bf, qkv, cu_seqlens, h, part, s->batch, s->heads, s->head_dim,
+    return launch_attention(bf, qkv, cu_seqlens, aout, part, s->batch, s->heads, s->head_dim,
                             max_seq, st);
   });
   if (he != hipSuccess) return HILO_E_DEVICE;
@@ -411,7 +425,7 @@ hilo_status enqueue_attention(const hilo_shape *s, float *z, const int32_t *cu_s
     // the attention output's rows as FP8 codes and scales, in the QKV region (free again)
     uint8_t *ac = reinterpret_cast<uint8_t *>(qkv);
     float *as = reinterpret_cast<float *>(ac + align256(size_t(T) * D));
-    he = timed(K_QUANT_ATTN, st, [&] { return launch_quantize_rows(true, h, T, D, ac, as, st, cu_seqlens + s->batch); });
+    he = timed(K_QUANT_ATTN, st, [&] { return launch_quantize_rows(true, aout, T, D, ac, as, st, cu_seqlens + s->batch); });
     if (he != hipSuccess) return HILO_E_DEVICE;
     q.A = ac;
     q.W[0] = w8[0].w_o; q.W[1] = w8[1].w_o;
@@ -468,8 +482,8 @@ hilo_status enqueue_mlp(const hilo_shape *s, float *z, const int32_t *cu_seqlens
   q.N = D; q.K = F;
   q.z = z; q.ldz = D; q.gate_idx = 5;
   if (w8) {
-    // the hidden rows as FP8 codes and scales, behind everything the bf16 MLP uses
-    uint8_t *hc = reinterpret_cast<uint8_t *>(ws + ws_mlp(s));
+    // the hidden rows as FP8 codes and scales, behind everything the bf16 block uses
+    uint8_t *hc = reinterpret_cast<uint8_t *>(ws + ws_fp8_base(s));
     float *hs8 = reinterpret_cast<float *>(hc + align256(size_t(T) * F));
     he = timed(K_QUANT_MLP, st, [&] { return launch_quantize_rows(true, hid, T, F, hc, hs8, st, cu_seqlens + s->batch); });
     if (he != hipSuccess) return HILO_E_DEVICE;
@@ -515,8 +529,7 @@ hilo_status hilo_mlp(const hilo_shape *s, float *z, const int32_t *cu_seqlens,
 
 size_t hilo_workspace_bytes_fp8(const hilo_shape *s) {
   if (check_fp8_block(s) != HILO_OK) return 0;
-  const size_t a = ws_attention(s), m = ws_mlp_fp8(s);
-  return a > m ? a : m;
+  return ws_fp8(s);
 }
 
 hilo_status hilo_attention_fp8(const hilo_shape *s, float *z, const int32_t *cu_seqlens,
@@ -526,7 +539,7 @@ hilo_status hilo_attention_fp8(const hilo_shape *s, float *z, const int32_t *cu_
   if (e != HILO_OK) return e;
   if (!z || !cu_seqlens || !mod || !workspace) return HILO_E_NULL;
   if ((e = check_attn_w8(w)) != HILO_OK) return e;
-  if (ws_bytes < ws_attention(s)) return HILO_E_WORKSPACE;
+  if (ws_bytes < ws_fp8(s)) return HILO_E_WORKSPACE;
   if (!have_device()) return HILO_E_DEVICE;
   return enqueue_attention(s, z, cu_seqlens, nullptr, w, mod, workspace, reinterpret_cast<hipStream_t>(stream));
 }
@@ -538,7 +551,7 @@ hilo_status hilo_mlp_fp8(const hilo_shape *s, float *z, const int32_t *cu_seqlen
   if (e != HILO_OK) return e;
   if (!z || !cu_seqlens || !mod || !workspace) return HILO_E_NULL;
   if ((e = check_mlp_w8(w)) != HILO_OK) return e;
-  if (ws_bytes < ws_mlp_fp8(s)) return HILO_E_WORKSPACE;
+  if (ws_bytes < ws_fp8(s)) return HILO_E_WORKSPACE;
   if (!have_device()) return HILO_E_DEVICE;
   return enqueue_mlp(s, z, cu_seqlens, nullptr, w, mod, workspace, reinterpret_cast<hipStream_t>(stream));
 }

@@ -3,17 +3,13 @@
 // weights, tiles never straddling a segment.  Epilogues fuse the bias, the tanh-GELU, and the
 // gated residual update of the float32 stream z.
 //
-// bf16 path: gfx950 MFMA v_mfma_f32_16x16x32_bf16 with fp32 accumulation, persistent
-// workgroups running whole data-parallel waves of tiles, then a stream-K remainder, in one of two
-// tilings:
-//   * 128 x 128 tiles on 4 waves, accumulators in VGPRs, K steps of 64 through a double-buffered
-//     LDS ring (64 KiB) filled by direct global->LDS loads; two workgroups per CU (their barriers
-//     are independent, so one computes while the other waits for its loads);
-//   * 256 x 256 tiles on 4 waves (k_gemm_big), accumulators in AGPRs, 32-deep stages through a
-//     4-slot ring (128 KiB), one workgroup per CU: half the operand bytes per FLOP.
-//
-// The MFMA is issued with the weight fragment as its first operand, so each lane's 4
-// accumulators are 4 consecutive output columns of one row (contiguous epilogue stores).
+// bf16 and FP8 paths: one square-tile MFMA kernel (k_gemm_big), one persistent workgroup per CU
+// with 4 waves, 256 x 256 tiles (QKV, MLP up) or 192 x 192 (attention output, MLP down) as
+// 32 x 32 MFMA blocks (v_mfma_f32_32x32x16_bf16, or v_mfma_f32_32x32x64_f8f6f4 on E4M3 codes),
+// fp32 accumulators in AGPRs, K in 64-byte stages through a 4-slot LDS ring filled by direct
+// global->LDS loads.  Whole data-parallel waves of tiles run first, then a stream-K remainder;
+// cut tiles leave fp32 partials that k_gemm_fix adds in a fixed order before the epilogue.
+// float32 path: a plain LDS-tiled FMA kernel for the small float32 workloads.
 #include <type_traits>
 
 #include "common.h"
@@ -100,24 +96,11 @@ HILO_DEV void epilogue4(const GemmProblem &p, const TileRows &tr, int m, int n, 
 
 // ------------------------------------------------------------------------------- bf16 MFMA
 
-// LDS rows hold BK bf16 = BK/8 chunks of 16 bytes; chunk c of row r lives at slot c ^ swz(r).
-// An MFMA operand read touches one chunk of 16 consecutive rows: swz makes those 16 reads land
-// in 16 distinct 16-byte bank groups of a 256-byte bank window (64 banks), and any 8 consecutive
-// rows in 8 distinct groups of a 128-byte window (32 banks).
-template <int BK>
-HILO_DEV int swz(int r) {
-  if constexpr (BK == 64) return (r & 7) ^ ((r >> 3) & 1);
-  else return ((r >> 1) & 3) ^ ((r >> 3) & 1);
-}
-
 // One 16-byte global load per lane straight into LDS: lane l of the wave lands at byte 16*l of
 // the wave's 1 KiB destination (the destination base is uniform, held in M0).
 HILO_DEV void g2lds16(const void *g, void *lds_wave_base) {
   __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void *)lds_wave_base, 16, 0, 0);
 }
-
-template <int N>
-HILO_DEV void wait_vmem_le() { asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory"); }
 
 // Active row tiles of the ragged problem: per sample, ceil(image rows / BM) image tiles then
 // ceil(L / BM) text tiles.  Only the device knows the row counts, so every workgroup walks the
@@ -284,18 +267,13 @@ HILO_DEV SkItem sk_next_item(SkCursor &c, const SkPlan &q, const SkRange &rg, in
   return x;
 }
 
-// WM x WN waves, wave tile (BM/WM) x (BN/WN), K step 64 through a double-buffered LDS ring filled
-// by direct global->LDS loads one step ahead, one barrier per step.
+// Partial tiles of a BM x BN tile on WM x WN waves, in the 16 x 16 fragment order the fixup
+// reads, and the fixup's epilogue of one fragment row.
 template <int BM, int BN, int WM, int WN>
 struct SkTile {
   static constexpr int NW = WM * WN;
-  static constexpr int BK = 64;
-  static constexpr int RPI = 8;              // rows per wave load instruction (1 KiB)
   static constexpr int TM = BM / WM / 16;
   static constexpr int TN = BN / WN / 16;
-  static constexpr int IA = BM / RPI / NW;   // load instructions per wave per step
-  static constexpr int IB = BN / RPI / NW;
-  static_assert(IA * RPI * NW == BM && IB * RPI * NW == BN, "tile / wave mismatch");
   static constexpr size_t kPartFloats = size_t(BM) * BN;
 
   // partial-sum slot layout: register order, one float4 per lane per (wave, i, j)
@@ -384,213 +362,6 @@ struct SkTile {
     }
   }
 };
-
-// Epilogue of a WR x WC wave tile held as 32 x 32 blocks: lane (r, g) of block (i, j) holds row
-// 32 i + r and, in register 4 b + e, column 32 j + 8 b + 4 g + e (four runs of 4 columns).  For the
-// residual form the gate and bias of the lane's columns and the old z of one block row are loaded
-// before anything is stored (the compiler cannot prove that outputs do not alias inputs, so an
-// interleaved order would serialise one memory round trip per fragment).  Loads use indices
-// clamped into the tile; values outside it are never stored.
-template <int EPI, int WR, int WC>
-HILO_DEV void epilogue32(const GemmProblem &p, const TileRows &tr, int c0, int r0, int lane,
-                         const f32x16 (&acc)[WR / 32][WC / 32]) {
-  constexpr int TM2 = WR / 32, TN2 = WC / 32;
-  const int r32 = lane & 31, cg = c0 + 4 * (lane >> 5);
-  const uint16_t *bias = reinterpret_cast<const uint16_t *>(p.bias[tr.sigma]);
-  float bv[TN2][4][4];
-  float4 gt[TN2][4];
-#pragma unroll
-  for (int j = 0; j < TN2; ++j)
-#pragma unroll
-    for (int b = 0; b < 4; ++b) {
-      const int nc = min(cg + 32 * j + 8 * b, p.N - 4);
-      const uint2 bu = *reinterpret_cast<const uint2 *>(bias + nc);
-      bv[j][b][0] = __uint_as_float(bu.x << 16); bv[j][b][1] = __uint_as_float(bu.x & 0xffff0000u);
-      bv[j][b][2] = __uint_as_float(bu.y << 16); bv[j][b][3] = __uint_as_float(bu.y & 0xffff0000u);
-      if constexpr (EPI == EPI_RESID)
-        gt[j][b] = *reinterpret_cast<const float4 *>(p.mod + (size_t(tr.s * 2 + tr.sigma) * 6 + p.gate_idx) * p.D + nc);
-    }
-#pragma unroll
-  for (int i = 0; i < TM2; ++i) {
-    const int rl = r0 + 32 * i + r32;
-    float4 zv[TN2][4];
-    if constexpr (EPI == EPI_RESID) {
-      const size_t mz = size_t(tr.row0 + min(rl, tr.nrows - 1));
-#pragma unroll
-      for (int j = 0; j < TN2; ++j)
-#pragma unroll
-        for (int b = 0; b < 4; ++b)
-          zv[j][b] = *reinterpret_cast<const float4 *>(p.z + mz * p.ldz + min(cg + 32 * j + 8 * b, p.N - 4));
-    }
-    if (rl < tr.nrows) {
-      const size_t m = size_t(tr.row0 + rl);
-#pragma unroll
-      for (int j = 0; j < TN2; ++j)
-#pragma unroll
-        for (int b = 0; b < 4; ++b) {
-          const int n = cg + 32 * j + 8 * b;
-          if (n >= p.N) continue;
-          float v[4];
-#pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] = acc[i][j][4 * b + e] + bv[j][b][e];
-          if constexpr (EPI == EPI_RESID) {
-            float4 z = zv[j][b];
-            z.x += gt[j][b].x * v[0];
-            z.y += gt[j][b].y * v[1];
-            z.z += gt[j][b].z * v[2];
-            z.w += gt[j][b].w * v[3];
-            *reinterpret_cast<float4 *>(p.z + m * p.ldz + n) = z;
-          } else {
-            if constexpr (EPI == EPI_GELU) {
-#pragma unroll
-              for (int e = 0; e < 4; ++e) v[e] = gelu_tanh(v[e]);
-            }
-            uint2 u;
-            u.x = pack_bf16x2(v[0], v[1]);
-            u.y = pack_bf16x2(v[2], v[3]);
-            *reinterpret_cast<uint2 *>(reinterpret_cast<uint16_t *>(p.out) + m * p.ldo + n) = u;
-          }
-        }
-    }
-  }
-}
-
-template <int BM, int BN, int WM, int WN, int EPI, int ROLE>
-__global__ __launch_bounds__(WM *WN * 64) void k_gemm_sk(GemmProblem p) {
-  using T = SkTile<BM, BN, WM, WN>;
-  constexpr int BK = T::BK, TM = T::TM, TN = T::TN, IA = T::IA, IB = T::IB, NW = T::NW;
-  __shared__ __attribute__((aligned(1024))) uint16_t sA[2][BM * BK];
-  __shared__ __attribute__((aligned(1024))) uint16_t sB[2][BN * BK];
-
-  // logical workgroup index: each XCD gets a contiguous run of workgroup indices, hence of
-  // neighbouring tiles in every data-parallel wave and of the stream-K iteration space
-  const int P = gridDim.x;
-  const int pid = xcd_remap(blockIdx.x, P);
-  const SkPlan q = sk_plan(p, BM, BN, P);
-  const SkRange rg = sk_range(q, pid);
-
-  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  const int wrow = (wid / WN) * (BM / WM), wcol = (wid % WN) * (BN / WN);
-  constexpr int TM2 = BM / WM / 32, TN2 = BN / WN / 32;
-  const int r32 = lane & 31, g32 = lane >> 5;
-  const int lrow = lane >> 3, lslot = lane & 7;
-  const uint16_t *A = reinterpret_cast<const uint16_t *>(p.A);
-
-  SkCursor cur_c{pid, rg.beg};
-  auto next_item = [&]() { return sk_next_item(cur_c, q, rg, P, pid, p.part, T::kPartFloats); };
-  // a tile's rows and this lane's load sources: row (wave band + 8 i + lane / 8), chunk
-  // (lane % 8) ^ swz(row); rows past the tile edge re-read the last valid row (never stored)
-  struct Src {
-    TileRows tr;
-    int n0;
-    const uint16_t *a[IA];
-    const uint16_t *b[IB];
-  };
-  auto make_src = [&](int t) {
-    Src x;
-    int rt, tn;
-    tile_coords(q, t, rt, tn);
-    x.tr = decode_row_tile(p, BM, rt);
-    x.n0 = tn * BN;
-    const uint16_t *Wt = reinterpret_cast<const uint16_t *>(p.W[x.tr.sigma]);
-#pragma unroll
-    for (int i = 0; i < IA; ++i) {
-      const int r = wid * (BM / NW) + 8 * i + lrow;
-      x.a[i] = A + size_t(x.tr.row0 + min(r, x.tr.nrows - 1)) * p.lda + ((lslot ^ swz<BK>(r)) * 8);
-    }
-#pragma unroll
-    for (int i = 0; i < IB; ++i) {
-      const int r = wid * (BN / NW) + 8 * i + lrow;
-      x.b[i] = Wt + size_t(min(x.n0 + r, p.N - 1)) * p.K + ((lslot ^ swz<BK>(r)) * 8);
-    }
-    return x;
-  };
-  auto issue = [&](const Src &x, int k0, int buf) {
-#pragma unroll
-    for (int i = 0; i < IA; ++i) g2lds16(x.a[i] + k0, &sA[buf][(wid * (BM / NW) + 8 * i) * BK]);
-#pragma unroll
-    for (int i = 0; i < IB; ++i) g2lds16(x.b[i] + k0, &sB[buf][(wid * (BN / NW) + 8 * i) * BK]);
-  };
-
-  SkItem cur = next_item();
-  if (!cur.valid) return;
-  Src sc = make_src(cur.t);
-  issue(sc, cur.kb * BK, 0);
-  int buf = 0;  // the LDS ring alternates over the steps of all of this workgroup's items
-  while (true) {
-    // the next item is known before this one's last step: its first loads go out then, so they
-    // overlap this item's epilogue instead of starting an empty pipeline after it
-    const SkItem nxt = next_item();
-    const Src sn = make_src(nxt.valid ? nxt.t : cur.t);
-
-    // wave tile (BM / WM) x (BN / WN) as TM2 x TN2 blocks of 32 x 32 (v_mfma_f32_32x32x16_bf16);
-    // lane (r, g) = (lane % 32, lane / 32) of a fragment reads row r, chunk h + (BK / 16) g for the
-    // K slice h of 16 values (chunks {h, h + BK / 16}): each half-wave reads one chunk of 32
-    // consecutive rows, which the swizzle spreads over all banks (the 16 x 16 fragment order, 16
-    // rows of several chunks per half-wave, measured 2-way bank conflicts)
-    f32x16 acc[TM2][TN2];
-#pragma unroll
-    for (int i = 0; i < TM2; ++i)
-#pragma unroll
-      for (int j = 0; j < TN2; ++j) acc[i][j] = f32x16{};
-
-    // one K step: wait for this step's tile, then read fragments and multiply; `next` issues the
-    // following step's loads right after the last fragment reads (the LDS then serves the reads
-    // first and the MFMAs start sooner after the barrier)
-    auto step = [&](auto &&next) {
-      wait_vmem_le<0>();
-      __syncthreads();
-#pragma unroll
-      for (int h = 0; h < BK / 16; ++h) {
-        const int ch = h + (BK / 16) * g32;
-        bf16x8 fa[TM2], fb[TN2];
-#pragma unroll
-        for (int i = 0; i < TM2; ++i) {
-          const int r = wrow + i * 32 + r32;
-          fa[i] = *reinterpret_cast<const bf16x8 *>(&sA[buf][r * BK + ((ch ^ swz<BK>(r)) * 8)]);
-        }
-#pragma unroll
-        for (int j = 0; j < TN2; ++j) {
-          const int r = wcol + j * 32 + r32;
-          fb[j] = *reinterpret_cast<const bf16x8 *>(&sB[buf][r * BK + ((ch ^ swz<BK>(r)) * 8)]);
-        }
-        if (h == BK / 16 - 1) next();
-#pragma unroll
-        for (int i = 0; i < TM2; ++i)
-#pragma unroll
-          for (int j = 0; j < TN2; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[j], fa[i], acc[i][j], 0, 0, 0);
-      }
-      buf ^= 1;
-    };
-    // all steps but the last issue their successor unconditionally: no branch inside the loop
-    // body, so the scheduler overlaps each slice's fragment reads with the previous MFMAs
-    for (int kt = cur.kb; kt < cur.ke - 1; ++kt) step([&] { issue(sc, (kt + 1) * BK, buf ^ 1); });
-    step([&] {
-      if (nxt.valid) issue(sn, nxt.kb * BK, buf ^ 1);
-    });
-
-    if (cur.slot == nullptr) {
-      epilogue32<EPI, BM / WM, BN / WN>(p, sc.tr, sc.n0 + wcol, wrow, lane, acc);
-    } else {
-      // the partial tile in the 16 x 16 fragment layout k_gemm_fix reads: row 32 i + r is fragment
-      // row 2 i + r / 16; columns 32 j + 8 b + 4 g .. + 3 are lane r % 16 + 16 (2 (b % 2) + g) of
-      // fragment column 2 j + b / 2
-      float *base = cur.slot + (size_t(wid) * TM * TN * 64 + (r32 >> 4) * TN * 64 + (r32 & 15) + 16 * g32) * 4;
-#pragma unroll
-      for (int i = 0; i < TM2; ++i)
-#pragma unroll
-        for (int j = 0; j < TN2; ++j)
-#pragma unroll
-          for (int b = 0; b < 4; ++b)
-            *reinterpret_cast<f32x4 *>(base + ((2 * i * TN + 2 * j + b / 2) * 64 + 32 * (b % 2)) * 4) =
-                f32x4{acc[i][j][4 * b], acc[i][j][4 * b + 1], acc[i][j][4 * b + 2], acc[i][j][4 * b + 3]};
-    }
-    if (!nxt.valid) break;
-    cur = nxt;
-    sc = sn;
-  }
-}
 
 // ------------------------------------------------------------------- MFMA, 256 x 256 tiles
 //
@@ -1160,40 +931,7 @@ int device_cus() {
   return ncu[dev];
 }
 
-// Persistent workgroups of the bf16 GEMM: two per CU.
-int sk_workgroups() {
-  static int ncu[64] = {0};
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) dev = 0;
-  if (ncu[dev] == 0) {
-    int n = 0;
-    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
-      n = kSkMaxWorkgroups / 2;
-    ncu[dev] = n;
-  }
-  return 2 * ncu[dev] < kSkMaxWorkgroups ? 2 * ncu[dev] : kSkMaxWorkgroups;
-}
-
-template <int BM, int BN, int WM, int WN, int ROLE>
-static hipError_t run_bf16(const GemmProblem &p, hipStream_t st) {
-  static_assert(size_t(BM) * BN <= kSkPartFloats, "partial slot too small");
-  const int P = sk_workgroups();
-  hipLaunchKernelGGL((k_gemm_sk<BM, BN, WM, WN, role_epilogue(ROLE), ROLE>), dim3(P), dim3(WM * WN * 64), 0, st, p);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  // with at most B * (ceil(images * N / BM) + ceil(L / BM)) row tiles, a short-K problem below P
-  // tiles always runs unsplit and leaves no partials: no fixup launch
-  const long long tiles_max = (long long)p.B * ((p.max_img_rows + BM - 1) / BM + (p.L + BM - 1) / BM) *
-                              ((p.N + BN - 1) / BN);
-  if (tiles_max < P && p.K / 64 <= kNoSplitSteps) return hipSuccess;
-  // fewer than P tiles are ever left in partials; one fixup wave per (tile, wave, fragment row)
-  constexpr int kFixBlocks = (WM * WN) * (BM / WM / 16) / (kFixThreads / 64);
-  hipLaunchKernelGGL((k_gemm_fix<BM, BN, WM, WN, role_epilogue(ROLE), ROLE>), dim3(P * kFixBlocks), dim3(kFixThreads), 0,
-                     st, p, P);
-  return hipGetLastError();
-}
-
-// 256 x BN tiles: one persistent workgroup per CU.
+// Square TB x TB tiles: one persistent workgroup per CU.
 template <int TB, int ROLE, bool F8 = false>
 static hipError_t run_big(const GemmProblem &p, hipStream_t st) {
   constexpr int BM = TB, BN = TB;
@@ -1233,11 +971,8 @@ hipError_t launch_gemm(bool bf16, int role, const GemmProblem &p, hipStream_t st
   }
   // Tiling per projection, as measured on the 64 x 64 workload (2766 rows): QKV and MLP up run
   // 256 x 256 tiles (QKV: 396 tiles, two waves of whole tiles; MLP up: 528 tiles, two waves plus a
-  // short stream-K tail); the attention output and MLP down projections have only 132 such tiles
-  // for 256 CUs, so they would need split K with 256 KiB partials, and keep 128 x 128 tiles
-  // (528 of them for 512 workgroups).  256 x 128 tiles for these two (264 tiles: one wave and an
-  // 8-tile stream-K tail) measured slower than 128 x 128 (attention output 81 -> 88 us, MLP down
-  // 226 -> 234 us in isolation): with a 128 x 64 wave tile the stage reads more LDS per MFMA.
+  // short stream-K tail); the attention output and MLP down projections (N = 3072) run 192 x 192
+  // tiles, 240 of them: one wave on 256 CUs with no K split and no partials.
   switch (role) {
     case GEMM_QKV: return run_big<256, GEMM_QKV>(p, st);
     case GEMM_O: return run_big<192, GEMM_O>(p, st);

@@ -72,15 +72,11 @@ struct GemmProblem {
   const float *w_scale[2];  // ... and W row n of stream s is codes * w_scale[s][n]
 };
 
-// Partial-sum area of the bf16 GEMMs (part of the caller's workspace): one slot per data-parallel
-// unit of a split wave plus two per workgroup for its stream-K range.  128 x 128 tiles: two
-// workgroups per CU, at most 512; 256 x 256 tiles: one per CU, at most 256.
-constexpr int kSkMaxWorkgroups = 512;
+// Partial-sum area of the GEMMs (part of the caller's workspace): one slot per data-parallel unit
+// of a split wave plus two per workgroup for its stream-K range, one fp32 256 x 256 tile per slot,
+// one workgroup per CU (at most 256).
 constexpr int kBigMaxWorkgroups = 256;
-constexpr size_t kSkPartFloats = size_t(128) * 128;  // one 128 x 128 fp32 tile per slot
 constexpr size_t kSkPartBytes = size_t(kBigMaxWorkgroups) * 3 * 256 * 256 * sizeof(float);
-static_assert(size_t(kSkMaxWorkgroups) * 3 * kSkPartFloats * sizeof(float) <= kSkPartBytes,
-              "partial area must hold both tilings");
 hipError_t launch_gemm(bool bf16, int role, const GemmProblem &p, hipStream_t st);
 // FP8 E4M3 operands (A [Tmax][K] codes, W[s] [N][K] codes, per-row scales), bf16 bias; the
 // epilogue of the role (bf16 output or the float32 residual update); K % 128 == 0, N % 16 == 0.

@@ -211,15 +211,20 @@ def block_weights(rng: np.random.Generator, d: int, f: int, dtype: str) -> List[
     return out
 
 
-def modulation(rng: np.random.Generator, b: int, d: int) -> np.ndarray:
-    """adaLN modulation [B][2 streams][6][D]: shift, scale and gate all ~ N(0, 0.1).
+def modulation(rng: np.random.Generator, b: int, d: int, gate_std: float = 0.1) -> np.ndarray:
+    """adaLN modulation [B][2 streams][6][D]: shift and scale ~ N(0, 0.1), gate ~ N(0, gate_std)
+    (the same draws as gate_std = 0.1, the gates scaled).
 
     The gate scale sets how large the block's update is next to the residual stream (here a
     perturbation of ~20%).  It also sets the size of the unavoidable bf16 error: rounding the
     projection inputs (normalised rows, GELU activations) to bf16 costs ~0.1% of each update, so
     gates of std 0.3 would put even an exact emulation of the bf16 roundings at a max-abs error of
     ~0.024 against a float64 reference, above the 2e-2 bar; std 0.1 keeps it near 0.016."""
-    return rng.normal(0.0, 0.1, size=(b, 2, 6, d)).astype(np.float32)
+    m = rng.normal(0.0, 0.1, size=(b, 2, 6, d)).astype(np.float32)
+    if gate_std != 0.1:
+        m[:, :, 2] *= np.float32(gate_std / 0.1)
+        m[:, :, 5] *= np.float32(gate_std / 0.1)
+    return m
 
 
 # --------------------------------------------------------------------------------------------
@@ -307,9 +312,11 @@ def make_stack(name: str, n_blocks: int, steps: int, *, seed: Optional[int] = No
 
 
 def make_workload(name: str, *, with_block: bool = True, keep_frac: Optional[float] = None,
-                  seed: Optional[int] = None, shape: Optional[BlockShape] = None) -> Workload:
+                  seed: Optional[int] = None, shape: Optional[BlockShape] = None,
+                  gate_std: float = 0.1) -> Workload:
     """Build the named workload.  `keep_frac` overrides the kept-fine block fraction of every grid
-    (used for the dense baseline, keep_frac=1, and the kept-fraction sweep)."""
+    (used for the dense baseline, keep_frac=1, and the kept-fraction sweep); `gate_std` the
+    standard deviation of the adaLN gates."""
     shp = shape or SHAPES[name]
     ss = np.random.SeedSequence(seed if seed is not None else _SEED.get(name, 3000))
     (c_bg, c_noise, c_reg, c_tex, c_txt, c_w, c_mod, c_mask, c_frac) = [
@@ -354,6 +361,6 @@ def make_workload(name: str, *, with_block: bool = True, keep_frac: Optional[flo
     weights = mod = None
     if with_block:
         weights = block_weights(c_w, d, shp.mlp_dim, shp.dtype)
-        mod = modulation(c_mod, B, d)
+        mod = modulation(c_mod, B, d, gate_std)
     return Workload(name, shp, _store(x, shp.dtype), _store(x_txt, shp.dtype), force, keep,
                     dilate_r, weights, mod)

@@ -75,7 +75,8 @@ class DeviceBlock:
                            self.counts, self.cu, self.seg, self.z, stream)
 
     def prepare_fp8(self, stream=None):
-        """FP8 codes and per-output-channel scales of W_qkv and W1 (once; weights are static)."""
+        """FP8 codes and per-output-channel scales of the four projection weights (once; weights
+        are static)."""
         if getattr(self, "weights8", None) is None:
             self.weights8 = hilo.quantize_fp8_weights(self.weights, stream)
             self.aw8 = hilo.attn_weights_fp8(self.weights8)
@@ -106,7 +107,7 @@ class DeviceBlock:
     def run(self, mode: int = hilo.TOPK, keep=None, tau=None, dilate_r=None, stream=None,
             tokens: int = hilo.PARTITION, delta: bool = False, fp8: bool = False):
         """One pass of the whole hot path: score, select, compress, attention, MLP, decompress
-        (fp8: the QKV and MLP-up projections in FP8)."""
+        (fp8: all four projections on FP8 operands)."""
         self.score(stream)
         self.select(mode, keep, tau, dilate_r, stream, tokens)
         self.compress(stream)

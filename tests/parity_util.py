@@ -11,14 +11,22 @@ from paper_2606_13898_amd.pipeline import DeviceBlock
 #  bf16 storage: max-abs 2e-2 and relative L2 5e-3 (the target stated for this block).
 #  f32 storage: max-abs 1e-4 and relative L2 1e-5 -- fp32 products over K <= 4096 terms of O(1)
 #  values carry a rounding error of order sqrt(K) * 2^-24 * |terms| ~ 1e-6 relative.
-#  fp8 (the FP8 block against the FP8 oracle): max-abs 6e-2 and relative L2 1e-2.  The block takes
-#  its E4M3 decisions on operands that carry the device's bf16 rounding (q, k, v and the stored
-#  activations); an operand one bf16 ulp (2^-8) away from the oracle's crosses an E4M3 rounding
-#  midpoint with probability ~2^-4 and then moves by one E4M3 step (2^-3 relative), so a few percent
-#  of the codes move and a projection's output deviates by ~sqrt(p) 2^-3 ~ 1-3% of its RMS (measured:
-#  0.5% on hidden size 256, 1-3% on 4608) -- about three times the bf16 path's deviation in z.  The
-#  FP8 kernels themselves are checked exactly on the device's own operands (codes bit for bit).
+#  fp8 (the FP8 block against the oracle's FP8 block, which quantises the exact activations):
+#  max-abs 6e-2 and relative L2 1e-2, a statistical bound derived from the arithmetic.  E4M3 keeps
+#  3 mantissa bits, a relative step s of 2^-4 .. 2^-3 (~2^-3.5).  The activations the output and
+#  down projections quantise (attention output, GELU output) carry the device's bf16-level rounding
+#  (q, k, v, probabilities, the stored row: relative noise d ~ 2 * 2^-9 / sqrt(3) ~ 2.3e-3), so a
+#  code flips to its neighbour with probability p ~ 2 d / s ~ 5%, and the projection's output moves
+#  by ~sqrt(p) s ~ 2% of its RMS.  The update is ~20% of z (gates N(0, 0.1)): relative L2 on z
+#  ~ 0.2 * sqrt(2) * 2% ~ 0.6% (bound 1e-2); max-abs ~ a few sigma of 2% of the update plus the
+#  bf16 output rounding (0.0156 below 8) (bound 6e-2).  The FP8 kernels themselves are checked
+#  exactly on the device's own operands (codes bit for bit, outputs to float32 accumulation).
+#  update: the block's own change of z (z1 - Z, z2 - z1), relative L2 1e-2 -- the roundings of its
+#  bf16 operands (h, q/k/v, probabilities, a, the GELU output; each 2^-9 / sqrt(3) relative RMS)
+#  add up to ~0.3% of the update, and the residual stream no longer dilutes the comparison;
+#  float32 workloads 1e-4 (float32 products and softmax, ~1e-5 of the update).
 TOL = {"bf16": (2e-2, 5e-3), "f32": (1e-4, 1e-5), "fp8": (6e-2, 1e-2)}
+UPDATE_REL = {"bf16": 1e-2, "f32": 1e-4}
 
 
 def float_report(got, want):
@@ -88,3 +96,41 @@ def midpoint_tau(E, force, shape, r, keep):
         else:
             taus.append(0.5 * (float(vals[k - 1]) + float(vals[k])))
     return taus
+
+
+def assert_update_close(got, want, base_got, base_want, dtype, what=""):
+    """The block's update of the residual stream, got - base_got against want - base_want: its
+    relative L2 error (UPDATE_REL) with the residual stream taken out."""
+    du = np.asarray(got, np.float64) - np.asarray(base_got, np.float64)
+    dw = np.asarray(want, np.float64) - np.asarray(base_want, np.float64)
+    max_abs, rel = float_report(du, dw)
+    lim = UPDATE_REL[dtype]
+    print(f"[update] {what}: rel_l2 {rel:.3g} (<= {lim}), max_abs {max_abs:.3g}", flush=True)
+    assert np.isfinite(du).all(), f"{what}: non-finite update"
+    assert rel <= lim, f"{what}: update rel_l2 {rel:.3g} (<= {lim})"
+    return max_abs, rel
+
+
+def check_compressed(z_dev, ref, wl):
+    """The compressed sequence: fine and text rows are copies of their input rows (float32 widening
+    of the stored values), so bit for bit; a pooled row is ((x00 + x01) + (x10 + x11)) * 0.25 in
+    float32, within three float32 roundings of the exact mean (2^-22 of the mean of |x|)."""
+    s = wl.shape
+    z = np.asarray(z_dev, dtype=np.float64)
+    Z = ref["Z"]
+    W2, W = s.grid_w // 2, s.grid_w
+    for g in range(s.grids):
+        nf, npool = (int(v) for v in ref["counts"][g])
+        base = int(ref["seg"][g])
+        np.testing.assert_array_equal(z[base:base + nf], Z[base:base + nf], err_msg=f"grid {g} fine rows")
+        b = ref["pool_idx"][g, :npool].astype(np.int64)
+        p00 = (b // W2) * 2 * W + (b % W2) * 2
+        x = np.abs(wl.x_img[g].astype(np.float64))
+        mag = (x[p00] + x[p00 + 1] + x[p00 + W] + x[p00 + W + 1]) / 4.0
+        pooled = slice(base + nf, base + nf + npool)
+        bad = np.abs(z[pooled] - Z[pooled]) > 2.0 ** -22 * mag
+        assert not bad.any(), f"grid {g}: {int(bad.sum())} pooled values off by more than float32 rounding"
+    L = s.text_len
+    for b_ in range(s.batch):
+        hi = int(ref["cu"][b_ + 1])
+        np.testing.assert_array_equal(z[hi - L:hi], Z[hi - L:hi], err_msg=f"sample {b_} text rows")

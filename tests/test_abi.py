@@ -31,7 +31,7 @@ def test_exports_every_declared_symbol():
 
 
 def test_version_and_status_strings():
-    assert hilo.hilo_abi_version() == 4
+    assert hilo.hilo_abi_version() == 5
     for st in range(7):
         assert hilo.status_str(st)
     assert hilo.status_str(99) == "unknown status"
@@ -207,9 +207,10 @@ def test_fp8_validation():
     aw = (hilo.hilo_attn_w_fp8 * 2)(*[hilo.hilo_attn_w_fp8(*[FAKE] * 6)] * 2)
     mw = (hilo.hilo_mlp_w_fp8 * 2)(*[hilo.hilo_mlp_w_fp8(*[FAKE] * 6)] * 2)
     need8 = hilo.hilo_workspace_bytes_fp8(s)
-    assert need8 > need  # the hidden rows' codes and scales come on top
-    T, F = hilo.hilo_max_tokens(s), s.mlp_dim
-    assert need8 == need + -(-T * F // 256) * 256 + -(-T * 4 // 256) * 256
+    assert need8 > need  # one more region on top: the attention output, later the hidden rows' codes
+    T, F, D = hilo.hilo_max_tokens(s), s.mlp_dim, s.dim
+    up = lambda x: -(-x // 256) * 256  # noqa: E731
+    assert need8 == need + max(up(T * F) + up(T * 4), up(T * D * 2))
     f = good_shape(hilo.F32)
     assert L.hilo_attention_fp8(ctypes.byref(f), FAKE, FAKE, aw, FAKE, FAKE, 1 << 40, None) == 3
     assert L.hilo_mlp_fp8(ctypes.byref(f), FAKE, FAKE, mw, FAKE, FAKE, 1 << 40, None) == 3
@@ -226,6 +227,7 @@ def test_fp8_validation():
     bad_mw[0] = hilo.hilo_mlp_w_fp8(FAKE, None, FAKE, FAKE, FAKE, FAKE)
     assert L.hilo_mlp_fp8(ctypes.byref(s), FAKE, FAKE, bad_mw, FAKE, FAKE, need8, None) == 1
     assert L.hilo_attention_fp8(ctypes.byref(s), FAKE, FAKE, aw, FAKE, FAKE, 100, None) == 5
+    assert L.hilo_attention_fp8(ctypes.byref(s), FAKE, FAKE, aw, FAKE, FAKE, need8 - 1, None) == 5
     assert L.hilo_mlp_fp8(ctypes.byref(s), FAKE, FAKE, mw, FAKE, FAKE, need8 - 1, None) == 5
     assert L.hilo_attention_fp8(ctypes.byref(s), None, FAKE, aw, FAKE, FAKE, need, None) == 1
     q = L.hilo_quantize_rows
@@ -238,5 +240,5 @@ def test_fp8_validation():
     assert q(hilo.F32, FAKE, 0, 8, FAKE, FAKE, None) == 0    # nothing to do
     if not torch.cuda.is_available():
         assert q(hilo.F32, FAKE, 4, 8, FAKE, FAKE, None) == 6
-        assert L.hilo_attention_fp8(ctypes.byref(s), FAKE, FAKE, aw, FAKE, FAKE, need, None) == 6
+        assert L.hilo_attention_fp8(ctypes.byref(s), FAKE, FAKE, aw, FAKE, FAKE, need8, None) == 6
         assert L.hilo_mlp_fp8(ctypes.byref(s), FAKE, FAKE, mw, FAKE, FAKE, need8, None) == 6

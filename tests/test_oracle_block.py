@@ -184,3 +184,29 @@ def test_tiny_workload_pipeline_runs_and_guards_range():
     assert res["counts"][0].tolist() == [4 * 77, 256 - 77]
     assert res["cu"][-1] == 4 * 77 + 256 - 77 + 64  # 551 tokens
     assert np.abs(res["y_img"]).max() < 8.0  # bf16 tolerance is attainable only below 8
+
+
+def test_attention_core_on_packed_rows_is_per_sample_sdpa():
+    """The oracle's attention step on a packed ragged [T][3D] projection: every row attends to the
+    rows of its own sample only, so it must equal torch's float64 scaled_dot_product_attention run
+    on each sample's slice alone; with `rows` it returns exactly those rows of that result, in the
+    order asked for."""
+    rng = np.random.default_rng(77)
+    heads, hd = 3, 8
+    D = heads * hd
+    lens = [1, 7, 13, 2]
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    T = int(cu[-1])
+    qkv = rng.standard_normal((T, 3 * D))
+    want = np.empty((T, D))
+    for s in range(len(lens)):
+        lo, hi = int(cu[s]), int(cu[s + 1])
+        x = torch.from_numpy(qkv[lo:hi])
+        q, k, v = (x[:, i * D:(i + 1) * D].reshape(hi - lo, heads, hd).transpose(0, 1) for i in range(3))
+        want[lo:hi] = F.scaled_dot_product_attention(q[None], k[None], v[None])[0].transpose(0, 1).reshape(hi - lo, D).numpy()
+    got = O.attention_core(qkv, cu, heads)
+    np.testing.assert_allclose(got, want, rtol=0, atol=1e-12)
+    rows = np.array([20, 0, 8, 21, 7, 13])
+    np.testing.assert_allclose(O.attention_core(qkv, cu, heads, rows), want[rows], rtol=0, atol=1e-12)
+    # a one-row sample returns its own value row
+    np.testing.assert_allclose(got[0], qkv[0, 2 * D:], rtol=0, atol=1e-12)

@@ -12,7 +12,7 @@ from oracle import hilo_oracle as O
 from paper_2606_13898_amd import hilo, inputs
 from paper_2606_13898_amd.pipeline import DeviceBlock
 
-from parity_util import assert_close, check_selection, oracle_for, to_np
+from parity_util import assert_close, assert_update_close, check_compressed, check_selection, oracle_for, to_np
 
 pytestmark = pytest.mark.gpu
 
@@ -34,20 +34,38 @@ def _sample_rows(counts, cu, seg, images, L, per_seg=6, seed=0):
     return np.array(sorted(set(int(r) for r in rows)))
 
 
-@pytest.mark.parametrize("name", ["m1024", "edit", "h2048", "ragged"])
-def test_full_size_parity_sampled(name):
-    print(f"[parity-full] workload={name}", flush=True)
+@pytest.mark.parametrize("name,r", [("m1024", 0), ("edit", 0), ("edit", 1), ("h2048", 0), ("ragged", 0)],
+                         ids=["m1024", "edit", "edit_r1", "h2048", "ragged"])
+def test_full_size_parity_sampled(name, r):
+    """(edit, r = 1): the edit mask dilated by one patch before it forces blocks fine."""
+    print(f"[parity-full] workload={name} dilate_r={r}", flush=True)
     wl = inputs.make_workload(name)
     s = wl.shape
     db = DeviceBlock(wl)
-    db.run(hilo.TOPK)
+    db.score()
+    db.select(hilo.TOPK, dilate_r=r)
+    db.compress()
     torch.cuda.synchronize()
-    front = oracle_for(wl, with_block=False)
+    front = oracle_for(wl, r=r, with_block=False)
     check_selection(db, front)
-    print(f"[parity-full] {name}: selection bit-exact, tokens {int(front['cu'][-1])}", flush=True)
+    T = int(front["cu"][-1])
+    check_compressed(to_np(db.z)[:T], front, wl)
+    print(f"[parity-full] {name}: selection bit-exact, compressed rows exact, tokens {T}", flush=True)
     rows = _sample_rows(front["counts"], front["cu"], front["seg"], s.images, s.text_len)
+    z0_dev = to_np(db.z)[rows].astype(np.float64)
+    db.attention()
+    torch.cuda.synchronize()
+    z1_dev = to_np(db.z)[rows].astype(np.float64)
+    db.mlp()
+    torch.cuda.synchronize()
+    z2_dev = to_np(db.z)[rows].astype(np.float64)
+    db.decompress()
+    torch.cuda.synchronize()
     z1, z2 = O.block(front["Z"], front["cu"], s.text_len, s.heads, wl.weights, wl.mod, rows)
     assert np.abs(z2).max() < 8.0
+    # each half's own update of the sampled rows, the residual stream taken out
+    assert_update_close(z1_dev, z1, z0_dev, front["Z"][rows], "bf16", f"{name} attention update")
+    assert_update_close(z2_dev, z2, z1_dev, z1, "bf16", f"{name} mlp update")
     # y at every patch whose compressed row was sampled, and text rows
     y = to_np(db.y_img)
     got, want = [], []

@@ -9,22 +9,18 @@ from oracle import hilo_oracle as O
 from paper_2606_13898_amd import hilo, inputs
 from paper_2606_13898_amd.pipeline import DeviceBlock, DeviceStack
 
-from parity_util import assert_close, check_selection, midpoint_tau, oracle_for, to_np
+from parity_util import (assert_close, assert_update_close, check_compressed, check_selection,
+                         float_report, midpoint_tau, oracle_for, to_np)
 
 pytestmark = pytest.mark.gpu
 
 SMALL = ["tiny", "small128", "small64", "smallf32"]
 
 
-def _stage_compare(db, ref, dtype, tag):
-    T = int(ref["cu"][-1])
-    assert_close(to_np(db.z)[:T], ref["Z"], dtype, f"{tag} Z after compress")
-
-
-@pytest.mark.parametrize("name", SMALL)
-def test_pipeline_parity(name):
-    print(f"[parity] workload={name}", flush=True)
-    wl = inputs.make_workload(name)
+def _block_stages(name, wl, check_z=True):
+    """Score, select and compress, then the block one half at a time: the selection bit for bit,
+    the compressed sequence bit for bit (pooled rows to float32 rounding), each half's update of z
+    against the oracle's update, z and y against the oracle."""
     dt = wl.shape.dtype
     db = DeviceBlock(wl)
     ref = oracle_for(wl)
@@ -34,18 +30,46 @@ def test_pipeline_parity(name):
     torch.cuda.synchronize()
     check_selection(db, ref)
     T = int(ref["cu"][-1])
-    assert_close(to_np(db.z)[:T], ref["Z"], "f32", f"{name} Z after compress")
+    z0 = to_np(db.z)[:T].copy()
+    check_compressed(z0, ref, wl)
     db.attention()
     torch.cuda.synchronize()
-    assert_close(to_np(db.z)[:T], ref["z1"], dt, f"{name} z after attention")
+    z1 = to_np(db.z)[:T].copy()
+    assert_update_close(z1, ref["z1"], z0, ref["Z"], dt, f"{name} attention update z1 - Z")
+    if check_z:
+        assert_close(z1, ref["z1"], dt, f"{name} z after attention")
     db.mlp()
     torch.cuda.synchronize()
-    assert_close(to_np(db.z)[:T], ref["z2"], dt, f"{name} z after mlp")
+    z2 = to_np(db.z)[:T].copy()
+    assert_update_close(z2, ref["z2"], z1, ref["z1"], dt, f"{name} mlp update z2 - z1")
+    if check_z:
+        assert_close(z2, ref["z2"], dt, f"{name} z after mlp")
     db.decompress()
     torch.cuda.synchronize()
+    return db, ref
+
+
+@pytest.mark.parametrize("name", SMALL)
+def test_pipeline_parity(name):
+    print(f"[parity] workload={name}", flush=True)
+    wl = inputs.make_workload(name)
+    dt = wl.shape.dtype
+    db, ref = _block_stages(name, wl)
     assert_close(to_np(db.y_img), ref["y_img"], dt, f"{name} y_img")
     assert_close(to_np(db.y_txt), ref["y_txt"], dt, f"{name} y_txt")
     assert np.abs(ref["y_img"]).max() < 8.0
+
+
+def test_pipeline_parity_gate_std_0_3():
+    """adaLN gates ~ N(0, 0.3): the block's update is ~3x larger next to the residual stream.  The
+    output's own bf16 rounding then takes most of the max-abs bar wherever |y| reaches [4, 8), so
+    this workload is judged on each half's update (relative L2) and on y's relative L2."""
+    print("[parity] workload=small128 gate std 0.3", flush=True)
+    wl = inputs.make_workload("small128", gate_std=0.3)
+    db, ref = _block_stages("small128 gate 0.3", wl, check_z=False)
+    _, rel = float_report(to_np(db.y_img), ref["y_img"])
+    print(f"[parity] gate 0.3 y_img rel_l2 {rel:.3g}", flush=True)
+    assert rel <= 5e-3
 
 
 @pytest.mark.parametrize("name", ["tiny", "small128", "small64"])
@@ -290,8 +314,10 @@ def test_token_sets(name, tokens, delta):
     inputs.BlockShape(1, 1, 64, 64, 512, 3072, 24, 128, 12288, "bf16"),  # the 1024 px image
 ], ids=["8x10", "batch2x2_16x20", "1024px"])
 def test_pixel_score_and_paper_threshold(shp):
-    """Sobel on the RGB image summed per token (bit for bit), then the paper's threshold 0.1 on the
-    normalised map selects the same blocks as the oracle."""
+    """Sobel on the RGB image summed per token (bit for bit), then the threshold selects the same
+    blocks as the oracle.  The paper cuts its normalised Sobel magnitude map at 0.1; the energy is
+    the magnitude squared, so the counterpart on the normalised energy map is 0.1^2 = 0.01 (exact
+    where a token's magnitude is uniform; the mean of squares weights strong edges more)."""
     print(f"[parity] pixel score {shp.grid_h}x{shp.grid_w} grids={shp.grids}", flush=True)
     rgb = inputs.pixel_image(shp, 41)
     H, W, G, N = shp.grid_h, shp.grid_w, shp.grids, shp.n_patches
@@ -302,7 +328,7 @@ def test_pixel_score_and_paper_threshold(shp):
     hilo.hilo_score_pixels(shape, rgb_d, E)
     torch.cuda.synchronize()
     np.testing.assert_array_equal(to_np(E), want)
-    tau = [0.1] * G
+    tau = [0.01] * G
     fine = O.select(want, None, H, W, 0, "threshold", tau=tau)
     idx_map, _, _, counts = O.compact(fine, H, W)
     i32 = dict(dtype=torch.int32, device="cuda")
