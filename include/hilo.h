@@ -285,6 +285,20 @@ hilo_status hilo_attention_core(const hilo_shape *shape, const void *qkv,
                                 const int32_t *cu_seqlens, void *out, void *workspace,
                                 size_t ws_bytes, void *stream);
 
+/* hilo_attention_core without a workspace, for callers that cannot allocate device memory (code
+ * under HIP graph capture, serving loops and harnesses that forbid hipMalloc): the same kernels and
+ * launch, with the stream-K partial results in a scratch array the library holds on each device
+ * it runs on (HILO_ATTN_SCRATCH_BYTES, set up on the first call on a device, kept until the process
+ * ends).  It calls no allocating routine.  Nothing in the scratch needs clearing between calls,
+ * but every call on one device shares it: calls that overlap on one device (on different streams,
+ * or from several host threads) race and give undefined results.  The core sizes its launch so
+ * that its partial results fit the scratch at any sequence length; HILO_E_WORKSPACE reports a
+ * breach of that bound, HILO_E_DEVICE a failed lookup of the scratch; other statuses as
+ * hilo_attention_core.  No kernel timing.                                                       */
+#define HILO_ATTN_SCRATCH_BYTES ((size_t)72 * 1024 * 1024)
+hilo_status hilo_attention_core_noalloc(const hilo_shape *shape, const void *qkv,
+                                        const int32_t *cu_seqlens, void *out, void *stream);
+
 size_t hilo_workspace_bytes(const hilo_shape *shape); /* 0 if the shape is invalid */
 /* T_max = batch * (images * (N + N/4) + text_len): the most rows any token set can produce
  * (OVERLAP with every block kept); z and the workspace are sized for it, -1 if invalid.         */

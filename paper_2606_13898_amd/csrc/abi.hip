@@ -1,6 +1,7 @@
 // C ABI of libhilo: argument validation, workspace layout, kernel sequencing and the optional
 // per-kernel event timing.  Nothing here allocates device memory or synchronises.
 #include <cmath>
+#include <mutex>
 #include <vector>
 
 #include "../../include/hilo.h"
@@ -321,6 +322,61 @@ hilo_status hilo_attention_core(const hilo_shape *s, const void *qkv, const int3
                             reinterpret_cast<float *>(workspace), s->batch, s->heads, s->head_dim,
                             max_seq, st);
   }));
+}
+
+}  // extern "C"
+
+// ----------------------------------------------------------------- allocation-free attention core
+
+// Scratch of hilo_attention_core_noalloc: the attention core's stream-K partial results, in a
+// device array of the library's own (each GPU the library runs on holds one copy, allocated when
+// the library's code is loaded there and kept until the process ends).  Host code never passes
+// `scratch` itself to a kernel (on the host the name is only a stand-in for the symbol): it passes
+// the device address hipGetSymbolAddress returns for the current device.
+static __device__ __align__(256) uint8_t scratch[HILO_ATTN_SCRATCH_BYTES];
+static_assert(HILO_ATTN_SCRATCH_BYTES >= kAttnPartBytes, "scratch smaller than the attention partials");
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's address of `scratch`, looked up once per device (with that device current:
+// every device has its own copy at its own address); nullptr if the lookup fails.
+void *scratch_ptr() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void *ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || ptr == nullptr) return nullptr;
+    g_scratch_ptr[dev] = ptr;
+  }
+  return g_scratch_ptr[dev];
+}
+
+}  // namespace
+
+extern "C" {
+
+hilo_status hilo_attention_core_noalloc(const hilo_shape *s, const void *qkv,
+                                        const int32_t *cu_seqlens, void *out, void *stream) {
+  hilo_status e = check_block(s);
+  if (e != HILO_OK) return e;
+  if (!qkv || !cu_seqlens || !out) return HILO_E_NULL;
+  if (!have_device()) return HILO_E_DEVICE;
+  const bool bf = s->dtype == HILO_BF16;
+  if (attention_part_bytes(bf, s->head_dim) > HILO_ATTN_SCRATCH_BYTES) return HILO_E_WORKSPACE;
+  float *part = nullptr;
+  if (bf) {
+    part = reinterpret_cast<float *>(scratch_ptr());
+    if (!part) return HILO_E_DEVICE;
+  }
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  const int max_seq = int(s->images * grid_rows_max(s) + s->text_len);
+  return dev_status(launch_attention(bf, qkv, cu_seqlens, out, part, s->batch, s->heads, s->head_dim,
+                                     max_seq, st));
 }
 
 }  // extern "C"

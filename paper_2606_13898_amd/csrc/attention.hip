@@ -624,6 +624,12 @@ static hipError_t run_attn_f32(const void *qkv, const int *cu, void *out, int B,
   return hipGetLastError();
 }
 
+size_t attention_part_bytes(bool bf16, int hd) {
+  if (!bf16) return 0;
+  const size_t slot = hd == 128 ? AttnShape<128, 32, 8>::kSlotFloats : AttnShape<64, 32, 4>::kSlotFloats;
+  return size_t(2) * attn_workgroups(hd == 128 ? 1 : 2, slot) * slot * sizeof(float);
+}
+
 hipError_t launch_attention(bool bf16, const void *qkv, const int *cu, void *out, float *part, int B,
                             int heads, int hd, int max_seq, hipStream_t st) {
   if (bf16) {

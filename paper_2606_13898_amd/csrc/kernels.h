@@ -92,5 +92,8 @@ constexpr size_t kAttnPartBytes = size_t(kAttnMaxWorkgroups) * 2 * kAttnSlotFloa
 // device scratch for the bf16 path (unused by the fp32 path).
 hipError_t launch_attention(bool bf16, const void *qkv, const int *cu, void *out, float *part, int B,
                             int heads, int hd, int max_seq, hipStream_t st);
+// Bytes of partial results launch_attention uses on the current device (0 for the fp32 path);
+// never more than kAttnPartBytes.
+size_t attention_part_bytes(bool bf16, int hd);
 
 }  // namespace hilo

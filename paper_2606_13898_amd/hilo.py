@@ -78,6 +78,7 @@ _SIG = {
                     ctypes.POINTER(hilo_mlp_w), _P, ctypes.c_int32, _P, ctypes.c_size_t, _P],
     "hilo_decompress": [ctypes.POINTER(hilo_shape), _P, _P, _P, _P, _P, _P, _P],
     "hilo_attention_core": [ctypes.POINTER(hilo_shape), _P, _P, _P, _P, ctypes.c_size_t, _P],
+    "hilo_attention_core_noalloc": [ctypes.POINTER(hilo_shape), _P, _P, _P, _P],
     "hilo_workspace_bytes": [ctypes.POINTER(hilo_shape)],
     "hilo_workspace_bytes_fp8": [ctypes.POINTER(hilo_shape)],
     "hilo_max_tokens": [ctypes.POINTER(hilo_shape)],
@@ -317,6 +318,11 @@ def hilo_attention_core(shape, qkv, cu_seqlens, out, workspace=None, stream=None
     _check("hilo_attention_core", lib().hilo_attention_core(
         ctypes.byref(shape), _ptr(qkv), _ptr(cu_seqlens), _ptr(out), _ptr(workspace), ws_bytes,
         _stream(stream)))
+
+
+def hilo_attention_core_noalloc(shape, qkv, cu_seqlens, out, stream=None):
+    _check("hilo_attention_core_noalloc", lib().hilo_attention_core_noalloc(
+        ctypes.byref(shape), _ptr(qkv), _ptr(cu_seqlens), _ptr(out), _stream(stream)))
 
 
 def hilo_profile_enable(on: bool):
