@@ -2,9 +2,13 @@
 """Benchmark of the HiLo-Token compressed DiT block on one MI355X.
 
 One step = one pass of the whole hot path over one batch: score, select, compress, attention,
-MLP, decompress (six C-ABI calls, all kernels on the GPU), inputs resident in HBM.  Prints ONE JSON
-line with the step latency, throughput, the dense (uncompressed) block for the speedup, per-kernel
-times from HIP events with their roofline fractions, and the CPU oracle timed on a bounded sample.
+MLP, decompress (six C-ABI calls, all kernels on the GPU), inputs resident in HBM.  Consecutive
+steps read different copies of the step's inputs (latents and text tokens, more than 512 MB in
+all) and alternate between two copies of the block's weights, so no step finds its operands in the
+256 MB last-level cache (MALL) from an earlier step.  Prints ONE JSON line with the step latency,
+throughput, the dense (uncompressed) block for the speedup, per-kernel times from HIP events with
+their roofline fractions, the other workloads and a kept-fraction sweep, and the CPU oracle timed
+on a bounded sample.
 
     python bench.py [--steps K] [--warmup W] [--workload m1024] [--no-cpu-baseline]
 """
@@ -90,28 +94,257 @@ def traffic_for(kind):
     return ent["bytes_per_launch"]
 
 
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(wl):
-    """The oracle, untuned, on one full step of the same workload (bounded: ~10-30 s)."""
+    """The oracle, untuned, on one full step of the same workload (bounded: ~10-30 s), its BLAS
+    threads set to the cores this process may run on."""
     import threadpoolctl
 
     from oracle import hilo_oracle as O
 
-    info = threadpoolctl.threadpool_info()
-    threads = max([i.get("num_threads", 1) for i in info if i.get("user_api") == "blas"] or [1])
-    t0 = time.perf_counter()
-    O.pipeline(wl.x_img, wl.x_txt, wl.shape, wl.force, wl.dilate_r, "topk", keep=wl.keep,
-               weights=wl.weights, mod=wl.mod)
-    dt = time.perf_counter() - t0
+    cores = len(os.sched_getaffinity(0))
+    with threadpoolctl.threadpool_limits(limits=cores, user_api="blas"):
+        info = threadpoolctl.threadpool_info()
+        threads = max([i.get("num_threads", 1) for i in info if i.get("user_api") == "blas"] or [1])
+        t0 = time.perf_counter()
+        O.pipeline(wl.x_img, wl.x_txt, wl.shape, wl.force, wl.dilate_r, "topk", keep=wl.keep,
+                   weights=wl.weights, mod=wl.mod)
+        dt = time.perf_counter() - t0
     return {"value": round(dt * 1e3, 1), "unit": "ms", "cores": int(threads), "kind": "oracle",
             "sample": f"one full step (score..decompress) of the {wl.name} workload in float64 "
-                      f"numpy, BLAS threads={threads}"}
+                      f"numpy (matrix products on BLAS with {threads} threads, "
+                      f"{cores} cores in this process's affinity)",
+            "cpu_model": cpu_model(), "affinity_cores": cores}
+
+
+class Rotation:
+    """Copies of a step's inputs for MALL-proof timing: R copies of (x_img, x_txt) totalling more
+    than `min_bytes`, and two copies of the block weights; step k reads input copy k % R and weight
+    copy k % 2."""
+
+    def __init__(self, db, min_bytes=512 << 20, weight_sets=None):
+        import math
+
+        per = db.x_img.numel() * db.x_img.element_size()
+        if db.x_txt is not None:
+            per += db.x_txt.numel() * db.x_txt.element_size()
+        self.R = max(3, math.ceil(min_bytes / per))
+        self.xs = [(db.x_img, db.x_txt)] + [
+            (db.x_img.clone(), db.x_txt.clone() if db.x_txt is not None else None) for _ in range(self.R - 1)]
+        self.bytes = per * self.R
+        self.ws = weight_sets if weight_sets is not None else ([(db.aw, db.mw)] if db.with_block else [])
+
+    @staticmethod
+    def weight_sets(db):
+        from paper_2606_13898_amd import hilo
+
+        w2 = [{k: v.clone() for k, v in w.items()} for w in db.weights]
+        return [(db.aw, db.mw), (hilo.attn_weights(w2), hilo.mlp_weights(w2))], w2
+
+    def use(self, db, k):
+        db.x_img, db.x_txt = self.xs[k % self.R]
+        if self.ws:
+            db.aw, db.mw = self.ws[k % len(self.ws)]
+
+
+def timed(stream, steps, fn):
+    """Runs fn(k) for k < steps with an event between consecutive calls: (mean ms, sorted ms)."""
+    import numpy as np
+    import torch
+
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    torch.cuda.synchronize()
+    evs[0].record(stream)
+    for k in range(steps):
+        fn(k)
+        evs[k + 1].record(stream)
+    torch.cuda.synchronize()
+    return evs[0].elapsed_time(evs[-1]) / steps, np.sort([evs[k].elapsed_time(evs[k + 1]) for k in range(steps)])
+
+
+def kernel_profile(steps, fn, work):
+    """The same calls again with the library's event pairs around every kernel: per kernel kind the
+    mean duration and, where the algorithmic work is known, the achieved rate and roofline fraction."""
+    import torch
+
+    from paper_2606_13898_amd import hilo
+
+    hilo.hilo_profile_enable(True)
+    for k in range(steps):
+        fn(k)
+    torch.cuda.synchronize()
+    kinds = {hilo.hilo_profile_name(k): hilo.hilo_profile_read(k) for k in range(hilo.hilo_profile_kinds())}
+    hilo.hilo_profile_enable(False)
+    kern = {}
+    for name, (tot, n) in kinds.items():
+        if n == 0:
+            continue
+        avg = tot / n
+        ent = {"ms": round(avg, 4), "launches_per_step": n // steps}
+        if name in work:
+            amt, unit, peak = work[name]
+            ach = amt / (avg * 1e-3)  # GB/s or TFLOP/s
+            ent.update(achieved=round(ach, 1), unit=unit + "/s", peak=peak,
+                       frac=round(ach / peak, 4), work_per_launch=f"{amt:.4g} {unit}")
+        kern[name] = ent
+    return kern
+
+
+BLOCK_KERNELS = ("rownorm_attn", "gemm_qkv", "attention_core", "gemm_o", "rownorm_mlp", "gemm_fc1", "gemm_fc2")
+
+
+def block_flops(shape, seqlens):
+    """Algorithmic FLOPs of the block on packed samples of the given lengths: the four projections
+    (2 n D (3D + D + F + F)) and the attention core (4 n^2 D per sample)."""
+    import numpy as np
+
+    n = np.asarray(seqlens, dtype=np.float64)
+    D, F = shape.dim, shape.mlp_dim
+    return float(2.0 * n.sum() * D * (4 * D + 2 * F) + 4.0 * (n ** 2).sum() * D)
+
+
+def dense_block_ms(db, rot, steps, warmup, stream, dilate_r=None):
+    """The block (attention + MLP) on the uncompressed sequence: every block kept fine (the dense
+    token order), timed per step around the two calls."""
+    import torch
+
+    from paper_2606_13898_amd import hilo
+
+    s = db.wl.shape
+    db.score()
+    db.select(hilo.TOPK, keep=[s.n_blocks] * s.grids, dilate_r=dilate_r)
+    for k in range(warmup):
+        rot.use(db, k)
+        db.compress()
+        db.attention()
+        db.mlp()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    for k, (a, b) in enumerate(ev):
+        rot.use(db, k)
+        db.compress()
+        a.record(stream)
+        db.attention()
+        db.mlp()
+        b.record(stream)
+    torch.cuda.synchronize()
+    n = int(db.cu.cpu().numpy()[-1])
+    return sum(a.elapsed_time(b) for a, b in ev) / steps, n, db.cu.cpu().numpy()
+
+
+def config_leg(name, base, rot_w, steps, warmup, stream, dilate_r=0):
+    """Another workload at full size (its own seeded latents, grids, masks and keep rule; the m1024
+    block weights, since their values do not change the timing): step and block latency, the dense
+    block, tokens and FLOPs, and the per-kernel roofline fractions."""
+    import numpy as np
+    import torch
+
+    from paper_2606_13898_amd import hilo, inputs
+    from paper_2606_13898_amd.pipeline import DeviceBlock
+
+    wl = inputs.make_workload(name, with_block=False)
+    s = wl.shape
+    db = DeviceBlock(wl, with_block=False)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(77)
+    mod = torch.randn(s.batch, 2, 6, s.dim, generator=g, device="cuda") * 0.1
+    db.attach_block(base.weights, mod)
+    rot = Rotation(db, weight_sets=rot_w)
+
+    def step(k):
+        rot.use(db, k)
+        db.run(hilo.TOPK, dilate_r=dilate_r)
+
+    for k in range(warmup):
+        step(k)
+    ms, per = timed(stream, steps, step)
+    cu = db.cu.cpu().numpy()
+    counts = db.counts.cpu().numpy()
+    kern = kernel_profile(steps, step, kernel_work(s, counts, cu))
+    t_blk = sum(kern[k]["ms"] for k in BLOCK_KERNELS if k in kern)
+    dense_ms, nd, cud = dense_block_ms(db, rot, steps, warmup, stream, dilate_r)
+    nc = int(cu[-1])
+    f_c, f_d = block_flops(s, np.diff(cu)), block_flops(s, np.diff(cud))
+    out = {"workload": f"{name}: {DESCR[name]}" + (f"; mask dilated by r = {dilate_r}" if dilate_r else ""),
+           "ms_per_step": round(ms, 4), "ms_per_step_median": round(float(per[len(per) // 2]), 4),
+           "block_ms": round(t_blk, 4), "dense_block_ms": round(dense_ms, 4),
+           "compressed_tokens": nc, "dense_tokens": nd, "token_ratio": round(nd / nc, 3),
+           "flop_ratio": round(f_d / f_c, 3),
+           "speedup_vs_dense": round(dense_ms / ms, 3), "block_speedup_vs_dense": round(dense_ms / t_blk, 3),
+           "compressed_tokens_per_s": round(nc / (ms * 1e-3), 1),
+           "kernels": {k: {kk: v[kk] for kk in ("ms", "achieved", "unit", "frac") if kk in v} for k, v in kern.items()}}
+    del db, rot
+    torch.cuda.empty_cache()
+    return out
+
+
+def sweep_leg(db, rot, steps, warmup, stream, keeps):
+    """The kept-fraction sweep on one 64x64 sample (Sec. 3.3 reports the speedup as a function of the
+    mask ratio): for each number of kept blocks the whole step, the block alone, tokens and FLOPs,
+    against the dense block (every block kept)."""
+    import numpy as np
+    import torch
+
+    from paper_2606_13898_amd import hilo
+
+    s = db.wl.shape
+    rows = []
+    for keep in keeps:
+        kk = [keep] * s.grids
+
+        def step(k):
+            rot.use(db, k)
+            db.run(hilo.TOPK, keep=kk)
+
+        for k in range(warmup):
+            step(k)
+        ms, _ = timed(stream, steps, step)
+        blk = []
+        for k in range(steps):
+            rot.use(db, k)
+            db.score()
+            db.select(hilo.TOPK, keep=kk)
+            db.compress()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            db.attention()
+            db.mlp()
+            b.record(stream)
+            blk.append((a, b))
+        torch.cuda.synchronize()
+        blk_ms = sum(a.elapsed_time(b) for a, b in blk) / steps
+        cu = db.cu.cpu().numpy()
+        rows.append({"kept_fraction": round(keep / s.n_blocks, 3), "kept_blocks": keep,
+                     "tokens": int(cu[-1]), "ms_per_step": round(ms, 4), "block_ms": round(blk_ms, 4),
+                     "flops": block_flops(s, np.diff(cu))})
+    dense = rows[-1] if keeps[-1] == s.n_blocks else None
+    for r in rows:
+        if dense:
+            r["token_ratio"] = round(dense["tokens"] / r["tokens"], 3)
+            r["flop_ratio"] = round(dense["flops"] / r["flops"], 3)
+            r["block_speedup_vs_dense"] = round(dense["block_ms"] / r["block_ms"], 3)
+            r["step_speedup_vs_dense_block"] = round(dense["block_ms"] / r["ms_per_step"], 3)
+        r["flops"] = f"{r['flops']:.4g}"
+    db.run(hilo.TOPK)  # leave the buffers as the default step left them
+    torch.cuda.synchronize()
+    return rows
 
 
 def pixel_leg(db, steps, warmup, stream):
     """The paper's own selector input: Sobel on the RGB image at 16x the token grid (1024 x 1024
-    pixels for the 64 x 64 grid), summed per token (hilo_score_pixels), then its threshold 0.1 on
-    the normalised map.  The image is synthetic (inputs.pixel_image).  HBM-bound: one read of the
-    image plus the 8-byte energies."""
+    pixels for the 64 x 64 grid), summed per token (hilo_score_pixels), then the threshold.  The
+    paper cuts its normalised Sobel magnitude map at 0.1; the energy is the magnitude squared, so
+    its counterpart is 0.01 on the normalised energy map.  The image is synthetic
+    (inputs.pixel_image).  HBM-bound: one read of the image plus the 8-byte energies."""
     import numpy as np
     import torch
 
@@ -134,18 +367,18 @@ def pixel_leg(db, steps, warmup, stream):
     nbytes = rgb.numel() * 4 + E.numel() * 8
     gbs = nbytes / (ms * 1e-3) / 1e9
     db.energy.copy_(E)
-    db.select(hilo.THRESHOLD, tau=[0.1] * G)
+    db.select(hilo.THRESHOLD, tau=[0.01] * G)
     counts = db.counts.cpu().numpy()
     res = {"ms": round(ms, 4), "image": f"{G}x3x{16 * s.grid_h}x{16 * s.grid_w} float32",
            "achieved": round(gbs, 1), "unit": "GB/s", "peak": 8000.0, "frac": round(gbs / 8000.0, 4),
            "work_per_launch": f"{nbytes / 1e9:.4g} GB",
-           "kept_fine_fraction_tau_0.1": round(float(counts[:, 0].sum()) / (G * N), 4)}
+           "kept_fine_fraction_energy_tau_0.01": round(float(counts[:, 0].sum()) / (G * N), 4)}
     db.run(hilo.TOPK)  # leave the buffers as the default step left them
     torch.cuda.synchronize()
     return res
 
 
-def token_set_leg(db, steps, warmup, stream, dense_ms):
+def token_set_leg(db, rot, steps, warmup, stream, dense_ms):
     """The whole step with the other token sets (same selection rule): overlap -- every block's
     pooled token kept next to the fine patches, the paper's own token set (Sec. 2.3) -- and drop --
     the fine patches alone (Sec. 3.2) -- both reassembled in the delta form; partition with the
@@ -156,16 +389,13 @@ def token_set_leg(db, steps, warmup, stream, dense_ms):
 
     res = {}
     for name, tokens in (("overlap", hilo.OVERLAP), ("drop", hilo.DROP), ("partition", hilo.PARTITION)):
-        for _ in range(warmup):
+        def step(k):
+            rot.use(db, k)
             db.run(hilo.TOPK, tokens=tokens, delta=True)
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
-        e0.record(stream)
-        for _ in range(steps):
-            db.run(hilo.TOPK, tokens=tokens, delta=True)
-        e1.record(stream)
-        torch.cuda.synchronize()
-        ms = e0.elapsed_time(e1) / steps
+
+        for k in range(warmup):
+            step(k)
+        ms, _ = timed(stream, steps, step)
         nc = int(db.cu.cpu().numpy()[-1])
         ent = {"ms_per_step": round(ms, 4), "compressed_tokens": nc, "decompress": "delta"}
         if dense_ms:
@@ -176,7 +406,7 @@ def token_set_leg(db, steps, warmup, stream, dense_ms):
     return res
 
 
-def fp8_leg(db, steps, warmup, stream, work, bf16_ms):
+def fp8_leg(db, rot, steps, warmup, stream, work, bf16_ms):
     """The step with all four projections in FP8 (per-row E4M3 operands: one scale per token for the
     activations, one per output channel for the weights; Sec. 3.3 combines the compression with FP8
     quantisation): step latency, the projections' rates against the fp8 MFMA peak, the two passes
@@ -204,21 +434,17 @@ def fp8_leg(db, steps, warmup, stream, work, bf16_ms):
     upd8 = (db.z - z0)[:nc].double()
     rel = float(torch.linalg.norm(upd8 - upd16) / torch.linalg.norm(upd16))
 
-    for _ in range(warmup):
+    def step(k):
+        db.x_img, db.x_txt = rot.xs[k % rot.R]
         db.run(hilo.TOPK, fp8=True)
-    evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
-    torch.cuda.synchronize()
-    evs[0].record(stream)
-    for k in range(steps):
-        db.run(hilo.TOPK, fp8=True)
-        evs[k + 1].record(stream)
-    torch.cuda.synchronize()
-    ms = evs[0].elapsed_time(evs[-1]) / steps
-    per_step = np.sort([evs[k].elapsed_time(evs[k + 1]) for k in range(steps)])
+
+    for k in range(warmup):
+        step(k)
+    ms, per_step = timed(stream, steps, step)
 
     hilo.hilo_profile_enable(True)
-    for _ in range(steps):
-        db.run(hilo.TOPK, fp8=True)
+    for k in range(steps):
+        step(k)
     torch.cuda.synchronize()
     kern = {}
     for k in range(hilo.hilo_profile_kinds()):
@@ -238,6 +464,7 @@ def fp8_leg(db, steps, warmup, stream, work, bf16_ms):
     torch.cuda.synchronize()
     res = {"ms_per_step": round(ms, 4), "ms_per_step_median": round(float(per_step[len(per_step) // 2]), 4),
            "projections_in_fp8": ["qkv", "attention_output", "mlp_up", "mlp_down"], "kernels": kern,
+           "timing": "latents rotated as in the main step; one FP8 weight set (quantised once)",
            "block_update_rel_l2_vs_bf16": round(rel, 5)}
     if bf16_ms:
         res["speedup_vs_bf16_step"] = round(bf16_ms / ms, 3)
@@ -344,6 +571,10 @@ def main():
                     help="skip the pixel-space scorer leg (Sobel on the 16x-resolution RGB image)")
     ap.add_argument("--no-fp8", action="store_true",
                     help="skip the step with FP8 projections")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the other workloads (2048 px, edit with r = 0 and 1, ragged batch of 8)")
+    ap.add_argument("--no-sweep", action="store_true",
+                    help="skip the kept-fraction sweep (0, 25, 50, 75, 100% of the blocks on one sample)")
     ap.add_argument("--stack-blocks", type=int, default=8)
     ap.add_argument("--stack-steps", type=int, default=8)
     ap.add_argument("--copy-mib", type=int, default=0,
@@ -377,97 +608,81 @@ def main():
     s = wl.shape
     db = DeviceBlock(wl)
     stream = torch.cuda.current_stream()
+    weight_sets, _w2 = Rotation.weight_sets(db)
+    rot = Rotation(db, weight_sets=weight_sets)
+    sec_steps, sec_warm = min(args.steps, 10), min(args.warmup, 3)
 
-    def step():
+    def step(k):
+        rot.use(db, k)
         db.run(hilo.TOPK)
 
-    for _ in range(args.warmup):
-        step()
+    for k in range(args.warmup):
+        step(k)
     torch.cuda.synchronize()
     # one event between consecutive steps: the mean over the K steps is the value, the per-step
     # durations give the median and the 10th / 90th percentiles
-    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     t0 = time.perf_counter()
-    evs[0].record(stream)
-    for k in range(args.steps):
-        step()
-        evs[k + 1].record(stream)
-    torch.cuda.synchronize()
+    ms, per_step = timed(stream, args.steps, step)
     wall = (time.perf_counter() - t0) * 1e3 / args.steps
-    ms = evs[0].elapsed_time(evs[-1]) / args.steps
-    per_step = np.sort([evs[k].elapsed_time(evs[k + 1]) for k in range(args.steps)])
     pct = lambda q: float(per_step[min(len(per_step) - 1, int(round(q * (len(per_step) - 1))))])
     counts = db.counts.cpu().numpy()
     cu = db.cu.cpu().numpy()
     nc = int(cu[-1])
 
     # per-kernel durations: the same steps again with the library's event pairs around each kernel
-    hilo.hilo_profile_enable(True)
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    kinds = {hilo.hilo_profile_name(k): hilo.hilo_profile_read(k) for k in range(hilo.hilo_profile_kinds())}
-    hilo.hilo_profile_enable(False)
     work = kernel_work(s, counts, cu)
-    kern = {}
-    for name, (tot, n) in kinds.items():
-        if n == 0:
-            continue
-        avg = tot / n
-        ent = {"ms": round(avg, 4), "launches_per_step": n // args.steps}
-        if name in work:
-            amt, unit, peak = work[name]
-            ach = amt / (avg * 1e-3)  # GB/s or TFLOP/s
-            ent.update(achieved=round(ach, 1), unit=unit + "/s", peak=peak,
-                       frac=round(ach / peak, 4), work_per_launch=f"{amt:.4g} {unit}")
-        kern[name] = ent
+    kern = kernel_profile(args.steps, step, work)
     dom = max((k for k in kern if k in work), key=lambda k: kern[k]["ms"])
     d = kern[dom]
     roof = {"kernel": dom, "bound": "mfma" if d["unit"] == "TFLOP/s" else "hbm",
             "achieved": d["achieved"], "peak": d["peak"], "unit": d["unit"], "frac": d["frac"],
             "traffic": traffic_for(dom)}
-    t_blk = sum(kern[k]["ms"] for k in ("rownorm_attn", "gemm_qkv", "attention_core", "gemm_o",
-                                        "rownorm_mlp", "gemm_fc1", "gemm_fc2") if k in kern)
+    t_blk = sum(kern[k]["ms"] for k in BLOCK_KERNELS if k in kern)
+
+    # the box's plain device copy, for the memory-bound kernels' fractions (read + write bytes)
+    cp_a = torch.empty(256 << 20, dtype=torch.uint8, device="cuda")
+    cp_b = torch.empty_like(cp_a)
+    for _ in range(3):
+        cp_b.copy_(cp_a)
+    cp_ms, _ = timed(stream, 10, lambda k: cp_b.copy_(cp_a))
+    copy_ref = {"bytes_per_copy": 2 * cp_a.numel(), "gbs": round(2 * cp_a.numel() / (cp_ms * 1e-3) / 1e9, 1)}
+    del cp_a, cp_b
 
     # the same block on the uncompressed sequence (every block kept fine)
     dense = None
     if not args.no_dense:
+        dense_ms, n_dense, cud = dense_block_ms(db, rot, args.steps, args.warmup, stream)
+        dense = {"block_ms": round(dense_ms, 4), "tokens": n_dense,
+                 "flop_ratio": round(block_flops(s, np.diff(cud)) / block_flops(s, np.diff(cu)), 3)}
+        db.run(hilo.TOPK)
+
+    sweep = None
+    if not args.no_sweep and s.batch == 1 and s.images == 1:
         NB = s.n_blocks
-        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-              for _ in range(args.steps)]
-        db.score()
-        db.select(hilo.TOPK, keep=[NB] * s.grids)
-        for _ in range(args.warmup):
-            db.compress()
-            db.attention()
-            db.mlp()
-        for a, b in ev:
-            db.compress()
-            a.record(stream)
-            db.attention()
-            db.mlp()
-            b.record(stream)
-        torch.cuda.synchronize()
-        dense_ms = sum(a.elapsed_time(b) for a, b in ev) / args.steps
-        n_dense = int(db.cu.cpu().numpy()[-1])
-        dense = {"block_ms": round(dense_ms, 4), "tokens": n_dense}
+        sweep = sweep_leg(db, rot, sec_steps, sec_warm, stream, [0, NB // 4, NB // 2, 3 * NB // 4, NB])
 
     token_sets = None
     if not args.no_token_sets:
-        token_sets = token_set_leg(db, args.steps, args.warmup, stream,
-                                   dense["block_ms"] if dense else None)
+        token_sets = token_set_leg(db, rot, sec_steps, sec_warm, stream, dense["block_ms"] if dense else None)
 
     pixel = None
     if not args.no_pixel_score:
-        pixel = pixel_leg(db, args.steps, args.warmup, stream)
+        pixel = pixel_leg(db, sec_steps, sec_warm, stream)
 
     fp8 = None
     if not args.no_fp8 and s.dtype == "bf16" and s.dim % 128 == 0 and s.mlp_dim % 128 == 0:
-        fp8 = fp8_leg(db, args.steps, args.warmup, stream, work, ms)
+        fp8 = fp8_leg(db, rot, sec_steps, sec_warm, stream, work, ms)
 
     stack = None
     if not args.no_stack:
         stack = stack_leg(db, wl, args.stack_blocks, args.stack_steps, stream)
+
+    configs = None
+    if not args.no_configs and args.workload == "m1024":
+        configs = {}
+        for name, r in (("h2048", 0), ("edit", 0), ("edit", 1), ("ragged", 0)):
+            key = name + (f"_r{r}" if r else "")
+            configs[key] = config_leg(name, db, weight_sets, sec_steps, sec_warm, stream, r)
 
     attn = kern.get("attention_core", {})
     out = {
@@ -492,18 +707,26 @@ def main():
                    "text_tokens": s.text_len, "dim": s.dim, "heads": s.heads,
                    "head_dim": s.head_dim, "mlp_dim": s.mlp_dim,
                    "compressed_tokens": nc, "dense_tokens": s.max_tokens},
+        "timing": {"input_copies": rot.R, "input_bytes_rotated": rot.bytes, "weight_copies": len(weight_sets),
+                   "note": "step k reads input copy k % input_copies and weight copy k % weight_copies"},
         "block_ms": round(t_blk, 4),
         "attn_tflops": attn.get("achieved"),
         "compressed_tokens_per_s": round(nc / (ms * 1e-3), 1),
         "represented_tokens_per_s": round(s.max_tokens / (ms * 1e-3), 1),
         "roofline": roof,
         "kernels": kern,
+        "hbm_copy_reference": copy_ref,
     }
     if dense:
         out["dense"] = dense
         out["speedup_vs_dense"] = round(dense["block_ms"] / ms, 3)
         out["block_speedup_vs_dense"] = round(dense["block_ms"] / t_blk, 3) if t_blk else None
         out["token_ratio"] = round(dense["tokens"] / nc, 3)
+        out["flop_ratio"] = dense["flop_ratio"]
+    if sweep:
+        out["kept_fraction_sweep"] = sweep
+    if configs:
+        out["configs"] = configs
     if token_sets:
         out["token_sets"] = token_sets
     if pixel:

@@ -102,6 +102,8 @@ typedef struct {
  *   gy = ((x[i+1][j-1] + 2x[i+1][j]) + x[i+1][j+1]) - ((x[i-1][j-1] + 2x[i-1][j]) + x[i-1][j+1])
  *   q  = floor(min(gx*gx + gy*gy, 2^22) * 2^16)   (float32, every operation rounded, no fusion;
  *                                                  a NaN energy counts as 2^22)
+ * (for bf16 latents the device forms a + 2b as one fused multiply-add: 2b is exact, so the result
+ * is the same for every input below 2^127 in magnitude)
  *   energy[g][p] = sum over c of q, exact in int64.
  * x_img [G][N][D] dtype  ->  energy [G][N] int64.                                               */
 hilo_status hilo_score(const hilo_shape *shape, const void *x_img, int64_t *energy, void *stream);

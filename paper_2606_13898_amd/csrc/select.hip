@@ -27,8 +27,8 @@ HILO_DEV void load_vec(const void *base, size_t elem, float *f) {
   }
 }
 
-// Workgroup = one row i of one grid, TJ consecutive patches j0..j0+TJ-1; threads split the
-// channels in 16-byte groups and slide a 3x3 window of columns along j.
+// float32 latents: workgroup = one row i of one grid, TJ consecutive patches j0..j0+TJ-1; threads
+// split the channels in 16-byte groups and slide a 3x3 window of columns along j.
 template <bool BF16, int TJ>
 __global__ __launch_bounds__(512) void k_score(const void *__restrict__ x, long long *__restrict__ E,
                                                int H, int W, int D, int tilesJ) {
@@ -114,23 +114,105 @@ __global__ __launch_bounds__(512) void k_score(const void *__restrict__ x, long 
   }
 }
 
+// bf16 latents: workgroup = one patch row x TJ columns with every channel; a lane holds 4
+// channels (8-byte loads) of the 3 rows x (TJ + 2) columns it needs, all loaded before any
+// arithmetic (the kernel is bound by the vector ALU, so the loads of every resident workgroup go
+// out at once).  Per channel a slide along the columns forms the vertical sums once per column;
+// (u + 2m) is one fma: 2m is exact, so its single rounding equals the two-step sum of the
+// definition for every input below 2^127 in magnitude (above, the two-step form overflows to
+// infinity first).  The per-output sums over channels meet in LDS (exact in double).
+template <int TJ, int NT>
+__global__ __launch_bounds__(NT) void k_score_bf16(const uint16_t *__restrict__ x, long long *__restrict__ E,
+                                                   int H, int W, int D, int tilesJ) {
+#pragma clang fp contract(off)
+  const int CG = D / 4;
+  const int t = xcd_remap(blockIdx.x, gridDim.x);
+  const int jt = t % tilesJ, gi = t / tilesJ, i = gi % H, g = gi / H;
+  const int j0 = jt * TJ, nj = min(TJ, W - j0);
+  const size_t rU = (size_t(g) * H + max(i - 1, 0)) * W;
+  const size_t rM = (size_t(g) * H + i) * W;
+  const size_t rD = (size_t(g) * H + min(i + 1, H - 1)) * W;
+  double acc[TJ];
+#pragma unroll
+  for (int k = 0; k < TJ; ++k) acc[k] = 0.0;
+  for (int cg = threadIdx.x; cg < CG; cg += NT) {
+    const size_t c0 = size_t(cg) * 4;
+    uint2 u[TJ + 2], m[TJ + 2], d[TJ + 2];
+#pragma unroll
+    for (int c = 0; c < TJ + 2; ++c) {
+      const int col = min(max(j0 - 1 + c, 0), W - 1);
+      u[c] = *reinterpret_cast<const uint2 *>(x + (rU + col) * D + c0);
+      m[c] = *reinterpret_cast<const uint2 *>(x + (rM + col) * D + c0);
+      d[c] = *reinterpret_cast<const uint2 *>(x + (rD + col) * D + c0);
+    }
+#pragma unroll
+    for (int w = 0; w < 2; ++w) {
+#pragma unroll
+      for (int hb = 0; hb < 2; ++hb) {
+        auto f = [&](const uint2 &v) {
+          const uint32_t b = w ? v.y : v.x;
+          return __uint_as_float(hb ? (b & 0xffff0000u) : (b << 16));
+        };
+        float pu = f(u[0]), pd = f(d[0]);
+        float cu = f(u[1]), cd = f(d[1]);
+        float Vp = __builtin_fmaf(2.0f, f(m[0]), pu) + pd;  // vertical sums of columns j-1, j
+        float Vc = __builtin_fmaf(2.0f, f(m[1]), cu) + cd;
+#pragma unroll
+        for (int k = 0; k < TJ; ++k) {
+          const float nu = f(u[k + 2]), nd = f(d[k + 2]);
+          const float Vn = __builtin_fmaf(2.0f, f(m[k + 2]), nu) + nd;
+          const float gx = Vn - Vp;
+          const float gy = (__builtin_fmaf(2.0f, cd, pd) + nd) - (__builtin_fmaf(2.0f, cu, pu) + nu);
+          const float t1 = gx * gx;
+          const float t2 = gy * gy;
+          const float e = t1 + t2;
+          acc[k] += double(floorf(fminf(e, 4194304.0f) * 65536.0f));  // fminf(NaN, cap) = cap
+          pu = cu; pd = cd; cu = nu; cd = nd;
+          Vp = Vc; Vc = Vn;
+        }
+      }
+    }
+  }
+  __shared__ double red[TJ][NT];
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  constexpr int NW = NT / 64;
+#pragma unroll
+  for (int k = 0; k < TJ; ++k) red[k][tid] = acc[k];
+  __syncthreads();
+  for (int k = wid; k < nj; k += NW) {
+    double s = 0.0;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) s += red[k][w * 64 + lane];
+    const long long v = wave_sum_i64(static_cast<long long>(s));
+    if (lane == 0) E[rM + j0 + k] = v;
+  }
+}
+
 constexpr int kScoreTJ = 8;
 
 hipError_t launch_score(bool bf16, const void *x, long long *E, int G, int H, int W, int D,
                         hipStream_t st) {
-  const int V = bf16 ? 8 : 4;
-  const int CG = D / V;
-  int threads = ((CG + 63) / 64) * 64;
-  if (threads > 512) threads = 512;
   const int tilesJ = (W + kScoreTJ - 1) / kScoreTJ;
   const long long nblk = (long long)G * H * tilesJ;
   if (nblk <= 0) return hipSuccess;
-  if (bf16)
-    hipLaunchKernelGGL((k_score<true, kScoreTJ>), dim3(unsigned(nblk)), dim3(threads), 0, st, x, E,
-                       H, W, D, tilesJ);
-  else
-    hipLaunchKernelGGL((k_score<false, kScoreTJ>), dim3(unsigned(nblk)), dim3(threads), 0, st, x, E,
-                       H, W, D, tilesJ);
+  if (bf16) {
+    const uint16_t *xb = reinterpret_cast<const uint16_t *>(x);
+    const int lanes = D / 4;  // D % 64 == 0
+#define HILO_SCORE(NTV) \
+  hipLaunchKernelGGL((k_score_bf16<kScoreTJ, NTV>), dim3(unsigned(nblk)), dim3(NTV), 0, st, xb, E, H, W, D, tilesJ)
+    if (lanes <= 64) HILO_SCORE(64);
+    else if (lanes <= 128) HILO_SCORE(128);
+    else if (lanes <= 256) HILO_SCORE(256);
+    else if (lanes <= 512) HILO_SCORE(512);
+    else HILO_SCORE(768);
+#undef HILO_SCORE
+    return hipGetLastError();
+  }
+  const int CG = D / 4;
+  int threads = ((CG + 63) / 64) * 64;
+  if (threads > 512) threads = 512;
+  hipLaunchKernelGGL((k_score<false, kScoreTJ>), dim3(unsigned(nblk)), dim3(threads), 0, st, x, E,
+                     H, W, D, tilesJ);
   return hipGetLastError();
 }
 

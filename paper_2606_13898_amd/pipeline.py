@@ -53,6 +53,17 @@ class DeviceBlock:
             self.aw = hilo.attn_weights(self.weights)
             self.mw = hilo.mlp_weights(self.weights)
 
+    def attach_block(self, weights, mod: torch.Tensor):
+        """Run the block with the given device weights (two stream dicts) and modulation
+        [B][2][6][D] instead of the workload's own (benchmarks reuse one weight set across shapes)."""
+        self.weights = weights
+        self.mod = mod
+        nbytes = max(hilo.hilo_workspace_bytes(self.shape), hilo.hilo_workspace_bytes_fp8(self.shape))
+        self.ws = torch.empty(nbytes, dtype=torch.uint8, device=mod.device)
+        self.aw = hilo.attn_weights(weights)
+        self.mw = hilo.mlp_weights(weights)
+        self.with_block = True
+
     # -- the six steps ---------------------------------------------------------------------
     def score(self, stream=None):
         hilo.hilo_score(self.shape, self.x_img, self.energy, stream)
