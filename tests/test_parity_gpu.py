@@ -195,10 +195,15 @@ def test_run_to_run_determinism():
 
 # (128, [150, 300, 3]): fewer key steps than workgroups, so every step is its own range and the
 # query tiles are cut into 3 and 5 pieces -- the merge's odd, unpaired last contributor
-@pytest.mark.parametrize("hd,lens", [(128, [1, 17, 64, 65, 200]), (128, [150, 300, 3]), (64, [3, 130, 31])])
-def test_attention_core_ragged(hd, lens):
-    print(f"[parity] attention core hd={hd} lens={lens}", flush=True)
-    heads = 2
+# Many units per workgroup (256 workgroups for head dim 128, 512 for 64): (128, 24 heads, 3 x 1100)
+# is 360 query tiles of 256 rows; (64, 8 heads, 8 x 1000) 512 tiles of 128 rows, as many as
+# workgroups, so every range boundary falls at a tile's key step 0 or mid-tile alike; (64, 8 heads,
+# 9 x 1000) 576 tiles
+@pytest.mark.parametrize("hd,lens,heads", [(128, [1, 17, 64, 65, 200], 2), (128, [150, 300, 3], 2),
+                                           (64, [3, 130, 31], 2), (128, [1100] * 3, 24),
+                                           (64, [1000] * 8, 8), (64, [1000] * 9, 8)])
+def test_attention_core_ragged(hd, lens, heads):
+    print(f"[parity] attention core hd={hd} heads={heads} lens={lens}", flush=True)
     D = heads * hd
     cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
     T = int(cu[-1])

@@ -1,5 +1,6 @@
 #!/usr/bin/env python3
-"""HBM traffic per launch of every kernel kind of the bench, from rocprofv3 counters.
+"""HBM traffic and MFMA utilisation per launch of every kernel kind of the bench, from rocprofv3
+counters.
 
 Two counter passes over a short bench run (FETCH_SIZE, then WRITE_SIZE: bytes between the L2 and
 memory, per dispatch) and the same two passes over one plain device copy of known size, which
@@ -7,8 +8,13 @@ calibrates each counter (calibrated bytes = counter / (counter of the copy / byt
 The result, profiles/traffic.json, is what bench.py reports as roofline.traffic; each entry carries
 a digest of the kernel sources it was measured on, and bench.py drops it once they change.
 
-    python traffic.py commands OUTDIR        # print the four rocprofv3 commands (run them on the GPU)
-    python traffic.py summarize OUTDIR       # write profiles/traffic.json and profiles/traffic_m1024.md
+A fifth pass reads the matrix-core counters: SQ_VALU_MFMA_BUSY_CYCLES (summed over the SIMDs: 32
+busy cycles per 32x32x16 bf16 MFMA, 16 per 16x16x32), GRBM_GUI_ACTIVE (summed over the 8 XCDs:
+divided by 8 it is the dispatch's length in GPU cycles), SQ_INSTS_MFMA and SQ_INSTS_VALU.  MFMA
+utilisation = busy cycles / (SIMDs x GUI cycles / 8), written to profiles/mfma_m1024.md.
+
+    python traffic.py commands OUTDIR        # print the five rocprofv3 commands (run them on the GPU)
+    python traffic.py summarize OUTDIR       # write profiles/traffic.json, traffic_m1024.md, mfma_m1024.md
 """
 from __future__ import annotations
 
@@ -25,9 +31,12 @@ from bench import source_digest  # noqa: E402
 
 COPY_MIB = 256
 BENCH = ("python3 {root}/bench.py --steps 2 --warmup 1 --no-dense --no-cpu-baseline --no-fp8 --no-stack "
-         "--no-token-sets --no-pixel-score")
+         "--no-token-sets --no-pixel-score --no-configs --no-sweep")
 COPY = "python3 {root}/bench.py --copy-mib %d" % COPY_MIB
 COUNTERS = ("FETCH_SIZE", "WRITE_SIZE")
+MFMA_COUNTERS = "SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_MFMA SQ_INSTS_VALU SQ_BUSY_CYCLES GRBM_GUI_ACTIVE"
+SIMDS = 256 * 4      # MI355X: 256 compute units of 4 SIMDs
+XCDS = 8
 
 CSRC = "paper_2606_13898_amd/csrc/"
 HDRS = [CSRC + "common.h", CSRC + "kernels.h"]
@@ -47,7 +56,60 @@ def commands(out):
         for tag, prog in (("bench", BENCH), ("copy", COPY)):
             cmds.append(f"timeout -s KILL 120 rocprofv3 --pmc {cnt} --output-format csv "
                         f"-d {out}/{cnt} -o {tag} -- {prog.format(root=ROOT)}")
+    cmds.append(f"timeout -s KILL 120 rocprofv3 --pmc {MFMA_COUNTERS} --output-format csv "
+                f"-d {out}/MFMA -o bench -- {BENCH.format(root=ROOT)}")
     return cmds
+
+
+def load_multi(path):
+    """{dispatch id: (kernel name, duration ns, {counter: value})} of a multi-counter pass."""
+    per = collections.OrderedDict()
+    with open(path) as f:
+        for r in csv.DictReader(f):
+            key = int(r["Dispatch_Id"])
+            ent = per.setdefault(key, [r["Kernel_Name"], int(r["End_Timestamp"]) - int(r["Start_Timestamp"]), {}])
+            ent[2][r["Counter_Name"]] = ent[2].get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    return per
+
+
+def summarize_mfma(out):
+    path = os.path.join(out, "MFMA", "bench_counter_collection.csv")
+    if not os.path.exists(path):
+        return None
+    agg = collections.defaultdict(lambda: collections.defaultdict(float))
+    n = collections.Counter()
+    state = {}
+    for _, (name, dur, cs) in load_multi(path).items():
+        k = kind_of(name, state)
+        if k is None or not primary(name):
+            continue
+        n[k] += 1
+        agg[k]["dur_ns"] += dur
+        for c, v in cs.items():
+            agg[k][c] += v
+    rows = {}
+    for k, a in agg.items():
+        c = n[k]
+        gui = a["GRBM_GUI_ACTIVE"] / c / XCDS
+        rows[k] = {"us": a["dur_ns"] / c / 1e3, "clock_ghz": gui / (a["dur_ns"] / c),
+                   "mfma_busy": a["SQ_VALU_MFMA_BUSY_CYCLES"] / c / (SIMDS * gui) if gui else 0.0,
+                   "mfma_insts": a["SQ_INSTS_MFMA"] / c, "valu_insts": a["SQ_INSTS_VALU"] / c}
+    lines = ["# MFMA utilisation per call, m1024 workload (rocprofv3 SQ_VALU_MFMA_BUSY_CYCLES)", "",
+             "MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (%d SIMDs x GRBM_GUI_ACTIVE / %d): the share of the "
+             "dispatch's GPU cycles the matrix cores were busy (the counter adds 32 cycles per "
+             "32x32x16 and 16 per 16x16x32 bf16 MFMA over all SIMDs; GRBM_GUI_ACTIVE adds the "
+             "dispatch's cycles over the %d XCDs).  Main kernels only (the GEMM fixups and the "
+             "attention merge issue no MFMA)." % (SIMDS, XCDS, XCDS), "",
+             "Command:", "", "    " + commands(out)[-1], "",
+             "| kind | us | clock GHz | MFMA busy | MFMA insts | VALU insts | VALU per MFMA |",
+             "|---|---:|---:|---:|---:|---:|---:|"]
+    for k, r in sorted(rows.items(), key=lambda kv: -kv[1]["us"]):
+        vpm = r["valu_insts"] / r["mfma_insts"] if r["mfma_insts"] else float("nan")
+        lines.append(f"| {k} | {r['us']:.1f} | {r['clock_ghz']:.2f} | {100 * r['mfma_busy']:.1f}% | "
+                     f"{r['mfma_insts']:.4g} | {r['valu_insts']:.4g} | {vpm:.2f} |")
+    with open(os.path.join(ROOT, "profiles", "mfma_m1024.md"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+    return rows
 
 
 def load(out, cnt, tag):
@@ -79,6 +141,8 @@ def kind_of(name, state):
     if "k_rownorm" in base:
         state["rownorm"] = state.get("rownorm", 0) + 1
         return "rownorm_attn" if state["rownorm"] % 2 == 1 else "rownorm_mlp"
+    if "k_score_bf16<" in base:
+        return "score"
     for k in ("k_score", "k_select", "k_layout", "k_compress", "k_decompress"):
         if k + "<" in base or base.endswith(k):
             return k[2:]
@@ -129,7 +193,7 @@ def summarize(out):
              "of the bytes the copy moves; every figure below is divided by that factor." %
              (COPY_MIB, factor["FETCH_SIZE"], factor["WRITE_SIZE"]), "",
              "Commands (then `python traffic.py summarize %s`):" % out, ""]
-    lines += ["    " + c for c in commands(out)]
+    lines += ["    " + c for c in commands(out)[:4]]
     lines += ["", "| kind | read MB | write MB | total MB |", "|---|---:|---:|---:|"]
     for k, e in sorted(kernels.items(), key=lambda kv: -kv[1]["bytes_per_launch"]):
         lines.append(f"| {k} | {e['fetch_bytes_per_launch'] / 1e6:.1f} | "
@@ -137,6 +201,9 @@ def summarize(out):
     with open(os.path.join(ROOT, "profiles", "traffic_m1024.md"), "w") as f:
         f.write("\n".join(lines) + "\n")
     print(json.dumps({k: v["bytes_per_launch"] for k, v in kernels.items()}, indent=1))
+    mf = summarize_mfma(out)
+    if mf:
+        print(json.dumps({k: round(100 * v["mfma_busy"], 1) for k, v in mf.items()}, indent=1))
 
 
 if __name__ == "__main__":
