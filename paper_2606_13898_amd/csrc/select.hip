@@ -334,7 +334,9 @@ __global__ __launch_bounds__(kSelThreads) void k_select(
   int *itmp = reinterpret_cast<int *>(flag + ((NB + 15) & ~15));         // [kSelWaves + 1]
   int *hist = itmp + 32;                                                 // [256]
   long long *ltmp = reinterpret_cast<long long *>(hist + 256);          // [kSelWaves]
-  int *bcast = reinterpret_cast<int *>(ltmp + kSelWaves);               // [4]
+  unsigned long long *lor = reinterpret_cast<unsigned long long *>(ltmp + kSelWaves);  // [1]
+  int *bcast = reinterpret_cast<int *>(lor + 1);                        // [4]
+  if (tid == 0) *lor = 0;
   const long long *Eg = E + size_t(g) * N;
 
   // block sums and the grid maximum
@@ -372,20 +374,32 @@ __global__ __launch_bounds__(kSelThreads) void k_select(
     }
     __syncthreads();
   } else {  // top-k
+    // forced blocks, and the OR of the other blocks' sums: its top byte is where the radix starts
     int nf_local = 0;
-    for (int b = tid; b < NB; b += kSelThreads) nf_local += (flag[b] & 2) ? 1 : 0;
+    unsigned long long orv = 0;
+    for (int b = tid; b < NB; b += kSelThreads) {
+      const bool forced = flag[b] & 2;
+      nf_local += forced ? 1 : 0;
+      if (!forced) orv |= static_cast<unsigned long long>(Bs[b]);
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) orv |= __shfl_xor(orv, off, 64);
+    if ((tid & 63) == 0 && orv != 0) atomicOr(lor, orv);
     int nF;
-    (void)block_excl_scan(nf_local, itmp, nF);
+    (void)block_excl_scan(nf_local, itmp, nF);  // its barriers also complete the OR
+    const unsigned long long allor = *lor;
+    const int top = allor == 0 ? 0 : ((63 - __clzll(static_cast<long long>(allor))) / 8) * 8;
     const int kp = max(0, prm.keep[gl] - nF);
     const int nN = NB - nF;
     if (kp >= nN) {
       for (int b = tid; b < NB; b += kSelThreads) flag[b] |= 1;
       __syncthreads();
     } else if (kp > 0) {
-      // MSB radix select of the kp-th largest block sum among non-forced blocks (sums < 2^53).
+      // MSB radix select of the kp-th largest block sum among non-forced blocks (sums < 2^53),
+      // from the highest byte any of them has set (the bytes above are zero in all of them)
       long long prefix = 0, mask = 0;
       int rem = kp;
-      for (int shift = 48; shift >= 0; shift -= 8) {
+      for (int shift = top; shift >= 0; shift -= 8) {
         for (int d = tid; d < 256; d += kSelThreads) hist[d] = 0;
         __syncthreads();
         for (int b = tid; b < NB; b += kSelThreads) {
@@ -515,7 +529,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(
 }
 
 size_t select_lds_bytes(int NB) {
-  return size_t(NB) * 8 + ((NB + 15) & ~15) + 32 * 4 + 256 * 4 + kSelWaves * 8 + 16;
+  return size_t(NB) * 8 + ((NB + 15) & ~15) + 32 * 4 + 256 * 4 + kSelWaves * 8 + 8 + 16;
 }
 
 hipError_t launch_select(const long long *E, const uint8_t *force, int G, int H, int W, int r,
