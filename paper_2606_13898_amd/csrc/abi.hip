@@ -37,14 +37,21 @@ hipError_t timed(int kind, hipStream_t st, F &&launch) {
   if (!g_prof || g_used >= kMaxRecs) return launch();
   if (g_used == g_recs.size()) {
     ProfRec r{kind, nullptr, nullptr};
-    if (hipEventCreate(&r.a) != hipSuccess || hipEventCreate(&r.b) != hipSuccess) return launch();
+    if (hipEventCreate(&r.a) != hipSuccess) return launch();
+    if (hipEventCreate(&r.b) != hipSuccess) {
+      (void)hipEventDestroy(r.a);
+      return launch();
+    }
     g_recs.push_back(r);
   }
-  ProfRec &r = g_recs[g_used++];
+  ProfRec &r = g_recs[g_used];
   r.kind = kind;
-  hipEventRecord(r.a, st);
-  hipError_t e = launch();
-  hipEventRecord(r.b, st);
+  hipError_t e = hipEventRecord(r.a, st);
+  if (e != hipSuccess) return e;
+  e = launch();
+  if (e != hipSuccess) return e;
+  e = hipEventRecord(r.b, st);
+  if (e == hipSuccess) ++g_used;  // only a launch bracketed by both events is read back
   return e;
 }
 
