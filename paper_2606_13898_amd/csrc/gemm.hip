@@ -3,8 +3,9 @@
 // weights, tiles never straddling a segment.  Epilogues fuse the bias, the tanh-GELU, and the
 // gated residual update of the float32 stream z.
 //
-// bf16 and FP8 paths: one square-tile MFMA kernel (k_gemm_big), one persistent workgroup per CU
-// with 4 waves, 256 x 256 tiles (QKV, MLP up) or 192 x 192 (attention output, MLP down) as
+// bf16 and FP8 paths: one MFMA kernel (k_gemm_big), one persistent workgroup per CU with 4 waves,
+// 256 x 256 tiles (MLP up; QKV's first launch), 256 x 192 (QKV's second launch: the columns one
+// wave of 256 x 256 tiles cannot hold) or 192 x 192 (attention output, MLP down) as
 // 32 x 32 MFMA blocks (v_mfma_f32_32x32x16_bf16, or v_mfma_f32_32x32x64_f8f6f4 on E4M3 codes),
 // fp32 accumulators in AGPRs, K in 64-byte stages through a 4-slot LDS ring filled by direct
 // global->LDS loads.  Whole data-parallel waves of tiles run first, then a stream-K remainder;
@@ -146,6 +147,7 @@ HILO_DEV TileRows decode_row_tile(const GemmProblem &p, int BM, int r) {
 // fixed order and runs the epilogue -- deterministic, and no workgroup ever waits for another.
 struct SkPlan {
   int R, TN, T, nk;  // row tiles, column tiles, tiles, K steps
+  int c0;          // first column of the plan's range (column tile tn starts at c0 + tn * BN)
   int s, U, dp;    // pieces per tile, units, data-parallel units
   int len;         // K steps of a stream-K unit
   long long I;     // stream-K iterations
@@ -161,10 +163,31 @@ constexpr int kNoSplitSteps = 64;
 // at 256 x 256) that the fixup reads back, so a short tail goes to fewer workgroups.
 constexpr int kSkMinSteps = 12;
 
+// Column range [c0, c1) of the problem's launch.  A split projection (phase 1 / 2) hands the
+// leading 256-column tiles to one wave of 256 x 256 tiles and the rest to one wave of 256 x 192
+// tiles, when its 256 x 256 tiles would need more than one wave but at most two and the rest then
+// fits one wave of the narrower tiles (so two waves of whole tiles become one whole wave plus three
+// quarters of one, without partial tiles); otherwise phase 1 holds every column and phase 2 none.
+HILO_DEV void col_range(const GemmProblem &p, int P, int &c0, int &c1) {
+  c0 = 0;
+  c1 = p.N;
+  if (p.phase == 0) return;
+  const int R = row_tiles_total(p, 256), TN = (p.N + 255) / 256;
+  int split = p.N;
+  if (R > 0 && R * TN > P && R * TN <= 2 * P) {
+    const int ta = P / R;
+    if (ta >= 1 && R * ((p.N - ta * 256 + 191) / 192) <= P) split = ta * 256;
+  }
+  if (p.phase == 1) c1 = split;
+  else c0 = split;
+}
+
 HILO_DEV SkPlan sk_plan(const GemmProblem &p, int BM, int BN, int P, int kstep = 64) {
   SkPlan q;
   q.R = row_tiles_total(p, BM);
-  q.TN = (p.N + BN - 1) / BN;
+  int c1;
+  col_range(p, P, q.c0, c1);
+  q.TN = c1 > q.c0 ? (c1 - q.c0 + BN - 1) / BN : 0;
   q.T = q.R * q.TN;
   q.nk = p.K / kstep;
   // 256 x 256 tiles: a stream-K tail costs a 256 KiB partial per piece; when the last wave holds
@@ -363,13 +386,15 @@ struct SkTile {
   }
 };
 
-// ------------------------------------------------------------------- MFMA, 256 x 256 tiles
+// ------------------------------------------------------------------------------ MFMA tiles
 //
-// One persistent workgroup per CU, 4 waves (2 x 2), wave tile 128 x 128 as 4 x 4 blocks of 32 x 32:
-// 256 fp32 accumulators per lane, held in AGPRs.  Per K step the CU loads half the operand bytes
-// per FLOP of a 128 x 128 tile.  K runs in stages of 64 bytes per row (32 bf16 or 64 FP8 values)
-// through a 4-slot LDS ring (32 KiB per stage: the stage's 256 A rows, then its 256 W rows, 16-byte
-// chunks swizzled), loaded by direct global->LDS loads three stages ahead.  A stage is 16 blocks:
+// One persistent workgroup per CU, 4 waves (2 x 2).  For 256 x 256 tiles the wave tile is 128 x 128
+// as 4 x 4 blocks of 32 x 32: 256 fp32 accumulators per lane, held in AGPRs, and per K step the CU
+// loads half the operand bytes per FLOP of a 128 x 128 tile (BM x BN tiles: BM/64 x BN/64 blocks per
+// wave, the same schedule).  K runs in stages of 64 bytes per row (32 bf16 or 64 FP8 values)
+// through a 4-slot LDS ring (32 KiB per 256 x 256 stage: the stage's A rows, then its W rows, 16-byte
+// chunks swizzled), loaded by direct global->LDS loads three stages ahead.  A 256 x 256 stage is
+// 16 blocks:
 //   * bf16: two v_mfma_f32_32x32x16_bf16 per block, one per K half (chunks {h, h + 2});
 //   * FP8:  one v_mfma_f32_32x32x64_f8f6f4 per block (all four chunks, 8 registers per operand).
 // Either way lane (r, g) = (l % 32, l / 32) of a fragment reads chunks 2 g and 2 g + 1 of row r of a
@@ -414,16 +439,21 @@ HILO_DEV int swz(int r) { return ((r >> 1) & 3) ^ ((r >> 3) & 1); }
 // there gives lane half g the columns 16 g .. 16 g + 15 in register order.  These LDS reads are
 // conflict-free like the natural order (measured; shifting the second half by 8 rows is not).
 HILO_DEV int perm_w(int r) { return ((r & 4) ? 16 : 0) + 4 * (r >> 3) + (r & 3); }
-// A TB x TB tile on 4 waves (2 x 2), wave tile TB/2 x TB/2 as NB x NB blocks of 32 x 32.
-template <int TB>
+// A BM x BN tile on 4 waves (2 x 2), wave tile BM/2 x BN/2 as NBM x NBN blocks of 32 x 32.
+template <int BM, int BN>
 struct Geo {
-  static_assert(TB == 256 || TB == 192, "tile sizes of the square MFMA kernel");
-  static constexpr int NB = TB / 64;     // blocks per wave row / column
-  static constexpr int LQ = 2 * NB;      // load instructions per wave per stage (A rows, then W rows)
-  static constexpr int NR = 4 * NB;      // fragment reads per wave per stage
-  static constexpr int AB = TB * 64;     // bytes of a stage's A rows
-  static constexpr int SB = 2 * TB * 64; // bytes of a stage
+  static_assert((BM == 256 && BN == 256) || (BM == 192 && BN == 192) || (BM == 256 && BN == 192),
+                "tile shapes of the MFMA kernel");
+  static constexpr int NBM = BM / 64;        // blocks per wave column (A side)
+  static constexpr int NBN = BN / 64;        // blocks per wave row (W side)
+  static constexpr int LQ = NBM + NBN;       // load instructions per wave per stage (A rows, then W rows)
+  static constexpr int NR = 2 * LQ;          // fragment reads per wave per stage
+  static constexpr int AB = BM * 64;         // bytes of a stage's A rows
+  static constexpr int SB = (BM + BN) * 64;  // bytes of a stage
   static constexpr int LDS = S * SB + 4 * kEpiWave;
+  // every load and fragment read of a stage is issued after its barrier (block NBN) and before
+  // its last block
+  static_assert(NBN + LQ <= NBM * NBN, "stage schedule does not fit the blocks");
 };
 }  // namespace big
 
@@ -472,27 +502,27 @@ HILO_DEV void wait_lgkm_rt(int n) {  // n is a compile-time constant after unrol
   }
 }
 
-// Epilogue of a TB x TB tile from the AGPR accumulators of wave wid.  The W fragments are read in
+// Epilogue of a BM x BN tile from the AGPR accumulators of wave wid.  The W fragments are read in
 // the row order perm_w, so lane l of block (bi, bj) holds row 32 bi + l % 32 of the wave tile and, in
 // register v, column 32 bj + 16 (l / 32) + v: 16 consecutive columns, stored as two 16-byte pieces
 // (bf16) or four (float32 z).  Column operands (bias, FP8 weight scales, the gate) come from the
 // wave's LDS area `epi`, once per block column; FP8 row scales once per tile.  Bias / GELU outputs
 // are rounded to bf16, the residual update adds gate * (acc + bias) to the float32 z.  Blocks leave
 // the AGPRs one at a time.
-template <int TB, int EPI, bool F8>
+template <int BM, int BN, int EPI, bool F8>
 HILO_DEV void big_epilogue(const GemmProblem &p, const TileRows &tr, int n0, int wid, int lane,
-                           const uint8_t *epi, f32x16 (&acc)[TB / 64][TB / 64]) {
+                           const uint8_t *epi, f32x16 (&acc)[BM / 64][BN / 64]) {
   using namespace big;
-  constexpr int NB = Geo<TB>::NB;
-  const int rbase = (wid >> 1) * (TB / 2) + (lane & 31);
+  constexpr int NBM = Geo<BM, BN>::NBM, NBN = Geo<BM, BN>::NBN;
+  const int rbase = (wid >> 1) * (BM / 2) + (lane & 31);
   const int cl0 = 16 * (lane >> 5);              // this lane's first column within a 32-column block
-  const int cbase = n0 + (wid & 1) * (TB / 2) + cl0;
-  float sa[NB];
+  const int cbase = n0 + (wid & 1) * (BN / 2) + cl0;
+  float sa[NBM];
 #pragma unroll
-  for (int bi = 0; bi < NB; ++bi)
+  for (int bi = 0; bi < NBM; ++bi)
     sa[bi] = F8 ? *reinterpret_cast<const float *>(epi + kEpiRow + 4 * (32 * bi + (lane & 31))) : 1.f;
 #pragma unroll
-  for (int bj = 0; bj < NB; ++bj) {
+  for (int bj = 0; bj < NBN; ++bj) {
     const int cl = cl0 + 32 * bj, n = cbase + 32 * bj;
     u32x4 bu[2];
     f32x4 cv[4], gv[4];  // FP8 weight scales and the residual gate of the lane's 16 columns
@@ -507,7 +537,7 @@ HILO_DEV void big_epilogue(const GemmProblem &p, const TileRows &tr, int n0, int
       for (int h = 0; h < 4; ++h) gv[h] = *reinterpret_cast<const f32x4 *>(epi + kEpiGate + 4 * cl + 16 * h);
     }
 #pragma unroll
-    for (int bi = 0; bi < NB; ++bi) {
+    for (int bi = 0; bi < NBM; ++bi) {
       f32x16 blk = acc[bi][bj];  // one block out of the AGPRs at a time
       asm volatile("" : "+v"(blk));
       const int rl = rbase + 32 * bi;
@@ -551,18 +581,18 @@ HILO_DEV void big_epilogue(const GemmProblem &p, const TileRows &tr, int n0, int
   }
 }
 
-template <int TB, int EPI, int ROLE, bool F8>
+template <int BM, int BN, int EPI, int ROLE, bool F8>
 __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
   using namespace big;
-  using G = Geo<TB>;
-  constexpr int NB = G::NB, LQ = G::LQ, NR = G::NR, AB = G::AB, SB = G::SB;
-  using T = SkTile<TB, TB, 2, 2>;       // partial slot size and layout (16 x 16 fragment order)
+  using G = Geo<BM, BN>;
+  constexpr int NBM = G::NBM, NBN = G::NBN, LQ = G::LQ, NR = G::NR, AB = G::AB, SB = G::SB;
+  using T = SkTile<BM, BN, 2, 2>;       // partial slot size and layout (16 x 16 fragment order)
   constexpr int ESZ = F8 ? 1 : 2;       // operand bytes per element
   __shared__ __attribute__((aligned(1024))) uint8_t lds[G::LDS];
 
   const int P = gridDim.x;
   const int pid = xcd_remap(blockIdx.x, P);
-  const SkPlan q = sk_plan(p, TB, TB, P, F8 ? 128 : 64);
+  const SkPlan q = sk_plan(p, BM, BN, P, F8 ? 128 : 64);
   const SkRange rg = sk_range(q, pid);
 
   const int lane = threadIdx.x & 63;
@@ -571,21 +601,26 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
   const uint8_t *A = reinterpret_cast<const uint8_t *>(p.A);
 
   // ---- loader: its own cursor over this workgroup's items, three stages ahead of the MFMAs; wave
-  // wid loads rows wid TB/4 .. + TB/4 - 1 of A and of W, 16 rows (1 KiB) per instruction
+  // wid loads rows wid BM/4 .. + BM/4 - 1 of A and wid BN/4 .. + BN/4 - 1 of W, 16 rows (1 KiB) per
+  // instruction
   SkCursor lc{pid, rg.beg};
-  const uint8_t *la[NB], *lb[NB];
+  const uint8_t *la[NBM], *lb[NBN];
   int lk = 0, lke = 0;  // next stage to load (absolute in K) and the end of its item
   auto ld_src = [&](int t) __attribute__((always_inline)) {
     int rt, tn;
     tile_coords(q, t, rt, tn);
     tn = uni(tn);
-    const TileRows tr = uni(decode_row_tile(p, TB, uni(rt)));
+    const TileRows tr = uni(decode_row_tile(p, BM, uni(rt)));
     const uint8_t *Wt = reinterpret_cast<const uint8_t *>(tr.sigma ? p.W[1] : p.W[0]);
 #pragma unroll
-    for (int i = 0; i < NB; ++i) {
-      const int r = wid * (TB / 4) + 16 * i + lrow;
+    for (int i = 0; i < NBM; ++i) {
+      const int r = wid * (BM / 4) + 16 * i + lrow;
       la[i] = A + size_t(tr.row0 + min(r, tr.nrows - 1)) * p.lda * ESZ + (lslot ^ swz(r)) * 16;
-      lb[i] = Wt + size_t(min(tn * TB + r, p.N - 1)) * p.K * ESZ + (lslot ^ swz(r)) * 16;
+    }
+#pragma unroll
+    for (int i = 0; i < NBN; ++i) {
+      const int r = wid * (BN / 4) + 16 * i + lrow;
+      lb[i] = Wt + size_t(min(q.c0 + tn * BN + r, p.N - 1)) * p.K * ESZ + (lslot ^ swz(r)) * 16;
     }
   };
   auto ld_advance = [&]() __attribute__((always_inline)) {
@@ -600,29 +635,28 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
     lk = uni(lk);
     lke = uni(lke);
   };
-  // load instruction j (0..LQ-1) of the current loader stage into `slot`: A rows for j < NB
+  // load instruction j (0..LQ-1) of the current loader stage into `slot`: A rows for j < NBM
   auto ld_one = [&](int slot, int j) __attribute__((always_inline)) {
-    uint8_t *base = lds + slot * SB + wid * (TB / 4) * 64;
     const int k0 = lk * 64;  // bytes
-    if (j < NB) g2lds16(la[j] + k0, base + j * 1024);
-    else g2lds16(lb[j - NB] + k0, base + AB + (j - NB) * 1024);
+    if (j < NBM) g2lds16(la[j] + k0, lds + slot * SB + wid * (BM / 4) * 64 + j * 1024);
+    else g2lds16(lb[j - NBM] + k0, lds + slot * SB + AB + wid * (BN / 4) * 64 + (j - NBM) * 1024);
   };
 
   // ---- fragment reads: lane (r, g) = (lane % 32, lane / 32) reads chunk 2 g (low half) and 2 g + 1
   // (high half) of row r (A) or perm_w(r) (W) of a 32-row fragment; read t of a stage (slot byte
-  // offset so) is half t % 2 of W fragment t / 2 for t < 2 NB, then of A fragment (t - 2 NB) / 2
+  // offset so) is half t % 2 of W fragment t / 2 for t < 2 NBN, then of A fragment (t - 2 NBN) / 2
   const int r8 = lane & 31, g8 = lane >> 5, w8 = perm_w(r8);
   const uint32_t lds0 = (uint32_t)(uintptr_t)lds;
-  const uint32_t fa8 = lds0 + (wid >> 1) * (TB / 2) * 64, fb8 = lds0 + AB + (wid & 1) * (TB / 2) * 64;
+  const uint32_t fa8 = lds0 + (wid >> 1) * (BM / 2) * 64, fb8 = lds0 + AB + (wid & 1) * (BN / 2) * 64;
   const uint32_t fa8l = fa8 + r8 * 64 + (((2 * g8) ^ swz(r8)) * 16), fa8h = fa8 + r8 * 64 + (((2 * g8 + 1) ^ swz(r8)) * 16);
   const uint32_t fb8l = fb8 + w8 * 64 + (((2 * g8) ^ swz(w8)) * 16), fb8h = fb8 + w8 * 64 + (((2 * g8 + 1) ^ swz(w8)) * 16);
-  auto rd_one = [&](u32x4 (&fa)[2 * NB], u32x4 (&fb)[2 * NB], uint32_t so, int t) __attribute__((always_inline)) {
+  auto rd_one = [&](u32x4 (&fa)[2 * NBM], u32x4 (&fb)[2 * NBN], uint32_t so, int t) __attribute__((always_inline)) {
 #define HILO_RD_CASE(C)                                                                                     \
   case C:                                                                                                   \
-    if constexpr (C < 2 * NB)                                                                               \
-      HILO_DS_READ16(fb[C % (2 * NB)], ((C & 1) ? fb8h : fb8l) + so, ((C % (2 * NB)) >> 1) * 2048);         \
-    else if constexpr (C < 4 * NB)                                                                          \
-      HILO_DS_READ16(fa[(C - 2 * NB) % (2 * NB)], ((C & 1) ? fa8h : fa8l) + so, (((C - 2 * NB) % (2 * NB)) >> 1) * 2048); \
+    if constexpr (C < 2 * NBN)                                                                              \
+      HILO_DS_READ16(fb[C % (2 * NBN)], ((C & 1) ? fb8h : fb8l) + so, ((C % (2 * NBN)) >> 1) * 2048);       \
+    else if constexpr (C < 2 * NBN + 2 * NBM)                                                               \
+      HILO_DS_READ16(fa[(C - 2 * NBN) % (2 * NBM)], ((C & 1) ? fa8h : fa8l) + so, (((C - 2 * NBN) % (2 * NBM)) >> 1) * 2048); \
     break;
     switch (t) {
       HILO_RD_CASE(0) HILO_RD_CASE(1) HILO_RD_CASE(2) HILO_RD_CASE(3) HILO_RD_CASE(4) HILO_RD_CASE(5)
@@ -633,13 +667,13 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
 #undef HILO_RD_CASE
   };
 
-  // ---- epilogue operands of the current item: this wave's TB/2 columns (and FP8 rows) into its
+  // ---- epilogue operands of the current item: this wave's BN/2 columns (and FP8 rows) into its
   // LDS area, by DMA (4 bytes per lane), indices clamped into the tile
   uint8_t *epi = lds + S * SB + wid * kEpiWave;
   TileRows etr{0, 0, 0, 1};
   int en0 = 0;
   auto epi_load = [&]() __attribute__((always_inline)) {
-    const int c0 = en0 + (wid & 1) * (TB / 2);
+    const int c0 = en0 + (wid & 1) * (BN / 2);
     const uint16_t *bias = reinterpret_cast<const uint16_t *>(etr.sigma ? p.bias[1] : p.bias[0]);
     g2lds4(bias + min(c0 + 2 * lane, p.N - 2), epi + kEpiBias);
     if constexpr (F8) {
@@ -653,31 +687,31 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
       g2lds4(gate + min(c0 + 64 + lane, p.N - 1), epi + kEpiGate + 256);
     }
     if constexpr (F8) {
-      const int r0 = (wid >> 1) * (TB / 2);
+      const int r0 = (wid >> 1) * (BM / 2);
       g2lds4(p.a_scale + etr.row0 + min(r0 + lane, etr.nrows - 1), epi + kEpiRow);
       g2lds4(p.a_scale + etr.row0 + min(r0 + 64 + lane, etr.nrows - 1), epi + kEpiRow + 256);
     }
   };
 
-  f32x16 acc[NB][NB];
-  u32x4 xa[2 * NB], xb[2 * NB], ya[2 * NB], yb[2 * NB];
+  f32x16 acc[NBM][NBN];
+  u32x4 xa[2 * NBM], xb[2 * NBN], ya[2 * NBM], yb[2 * NBN];
 
   // one stage (ring slot gs % S) on fragments (fa, fb); reads stage gs + 1 into (na, nb); the first
   // stage of a tile (first = true_type) starts the accumulators from zero and, for a tile finished
-  // here, fetches the epilogue operands after its loads.  Before block NB: barrier; after each of
-  // blocks NB .. NB + LQ - 1: one load of the stage three ahead and two fragment reads of the next.
-  auto stage = [&](auto first, u32x4 (&fa)[2 * NB], u32x4 (&fb)[2 * NB], u32x4 (&na)[2 * NB],
-                   u32x4 (&nb)[2 * NB], int gs, bool with_epi) __attribute__((always_inline)) {
+  // here, fetches the epilogue operands after its loads.  Before block NBN: barrier; after each of
+  // blocks NBN .. NBN + LQ - 1: one load of the stage three ahead and two fragment reads of the next.
+  auto stage = [&](auto first, u32x4 (&fa)[2 * NBM], u32x4 (&fb)[2 * NBN], u32x4 (&na)[2 * NBM],
+                   u32x4 (&nb)[2 * NBN], int gs, bool with_epi) __attribute__((always_inline)) {
     const int lslot_w = (gs + S - 1) & (S - 1);
     const uint32_t so = uint32_t(((gs + 1) & (S - 1)) * SB);
 #pragma unroll
-    for (int bi = 0; bi < NB; ++bi) {
+    for (int bi = 0; bi < NBM; ++bi) {
       // outstanding reads allowed: this stage's A halves of blocks bi+1.., the next stage's so far
-      wait_lgkm_rt(2 * (NB - 1 - bi) + 2 * min(max(NB * bi - NB, 0), LQ));
+      wait_lgkm_rt(2 * (NBM - 1 - bi) + 2 * min(max(NBN * bi - NBN, 0), LQ));
 #pragma unroll
-      for (int bj = 0; bj < NB; ++bj) {
-        const int qq = NB * bi + bj;
-        if (qq == NB) asm volatile("s_waitcnt vmcnt(%0)\n s_barrier" ::"n"((S - 3) * LQ) : "memory");
+      for (int bj = 0; bj < NBN; ++bj) {
+        const int qq = NBN * bi + bj;
+        if (qq == NBN) asm volatile("s_waitcnt vmcnt(%0)\n s_barrier" ::"n"((S - 3) * LQ) : "memory");
         if constexpr (F8) {
           if constexpr (decltype(first)::value)
             HILO_MFMA8_AGPR0(acc[bi][bj], cat8(fb[2 * bj], fb[2 * bj + 1]), cat8(fa[2 * bi], fa[2 * bi + 1]));
@@ -688,13 +722,13 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
           else HILO_MFMA16_AGPR(acc[bi][bj], fb[2 * bj], fa[2 * bi]);
           HILO_MFMA16_AGPR(acc[bi][bj], fb[2 * bj + 1], fa[2 * bi + 1]);
         }
-        if (qq >= NB && qq < NB + LQ) {
-          ld_one(lslot_w, qq - NB);
-          rd_one(na, nb, so, 2 * (qq - NB));
-          rd_one(na, nb, so, 2 * (qq - NB) + 1);
+        if (qq >= NBN && qq < NBN + LQ) {
+          ld_one(lslot_w, qq - NBN);
+          rd_one(na, nb, so, 2 * (qq - NBN));
+          rd_one(na, nb, so, 2 * (qq - NBN) + 1);
         }
         if constexpr (decltype(first)::value) {
-          if (qq == NB + LQ - 1 && with_epi) epi_load();
+          if (qq == NBN + LQ - 1 && with_epi) epi_load();
         }
       }
     }
@@ -726,8 +760,8 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
     if (whole) {
       int rt, tn;
       tile_coords(q, cur.t, rt, tn);
-      en0 = uni(tn) * TB;
-      etr = uni(decode_row_tile(p, TB, uni(rt)));
+      en0 = q.c0 + uni(tn) * BN;
+      etr = uni(decode_row_tile(p, BM, uni(rt)));
     }
     ld_check();
     stage(std::true_type{}, xa, xb, ya, yb, gs, whole);
@@ -747,29 +781,29 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
     // stage's fragments must be complete before the compiler may move those registers.
     asm volatile("s_waitcnt lgkmcnt(0)\n s_nop 7\n s_nop 7\n s_nop 7\n s_nop 7" ::: "memory");
 #pragma unroll
-    for (int i = 0; i < NB; ++i)
+    for (int i = 0; i < NBM; ++i)
 #pragma unroll
-      for (int j = 0; j < NB; ++j) asm volatile("" : "+a"(acc[i][j]));
+      for (int j = 0; j < NBN; ++j) asm volatile("" : "+a"(acc[i][j]));
     if (whole) {
       // the epilogue-operand DMA of the first stage is complete once two later stages have passed
       // their barriers (each waits for all but the last stage's loads); a one-step item waits here
       if (cur.ke - cur.kb < 2) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-      big_epilogue<TB, EPI, F8>(p, etr, en0, wid, lane, epi, acc);
+      big_epilogue<BM, BN, EPI, F8>(p, etr, en0, wid, lane, epi, acc);
     } else {
-      // the partial tile in the 16 x 16 fragment layout k_gemm_fix reads (2 NB x 2 NB fragments per
+      // the partial tile in the 16 x 16 fragment layout k_gemm_fix reads (2 NBM x 2 NBN fragments per
       // wave): row 32 bi + l % 32 is fragment row 2 bi + (l % 32) / 16; columns 32 bj + 16 (l / 32)
       // + 4 b .. + 3 are lane l % 16 + 16 b of fragment column 2 bj + l / 32
-      constexpr int TF = 2 * NB;
-      float *base = cur.slot + (size_t(wid) * TF * TF * 64 + ((lane & 31) >> 4) * TF * 64 + (lane >> 5) * 64 + (lane & 15)) * 4;
+      constexpr int TFM = 2 * NBM, TFN = 2 * NBN;
+      float *base = cur.slot + (size_t(wid) * TFM * TFN * 64 + ((lane & 31) >> 4) * TFN * 64 + (lane >> 5) * 64 + (lane & 15)) * 4;
 #pragma unroll
-      for (int bi = 0; bi < NB; ++bi)
+      for (int bi = 0; bi < NBM; ++bi)
 #pragma unroll
-        for (int bj = 0; bj < NB; ++bj) {
+        for (int bj = 0; bj < NBN; ++bj) {
           f32x16 blk = acc[bi][bj];
           asm volatile("" : "+v"(blk));
 #pragma unroll
           for (int b = 0; b < 4; ++b)
-            *reinterpret_cast<f32x4 *>(base + ((2 * bi * TF + 2 * bj) * 64 + 16 * b) * 4) =
+            *reinterpret_cast<f32x4 *>(base + ((2 * bi * TFN + 2 * bj) * 64 + 16 * b) * 4) =
                 f32x4{blk[4 * b], blk[4 * b + 1], blk[4 * b + 2], blk[4 * b + 3]};
           asm volatile("" ::: "memory");
         }
@@ -862,7 +896,7 @@ __global__ __launch_bounds__(kFixThreads) void k_gemm_fix(GemmProblem p, int P) 
     int rt, tn;
     tile_coords(q, t, rt, tn);
     const TileRows tr = decode_row_tile(p, BM, rt);
-    T::template epilogue_rows<EPI, 1, F8>(p, tr, tn * BN, wid, i, lane, acc);
+    T::template epilogue_rows<EPI, 1, F8>(p, tr, q.c0 + tn * BN, wid, i, lane, acc);
   }
 }
 
@@ -931,22 +965,35 @@ int device_cus() {
   return ncu[dev];
 }
 
-// Square TB x TB tiles: one persistent workgroup per CU.
-template <int TB, int ROLE, bool F8 = false>
+// BM x BN tiles: one persistent workgroup per CU.  The second launch of a split projection
+// (phase 2) holds at most one wave of tiles, so it leaves partial tiles only for a long K.
+template <int BM, int BN, int ROLE, bool F8 = false>
 static hipError_t run_big(const GemmProblem &p, hipStream_t st) {
-  constexpr int BM = TB, BN = TB;
   static_assert(size_t(BM) * BN * 3 * kBigMaxWorkgroups * sizeof(float) <= kSkPartBytes, "partial area too small");
   const int P = device_cus() < kBigMaxWorkgroups ? device_cus() : kBigMaxWorkgroups;
-  hipLaunchKernelGGL((k_gemm_big<TB, role_epilogue(ROLE), ROLE, F8>), dim3(P), dim3(256), 0, st, p);
+  hipLaunchKernelGGL((k_gemm_big<BM, BN, role_epilogue(ROLE), ROLE, F8>), dim3(P), dim3(256), 0, st, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  const bool long_k = p.K / (F8 ? 128 : 64) > kNoSplitSteps;
   const long long tiles_max = (long long)p.B * ((p.max_img_rows + BM - 1) / BM + (p.L + BM - 1) / BM) *
                               ((p.N + BN - 1) / BN);
-  if (tiles_max < P && p.K / (F8 ? 128 : 64) <= kNoSplitSteps) return hipSuccess;
+  if (p.phase == 2 ? !long_k : (tiles_max < P && !long_k)) return hipSuccess;
   // P workgroups stride over the fixup's items: few enough that a launch with nothing to finish
   // (the device's row counts led to whole tiles) costs little
   hipLaunchKernelGGL((k_gemm_fix<BM, BN, 2, 2, role_epilogue(ROLE), ROLE, F8>), dim3(P), dim3(kFixThreads), 0, st, p, P);
   return hipGetLastError();
+}
+
+// A projection in two launches (phase 1: 256 x 256 tiles, phase 2: 256 x 192 tiles; the column split
+// is decided on the device, see col_range).
+template <int ROLE, bool F8 = false>
+static hipError_t run_split(const GemmProblem &p, hipStream_t st) {
+  GemmProblem a = p;
+  a.phase = 1;
+  hipError_t e = run_big<256, 256, ROLE, F8>(a, st);
+  if (e != hipSuccess) return e;
+  a.phase = 2;
+  return run_big<256, 192, ROLE, F8>(a, st);
 }
 
 template <int EPI>
@@ -969,24 +1016,26 @@ hipError_t launch_gemm(bool bf16, int role, const GemmProblem &p, hipStream_t st
       default: return run_f32<EPI_RESID>(p, st);
     }
   }
-  // Tiling per projection, as measured on the 64 x 64 workload (2766 rows): QKV and MLP up run
-  // 256 x 256 tiles (QKV: 396 tiles, two waves of whole tiles; MLP up: 528 tiles, two waves plus a
-  // short stream-K tail); the attention output and MLP down projections (N = 3072) run 192 x 192
-  // tiles, 240 of them: one wave on 256 CUs with no K split and no partials.
+  // Tiling per projection, as measured on the 64 x 64 workload (2766 rows): QKV split in two
+  // launches (253 tiles of 256 x 256 over its first 23 column tiles, then 198 tiles of 256 x 192
+  // over the other 3328 columns: one wave each, where 396 tiles of 256 x 256 took two); MLP up
+  // 256 x 256 tiles (528 tiles: two waves plus a short stream-K tail); the attention output and MLP
+  // down projections (N = 3072) 192 x 192 tiles, 240 of them: one wave on 256 CUs with no K split
+  // and no partials.
   switch (role) {
-    case GEMM_QKV: return run_big<256, GEMM_QKV>(p, st);
-    case GEMM_O: return run_big<192, GEMM_O>(p, st);
-    case GEMM_FC1: return run_big<256, GEMM_FC1>(p, st);
-    default: return run_big<192, GEMM_FC2>(p, st);
+    case GEMM_QKV: return run_split<GEMM_QKV>(p, st);
+    case GEMM_O: return run_big<192, 192, GEMM_O>(p, st);
+    case GEMM_FC1: return run_big<256, 256, GEMM_FC1>(p, st);
+    default: return run_big<192, 192, GEMM_FC2>(p, st);
   }
 }
 
 hipError_t launch_gemm_fp8(int role, const GemmProblem &p, hipStream_t st) {
   switch (role) {
-    case GEMM_QKV: return run_big<256, GEMM_QKV, true>(p, st);
-    case GEMM_O: return run_big<192, GEMM_O, true>(p, st);
-    case GEMM_FC1: return run_big<256, GEMM_FC1, true>(p, st);
-    default: return run_big<192, GEMM_FC2, true>(p, st);
+    case GEMM_QKV: return run_split<GEMM_QKV, true>(p, st);
+    case GEMM_O: return run_big<192, 192, GEMM_O, true>(p, st);
+    case GEMM_FC1: return run_big<256, 256, GEMM_FC1, true>(p, st);
+    default: return run_big<192, 192, GEMM_FC2, true>(p, st);
   }
 }
 

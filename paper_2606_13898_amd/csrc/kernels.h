@@ -70,6 +70,10 @@ struct GemmProblem {
   float *part;            // bf16 path: partial tiles (kSkPartBytes)
   const float *a_scale;   // FP8 operands: A row m is codes * a_scale[m] ...
   const float *w_scale[2];  // ... and W row n of stream s is codes * w_scale[s][n]
+  // 0: all N columns.  1 / 2: the two launches of a split projection (launch_gemm for QKV): the
+  // leading 256-column tiles one wave of 256 x 256 tiles can hold, then the remaining columns in
+  // 256 x 192 tiles -- decided on the device from the row counts, identically in both launches.
+  int phase;
 };
 
 // Partial-sum area of the GEMMs (part of the caller's workspace): one slot per data-parallel unit

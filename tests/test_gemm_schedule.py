@@ -125,3 +125,43 @@ def test_schedule_random_cases():
     r = random.Random(0)
     for _ in range(600):
         check(r.randint(0, 700), r.choice([1, 2, 7, 64, 255, 256]), r.randint(1, 200))
+
+
+# The column split of a two-launch projection (gemm.hip: col_range): R row tiles of 256 rows, N
+# columns, P workgroups.  Phase 1 takes [0, split) in 256 x 256 tiles, phase 2 [split, N) in
+# 256 x 192 tiles.
+def col_split(R, N, P):
+    TN = -(-N // 256)
+    split = N
+    if R > 0 and P < R * TN <= 2 * P:
+        ta = P // R
+        if ta >= 1 and R * (-(-(N - ta * 256) // 192)) <= P:
+            split = ta * 256
+    return split
+
+
+def test_qkv_split_at_the_64x64_workload():
+    # 2254 image rows (9 tiles) + 512 text rows (2): 11 row tiles; QKV N = 9216 on 256 CUs
+    split = col_split(11, 9216, 256)
+    assert split == 23 * 256
+    assert 11 * 23 == 253 and 11 * -(-(9216 - split) // 192) == 198
+    # the MLP up projection (528 tiles, more than two waves) is not split
+    assert col_split(11, 12288, 256) == 12288
+
+
+@pytest.mark.parametrize("seed", range(100))
+def test_col_split_partitions_the_columns_into_single_waves(seed):
+    r = random.Random(seed)
+    P = r.choice([64, 104, 256, 304])
+    R = r.randint(1, 40)
+    N = 64 * r.randint(1, 300)
+    split = col_split(R, N, P)
+    assert 0 < split <= N
+    if split < N:
+        # both launches are one wave of whole tiles, and together they cover every column once
+        assert split % 256 == 0
+        assert R * (split // 256) <= P
+        assert R * -(-(N - split) // 192) <= P
+        assert R * -(-N // 256) > P  # only a projection that needed a second wave is split
+    else:
+        assert not (P < R * -(-N // 256) <= 2 * P) or R * -(-(N - (P // R) * 256) // 192) > P or P // R < 1

@@ -81,9 +81,9 @@ def summarize_mfma(out):
     state = {}
     for _, (name, dur, cs) in load_multi(path).items():
         k = kind_of(name, state)
-        if k is None or not primary(name):
+        if k is None or not is_main(name):
             continue
-        n[k] += 1
+        n[k] += 1 if primary(name) else 0
         agg[k]["dur_ns"] += dur
         for c, v in cs.items():
             agg[k][c] += v
@@ -99,7 +99,8 @@ def summarize_mfma(out):
              "dispatch's GPU cycles the matrix cores were busy (the counter adds 32 cycles per "
              "32x32x16 and 16 per 16x16x32 bf16 MFMA over all SIMDs; GRBM_GUI_ACTIVE adds the "
              "dispatch's cycles over the %d XCDs).  Main kernels only (the GEMM fixups and the "
-             "attention merge issue no MFMA)." % (SIMDS, XCDS, XCDS), "",
+             "attention merge issue no MFMA); the QKV projection's two launches count as one call." %
+             (SIMDS, XCDS, XCDS), "",
              "Command:", "", "    " + commands(out)[-1], "",
              "| kind | us | clock GHz | MFMA busy | MFMA insts | VALU insts | VALU per MFMA |",
              "|---|---:|---:|---:|---:|---:|---:|"]
@@ -125,16 +126,16 @@ def load(out, cnt, tag):
 
 
 def gemm_role(base):
-    """Projection of a GEMM kernel from its template arguments: k_gemm_sk<BM, BN, WM, WN, EPI, ROLE>,
-    k_gemm_fix<BM, BN, WM, WN, EPI, ROLE, F8>, k_gemm_big<TB, EPI, ROLE, F8>."""
+    """Projection of a GEMM kernel from its template arguments: k_gemm_fix<BM, BN, WM, WN, EPI, ROLE,
+    F8>, k_gemm_big<BM, BN, EPI, ROLE, F8>."""
     args = [a.strip() for a in base[base.index("<") + 1:base.rindex(">")].split(",")]
-    return ROLES[args[2] if base.startswith("hilo::k_gemm_big") else args[5]]
+    return ROLES[args[3] if base.startswith("hilo::k_gemm_big") else args[5]]
 
 
 def kind_of(name, state):
     """Bench kernel kind of a dispatch; rownorm launches alternate attention / MLP per step."""
     base = name.split("(")[0].replace("void ", "").strip()
-    if "k_gemm_sk<" in base or "k_gemm_fix<" in base or "k_gemm_big<" in base:
+    if "k_gemm_fix<" in base or "k_gemm_big<" in base:
         return gemm_role(base)
     if "k_attn" in base:
         return "attention_core"
@@ -149,9 +150,15 @@ def kind_of(name, state):
     return None
 
 
-def primary(name):
-    """The first kernel of each kind's call (its dispatch count = the number of calls)."""
+def is_main(name):
+    """A kernel that does a call's MFMA work (not a GEMM fixup or the attention merge)."""
     return "k_gemm_fix" not in name and "k_attn_fix" not in name
+
+
+def primary(name):
+    """The first kernel of each kind's call (its dispatch count = the number of calls): a main
+    kernel, and not the second launch of a split projection (its 256 x 192 tiles)."""
+    return is_main(name) and "k_gemm_big<256, 192," not in name
 
 
 def summarize(out):
