@@ -8,7 +8,8 @@
 // wave of 256 x 256 tiles cannot hold) or 192 x 192 (attention output, MLP down) as
 // 32 x 32 MFMA blocks (v_mfma_f32_32x32x16_bf16, or v_mfma_f32_32x32x64_f8f6f4 on E4M3 codes),
 // fp32 accumulators in AGPRs, K in 64-byte stages through a 4-slot LDS ring filled by direct
-// global->LDS loads.  Whole data-parallel waves of tiles run first, then a stream-K remainder;
+// global->LDS loads (192 x 192 tiles: 128-byte K-step windows, both stages of a row's K step
+// together, through a 3-slot ring).  Whole data-parallel waves of tiles run first, then a stream-K remainder;
 // cut tiles leave fp32 partials that k_gemm_fix adds in a fixed order before the epilogue.
 // float32 path: a plain LDS-tiled FMA kernel for the small float32 workloads.
 #include <type_traits>
@@ -393,7 +394,8 @@ struct SkTile {
 // loads half the operand bytes per FLOP of a 128 x 128 tile (BM x BN tiles: BM/64 x BN/64 blocks per
 // wave, the same schedule).  K runs in stages of 64 bytes per row (32 bf16 or 64 FP8 values)
 // through a 4-slot LDS ring (32 KiB per 256 x 256 stage: the stage's A rows, then its W rows, 16-byte
-// chunks swizzled), loaded by direct global->LDS loads three stages ahead.  A 256 x 256 stage is
+// chunks swizzled), loaded by direct global->LDS loads three stages ahead (window mode, below: the
+// LDS holds three 128-byte K-step windows per row, loaded two K steps ahead).  A 256 x 256 stage is
 // 16 blocks:
 //   * bf16: two v_mfma_f32_32x32x16_bf16 per block, one per K half (chunks {h, h + 2});
 //   * FP8:  one v_mfma_f32_32x32x64_f8f6f4 per block (all four chunks, 8 registers per operand).
@@ -450,11 +452,25 @@ struct Geo {
   static constexpr int NR = 2 * LQ;          // fragment reads per wave per stage
   static constexpr int AB = BM * 64;         // bytes of a stage's A rows
   static constexpr int SB = (BM + BN) * 64;  // bytes of a stage
-  static constexpr int LDS = S * SB + 4 * kEpiWave;
+  // Window mode: when three K steps of the tile fit in LDS, each row's 128 bytes of a K step (both
+  // of its stages) stay together, so one load instruction fetches 8 whole 128-byte lines instead of
+  // 16 half lines (measured: fewer, fuller requests to the L2); three window slots keep the loads
+  // two K steps ahead.  The 256-wide tiles hold only two windows, and one K step of prefetch
+  // measured slower than the half-line ring.
+  static constexpr int WS = 3;                          // window slots
+  static constexpr int SBW = (BM + BN) * 128;           // bytes of a window
+  static constexpr bool WIN = BM == BN && WS * SBW + 4 * kEpiWave <= 160 * 1024;
+  static constexpr int LDS = WIN ? WS * SBW + 4 * kEpiWave : S * SB + 4 * kEpiWave;
   // every load and fragment read of a stage is issued after its barrier (block NBN) and before
-  // its last block
+  // its last block; in window mode a stage loads BM / 32 instructions of 8 rows (its wave's A rows
+  // in the first stage of a K step, its W rows in the second), the same count as LQ for BM == BN
   static_assert(NBN + LQ <= NBM * NBN, "stage schedule does not fit the blocks");
+  static_assert(!WIN || BM / 32 == LQ, "window loads per stage");
 };
+// Chunk swizzle of a 128-byte window row: the 16-byte chunk that global chunk c of row r occupies is
+// c ^ swzw(r).  A ds_read_b128 serves 16 lanes per cycle from 64 banks; with it every 16-lane group
+// of a fragment read (16 consecutive rows, or the perm_w rows of W) hits 16 distinct bank groups.
+HILO_DEV int swzw(int r) { return ((r >> 1) & 3) ^ ((((r >> 3) ^ (r >> 4)) & 1) << 2); }
 }  // namespace big
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -586,6 +602,8 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
   using namespace big;
   using G = Geo<BM, BN>;
   constexpr int NBM = G::NBM, NBN = G::NBN, LQ = G::LQ, NR = G::NR, AB = G::AB, SB = G::SB;
+  constexpr bool WIN = G::WIN;
+  constexpr int SBW = G::SBW, NLA = WIN ? 2 * NBM : NBM, NLB = WIN ? 2 * NBN : NBN;
   using T = SkTile<BM, BN, 2, 2>;       // partial slot size and layout (16 x 16 fragment order)
   constexpr int ESZ = F8 ? 1 : 2;       // operand bytes per element
   __shared__ __attribute__((aligned(1024))) uint8_t lds[G::LDS];
@@ -600,35 +618,48 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
   const int lrow = lane >> 2, lslot = lane & 3;
   const uint8_t *A = reinterpret_cast<const uint8_t *>(p.A);
 
-  // ---- loader: its own cursor over this workgroup's items, three stages ahead of the MFMAs; wave
-  // wid loads rows wid BM/4 .. + BM/4 - 1 of A and wid BN/4 .. + BN/4 - 1 of W, 16 rows (1 KiB) per
-  // instruction
+  // ---- loader: its own cursor over this workgroup's items, three stages ahead of the MFMAs (window
+  // mode: two K steps ahead); wave wid loads rows wid BM/4 .. + BM/4 - 1 of A and wid BN/4 .. +
+  // BN/4 - 1 of W, 16 rows of 64 bytes (window mode: 8 rows of 128 bytes) per 1 KiB instruction
   SkCursor lc{pid, rg.beg};
-  const uint8_t *la[NBM], *lb[NBN];
-  int lk = 0, lke = 0;  // next stage to load (absolute in K) and the end of its item
+  const uint8_t *la[NLA], *lb[NLB];
+  int lk = 0, lke = 0;  // next stage (window mode: K step) to load, absolute in K, and its item's end
   auto ld_src = [&](int t) __attribute__((always_inline)) {
     int rt, tn;
     tile_coords(q, t, rt, tn);
     tn = uni(tn);
     const TileRows tr = uni(decode_row_tile(p, BM, uni(rt)));
     const uint8_t *Wt = reinterpret_cast<const uint8_t *>(tr.sigma ? p.W[1] : p.W[0]);
+    if constexpr (WIN) {
 #pragma unroll
-    for (int i = 0; i < NBM; ++i) {
-      const int r = wid * (BM / 4) + 16 * i + lrow;
-      la[i] = A + size_t(tr.row0 + min(r, tr.nrows - 1)) * p.lda * ESZ + (lslot ^ swz(r)) * 16;
-    }
+      for (int i = 0; i < NLA; ++i) {
+        const int r = wid * (BM / 4) + 8 * i + (lane >> 3);
+        la[i] = A + size_t(tr.row0 + min(r, tr.nrows - 1)) * p.lda * ESZ + ((lane & 7) ^ swzw(r)) * 16;
+      }
 #pragma unroll
-    for (int i = 0; i < NBN; ++i) {
-      const int r = wid * (BN / 4) + 16 * i + lrow;
-      lb[i] = Wt + size_t(min(q.c0 + tn * BN + r, p.N - 1)) * p.K * ESZ + (lslot ^ swz(r)) * 16;
+      for (int i = 0; i < NLB; ++i) {
+        const int r = wid * (BN / 4) + 8 * i + (lane >> 3);
+        lb[i] = Wt + size_t(min(q.c0 + tn * BN + r, p.N - 1)) * p.K * ESZ + ((lane & 7) ^ swzw(r)) * 16;
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < NBM; ++i) {
+        const int r = wid * (BM / 4) + 16 * i + lrow;
+        la[i] = A + size_t(tr.row0 + min(r, tr.nrows - 1)) * p.lda * ESZ + (lslot ^ swz(r)) * 16;
+      }
+#pragma unroll
+      for (int i = 0; i < NBN; ++i) {
+        const int r = wid * (BN / 4) + 16 * i + lrow;
+        lb[i] = Wt + size_t(min(q.c0 + tn * BN + r, p.N - 1)) * p.K * ESZ + (lslot ^ swz(r)) * 16;
+      }
     }
   };
   auto ld_advance = [&]() __attribute__((always_inline)) {
     const SkItem x = uni(sk_next_item(lc, q, rg, P, pid, p.part, T::kPartFloats));
     if (x.valid) {
       ld_src(x.t);
-      lk = 2 * x.kb;
-      lke = 2 * x.ke;
+      lk = WIN ? x.kb : 2 * x.kb;
+      lke = WIN ? x.ke : 2 * x.ke;
     } else {
       lk = lke - 1;  // no further item: repeat the last stage
     }
@@ -641,6 +672,13 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
     if (j < NBM) g2lds16(la[j] + k0, lds + slot * SB + wid * (BM / 4) * 64 + j * 1024);
     else g2lds16(lb[j - NBM] + k0, lds + slot * SB + AB + wid * (BN / 4) * 64 + (j - NBM) * 1024);
   };
+  // window mode: load instruction j of half h (0: the wave's A rows, 1: its W rows) of the loader's
+  // K step into window slot `ws`
+  auto ld_win = [&](int ws, int h, int j) __attribute__((always_inline)) {
+    const int k0 = lk * 128;  // bytes
+    if (h == 0) g2lds16(la[j] + k0, lds + ws * SBW + (wid * (BM / 4) + 8 * j) * 128);
+    else g2lds16(lb[j] + k0, lds + ws * SBW + BM * 128 + (wid * (BN / 4) + 8 * j) * 128);
+  };
 
   // ---- fragment reads: lane (r, g) = (lane % 32, lane / 32) reads chunk 2 g (low half) and 2 g + 1
   // (high half) of row r (A) or perm_w(r) (W) of a 32-row fragment; read t of a stage (slot byte
@@ -650,13 +688,25 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
   const uint32_t fa8 = lds0 + (wid >> 1) * (BM / 2) * 64, fb8 = lds0 + AB + (wid & 1) * (BN / 2) * 64;
   const uint32_t fa8l = fa8 + r8 * 64 + (((2 * g8) ^ swz(r8)) * 16), fa8h = fa8 + r8 * 64 + (((2 * g8 + 1) ^ swz(r8)) * 16);
   const uint32_t fb8l = fb8 + w8 * 64 + (((2 * g8) ^ swz(w8)) * 16), fb8h = fb8 + w8 * 64 + (((2 * g8 + 1) ^ swz(w8)) * 16);
-  auto rd_one = [&](u32x4 (&fa)[2 * NBM], u32x4 (&fb)[2 * NBN], uint32_t so, int t) __attribute__((always_inline)) {
+  // window mode: the same lane mapping on 128-byte rows; half h (0, 1) of a K step holds its global
+  // chunks 4 h .. 4 h + 3, and a fragment spans 32 rows of 128 bytes
+  const uint32_t wa = lds0 + (wid >> 1) * (BM / 2) * 128 + r8 * 128;
+  const uint32_t wb = lds0 + BM * 128 + (wid & 1) * (BN / 2) * 128 + w8 * 128;
+  const uint32_t fwa[4] = {wa + (((2 * g8) ^ swzw(r8)) * 16), wa + (((2 * g8 + 1) ^ swzw(r8)) * 16),
+                           wa + (((4 + 2 * g8) ^ swzw(r8)) * 16), wa + (((5 + 2 * g8) ^ swzw(r8)) * 16)};
+  const uint32_t fwb[4] = {wb + (((2 * g8) ^ swzw(w8)) * 16), wb + (((2 * g8 + 1) ^ swzw(w8)) * 16),
+                           wb + (((4 + 2 * g8) ^ swzw(w8)) * 16), wb + (((5 + 2 * g8) ^ swzw(w8)) * 16)};
+  constexpr int FRB = WIN ? 4096 : 2048;  // bytes between fragments
+  // read t of the stage at byte offset so; hs: the stage's half of its K step (window mode only)
+  auto rd_one = [&](u32x4 (&fa)[2 * NBM], u32x4 (&fb)[2 * NBN], uint32_t so, int t, int hs) __attribute__((always_inline)) {
+    const uint32_t al = WIN ? fwa[2 * hs] : fa8l, ah = WIN ? fwa[2 * hs + 1] : fa8h;
+    const uint32_t bl = WIN ? fwb[2 * hs] : fb8l, bh = WIN ? fwb[2 * hs + 1] : fb8h;
 #define HILO_RD_CASE(C)                                                                                     \
   case C:                                                                                                   \
     if constexpr (C < 2 * NBN)                                                                              \
-      HILO_DS_READ16(fb[C % (2 * NBN)], ((C & 1) ? fb8h : fb8l) + so, ((C % (2 * NBN)) >> 1) * 2048);       \
+      HILO_DS_READ16(fb[C % (2 * NBN)], ((C & 1) ? bh : bl) + so, ((C % (2 * NBN)) >> 1) * FRB);            \
     else if constexpr (C < 2 * NBN + 2 * NBM)                                                               \
-      HILO_DS_READ16(fa[(C - 2 * NBN) % (2 * NBM)], ((C & 1) ? fa8h : fa8l) + so, (((C - 2 * NBN) % (2 * NBM)) >> 1) * 2048); \
+      HILO_DS_READ16(fa[(C - 2 * NBN) % (2 * NBM)], ((C & 1) ? ah : al) + so, (((C - 2 * NBN) % (2 * NBM)) >> 1) * FRB); \
     break;
     switch (t) {
       HILO_RD_CASE(0) HILO_RD_CASE(1) HILO_RD_CASE(2) HILO_RD_CASE(3) HILO_RD_CASE(4) HILO_RD_CASE(5)
@@ -669,7 +719,7 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
 
   // ---- epilogue operands of the current item: this wave's BN/2 columns (and FP8 rows) into its
   // LDS area, by DMA (4 bytes per lane), indices clamped into the tile
-  uint8_t *epi = lds + S * SB + wid * kEpiWave;
+  uint8_t *epi = lds + (WIN ? G::WS * SBW : S * SB) + wid * kEpiWave;
   TileRows etr{0, 0, 0, 1};
   int en0 = 0;
   auto epi_load = [&]() __attribute__((always_inline)) {
@@ -700,10 +750,20 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
   // stage of a tile (first = true_type) starts the accumulators from zero and, for a tile finished
   // here, fetches the epilogue operands after its loads.  Before block NBN: barrier; after each of
   // blocks NBN .. NBN + LQ - 1: one load of the stage three ahead and two fragment reads of the next.
-  auto stage = [&](auto first, u32x4 (&fa)[2 * NBM], u32x4 (&fb)[2 * NBN], u32x4 (&na)[2 * NBM],
+  auto stage = [&](auto first, auto odd, u32x4 (&fa)[2 * NBM], u32x4 (&fb)[2 * NBN], u32x4 (&na)[2 * NBM],
                    u32x4 (&nb)[2 * NBN], int gs, bool with_epi) __attribute__((always_inline)) {
-    const int lslot_w = (gs + S - 1) & (S - 1);
-    const uint32_t so = uint32_t(((gs + 1) & (S - 1)) * SB);
+    constexpr bool ODD = decltype(odd)::value;  // second stage of its K step
+    int lslot_w;
+    uint32_t so;
+    if constexpr (WIN) {
+      // window slot of this K step; loads go two K steps ahead, reads to the next stage
+      const int w3 = (gs >> 1) % G::WS;
+      lslot_w = w3 == 0 ? G::WS - 1 : w3 - 1;
+      so = uint32_t((ODD ? (w3 == G::WS - 1 ? 0 : w3 + 1) : w3) * SBW);
+    } else {
+      lslot_w = (gs + S - 1) & (S - 1);
+      so = uint32_t(((gs + 1) & (S - 1)) * SB);
+    }
 #pragma unroll
     for (int bi = 0; bi < NBM; ++bi) {
       // outstanding reads allowed: this stage's A halves of blocks bi+1.., the next stage's so far
@@ -711,7 +771,15 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
 #pragma unroll
       for (int bj = 0; bj < NBN; ++bj) {
         const int qq = NBN * bi + bj;
-        if (qq == NBN) asm volatile("s_waitcnt vmcnt(%0)\n s_barrier" ::"n"((S - 3) * LQ) : "memory");
+        if (qq == NBN) {
+          // window mode: the second stage of K step w waits for K step w + 1 (only the loads of w + 2
+          // issued by the first stage may be outstanding); the first stage reads the second half of
+          // its own K step, which is complete already.  Either barrier also frees the slot the stage
+          // loads into: every wave has finished the K step before.
+          if constexpr (!WIN) asm volatile("s_waitcnt vmcnt(%0)\n s_barrier" ::"n"((S - 3) * LQ) : "memory");
+          else if constexpr (ODD) asm volatile("s_waitcnt vmcnt(%0)\n s_barrier" ::"n"(LQ) : "memory");
+          else asm volatile("s_barrier" ::: "memory");
+        }
         if constexpr (F8) {
           if constexpr (decltype(first)::value)
             HILO_MFMA8_AGPR0(acc[bi][bj], cat8(fb[2 * bj], fb[2 * bj + 1]), cat8(fa[2 * bi], fa[2 * bi + 1]));
@@ -723,32 +791,54 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
           HILO_MFMA16_AGPR(acc[bi][bj], fb[2 * bj + 1], fa[2 * bi + 1]);
         }
         if (qq >= NBN && qq < NBN + LQ) {
-          ld_one(lslot_w, qq - NBN);
-          rd_one(na, nb, so, 2 * (qq - NBN));
-          rd_one(na, nb, so, 2 * (qq - NBN) + 1);
+          if constexpr (WIN) {
+            // the epilogue DMA goes ahead of the stage's loads, so the next stage's vmcnt covers it
+            if constexpr (decltype(first)::value) {
+              if (qq == NBN && with_epi) epi_load();
+            }
+            ld_win(lslot_w, ODD ? 1 : 0, qq - NBN);
+          } else {
+            ld_one(lslot_w, qq - NBN);
+          }
+          rd_one(na, nb, so, 2 * (qq - NBN), ODD ? 0 : 1);
+          rd_one(na, nb, so, 2 * (qq - NBN) + 1, ODD ? 0 : 1);
         }
-        if constexpr (decltype(first)::value) {
+        if constexpr (decltype(first)::value && !WIN) {
           if (qq == NBN + LQ - 1 && with_epi) epi_load();
         }
       }
     }
-    ++lk;
+    if constexpr (!WIN || ODD) ++lk;
   };
 
   SkCursor cc{pid, rg.beg};
   SkItem cur = uni(sk_next_item(cc, q, rg, P, pid, p.part, T::kPartFloats));
   if (!cur.valid) return;
   ld_advance();  // the same first item
+  if constexpr (WIN) {
+    // the first two K steps, then wait for the first
 #pragma unroll 1
-  for (int st = 0; st < S - 1; ++st) {
-    if (lk == lke) ld_advance();
+    for (int wv = 0; wv < G::WS - 1; ++wv) {
+      if (lk == lke) ld_advance();
 #pragma unroll
-    for (int j = 0; j < LQ; ++j) ld_one(st, j);
-    ++lk;
+      for (int j = 0; j < NLA; ++j) ld_win(wv, 0, j);
+#pragma unroll
+      for (int j = 0; j < NLB; ++j) ld_win(wv, 1, j);
+      ++lk;
+    }
+    asm volatile("s_waitcnt vmcnt(%0)\n s_barrier" ::"n"(NLA + NLB) : "memory");
+  } else {
+#pragma unroll 1
+    for (int st = 0; st < S - 1; ++st) {
+      if (lk == lke) ld_advance();
+#pragma unroll
+      for (int j = 0; j < LQ; ++j) ld_one(st, j);
+      ++lk;
+    }
+    asm volatile("s_waitcnt vmcnt(%0)\n s_barrier" ::"n"((S - 2) * LQ) : "memory");
   }
-  asm volatile("s_waitcnt vmcnt(%0)\n s_barrier" ::"n"((S - 2) * LQ) : "memory");
 #pragma unroll
-  for (int t = 0; t < NR; ++t) rd_one(xa, xb, 0, t);
+  for (int t = 0; t < NR; ++t) rd_one(xa, xb, 0, t, 0);
 
   // the loader moves to its next item between stages, outside the MFMA schedule
   auto ld_check = [&]() __attribute__((always_inline)) {
@@ -764,16 +854,16 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
       etr = uni(decode_row_tile(p, BM, uni(rt)));
     }
     ld_check();
-    stage(std::true_type{}, xa, xb, ya, yb, gs, whole);
+    stage(std::true_type{}, std::false_type{}, xa, xb, ya, yb, gs, whole);
     ld_check();
-    stage(std::false_type{}, ya, yb, xa, xb, gs + 1, false);
+    stage(std::false_type{}, std::true_type{}, ya, yb, xa, xb, gs + 1, false);
     gs += 2;
 #pragma unroll 1
     for (int kt = cur.kb + 1; kt < cur.ke; ++kt) {
       ld_check();
-      stage(std::false_type{}, xa, xb, ya, yb, gs, false);
+      stage(std::false_type{}, std::false_type{}, xa, xb, ya, yb, gs, false);
       ld_check();
-      stage(std::false_type{}, ya, yb, xa, xb, gs + 1, false);
+      stage(std::false_type{}, std::true_type{}, ya, yb, xa, xb, gs + 1, false);
       gs += 2;
     }
     // The last MFMAs' results must land before the accumulators are read (the empty asm ties each
@@ -786,8 +876,9 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
       for (int j = 0; j < NBN; ++j) asm volatile("" : "+a"(acc[i][j]));
     if (whole) {
       // the epilogue-operand DMA of the first stage is complete once two later stages have passed
-      // their barriers (each waits for all but the last stage's loads); a one-step item waits here
-      if (cur.ke - cur.kb < 2) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      // their barriers (each waits for all but the last stage's loads); a one-step item waits here.
+      // In window mode the item's second stage waited for it already.
+      if (!WIN && cur.ke - cur.kb < 2) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
       big_epilogue<BM, BN, EPI, F8>(p, etr, en0, wid, lane, epi, acc);
     } else {
       // the partial tile in the 16 x 16 fragment layout k_gemm_fix reads (2 NBM x 2 NBN fragments per
