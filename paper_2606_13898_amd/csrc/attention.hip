@@ -112,7 +112,7 @@ struct AttnUnit {
 HILO_DEV long long attn_iterations(const int *cu, int B, int heads, int BQ) {
   long long I = 0;
   for (int s = 0; s < B; ++s) {
-    const int n = cu[s + 1] - cu[s];
+    const int n = cu_at(cu, s + 1) - cu_at(cu, s);
     I += (long long)heads * ((n + BQ - 1) / BQ) * ((n + 63) / 64);
   }
   return I;
@@ -121,7 +121,7 @@ HILO_DEV long long attn_iterations(const int *cu, int B, int heads, int BQ) {
 HILO_DEV AttnUnit attn_unit(const int *cu, int B, int heads, int BQ, long long it) {
   long long base = 0;
   for (int s = 0; s < B; ++s) {
-    const int n = cu[s + 1] - cu[s];
+    const int n = cu_at(cu, s + 1) - cu_at(cu, s);
     const int qtiles = (n + BQ - 1) / BQ, nkv = (n + 63) / 64;
     const long long span = (long long)heads * qtiles * nkv;
     if (it < base + span) {
@@ -162,7 +162,7 @@ template <int HD, int QW, int NW>
 HILO_DEV void attn_store_out(const AttnArgs &a, const AttnUnit &u, int wid, int lane,
                              f32x4 (&o)[QW / 16][HD / 16], const float (&l)[QW / 16]) {
   constexpr int QS = QW / 16, DS = HD / 16;
-  const int lo = a.cu[u.s], n = a.cu[u.s + 1] - lo;
+  const int lo = cu_at(a.cu, u.s), n = cu_at(a.cu, u.s + 1) - lo;
   const int D = a.heads * HD;
   const int lr = lane & 15, lg = lane >> 4;
 #pragma unroll
@@ -212,8 +212,8 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void k_attn_bf16(AttnArgs a) {
     const AttnUnit u = attn_unit(a.cu, a.B, a.heads, BQ, it);
     const int kb = int(it - u.start);
     const int ke = int(min((long long)u.nkv, (long long)kb + (end - it)));
-    const int lo = a.cu[u.s];
-    const int n = a.cu[u.s + 1] - lo;
+    const int lo = cu_at(a.cu, u.s);
+    const int n = cu_at(a.cu, u.s + 1) - lo;
     const int q0 = u.qt * BQ;
     const uint16_t *Q = a.qkv + size_t(lo) * ld + size_t(u.h) * HD;
     const uint16_t *Kp = Q + D;

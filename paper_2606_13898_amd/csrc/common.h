@@ -63,6 +63,12 @@ HILO_DEV float wave_sum_f32(float v) {
   return v;
 }
 
+// Sample boundary i of the packed sequence.  The boundaries do not change while a kernel runs, so
+// they are read through the constant address space: the compiler then uses scalar loads with their
+// own wait, where a vector load inside a pipelined loop is followed by a wait for every global load
+// in flight (a drained prefetch per tile or unit).
+HILO_DEV int cu_at(const int *cu, int i) { return ((const __attribute__((address_space(4))) int *)cu)[i]; }
+
 // Sample that packed row r belongs to: largest s with cu[s] <= r (cu has B+1 entries).
 HILO_DEV int sample_of_row(const int32_t *cu, int B, int r) {
   int lo = 0, hi = B;  // answer in [lo, hi)

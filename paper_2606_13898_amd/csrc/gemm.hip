@@ -110,7 +110,7 @@ HILO_DEV void g2lds16(const void *g, void *lds_wave_base) {
 HILO_DEV int row_tiles_total(const GemmProblem &p, int BM) {
   int R = 0;
   for (int s = 0; s < p.B; ++s) {
-    const int nimg = p.cu[s + 1] - p.L - p.cu[s];
+    const int nimg = cu_at(p.cu, s + 1) - p.L - cu_at(p.cu, s);
     R += (nimg + BM - 1) / BM + (p.L + BM - 1) / BM;
   }
   return R;
@@ -119,7 +119,7 @@ HILO_DEV int row_tiles_total(const GemmProblem &p, int BM) {
 HILO_DEV TileRows decode_row_tile(const GemmProblem &p, int BM, int r) {
   TileRows tr{0, 0, 0, 0};
   for (int s = 0; s < p.B; ++s) {
-    const int lo = p.cu[s], hi = p.cu[s + 1], ts = hi - p.L;
+    const int lo = cu_at(p.cu, s), hi = cu_at(p.cu, s + 1), ts = hi - p.L;
     const int ti = (ts - lo + BM - 1) / BM, tt = (p.L + BM - 1) / BM;
     if (r < ti) {
       tr = TileRows{s, 0, lo + r * BM, min(BM, ts - (lo + r * BM))};
