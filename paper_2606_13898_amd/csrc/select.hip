@@ -399,6 +399,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(
       // from the highest byte any of them has set (the bytes above are zero in all of them)
       long long prefix = 0, mask = 0;
       int rem = kp;
+      bool whole_bin = false;  // the candidates with the resolved prefix are exactly the rem still needed
       for (int shift = top; shift >= 0; shift -= 8) {
         for (int d = tid; d < 256; d += kSelThreads) hist[d] = 0;
         __syncthreads();
@@ -434,39 +435,49 @@ __global__ __launch_bounds__(kSelThreads) void k_select(
           }
           const int excl = x - s;
           if (excl < rem && rem <= x) {
-            int cum = excl, d = 0;
+            int cum = excl, d = 0, hd = 0;
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
-              if (cum + h[u] >= rem) { d = 255 - 4 * tid - u; break; }
+              if (cum + h[u] >= rem) { d = 255 - 4 * tid - u; hd = h[u]; break; }
               cum += h[u];
             }
             bcast[0] = d;
             bcast[1] = rem - cum;
+            bcast[2] = rem - cum == hd ? 1 : 0;
           }
         }
         __syncthreads();
         prefix |= (long long)bcast[0] << shift;
         mask |= 255LL << shift;
         rem = bcast[1];
+        whole_bin = bcast[2] != 0;
         __syncthreads();
+        // every candidate of the digit's bin is selected: the lower bits cannot change the selection
+        if (whole_bin) break;
       }
       // all candidates above the threshold value, and the first `rem` equal ones in block order
       const int chunk = (NB + kSelThreads - 1) / kSelThreads;
       const int b0 = tid * chunk, b1 = min(b0 + chunk, NB);
-      int neq = 0;
-      for (int b = b0; b < b1; ++b)
-        if (!(flag[b] & 2) && Bs[b] == prefix) ++neq;
-      int tot;
-      int before = block_excl_scan(neq, itmp, tot);
-      for (int b = b0; b < b1; ++b) {
-        if (flag[b] & 2) continue;
-        if (Bs[b] > prefix) flag[b] |= 1;
-        else if (Bs[b] == prefix) {
-          if (before < rem) flag[b] |= 1;
-          ++before;
+      if (whole_bin) {  // the bin is taken whole: every candidate at or above its prefix
+        for (int b = b0; b < b1; ++b)
+          if (!(flag[b] & 2) && (Bs[b] & mask) >= prefix) flag[b] |= 1;
+        __syncthreads();
+      } else {
+        int neq = 0;
+        for (int b = b0; b < b1; ++b)
+          if (!(flag[b] & 2) && Bs[b] == prefix) ++neq;
+        int tot;
+        int before = block_excl_scan(neq, itmp, tot);
+        for (int b = b0; b < b1; ++b) {
+          if (flag[b] & 2) continue;
+          if (Bs[b] > prefix) flag[b] |= 1;
+          else if (Bs[b] == prefix) {
+            if (before < rem) flag[b] |= 1;
+            ++before;
+          }
         }
+        __syncthreads();
       }
-      __syncthreads();
     }
   }
 
