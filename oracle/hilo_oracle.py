@@ -22,7 +22,7 @@ diffusion-transformer block on the shortened sequence and the reassembly of the 
   stack      blocks in order; request = one selection, then per   (Sec. 2.3: selection once per
              step compress -> stack -> decompress                   request; Sec. 3.3: 8 steps)
   fp8        per-row E4M3 quantisation of the operands of the     (Sec. 3.3: FP8 quantisation
-             four projections                                       on top of the compression)
+             four projections and of the attention's q and k        on top of the compression)
   decompress scatter fine rows, broadcast pooled rows to 4 patches
 
 Precision.  Floating point that decides an integer (the energy that decides which blocks stay
@@ -36,7 +36,8 @@ below states the reading it implements.
 
 Parity status per function (what pins it is in tests/test_oracle_*.py):
   score, score_pixels, dilate, block_sums, select_*, compact, layout, compress, decompress,
-  attention, mlp, stack, request, e4m3_value, quantize_rows:
+  attention, mlp, stack, request, e4m3_value, quantize_rows, pow2_exponent, quantize_rows_pow2,
+  attend_codes:
   pinned by closed forms, library routines (scipy Sobel / binary dilation, torch SDPA / layer_norm
   / gelu), hand-worked fixtures under tests/golden/, and the identities of the method (0% compression
   equals the dense block, pooling a constant block then broadcasting is lossless, kept-token count
@@ -375,6 +376,35 @@ def dequant_rows(codes: np.ndarray, scale: np.ndarray) -> np.ndarray:
     return e4m3_value(codes) * np.asarray(scale, dtype=np.float64)[:, None]
 
 
+def pow2_exponent(amax: np.ndarray) -> np.ndarray:
+    """Smallest integer k with 448 * 2^k >= amax (0 where amax is 0), from the exact binary
+    decomposition amax = m * 2^E, m in [0.5, 1): 448 = 0.875 * 2^9, so k = E - 9 when m <= 0.875 and
+    E - 8 otherwise; clamped below at -127, the least E8M0 scale (a row that small still fits:
+    amax * 2^127 < 448).  amax float32 [R] -> int64 [R]."""
+    m, E = np.frexp(np.asarray(amax, dtype=np.float64))
+    k = np.maximum(np.where(m <= 0.875, E - 9, E - 8), -127).astype(np.int64)
+    return np.where(np.asarray(amax) > 0, k, 0)
+
+
+def quantize_rows_pow2(x: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
+    """Per-row FP8 E4M3 quantisation with a power-of-two scale (the form an E8M0 block scale takes):
+      k = pow2_exponent(max |x| over the row);  code = round-to-nearest-even E4M3 of x * 2^-k
+    (x * 2^-k is exact and lies in [-448, 448], so nothing saturates), code value * 2^k approximates
+    x.  x [R][C] float32 -> codes uint8 [R][C], exponents int64 [R].  (The rounding to E4M3 uses
+    torch's float8_e4m3fn cast as a library primitive.)"""
+    import torch
+
+    x = np.asarray(x, dtype=np.float32)
+    k = pow2_exponent(np.abs(x).max(axis=1))
+    y = (x.astype(np.float64) * np.exp2(-k.astype(np.float64))[:, None]).astype(np.float32)
+    codes = torch.from_numpy(y).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+    return codes, k
+
+
+def dequant_rows_pow2(codes: np.ndarray, k: np.ndarray) -> np.ndarray:
+    return e4m3_value(codes) * np.exp2(np.asarray(k, dtype=np.float64))[:, None]
+
+
 def _fp8_matmul(h: np.ndarray, q) -> np.ndarray:
     """h @ W^T with both operands FP8 per row: h quantised per row (rounded to float32 first), W given
     as its per-output-channel codes and scales q = quantize_rows(W)."""
@@ -399,6 +429,46 @@ def _attend(q: np.ndarray, k: np.ndarray, v: np.ndarray, heads: int) -> np.ndarr
         p = np.exp(sc)
         p /= p.sum(axis=1, keepdims=True)
         out[:, cols] = p @ v[:, cols]
+    return out
+
+
+def _attend_scores(qh: np.ndarray, kh: np.ndarray, v: np.ndarray) -> np.ndarray:
+    """softmax(qh kh^T / sqrt(head_dim)) v for one head given its (dequantised) q and k, float64."""
+    sc = (qh @ kh.T) / np.sqrt(qh.shape[1])
+    sc = sc - sc.max(axis=1, keepdims=True)
+    p = np.exp(sc)
+    p /= p.sum(axis=1, keepdims=True)
+    return p @ v
+
+
+def _attend_fp8(q: np.ndarray, k: np.ndarray, v: np.ndarray, heads: int) -> np.ndarray:
+    """_attend with the score product on FP8 operands: every (token, head) row of q and of k is
+    quantised per row with a power-of-two scale (quantize_rows_pow2, from the computed value rounded
+    once to float32); the probabilities and v are not quantised.  float64."""
+    D = q.shape[1]
+    hd = D // heads
+    out = np.empty((q.shape[0], D), dtype=np.float64)
+    for hh in range(heads):
+        cols = slice(hh * hd, (hh + 1) * hd)
+        qh = dequant_rows_pow2(*quantize_rows_pow2(q[:, cols].astype(np.float32)))
+        kh = dequant_rows_pow2(*quantize_rows_pow2(k[:, cols].astype(np.float32)))
+        out[:, cols] = _attend_scores(qh, kh, v[:, cols])
+    return out
+
+
+def attend_codes(q_codes: np.ndarray, q_exp: np.ndarray, k_codes: np.ndarray, k_exp: np.ndarray,
+                 v: np.ndarray, heads: int) -> np.ndarray:
+    """The FP8-score attention of one sample from given codes: q_codes / k_codes uint8 [n][D] (head h
+    in columns h*hd ..), q_exp / k_exp int [n][heads] (row scale 2^exp of each (token, head)), v
+    [n][D].  The step after the quantisation of _attend_fp8, float64."""
+    D = q_codes.shape[1]
+    hd = D // heads
+    out = np.empty((q_codes.shape[0], D), dtype=np.float64)
+    for hh in range(heads):
+        cols = slice(hh * hd, (hh + 1) * hd)
+        qh = dequant_rows_pow2(q_codes[:, cols], q_exp[:, hh])
+        kh = dequant_rows_pow2(k_codes[:, cols], k_exp[:, hh])
+        out[:, cols] = _attend_scores(qh, kh, np.asarray(v, dtype=np.float64)[:, cols])
     return out
 
 
@@ -433,7 +503,8 @@ def attention(Z: np.ndarray, cu: np.ndarray, text_len: int, heads: int, weights,
     both projections multiply FP8 rows of their input by FP8 rows of the weight (quantize_rows): each
     input row is quantised from the value the block computes (h, then the attention output a), in
     float64 rounded once to float32 (Sec. 3.3 names FP8 quantisation of the network and nothing about
-    an intermediate storage precision, so none is assumed)."""
+    an intermediate storage precision, so none is assumed); and the attention's score product runs
+    on FP8 q and k, each (token, head) row with a power-of-two scale (_attend_fp8)."""
     T, D = Z.shape
     all_rows = np.arange(T) if rows is None else np.asarray(rows)
     out = np.empty((all_rows.size, D), dtype=np.float64)
@@ -450,7 +521,8 @@ def attention(Z: np.ndarray, cu: np.ndarray, text_len: int, heads: int, weights,
             prod = _fp8_matmul(h, fp8[sig]["w_qkv"]) if fp8 is not None else h @ _w(weights, sig, "w_qkv").T
             qkv[a - lo:b - lo] = prod + _w(weights, sig, "b_qkv")
         r_loc = all_rows[sel] - lo
-        a_out = _attend(qkv[r_loc, :D], qkv[:, D:2 * D], qkv[:, 2 * D:], heads)
+        attend = _attend_fp8 if fp8 is not None else _attend
+        a_out = attend(qkv[r_loc, :D], qkv[:, D:2 * D], qkv[:, 2 * D:], heads)
         text_start = hi - text_len
         for sig in (0, 1):
             m = (all_rows[sel] >= text_start) if sig == 1 else (all_rows[sel] < text_start)

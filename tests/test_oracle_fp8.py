@@ -83,3 +83,82 @@ def test_fp8_block_quantises_all_four_projections():
             Z = res["Z"]
             for (s_, sig, a, b) in O._segments(res["cu"], shp.text_len):
                 np.testing.assert_allclose(y1[a:b], Z[a:b] + wl.mod[s_, sig, 2] * np.asarray(wl.weights[sig]["b_o"], np.float64), atol=1e-12)
+
+
+def test_pow2_exponent_is_the_least_power_of_two_scale():
+    # against a brute-force search over k of the defining inequality 448 * 2^k >= amax
+    rng = np.random.default_rng(7)
+    amax = np.concatenate([np.float32([448.0, 449.0, 224.0, 0.875, 1.0, 3.0e-30, 1.0e30]),
+                           np.exp2(rng.uniform(-60, 60, 200)).astype(np.float32)])
+    k = O.pow2_exponent(amax)
+    for a, kk in zip(amax.astype(np.float64), k):
+        want = next(j for j in range(-140, 140) if 448.0 * 2.0 ** j >= a)
+        assert kk == max(want, -127), (a, kk, want)
+    assert O.pow2_exponent(np.float32([0.0]))[0] == 0
+    # hand-worked: 448 -> 0, 449 -> 1 (448 < 449 <= 896), 224 -> -1, 1.0 -> -8 (448 / 256 = 1.75 >= 1)
+    np.testing.assert_array_equal(k[:5], [0, 1, -1, -9, -8])
+
+
+def test_pow2_quantisation_of_representable_rows_is_exact():
+    # entries that are E4M3 values times 2^j with the row's max code 448: codes come back exactly and
+    # the exponent is j; a row of zeros gives zero codes
+    rng = np.random.default_rng(8)
+    vals = O.e4m3_value(np.arange(0x00, 0x7f, dtype=np.uint8))
+    base = rng.choice(vals, size=(4, 32)) * rng.choice([-1.0, 1.0], size=(4, 32))
+    base[:, 3] = 448.0
+    j = np.array([0, -5, 7, -20])
+    x = (base * np.exp2(j)[:, None]).astype(np.float32)
+    codes, k = O.quantize_rows_pow2(x)
+    np.testing.assert_array_equal(k, j)
+    np.testing.assert_array_equal(O.dequant_rows_pow2(codes, k), x.astype(np.float64))
+    codes, k = O.quantize_rows_pow2(np.zeros((1, 8), dtype=np.float32))
+    assert (codes == 0).all() and k[0] == 0
+
+
+def test_pow2_quantisation_error_is_within_half_an_e4m3_step():
+    # a normal E4M3 code is off by at most half its step, 2^-4 of its magnitude; below 2^-6 (in code
+    # units) the subnormal step 2^-9 bounds the absolute error
+    rng = np.random.default_rng(9)
+    x = (rng.standard_normal((32, 128)) * np.exp2(rng.uniform(-10, 10, (32, 1)))).astype(np.float32)
+    codes, k = O.quantize_rows_pow2(x)
+    y = x.astype(np.float64) * np.exp2(-k.astype(np.float64))[:, None]
+    assert np.abs(y).max() <= 448.0
+    err = np.abs(O.e4m3_value(codes) - y)
+    assert (err <= np.maximum(2.0 ** -4 * np.abs(y), 2.0 ** -10) + 1e-12).all()
+
+
+def test_fp8_scores_of_representable_q_and_k_equal_the_plain_attention():
+    # q and k rows that quantise exactly (E4M3 values times a power of two, max code 448 per head)
+    # give the FP8-score attention exactly the float64 attention
+    rng = np.random.default_rng(10)
+    vals = O.e4m3_value(np.arange(0x00, 0x60, dtype=np.uint8))
+    heads, hd, n = 2, 64, 12
+    q = rng.choice(vals, size=(n, heads * hd)) * rng.choice([-1.0, 1.0], size=(n, heads * hd))
+    k = rng.choice(vals, size=(n, heads * hd)) * rng.choice([-1.0, 1.0], size=(n, heads * hd))
+    for hh in range(heads):
+        q[:, hh * hd] = 448.0
+        k[:, hh * hd + 1] = -448.0
+    q *= 2.0 ** -9
+    k *= 2.0 ** -8
+    v = rng.standard_normal((n, heads * hd))
+    np.testing.assert_allclose(O._attend_fp8(q, k, v, heads), O._attend(q, k, v, heads), rtol=0, atol=1e-12)
+
+
+def test_attend_codes_is_the_fp8_attention_after_quantisation():
+    rng = np.random.default_rng(11)
+    heads, hd, n = 2, 128, 20
+    q, k, v = (rng.standard_normal((n, heads * hd)) for _ in range(3))
+    qc = np.empty((n, heads * hd), np.uint8); kc = np.empty_like(qc)
+    qe = np.empty((n, heads), np.int64); ke = np.empty_like(qe)
+    for hh in range(heads):
+        cols = slice(hh * hd, (hh + 1) * hd)
+        qc[:, cols], qe[:, hh] = O.quantize_rows_pow2(q[:, cols].astype(np.float32))
+        kc[:, cols], ke[:, hh] = O.quantize_rows_pow2(k[:, cols].astype(np.float32))
+    np.testing.assert_array_equal(O.attend_codes(qc, qe, kc, ke, v, heads), O._attend_fp8(q, k, v, heads))
+    # and the FP8 scores stay close to the exact ones.  Rounding to E4M3 leaves a relative error of
+    # RMS ~2^-4 / sqrt(3) ~ 3.6% per operand entry, so for unit-variance q and k a score (its
+    # variance 1) moves by ~sqrt(2) * 3.6% ~ 5% RMS, and the softmax-weighted mean of v moves by a
+    # fraction of that relative to its own size: the relative L2 stays well under 10%
+    a, b = O._attend_fp8(q, k, v, heads), O._attend(q, k, v, heads)
+    rel = np.linalg.norm(a - b) / np.linalg.norm(b)
+    assert 0 < rel < 0.1
