@@ -407,11 +407,13 @@ def token_set_leg(db, rot, steps, warmup, stream, dense_ms):
 
 
 def fp8_leg(db, rot, steps, warmup, stream, work, bf16_ms):
-    """The step with all four projections in FP8 (per-row E4M3 operands: one scale per token for the
-    activations, one per output channel for the weights; Sec. 3.3 combines the compression with FP8
-    quantisation): step latency, the projections' rates against the fp8 MFMA peak, the two passes
-    that quantise the attention and GELU outputs, and how far the block's update of the compressed
-    tokens moves from the bf16 step's (relative L2 over all rows)."""
+    """The step with all four projections and the attention's score product in FP8 (per-row E4M3
+    operands: one scale per token for the activations, one per output channel for the weights, one
+    power-of-two scale per (token, head) for q and k; Sec. 3.3 combines the compression with FP8
+    quantisation): step latency, the projections' rates against the fp8 MFMA peak, the attention
+    core (FP8 scores, bf16 P V), the two passes that quantise the attention and GELU outputs, and how
+    far the block's update of the compressed tokens moves from the bf16 step's (relative L2 over
+    all rows)."""
     import numpy as np
     import torch
 
@@ -450,20 +452,25 @@ def fp8_leg(db, rot, steps, warmup, stream, work, bf16_ms):
     for k in range(hilo.hilo_profile_kinds()):
         name = hilo.hilo_profile_name(k)
         tot, n = hilo.hilo_profile_read(k)
-        if n and name in ("rownorm_attn", "gemm_qkv", "quantize_attn", "gemm_o", "rownorm_mlp", "gemm_fc1",
-                          "quantize_mlp", "gemm_fc2"):
+        if n and name in ("rownorm_attn", "gemm_qkv", "attention_core", "quantize_attn", "gemm_o", "rownorm_mlp",
+                          "gemm_fc1", "quantize_mlp", "gemm_fc2"):
             avg = tot / n
             ent = {"ms": round(avg, 4)}
             if name.startswith("gemm"):
                 ach = work[name][0] / (avg * 1e-3)
                 ent.update(achieved=round(ach, 1), unit="TFLOP/s", peak=PEAK_FP8_TFLOPS,
                            frac=round(ach / PEAK_FP8_TFLOPS, 4))
+            elif name == "attention_core":  # half its FLOPs on the fp8 rate (scores), half on bf16 (P V)
+                ach = work[name][0] / (avg * 1e-3)
+                ent.update(achieved=round(ach, 1), unit="TFLOP/s", note="scores FP8, P V bf16")
             kern[name] = ent
     hilo.hilo_profile_enable(False)
     db.run(hilo.TOPK)  # leave the buffers as the default step left them
     torch.cuda.synchronize()
     res = {"ms_per_step": round(ms, 4), "ms_per_step_median": round(float(per_step[len(per_step) // 2]), 4),
-           "projections_in_fp8": ["qkv", "attention_output", "mlp_up", "mlp_down"], "kernels": kern,
+           "projections_in_fp8": ["qkv", "attention_output", "mlp_up", "mlp_down"],
+           "attention_in_fp8": "scores q k^T (E4M3 q and k, power-of-two scale per token and head); P V bf16",
+           "kernels": kern,
            "timing": "latents rotated as in the main step; one FP8 weight set (quantised once)",
            "block_update_rel_l2_vs_bf16": round(rel, 5)}
     if bf16_ms:

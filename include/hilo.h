@@ -240,11 +240,14 @@ hilo_status hilo_quantize_rows(int32_t dtype, const void *x, int64_t rows, int64
  * codes and scales in the MLP half; 0 if the shape is invalid for the FP8 block.                 */
 size_t hilo_workspace_bytes_fp8(const hilo_shape *shape);
 
-/* hilo_attention with both projections in FP8: h = LN(z) * (1 + scale1) + shift1 is formed in
- * float32 and quantised per row straight from registers, then multiplied by the FP8 W_qkv; the
- * attention core is that of hilo_attention (bf16 q, k, v, output); its output rows are quantised and
- * multiplied by the FP8 W_o.  shape->dtype must be HILO_BF16 (HILO_E_DTYPE), dim and mlp_dim
- * multiples of 128 (HILO_E_SHAPE).  workspace: ws_bytes >= hilo_workspace_bytes_fp8(shape).       */
+/* hilo_attention with both projections and the attention's score product in FP8 (Sec. 3.3): h =
+ * LN(z) * (1 + scale1) + shift1 is formed in float32 and quantised per row straight from
+ * registers, then multiplied by the FP8 W_qkv; that projection's q and k leave as E4M3 codes with a
+ * power-of-two scale per (row, head) -- 2^k, k the least integer with 448 2^k >= the row's amax --
+ * formed from its float32 values, v as bf16; the attention core multiplies the FP8 q and k
+ * (hilo_attention_core_fp8), softmax and P V as in hilo_attention; its output rows are quantised
+ * and multiplied by the FP8 W_o.  shape->dtype must be HILO_BF16 (HILO_E_DTYPE), dim a multiple of
+ * 256 and mlp_dim of 128 (HILO_E_SHAPE).  workspace: ws_bytes >= hilo_workspace_bytes_fp8(shape). */
 hilo_status hilo_attention_fp8(const hilo_shape *shape, float *z, const int32_t *cu_seqlens,
                                const hilo_attn_w_fp8 w[2], const float *mod, void *workspace,
                                size_t ws_bytes, void *stream);
@@ -286,6 +289,19 @@ hilo_status hilo_decompress_delta(const hilo_shape *shape, const float *z, const
 hilo_status hilo_attention_core(const hilo_shape *shape, const void *qkv,
                                 const int32_t *cu_seqlens, void *out, void *workspace,
                                 size_t ws_bytes, void *stream);
+
+/* The FP8 block's attention core alone (Sec. 3.3, "Compatibility with Quantization and
+ * Distillation": FP8 on top of the compression; here the score product q k^T runs on FP8 operands):
+ * qkv8 holds T_max rows of 6 D bytes -- bytes [0, D) the q codes, [D, 2 D) the k codes (OCP E4M3,
+ * head h in bytes h hd .. of each), [2 D, 2 D + 2 H) one E8M0 scale byte per (row, head), q heads
+ * then k heads (row scale 2^(byte - 127)), and bytes [4 D, 6 D) the v row in bf16 -- the layout
+ * hilo_attention_fp8's QKV projection writes.  out [T_max][D] bf16 = softmax(q k^T / sqrt(hd)) v
+ * with q, k dequantised (code value times scale) and the probabilities and v as in the bf16 core;
+ * rows of sample s attend to the rows of sample s.  Shape: as hilo_attention_fp8 (bf16, dim a
+ * multiple of 256).  workspace: device scratch of ws_bytes >= hilo_workspace_bytes(shape).      */
+hilo_status hilo_attention_core_fp8(const hilo_shape *shape, const void *qkv8,
+                                    const int32_t *cu_seqlens, void *out, void *workspace,
+                                    size_t ws_bytes, void *stream);
 
 /* hilo_attention_core without a workspace, for callers that cannot allocate device memory (code
  * under HIP graph capture, serving loops and harnesses that forbid hipMalloc): the same kernels and

@@ -418,12 +418,13 @@ hilo_status check_mlp_w8(const hilo_mlp_w_fp8 *w) {
   return HILO_OK;
 }
 
-// The FP8 block: bf16 shape; every projection's K (dim, mlp_dim) in whole 128-deep steps.
+// The FP8 block: bf16 shape; every projection's K (dim, mlp_dim) in whole 128-deep steps, and dim a
+// multiple of 256, so that the QKV projection's 256-column tiles hold whole heads of q and k.
 hilo_status check_fp8_block(const hilo_shape *s) {
   hilo_status e = check_block(s);
   if (e != HILO_OK) return e;
   if (s->dtype != HILO_BF16) return HILO_E_DTYPE;
-  if (s->dim % 128 != 0 || s->mlp_dim % 128 != 0) return HILO_E_SHAPE;
+  if (s->dim % 256 != 0 || s->mlp_dim % 128 != 0) return HILO_E_SHAPE;
   return HILO_OK;
 }
 
@@ -457,11 +458,17 @@ hilo_status enqueue_attention(const hilo_shape *s, float *z, const int32_t *cu_s
   p.A = h; p.lda = D;
   p.N = 3 * D; p.K = D;
   p.out = qkv; p.ldo = 3 * D;
+  // FP8 block: q and k leave the projection as E4M3 codes with per-(row, head) power-of-two scales,
+  // in the first 2 D bytes (codes) and the next 2 H bytes (scales) of each row of the qkv region;
+  // v stays bf16 in its columns
+  uint8_t *qk8 = w8 ? reinterpret_cast<uint8_t *>(qkv) : nullptr;
+  const int ldq8 = 3 * D * 2;
   if (w8) {
     p.W[0] = w8[0].w_qkv; p.W[1] = w8[1].w_qkv;
     p.bias[0] = w8[0].b_qkv; p.bias[1] = w8[1].b_qkv;
     p.a_scale = hs;
     p.w_scale[0] = w8[0].s_qkv; p.w_scale[1] = w8[1].s_qkv;
+    p.qk8 = qk8; p.ldq8 = ldq8; p.head_dim = s->head_dim;
     he = timed(K_GEMM_QKV, st, [&] { return launch_gemm_fp8(GEMM_QKV, p, st); });
   } else {
     p.W[0] = w[0].w_qkv; p.W[1] = w[1].w_qkv;
@@ -476,7 +483,7 @@ hilo_status enqueue_attention(const hilo_shape *s, float *z, const int32_t *cu_s
   void *aout = w8 ? static_cast<void *>(ws + ws_fp8_base(s)) : h;
   he = timed(K_ATTN_CORE, st, [&] {
     return launch_attention(bf, qkv, cu_seqlens, aout, part, s->batch, s->heads, s->head_dim,
-                            max_seq, st);
+                            max_seq, st, qk8, ldq8);
   });
   if (he != hipSuccess) return HILO_E_DEVICE;
 
@@ -617,6 +624,22 @@ hilo_status hilo_mlp_fp8(const hilo_shape *s, float *z, const int32_t *cu_seqlen
   if (ws_bytes < ws_fp8(s)) return HILO_E_WORKSPACE;
   if (!have_device()) return HILO_E_DEVICE;
   return enqueue_mlp(s, z, cu_seqlens, nullptr, w, mod, workspace, reinterpret_cast<hipStream_t>(stream));
+}
+
+hilo_status hilo_attention_core_fp8(const hilo_shape *s, const void *qkv8, const int32_t *cu_seqlens,
+                                    void *out, void *workspace, size_t ws_bytes, void *stream) {
+  hilo_status e = check_fp8_block(s);
+  if (e != HILO_OK) return e;
+  if (!qkv8 || !cu_seqlens || !out || !workspace) return HILO_E_NULL;
+  if (ws_bytes < ws_part(s)) return HILO_E_WORKSPACE;
+  if (!have_device()) return HILO_E_DEVICE;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  const int max_seq = int(s->images * grid_rows_max(s) + s->text_len);
+  return dev_status(timed(K_ATTN_CORE, st, [&] {
+    return launch_attention(true, qkv8, cu_seqlens, out, reinterpret_cast<float *>(workspace), s->batch,
+                            s->heads, s->head_dim, max_seq, st, reinterpret_cast<const uint8_t *>(qkv8),
+                            6 * s->dim);
+  }));
 }
 
 hilo_status hilo_quantize_rows(int32_t dtype, const void *x, int64_t rows, int64_t cols, uint8_t *codes,

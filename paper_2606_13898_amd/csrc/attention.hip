@@ -93,6 +93,25 @@ HILO_DEV void lds_tie(T &x) {
   asm volatile("" : "+v"(x));
 }
 
+// FP8 K tile rows (head_dim bytes) keep 16-byte chunk c of row r at slot c ^ kswz8(r): the 16
+// lanes reading one chunk of 16 consecutive rows hit 16 distinct bank groups (rows of 128 bytes:
+// even and odd rows fall in opposite halves of the 256 banked bytes, so the 8 rows of each parity
+// need 8 distinct slots; rows of 64 bytes: the 4 rows r, r + 4, r + 8, r + 12 need 4).
+template <int HD>
+HILO_DEV int kswz8(int r) {
+  if constexpr (HD == 128) return (r >> 1) & 7;
+  else return ((r >> 1) & 3) ^ ((r >> 3) & 1);
+}
+template <int OFF>
+HILO_DEV void lds_read_b32(uint32_t &dst, uint32_t addr) {
+  asm volatile("ds_read_b32 %0, %1 offset:%2" : "=v"(dst) : "v"(addr), "n"(OFF) : "memory");
+}
+typedef int i32x8 __attribute__((ext_vector_type(8)));
+
+HILO_DEV void g2lds4(const void *g, void *lds_wave_base) {
+  __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void *)lds_wave_base, 4, 0, 0);
+}
+
 HILO_DEV void g2lds16(const void *g, void *lds_wave_base) {
   __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void *)lds_wave_base, 16, 0, 0);
 }
@@ -140,6 +159,10 @@ struct AttnArgs {
   float *part;  // partial slots: 2 per workgroup
   int B, heads;
   float scale_log2;
+  // FP8 scores: row m's q and k codes at qk8 + m * ldq8 (q heads, then k heads), its E8M0 scale
+  // bytes at + 2 D (q heads, then k heads); v stays bf16 in qkv
+  const uint8_t *qk8;
+  int ldq8;
 };
 
 template <int HD, int QW, int NW>
@@ -181,7 +204,7 @@ HILO_DEV void attn_store_out(const AttnArgs &a, const AttnUnit &u, int wid, int 
   }
 }
 
-template <int HD, int QW, int NW>
+template <int HD, int QW, int NW, bool F8S>
 __global__ __launch_bounds__(NW * 64, 8 / NW) void k_attn_bf16(AttnArgs a) {
   using S = AttnShape<HD, QW, NW>;
   constexpr int BKV = 64;
@@ -193,8 +216,14 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void k_attn_bf16(AttnArgs a) {
   constexpr int RPI = 64 / CPR;     // K rows per wave load instruction (1 KiB)
   constexpr int KI = BKV / RPI / NW;  // K load instructions per wave per tile
   static_assert(KI * RPI * NW == BKV, "K tile / wave mismatch");
-  __shared__ __attribute__((aligned(1024))) uint16_t sK[2][BKV * HD];
+  __shared__ __attribute__((aligned(1024))) uint16_t sK[2][F8S ? 8 : BKV * HD];
   __shared__ __attribute__((aligned(1024))) uint16_t sV[2][BKV * HD];
+  // FP8 scores: the K tile's codes (head_dim bytes per key) and its keys' scale dwords
+  constexpr int K8I = BKV * HD / 1024 / NW;  // 1 KiB K-code load instructions per wave per tile
+  static_assert(!F8S || K8I == 1, "FP8 K tile / wave mismatch");
+  constexpr int R8 = 1024 / HD;              // K-code rows per load instruction
+  __shared__ __attribute__((aligned(1024))) uint8_t sK8[2][F8S ? BKV * HD : 16];
+  __shared__ __attribute__((aligned(256))) uint32_t sKs[2][F8S ? BKV : 4];
 
   const int P = gridDim.x;
   const int pid = xcd_remap(blockIdx.x, P);
@@ -219,14 +248,25 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void k_attn_bf16(AttnArgs a) {
     const uint16_t *Kp = Q + D;
     const uint16_t *Vp = Q + 2 * D;
 
-    // query fragments (second MFMA operand): row q, dims kk*32 + 8*lg .. +7
-    bf16x8 qf[QS][KK];
+    // query fragments (second MFMA operand): row q, dims kk*32 + 8*lg .. +7; FP8 scores: codes
+    // 32 lg .. 32 lg + 31 of the row's head (head dim 64: lanes 32..63 hold the 128-deep MFMA's K
+    // range 64..127, zero) and the row's scale byte
+    bf16x8 qf[F8S ? 1 : QS][F8S ? 1 : KK];
+    i32x8 qf8[QS];
+    uint32_t qsc[QS];
 #pragma unroll
     for (int qs = 0; qs < QS; ++qs) {
       const int q = min(q0 + wid * QW + qs * 16 + lr, n - 1);
+      if constexpr (F8S) {
+        const uint8_t *qr = a.qk8 + size_t(lo + q) * a.ldq8;
+        const i32x8 c = *reinterpret_cast<const i32x8 *>(qr + u.h * HD + 32 * (HD == 128 ? lg : (lg & 1)));
+        qf8[qs] = (HD == 128 || lg < 2) ? c : i32x8{0, 0, 0, 0, 0, 0, 0, 0};
+        qsc[qs] = qr[2 * D + u.h];
+      } else {
 #pragma unroll
-      for (int kk = 0; kk < KK; ++kk)
-        qf[qs][kk] = *reinterpret_cast<const bf16x8 *>(Q + size_t(q) * ld + kk * 32 + 8 * lg);
+        for (int kk = 0; kk < KK; ++kk)
+          qf[qs][kk] = *reinterpret_cast<const bf16x8 *>(Q + size_t(q) * ld + kk * 32 + 8 * lg);
+      }
     }
 
     // K and V: direct global->LDS, lane -> (row wid*KI*RPI + RPI*i + lane/CPR, slot lane%CPR),
@@ -242,9 +282,30 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void k_attn_bf16(AttnArgs a) {
       koff[i] = uint32_t(r) * ldb + uint32_t((kslot ^ kswz<HD>(r)) * 16);
       voff[i] = uint32_t(r) * ldb + uint32_t((kslot ^ vsw<HD>(r)) * 16);
     }
+    // FP8 scores: the K codes, lane -> (row wid*R8 + lane/(HD/16), slot lane%(HD/16)), chunks placed
+    // by kswz8; wave 0 also fetches the dword holding each of the tile's 64 keys' scale byte
+    const uint32_t ld8 = uint32_t(a.ldq8);
+    const int r8 = wid * R8 + lane / (HD / 16);
+    const uint32_t k8off = uint32_t(r8) * ld8 + uint32_t(((lane % (HD / 16)) ^ kswz8<HD>(r8)) * 16);
+    const int sbyte = 2 * D + a.heads + u.h;  // the k scale byte of this head within a row
     auto issue_kv = [&](int kv0, int buf) {
       const char *kb = reinterpret_cast<const char *>(Kp) + size_t(kv0) * ldb;
       const char *vb = reinterpret_cast<const char *>(Vp) + size_t(kv0) * ldb;
+      if constexpr (F8S) {
+        const uint8_t *k8b = a.qk8 + size_t(lo + kv0) * a.ldq8 + D + u.h * HD;
+        const bool full = kv0 + BKV <= n;
+        const uint32_t back8 = full ? 0u : uint32_t(r8 - (min(kv0 + r8, n - 1) - kv0)) * ld8;  // rows re-read
+        g2lds16(k8b + (k8off - back8), &sK8[buf][wid * 1024]);
+        if (wid == 0)
+          g2lds4(a.qk8 + size_t(lo + min(kv0 + lane, n - 1)) * a.ldq8 + (sbyte & ~3), &sKs[buf][0]);
+#pragma unroll
+        for (int i = 0; i < KI; ++i) {
+          const int r = (wid * KI + i) * RPI + krow;
+          const uint32_t back = full ? 0u : uint32_t(r - (min(kv0 + r, n - 1) - kv0)) * ldb;
+          g2lds16(vb + (voff[i] - back), &sV[buf][(wid * KI + i) * RPI * HD]);
+        }
+        return;
+      }
       if (kv0 + BKV <= n) {
 #pragma unroll
         for (int i = 0; i < KI; ++i) {
@@ -269,6 +330,15 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void k_attn_bf16(AttnArgs a) {
     uint32_t kaddr[KK];
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) kaddr[kk] = sK0 + (lr * HD + (((kk * 4 + lg) ^ kswz<HD>(lr)) * 8)) * 2;
+    // FP8 K of key subtile ks: row ks*16 + lr, chunks 2 lg and 2 lg + 1 (head dim 64: lanes 32..63
+    // read the chunks of lanes 0..31, real codes that meet zero query entries); kswz8 depends on lr
+    // only, so ks is an immediate offset.  The scale dword of key ks*16 + lr: immediate ks * 64.
+    constexpr uint32_t kTile8 = BKV * HD;
+    const uint32_t sK80 = (uint32_t)(uintptr_t)&sK8[0][0], sKs0 = (uint32_t)(uintptr_t)&sKs[0][0];
+    const int lg8 = HD == 128 ? lg : (lg & 1);
+    const uint32_t k8a0 = sK80 + lr * HD + (((2 * lg8) ^ kswz8<HD>(lr)) * 16);
+    const uint32_t k8a1 = sK80 + lr * HD + (((2 * lg8 + 1) ^ kswz8<HD>(lr)) * 16);
+    const int ssh = (sbyte & 3) * 8;
     // V^T of output subtile d: lane (g = lg, s = lr) reads dims d*16 + 4 (s % 4) .. +3 of key rows
     // 32 kk2 + 4 g + s / 4 and 16 rows further (the transpose gives lane s dim d*16 + s of those 8
     // keys); the swizzle of those rows depends on lane bits only, so kk2 and the +16 rows are
@@ -334,17 +404,53 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void k_attn_bf16(AttnArgs a) {
       for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
         for (int qs = 0; qs < QS; ++qs) sc[ks][qs] = f32x4{0.f, 0.f, 0.f, 0.f};
-      bf16x8 kf[2][KK];
-      read_k(kb, 0, kf[0]);
+      if constexpr (F8S) {
+        // one 128-deep FP8 MFMA per (key subtile, query subtile); the E8M0 scales of the lane's key
+        // row and query row scale the product in the matrix core
+        const uint32_t b8 = buf ? kTile8 : 0u;
+        const uint32_t sa = sKs0 + (buf ? BKV * 4 : 0) + lr * 4;
+        uint32_t kw[4];
+        lds_read_b32<0>(kw[0], sa);
+        lds_read_b32<64>(kw[1], sa);
+        lds_read_b32<128>(kw[2], sa);
+        lds_read_b32<192>(kw[3], sa);
+        bf16x8 kh[2][2];  // the two 16-byte halves of a 32-byte FP8 fragment
+        auto read_k8 = [&](int ks, bf16x8 (&h)[2]) {
+          switch (ks) {
+            case 0: lds_read_b128<0>(h[0], k8a0 + b8); lds_read_b128<0>(h[1], k8a1 + b8); break;
+            case 1: lds_read_b128<16 * HD>(h[0], k8a0 + b8); lds_read_b128<16 * HD>(h[1], k8a1 + b8); break;
+            case 2: lds_read_b128<32 * HD>(h[0], k8a0 + b8); lds_read_b128<32 * HD>(h[1], k8a1 + b8); break;
+            default: lds_read_b128<48 * HD>(h[0], k8a0 + b8); lds_read_b128<48 * HD>(h[1], k8a1 + b8); break;
+          }
+        };
+        read_k8(0, kh[0]);
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        if (ks + 1 < 4) read_k(kb, ks + 1, kf[(ks + 1) & 1]);
-#pragma unroll
-        for (int kk = 0; kk < KK; ++kk) {
-          lds_wait_n((KK - 1 - kk) + (ks + 1 < 4 ? KK : 0), kf[ks & 1][kk]);
+        for (int ks = 0; ks < 4; ++ks) {
+          if (ks + 1 < 4) read_k8(ks + 1, kh[(ks + 1) & 1]);
+          lds_wait_n(ks + 1 < 4 ? 2 : 0, kh[ks & 1][1]);
+          lds_tie(kh[ks & 1][0]);
+          if (ks == 0) {  // the scale reads went first: complete with the first K fragment
+            lds_tie(kw[0]); lds_tie(kw[1]); lds_tie(kw[2]); lds_tie(kw[3]);
+          }
+          const i32x8 kf = __builtin_bit_cast(i32x8, __builtin_shufflevector(kh[ks & 1][0], kh[ks & 1][1], 0, 1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11, 12, 13, 14, 15));
+          const int ksc = int((kw[ks] >> ssh) & 0xffu);
 #pragma unroll
           for (int qs = 0; qs < QS; ++qs)
-            sc[ks][qs] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[ks & 1][kk], qf[qs][kk], sc[ks][qs], 0, 0, 0);
+            sc[ks][qs] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(kf, qf8[qs], sc[ks][qs], 0, 0, 0, ksc, 0, int(qsc[qs]));
+        }
+      } else {
+        bf16x8 kf[2][KK];
+        read_k(kb, 0, kf[0]);
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) {
+          if (ks + 1 < 4) read_k(kb, ks + 1, kf[(ks + 1) & 1]);
+#pragma unroll
+          for (int kk = 0; kk < KK; ++kk) {
+            lds_wait_n((KK - 1 - kk) + (ks + 1 < 4 ? KK : 0), kf[ks & 1][kk]);
+#pragma unroll
+            for (int qs = 0; qs < QS; ++qs)
+              sc[ks][qs] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[ks & 1][kk], qf[qs][kk], sc[ks][qs], 0, 0, 0);
+          }
         }
       }
       // the first two V^T subtiles load while the softmax runs, later ones two subtiles ahead
@@ -597,14 +703,15 @@ int attn_workgroups(int per_cu, size_t slot_floats) {
 
 template <int HD, int QW, int NW>
 static hipError_t run_attn_bf16(const void *qkv, const int *cu, void *out, float *part, int B,
-                                int heads, hipStream_t st) {
+                                int heads, const uint8_t *qk8, int ldq8, hipStream_t st) {
   using S = AttnShape<HD, QW, NW>;
   static_assert(S::kSlotFloats <= 2 * kAttnSlotFloats, "partial slot too large for the workspace");
   AttnArgs a{reinterpret_cast<const uint16_t *>(qkv), cu, reinterpret_cast<uint16_t *>(out), part, B,
-             heads, kLog2e / sqrtf(float(HD))};
+             heads, kLog2e / sqrtf(float(HD)), qk8, ldq8};
   // 4 waves: two workgroups per CU; 8 waves: one (two waves per SIMD either way)
   const int P = attn_workgroups(NW == 8 ? 1 : 2, S::kSlotFloats);
-  hipLaunchKernelGGL((k_attn_bf16<HD, QW, NW>), dim3(P), dim3(NW * 64), 0, st, a);
+  if (qk8) hipLaunchKernelGGL((k_attn_bf16<HD, QW, NW, true>), dim3(P), dim3(NW * 64), 0, st, a);
+  else hipLaunchKernelGGL((k_attn_bf16<HD, QW, NW, false>), dim3(P), dim3(NW * 64), 0, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((k_attn_fix<HD, QW, NW>), dim3(P), dim3(NW * 64), 0, st, a);
@@ -631,10 +738,10 @@ size_t attention_part_bytes(bool bf16, int hd) {
 }
 
 hipError_t launch_attention(bool bf16, const void *qkv, const int *cu, void *out, float *part, int B,
-                            int heads, int hd, int max_seq, hipStream_t st) {
+                            int heads, int hd, int max_seq, hipStream_t st, const uint8_t *qk8, int ldq8) {
   if (bf16) {
-    if (hd == 128) return run_attn_bf16<128, 32, 8>(qkv, cu, out, part, B, heads, st);
-    return run_attn_bf16<64, 32, 4>(qkv, cu, out, part, B, heads, st);
+    if (hd == 128) return run_attn_bf16<128, 32, 8>(qkv, cu, out, part, B, heads, qk8, ldq8, st);
+    return run_attn_bf16<64, 32, 4>(qkv, cu, out, part, B, heads, qk8, ldq8, st);
   }
   if (hd == 128) return run_attn_f32<128>(qkv, cu, out, B, heads, max_seq, st);
   return run_attn_f32<64>(qkv, cu, out, B, heads, max_seq, st);

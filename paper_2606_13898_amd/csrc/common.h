@@ -63,6 +63,31 @@ HILO_DEV float wave_sum_f32(float v) {
   return v;
 }
 
+// FP8 E4M3 codes of four values after scaling: clamp to the format's range (the conversion itself
+// would turn an overflow into NaN), then round to nearest even.
+HILO_DEV uint32_t fp8x4(float a, float b, float c, float d) {
+  const float m = 448.0f;
+  a = fminf(fmaxf(a, -m), m); b = fminf(fmaxf(b, -m), m);
+  c = fminf(fmaxf(c, -m), m); d = fminf(fmaxf(d, -m), m);
+  int w = __builtin_amdgcn_cvt_pk_fp8_f32(a, b, 0, false);
+  w = __builtin_amdgcn_cvt_pk_fp8_f32(c, d, w, true);
+  return uint32_t(w);
+}
+
+// Power-of-two scale of a row for E4M3 codes: the least k with 448 * 2^k >= amax (amax = f * 2^e,
+// f in [1, 2): k = e - 8 when f <= 1.75, else e - 7), clamped below at -127, the least E8M0 scale;
+// 0 for an all-zero row.  Codes are then x * 2^-k (exact), all within [-448, 448].
+HILO_DEV int pow2_exponent(float amax) {
+  const uint32_t b = __float_as_uint(amax);
+  const int e = int((b >> 23) & 0xff);
+  if (amax == 0.f) return 0;
+  if (e == 0) return -127;  // subnormal: far below 448 * 2^-127
+  const int k = e - 127 - ((b & 0x7fffff) <= 0x600000u ? 8 : 7);
+  return k < -127 ? -127 : k;
+}
+// 2^-k for k in [-127, 127] as a float (always a normal number for the k above)
+HILO_DEV float pow2_inverse(int k) { return __uint_as_float(uint32_t(127 - k) << 23); }
+
 // Sample boundary i of the packed sequence.  The boundaries do not change while a kernel runs, so
 // they are read through the constant address space: the compiler then uses scalar loads with their
 // own wait, where a vector load inside a pipelined loop is followed by a wait for every global load

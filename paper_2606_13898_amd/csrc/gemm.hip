@@ -305,6 +305,54 @@ struct SkTile {
     return ((size_t(wid) * TM * TN + i * TN + j) * 64 + lane) * 4;
   }
 
+  // The FP8 q / k codes of fragment row i0 of wave wid (the whole-tile form is big_epilogue_qk8):
+  // the wave's BN / WN columns hold whole heads; a row's columns of one head are spread over the 4
+  // lanes l % 16 + 16 m, each holding 4 columns of every 16.
+  HILO_DEV static void epilogue_rows_qk8(const GemmProblem &p, const TileRows &tr, int n0, int wid, int i0,
+                                         int lane, const f32x4 (&acc)[1][TN]) {
+    const int rl = (wid / WN) * (BM / WM) + i0 * 16 + (lane & 15);
+    const int wc0 = n0 + (wid % WN) * (BN / WN);
+    const int cbase = wc0 + 4 * (lane >> 4);
+    const int hd = p.head_dim, jph = hd / 16;  // fragment columns per head
+    const uint16_t *bias = reinterpret_cast<const uint16_t *>(p.bias[tr.sigma]);
+    const float *ws = tr.sigma ? p.w_scale[1] : p.w_scale[0];
+    const float asc = p.a_scale[tr.row0 + min(rl, tr.nrows - 1)];
+    float v[TN][4];
+    float am0 = 0.f, am1 = 0.f;
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const int nc = cbase + j * 16;
+      const uint2 bu = *reinterpret_cast<const uint2 *>(bias + nc);
+      const float4 wsc = *reinterpret_cast<const float4 *>(ws + nc);
+      const float b[4] = {__uint_as_float(bu.x << 16), __uint_as_float(bu.x & 0xffff0000u),
+                          __uint_as_float(bu.y << 16), __uint_as_float(bu.y & 0xffff0000u)};
+      v[j][0] = acc[0][j][0] * (asc * wsc.x) + b[0];
+      v[j][1] = acc[0][j][1] * (asc * wsc.y) + b[1];
+      v[j][2] = acc[0][j][2] * (asc * wsc.z) + b[2];
+      v[j][3] = acc[0][j][3] * (asc * wsc.w) + b[3];
+      const float m = fmaxf(fmaxf(fabsf(v[j][0]), fabsf(v[j][1])), fmaxf(fabsf(v[j][2]), fabsf(v[j][3])));
+      if (j / jph == 0) am0 = fmaxf(am0, m);
+      else am1 = fmaxf(am1, m);
+    }
+    am0 = fmaxf(am0, __shfl_xor(am0, 16, 64));
+    am0 = fmaxf(am0, __shfl_xor(am0, 32, 64));
+    am1 = fmaxf(am1, __shfl_xor(am1, 16, 64));
+    am1 = fmaxf(am1, __shfl_xor(am1, 32, 64));
+    const int k0 = pow2_exponent(am0), k1 = pow2_exponent(am1);
+    const float inv0 = pow2_inverse(k0), inv1 = pow2_inverse(k1);
+    if (rl >= tr.nrows) return;
+    uint8_t *row = p.qk8 + size_t(tr.row0 + rl) * p.ldq8;
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const float s = j / jph == 0 ? inv0 : inv1;
+      *reinterpret_cast<uint32_t *>(row + cbase + j * 16) = fp8x4(v[j][0] * s, v[j][1] * s, v[j][2] * s, v[j][3] * s);
+    }
+    if ((lane >> 4) == 0) {
+      row[2 * p.D + wc0 / hd] = uint8_t(127 + k0);
+      if (jph * 2 == TN) row[2 * p.D + wc0 / hd + 1] = uint8_t(127 + k1);
+    }
+  }
+
   // Epilogue of fragment rows i0 .. i0 + ROWS - 1 of wave wid (each fragment: 4 consecutive
   // columns of one row).  Every load the epilogue needs (bias, gate, the old z) is issued before
   // the first store: the compiler cannot prove that the outputs do not alias the inputs, so an
@@ -597,6 +645,82 @@ HILO_DEV void big_epilogue(const GemmProblem &p, const TileRows &tr, int n0, int
   }
 }
 
+// FP8 q and k for the attention's score product, from the QKV projection's accumulators of a
+// 256 x 256 tile of FP8 operands whose columns lie below 2 D.  The wave's 128 columns hold whole
+// heads (128 / head_dim of them); per (row, head): the values acc * (row scale * weight scale) +
+// bias (as the bf16 output would take them), their amax over the head -- this lane's 16 columns of
+// each block and those of lane l ^ 32, which holds the block's other 16 -- the power-of-two scale
+// 2^k, and the E4M3 codes of the values times 2^-k (16 bytes per lane and block); then one E8M0
+// byte 127 + k per (row, head).  The values are formed twice (amax, then codes) instead of held.
+template <int BM, int BN>
+HILO_DEV void big_epilogue_qk8(const GemmProblem &p, const TileRows &tr, int n0, int wid, int lane,
+                               const uint8_t *epi, f32x16 (&acc)[BM / 64][BN / 64]) {
+  using namespace big;
+  static_assert(BN == 256, "a wave's 128 columns hold whole heads");
+  constexpr int NBM = BM / 64, NBN = BN / 64;
+  const int hd = p.head_dim, bph = hd / 32;  // blocks per head
+  const int rbase = (wid >> 1) * (BM / 2) + (lane & 31);
+  const int cl0 = 16 * (lane >> 5);
+  const int wc0 = n0 + (wid & 1) * (BN / 2);
+  auto values = [&](int bi, int bj, float sa, float (&v)[16]) __attribute__((always_inline)) {
+    const int cl = cl0 + 32 * bj;
+    u32x4 bu[2];
+    f32x4 cv[4];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) bu[h] = *reinterpret_cast<const u32x4 *>(epi + kEpiBias + 2 * cl + 16 * h);
+#pragma unroll
+    for (int h = 0; h < 4; ++h) cv[h] = *reinterpret_cast<const f32x4 *>(epi + kEpiCol + 4 * cl + 16 * h);
+    f32x16 blk = acc[bi][bj];
+    asm volatile("" : "+v"(blk));
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const uint32_t w = bu[e >> 3][(e >> 1) & 3];
+      const float bias = __uint_as_float((e & 1) ? (w & 0xffff0000u) : (w << 16));
+      v[e] = blk[e] * (sa * cv[e >> 2][e & 3]) + bias;
+    }
+  };
+#pragma unroll
+  for (int bi = 0; bi < NBM; ++bi) {
+    const float sa = *reinterpret_cast<const float *>(epi + kEpiRow + 4 * (32 * bi + (lane & 31)));
+    float am0 = 0.f, am1 = 0.f;
+#pragma unroll
+    for (int bj = 0; bj < NBN; ++bj) {
+      float v[16];
+      values(bi, bj, sa, v);
+      float m = 0.f;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) m = fmaxf(m, fabsf(v[e]));
+      if (bj / bph == 0) am0 = fmaxf(am0, m);
+      else am1 = fmaxf(am1, m);
+    }
+    am0 = fmaxf(am0, __shfl_xor(am0, 32, 64));
+    am1 = fmaxf(am1, __shfl_xor(am1, 32, 64));
+    const int k0 = pow2_exponent(am0), k1 = pow2_exponent(am1);
+    const float i0 = pow2_inverse(k0), i1 = pow2_inverse(k1);
+    const int rl = rbase + 32 * bi;
+    if (rl < tr.nrows) {
+      uint8_t *row = p.qk8 + size_t(tr.row0 + rl) * p.ldq8;
+#pragma unroll
+      for (int bj = 0; bj < NBN; ++bj) {
+        float v[16];
+        values(bi, bj, sa, v);
+        const float s = bj / bph == 0 ? i0 : i1;
+        uint4 c;
+        c.x = fp8x4(v[0] * s, v[1] * s, v[2] * s, v[3] * s);
+        c.y = fp8x4(v[4] * s, v[5] * s, v[6] * s, v[7] * s);
+        c.z = fp8x4(v[8] * s, v[9] * s, v[10] * s, v[11] * s);
+        c.w = fp8x4(v[12] * s, v[13] * s, v[14] * s, v[15] * s);
+        *reinterpret_cast<uint4 *>(row + wc0 + cl0 + 32 * bj) = c;
+      }
+      if (lane < 32) {
+        row[2 * p.D + wc0 / hd] = uint8_t(127 + k0);
+        if (bph * 2 == NBN) row[2 * p.D + wc0 / hd + 1] = uint8_t(127 + k1);
+      }
+    }
+    asm volatile("" ::: "memory");
+  }
+}
+
 template <int BM, int BN, int EPI, int ROLE, bool F8>
 __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
   using namespace big;
@@ -879,7 +1003,12 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
       // their barriers (each waits for all but the last stage's loads); a one-step item waits here.
       // In window mode the item's second stage waited for it already.
       if (!WIN && cur.ke - cur.kb < 2) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-      big_epilogue<BM, BN, EPI, F8>(p, etr, en0, wid, lane, epi, acc);
+      if constexpr (F8 && EPI == EPI_BIAS && BN == 256) {
+        if (p.qk8 != nullptr && en0 < 2 * p.D) big_epilogue_qk8<BM, BN>(p, etr, en0, wid, lane, epi, acc);
+        else big_epilogue<BM, BN, EPI, F8>(p, etr, en0, wid, lane, epi, acc);
+      } else {
+        big_epilogue<BM, BN, EPI, F8>(p, etr, en0, wid, lane, epi, acc);
+      }
     } else {
       // the partial tile in the 16 x 16 fragment layout k_gemm_fix reads (2 NBM x 2 NBN fragments per
       // wave): row 32 bi + l % 32 is fragment row 2 bi + (l % 32) / 16; columns 32 bj + 16 (l / 32)
@@ -987,6 +1116,12 @@ __global__ __launch_bounds__(kFixThreads) void k_gemm_fix(GemmProblem p, int P) 
     int rt, tn;
     tile_coords(q, t, rt, tn);
     const TileRows tr = decode_row_tile(p, BM, rt);
+    if constexpr (F8 && EPI == EPI_BIAS && BN == 256) {
+      if (p.qk8 != nullptr && q.c0 + tn * BN < 2 * p.D) {
+        T::epilogue_rows_qk8(p, tr, q.c0 + tn * BN, wid, i, lane, acc);
+        continue;
+      }
+    }
     T::template epilogue_rows<EPI, 1, F8>(p, tr, q.c0 + tn * BN, wid, i, lane, acc);
   }
 }
@@ -1123,7 +1258,8 @@ hipError_t launch_gemm(bool bf16, int role, const GemmProblem &p, hipStream_t st
 
 hipError_t launch_gemm_fp8(int role, const GemmProblem &p, hipStream_t st) {
   switch (role) {
-    case GEMM_QKV: return run_split<GEMM_QKV, true>(p, st);
+    // with FP8 q / k output every tile must be 256 columns wide (whole heads per wave)
+    case GEMM_QKV: return p.qk8 ? run_big<256, 256, GEMM_QKV, true>(p, st) : run_split<GEMM_QKV, true>(p, st);
     case GEMM_O: return run_big<192, 192, GEMM_O, true>(p, st);
     case GEMM_FC1: return run_big<256, 256, GEMM_FC1, true>(p, st);
     default: return run_big<192, 192, GEMM_FC2, true>(p, st);

@@ -70,6 +70,12 @@ struct GemmProblem {
   float *part;            // bf16 path: partial tiles (kSkPartBytes)
   const float *a_scale;   // FP8 operands: A row m is codes * a_scale[m] ...
   const float *w_scale[2];  // ... and W row n of stream s is codes * w_scale[s][n]
+  // FP8 attention scores (the FP8 block's QKV projection, 256 x 256 tiles): when set, the columns
+  // below 2 D (q then k) leave as E4M3 codes with one power-of-two scale per (row, head) instead of
+  // bf16 -- row m's codes at qk8 + m * ldq8 + column, its E8M0 scale bytes (127 + k) at qk8 + m *
+  // ldq8 + 2 D + head (the q heads, then the k heads) -- and only the v columns go to out.
+  uint8_t *qk8;
+  int ldq8, head_dim;
   // 0: all N columns.  1 / 2: the two launches of a split projection (launch_gemm for QKV): the
   // leading 256-column tiles one wave of 256 x 256 tiles can hold, then the remaining columns in
   // 256 x 192 tiles -- decided on the device from the row counts, identically in both launches.
@@ -93,9 +99,12 @@ constexpr size_t kAttnSlotFloats = size_t(4) * 2 * 8 * 64 * 4 + size_t(4) * 2 * 
 constexpr size_t kAttnPartBytes = size_t(kAttnMaxWorkgroups) * 2 * kAttnSlotFloats * sizeof(float);
 
 // qkv [Tmax][3D] -> out [Tmax][D] (ld = D), per sample and head over cu.  part: kAttnPartBytes of
-// device scratch for the bf16 path (unused by the fp32 path).
+// device scratch for the bf16 path (unused by the fp32 path).  qk8 (bf16 path only): the score
+// product on FP8 q and k, codes and E8M0 scale bytes in rows of ldq8 bytes (GemmProblem::qk8); the
+// v columns of qkv stay bf16.
 hipError_t launch_attention(bool bf16, const void *qkv, const int *cu, void *out, float *part, int B,
-                            int heads, int hd, int max_seq, hipStream_t st);
+                            int heads, int hd, int max_seq, hipStream_t st, const uint8_t *qk8 = nullptr,
+                            int ldq8 = 0);
 // Bytes of partial results launch_attention uses on the current device (0 for the fp32 path);
 // never more than kAttnPartBytes.
 size_t attention_part_bytes(bool bf16, int hd);

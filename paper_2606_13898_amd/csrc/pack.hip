@@ -267,17 +267,6 @@ hipError_t launch_decompress(bool bf16, const float *z, const int *idx_map, cons
 
 // ------------------------------------------------------------------------------- row norm
 
-// FP8 E4M3 quantisation of one value after scaling: clamp to the format's range (the conversion
-// itself would turn an overflow into NaN), then round to nearest even.
-HILO_DEV uint32_t fp8x4(float a, float b, float c, float d) {
-  const float m = 448.0f;
-  a = fminf(fmaxf(a, -m), m); b = fminf(fmaxf(b, -m), m);
-  c = fminf(fmaxf(c, -m), m); d = fminf(fmaxf(d, -m), m);
-  int w = __builtin_amdgcn_cvt_pk_fp8_f32(a, b, 0, false);
-  w = __builtin_amdgcn_cvt_pk_fp8_f32(c, d, w, true);
-  return uint32_t(w);
-}
-
 // One wave per row: LN(z) (biased variance, eps 1e-6) * (1 + scale) + shift for the row's sample
 // and stream, written in the projection's input form: OUT 0 float32, 1 bf16, 2 FP8 E4M3 codes plus
 // the row's scale (amax / 448; codes of h * (448 / amax), both divisions correctly rounded).

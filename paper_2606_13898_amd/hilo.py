@@ -79,6 +79,7 @@ _SIG = {
     "hilo_decompress": [ctypes.POINTER(hilo_shape), _P, _P, _P, _P, _P, _P, _P],
     "hilo_attention_core": [ctypes.POINTER(hilo_shape), _P, _P, _P, _P, ctypes.c_size_t, _P],
     "hilo_attention_core_noalloc": [ctypes.POINTER(hilo_shape), _P, _P, _P, _P],
+    "hilo_attention_core_fp8": [ctypes.POINTER(hilo_shape), _P, _P, _P, _P, ctypes.c_size_t, _P],
     "hilo_workspace_bytes": [ctypes.POINTER(hilo_shape)],
     "hilo_workspace_bytes_fp8": [ctypes.POINTER(hilo_shape)],
     "hilo_max_tokens": [ctypes.POINTER(hilo_shape)],
@@ -317,6 +318,13 @@ def hilo_attention_core(shape, qkv, cu_seqlens, out, workspace=None, stream=None
     ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
     _check("hilo_attention_core", lib().hilo_attention_core(
         ctypes.byref(shape), _ptr(qkv), _ptr(cu_seqlens), _ptr(out), _ptr(workspace), ws_bytes,
+        _stream(stream)))
+
+
+def hilo_attention_core_fp8(shape, qkv8, cu_seqlens, out, workspace, stream=None):
+    ws_bytes = workspace.numel() * workspace.element_size()
+    _check("hilo_attention_core_fp8", lib().hilo_attention_core_fp8(
+        ctypes.byref(shape), _ptr(qkv8), _ptr(cu_seqlens), _ptr(out), _ptr(workspace), ws_bytes,
         _stream(stream)))
 
 

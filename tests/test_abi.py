@@ -199,8 +199,9 @@ def test_select_tokens_validation():
 
 
 def test_fp8_validation():
-    """The FP8 block takes bf16 shapes with dim % 128 == 0 and every weight pointer, scales included;
-    the row quantiser takes float32 / bf16 rows of a multiple of 4 columns."""
+    """The FP8 block takes bf16 shapes with dim % 256 == 0 (whole heads of q and k in each 256-column
+    tile of the QKV projection), mlp_dim % 128 == 0 and every weight pointer, scales included; the
+    row quantiser takes float32 / bf16 rows of a multiple of 4 columns."""
     L = hilo.lib()
     s = good_shape()
     need = hilo.hilo_workspace_bytes(s)
@@ -217,6 +218,15 @@ def test_fp8_validation():
     odd = hilo.hilo_shape(2, 1, 8, 10, 5, 192, 3, 64, 1024, hilo.BF16)  # 192 is not a multiple of 128
     assert L.hilo_attention_fp8(ctypes.byref(odd), FAKE, FAKE, aw, FAKE, FAKE, 1 << 40, None) == 2
     assert L.hilo_mlp_fp8(ctypes.byref(odd), FAKE, FAKE, mw, FAKE, FAKE, 1 << 40, None) == 2
+    odd_d = hilo.hilo_shape(2, 1, 8, 10, 5, 384, 3, 128, 1024, hilo.BF16)  # 384 is not a multiple of 256
+    assert L.hilo_attention_fp8(ctypes.byref(odd_d), FAKE, FAKE, aw, FAKE, FAKE, 1 << 40, None) == 2
+    assert L.hilo_attention_core_fp8(ctypes.byref(odd_d), FAKE, FAKE, FAKE, FAKE, 1 << 40, None) == 2
+    assert hilo.hilo_workspace_bytes_fp8(odd_d) == 0
+    core8 = L.hilo_attention_core_fp8
+    assert core8(ctypes.byref(f), FAKE, FAKE, FAKE, FAKE, 1 << 40, None) == 3
+    assert core8(ctypes.byref(s), None, FAKE, FAKE, FAKE, 1 << 40, None) == 1
+    assert core8(ctypes.byref(s), FAKE, FAKE, FAKE, None, 1 << 40, None) == 1
+    assert core8(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, 10, None) == 5
     odd_f = hilo.hilo_shape(2, 1, 8, 10, 5, 256, 2, 128, 1088, hilo.BF16)  # mlp_dim 1088: K of MLP down
     assert L.hilo_mlp_fp8(ctypes.byref(odd_f), FAKE, FAKE, mw, FAKE, FAKE, 1 << 40, None) == 2
     assert hilo.hilo_workspace_bytes_fp8(odd_f) == 0
@@ -242,3 +252,4 @@ def test_fp8_validation():
         assert q(hilo.F32, FAKE, 4, 8, FAKE, FAKE, None) == 6
         assert L.hilo_attention_fp8(ctypes.byref(s), FAKE, FAKE, aw, FAKE, FAKE, need8, None) == 6
         assert L.hilo_mlp_fp8(ctypes.byref(s), FAKE, FAKE, mw, FAKE, FAKE, need8, None) == 6
+        assert core8(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, need8, None) == 6

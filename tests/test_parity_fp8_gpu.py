@@ -126,6 +126,40 @@ def _check_codes_near(codes, scales, h, what):
     return frac
 
 
+def _check_qk_codes(codes, exps, want, hd):
+    """The FP8 q and k the QKV projection wrote (E4M3 codes, one power-of-two exponent per (row,
+    head)) against the float64 product of the same codes.  The device quantises its float32
+    accumulation, whose error reaches ~1e-4 of the sum of |terms| (a fraction of 1e-3 of the row's
+    RMS here); so every dequantised code must lie within half an E4M3 step of the exact value (2^-4
+    of it; below the normal range half the subnormal step, 2^-10 of the row scale) plus 1e-3 of the
+    row's RMS, the exponent must be the oracle's power-of-two scale of the exact row except where
+    the row's amax sits within that error of 448 2^k (then one off), and most codes must match the
+    oracle's quantisation of the exact row."""
+    heads2 = exps.shape[1]
+    same_c = total = 0
+    same_e = np.zeros(exps.shape, bool)
+    worst = 0.0
+    for j in range(heads2):
+        cols = slice(j * hd, (j + 1) * hd)
+        w = want[:, cols]
+        wc, wk = O.quantize_rows_pow2(w.astype(np.float32))
+        same_e[:, j] = exps[:, j] == wk
+        assert (np.abs(exps[:, j] - wk) <= 1).all(), "a q / k exponent off by more than one"
+        got = O.dequant_rows_pow2(codes[:, cols], exps[:, j])
+        rms = np.sqrt(np.mean(w ** 2, axis=1, keepdims=True))
+        tol = 2.0 ** -4 * np.abs(w) + np.exp2(exps[:, j:j + 1] - 10.0) + 1e-3 * rms
+        err = np.abs(got - w)
+        worst = max(worst, float((err / tol).max()))
+        assert (err <= tol).all(), f"q / k head {j}: {int((err > tol).sum())} codes off, worst {err.max():.3g}"
+        eq = codes[:, cols] == wc
+        same_c += int(eq[same_e[:, j]].sum())
+        total += int(same_e[:, j].sum()) * hd
+    print(f"[parity-fp8] q/k codes equal {same_c / max(total, 1):.5f}, exponents equal {same_e.mean():.5f}, "
+          f"worst error / bound {worst:.3f}", flush=True)
+    assert same_e.mean() >= 0.99, f"q / k exponents: only {same_e.mean():.4f} match"
+    assert same_c >= 0.97 * total, f"q / k codes: only {same_c / total:.4f} match"
+
+
 def _check_bf16_output(got, want, what):
     """A projection output the device rounded to bf16 against the float64 product of the same
     codes: within one bf16 ulp (the rounding, which an accumulation error can push over a midpoint)
@@ -173,18 +207,23 @@ def fp8_block_checked(db, wl, rows=None):
     for k, (a, b) in enumerate(zip(smp, sig)):
         h[k] = O.layer_norm(z0[k:k + 1])[0] * (1.0 + wl.mod[a, b, 1]) + wl.mod[a, b, 0]
     frac_h = _check_codes_near(hc, hs, h, "h")
-    # the QKV output survives past the attention output's codes and scales
+    # the QKV output (rows of 6 D bytes: q and k codes, their scale bytes, v in bf16) survives past
+    # the attention output's codes and scales
     first_qkv = -(-(_align(Tmax * D) + _align(Tmax * 4)) // (6 * D))
     keep = rows >= first_qkv
     if keep.any():
-        qkv = _bf16_rows(db, hsz, rows[keep], 3 * D)
-        want = np.empty_like(qkv)
+        raw = _gather(db, hsz, 6 * D, rows[keep], 6 * D)
+        want = np.empty((int(keep.sum()), 3 * D))
         hd = O.dequant_rows(hc[keep], hs[keep])
         for st in (0, 1):
             m = sig[keep] == st
             if m.any():
                 want[m] = hd[m] @ _w8(db, st, "w_qkv", "s_qkv").T + _bias(db, st, "b_qkv")
-        _check_bf16_output(qkv, want, "QKV projection")
+        v = np.ascontiguousarray(raw[:, 4 * D:]).view(np.uint16).astype(np.int32) << 16
+        v = torch.from_numpy(v).view(torch.float32).numpy().astype(np.float64)
+        _check_bf16_output(v, want[:, 2 * D:], "QKV projection (v)")
+        _check_qk_codes(raw[:, :2 * D], raw[:, 2 * D:2 * D + 2 * s.heads].astype(np.int64) - 127,
+                        want[:, :2 * D], s.head_dim)
     # attention output projection: a's codes from the device's bf16 a, then the residual update
     a_bf = _bf16_rows(db, base, rows, D)
     ac, as_ = _codes_scales(db, hsz, Tmax, rows, D)
@@ -335,3 +374,52 @@ def test_fp8_full_size_sampled():
     print(f"[parity-fp8] m1024: {rows.size} rows, max_abs {ma:.3g}, rel_l2 {rel:.3g}", flush=True)
     b1, b2 = O.block(front["Z"], front["cu"], s.text_len, s.heads, wl.weights, wl.mod, rows)
     _updates_vs_oracles("m1024", Z, z1, z2, {"z1": w1, "z2": w2}, {"z1": b1, "z2": b2})
+
+
+def _pack_qkv8(q, k, v, heads):
+    """Host side of hilo_attention_core_fp8's input: q and k quantised per (token, head) with
+    power-of-two scales (the oracle's quantize_rows_pow2), v rounded to bf16, in rows of 6 D bytes.
+    Returns (packed uint8 [T][6D], q codes, q exponents, k codes, k exponents, v as float64)."""
+    T, D = q.shape
+    hd = D // heads
+    qc = np.empty((T, D), np.uint8); kc = np.empty_like(qc)
+    qe = np.empty((T, heads), np.int64); ke = np.empty_like(qe)
+    for h in range(heads):
+        cols = slice(h * hd, (h + 1) * hd)
+        qc[:, cols], qe[:, h] = O.quantize_rows_pow2(q[:, cols].astype(np.float32))
+        kc[:, cols], ke[:, h] = O.quantize_rows_pow2(k[:, cols].astype(np.float32))
+    vb = torch.from_numpy(v.astype(np.float32)).to(torch.bfloat16)
+    buf = np.zeros((T, 6 * D), np.uint8)
+    buf[:, :D], buf[:, D:2 * D] = qc, kc
+    buf[:, 2 * D:2 * D + heads] = (qe + 127).astype(np.uint8)
+    buf[:, 2 * D + heads:2 * D + 2 * heads] = (ke + 127).astype(np.uint8)
+    buf[:, 4 * D:] = vb.view(torch.int16).numpy().view(np.uint8).reshape(T, 2 * D)
+    return buf, qc, qe, kc, ke, vb.float().numpy().astype(np.float64)
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("hd,lens,heads", [(128, [1, 17, 64, 65, 200], 2), (128, [150, 300, 3], 2),
+                                           (64, [3, 130, 31], 4), (128, [1100] * 3, 24),
+                                           (64, [1000] * 8, 8)])
+def test_fp8_attention_core_ragged(hd, lens, heads):
+    """The FP8-score attention core alone on codes formed on the host: against the oracle's
+    attention from the same codes (attend_codes) at the bf16 core's tolerance -- the probabilities
+    and v are bf16 as there, and the FP8 products are exact with float32 accumulation."""
+    print(f"[parity-fp8] FP8 attention core hd={hd} heads={heads} lens={lens}", flush=True)
+    D = heads * hd
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    T = int(cu[-1])
+    rng = np.random.default_rng(hd + 7 * len(lens))
+    q, k, v = (rng.standard_normal((T, D)) for _ in range(3))
+    buf, qc, qe, kc, ke, vd = _pack_qkv8(q, k, v, heads)
+    want = np.empty((T, D))
+    for a, b in zip(cu[:-1], cu[1:]):
+        want[a:b] = O.attend_codes(qc[a:b], qe[a:b], kc[a:b], ke[a:b], vd[a:b], heads)
+    maxlen = max(lens)
+    W = 2 * ((maxlen + 3) // 4)
+    shp = hilo.hilo_shape(len(lens), 1, 2, W, 0, D, heads, hd, 4 * D, hilo.BF16)
+    out = torch.zeros(T, D, dtype=torch.bfloat16, device="cuda")
+    ws = torch.empty(hilo.hilo_workspace_bytes(shp), dtype=torch.uint8, device="cuda")
+    hilo.hilo_attention_core_fp8(shp, torch.from_numpy(buf).cuda(), torch.from_numpy(cu).cuda(), out, ws)
+    torch.cuda.synchronize()
+    assert_close(to_np(out), want, "bf16", f"FP8 attention core hd={hd}")
