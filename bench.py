@@ -30,6 +30,9 @@ PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_FP8_TFLOPS = 5000.0    # MI355X dense fp8 MFMA
 PEAK_F32_TFLOPS = 157.3     # MI355X fp32 vector
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+# vector-ALU issue peak: 256 CUs x 4 SIMDs, one wave64 instruction per SIMD every 4 cycles (16 lanes
+# per cycle: fp32 157.3 TFLOP/s counts the packed two-wide FMA), 2.4 GHz
+PEAK_VALU_INSTS_PER_S = 256 * 4 * 2.4e9 / 4
 
 DESCR = {
     "m1024": "one MMDiT-style DiT block at 1024px: 64x64 latent grid + 512 text tokens, D=3072, "
@@ -92,6 +95,19 @@ def traffic_for(kind):
     if source_digest(ent["sources"]) != ent["source_digest"]:
         return None
     return ent["bytes_per_launch"]
+
+
+def valu_for(kind):
+    """Vector-ALU wave instructions per launch measured with rocprofv3 (SQ_INSTS_VALU, the counter
+    pass of profiles/traffic.json), or None when missing or the kernel source changed since."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        ent = json.load(f).get("kernels", {}).get(kind)
+    if not ent or "valu_insts_per_launch" not in ent or source_digest(ent["sources"]) != ent["source_digest"]:
+        return None
+    return ent["valu_insts_per_launch"]
 
 
 def cpu_model():
@@ -271,6 +287,14 @@ def config_leg(name, base, rot_w, steps, warmup, stream, dilate_r=0):
     counts = db.counts.cpu().numpy()
     kern = kernel_profile(steps, step, kernel_work(s, counts, cu))
     t_blk = sum(kern[k]["ms"] for k in BLOCK_KERNELS if k in kern)
+    # the Sobel score is bound by the vector ALU (its exact fixed-point energy), not by HBM: its
+    # instruction count at the issue peak is the floor it is measured against as well
+    nv = valu_for("score")
+    if "score" in kern and nv:
+        floor = nv / PEAK_VALU_INSTS_PER_S * 1e3
+        kern["score"]["alu"] = {"bound": "alu", "valu_insts_per_launch": nv,
+                                "peak": "%.4g wave64 instructions/s" % PEAK_VALU_INSTS_PER_S,
+                                "floor_ms": round(floor, 4), "frac": round(floor / kern["score"]["ms"], 4)}
     dense_ms, nd, cud = dense_block_ms(db, rot, steps, warmup, stream, dilate_r)
     nc = int(cu[-1])
     f_c, f_d = block_flops(s, np.diff(cu)), block_flops(s, np.diff(cud))
@@ -645,6 +669,14 @@ def main():
             "achieved": d["achieved"], "peak": d["peak"], "unit": d["unit"], "frac": d["frac"],
             "traffic": traffic_for(dom)}
     t_blk = sum(kern[k]["ms"] for k in BLOCK_KERNELS if k in kern)
+    # the Sobel score is bound by the vector ALU (its exact fixed-point energy), not by HBM: its
+    # instruction count at the issue peak is the floor it is measured against as well
+    nv = valu_for("score")
+    if "score" in kern and nv:
+        floor = nv / PEAK_VALU_INSTS_PER_S * 1e3
+        kern["score"]["alu"] = {"bound": "alu", "valu_insts_per_launch": nv,
+                                "peak": "%.4g wave64 instructions/s" % PEAK_VALU_INSTS_PER_S,
+                                "floor_ms": round(floor, 4), "frac": round(floor / kern["score"]["ms"], 4)}
 
     # the box's plain device copy, for the memory-bound kernels' fractions (read + write bytes)
     cp_a = torch.empty(256 << 20, dtype=torch.uint8, device="cuda")

@@ -188,6 +188,11 @@ def summarize(out):
                       "fetch_bytes_per_launch": round(t["FETCH_SIZE"] / n),
                       "write_bytes_per_launch": round(t["WRITE_SIZE"] / n),
                       "launches_measured": n, "sources": srcs, "source_digest": source_digest(srcs)}
+    # vector-ALU instructions per launch (the counter pass), for the kernels bound by the vector ALU
+    mf = summarize_mfma(out)
+    for k, e in kernels.items():
+        if mf and k in mf:
+            e["valu_insts_per_launch"] = round(mf[k]["valu_insts"])
     res = {"workload": "m1024", "calibration": {"copy_bytes": COPY_MIB << 20,
                                                 "fetch_counter_per_byte": factor["FETCH_SIZE"],
                                                 "write_counter_per_byte": factor["WRITE_SIZE"]},
@@ -208,7 +213,6 @@ def summarize(out):
     with open(os.path.join(ROOT, "profiles", "traffic_m1024.md"), "w") as f:
         f.write("\n".join(lines) + "\n")
     print(json.dumps({k: v["bytes_per_launch"] for k, v in kernels.items()}, indent=1))
-    mf = summarize_mfma(out)
     if mf:
         print(json.dumps({k: round(100 * v["mfma_busy"], 1) for k, v in mf.items()}, indent=1))
 
