@@ -1,11 +1,13 @@
 // Projections of the block (QKV, attention output, MLP up and down): C = A W^T on the ragged
 // packed sequence, image rows with the image-stream weights and text rows with the text-stream
 // weights, tiles never straddling a segment.  Epilogues fuse the bias, the tanh-GELU, and the
-// gated residual update of the float32 stream z.
+// gated residual update of the float32 stream z; for the FP8 block's QKV projection, the q and k
+// columns leave as E4M3 codes with a power-of-two scale per (row, head).
 //
 // bf16 and FP8 paths: one MFMA kernel (k_gemm_big), one persistent workgroup per CU with 4 waves,
-// 256 x 256 tiles (MLP up; QKV's first launch), 256 x 192 (QKV's second launch: the columns one
-// wave of 256 x 256 tiles cannot hold) or 192 x 192 (attention output, MLP down) as
+// 256 x 256 tiles (MLP up; QKV's first launch, or all of the FP8 QKV with FP8 q / k), 256 x 192
+// (QKV's second launch: the columns one wave of 256 x 256 tiles cannot hold) or 192 x 192
+// (attention output, MLP down) as
 // 32 x 32 MFMA blocks (v_mfma_f32_32x32x16_bf16, or v_mfma_f32_32x32x64_f8f6f4 on E4M3 codes),
 // fp32 accumulators in AGPRs, K in 64-byte stages through a 4-slot LDS ring filled by direct
 // global->LDS loads (192 x 192 tiles: 128-byte K-step windows, both stages of a row's K step
