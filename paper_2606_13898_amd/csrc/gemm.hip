@@ -587,6 +587,26 @@ HILO_DEV void big_epilogue(const GemmProblem &p, const TileRows &tr, int n0, int
 #pragma unroll
   for (int bi = 0; bi < NBM; ++bi)
     sa[bi] = F8 ? *reinterpret_cast<const float *>(epi + kEpiRow + 4 * (32 * bi + (lane & 31))) : 1.f;
+  // The residual update loads every z piece of the wave before it stores any: stores count in
+  // vmcnt, so a z load issued after a block's stores would wait for them too (one memory round
+  // trip per block: 16.4 us per 192 x 192 tile epilogue against 13.4-14.1 with one).
+  // Lanes outside the tile load a valid element they do not store.
+  constexpr int ZB = EPI == EPI_RESID ? NBM * NBN : 1;
+  static_assert(EPI != EPI_RESID || ZB <= 9, "the wave's z pieces are held in registers");
+  float4 zz[ZB][4];
+  if constexpr (EPI == EPI_RESID) {
+#pragma unroll
+    for (int bj = 0; bj < NBN; ++bj)
+#pragma unroll
+      for (int bi = 0; bi < NBM; ++bi) {
+        const int rl = rbase + 32 * bi, n = cbase + 32 * bj;
+        const bool in = rl < tr.nrows && n < p.N;
+        const float4 *zp =
+            reinterpret_cast<const float4 *>(p.z + size_t(tr.row0 + (in ? rl : 0)) * p.ldz + (in ? n : 0));
+#pragma unroll
+        for (int h = 0; h < 4; ++h) zz[bj * NBM + bi][h] = zp[h];
+      }
+  }
 #pragma unroll
   for (int bj = 0; bj < NBN; ++bj) {
     const int cl = cl0 + 32 * bj, n = cbase + 32 * bj;
@@ -619,16 +639,14 @@ HILO_DEV void big_epilogue(const GemmProblem &p, const TileRows &tr, int n0, int
         }
         if constexpr (EPI == EPI_RESID) {
           float4 *zp = reinterpret_cast<float4 *>(p.z + m * p.ldz + n);
-          float4 z[4];
-#pragma unroll
-          for (int h = 0; h < 4; ++h) z[h] = zp[h];
 #pragma unroll
           for (int h = 0; h < 4; ++h) {
-            z[h].x += gv[h][0] * v[4 * h + 0];
-            z[h].y += gv[h][1] * v[4 * h + 1];
-            z[h].z += gv[h][2] * v[4 * h + 2];
-            z[h].w += gv[h][3] * v[4 * h + 3];
-            zp[h] = z[h];
+            float4 z = zz[bj * NBM + bi][h];
+            z.x += gv[h][0] * v[4 * h + 0];
+            z.y += gv[h][1] * v[4 * h + 1];
+            z.z += gv[h][2] * v[4 * h + 2];
+            z.w += gv[h][3] * v[4 * h + 3];
+            zp[h] = z;
           }
         } else {
           if constexpr (EPI == EPI_GELU) {
@@ -642,7 +660,7 @@ HILO_DEV void big_epilogue(const GemmProblem &p, const TileRows &tr, int n0, int
                                pack_bf16x2(v[8 * h + 4], v[8 * h + 5]), pack_bf16x2(v[8 * h + 6], v[8 * h + 7]));
         }
       }
-      asm volatile("" ::: "memory");  // the next block's loads stay below these stores
+      asm volatile("" ::: "memory");  // the next block's operands stay below these stores
     }
   }
 }
