@@ -5,9 +5,8 @@
 // columns leave as E4M3 codes with a power-of-two scale per (row, head).
 //
 // bf16 and FP8 paths: one MFMA kernel (k_gemm_big), one persistent workgroup per CU with 4 waves,
-// 256 x 256 tiles (MLP up; QKV's first launch, or all of the FP8 QKV with FP8 q / k), 256 x 192
-// (QKV's second launch: the columns one wave of 256 x 256 tiles cannot hold) or 192 x 192
-// (attention output, MLP down) as
+// 192 x 192 tiles (every bf16 projection; the FP8 attention output and MLP down) or 256 x 256 (the
+// FP8 QKV with FP8 q / k and the FP8 MLP up) as
 // 32 x 32 MFMA blocks (v_mfma_f32_32x32x16_bf16, or v_mfma_f32_32x32x64_f8f6f4 on E4M3 codes),
 // fp32 accumulators in AGPRs, K in 64-byte stages through a 4-slot LDS ring filled by direct
 // global->LDS loads (192 x 192 tiles: 128-byte K-step windows, both stages of a row's K step
@@ -150,7 +149,6 @@ HILO_DEV TileRows decode_row_tile(const GemmProblem &p, int BM, int r) {
 // fixed order and runs the epilogue -- deterministic, and no workgroup ever waits for another.
 struct SkPlan {
   int R, TN, T, nk;  // row tiles, column tiles, tiles, K steps
-  int c0;          // first column of the plan's range (column tile tn starts at c0 + tn * BN)
   int s, U, dp;    // pieces per tile, units, data-parallel units
   int len;         // K steps of a stream-K unit
   long long I;     // stream-K iterations
@@ -166,36 +164,15 @@ constexpr int kNoSplitSteps = 64;
 // at 256 x 256) that the fixup reads back, so a short tail goes to fewer workgroups.
 constexpr int kSkMinSteps = 12;
 
-// Column range [c0, c1) of the problem's launch.  A split projection (phase 1 / 2) hands the
-// leading 256-column tiles to one wave of 256 x 256 tiles and the rest to one wave of 256 x 192
-// tiles, when its 256 x 256 tiles would need more than one wave but at most two and the rest then
-// fits one wave of the narrower tiles (so two waves of whole tiles become one whole wave plus three
-// quarters of one, without partial tiles); otherwise phase 1 holds every column and phase 2 none.
-HILO_DEV void col_range(const GemmProblem &p, int P, int &c0, int &c1) {
-  c0 = 0;
-  c1 = p.N;
-  if (p.phase == 0) return;
-  const int R = row_tiles_total(p, 256), TN = (p.N + 255) / 256;
-  int split = p.N;
-  if (R > 0 && R * TN > P && R * TN <= 2 * P) {
-    const int ta = P / R;
-    if (ta >= 1 && R * ((p.N - ta * 256 + 191) / 192) <= P) split = ta * 256;
-  }
-  if (p.phase == 1) c1 = split;
-  else c0 = split;
-}
-
 HILO_DEV SkPlan sk_plan(const GemmProblem &p, int BM, int BN, int P, int kstep = 64) {
   SkPlan q;
   q.R = row_tiles_total(p, BM);
-  int c1;
-  col_range(p, P, q.c0, c1);
-  q.TN = c1 > q.c0 ? (c1 - q.c0 + BN - 1) / BN : 0;
+  q.TN = (p.N + BN - 1) / BN;
   q.T = q.R * q.TN;
   q.nk = p.K / kstep;
-  // 256 x 256 tiles: a stream-K tail costs a 256 KiB partial per piece; when the last wave holds
-  // at least half of P tiles, whole tiles in ceil(T / P) waves finish sooner
-  const bool whole_waves = BM * BN >= 256 * 256 && q.T >= P && 2 * (q.T % P) >= P;
+  // a stream-K tail costs a partial tile (144 or 256 KiB) per piece; when the last wave holds at
+  // least half of P tiles, whole tiles in ceil(T / P) waves finish sooner
+  const bool whole_waves = q.T >= P && 2 * (q.T % P) >= P;
   // a single wave that fills at least 7/8 of the workgroups also runs whole tiles (cutting K would
   // add a partial per tile to save at most an eighth)
   const bool full_wave = q.T < P && 8 * q.T >= 7 * P;
@@ -783,7 +760,7 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
 #pragma unroll
       for (int i = 0; i < NLB; ++i) {
         const int r = wid * (BN / 4) + 8 * i + (lane >> 3);
-        lb[i] = Wt + size_t(min(q.c0 + tn * BN + r, p.N - 1)) * p.K * ESZ + ((lane & 7) ^ swzw(r)) * 16;
+        lb[i] = Wt + size_t(min(tn * BN + r, p.N - 1)) * p.K * ESZ + ((lane & 7) ^ swzw(r)) * 16;
       }
     } else {
 #pragma unroll
@@ -794,7 +771,7 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
 #pragma unroll
       for (int i = 0; i < NBN; ++i) {
         const int r = wid * (BN / 4) + 16 * i + lrow;
-        lb[i] = Wt + size_t(min(q.c0 + tn * BN + r, p.N - 1)) * p.K * ESZ + (lslot ^ swz(r)) * 16;
+        lb[i] = Wt + size_t(min(tn * BN + r, p.N - 1)) * p.K * ESZ + (lslot ^ swz(r)) * 16;
       }
     }
   };
@@ -994,7 +971,7 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmProblem p) {
     if (whole) {
       int rt, tn;
       tile_coords(q, cur.t, rt, tn);
-      en0 = q.c0 + uni(tn) * BN;
+      en0 = uni(tn) * BN;
       etr = uni(decode_row_tile(p, BM, uni(rt)));
     }
     ld_check();
@@ -1137,12 +1114,12 @@ __global__ __launch_bounds__(kFixThreads) void k_gemm_fix(GemmProblem p, int P) 
     tile_coords(q, t, rt, tn);
     const TileRows tr = decode_row_tile(p, BM, rt);
     if constexpr (F8 && EPI == EPI_BIAS && BN == 256) {
-      if (p.qk8 != nullptr && q.c0 + tn * BN < 2 * p.D) {
-        T::epilogue_rows_qk8(p, tr, q.c0 + tn * BN, wid, i, lane, acc);
+      if (p.qk8 != nullptr && tn * BN < 2 * p.D) {
+        T::epilogue_rows_qk8(p, tr, tn * BN, wid, i, lane, acc);
         continue;
       }
     }
-    T::template epilogue_rows<EPI, 1, F8>(p, tr, q.c0 + tn * BN, wid, i, lane, acc);
+    T::template epilogue_rows<EPI, 1, F8>(p, tr, tn * BN, wid, i, lane, acc);
   }
 }
 
@@ -1211,8 +1188,7 @@ int device_cus() {
   return ncu[dev];
 }
 
-// BM x BN tiles: one persistent workgroup per CU.  The second launch of a split projection
-// (phase 2) holds at most one wave of tiles, so it leaves partial tiles only for a long K.
+// BM x BN tiles: one persistent workgroup per CU.
 template <int BM, int BN, int ROLE, bool F8 = false>
 static hipError_t run_big(const GemmProblem &p, hipStream_t st) {
   static_assert(size_t(BM) * BN * 3 * kBigMaxWorkgroups * sizeof(float) <= kSkPartBytes, "partial area too small");
@@ -1223,23 +1199,11 @@ static hipError_t run_big(const GemmProblem &p, hipStream_t st) {
   const bool long_k = p.K / (F8 ? 128 : 64) > kNoSplitSteps;
   const long long tiles_max = (long long)p.B * ((p.max_img_rows + BM - 1) / BM + (p.L + BM - 1) / BM) *
                               ((p.N + BN - 1) / BN);
-  if (p.phase == 2 ? !long_k : (tiles_max < P && !long_k)) return hipSuccess;
+  if (tiles_max < P && !long_k) return hipSuccess;
   // P workgroups stride over the fixup's items: few enough that a launch with nothing to finish
   // (the device's row counts led to whole tiles) costs little
   hipLaunchKernelGGL((k_gemm_fix<BM, BN, 2, 2, role_epilogue(ROLE), ROLE, F8>), dim3(P), dim3(kFixThreads), 0, st, p, P);
   return hipGetLastError();
-}
-
-// A projection in two launches (phase 1: 256 x 256 tiles, phase 2: 256 x 192 tiles; the column split
-// is decided on the device, see col_range).
-template <int ROLE, bool F8 = false>
-static hipError_t run_split(const GemmProblem &p, hipStream_t st) {
-  GemmProblem a = p;
-  a.phase = 1;
-  hipError_t e = run_big<256, 256, ROLE, F8>(a, st);
-  if (e != hipSuccess) return e;
-  a.phase = 2;
-  return run_big<256, 192, ROLE, F8>(a, st);
 }
 
 template <int EPI>
@@ -1262,24 +1226,24 @@ hipError_t launch_gemm(bool bf16, int role, const GemmProblem &p, hipStream_t st
       default: return run_f32<EPI_RESID>(p, st);
     }
   }
-  // Tiling per projection, as measured on the 64 x 64 workload (2766 rows): QKV split in two
-  // launches (253 tiles of 256 x 256 over its first 23 column tiles, then 198 tiles of 256 x 192
-  // over the other 3328 columns: one wave each, where 396 tiles of 256 x 256 took two); MLP up
-  // 256 x 256 tiles (528 tiles: two waves plus a short stream-K tail); the attention output and MLP
-  // down projections (N = 3072) 192 x 192 tiles, 240 of them: one wave on 256 CUs with no K split
-  // and no partials.
+  // Every projection on 192 x 192 tiles, whose K steps run through the LDS as whole 128-byte
+  // lines.  At 2766 rows (the 64 x 64 workload): QKV 720 tiles in three whole waves, MLP up 960 in
+  // four, the attention output and MLP down (N = 3072) 240 tiles in one wave with no K split.  256 x
+  // 256 tiles (half-line stages) cost slightly less per output but quantise these row counts worse:
+  // QKV took 178 us as two launches (256 x 256, then 256 x 192 for the columns one wave could not
+  // hold) against 161, MLP up 230 us as two waves plus a stream-K tail against 218.
   switch (role) {
-    case GEMM_QKV: return run_split<GEMM_QKV>(p, st);
+    case GEMM_QKV: return run_big<192, 192, GEMM_QKV>(p, st);
     case GEMM_O: return run_big<192, 192, GEMM_O>(p, st);
-    case GEMM_FC1: return run_big<256, 256, GEMM_FC1>(p, st);
+    case GEMM_FC1: return run_big<192, 192, GEMM_FC1>(p, st);
     default: return run_big<192, 192, GEMM_FC2>(p, st);
   }
 }
 
 hipError_t launch_gemm_fp8(int role, const GemmProblem &p, hipStream_t st) {
   switch (role) {
-    // with FP8 q / k output every tile must be 256 columns wide (whole heads per wave)
-    case GEMM_QKV: return p.qk8 ? run_big<256, 256, GEMM_QKV, true>(p, st) : run_split<GEMM_QKV, true>(p, st);
+    // the FP8 QKV projection always writes FP8 q / k: 256-column tiles (whole heads per wave)
+    case GEMM_QKV: return p.qk8 ? run_big<256, 256, GEMM_QKV, true>(p, st) : hipErrorInvalidValue;
     case GEMM_O: return run_big<192, 192, GEMM_O, true>(p, st);
     case GEMM_FC1: return run_big<256, 256, GEMM_FC1, true>(p, st);
     default: return run_big<192, 192, GEMM_FC2, true>(p, st);

@@ -76,10 +76,6 @@ struct GemmProblem {
   // ldq8 + 2 D + head (the q heads, then the k heads) -- and only the v columns go to out.
   uint8_t *qk8;
   int ldq8, head_dim;
-  // 0: all N columns.  1 / 2: the two launches of a split projection (launch_gemm for QKV): the
-  // leading 256-column tiles one wave of 256 x 256 tiles can hold, then the remaining columns in
-  // 256 x 192 tiles -- decided on the device from the row counts, identically in both launches.
-  int phase;
 };
 
 // Partial-sum area of the GEMMs (part of the caller's workspace): one slot per data-parallel unit

@@ -6,7 +6,8 @@ stream-K tail over the first Pk workgroups, whose range cuts leave fp32 partial 
 adds.  This model restates those formulas and checks, for fixed and random (T, P, nk), that every
 (tile, K step) is computed exactly once, that every partial slot is written once and read by exactly
 the fixup of its tile, and that the fixup's pieces of a tile cover K in order.  The plan's whole-tile
-rules (one short wave, whole waves of 256 x 256 tiles) give an empty tail and are not modelled.
+rules (a short K with fewer tiles than workgroups, one wave at least 7/8 full, whole waves when the
+last one is at least half full) give an empty tail; `whole_tiles` restates them.
 """
 import random
 
@@ -28,6 +29,11 @@ def plan(T, P, nk):
     I = tail * ln
     Pk = min(P, max(tail, -(-I // MIN_STEPS))) if I > 0 else P
     return s, U, dp, ln, I, Pk
+
+
+def whole_tiles(T, P, nk):
+    """True when the plan runs every tile whole (no K pieces, no stream-K tail)."""
+    return (T < P and nk <= NO_SPLIT_STEPS) or (T >= P and 2 * (T % P) >= P) or (T < P and 8 * T >= 7 * P)
 
 
 def rng(I, P, w):
@@ -115,53 +121,26 @@ def test_schedule_fixed_cases(T, P, nk):
     check(T, P, nk)
 
 
-def test_mlp_up_tail_goes_to_fewer_workgroups():
+def test_short_tail_goes_to_fewer_workgroups():
     # 528 tiles on 256 workgroups: two whole waves, then 16 tiles x 48 steps over 64 workgroups
+    assert not whole_tiles(528, 256, 48)
     s, U, dp, ln, I, Pk = plan(528, 256, 48)
     assert (s, dp, ln, I, Pk) == (1, 512, 48, 768, 64)
+
+
+def test_projections_at_the_64x64_workload():
+    # 2254 image rows (12 row tiles of 192) + 512 text rows (3): 15 row tiles, D = 3072, F = 12288,
+    # 256 CUs.  QKV 720 tiles and MLP up 960 run whole waves (3 and 4, the last 208 and 192 tiles),
+    # the attention output and MLP down 240 tiles in one wave (K = 3072: 48 steps; K = 12288: 192
+    # steps, but the wave is more than 7/8 full)
+    R = 12 + 3
+    for N, K in [(3 * 3072, 3072), (12288, 3072), (3072, 3072), (3072, 12288)]:
+        T = R * -(-N // 192)
+        assert whole_tiles(T, 256, K // 64), (N, K)
+    assert [R * -(-N // 192) for N in (9216, 12288, 3072)] == [720, 960, 240]
 
 
 def test_schedule_random_cases():
     r = random.Random(0)
     for _ in range(600):
         check(r.randint(0, 700), r.choice([1, 2, 7, 64, 255, 256]), r.randint(1, 200))
-
-
-# The column split of a two-launch projection (gemm.hip: col_range): R row tiles of 256 rows, N
-# columns, P workgroups.  Phase 1 takes [0, split) in 256 x 256 tiles, phase 2 [split, N) in
-# 256 x 192 tiles.
-def col_split(R, N, P):
-    TN = -(-N // 256)
-    split = N
-    if R > 0 and P < R * TN <= 2 * P:
-        ta = P // R
-        if ta >= 1 and R * (-(-(N - ta * 256) // 192)) <= P:
-            split = ta * 256
-    return split
-
-
-def test_qkv_split_at_the_64x64_workload():
-    # 2254 image rows (9 tiles) + 512 text rows (2): 11 row tiles; QKV N = 9216 on 256 CUs
-    split = col_split(11, 9216, 256)
-    assert split == 23 * 256
-    assert 11 * 23 == 253 and 11 * -(-(9216 - split) // 192) == 198
-    # the MLP up projection (528 tiles, more than two waves) is not split
-    assert col_split(11, 12288, 256) == 12288
-
-
-@pytest.mark.parametrize("seed", range(100))
-def test_col_split_partitions_the_columns_into_single_waves(seed):
-    r = random.Random(seed)
-    P = r.choice([64, 104, 256, 304])
-    R = r.randint(1, 40)
-    N = 64 * r.randint(1, 300)
-    split = col_split(R, N, P)
-    assert 0 < split <= N
-    if split < N:
-        # both launches are one wave of whole tiles, and together they cover every column once
-        assert split % 256 == 0
-        assert R * (split // 256) <= P
-        assert R * -(-(N - split) // 192) <= P
-        assert R * -(-N // 256) > P  # only a projection that needed a second wave is split
-    else:
-        assert not (P < R * -(-N // 256) <= 2 * P) or R * -(-(N - (P // R) * 256) // 192) > P or P // R < 1

@@ -227,8 +227,9 @@ def test_attention_core_ragged(hd, lens, heads):
 @pytest.mark.parametrize("shp", [
     # down projection: ~6 tiles, K = 8192 (128 steps) -> tiles cut into K pieces plus a stream-K tail
     inputs.BlockShape(3, 1, 16, 20, 40, 256, 2, 128, 8192, "bf16"),
-    # a single tile: every K piece is one step, the fixup sums 128 partial tiles
-    inputs.BlockShape(1, 1, 16, 16, 0, 256, 2, 128, 8192, "bf16"),
+    # a single 192 x 192 down-projection tile (at most 144 rows, N = 192): every K piece is one
+    # step, the fixup sums 128 partial tiles
+    inputs.BlockShape(1, 1, 12, 12, 0, 192, 3, 64, 8192, "bf16"),
 ], ids=["pieces_and_tail", "one_tile_128_pieces"])
 def test_mlp_split_k(shp):
     """MLP with a long down-projection K and few output tiles: the projection is split along K
@@ -245,20 +246,21 @@ def test_mlp_split_k(shp):
     assert_close(to_np(db.y_img), ref["y_img"], "bf16", "y_img split-K")
 
 
-# On a 256-CU device these reach every schedule of the 256 x 256 GEMM tiling (QKV, MLP up); every
-# block is kept fine so the row counts are fixed.
+# On a 256-CU device these reach every schedule of the 192 x 192 GEMM tiling (tests/
+# test_gemm_schedule.py models the same plans); every block is kept fine so the row counts are fixed.
 @pytest.mark.parametrize("shp", [
-    # 17 row tiles x 16 column tiles = 272 MLP-up tiles: one wave of whole tiles plus a 16-tile
-    # stream-K tail finished by the fixup
-    inputs.BlockShape(1, 1, 64, 64, 256, 256, 2, 128, 4096, "bf16"),
-    # 17 x 24 = 408 MLP-up tiles: the last wave holds 152 >= 128 tiles, so two waves of whole tiles
-    inputs.BlockShape(1, 1, 64, 64, 256, 256, 2, 128, 6144, "bf16"),
-    # few tiles and K = 4608 (72 steps): QKV cut into 5 K pieces plus a stream-K tail, MLP up into
-    # 64 pieces of one or two steps
+    # 12 + 2 row tiles x 19 column tiles = 266 MLP-up tiles of 16 K steps: one wave of whole tiles,
+    # then a 10-tile stream-K tail over 14 workgroups whose range boundaries cut tiles (fixup)
+    inputs.BlockShape(1, 1, 48, 48, 256, 1024, 8, 128, 3648, "bf16"),
+    # 22 + 2 row tiles x 16 = 384 MLP-up tiles: the last wave holds 128 >= 128 tiles, so two waves of
+    # whole tiles
+    inputs.BlockShape(1, 1, 64, 64, 256, 256, 2, 128, 3072, "bf16"),
+    # few tiles and K = 4608 (72 steps): QKV cut into 2 K pieces plus a stream-K tail, the attention
+    # output into 6, MLP up into 22 pieces of three or four steps
     inputs.BlockShape(1, 1, 16, 16, 0, 4608, 36, 128, 1024, "bf16"),
 ], ids=["sk_tail", "whole_waves", "k_pieces"])
-def test_gemm_256_schedules(shp):
-    print(f"[parity] 256-tile GEMM schedules shape={shp}", flush=True)
+def test_gemm_schedules(shp):
+    print(f"[parity] 192-tile GEMM schedules shape={shp}", flush=True)
     wl = inputs.make_workload("splitk", shape=shp, seed=5, keep_frac=1.0)
     db = DeviceBlock(wl)
     ref = oracle_for(wl)
