@@ -5,8 +5,8 @@
 // columns leave as E4M3 codes with a power-of-two scale per (row, head).
 //
 // bf16 and FP8 paths: one MFMA kernel (k_gemm_big), one persistent workgroup per CU with 4 waves,
-// 192 x 192 tiles (every bf16 projection; the FP8 attention output and MLP down) or 256 x 256 (the
-// FP8 QKV with FP8 q / k and the FP8 MLP up) as
+// 192 x 192 tiles (every projection but the FP8 QKV) or 256 x 256 (the FP8 QKV, which writes FP8
+// q / k with one scale per row and head: a wave's 128 columns hold whole heads) as
 // 32 x 32 MFMA blocks (v_mfma_f32_32x32x16_bf16, or v_mfma_f32_32x32x64_f8f6f4 on E4M3 codes),
 // fp32 accumulators in AGPRs, K in 64-byte stages through a 4-slot LDS ring filled by direct
 // global->LDS loads (192 x 192 tiles: 128-byte K-step windows, both stages of a row's K step
@@ -1245,7 +1245,7 @@ hipError_t launch_gemm_fp8(int role, const GemmProblem &p, hipStream_t st) {
     // the FP8 QKV projection always writes FP8 q / k: 256-column tiles (whole heads per wave)
     case GEMM_QKV: return p.qk8 ? run_big<256, 256, GEMM_QKV, true>(p, st) : hipErrorInvalidValue;
     case GEMM_O: return run_big<192, 192, GEMM_O, true>(p, st);
-    case GEMM_FC1: return run_big<256, 256, GEMM_FC1, true>(p, st);
+    case GEMM_FC1: return run_big<192, 192, GEMM_FC1, true>(p, st);
     default: return run_big<192, 192, GEMM_FC2, true>(p, st);
   }
 }

@@ -314,22 +314,25 @@ def test_fp8_block_parity(name):
     assert_close(to_np(db.y_txt), ref["y_txt"], "fp8", f"{name} y_txt")
 
 
-# The schedules of the FP8 256 x 256 tiling on a 256-CU device (every block kept fine, so the row
-# counts are fixed).  With K = dim <= 8192 an FP8 projection has at most 64 K steps of 128, so a
+# The schedules of the FP8 tilings on a 256-CU device (QKV 256 x 256 with FP8 q / k, the others
+# 192 x 192; every block kept fine, so the row counts are fixed; tests/test_gemm_schedule.py models
+# the same plans).  With K = dim <= 8192 an FP8 projection has at most 64 K steps of 128, so a
 # problem below one wave of tiles always runs whole tiles; the two larger problems reach the
-# stream-K tail (partials in the bf16 fragment layout, finished by the fixup) and the rule that
-# prefers two waves of whole tiles.
+# stream-K tail (partials in the bf16 fragment layout, finished by the fixup, for QKV through the
+# FP8 q / k epilogue) and the rule that prefers whole waves.
 @pytest.mark.parametrize("shp", [
-    # 17 row tiles x 16 column tiles = 272 MLP-up tiles: one wave plus a 16-tile stream-K tail
-    inputs.BlockShape(1, 1, 64, 64, 256, 256, 2, 128, 4096, "bf16"),
-    # 17 x 24 = 408 MLP-up tiles: two waves of whole tiles
-    inputs.BlockShape(1, 1, 64, 64, 256, 256, 2, 128, 6144, "bf16"),
+    # 2816 rows, dim 2048 (16 K steps): QKV 11 x 24 = 264 tiles of 256, one wave plus an 8-tile tail
+    # over 11 workgroups; MLP up 15 x 19 = 285 tiles of 192, one wave plus a 29-tile tail over 39
+    # workgroups -- both tails cut tiles
+    inputs.BlockShape(1, 1, 48, 48, 512, 2048, 16, 128, 3584, "bf16"),
+    # 4352 rows: MLP up 24 x 16 = 384 tiles of 192, the last wave half full: two waves of whole tiles
+    inputs.BlockShape(1, 1, 64, 64, 256, 256, 2, 128, 3072, "bf16"),
     # K = 4608 in 36 steps of 128, few tiles: whole tiles; MLP up N = 1152 ends in a 128-column tile;
     # MLP down has K = 1152, 9 steps of 128
     inputs.BlockShape(1, 1, 16, 16, 0, 4608, 36, 128, 1152, "bf16"),
 ], ids=["sk_tail", "whole_waves", "long_k"])
 def test_fp8_gemm_schedules(shp):
-    print(f"[parity-fp8] 256-tile FP8 schedules shape={shp}", flush=True)
+    print(f"[parity-fp8] FP8 GEMM schedules shape={shp}", flush=True)
     wl = inputs.make_workload("splitk", shape=shp, seed=5, keep_frac=1.0)
     db = DeviceBlock(wl)
     ref = oracle_for(wl, fp8=True)
