@@ -99,7 +99,7 @@ def summarize_mfma(out):
              "dispatch's GPU cycles the matrix cores were busy (the counter adds 32 cycles per "
              "32x32x16 and 16 per 16x16x32 bf16 MFMA over all SIMDs; GRBM_GUI_ACTIVE adds the "
              "dispatch's cycles over the %d XCDs).  Main kernels only (the GEMM fixups and the "
-             "attention merge issue no MFMA); the QKV projection's two launches count as one call." %
+             "attention merge issue no MFMA)." %
              (SIMDS, XCDS, XCDS), "",
              "Command:", "", "    " + commands(out)[-1], "",
              "| kind | us | clock GHz | MFMA busy | MFMA insts | VALU insts | VALU per MFMA |",
@@ -156,9 +156,8 @@ def is_main(name):
 
 
 def primary(name):
-    """The first kernel of each kind's call (its dispatch count = the number of calls): a main
-    kernel, and not the second launch of a split projection (its 256 x 192 tiles)."""
-    return is_main(name) and "k_gemm_big<256, 192," not in name
+    """The kernel of each kind's call whose dispatch count is the number of calls: its main kernel."""
+    return is_main(name)
 
 
 def summarize(out):
