@@ -114,10 +114,13 @@ __global__ __launch_bounds__(512) void k_score(const void *__restrict__ x, long 
   }
 }
 
-// bf16 latents: workgroup = one patch row x TJ columns with every channel; a lane holds 4
-// channels (8-byte loads) of the 3 rows x (TJ + 2) columns it needs, all loaded before any
-// arithmetic (the kernel is bound by the vector ALU, so the loads of every resident workgroup go
-// out at once).  Per channel a slide along the columns forms the vertical sums once per column;
+// bf16 latents: workgroup = one patch row x TJ columns with every channel; a lane takes 4
+// channels at a time (8-byte loads) of the 3 rows x (TJ + 2) columns it needs, all loaded before
+// any arithmetic, and loops over its channel groups.  Workgroups of at most 256 threads leave
+// several resident per CU, so the loads of one overlap the arithmetic of another (the kernel is
+// bound by the vector ALU: 3072 channels, 64x64 grid, 15.8 us against 17.8 with 768 threads, one
+// workgroup per CU; 128 threads 20.4, 192 17.3).  Per channel a slide along the columns forms the
+// vertical sums once per column;
 // (u + 2m) is one fma: 2m is exact, so its single rounding equals the two-step sum of the
 // definition for every input below 2^127 in magnitude (above, the two-step form overflows to
 // infinity first).  The per-output sums over channels meet in LDS (exact in double).
@@ -202,9 +205,7 @@ hipError_t launch_score(bool bf16, const void *x, long long *E, int G, int H, in
   hipLaunchKernelGGL((k_score_bf16<kScoreTJ, NTV>), dim3(unsigned(nblk)), dim3(NTV), 0, st, xb, E, H, W, D, tilesJ)
     if (lanes <= 64) HILO_SCORE(64);
     else if (lanes <= 128) HILO_SCORE(128);
-    else if (lanes <= 256) HILO_SCORE(256);
-    else if (lanes <= 512) HILO_SCORE(512);
-    else HILO_SCORE(768);
+    else HILO_SCORE(256);
 #undef HILO_SCORE
     return hipGetLastError();
   }
