@@ -61,7 +61,9 @@ def kernel_work(shape, counts, cu):
     gemm = lambda n_out, k: (2.0 * nc * n_out * k / 1e12, "TFLOP", mfma)
     return {
         "score": ((G * N * D * es + 8 * G * N) / 1e9, "GB", PEAK_HBM_GBS),
-        "compress": ((G * N * D * es + n_img * D * 4 + B * L * D * (es + 4)) / 1e9, "GB", PEAK_HBM_GBS),
+        # the step's compress pass also writes the attention half's normalised rows (hilo_compress_norm)
+        "compress": ((G * N * D * es + n_img * D * 4 + B * L * D * (es + 4) + nc * D * es) / 1e9, "GB",
+                     PEAK_HBM_GBS),
         "rownorm_attn": (nc * D * (4 + es) / 1e9, "GB", PEAK_HBM_GBS),
         "gemm_qkv": gemm(3 * D, D),
         "attention_core": (4.0 * float((seqs ** 2).sum()) * D / 1e12, "TFLOP", mfma),
@@ -231,7 +233,9 @@ def block_flops(shape, seqlens):
 
 def dense_block_ms(db, rot, steps, warmup, stream, dilate_r=None):
     """The block (attention + MLP) on the uncompressed sequence: every block kept fine (the dense
-    token order), timed per step around the two calls."""
+    token order), timed per step around the two calls.  As in the compressed step, the attention
+    half's first row norm runs in the compress pass before it (hilo_compress_norm), outside the
+    block's time in both."""
     import torch
 
     from paper_2606_13898_amd import hilo
@@ -241,15 +245,15 @@ def dense_block_ms(db, rot, steps, warmup, stream, dilate_r=None):
     db.select(hilo.TOPK, keep=[s.n_blocks] * s.grids, dilate_r=dilate_r)
     for k in range(warmup):
         rot.use(db, k)
-        db.compress()
-        db.attention()
+        db.compress(norm=True)
+        db.attention(normed=True)
         db.mlp()
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
     for k, (a, b) in enumerate(ev):
         rot.use(db, k)
-        db.compress()
+        db.compress(norm=True)
         a.record(stream)
-        db.attention()
+        db.attention(normed=True)
         db.mlp()
         b.record(stream)
     torch.cuda.synchronize()
@@ -337,10 +341,10 @@ def sweep_leg(db, rot, steps, warmup, stream, keeps):
             rot.use(db, k)
             db.score()
             db.select(hilo.TOPK, keep=kk)
-            db.compress()
+            db.compress(norm=True)
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             a.record(stream)
-            db.attention()
+            db.attention(normed=True)
             db.mlp()
             b.record(stream)
             blk.append((a, b))

@@ -11,6 +11,8 @@
  *   hilo_attention  pre-LN adaLN joint attention over image + text tokens of each sample
  *   hilo_mlp        pre-LN adaLN GELU MLP
  *   hilo_decompress scatter fine tokens and broadcast pooled tokens back to the full grid
+ * hilo_compress_norm + hilo_attention_normed are hilo_compress + hilo_attention with the attention
+ * half's first row norm done in the compress pass, on the rows it just formed.
  *
  * Conventions shared by every call
  *   - Every tensor pointer is a caller-owned DEVICE pointer unless stated otherwise; tensors are
@@ -42,7 +44,7 @@
 extern "C" {
 #endif
 
-#define HILO_ABI_VERSION 5
+#define HILO_ABI_VERSION 6
 
 typedef enum {
   HILO_OK = 0,
@@ -172,6 +174,26 @@ hilo_status hilo_compress(const hilo_shape *shape, const void *x_img, const void
 hilo_status hilo_attention(const hilo_shape *shape, float *z, const int32_t *cu_seqlens,
                            const hilo_attn_w w[2], const float *mod, void *workspace,
                            size_t ws_bytes, void *stream);
+
+/* S3 and the first step of S4 in one pass (Sec. 2.3: the compressed tokens are what the DiT's
+ * block normalises first): z exactly as hilo_compress, and the attention half's normalised,
+ * modulated rows h = LN(z) * (1 + scale1) + shift1 (as hilo_attention forms them, bit for bit)
+ * written into the first bytes of `workspace`, where hilo_attention_normed reads them; z is not
+ * read back.  shape must also be a valid block shape (HILO_E_SHAPE / HILO_E_DTYPE as
+ * hilo_attention); mod as hilo_attention; workspace: ws_bytes >= hilo_workspace_bytes(shape),
+ * the same workspace then passed to hilo_attention_normed with nothing enqueued on it in between.
+ * Errors as hilo_compress, plus HILO_E_NULL for mod or workspace and HILO_E_WORKSPACE.          */
+hilo_status hilo_compress_norm(const hilo_shape *shape, const void *x_img, const void *x_txt,
+                               const int32_t *fine_idx, const int32_t *pool_idx, const int32_t *counts,
+                               const int32_t *cu_seqlens, const int32_t *seg_off, const float *mod,
+                               float *z, void *workspace, size_t ws_bytes, void *stream);
+
+/* S4 without its first step: hilo_attention on the normalised rows hilo_compress_norm left in the
+ * workspace (the same z, cu_seqlens, mod and workspace; same results as hilo_compress followed by
+ * hilo_attention).  Arguments and errors as hilo_attention.                                      */
+hilo_status hilo_attention_normed(const hilo_shape *shape, float *z, const int32_t *cu_seqlens,
+                                  const hilo_attn_w w[2], const float *mod, void *workspace,
+                                  size_t ws_bytes, void *stream);
 
 /* S5 -- MLP half of the block, in place on z (Sec. 2.3: the DiT runs on the HiLo tokens; Sec. 2.2:
  * the DiT is most of the model's latency):

@@ -437,7 +437,7 @@ float *fp8_row_scales(const hilo_shape *s, void *h) {
 // FP8 QKV projection.
 hilo_status enqueue_attention(const hilo_shape *s, float *z, const int32_t *cu_seqlens,
                               const hilo_attn_w *w, const hilo_attn_w_fp8 *w8, const float *mod,
-                              void *workspace, hipStream_t st) {
+                              void *workspace, hipStream_t st, bool normed = false) {
   const bool bf = s->dtype == HILO_BF16;
   const int D = s->dim;
   const int T = int(tmax_of(s));
@@ -447,12 +447,16 @@ hilo_status enqueue_attention(const hilo_shape *s, float *z, const int32_t *cu_s
   float *part = reinterpret_cast<float *>(ws + ws_h(s) + align256(size_t(T) * 3 * D * esize(s)));
   float *hs = fp8_row_scales(s, h);
 
-  hipError_t he = timed(K_NORM_ATTN, st, [&] {
-    return w8 ? launch_rownorm_fp8(z, cu_seqlens, mod, s->batch, s->text_len, D, T, 0,
-                                   reinterpret_cast<uint8_t *>(h), hs, st)
-              : launch_rownorm(bf, z, cu_seqlens, mod, s->batch, s->text_len, D, T, 0, h, st);
-  });
-  if (he != hipSuccess) return HILO_E_DEVICE;
+  hipError_t he = hipSuccess;
+  // the normalised rows are already in place when hilo_compress_norm wrote them
+  if (!normed) {
+    he = timed(K_NORM_ATTN, st, [&] {
+      return w8 ? launch_rownorm_fp8(z, cu_seqlens, mod, s->batch, s->text_len, D, T, 0,
+                                     reinterpret_cast<uint8_t *>(h), hs, st)
+                : launch_rownorm(bf, z, cu_seqlens, mod, s->batch, s->text_len, D, T, 0, h, st);
+    });
+    if (he != hipSuccess) return HILO_E_DEVICE;
+  }
 
   GemmProblem p = base_problem(s, cu_seqlens, mod, part);
   p.A = h; p.lda = D;
@@ -583,6 +587,38 @@ hilo_status hilo_attention(const hilo_shape *s, float *z, const int32_t *cu_seql
   if (ws_bytes < ws_attention(s)) return HILO_E_WORKSPACE;
   if (!have_device()) return HILO_E_DEVICE;
   return enqueue_attention(s, z, cu_seqlens, w, nullptr, mod, workspace, reinterpret_cast<hipStream_t>(stream));
+}
+
+hilo_status hilo_compress_norm(const hilo_shape *s, const void *x_img, const void *x_txt,
+                               const int32_t *fine_idx, const int32_t *pool_idx, const int32_t *counts,
+                               const int32_t *cu_seqlens, const int32_t *seg_off, const float *mod,
+                               float *z, void *workspace, size_t ws_bytes, void *stream) {
+  hilo_status e = check_block(s);
+  if (e != HILO_OK) return e;
+  if (!x_img || !fine_idx || !pool_idx || !counts || !cu_seqlens || !seg_off || !mod || !z || !workspace)
+    return HILO_E_NULL;
+  if (s->text_len > 0 && !x_txt) return HILO_E_NULL;
+  if (ws_bytes < ws_attention(s)) return HILO_E_WORKSPACE;
+  if (!have_device()) return HILO_E_DEVICE;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  return dev_status(timed(K_COMPRESS, st, [&] {
+    return launch_compress_norm(s->dtype == HILO_BF16, x_img, x_txt, fine_idx, pool_idx, counts,
+                                cu_seqlens, seg_off, mod, z, s->batch, s->images, s->grid_h,
+                                s->grid_w, s->dim, s->text_len, workspace, st);
+  }));
+}
+
+hilo_status hilo_attention_normed(const hilo_shape *s, float *z, const int32_t *cu_seqlens,
+                                  const hilo_attn_w w[2], const float *mod, void *workspace,
+                                  size_t ws_bytes, void *stream) {
+  hilo_status e = check_block(s);
+  if (e != HILO_OK) return e;
+  if (!z || !cu_seqlens || !mod || !workspace) return HILO_E_NULL;
+  if ((e = check_attn_w(w)) != HILO_OK) return e;
+  if (ws_bytes < ws_attention(s)) return HILO_E_WORKSPACE;
+  if (!have_device()) return HILO_E_DEVICE;
+  return enqueue_attention(s, z, cu_seqlens, w, nullptr, mod, workspace, reinterpret_cast<hipStream_t>(stream),
+                           true);
 }
 
 hilo_status hilo_mlp(const hilo_shape *s, float *z, const int32_t *cu_seqlens,

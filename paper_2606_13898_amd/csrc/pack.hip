@@ -267,31 +267,18 @@ hipError_t launch_decompress(bool bf16, const float *z, const int *idx_map, cons
 
 // ------------------------------------------------------------------------------- row norm
 
-// One wave per row: LN(z) (biased variance, eps 1e-6) * (1 + scale) + shift for the row's sample
-// and stream, written in the projection's input form: OUT 0 float32, 1 bf16, 2 FP8 E4M3 codes plus
-// the row's scale (amax / 448; codes of h * (448 / amax), both divisions correctly rounded).
-// NV = float4s per lane covers D <= 256 NV; the row stays in registers between the passes.
+// LN(v) (biased variance, eps 1e-6) * (1 + scale) + shift of one row held by a wave (lane l holds
+// the float4 at columns (64 k + l) * 4, k < NV), written in the projection's input form: OUT 0
+// float32, 1 bf16, 2 FP8 E4M3 codes plus the row's scale (amax / 448; codes of h * (448 / amax),
+// both divisions correctly rounded).  shift points at the row's (sample, stream) shift vector, the
+// scale vector follows it.  Every lane takes part (wave reductions).
 template <int OUT, int NV>
-__global__ __launch_bounds__(256) void k_rownorm(const float *__restrict__ z, const int *__restrict__ cu,
-                                                 const float *__restrict__ mod, int B, int L, int D,
-                                                 int Tmax, int which, void *__restrict__ out,
-                                                 float *__restrict__ row_scale) {
-  const int lane = threadIdx.x & 63;
-  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (row >= Tmax || row >= cu[B]) return;
-  const int s = sample_of_row(cu, B, row);
-  const int sigma = row >= cu[s + 1] - L ? 1 : 0;
-  const float *shift = mod + (size_t(s * 2 + sigma) * 6 + which * 3) * D;
+HILO_DEV void norm_row(float4 (&v)[NV], int lane, int D, const float *__restrict__ shift, size_t row,
+                       void *__restrict__ out, float *__restrict__ row_scale) {
   const float *scale = shift + D;
-  const float *zr = z + size_t(row) * D;
-  float4 v[NV];
   float sum = 0.f;
 #pragma unroll
-  for (int k = 0; k < NV; ++k) {
-    const int c = (k * 64 + lane) * 4;
-    v[k] = c < D ? *reinterpret_cast<const float4 *>(zr + c) : make_float4(0.f, 0.f, 0.f, 0.f);
-    sum += (v[k].x + v[k].y) + (v[k].z + v[k].w);
-  }
+  for (int k = 0; k < NV; ++k) sum += (v[k].x + v[k].y) + (v[k].z + v[k].w);
   const float mean = wave_sum_f32(sum) / float(D);
   float sq = 0.f;
 #pragma unroll
@@ -323,7 +310,7 @@ __global__ __launch_bounds__(256) void k_rownorm(const float *__restrict__ z, co
     for (int off = 32; off > 0; off >>= 1) amax = fmaxf(amax, __shfl_xor(amax, off, 64));
     const float inv = amax > 0.f ? __fdiv_rn(448.0f, amax) : 0.f;
     if (lane == 0) row_scale[row] = __fdiv_rn(amax, 448.0f);
-    uint8_t *o = reinterpret_cast<uint8_t *>(out) + size_t(row) * D;
+    uint8_t *o = reinterpret_cast<uint8_t *>(out) + row * D;
 #pragma unroll
     for (int k = 0; k < NV; ++k) {
       const int c = (k * 64 + lane) * 4;
@@ -346,13 +333,145 @@ __global__ __launch_bounds__(256) void k_rownorm(const float *__restrict__ z, co
         uint2 u;
         u.x = pack_bf16x2(h0, h1);
         u.y = pack_bf16x2(h2, h3);
-        *reinterpret_cast<uint2 *>(reinterpret_cast<uint16_t *>(out) + size_t(row) * D + c) = u;
+        *reinterpret_cast<uint2 *>(reinterpret_cast<uint16_t *>(out) + row * D + c) = u;
       } else {
-        *reinterpret_cast<float4 *>(reinterpret_cast<float *>(out) + size_t(row) * D + c) =
-            make_float4(h0, h1, h2, h3);
+        *reinterpret_cast<float4 *>(reinterpret_cast<float *>(out) + row * D + c) = make_float4(h0, h1, h2, h3);
       }
     }
   }
+}
+
+// One wave per row of z: norm_row with the row's sample and stream (modulation set `which`: 0 for
+// the attention half, 1 for the MLP half).  NV = float4s per lane covers D <= 256 NV; the row stays
+// in registers between the passes.
+template <int OUT, int NV>
+__global__ __launch_bounds__(256) void k_rownorm(const float *__restrict__ z, const int *__restrict__ cu,
+                                                 const float *__restrict__ mod, int B, int L, int D,
+                                                 int Tmax, int which, void *__restrict__ out,
+                                                 float *__restrict__ row_scale) {
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= Tmax || row >= cu[B]) return;
+  const int s = sample_of_row(cu, B, row);
+  const int sigma = row >= cu[s + 1] - L ? 1 : 0;
+  const float *shift = mod + (size_t(s * 2 + sigma) * 6 + which * 3) * D;
+  const float *zr = z + size_t(row) * D;
+  float4 v[NV];
+#pragma unroll
+  for (int k = 0; k < NV; ++k) {
+    const int c = (k * 64 + lane) * 4;
+    v[k] = c < D ? *reinterpret_cast<const float4 *>(zr + c) : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+  norm_row<OUT, NV>(v, lane, D, shift, size_t(row), out, row_scale);
+}
+
+// S3 and the attention half's row norm in one pass: the row slots of k_compress, one wave each,
+// form the z row in registers in norm_row's lane layout (lane l: the float4 at columns (64 k + l) *
+// 4), store it, and norm_row writes its normalised, modulated form (modulation set 0) -- the z
+// values and the normalised rows are those of k_compress followed by k_rownorm, bit for bit, and
+// z is not read back.  Image rows take the shift and scale of their grid's sample, text rows the
+// text stream's.
+template <bool BF16, int OUT, int NV>
+__global__ __launch_bounds__(kPackThreads) void k_compress_norm(
+    const void *__restrict__ x_img, const void *__restrict__ x_txt, const int *__restrict__ fine_idx,
+    const int *__restrict__ pool_idx, const int *__restrict__ counts, const int *__restrict__ cu,
+    const int *__restrict__ seg, const float *__restrict__ mod, float *__restrict__ z, int G, int I,
+    int N, int W, int D, int L, long long nslots, void *__restrict__ out, float *__restrict__ row_scale) {
+#pragma clang fp contract(off)
+  const int lane = threadIdx.x & 63;
+  const int R = N + N / 4;
+  const long long imgSlots = (long long)G * R;
+  const long long slot = (long long)blockIdx.x * kPackRows + (threadIdx.x >> 6);
+  if (slot >= nslots) return;
+  size_t dst, s0, s1 = 0, s2 = 0, s3 = 0;
+  bool pooled = false;
+  const void *src = x_img;
+  int sample, sigma;
+  if (slot < imgSlots) {
+    const int g = int(slot / R), k = int(slot % R);
+    const int nf = counts[2 * g], np = counts[2 * g + 1];
+    if (k >= nf + np) return;
+    dst = size_t(seg[g] + k);
+    sample = g / I;
+    sigma = 0;
+    if (k < nf) {
+      s0 = size_t(g) * N + fine_idx[size_t(g) * N + k];
+    } else {
+      const int b = pool_idx[size_t(g) * (N / 4) + (k - nf)];
+      const int W2 = W / 2;
+      const size_t p00 = size_t(g) * N + size_t(b / W2) * 2 * W + size_t(b % W2) * 2;
+      s0 = p00; s1 = p00 + 1; s2 = p00 + W; s3 = p00 + W + 1;
+      pooled = true;
+    }
+  } else {
+    const long long t = slot - imgSlots;
+    sample = int(t / L);
+    const int j = int(t % L);
+    dst = size_t(cu[sample + 1] - L + j);
+    s0 = size_t(sample) * L + j;
+    src = x_txt;
+    sigma = 1;
+  }
+  auto load4 = [&](size_t e) __attribute__((always_inline)) {
+    if constexpr (BF16) {
+      const uint2 u = *reinterpret_cast<const uint2 *>(reinterpret_cast<const uint16_t *>(src) + e);
+      return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u),
+                         __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xffff0000u));
+    } else {
+      return *reinterpret_cast<const float4 *>(reinterpret_cast<const float *>(src) + e);
+    }
+  };
+  float4 v[NV];
+#pragma unroll
+  for (int k = 0; k < NV; ++k) {
+    const int c = (k * 64 + lane) * 4;
+    if (c < D) {
+      if (pooled) {
+        const float4 a = load4(s0 * D + c), b = load4(s1 * D + c), e = load4(s2 * D + c), f = load4(s3 * D + c);
+        v[k] = make_float4(((a.x + b.x) + (e.x + f.x)) * 0.25f, ((a.y + b.y) + (e.y + f.y)) * 0.25f,
+                           ((a.z + b.z) + (e.z + f.z)) * 0.25f, ((a.w + b.w) + (e.w + f.w)) * 0.25f);
+      } else {
+        v[k] = load4(s0 * D + c);
+      }
+      *reinterpret_cast<float4 *>(z + dst * D + c) = v[k];
+    } else {
+      v[k] = make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+  }
+  norm_row<OUT, NV>(v, lane, D, mod + size_t(sample * 2 + sigma) * 6 * D, dst, out, row_scale);
+}
+
+template <bool BF16, int OUT>
+static hipError_t run_compress_norm(const void *x_img, const void *x_txt, const int *fine_idx,
+                                    const int *pool_idx, const int *counts, const int *cu, const int *seg,
+                                    const float *mod, float *z, int G, int I, int N, int W, int D, int L,
+                                    long long nslots, void *out, float *row_scale, hipStream_t st) {
+  const long long nblk = (nslots + kPackRows - 1) / kPackRows;
+  const int nv = (D + 255) / 256;
+#define HILO_CN(NVV)                                                                                  \
+  hipLaunchKernelGGL((k_compress_norm<BF16, OUT, NVV>), dim3(unsigned(nblk)), dim3(kPackThreads), 0, st, \
+                     x_img, x_txt, fine_idx, pool_idx, counts, cu, seg, mod, z, G, I, N, W, D, L, nslots, \
+                     out, row_scale)
+  if (nv <= 4) HILO_CN(4);
+  else if (nv <= 8) HILO_CN(8);
+  else if (nv <= 12) HILO_CN(12);
+  else if (nv <= 16) HILO_CN(16);
+  else HILO_CN(32);
+#undef HILO_CN
+  return hipGetLastError();
+}
+
+hipError_t launch_compress_norm(bool bf16, const void *x_img, const void *x_txt, const int *fine_idx,
+                                const int *pool_idx, const int *counts, const int *cu, const int *seg,
+                                const float *mod, float *z, int B, int I, int H, int W, int D, int L,
+                                void *out, hipStream_t st) {
+  const int G = B * I, N = H * W;
+  const long long nslots = (long long)G * (N + N / 4) + (long long)B * L;
+  if (nslots <= 0) return hipSuccess;
+  return bf16 ? run_compress_norm<true, 1>(x_img, x_txt, fine_idx, pool_idx, counts, cu, seg, mod, z, G,
+                                           I, N, W, D, L, nslots, out, nullptr, st)
+              : run_compress_norm<false, 0>(x_img, x_txt, fine_idx, pool_idx, counts, cu, seg, mod, z,
+                                            G, I, N, W, D, L, nslots, out, nullptr, st);
 }
 
 template <int OUT>

@@ -64,6 +64,10 @@ _SIG = {
                            ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int32),
                            ctypes.c_int32, _P, _P, _P, _P, _P, _P, _P],
     "hilo_compress": [ctypes.POINTER(hilo_shape), _P, _P, _P, _P, _P, _P, _P, _P, _P],
+    "hilo_compress_norm": [ctypes.POINTER(hilo_shape), _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
+                           ctypes.c_size_t, _P],
+    "hilo_attention_normed": [ctypes.POINTER(hilo_shape), _P, _P, ctypes.POINTER(hilo_attn_w), _P, _P,
+                              ctypes.c_size_t, _P],
     "hilo_decompress_delta": [ctypes.POINTER(hilo_shape), _P, _P, _P, _P, _P, _P, _P, _P, _P],
     "hilo_attention": [ctypes.POINTER(hilo_shape), _P, _P, ctypes.POINTER(hilo_attn_w), _P, _P,
                        ctypes.c_size_t, _P],
@@ -206,6 +210,14 @@ def hilo_compress(shape, x_img, x_txt, fine_idx, pool_idx, counts, cu_seqlens, s
         _ptr(counts), _ptr(cu_seqlens), _ptr(seg_off), _ptr(z), _stream(stream)))
 
 
+def hilo_compress_norm(shape, x_img, x_txt, fine_idx, pool_idx, counts, cu_seqlens, seg_off, mod, z,
+                       workspace, stream=None):
+    _check("hilo_compress_norm", lib().hilo_compress_norm(
+        ctypes.byref(shape), _ptr(x_img), _ptr(x_txt), _ptr(fine_idx), _ptr(pool_idx),
+        _ptr(counts), _ptr(cu_seqlens), _ptr(seg_off), _ptr(mod), _ptr(z), _ptr(workspace),
+        workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
 def attn_weights(ws: Sequence[dict]):
     arr = (hilo_attn_w * 2)()
     for k in range(2):
@@ -224,6 +236,12 @@ def mlp_weights(ws: Sequence[dict]):
 
 def hilo_attention(shape, z, cu_seqlens, w, mod, workspace, stream=None):
     _check("hilo_attention", lib().hilo_attention(
+        ctypes.byref(shape), _ptr(z), _ptr(cu_seqlens), w, _ptr(mod), _ptr(workspace),
+        workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def hilo_attention_normed(shape, z, cu_seqlens, w, mod, workspace, stream=None):
+    _check("hilo_attention_normed", lib().hilo_attention_normed(
         ctypes.byref(shape), _ptr(z), _ptr(cu_seqlens), w, _ptr(mod), _ptr(workspace),
         workspace.numel() * workspace.element_size(), _stream(stream)))
 

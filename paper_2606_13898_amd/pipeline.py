@@ -81,9 +81,15 @@ class DeviceBlock:
                                     self.idx_map, self.fine_idx, self.pool_idx, self.counts, self.cu,
                                     self.seg, stream)
 
-    def compress(self, stream=None):
-        hilo.hilo_compress(self.shape, self.x_img, self.x_txt, self.fine_idx, self.pool_idx,
-                           self.counts, self.cu, self.seg, self.z, stream)
+    def compress(self, stream=None, norm: bool = False):
+        """S3; with norm (a block attached) also the attention half's first row norm, whose rows
+        land in the workspace for attention(normed=True)."""
+        if norm:
+            hilo.hilo_compress_norm(self.shape, self.x_img, self.x_txt, self.fine_idx, self.pool_idx,
+                                    self.counts, self.cu, self.seg, self.mod, self.z, self.ws, stream)
+        else:
+            hilo.hilo_compress(self.shape, self.x_img, self.x_txt, self.fine_idx, self.pool_idx,
+                               self.counts, self.cu, self.seg, self.z, stream)
 
     def prepare_fp8(self, stream=None):
         """FP8 codes and per-output-channel scales of the four projection weights (once; weights
@@ -93,10 +99,12 @@ class DeviceBlock:
             self.aw8 = hilo.attn_weights_fp8(self.weights8)
             self.mw8 = hilo.mlp_weights_fp8(self.weights8)
 
-    def attention(self, stream=None, fp8: bool = False):
+    def attention(self, stream=None, fp8: bool = False, normed: bool = False):
         if fp8:
             self.prepare_fp8(stream)
             hilo.hilo_attention_fp8(self.shape, self.z, self.cu, self.aw8, self.mod, self.ws, stream)
+        elif normed:
+            hilo.hilo_attention_normed(self.shape, self.z, self.cu, self.aw, self.mod, self.ws, stream)
         else:
             hilo.hilo_attention(self.shape, self.z, self.cu, self.aw, self.mod, self.ws, stream)
 
@@ -116,14 +124,17 @@ class DeviceBlock:
                                  self.y_txt, stream)
 
     def run(self, mode: int = hilo.TOPK, keep=None, tau=None, dilate_r=None, stream=None,
-            tokens: int = hilo.PARTITION, delta: bool = False, fp8: bool = False):
+            tokens: int = hilo.PARTITION, delta: bool = False, fp8: bool = False, fused: bool = True):
         """One pass of the whole hot path: score, select, compress, attention, MLP, decompress
-        (fp8: all four projections on FP8 operands)."""
+        (fp8: all four projections on FP8 operands; fused: the attention half's first row norm in
+        the compress pass, hilo_compress_norm + hilo_attention_normed, for the bf16 / float32
+        block)."""
         self.score(stream)
         self.select(mode, keep, tau, dilate_r, stream, tokens)
-        self.compress(stream)
+        norm = fused and self.with_block and not fp8
+        self.compress(stream, norm)
         if self.with_block:
-            self.attention(stream, fp8)
+            self.attention(stream, fp8, norm)
             self.mlp(stream, fp8)
         self.decompress(stream, delta)
 

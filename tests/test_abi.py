@@ -31,7 +31,7 @@ def test_exports_every_declared_symbol():
 
 
 def test_version_and_status_strings():
-    assert hilo.hilo_abi_version() == 5
+    assert hilo.hilo_abi_version() == 6
     for st in range(7):
         assert hilo.status_str(st)
     assert hilo.status_str(99) == "unknown status"
@@ -109,6 +109,36 @@ def test_null_pointers():
     assert L.hilo_attention(ctypes.byref(s), FAKE, FAKE, aw, FAKE, FAKE, 1 << 40, None) == 1
     assert L.hilo_decompress(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, None, None, None) == 1
     assert L.hilo_compress(ctypes.byref(s), FAKE, None, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None) == 1
+
+
+def test_fused_compress_norm_validation():
+    """hilo_compress_norm / hilo_attention_normed: block shape, pointers and workspace checked
+    before anything is enqueued (status codes as hilo_compress and hilo_attention)."""
+    L = hilo.lib()
+    s = good_shape()
+    need = hilo.hilo_workspace_bytes(s)
+    aw = (hilo.hilo_attn_w * 2)(*[hilo.hilo_attn_w(FAKE, FAKE, FAKE, FAKE)] * 2)
+
+    def cn(shape, mod=FAKE, ws=FAKE, nbytes=1 << 40, x_txt=FAKE):
+        return L.hilo_compress_norm(ctypes.byref(shape), FAKE, x_txt, FAKE, FAKE, FAKE, FAKE, FAKE, mod,
+                                    FAKE, ws, nbytes, None)
+
+    bad = good_shape()
+    bad.heads = 3  # not a block shape: heads * head_dim != dim
+    assert cn(bad) == 2
+    grid = good_shape()
+    grid.grid_w = 9  # odd grid
+    assert cn(grid) == 2
+    assert cn(s, mod=None) == 1
+    assert cn(s, ws=None) == 1
+    assert cn(s, x_txt=None) == 1  # text_len > 0 needs the text rows
+    assert cn(s, nbytes=100) == 5
+    assert L.hilo_attention_normed(ctypes.byref(bad), FAKE, FAKE, aw, FAKE, FAKE, 1 << 40, None) == 2
+    assert L.hilo_attention_normed(ctypes.byref(s), FAKE, FAKE, aw, None, FAKE, 1 << 40, None) == 1
+    assert L.hilo_attention_normed(ctypes.byref(s), FAKE, FAKE, aw, FAKE, FAKE, 100, None) == 5
+    if not torch.cuda.is_available():
+        assert cn(s, nbytes=need) == 6
+        assert L.hilo_attention_normed(ctypes.byref(s), FAKE, FAKE, aw, FAKE, FAKE, need, None) == 6
 
 
 def test_select_parameter_validation():

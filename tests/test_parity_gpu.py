@@ -17,22 +17,23 @@ pytestmark = pytest.mark.gpu
 SMALL = ["tiny", "small128", "small64", "smallf32"]
 
 
-def _block_stages(name, wl, check_z=True):
+def _block_stages(name, wl, check_z=True, fused=False):
     """Score, select and compress, then the block one half at a time: the selection bit for bit,
     the compressed sequence bit for bit (pooled rows to float32 rounding), each half's update of z
-    against the oracle's update, z and y against the oracle."""
+    against the oracle's update, z and y against the oracle (fused: hilo_compress_norm, then
+    hilo_attention_normed on the rows it left in the workspace)."""
     dt = wl.shape.dtype
     db = DeviceBlock(wl)
     ref = oracle_for(wl)
     db.score()
     db.select(hilo.TOPK)
-    db.compress()
+    db.compress(norm=fused)
     torch.cuda.synchronize()
     check_selection(db, ref)
     T = int(ref["cu"][-1])
     z0 = to_np(db.z)[:T].copy()
     check_compressed(z0, ref, wl)
-    db.attention()
+    db.attention(normed=fused)
     torch.cuda.synchronize()
     z1 = to_np(db.z)[:T].copy()
     assert_update_close(z1, ref["z1"], z0, ref["Z"], dt, f"{name} attention update z1 - Z")
@@ -58,6 +59,24 @@ def test_pipeline_parity(name):
     assert_close(to_np(db.y_img), ref["y_img"], dt, f"{name} y_img")
     assert_close(to_np(db.y_txt), ref["y_txt"], dt, f"{name} y_txt")
     assert np.abs(ref["y_img"]).max() < 8.0
+
+
+@pytest.mark.parametrize("name", SMALL)
+def test_fused_compress_norm(name):
+    """The attention half's first row norm in the compress pass (hilo_compress_norm +
+    hilo_attention_normed, the benchmark's step): every stage against the oracle, and z, y_img and
+    y_txt bit for bit those of hilo_compress + hilo_attention."""
+    print(f"[parity] fused compress + norm workload={name}", flush=True)
+    wl = inputs.make_workload(name)
+    db, ref = _block_stages(f"{name} fused", wl, fused=True)
+    T = int(ref["cu"][-1])
+    z_f, yi_f, yt_f = db.z[:T].clone(), db.y_img.clone(), db.y_txt.clone()
+    db.run(hilo.TOPK, fused=False)
+    torch.cuda.synchronize()
+    assert int(db.cu[-1]) == T
+    assert torch.equal(db.z[:T], z_f), "z differs from the unfused calls"
+    assert torch.equal(db.y_img, yi_f), "y_img differs from the unfused calls"
+    assert torch.equal(db.y_txt, yt_f), "y_txt differs from the unfused calls"
 
 
 def test_pipeline_parity_gate_std_0_3():

@@ -139,7 +139,12 @@ def kind_of(name, state):
         return gemm_role(base)
     if "k_attn" in base:
         return "attention_core"
+    if "k_compress_norm<" in base:
+        state["fused"] = True  # the attention half's row norm runs in the compress pass
+        return "compress"
     if "k_rownorm" in base:
+        if state.get("fused"):
+            return "rownorm_mlp"
         state["rownorm"] = state.get("rownorm", 0) + 1
         return "rownorm_attn" if state["rownorm"] % 2 == 1 else "rownorm_mlp"
     if "k_score_bf16<" in base:
