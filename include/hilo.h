@@ -281,6 +281,20 @@ hilo_status hilo_mlp_fp8(const hilo_shape *shape, float *z, const int32_t *cu_se
                          const hilo_mlp_w_fp8 w[2], const float *mod, void *workspace,
                          size_t ws_bytes, void *stream);
 
+/* The FP8 block's counterparts of hilo_compress_norm / hilo_attention_normed (Sec. 2.3 and
+ * Sec. 3.3): z as hilo_compress, and the attention half's normalised rows as the FP8 block's
+ * projection input (per-row E4M3 codes and row scales, as hilo_attention_fp8 forms them, bit for
+ * bit) in the workspace; then hilo_attention_fp8 from its QKV projection on.  Shapes, pointers and
+ * workspace (ws_bytes >= hilo_workspace_bytes_fp8(shape), the same one for both calls with nothing
+ * enqueued on it in between) as hilo_attention_fp8 and hilo_compress_norm.                      */
+hilo_status hilo_compress_norm_fp8(const hilo_shape *shape, const void *x_img, const void *x_txt,
+                                   const int32_t *fine_idx, const int32_t *pool_idx, const int32_t *counts,
+                                   const int32_t *cu_seqlens, const int32_t *seg_off, const float *mod,
+                                   float *z, void *workspace, size_t ws_bytes, void *stream);
+hilo_status hilo_attention_fp8_normed(const hilo_shape *shape, float *z, const int32_t *cu_seqlens,
+                                      const hilo_attn_w_fp8 w[2], const float *mod, void *workspace,
+                                      size_t ws_bytes, void *stream);
+
 /* S6 -- decompress.  The paper does not say how the DiT's output on the HiLo tokens returns to the
  * full grid; this is the plain reading (each patch takes its token's output):
  * y_img[g][p] = z[seg_off[g] + idx_map[g][p]] (fine tokens scatter back to

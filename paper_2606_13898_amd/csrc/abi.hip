@@ -650,6 +650,38 @@ hilo_status hilo_attention_fp8(const hilo_shape *s, float *z, const int32_t *cu_
   return enqueue_attention(s, z, cu_seqlens, nullptr, w, mod, workspace, reinterpret_cast<hipStream_t>(stream));
 }
 
+hilo_status hilo_compress_norm_fp8(const hilo_shape *s, const void *x_img, const void *x_txt,
+                                   const int32_t *fine_idx, const int32_t *pool_idx, const int32_t *counts,
+                                   const int32_t *cu_seqlens, const int32_t *seg_off, const float *mod,
+                                   float *z, void *workspace, size_t ws_bytes, void *stream) {
+  hilo_status e = check_fp8_block(s);
+  if (e != HILO_OK) return e;
+  if (!x_img || !fine_idx || !pool_idx || !counts || !cu_seqlens || !seg_off || !mod || !z || !workspace)
+    return HILO_E_NULL;
+  if (s->text_len > 0 && !x_txt) return HILO_E_NULL;
+  if (ws_bytes < ws_fp8(s)) return HILO_E_WORKSPACE;
+  if (!have_device()) return HILO_E_DEVICE;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  return dev_status(timed(K_COMPRESS, st, [&] {
+    return launch_compress_norm(true, x_img, x_txt, fine_idx, pool_idx, counts, cu_seqlens, seg_off, mod, z,
+                                s->batch, s->images, s->grid_h, s->grid_w, s->dim, s->text_len, workspace, st,
+                                true, fp8_row_scales(s, workspace));
+  }));
+}
+
+hilo_status hilo_attention_fp8_normed(const hilo_shape *s, float *z, const int32_t *cu_seqlens,
+                                      const hilo_attn_w_fp8 w[2], const float *mod, void *workspace,
+                                      size_t ws_bytes, void *stream) {
+  hilo_status e = check_fp8_block(s);
+  if (e != HILO_OK) return e;
+  if (!z || !cu_seqlens || !mod || !workspace) return HILO_E_NULL;
+  if ((e = check_attn_w8(w)) != HILO_OK) return e;
+  if (ws_bytes < ws_fp8(s)) return HILO_E_WORKSPACE;
+  if (!have_device()) return HILO_E_DEVICE;
+  return enqueue_attention(s, z, cu_seqlens, nullptr, w, mod, workspace, reinterpret_cast<hipStream_t>(stream),
+                           true);
+}
+
 hilo_status hilo_mlp_fp8(const hilo_shape *s, float *z, const int32_t *cu_seqlens,
                          const hilo_mlp_w_fp8 w[2], const float *mod, void *workspace, size_t ws_bytes,
                          void *stream) {

@@ -27,11 +27,12 @@ hipError_t launch_compress(bool bf16, const void *x_img, const void *x_txt, cons
                            const int *pool_idx, const int *counts, const int *cu, const int *seg,
                            float *z, int B, int I, int H, int W, int D, int L, hipStream_t st);
 // S3 fused with the attention half's row norm: z as launch_compress, and out = the normalised,
-// modulated rows (bf16 for bf16 inputs, float32 otherwise), as launch_rownorm with set 0.
+// modulated rows (bf16 for bf16 inputs, float32 otherwise), as launch_rownorm with set 0; with
+// fp8 (bf16 inputs) their E4M3 codes and row scales, as launch_rownorm_fp8.
 hipError_t launch_compress_norm(bool bf16, const void *x_img, const void *x_txt, const int *fine_idx,
                                 const int *pool_idx, const int *counts, const int *cu, const int *seg,
                                 const float *mod, float *z, int B, int I, int H, int W, int D, int L,
-                                void *out, hipStream_t st);
+                                void *out, hipStream_t st, bool fp8 = false, float *row_scale = nullptr);
 hipError_t launch_decompress(bool bf16, const float *z, const int *idx_map, const int *cu,
                              const int *seg, void *y_img, void *y_txt, int B, int I, int N, int D,
                              int L, hipStream_t st);

@@ -464,10 +464,14 @@ static hipError_t run_compress_norm(const void *x_img, const void *x_txt, const 
 hipError_t launch_compress_norm(bool bf16, const void *x_img, const void *x_txt, const int *fine_idx,
                                 const int *pool_idx, const int *counts, const int *cu, const int *seg,
                                 const float *mod, float *z, int B, int I, int H, int W, int D, int L,
-                                void *out, hipStream_t st) {
+                                void *out, hipStream_t st, bool fp8, float *row_scale) {
   const int G = B * I, N = H * W;
   const long long nslots = (long long)G * (N + N / 4) + (long long)B * L;
   if (nslots <= 0) return hipSuccess;
+  if (fp8)
+    return bf16 ? run_compress_norm<true, 2>(x_img, x_txt, fine_idx, pool_idx, counts, cu, seg, mod, z, G,
+                                             I, N, W, D, L, nslots, out, row_scale, st)
+                : hipErrorInvalidValue;
   return bf16 ? run_compress_norm<true, 1>(x_img, x_txt, fine_idx, pool_idx, counts, cu, seg, mod, z, G,
                                            I, N, W, D, L, nslots, out, nullptr, st)
               : run_compress_norm<false, 0>(x_img, x_txt, fine_idx, pool_idx, counts, cu, seg, mod, z,

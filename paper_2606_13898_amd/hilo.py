@@ -73,6 +73,10 @@ _SIG = {
                        ctypes.c_size_t, _P],
     "hilo_mlp": [ctypes.POINTER(hilo_shape), _P, _P, ctypes.POINTER(hilo_mlp_w), _P, _P,
                  ctypes.c_size_t, _P],
+    "hilo_compress_norm_fp8": [ctypes.POINTER(hilo_shape), _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
+                               ctypes.c_size_t, _P],
+    "hilo_attention_fp8_normed": [ctypes.POINTER(hilo_shape), _P, _P, ctypes.POINTER(hilo_attn_w_fp8), _P,
+                                  _P, ctypes.c_size_t, _P],
     "hilo_attention_fp8": [ctypes.POINTER(hilo_shape), _P, _P, ctypes.POINTER(hilo_attn_w_fp8), _P, _P,
                            ctypes.c_size_t, _P],
     "hilo_mlp_fp8": [ctypes.POINTER(hilo_shape), _P, _P, ctypes.POINTER(hilo_mlp_w_fp8), _P, _P,
@@ -295,6 +299,20 @@ def mlp_weights_fp8(ws: Sequence[dict]):
 
 def hilo_attention_fp8(shape, z, cu_seqlens, w, mod, workspace, stream=None):
     _check("hilo_attention_fp8", lib().hilo_attention_fp8(
+        ctypes.byref(shape), _ptr(z), _ptr(cu_seqlens), w, _ptr(mod), _ptr(workspace),
+        workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def hilo_compress_norm_fp8(shape, x_img, x_txt, fine_idx, pool_idx, counts, cu_seqlens, seg_off, mod, z,
+                           workspace, stream=None):
+    _check("hilo_compress_norm_fp8", lib().hilo_compress_norm_fp8(
+        ctypes.byref(shape), _ptr(x_img), _ptr(x_txt), _ptr(fine_idx), _ptr(pool_idx),
+        _ptr(counts), _ptr(cu_seqlens), _ptr(seg_off), _ptr(mod), _ptr(z), _ptr(workspace),
+        workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def hilo_attention_fp8_normed(shape, z, cu_seqlens, w, mod, workspace, stream=None):
+    _check("hilo_attention_fp8_normed", lib().hilo_attention_fp8_normed(
         ctypes.byref(shape), _ptr(z), _ptr(cu_seqlens), w, _ptr(mod), _ptr(workspace),
         workspace.numel() * workspace.element_size(), _stream(stream)))
 

@@ -81,10 +81,13 @@ class DeviceBlock:
                                     self.idx_map, self.fine_idx, self.pool_idx, self.counts, self.cu,
                                     self.seg, stream)
 
-    def compress(self, stream=None, norm: bool = False):
+    def compress(self, stream=None, norm: bool = False, fp8: bool = False):
         """S3; with norm (a block attached) also the attention half's first row norm, whose rows
-        land in the workspace for attention(normed=True)."""
-        if norm:
+        land in the workspace for attention(normed=True) (fp8: in the FP8 block's form)."""
+        if norm and fp8:
+            hilo.hilo_compress_norm_fp8(self.shape, self.x_img, self.x_txt, self.fine_idx, self.pool_idx,
+                                        self.counts, self.cu, self.seg, self.mod, self.z, self.ws, stream)
+        elif norm:
             hilo.hilo_compress_norm(self.shape, self.x_img, self.x_txt, self.fine_idx, self.pool_idx,
                                     self.counts, self.cu, self.seg, self.mod, self.z, self.ws, stream)
         else:
@@ -102,7 +105,10 @@ class DeviceBlock:
     def attention(self, stream=None, fp8: bool = False, normed: bool = False):
         if fp8:
             self.prepare_fp8(stream)
-            hilo.hilo_attention_fp8(self.shape, self.z, self.cu, self.aw8, self.mod, self.ws, stream)
+            if normed:
+                hilo.hilo_attention_fp8_normed(self.shape, self.z, self.cu, self.aw8, self.mod, self.ws, stream)
+            else:
+                hilo.hilo_attention_fp8(self.shape, self.z, self.cu, self.aw8, self.mod, self.ws, stream)
         elif normed:
             hilo.hilo_attention_normed(self.shape, self.z, self.cu, self.aw, self.mod, self.ws, stream)
         else:
@@ -127,12 +133,13 @@ class DeviceBlock:
             tokens: int = hilo.PARTITION, delta: bool = False, fp8: bool = False, fused: bool = True):
         """One pass of the whole hot path: score, select, compress, attention, MLP, decompress
         (fp8: all four projections on FP8 operands; fused: the attention half's first row norm in
-        the compress pass, hilo_compress_norm + hilo_attention_normed, for the bf16 / float32
-        block)."""
+        the compress pass, hilo_compress_norm + hilo_attention_normed, or their FP8 counterparts)."""
         self.score(stream)
         self.select(mode, keep, tau, dilate_r, stream, tokens)
-        norm = fused and self.with_block and not fp8
-        self.compress(stream, norm)
+        norm = fused and self.with_block
+        if norm and fp8:
+            self.prepare_fp8(stream)
+        self.compress(stream, norm, fp8)
         if self.with_block:
             self.attention(stream, fp8, norm)
             self.mlp(stream, fp8)

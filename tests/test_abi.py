@@ -141,6 +141,31 @@ def test_fused_compress_norm_validation():
         assert L.hilo_attention_normed(ctypes.byref(s), FAKE, FAKE, aw, FAKE, FAKE, need, None) == 6
 
 
+def test_fused_compress_norm_fp8_validation():
+    """The FP8 block's pair: an FP8 block shape, pointers and the FP8 workspace checked first."""
+    L = hilo.lib()
+    s = good_shape()
+    need = hilo.hilo_workspace_bytes_fp8(s)
+    aw8 = (hilo.hilo_attn_w_fp8 * 2)(*[hilo.hilo_attn_w_fp8(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE)] * 2)
+
+    def cn(shape, mod=FAKE, nbytes=1 << 40):
+        return L.hilo_compress_norm_fp8(ctypes.byref(shape), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, mod,
+                                        FAKE, FAKE, nbytes, None)
+
+    odd = good_shape()
+    odd.dim, odd.heads = 384, 3  # a block shape, but not a multiple of 256
+    assert cn(odd) == 2
+    f32 = good_shape(hilo.F32)
+    assert cn(f32) == 3
+    assert cn(s, mod=None) == 1
+    assert cn(s, nbytes=100) == 5
+    assert L.hilo_attention_fp8_normed(ctypes.byref(odd), FAKE, FAKE, aw8, FAKE, FAKE, 1 << 40, None) == 2
+    assert L.hilo_attention_fp8_normed(ctypes.byref(s), FAKE, FAKE, aw8, FAKE, FAKE, 100, None) == 5
+    if not torch.cuda.is_available():
+        assert cn(s, nbytes=need) == 6
+        assert L.hilo_attention_fp8_normed(ctypes.byref(s), FAKE, FAKE, aw8, FAKE, FAKE, need, None) == 6
+
+
 def test_select_parameter_validation():
     s = good_shape()
     NB = 8 * 10 // 4

@@ -351,6 +351,26 @@ def test_fp8_gemm_schedules(shp):
     assert_close(to_np(db.y_img), ref["y_img"], "fp8", "y_img")
 
 
+@pytest.mark.parametrize("name", ["small128", "small64"])
+def test_fp8_fused_compress_norm(name):
+    """The FP8 block with its attention half's first row norm in the compress pass
+    (hilo_compress_norm_fp8 + hilo_attention_fp8_normed, the benchmark's FP8 step): z, y_img and
+    y_txt bit for bit those of hilo_compress + hilo_attention_fp8."""
+    print(f"[parity-fp8] fused compress + norm workload={name}", flush=True)
+    wl = inputs.make_workload(name)
+    db = DeviceBlock(wl)
+    db.run(hilo.TOPK, fp8=True, fused=False)
+    torch.cuda.synchronize()
+    T = int(db.cu[-1])
+    z_u, yi_u, yt_u = db.z[:T].clone(), db.y_img.clone(), db.y_txt.clone()
+    db.run(hilo.TOPK, fp8=True, fused=True)
+    torch.cuda.synchronize()
+    assert int(db.cu[-1]) == T
+    assert torch.equal(db.z[:T], z_u), "z differs from the unfused calls"
+    assert torch.equal(db.y_img, yi_u), "y_img differs from the unfused calls"
+    assert torch.equal(db.y_txt, yt_u), "y_txt differs from the unfused calls"
+
+
 def test_fp8_full_size_sampled():
     """The 1024 px workload (2766 tokens at 40% kept, dim 3072, MLP 12288) in the benchmark's launch
     configuration: all four projections exact on the device's own operands at sampled rows, then the
