@@ -217,8 +217,9 @@ HILO_DEV int sk_owner(long long I, int P, long long a) { return int(((a + 1) * P
 HILO_DEV int piece_k0(const SkPlan &q, int piece) { return piece * q.nk / q.s; }
 
 // Tile t -> (row tile, column tile): groups of kTileGroupRows row tiles by all column tiles, row
-// tile fastest within a group, so one XCD's 64 workgroups of a wave cover 8 row tiles by 8 column
-// tiles (16 operand slices per K step instead of up to 25 in plain row-fastest order).
+// tile fastest within a group, so one XCD's 32 workgroups of a wave (consecutive ids, xcd_remap)
+// cover 8 row tiles by 4 column tiles: 12 operand slices per K step, the least any 32 tiles need,
+// instead of 18 in plain row-fastest order over 15 row tiles.
 constexpr int kTileGroupRows = 8;
 
 HILO_DEV void tile_coords(const SkPlan &q, int t, int &r, int &tn) {
