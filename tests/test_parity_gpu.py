@@ -366,3 +366,33 @@ def test_pixel_score_and_paper_threshold(shp):
     np.testing.assert_array_equal(to_np(cnt), counts)
     np.testing.assert_array_equal(to_np(im), idx_map)
     assert 0 < counts[:, 0].sum() < G * N
+
+
+def _random_shape(i):
+    """Case i of a fixed seeded draw of valid block shapes: batch 1-3, one or two grids per sample,
+    even grids 4..40 a side, no text or 1..159 text tokens, 1..6 heads of 64 or 128, bf16 or
+    float32, kept fraction anywhere in [0, 1], the fused compress + LN pair on half the bf16 cases."""
+    rng = np.random.default_rng([7919, i])
+    hd = int(rng.choice([64, 128]))
+    heads = int(rng.integers(1, 7))
+    dim = hd * heads
+    shp = inputs.BlockShape(int(rng.integers(1, 4)), int(rng.integers(1, 3)), 2 * int(rng.integers(2, 21)),
+                            2 * int(rng.integers(2, 21)), int(rng.choice([0, int(rng.integers(1, 160))])),
+                            dim, heads, hd, 4 * dim, str(rng.choice(["bf16", "f32"])))
+    return shp, float(rng.uniform(0.0, 1.0)), int(rng.integers(0, 1 << 30)), bool(rng.integers(0, 2))
+
+
+@pytest.mark.parametrize("i", range(12))
+def test_random_shapes(i):
+    """The whole path on seeded random shapes (ragged grids, text or none, 1-6 heads, both head
+    dims and dtypes): the selection and compressed sequence bit for bit, both updates and z, y
+    against the oracle, as on the named workloads."""
+    shp, keep, seed, fused = _random_shape(i)
+    fused = fused and shp.dtype == "bf16"
+    name = f"random{i}"
+    print(f"[parity] {name} {shp} keep={keep:.2f} seed={seed} fused={fused}", flush=True)
+    wl = inputs.make_workload(name, shape=shp, seed=seed, keep_frac=keep)
+    db, ref = _block_stages(name, wl, fused=fused)
+    assert_close(to_np(db.y_img), ref["y_img"], shp.dtype, f"{name} y_img")
+    if shp.text_len:
+        assert_close(to_np(db.y_txt), ref["y_txt"], shp.dtype, f"{name} y_txt")
