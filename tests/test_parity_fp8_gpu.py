@@ -446,3 +446,43 @@ def test_fp8_attention_core_ragged(hd, lens, heads):
     hilo.hilo_attention_core_fp8(shp, torch.from_numpy(buf).cuda(), torch.from_numpy(cu).cuda(), out, ws)
     torch.cuda.synchronize()
     assert_close(to_np(out), want, "bf16", f"FP8 attention core hd={hd}")
+
+
+def _random_fp8_shape(i):
+    """Case i of a fixed seeded draw of valid FP8 block shapes: dim 256-1024, heads of 64 or 128,
+    mlp_dim any multiple of 128 up to 4 dim, batch 1-2, one or two grids, even grids 4..32 a side,
+    no text or 1..199 text tokens, any kept fraction."""
+    rng = np.random.default_rng([104729, i])
+    hd = int(rng.choice([64, 128]))
+    dim = 256 * int(rng.integers(1, 5))
+    mlp = 128 * int(rng.integers(2, 4 * dim // 128 + 1))
+    shp = inputs.BlockShape(int(rng.integers(1, 3)), int(rng.integers(1, 3)), 2 * int(rng.integers(2, 17)),
+                            2 * int(rng.integers(2, 17)), int(rng.choice([0, int(rng.integers(1, 200))])),
+                            dim, dim // hd, hd, mlp, "bf16")
+    return shp, float(rng.uniform(0.0, 1.0)), int(rng.integers(0, 1 << 30))
+
+
+@pytest.mark.parametrize("i", range(4))
+def test_fp8_random_shapes(i):
+    """The FP8 block on seeded random shapes: the exact per-projection checks on sampled rows, then z
+    and y against the oracle's FP8 block."""
+    shp, keep, seed = _random_fp8_shape(i)
+    print(f"[parity-fp8] random{i} {shp} keep={keep:.2f} seed={seed}", flush=True)
+    wl = inputs.make_workload(f"fp8random{i}", shape=shp, seed=seed, keep_frac=keep)
+    db = DeviceBlock(wl)
+    ref = oracle_for(wl, fp8=True)
+    db.prepare_fp8()
+    db.score()
+    db.select(hilo.TOPK)
+    db.compress()
+    torch.cuda.synchronize()
+    check_selection(db, ref)
+    T = int(ref["cu"][-1])
+    rows = np.unique(np.random.default_rng(7).choice(T, min(T, 64), replace=False))
+    fp8_block_checked(db, wl, rows)
+    db.decompress()
+    torch.cuda.synchronize()
+    assert_close(to_np(db.z)[:T], ref["z2"], "fp8", "z after FP8 block")
+    assert_close(to_np(db.y_img), ref["y_img"], "fp8", "y_img")
+    if shp.text_len:
+        assert_close(to_np(db.y_txt), ref["y_txt"], "fp8", "y_txt")
